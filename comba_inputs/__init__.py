@@ -40,12 +40,31 @@ __all__ = [
 ]
 
 
+_SLAB = 1 << 20  # elements per in-place processing slab (bounds temporaries)
+
+
+def bf16_round_(x: np.ndarray) -> np.ndarray:
+    """Round a float32 array to the nearest bfloat16 in place (ties to even)."""
+    assert x.dtype == np.float32 and x.flags.c_contiguous
+    u = x.reshape(-1).view(np.uint32)
+    for a in range(0, u.size, _SLAB):
+        blk = u[a:a + _SLAB]
+        lsb = (blk >> np.uint32(16)) & np.uint32(1)
+        blk += np.uint32(0x7FFF)
+        blk += lsb
+        blk &= np.uint32(0xFFFF0000)
+    return x
+
+
 def bf16_round(x: np.ndarray) -> np.ndarray:
     """Round float32 values to the nearest bfloat16 (ties to even); returns float32."""
-    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
-    lsb = (u >> np.uint32(16)) & np.uint32(1)
-    r = (u + np.uint32(0x7FFF) + lsb) & np.uint32(0xFFFF0000)
-    return r.view(np.float32)
+    return bf16_round_(np.array(x, dtype=np.float32, order="C", copy=True))
+
+
+def _normal(rng, shape) -> np.ndarray:
+    out = np.empty(shape, dtype=np.float32)
+    rng.standard_normal(dtype=np.float32, out=out)
+    return out
 
 
 def _softplus(x: np.ndarray) -> np.ndarray:
@@ -57,9 +76,19 @@ def _sigmoid(x: np.ndarray) -> np.ndarray:
     return (1.0 / (1.0 + np.exp(-x.astype(np.float64)))).astype(np.float32)
 
 
+def _l2norm_(x: np.ndarray) -> np.ndarray:
+    """Normalise a float32 array to unit L2 norm along the last axis, in place."""
+    flat = x.reshape(-1, x.shape[-1])
+    rows = max(1, _SLAB // x.shape[-1])
+    for a in range(0, flat.shape[0], rows):
+        blk = flat[a:a + rows]
+        n = np.sqrt(np.einsum("ij,ij->i", blk, blk))
+        blk /= np.maximum(n, np.float32(1e-12))[:, None]
+    return x
+
+
 def _l2norm(x: np.ndarray) -> np.ndarray:
-    n = np.sqrt(np.sum(x.astype(np.float32) ** 2, axis=-1, keepdims=True, dtype=np.float32))
-    return (x / np.maximum(n, np.float32(1e-12))).astype(np.float32)
+    return _l2norm_(np.array(x, dtype=np.float32, order="C", copy=True))
 
 
 @dataclass(frozen=True)
@@ -160,15 +189,45 @@ def _draw_h0(rng, mode: str, shape) -> Optional[np.ndarray]:
     raise ValueError(mode)
 
 
-def generate(spec, *, with_grad: Optional[bool] = None) -> Workload:
+def _fill_head(child_seed, h, arrays, in_dtype):
+    """Draw one head's slices, in order q, k, v, gate noise, beta noise, dO."""
+    rng = np.random.default_rng(child_seed)
+    q, k, v, g, beta, dO = arrays
+    B, T = q.shape[:2]
+    for dst, norm in ((q, True), (k, True), (v, False)):
+        x = _normal(rng, (B, T, dst.shape[-1]))
+        if norm:
+            _l2norm_(x)
+        if in_dtype == "bf16":
+            bf16_round_(x)
+        dst[:, :, h, :] = x
+    g[:, :, h] = -_softplus(_normal(rng, (B, T)))
+    b = _sigmoid(_normal(rng, (B, T)))
+    beta[:, :, h] = bf16_round_(b) if in_dtype == "bf16" else b
+    if dO is not None:
+        x = _normal(rng, (B, T, dO.shape[-1]))
+        if in_dtype == "bf16":
+            bf16_round_(x)
+        dO[:, :, h, :] = x
+
+
+def generate(spec, *, with_grad: Optional[bool] = None, threads: Optional[int] = None) -> Workload:
     """Draw the seeded inputs of one workload.
 
-    ``spec`` is a WorkloadSpec or an index into WORKLOADS.  Draw order: varlen
-    lengths (if any); q, k, v; gate noise; beta noise; d; h0; dO.
+    ``spec`` is a WorkloadSpec or an index into WORKLOADS.  A root PCG64 stream
+    seeded with spec.seed draws, in order, the varlen lengths (if any), d and
+    h0; each head h then draws its own q, k, v, gate noise, beta noise and dO
+    from child stream h of SeedSequence(spec.seed) (heads are filled in
+    parallel threads; the values do not depend on the thread count).
     """
+    import os
+    from concurrent.futures import ThreadPoolExecutor
+
     if isinstance(spec, int):
         spec = WORKLOADS[spec]
-    rng = np.random.default_rng(spec.seed)
+    ss = np.random.SeedSequence(spec.seed)
+    root_seed, head_seeds = ss.spawn(1)[0], None
+    rng = np.random.default_rng(root_seed)
     cu = None
     if spec.nseq_varlen > 0:
         lo, hi = spec.len_range
@@ -179,21 +238,26 @@ def generate(spec, *, with_grad: Optional[bool] = None) -> Workload:
     else:
         B, T = spec.B, spec.T
     H, dk, dv = spec.H, spec.dk, spec.dv
-    q = _l2norm(rng.standard_normal((B, T, H, dk), dtype=np.float32))
-    k = _l2norm(rng.standard_normal((B, T, H, dk), dtype=np.float32))
-    v = rng.standard_normal((B, T, H, dv), dtype=np.float32)
-    g = (-_softplus(rng.standard_normal((B, T, H), dtype=np.float32))).astype(np.float32)
-    beta = _sigmoid(rng.standard_normal((B, T, H), dtype=np.float32))
     d = _draw_d(rng, spec.d_mode, H)
     N = B if cu is None else len(cu) - 1
     h0 = _draw_h0(rng, spec.h0_mode, (N, H, dk, dv))
     if with_grad is None:
         with_grad = spec.work == "fwdbwd"
-    dO = rng.standard_normal((B, T, H, dv), dtype=np.float32) if with_grad else None
-    if spec.in_dtype == "bf16":
-        q, k, v, beta = bf16_round(q), bf16_round(k), bf16_round(v), bf16_round(beta)
-        if dO is not None:
-            dO = bf16_round(dO)
+    q = np.empty((B, T, H, dk), np.float32)
+    k = np.empty((B, T, H, dk), np.float32)
+    v = np.empty((B, T, H, dv), np.float32)
+    g = np.empty((B, T, H), np.float32)
+    beta = np.empty((B, T, H), np.float32)
+    dO = np.empty((B, T, H, dv), np.float32) if with_grad else None
+    head_seeds = np.random.SeedSequence(spec.seed).spawn(1 + H)[1:]
+    arrays = (q, k, v, g, beta, dO)
+    if threads is None:
+        try:
+            threads = len(os.sched_getaffinity(0))
+        except Exception:  # pragma: no cover
+            threads = os.cpu_count() or 1
+    with ThreadPoolExecutor(max_workers=max(1, min(threads, H, 16))) as ex:
+        list(ex.map(lambda h: _fill_head(head_seeds[h], h, arrays, spec.in_dtype), range(H)))
     return Workload(spec=spec, B=B, T=T, H=H, dk=dk, dv=dv, chunk=spec.chunk,
                     in_dtype=spec.in_dtype, q=q, k=k, v=v, g=g, beta=beta, d=d, h0=h0,
                     dO=dO, dht=None, cu_seqlens=cu)

@@ -1,0 +1,119 @@
+/*
+ * comba.h -- C ABI of the MI355X (gfx950) chunk-wise Comba operator.
+ *
+ * Comba (arXiv 2506.02475) is a bilinear RNN whose per-head state S_t (dv x dk)
+ * follows, for tokens t = 1..T of one sequence (Eq. comba-S, Section 3):
+ *
+ *     S_t = S_{t-1} (alpha_t I - beta_t k_t k_t^T) + beta_t v_t k_t^T
+ *     o_t = S_t (q_t - d k_t)
+ *
+ * with forget gate alpha_t = exp(g_t) in (0, 1], input gate beta_t, and a
+ * per-head output-feedback scalar d.  The state-feedback strength (tilde beta
+ * of Section 3.2) is taken equal to beta_t (the paper's ablation without the
+ * extra factor b).  The library evaluates this recurrence with the chunk-wise
+ * parallel algorithm of Section 3.3 (chunks of 64 tokens, WY/UT transform with
+ * one unit-lower-triangular inverse per chunk, inter-chunk state passing), and
+ * its reverse-mode derivative (derived from the same chunk form; the paper
+ * states no backward).
+ *
+ * Conventions shared by every entry point
+ *  - `shape` points to host memory; every other pointer (including
+ *    shape->cu_seqlens) is a DEVICE pointer on the current HIP device.  The
+ *    caller owns every buffer; the library allocates nothing and keeps no state
+ *    between calls.
+ *  - Layouts are C-contiguous.  Token-major tensors are [B, T, H, D]; in the
+ *    variable-length mode B == 1, T is the packed token count and sequence s
+ *    covers tokens [cu_seqlens[s], cu_seqlens[s+1]).  A sequence's last chunk
+ *    may be partial; states never cross sequences.
+ *  - The recurrent state is stored transposed, H = S^T, as [N, H, dk, dv] fp32
+ *    (N = number of sequences), the orientation of the paper's recurrent
+ *    pseudocode (Appendix B.1).
+ *  - q, k, v, beta and dO have dtype shape->in_dtype (bf16 or fp32); g (log
+ *    alpha), d, states and every output are fp32.
+ *  - g must be <= 0 (alpha in (0, 1]); other values are outside the contract
+ *    (results may overflow) but never cause out-of-bounds accesses.
+ *  - Calls are asynchronous on `stream` (a hipStream_t passed as void*; NULL is
+ *    the default stream).  Argument errors are detected before any launch and
+ *    then nothing is written.  A failed launch returns COMBA_ERR_HIP.
+ *  - Outputs must not alias inputs; outputs are overwritten, never accumulated.
+ *  - Calls on different streams with distinct workspaces may run concurrently;
+ *    a workspace must not be shared by calls that overlap in time.
+ */
+#ifndef COMBA_H
+#define COMBA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  COMBA_OK = 0,
+  COMBA_ERR_NULL = 1,      /* a required pointer is NULL                         */
+  COMBA_ERR_SHAPE = 2,     /* unsupported or inconsistent sizes                  */
+  COMBA_ERR_DTYPE = 3,     /* unknown dtype                                      */
+  COMBA_ERR_ALIGN = 4,     /* q/k/v/dO not 16-byte aligned, workspace not 256    */
+  COMBA_ERR_WORKSPACE = 5, /* workspace smaller than the *_workspace_bytes value */
+  COMBA_ERR_HIP = 6        /* a kernel launch failed                             */
+} comba_status;
+
+typedef enum { COMBA_F32 = 0, COMBA_BF16 = 1 } comba_dtype;
+
+typedef struct {
+  int32_t B;                  /* batch rows (1 in variable-length mode)                 */
+  int32_t T;                  /* tokens per row; packed total in variable-length mode   */
+  int32_t H;                  /* heads                                                  */
+  int32_t dk;                 /* key/query head dim: 64 or 128 (64 only for COMBA_F32)  */
+  int32_t dv;                 /* value head dim: 64 or 128 (64 only for COMBA_F32)      */
+  int32_t chunk;              /* chunk length; must be 64                               */
+  int32_t num_seqs;           /* N: sequences; must equal B when cu_seqlens == NULL     */
+  const int32_t *cu_seqlens;  /* device [N+1] offsets (0 = cu[0] <= ... <= cu[N] = T),
+                                 or NULL for fixed-length rows                           */
+  comba_dtype in_dtype;       /* dtype of q, k, v, beta, dO                             */
+} comba_shape;
+
+/* Workspace sizes in bytes for one call of the matching entry point. */
+size_t comba_fwd_workspace_bytes(const comba_shape *shape);
+size_t comba_bwd_workspace_bytes(const comba_shape *shape);
+
+/*
+ * Forward of the chunk-wise recurrence (Section 3.3: UT transform with one
+ * inverse M per chunk, Eq. prepare-WY_M; inter-chunk state update and output of
+ * the closing matrix form).
+ *   q, k  [B,T,H,dk] in_dtype      v   [B,T,H,dv] in_dtype
+ *   g     [B,T,H] fp32 (log alpha) beta [B,T,H] in_dtype    d [H] fp32
+ *   h0    [N,H,dk,dv] fp32 initial states, or NULL for zero states
+ *   o     [B,T,H,dv] fp32 output   ht  [N,H,dk,dv] fp32 final states, or NULL
+ *   ws    device workspace of at least comba_fwd_workspace_bytes(shape), 256-B aligned
+ */
+comba_status comba_chunk_fwd(const comba_shape *shape, const void *q, const void *k,
+                             const void *v, const float *g, const void *beta, const float *d,
+                             const float *h0, float *o, float *ht, void *ws, size_t ws_bytes,
+                             void *stream);
+
+/*
+ * Backward: gradients of L = <dO, o> + <dht, ht> with respect to every input.
+ * Recomputes the forward internally (no saved state is needed from a forward
+ * call).  Inputs as comba_chunk_fwd plus
+ *   dO    [B,T,H,dv] in_dtype     dht [N,H,dk,dv] fp32 or NULL (zero)
+ * Outputs (fp32): dq, dk [B,T,H,dk]; dv [B,T,H,dv]; dg, dbeta [B,T,H];
+ *   dd [H] (summed over all sequences and tokens); dh0 [N,H,dk,dv] or NULL.
+ * dbeta is the total derivative through both roles of beta (write strength
+ * and state-feedback strength).
+ */
+comba_status comba_chunk_bwd(const comba_shape *shape, const void *q, const void *k,
+                             const void *v, const float *g, const void *beta, const float *d,
+                             const float *h0, const void *dO, const float *dht, float *dq,
+                             float *dk, float *dv, float *dg, float *dbeta, float *dd,
+                             float *dh0, void *ws, size_t ws_bytes, void *stream);
+
+/* Human-readable name of a status code (static storage). */
+const char *comba_status_string(comba_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* COMBA_H */

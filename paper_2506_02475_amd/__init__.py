@@ -1,0 +1,216 @@
+"""MI355X (gfx950) chunk-wise Comba operator: Python binding of libcomba.so.
+
+The binding only marshals arguments: it checks dtypes/shapes/devices of torch
+tensors, allocates outputs and the workspace with torch (device memory and the
+current stream are the only things torch provides), and calls the C ABI of
+``include/comba.h``.  Every step of the computation runs in the HIP kernels.
+There is no fallback: if the library is missing or no GPU is present, the
+calls raise.
+
+    o, ht = comba_chunk_fwd(q, k, v, g, beta, d, h0)
+    grads = comba_chunk_bwd(q, k, v, g, beta, d, h0, dO, dht)
+
+Shapes (see include/comba.h): q, k [B,T,H,dk]; v, dO [B,T,H,dv]; g, beta [B,T,H];
+d [H]; h0, dht [N,H,dk,dv].  q, k, v, beta, dO share one dtype (bfloat16 or
+float32); g, d and states are float32; all outputs are float32.  Pass
+``cu_seqlens`` (int32 [N+1] on the device) for a packed variable-length batch
+with B == 1.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+import threading
+
+__all__ = ["comba_chunk_fwd", "comba_chunk_bwd", "load_library", "library_path",
+           "fwd_workspace_bytes", "bwd_workspace_bytes", "exported_symbols", "CombaError",
+           "CombaShape", "COMBA_F32", "COMBA_BF16", "CHUNK"]
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_PKG, "libcomba.so")
+_HEADER = os.path.join(os.path.dirname(_PKG), "include", "comba.h")
+_lock = threading.Lock()
+_lib = None
+
+COMBA_F32 = 0
+COMBA_BF16 = 1
+CHUNK = 64
+
+
+class CombaError(RuntimeError):
+    pass
+
+
+class CombaShape(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("T", ctypes.c_int32), ("H", ctypes.c_int32),
+                ("dk", ctypes.c_int32), ("dv", ctypes.c_int32), ("chunk", ctypes.c_int32),
+                ("num_seqs", ctypes.c_int32), ("cu_seqlens", ctypes.c_void_p),
+                ("in_dtype", ctypes.c_int)]
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def load_library():
+    """Load libcomba.so (built by ``paper_2506_02475_amd.build``); raises if absent."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(_LIB_PATH):
+                raise ImportError("libcomba.so is not built; run "
+                                  "`python -m paper_2506_02475_amd.build` (hipcc, gfx950)")
+            lib = ctypes.CDLL(_LIB_PATH)
+            P, Z, I = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int
+            SP = ctypes.POINTER(CombaShape)
+            lib.comba_fwd_workspace_bytes.argtypes = [SP]
+            lib.comba_fwd_workspace_bytes.restype = Z
+            lib.comba_bwd_workspace_bytes.argtypes = [SP]
+            lib.comba_bwd_workspace_bytes.restype = Z
+            lib.comba_chunk_fwd.argtypes = [SP] + [P] * 9 + [P, Z, P]
+            lib.comba_chunk_fwd.restype = I
+            lib.comba_chunk_bwd.argtypes = [SP] + [P] * 16 + [P, Z, P]
+            lib.comba_chunk_bwd.restype = I
+            lib.comba_status_string.argtypes = [I]
+            lib.comba_status_string.restype = ctypes.c_char_p
+            _lib = lib
+    return _lib
+
+
+def exported_symbols():
+    """Function names declared in include/comba.h (the C ABI)."""
+    with open(_HEADER) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"\b(comba_[a-z_]+)\s*\(", text)))
+
+
+def _check(status: int):
+    if status != 0:
+        msg = load_library().comba_status_string(status).decode()
+        raise CombaError("comba: %s (status %d)" % (msg, status))
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _make_shape(B, T, H, dk, dv, N, cu_ptr, dtype_code, chunk=CHUNK):
+    return CombaShape(B, T, H, dk, dv, chunk, N, cu_ptr, dtype_code)
+
+
+def fwd_workspace_bytes(B, T, H, dk, dv, *, num_seqs=None, varlen=False, bf16=True) -> int:
+    N = B if num_seqs is None else num_seqs
+    shp = _make_shape(B, T, H, dk, dv, N, ctypes.c_void_p(1) if varlen else None,
+                      COMBA_BF16 if bf16 else COMBA_F32)
+    return int(load_library().comba_fwd_workspace_bytes(ctypes.byref(shp)))
+
+
+def bwd_workspace_bytes(B, T, H, dk, dv, *, num_seqs=None, varlen=False, bf16=True) -> int:
+    N = B if num_seqs is None else num_seqs
+    shp = _make_shape(B, T, H, dk, dv, N, ctypes.c_void_p(1) if varlen else None,
+                      COMBA_BF16 if bf16 else COMBA_F32)
+    return int(load_library().comba_bwd_workspace_bytes(ctypes.byref(shp)))
+
+
+def _prepare(q, k, v, g, beta, d, h0, cu_seqlens, extra=()):
+    import torch
+
+    if not q.is_cuda:
+        raise CombaError("comba: tensors must be on a GPU device")
+    if q.dtype == torch.bfloat16:
+        code = COMBA_BF16
+    elif q.dtype == torch.float32:
+        code = COMBA_F32
+    else:
+        raise CombaError("comba: q must be bfloat16 or float32")
+    for name, t in (("k", k), ("v", v), ("beta", beta)) + tuple(extra):
+        if t.dtype != q.dtype:
+            raise CombaError("comba: %s must have the dtype of q" % name)
+    for name, t in (("g", g), ("d", d)):
+        if t.dtype != torch.float32:
+            raise CombaError("comba: %s must be float32" % name)
+    tensors = [q, k, v, g, beta, d] + [t for _, t in extra]
+    if h0 is not None:
+        tensors.append(h0)
+    for t in tensors:
+        if not t.is_contiguous() or t.device != q.device:
+            raise CombaError("comba: all tensors must be contiguous and on one device")
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    if k.shape != q.shape or v.shape[:3] != (B, T, H) or g.shape != (B, T, H) \
+            or beta.shape != (B, T, H) or d.shape != (H,):
+        raise CombaError("comba: inconsistent shapes")
+    if cu_seqlens is not None:
+        if cu_seqlens.dtype != torch.int32 or not cu_seqlens.is_contiguous() \
+                or cu_seqlens.device != q.device or B != 1:
+            raise CombaError("comba: cu_seqlens must be contiguous int32 on the device, B == 1")
+        N = cu_seqlens.numel() - 1
+    else:
+        N = B
+    if h0 is not None and (h0.dtype != torch.float32 or tuple(h0.shape) != (N, H, dk, dv)):
+        raise CombaError("comba: h0 must be float32 [N,H,dk,dv]")
+    shp = _make_shape(B, T, H, dk, dv, N, _ptr(cu_seqlens), code)
+    return shp, (B, T, H, dk, dv, N)
+
+
+def comba_chunk_fwd(q, k, v, g, beta, d, h0=None, *, cu_seqlens=None, output_final_state=True,
+                    workspace=None, stream=None):
+    """Chunk-wise forward.  Returns (o [B,T,H,dv] fp32, ht [N,H,dk,dv] fp32 or None)."""
+    import torch
+
+    lib = load_library()
+    shp, (B, T, H, dk, dv, N) = _prepare(q, k, v, g, beta, d, h0, cu_seqlens)
+    o = torch.empty((B, T, H, dv), dtype=torch.float32, device=q.device)
+    ht = torch.empty((N, H, dk, dv), dtype=torch.float32, device=q.device) \
+        if output_final_state else None
+    nbytes = lib.comba_fwd_workspace_bytes(ctypes.byref(shp))
+    if nbytes == 0:
+        _check(2)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=q.device)
+    st = torch.cuda.current_stream(q.device).cuda_stream if stream is None else stream
+    _check(lib.comba_chunk_fwd(ctypes.byref(shp), _ptr(q), _ptr(k), _ptr(v), _ptr(g),
+                               _ptr(beta), _ptr(d), _ptr(h0), _ptr(o), _ptr(ht),
+                               _ptr(workspace), ctypes.c_size_t(workspace.numel()),
+                               ctypes.c_void_p(st)))
+    return o, ht
+
+
+def comba_chunk_bwd(q, k, v, g, beta, d, h0, dO, dht=None, *, cu_seqlens=None,
+                    need_dh0=True, workspace=None, stream=None):
+    """Chunk-wise backward.  Returns dict dq, dk, dv, dg, dbeta, dd, dh0 (fp32)."""
+    import torch
+
+    lib = load_library()
+    shp, (B, T, H, dk, dv, N) = _prepare(q, k, v, g, beta, d, h0, cu_seqlens,
+                                         extra=(("dO", dO),))
+    if dht is not None and (dht.dtype != torch.float32 or tuple(dht.shape) != (N, H, dk, dv)
+                            or not dht.is_contiguous()):
+        raise CombaError("comba: dht must be contiguous float32 [N,H,dk,dv]")
+    if tuple(dO.shape) != (B, T, H, dv):
+        raise CombaError("comba: dO must be [B,T,H,dv]")
+    dev = q.device
+    f32 = torch.float32
+    out = {
+        "dq": torch.empty((B, T, H, dk), dtype=f32, device=dev),
+        "dk": torch.empty((B, T, H, dk), dtype=f32, device=dev),
+        "dv": torch.empty((B, T, H, dv), dtype=f32, device=dev),
+        "dg": torch.empty((B, T, H), dtype=f32, device=dev),
+        "dbeta": torch.empty((B, T, H), dtype=f32, device=dev),
+        "dd": torch.empty((H,), dtype=f32, device=dev),
+        "dh0": torch.empty((N, H, dk, dv), dtype=f32, device=dev) if need_dh0 else None,
+    }
+    nbytes = lib.comba_bwd_workspace_bytes(ctypes.byref(shp))
+    if nbytes == 0:
+        _check(2)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    st = torch.cuda.current_stream(dev).cuda_stream if stream is None else stream
+    _check(lib.comba_chunk_bwd(ctypes.byref(shp), _ptr(q), _ptr(k), _ptr(v), _ptr(g),
+                               _ptr(beta), _ptr(d), _ptr(h0), _ptr(dO), _ptr(dht),
+                               _ptr(out["dq"]), _ptr(out["dk"]), _ptr(out["dv"]),
+                               _ptr(out["dg"]), _ptr(out["dbeta"]), _ptr(out["dd"]),
+                               _ptr(out["dh0"]), _ptr(workspace),
+                               ctypes.c_size_t(workspace.numel()), ctypes.c_void_p(st)))
+    return out

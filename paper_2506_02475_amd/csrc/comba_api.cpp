@@ -1,0 +1,219 @@
+// Host side of the C ABI declared in include/comba.h: argument validation,
+// workspace layout and kernel sequencing on the caller's stream.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "comba.h"
+#include "comba_launch.h"
+
+namespace {
+
+constexpr int kChunk = 64;
+constexpr size_t kAlign = 256;
+
+size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Dims {
+  bool bf16;
+  int dk, dv, H, N, Tseq, Ttot, ncmax;
+};
+
+// Validates the shape; fills dims on success.
+comba_status check_shape(const comba_shape* s, Dims* out) {
+  if (!s) return COMBA_ERR_NULL;
+  if (s->in_dtype != COMBA_F32 && s->in_dtype != COMBA_BF16) return COMBA_ERR_DTYPE;
+  const bool bf16 = s->in_dtype == COMBA_BF16;
+  if (s->chunk != kChunk) return COMBA_ERR_SHAPE;
+  if (s->B < 0 || s->T < 0 || s->H <= 0 || s->H > 65535) return COMBA_ERR_SHAPE;
+  const bool dk_ok = s->dk == 64 || (bf16 && s->dk == 128);
+  const bool dv_ok = s->dv == 64 || (bf16 && s->dv == 128);
+  if (!dk_ok || !dv_ok) return COMBA_ERR_SHAPE;
+  Dims d;
+  d.bf16 = bf16;
+  d.dk = s->dk;
+  d.dv = s->dv;
+  d.H = s->H;
+  if (s->cu_seqlens) {
+    if (s->B != 1 || s->num_seqs < 0) return COMBA_ERR_SHAPE;
+    d.N = s->num_seqs;
+    d.Tseq = 0;
+  } else {
+    if (s->num_seqs != s->B) return COMBA_ERR_SHAPE;
+    d.N = s->B;
+    d.Tseq = s->T;
+  }
+  const int64_t ttot = s->cu_seqlens ? (int64_t)s->T : (int64_t)s->B * s->T;
+  if (ttot > INT32_MAX / 2) return COMBA_ERR_SHAPE;
+  if (d.N > 65535 * 1024) return COMBA_ERR_SHAPE;
+  d.Ttot = (int)ttot;
+  // fixed-length rows: ceil(T / 64) chunks each; packed sequences: each
+  // sequence adds at most one partial chunk to ceil(Ttot / 64)
+  const int64_t nc = s->cu_seqlens ? (ttot + kChunk - 1) / kChunk + d.N
+                                   : (int64_t)d.N * ((d.Tseq + kChunk - 1) / kChunk);
+  if (nc > INT32_MAX / 2) return COMBA_ERR_SHAPE;
+  d.ncmax = (int)nc;
+  *out = d;
+  return COMBA_OK;
+}
+
+struct Layout {
+  size_t cmap, smap, M, A, G, X, D, Y, dR, ddp, total;
+};
+
+Layout layout(const Dims& d, bool bwd) {
+  Layout L{};
+  const size_t chh = (size_t)d.ncmax * d.H;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += round_up(bytes);
+    return at;
+  };
+  L.cmap = take((size_t)d.ncmax * sizeof(comba::ChunkInfo));
+  L.smap = take((size_t)(d.N > 0 ? d.N : 1) * sizeof(comba::SeqInfo));
+  L.M = take(chh * kChunk * kChunk * sizeof(float));
+  L.A = take(chh * kChunk * kChunk * sizeof(float));
+  L.G = take(chh * kChunk * sizeof(float));
+  if (bwd) {
+    L.X = take(chh * d.dk * d.dv * sizeof(float));
+    L.D = take(chh * kChunk * d.dv * sizeof(float));
+    L.Y = take(chh * d.dk * d.dv * sizeof(float));
+    L.dR = take(chh * kChunk * d.dv * sizeof(float));
+    L.ddp = take(chh * sizeof(float));
+  }
+  L.total = off;
+  return L;
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+void carve(comba::LaunchArgs& a, const Layout& L, void* ws, bool bwd) {
+  char* base = static_cast<char*>(ws);
+  a.cmap = reinterpret_cast<comba::ChunkInfo*>(base + L.cmap);
+  a.smap = reinterpret_cast<comba::SeqInfo*>(base + L.smap);
+  a.Mw = reinterpret_cast<float*>(base + L.M);
+  a.Aw = reinterpret_cast<float*>(base + L.A);
+  a.Gw = reinterpret_cast<float*>(base + L.G);
+  if (bwd) {
+    a.Xw = reinterpret_cast<float*>(base + L.X);
+    a.Dw = reinterpret_cast<float*>(base + L.D);
+    a.Yw = reinterpret_cast<float*>(base + L.Y);
+    a.dRw = reinterpret_cast<float*>(base + L.dR);
+    a.ddp = reinterpret_cast<float*>(base + L.ddp);
+  }
+}
+
+void fill_common(comba::LaunchArgs& a, const Dims& d, const comba_shape* s) {
+  a.bf16 = d.bf16;
+  a.dk = d.dk;
+  a.dv = d.dv;
+  a.H = d.H;
+  a.N = d.N;
+  a.Tseq = d.Tseq;
+  a.Ttot = d.Ttot;
+  a.ncmax = d.ncmax;
+  a.cu_seqlens = s->cu_seqlens;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t comba_fwd_workspace_bytes(const comba_shape* shape) {
+  Dims d;
+  if (check_shape(shape, &d) != COMBA_OK) return 0;
+  return layout(d, false).total;
+}
+
+size_t comba_bwd_workspace_bytes(const comba_shape* shape) {
+  Dims d;
+  if (check_shape(shape, &d) != COMBA_OK) return 0;
+  return layout(d, true).total;
+}
+
+comba_status comba_chunk_fwd(const comba_shape* shape, const void* q, const void* k, const void* v,
+                             const float* g, const void* beta, const float* d, const float* h0,
+                             float* o, float* ht, void* ws, size_t ws_bytes, void* stream) {
+  Dims dm;
+  comba_status st = check_shape(shape, &dm);
+  if (st != COMBA_OK) return st;
+  if (!q || !k || !v || !g || !beta || !d || !o || !ws) return COMBA_ERR_NULL;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(ws, kAlign) ||
+      !aligned(g, 4) || !aligned(d, 4) || !aligned(o, 4) || (h0 && !aligned(h0, 4)) ||
+      (ht && !aligned(ht, 4)) || !aligned(beta, dm.bf16 ? 2 : 4))
+    return COMBA_ERR_ALIGN;
+  const Layout L = layout(dm, false);
+  if (ws_bytes < L.total) return COMBA_ERR_WORKSPACE;
+  comba::LaunchArgs a{};
+  fill_common(a, dm, shape);
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.beta = beta;
+  a.g = g;
+  a.d = d;
+  a.h0 = h0;
+  a.o = o;
+  a.ht = ht;
+  a.stream = static_cast<hipStream_t>(stream);
+  carve(a, L, ws, false);
+  if (dm.N == 0) return COMBA_OK;
+  return comba::launch_fwd(a) == hipSuccess ? COMBA_OK : COMBA_ERR_HIP;
+}
+
+comba_status comba_chunk_bwd(const comba_shape* shape, const void* q, const void* k, const void* v,
+                             const float* g, const void* beta, const float* d, const float* h0,
+                             const void* dO, const float* dht, float* dq, float* dk, float* dv,
+                             float* dg, float* dbeta, float* dd, float* dh0, void* ws,
+                             size_t ws_bytes, void* stream) {
+  Dims dm;
+  comba_status st = check_shape(shape, &dm);
+  if (st != COMBA_OK) return st;
+  if (!q || !k || !v || !g || !beta || !d || !dO || !dq || !dk || !dv || !dg || !dbeta || !dd ||
+      !ws)
+    return COMBA_ERR_NULL;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(dO, 16) ||
+      !aligned(ws, kAlign) || !aligned(g, 4) || !aligned(d, 4) || !aligned(dq, 4) ||
+      !aligned(dk, 4) || !aligned(dv, 4) || !aligned(dg, 4) || !aligned(dbeta, 4) ||
+      !aligned(dd, 4) || (h0 && !aligned(h0, 4)) || (dht && !aligned(dht, 4)) ||
+      (dh0 && !aligned(dh0, 4)) || !aligned(beta, dm.bf16 ? 2 : 4))
+    return COMBA_ERR_ALIGN;
+  const Layout L = layout(dm, true);
+  if (ws_bytes < L.total) return COMBA_ERR_WORKSPACE;
+  comba::LaunchArgs a{};
+  fill_common(a, dm, shape);
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.beta = beta;
+  a.dO = dO;
+  a.g = g;
+  a.d = d;
+  a.h0 = h0;
+  a.dht = dht;
+  a.dq = dq;
+  a.dk_ = dk;
+  a.dv_ = dv;
+  a.dg = dg;
+  a.dbeta = dbeta;
+  a.dd = dd;
+  a.dh0 = dh0;
+  a.stream = static_cast<hipStream_t>(stream);
+  carve(a, L, ws, true);
+  return comba::launch_bwd(a) == hipSuccess ? COMBA_OK : COMBA_ERR_HIP;
+}
+
+const char* comba_status_string(comba_status s) {
+  switch (s) {
+    case COMBA_OK: return "ok";
+    case COMBA_ERR_NULL: return "a required pointer is NULL";
+    case COMBA_ERR_SHAPE: return "unsupported or inconsistent shape";
+    case COMBA_ERR_DTYPE: return "unknown dtype";
+    case COMBA_ERR_ALIGN: return "misaligned pointer (q/k/v/dO need 16 B, workspace 256 B)";
+    case COMBA_ERR_WORKSPACE: return "workspace too small";
+    case COMBA_ERR_HIP: return "HIP kernel launch failed";
+  }
+  return "unknown status";
+}
+
+}  // extern "C"

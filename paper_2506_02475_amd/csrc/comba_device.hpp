@@ -1,0 +1,209 @@
+// Device building blocks for the gfx950 (CDNA4) Comba kernels.
+//
+// Every dense contraction in the chunk-wise algorithm is a product of 16x16
+// output tiles computed by one 64-lane wavefront with MFMA.  Operands are staged
+// in LDS with the reduction (k) index contiguous, so a lane fetches its 8 (bf16
+// MFMA) k-values with one or two vector LDS reads.
+//
+// Precision policy.  bf16 inputs (q, k, v, beta, dO) are exact in bf16.  Every
+// other operand (the inverse M, the masked gate/score matrices, states, pseudo
+// values and their gradients) is fp32; when it meets a bf16 MFMA it is split
+// into hi = bf16(x) and lo = bf16(x - hi), and the product keeps the hi*hi,
+// hi*lo and lo*hi terms (about 16 significant bits per fp32 operand, fp32
+// accumulation).  With fp32 inputs the fp32 MFMA (16x16x4) is used throughout.
+//
+// MFMA register layouts used below (wave64, 16x16 tiles):
+//   A operand (16 x K): lane l supplies row (l % 16), k-group (l / 16)
+//   B operand (K x 16): lane l supplies column (l % 16), k-group (l / 16)
+//   accumulator:        lane l holds column (l % 16), rows 4*(l/16) + i, i = 0..3
+// The order of k inside a group only has to agree between A and B.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace comba {
+
+constexpr int CH = 64;        // chunk length (tokens)
+constexpr int NTHR = 256;     // threads per workgroup: 4 wavefronts
+constexpr int NWAVE = 4;
+
+typedef uint16_t bf16_t;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+template <typename T> struct is_f32 { static constexpr bool value = false; };
+template <> struct is_f32<float> { static constexpr bool value = true; };
+
+__device__ __forceinline__ float bf2f(bf16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+__device__ __forceinline__ float to_f(float x) { return x; }
+__device__ __forceinline__ float to_f(bf16_t x) { return bf2f(x); }
+
+// Storage padding (elements) that keeps 16-byte row alignment and spreads the
+// 16 rows read by one MFMA operand fetch over distinct LDS banks.
+template <typename T> struct Pad { static constexpr int value = 16 / sizeof(T); };
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+__device__ __forceinline__ int wave_id() { return threadIdx.x >> 6; }
+
+__device__ __forceinline__ floatx4 zero4() { return floatx4{0.f, 0.f, 0.f, 0.f}; }
+
+template <int MT, int NT>
+__device__ __forceinline__ void zero_acc(floatx4 (&acc)[MT][NT]) {
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int j = 0; j < NT; ++j) acc[i][j] = zero4();
+}
+
+// ---- operand fragments -------------------------------------------------------
+
+// 8 consecutive-k bf16 values of an exact operand.
+__device__ __forceinline__ bf16x8 frag_exact(const bf16_t* p) {
+  return *reinterpret_cast<const bf16x8*>(p);
+}
+
+// 8 consecutive-k fp32 values split into bf16 hi and lo parts.
+__device__ __forceinline__ void frag_split(const float* p, bf16x8& hi, bf16x8& lo) {
+  const float4 a = *reinterpret_cast<const float4*>(p);
+  const float4 b = *reinterpret_cast<const float4*>(p + 4);
+  const float x[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const __bf16 h = (__bf16)x[e];
+    hi[e] = h;
+    lo[e] = (__bf16)(x[e] - (float)h);
+  }
+}
+
+template <typename T> struct Frag;
+template <> struct Frag<bf16_t> {
+  bf16x8 hi;
+  __device__ __forceinline__ void load(const bf16_t* p) { hi = frag_exact(p); }
+  static constexpr bool split = false;
+};
+template <> struct Frag<float> {
+  bf16x8 hi, lo;
+  __device__ __forceinline__ void load(const float* p) { frag_split(p, hi, lo); }
+  static constexpr bool split = true;
+};
+
+// acc[mt][nt] += sum_{k < K} A(16 mt + i, k) * B(k, 16 nt + j)
+//   A(m, k) = A[m * lda + k]   (row-major, k contiguous)
+//   B(k, n) = B[n * ldb + k]   (stored transposed, k contiguous)
+// F32 selects the fp32 MFMA (both operands fp32); otherwise the bf16 MFMA with
+// fp32 operands split as described above.
+template <bool F32, int MT, int NT, int K, typename TA, typename TB>
+__device__ __forceinline__ void mma(floatx4 (&acc)[MT][NT], const TA* __restrict__ A, int lda,
+                                    const TB* __restrict__ B, int ldb) {
+  const int lane = lane_id();
+  const int r = lane & 15, grp = lane >> 4;
+  if constexpr (F32) {
+    static_assert(is_f32<TA>::value && is_f32<TB>::value, "fp32 MFMA takes fp32 operands");
+#pragma unroll
+    for (int k0 = 0; k0 < K; k0 += 4) {
+      float a[MT], b[NT];
+#pragma unroll
+      for (int i = 0; i < MT; ++i) a[i] = A[(16 * i + r) * lda + k0 + grp];
+#pragma unroll
+      for (int j = 0; j < NT; ++j) b[j] = B[(16 * j + r) * ldb + k0 + grp];
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int j = 0; j < NT; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+  } else {
+    static_assert(K % 32 == 0, "bf16 MFMA reduces 32 at a time");
+#pragma unroll
+    for (int k0 = 0; k0 < K; k0 += 32) {
+      const int kk = k0 + 8 * grp;
+      Frag<TA> a[MT];
+      Frag<TB> b[NT];
+#pragma unroll
+      for (int i = 0; i < MT; ++i) a[i].load(A + (16 * i + r) * lda + kk);
+#pragma unroll
+      for (int j = 0; j < NT; ++j) b[j].load(B + (16 * j + r) * ldb + kk);
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) {
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i].hi, b[j].hi, acc[i][j], 0, 0, 0);
+          if constexpr (Frag<TA>::split)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i].lo, b[j].hi, acc[i][j], 0, 0, 0);
+          if constexpr (Frag<TB>::split)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i].hi, b[j].lo, acc[i][j], 0, 0, 0);
+        }
+    }
+  }
+}
+
+// Row / column of accumulator element e of tile (mt, nt), relative to the
+// block origin passed to mma().
+__device__ __forceinline__ int acc_row(int mt, int e) { return 16 * mt + 4 * (lane_id() >> 4) + e; }
+__device__ __forceinline__ int acc_col(int nt) { return 16 * nt + (lane_id() & 15); }
+
+// Sum over the 16 lanes that hold one accumulator row (same lane / 16 group).
+__device__ __forceinline__ float sum16(float x) {
+  x += __shfl_xor(x, 1);
+  x += __shfl_xor(x, 2);
+  x += __shfl_xor(x, 4);
+  x += __shfl_xor(x, 8);
+  return x;
+}
+// Sum over the 4 lane groups (lanes l, l^16, l^32, l^48).
+__device__ __forceinline__ float sum_groups(float x) {
+  x += __shfl_xor(x, 16);
+  x += __shfl_xor(x, 32);
+  return x;
+}
+__device__ __forceinline__ float wave_sum(float x) {
+  return sum_groups(sum16(x));
+}
+
+// ---- global -> LDS tile copies ---------------------------------------------
+
+// Copy `rows` rows of `cols` elements (row stride gs in global memory) into LDS
+// row-major with stride ld; rows in [rows, nrows) are zero-filled.  cols must
+// be a multiple of 16 bytes' worth of elements; all threads participate.
+template <typename T, int NROWS, int COLS>
+__device__ __forceinline__ void tile_to_lds(const T* __restrict__ g, long gs, int rows, T* s, int ld) {
+  constexpr int V = 16 / sizeof(T);
+  constexpr int PER_ROW = COLS / V;
+  for (int idx = threadIdx.x; idx < NROWS * PER_ROW; idx += NTHR) {
+    const int rr = idx / PER_ROW, cc = (idx % PER_ROW) * V;
+    uint4 val = make_uint4(0, 0, 0, 0);
+    if (rr < rows) val = *reinterpret_cast<const uint4*>(g + (long)rr * gs + cc);
+    *reinterpret_cast<uint4*>(s + rr * ld + cc) = val;
+  }
+}
+
+// Same copy, also (or only) writing the transpose: st[c * ldt + r] = tile[r][c].
+template <typename T, int NROWS, int COLS, bool ROWMAJOR>
+__device__ __forceinline__ void tile_to_lds_t(const T* __restrict__ g, long gs, int rows, T* s, int ld,
+                                              T* st, int ldt) {
+  constexpr int V = 16 / sizeof(T);
+  constexpr int PER_ROW = COLS / V;
+  for (int idx = threadIdx.x; idx < NROWS * PER_ROW; idx += NTHR) {
+    const int rr = idx / PER_ROW, cc = (idx % PER_ROW) * V;
+    union { uint4 u; T e[V]; } val;
+    val.u = make_uint4(0, 0, 0, 0);
+    if (rr < rows) val.u = *reinterpret_cast<const uint4*>(g + (long)rr * gs + cc);
+    if constexpr (ROWMAJOR) *reinterpret_cast<uint4*>(s + rr * ld + cc) = val.u;
+#pragma unroll
+    for (int e = 0; e < V; ++e) st[(cc + e) * ldt + rr] = val.e[e];
+  }
+}
+
+// Inclusive prefix sum across the 64 lanes of a wavefront.
+__device__ __forceinline__ float wave_prefix_sum(float x) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const float y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  return x;
+}
+
+}  // namespace comba

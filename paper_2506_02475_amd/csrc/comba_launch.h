@@ -1,0 +1,39 @@
+// Internal interface between the host API (comba_api.cpp) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace comba {
+
+// One chunk of at most 64 tokens of one sequence (len == 0: unused slot).
+struct ChunkInfo {
+  int32_t tok0, len, seq, pad;
+};
+// Chunk range and token range of one sequence.
+struct SeqInfo {
+  int32_t chunk0, nchunks, tok0, len;
+};
+
+struct LaunchArgs {
+  bool bf16;
+  int dk, dv, H, N, Tseq, Ttot, ncmax;
+  const int32_t* cu_seqlens;
+  const void *q, *k, *v, *beta, *dO;
+  const float *g, *d, *h0, *dht;
+  float *o, *ht;
+  float *dq, *dk_, *dv_, *dg, *dbeta, *dd, *dh0;
+  // workspace views
+  ChunkInfo* cmap;
+  SeqInfo* smap;
+  float *Mw, *Aw, *Gw;            // per chunk-head: M, A (64 x 64), G (64)
+  float *Xw, *Dw, *Yw, *dRw;      // per chunk-head: X (dk x dv), D (64 x dv), Y, dR
+  float* ddp;                     // per chunk-head partial dd
+  hipStream_t stream;
+};
+
+hipError_t launch_fwd(const LaunchArgs& a);
+hipError_t launch_bwd(const LaunchArgs& a);
+
+}  // namespace comba

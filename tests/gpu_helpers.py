@@ -1,0 +1,88 @@
+"""Shared helpers for the GPU parity tests: move a seeded workload to the
+device, call the HIP path through the C ABI, and compare with the fp64 oracle."""
+import numpy as np
+
+import oracle
+
+
+def maxrel(x, ref):
+    """Norm-wise max relative error ||x - ref||_inf / ||ref||_inf (ref = oracle)."""
+    x = np.asarray(x, np.float64)
+    ref = np.asarray(ref, np.float64)
+    den = np.max(np.abs(ref)) if ref.size else 0.0
+    num = np.max(np.abs(x - ref)) if ref.size else 0.0
+    if den == 0.0:
+        return num
+    return num / den
+
+
+def tol_for(w):
+    # tolerances stated for the operator: 1e-5 (fp32 inputs), 2e-3 (bf16 inputs,
+    # fp32 accumulation), on the norm-wise max relative error
+    return 1e-5 if w.in_dtype == "f32" else 2e-3
+
+
+def to_device(w, device="cuda"):
+    import torch
+
+    dt = torch.float32 if w.in_dtype == "f32" else torch.bfloat16
+
+    def t(x, dtype=None):
+        if x is None:
+            return None
+        return torch.from_numpy(np.ascontiguousarray(x)).to(device=device, dtype=dtype or torch.float32)
+
+    out = dict(q=t(w.q, dt), k=t(w.k, dt), v=t(w.v, dt), g=t(w.g), beta=t(w.beta, dt), d=t(w.d),
+               h0=t(w.h0), dO=t(w.dO, dt), dht=t(w.dht))
+    out["cu_seqlens"] = None if w.cu_seqlens is None else \
+        torch.from_numpy(w.cu_seqlens.astype(np.int32)).to(device)
+    return out
+
+
+def gpu_fwd(w, **kw):
+    import torch
+    import paper_2506_02475_amd as comba
+
+    a = to_device(w)
+    o, ht = comba.comba_chunk_fwd(a["q"], a["k"], a["v"], a["g"], a["beta"], a["d"], a["h0"],
+                                  cu_seqlens=a["cu_seqlens"], **kw)
+    torch.cuda.synchronize()
+    return o.cpu().numpy(), (None if ht is None else ht.cpu().numpy())
+
+
+def gpu_bwd(w, **kw):
+    import torch
+    import paper_2506_02475_amd as comba
+
+    a = to_device(w)
+    gr = comba.comba_chunk_bwd(a["q"], a["k"], a["v"], a["g"], a["beta"], a["d"], a["h0"],
+                               a["dO"], a["dht"], cu_seqlens=a["cu_seqlens"], **kw)
+    torch.cuda.synchronize()
+    return {k: (None if v is None else v.cpu().numpy()) for k, v in gr.items()}
+
+
+def check_fwd(w, heads=None, tol=None):
+    """GPU forward vs oracle; returns the error dict (asserts within tolerance)."""
+    tol = tol_for(w) if tol is None else tol
+    o, ht = gpu_fwd(w)
+    ro, rht = oracle.workload_fwd(w, heads=heads)
+    sel = slice(None) if heads is None else list(heads)
+    errs = {"o": maxrel(o[:, :, sel], ro), "ht": maxrel(ht[:, sel], rht)}
+    for name, e in errs.items():
+        assert np.all(np.isfinite(o)) and e <= tol, (w.spec.name, name, e, tol)
+    return errs
+
+
+def check_bwd(w, heads=None, tol=None):
+    tol = tol_for(w) if tol is None else tol
+    gr = gpu_bwd(w)
+    ref = oracle.workload_bwd(w, heads=heads)
+    sel = slice(None) if heads is None else list(heads)
+    errs = {}
+    for name in ("dq", "dk", "dv", "dg", "dbeta"):
+        errs[name] = maxrel(gr[name][:, :, sel], ref[name])
+    errs["dd"] = maxrel(gr["dd"][sel], ref["dd"])
+    errs["dh0"] = maxrel(gr["dh0"][:, sel], ref["dh0"])
+    for name, e in errs.items():
+        assert np.isfinite(e) and e <= tol, (w.spec.name, name, e, tol)
+    return errs

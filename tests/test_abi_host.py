@@ -1,0 +1,116 @@
+"""Host-side checks of the C ABI: the library loads, exports every symbol that
+include/comba.h declares, sizes workspaces, and rejects bad arguments before
+any kernel launch (these calls never reach the GPU, so they run without one)."""
+import ctypes
+import os
+import subprocess
+
+import pytest
+
+import paper_2506_02475_amd as comba
+
+pytestmark = pytest.mark.skipif(not os.path.exists(comba.library_path()),
+                                reason="libcomba.so not built")
+
+OK, ENULL, ESHAPE, EDTYPE, EALIGN, EWS = 0, 1, 2, 3, 4, 5
+FAKE = 0x100000  # aligned, never dereferenced: validation fails before any launch
+
+
+def shape(B=1, T=128, H=2, dk=128, dv=128, chunk=64, N=None, cu=None, dtype=comba.COMBA_BF16):
+    return comba.CombaShape(B, T, H, dk, dv, chunk, B if N is None else N,
+                            None if cu is None else ctypes.c_void_p(cu), dtype)
+
+
+def fwd(shp, ptrs=None, ws_bytes=1 << 40, **over):
+    lib = comba.load_library()
+    p = dict(q=FAKE, k=FAKE, v=FAKE, g=FAKE, beta=FAKE, d=FAKE, h0=None, o=FAKE, ht=None, ws=FAKE)
+    p.update(over)
+    P = ctypes.c_void_p
+    return lib.comba_chunk_fwd(ctypes.byref(shp), P(p["q"]), P(p["k"]), P(p["v"]), P(p["g"]),
+                               P(p["beta"]), P(p["d"]), P(p["h0"]), P(p["o"]), P(p["ht"]),
+                               P(p["ws"]), ctypes.c_size_t(ws_bytes), None)
+
+
+def bwd(shp, ws_bytes=1 << 40, **over):
+    lib = comba.load_library()
+    names = ["q", "k", "v", "g", "beta", "d", "h0", "dO", "dht", "dq", "dk", "dv", "dg",
+             "dbeta", "dd", "dh0", "ws"]
+    p = {n: FAKE for n in names}
+    p.update(h0=None, dht=None, dh0=None)
+    p.update(over)
+    P = ctypes.c_void_p
+    args = [P(p[n]) for n in names]
+    return lib.comba_chunk_bwd(ctypes.byref(shp), *args[:-1], args[-1],
+                               ctypes.c_size_t(ws_bytes), None)
+
+
+def test_library_exports_every_declared_symbol():
+    declared = comba.exported_symbols()
+    assert set(declared) == {"comba_fwd_workspace_bytes", "comba_bwd_workspace_bytes",
+                             "comba_chunk_fwd", "comba_chunk_bwd", "comba_status_string"}
+    out = subprocess.run(["nm", "-D", "--defined-only", comba.library_path()],
+                         capture_output=True, text=True, check=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
+    for name in declared:
+        assert name in exported, name
+        assert hasattr(comba.load_library(), name)
+
+
+def test_status_strings():
+    lib = comba.load_library()
+    for code in range(7):
+        assert lib.comba_status_string(code)
+    assert lib.comba_status_string(99) == b"unknown status"
+
+
+def test_workspace_sizes_grow_with_problem():
+    small = comba.fwd_workspace_bytes(1, 64, 1, 64, 64)
+    big = comba.fwd_workspace_bytes(4, 4096, 16, 128, 128)
+    assert 0 < small < big
+    assert comba.bwd_workspace_bytes(4, 4096, 16, 128, 128) > big
+    # variable-length: each sequence may add one partial chunk
+    assert comba.fwd_workspace_bytes(1, 1000, 2, 128, 128, num_seqs=16, varlen=True) > \
+        comba.fwd_workspace_bytes(1, 1000, 2, 128, 128)
+    # fixed-length rows with a ragged tail each hold their own partial chunk
+    assert comba.fwd_workspace_bytes(3, 1, 2, 64, 64) > comba.fwd_workspace_bytes(1, 3, 2, 64, 64)
+    lib = comba.load_library()
+    assert lib.comba_fwd_workspace_bytes(ctypes.byref(shape(chunk=32))) == 0
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(chunk=32), ESHAPE),
+    (dict(dk=96), ESHAPE),
+    (dict(dv=256), ESHAPE),
+    (dict(dk=128, dtype=comba.COMBA_F32), ESHAPE),   # fp32 path supports d = 64 only
+    (dict(H=0), ESHAPE),
+    (dict(T=-1), ESHAPE),
+    (dict(B=2, N=3), ESHAPE),                         # fixed-length: N must equal B
+    (dict(B=2, cu=FAKE, N=2), ESHAPE),                # varlen needs B == 1
+    (dict(dtype=7), EDTYPE),
+])
+def test_rejects_bad_shapes(kw, code):
+    assert fwd(shape(**kw)) == code
+    assert bwd(shape(**kw)) == code
+
+
+def test_rejects_null_and_misaligned_pointers():
+    s = shape()
+    for name in ("q", "k", "v", "g", "beta", "d", "o", "ws"):
+        assert fwd(s, **{name: None}) == ENULL, name
+    for name in ("q", "dO", "dq", "dk", "dv", "dg", "dbeta", "dd", "ws"):
+        assert bwd(s, **{name: None}) == ENULL, name
+    assert fwd(s, q=FAKE + 8) == EALIGN
+    assert fwd(s, ws=FAKE + 16) == EALIGN
+    assert fwd(s, o=FAKE + 2) == EALIGN
+    assert bwd(s, dO=FAKE + 4) == EALIGN
+    lib = comba.load_library()
+    assert lib.comba_chunk_fwd(None, *[ctypes.c_void_p(FAKE)] * 9, ctypes.c_void_p(FAKE),
+                               ctypes.c_size_t(1 << 40), None) == ENULL
+
+
+def test_rejects_small_workspace():
+    s = shape(B=2, T=256, H=4)
+    need = comba.load_library().comba_fwd_workspace_bytes(ctypes.byref(s))
+    assert fwd(s, ws_bytes=need - 1) == EWS
+    needb = comba.load_library().comba_bwd_workspace_bytes(ctypes.byref(s))
+    assert bwd(s, ws_bytes=needb - 1) == EWS
