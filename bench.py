@@ -1,0 +1,236 @@
+#!/usr/bin/env python3
+"""Benchmark of the chunk-wise Comba forward + backward on one MI355X.
+
+One step = one pass of the whole hot path over one batch: comba_chunk_fwd
+(chunk tables, gates/score matrix/UT inverse, state scan fused with the
+output) followed by comba_chunk_bwd (which recomputes the forward states, runs
+the reverse state scan and the intra-chunk gradients).  Workload: the 1.3B-model
+layer shape, B=4, H=16, T=4096, dk=dv=128, chunk 64, bf16 inputs, fp32 state and
+outputs, seeded synthetic inputs (comba_inputs, PCG64).
+
+Prints one JSON line with the whole-job throughput in tokens/s, the roofline of
+the dominant kernel (timed live with HIP events on the library's stream over
+the timed region) and the fp64 CPU oracle timed on this host's cores on a
+bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+# MI355X published peaks
+PEAK_HBM_GBS = 8000.0          # HBM3E, GB/s
+PEAK_BF16_TFLOPS = 2500.0      # dense bf16 MFMA
+RIDGE = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)   # flop / byte
+WORKLOAD_INDEX = 3             # l1p3b_fwdbwd
+
+
+def stage_model(name, B, T, H, dk, dv, C=64, in_bytes=2):
+    """Algorithmic (flops, bytes) of one launch of a kernel stage.
+
+    Per chunk-head (C tokens of one head) the dense products the stage performs
+    (2 m n k flops each) and the HBM bytes it must move at minimum (each operand
+    read once, each result written once; L2 re-reads excluded).
+    """
+    nch = B * math.ceil(T / C) * H
+    f4 = 4
+    if name == "prep":            # K K^T, Q K^T; read q, k, g, beta; write M, A, G
+        fl = 4 * C * C * dk
+        by = C * 2 * dk * in_bytes + C * (f4 + in_bytes) + 2 * C * C * f4 + C * f4
+    elif name == "scan_fwd":      # K X, Q X, M R, A D, K^T D; read q,k,v,M,A,G,beta; write o
+        fl = 6 * C * dk * dv + 4 * C * C * dv
+        by = C * (2 * dk + dv) * in_bytes + 2 * C * C * f4 + C * (f4 + in_bytes) + C * dv * f4
+    elif name == "scan_fwd_store":  # K X, M R, K^T D; read k,v,M,G,beta; write X, D
+        fl = 4 * C * dk * dv + 2 * C * C * dv
+        by = C * (dk + dv) * in_bytes + C * C * f4 + C * (f4 + in_bytes) + dk * dv * f4 + C * dv * f4
+    elif name == "scan_bwd":      # K Y, A^T dO, M^T dD, Q^T Pg, K^T W2; read q,k,dO,A,M,G,beta; write Y, dR
+        fl = 6 * C * dk * dv + 4 * C * C * dv
+        by = C * (2 * dk + dv) * in_bytes + 2 * C * C * f4 + C * (f4 + in_bytes) + dk * dv * f4 + C * dv * f4
+    elif name == "intra_bwd":     # 3 C x dk x dv, 2 C x C x dv, 5 C x C x dk products
+        fl = 6 * C * dk * dv + 4 * C * C * dv + 10 * C * C * dk
+        by = (C * (2 * dk + 2 * dv) * in_bytes + 2 * dk * dv * f4 + 2 * C * dv * f4 + C * (f4 + in_bytes)
+              + C * (2 * dk + dv) * f4 + 2 * C * f4)
+    else:
+        return 0.0, 0.0
+    return float(fl * nch), float(by * nch)
+
+
+def op_flops(B, T, H, dk, dv, C=64):
+    """Algorithmic fwd+bwd flops of the chunk-wise method (no recomputation)."""
+    nch = B * math.ceil(T / C) * H
+    fwd = 2 * C * C * (3 * dk + 2 * dv) + 6 * C * dk * dv
+    bwd = 12 * C * C * dk + 8 * C * C * dv + 12 * C * dk * dv + 4 * C ** 3
+    return float((fwd + bwd) * nch)
+
+
+def kernel_source_sha():
+    h = hashlib.sha256()
+    for f in ("comba_kernels.hip", "comba_device.hpp"):
+        with open(os.path.join(ROOT, "paper_2506_02475_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel, launches_per_step=1):
+    """HBM bytes per launch from committed rocprofv3 counter summaries, if they
+    were taken on the current kernel source (else None)."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_sha") != kernel_source_sha():
+        return None
+    k = rec.get("kernels", {}).get(kernel)
+    if not k:
+        return None
+    return float(k["bytes_per_launch"])
+
+
+def cpu_baseline(w, heads_sample, threads):
+    import oracle
+
+    t0 = time.perf_counter()
+    oracle.workload_fwd(w, heads=heads_sample, nthreads=threads)
+    oracle.workload_bwd(w, heads=heads_sample, nthreads=threads)
+    dt = time.perf_counter() - t0
+    tokens = w.B * w.T * len(heads_sample) / w.H   # layer-equivalent tokens
+    return {"value": tokens / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": "fp64 step recurrence fwd+bwd on %d of %d heads x all %d rows x T=%d "
+                      "(%.1f s wall), scaled to the full layer" % (len(heads_sample), w.H, w.B,
+                                                                  w.T, dt)}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this benchmark runs on exactly one GPU (the operator is measured "
+              "on one MI355X); got --gpus %d, WORLD_SIZE %d" % (args.gpus, world),
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2506_02475_amd as comba
+    from comba_inputs import WORKLOADS, generate
+
+    spec = WORKLOADS[WORKLOAD_INDEX]
+    w = generate(WORKLOAD_INDEX)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    bf = torch.bfloat16
+
+    def t(x, dt=torch.float32):
+        return None if x is None else torch.from_numpy(np.ascontiguousarray(x)).to(dev, dt)
+
+    q, k, v = t(w.q, bf), t(w.k, bf), t(w.v, bf)
+    g, beta, d, h0 = t(w.g), t(w.beta, bf), t(w.d), t(w.h0)
+    dO = t(w.dO, bf)
+    B, T, H, dk, dv = w.B, w.T, w.H, w.dk, w.dv
+    ws_f = torch.empty(comba.fwd_workspace_bytes(B, T, H, dk, dv), dtype=torch.uint8, device=dev)
+    ws_b = torch.empty(comba.bwd_workspace_bytes(B, T, H, dk, dv), dtype=torch.uint8, device=dev)
+
+    def step():
+        o, ht = comba.comba_chunk_fwd(q, k, v, g, beta, d, h0, workspace=ws_f)
+        gr = comba.comba_chunk_bwd(q, k, v, g, beta, d, h0, dO, None, workspace=ws_b)
+        return o, gr
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    comba.profile_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    stages = comba.profile_read()
+    comba.profile_enable(False)
+
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    tokens = B * T
+    value = tokens / ((t1 - t0) / args.steps)
+
+    # per-stage average launch duration (ms) over the timed region
+    agg = {}
+    for name, ms in stages:
+        s = agg.setdefault(name, [0.0, 0])
+        s[0] += ms
+        s[1] += 1
+    avg = {n: s[0] / s[1] for n, s in agg.items()}
+    tot = {n: s[0] / args.steps for n, s in agg.items()}
+    dom = max(tot, key=tot.get)
+    fl, by = stage_model(dom, B, T, H, dk, dv)
+    sec = avg[dom] * 1e-3
+    intensity = fl / by if by else 0.0
+    traffic = measured_traffic(dom)
+    if intensity < RIDGE:
+        achieved = by / sec / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
+    else:
+        achieved = fl / sec / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4)}
+    roof["traffic"] = traffic
+    roof["kernel"] = dom
+    roof["avg_launch_ms"] = round(avg[dom], 4)
+    roof["algorithmic_bytes"] = by
+    roof["algorithmic_flops"] = fl
+    op_fl = op_flops(B, T, H, dk, dv)
+    mfma_frac_op = op_fl / (ms_per_step * 1e-3) / (PEAK_BF16_TFLOPS * 1e12)
+
+    result = {
+        "metric": "Comba fwd+bwd tokens/sec at H=16,T=4096,d=128 bf16; % MFMA peak",
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded PCG64; q,k L2-normalised, log alpha=-softplus(N(0,1)), "
+                "beta=sigmoid(N(0,1)), d~U(0,1))",
+        "config": {"workload": spec.name, "B": B, "T": T, "H": H, "dk": dk, "dv": dv,
+                   "chunk": 64, "in_dtype": "bf16", "out_dtype": "f32"},
+        "mfma_pct_peak_op": round(100.0 * mfma_frac_op, 3),
+        "op_algorithmic_tflops": round(op_fl / (ms_per_step * 1e-3) / 1e12, 2),
+        "stages_ms": {n: round(x, 4) for n, x in tot.items()},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        try:
+            threads = len(os.sched_getaffinity(0))
+        except Exception:
+            threads = os.cpu_count() or 1
+        nh = min(H, max(1, math.ceil(2 * threads / B)))
+        heads = list(range(0, H, max(1, H // nh)))[:nh]
+        result["cpu_baseline"] = cpu_baseline(w, heads, threads)
+    else:
+        result["cpu_baseline"] = None
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

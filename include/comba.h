@@ -109,6 +109,21 @@ comba_status comba_chunk_bwd(const comba_shape *shape, const void *q, const void
                              float *dk, float *dv, float *dg, float *dbeta, float *dd,
                              float *dh0, void *ws, size_t ws_bytes, void *stream);
 
+/*
+ * Stage timing, for benchmarks (not part of the method).  comba_profile_enable(1)
+ * starts a recording session on the calling host thread: every following
+ * comba_chunk_fwd / comba_chunk_bwd call on this thread records a HIP event on
+ * its stream before each kernel stage and after its last stage (at most 4096
+ * events per session; calls beyond that are not recorded).  Events are created
+ * on first use on the current device and reused until the process ends.
+ * comba_profile_read waits for the last recorded event and writes, in call
+ * order, up to `capacity` stage durations in milliseconds (`ms`) and static
+ * stage names (`names`; either may be NULL).  It returns the number written,
+ * or -1 on a HIP error.  comba_profile_enable(0) stops recording (the default).
+ */
+comba_status comba_profile_enable(int enable);
+int comba_profile_read(float *ms, const char **names, int capacity);
+
 /* Human-readable name of a status code (static storage). */
 const char *comba_status_string(comba_status status);
 

@@ -24,6 +24,7 @@ import re
 import threading
 
 __all__ = ["comba_chunk_fwd", "comba_chunk_bwd", "load_library", "library_path",
+           "profile_enable", "profile_read",
            "fwd_workspace_bytes", "bwd_workspace_bytes", "exported_symbols", "CombaError",
            "CombaShape", "COMBA_F32", "COMBA_BF16", "CHUNK"]
 
@@ -72,10 +73,30 @@ def load_library():
             lib.comba_chunk_fwd.restype = I
             lib.comba_chunk_bwd.argtypes = [SP] + [P] * 16 + [P, Z, P]
             lib.comba_chunk_bwd.restype = I
+            lib.comba_profile_enable.argtypes = [I]
+            lib.comba_profile_enable.restype = I
+            lib.comba_profile_read.argtypes = [P, P, I]
+            lib.comba_profile_read.restype = I
             lib.comba_status_string.argtypes = [I]
             lib.comba_status_string.restype = ctypes.c_char_p
             _lib = lib
     return _lib
+
+
+def profile_enable(on: bool = True) -> None:
+    """Turn per-stage HIP-event timing of the entry points on or off (this thread)."""
+    _check(load_library().comba_profile_enable(1 if on else 0))
+
+
+def profile_read(capacity: int = 4096):
+    """(stage name, ms) of every stage recorded since profile_enable(True)."""
+    cap = capacity
+    ms = (ctypes.c_float * cap)()
+    names = (ctypes.c_char_p * cap)()
+    n = load_library().comba_profile_read(ms, names, cap)
+    if n < 0:
+        raise CombaError("comba: profile_read failed")
+    return [(names[i].decode(), float(ms[i])) for i in range(n)]
 
 
 def exported_symbols():

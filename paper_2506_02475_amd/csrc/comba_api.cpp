@@ -3,6 +3,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <vector>
+
 #include "comba.h"
 #include "comba_launch.h"
 
@@ -87,6 +89,41 @@ Layout layout(const Dims& d, bool bwd) {
 
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
+// Per-thread stage timing (comba_profile_enable / comba_profile_read).  A
+// session records, for every call, one event before each kernel stage and one
+// after the last; events come from a pool that is created on demand and
+// reused by later sessions.
+constexpr size_t kMaxEvents = 4096;
+constexpr size_t kMaxMarksPerCall = 16;
+struct Profile {
+  bool on = false;
+  size_t n = 0;
+  std::vector<hipEvent_t> ev;
+  std::vector<const char*> names;
+};
+thread_local Profile g_prof;
+
+void prof_mark(void* ctx, hipStream_t st, const char* name) {
+  Profile* p = static_cast<Profile*>(ctx);
+  if (p->n == p->ev.size()) {
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return;
+    p->ev.push_back(e);
+    p->names.push_back(nullptr);
+  }
+  if (hipEventRecord(p->ev[p->n], st) != hipSuccess) return;
+  p->names[p->n] = name;
+  ++p->n;
+}
+
+void attach_profile(comba::LaunchArgs& a) {
+  // a call records at most kMaxMarksPerCall marks; stop at the pool limit so
+  // that no call is recorded partially
+  if (!g_prof.on || g_prof.n + kMaxMarksPerCall > kMaxEvents) return;
+  a.hook.mark = prof_mark;
+  a.hook.ctx = &g_prof;
+}
+
 void carve(comba::LaunchArgs& a, const Layout& L, void* ws, bool bwd) {
   char* base = static_cast<char*>(ws);
   a.cmap = reinterpret_cast<comba::ChunkInfo*>(base + L.cmap);
@@ -157,6 +194,7 @@ comba_status comba_chunk_fwd(const comba_shape* shape, const void* q, const void
   a.ht = ht;
   a.stream = static_cast<hipStream_t>(stream);
   carve(a, L, ws, false);
+  attach_profile(a);
   if (dm.N == 0) return COMBA_OK;
   return comba::launch_fwd(a) == hipSuccess ? COMBA_OK : COMBA_ERR_HIP;
 }
@@ -200,7 +238,29 @@ comba_status comba_chunk_bwd(const comba_shape* shape, const void* q, const void
   a.dh0 = dh0;
   a.stream = static_cast<hipStream_t>(stream);
   carve(a, L, ws, true);
+  attach_profile(a);
   return comba::launch_bwd(a) == hipSuccess ? COMBA_OK : COMBA_ERR_HIP;
+}
+
+comba_status comba_profile_enable(int enable) {
+  g_prof.on = enable != 0;
+  g_prof.n = 0;
+  return COMBA_OK;
+}
+
+int comba_profile_read(float* ms, const char** names, int capacity) {
+  if (g_prof.n < 2) return 0;
+  if (hipEventSynchronize(g_prof.ev[g_prof.n - 1]) != hipSuccess) return -1;
+  int out = 0;
+  for (size_t i = 0; i + 1 < g_prof.n && out < capacity; ++i) {
+    if (!g_prof.names[i]) continue;  // end-of-call mark
+    float t = 0.f;
+    if (hipEventElapsedTime(&t, g_prof.ev[i], g_prof.ev[i + 1]) != hipSuccess) return -1;
+    if (ms) ms[out] = t;
+    if (names) names[out] = g_prof.names[i];
+    ++out;
+  }
+  return out;
 }
 
 const char* comba_status_string(comba_status s) {

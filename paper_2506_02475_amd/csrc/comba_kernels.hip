@@ -796,12 +796,16 @@ static hipError_t run_fwd(const LaunchArgs& a) {
   const Tin* k = static_cast<const Tin*>(a.k);
   const Tin* v = static_cast<const Tin*>(a.v);
   const Tin* beta = static_cast<const Tin*>(a.beta);
+  a.stage("chunk_map");
   k_chunk_map<<<1, NTHR, 0, st>>>(a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.ncmax, a.cmap, a.smap);
+  a.stage("prep");
   if (a.ncmax > 0)
     k_prep<Tin, DK><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(q, k, a.g, beta, a.d, a.cmap, a.H, a.Mw,
                                                          a.Aw, a.Gw);
+  a.stage("scan_fwd");
   k_scan_fwd<Tin, DK, DV, true, false><<<dim3(a.N, a.H, DV / 32), NTHR, 0, st>>>(
       q, k, v, beta, a.d, a.h0, a.cmap, a.smap, a.H, a.Mw, a.Aw, a.Gw, a.o, a.ht, nullptr, nullptr);
+  a.stage(nullptr);
   return hipGetLastError();
 }
 
@@ -818,20 +822,27 @@ static hipError_t run_bwd(const LaunchArgs& a) {
     k_reduce_dd<<<a.H, NTHR, 0, st>>>(a.ddp, 0, a.H, a.dd);
     return hipGetLastError();
   }
+  a.stage("chunk_map");
   k_chunk_map<<<1, NTHR, 0, st>>>(a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.ncmax, a.cmap, a.smap);
+  a.stage("prep");
   if (a.ncmax > 0)
     k_prep<Tin, DK><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(q, k, a.g, beta, a.d, a.cmap, a.H, a.Mw,
                                                          a.Aw, a.Gw);
+  a.stage("scan_fwd_store");
   k_scan_fwd<Tin, DK, DV, false, true><<<dim3(a.N, a.H, DV / 32), NTHR, 0, st>>>(
       q, k, v, beta, a.d, a.h0, a.cmap, a.smap, a.H, a.Mw, a.Aw, a.Gw, nullptr, nullptr, a.Xw,
       a.Dw);
+  a.stage("scan_bwd");
   k_scan_bwd<Tin, DK, DV><<<dim3(a.N, a.H, DV / 32), NTHR, 0, st>>>(
       q, k, dO, beta, a.d, a.dht, a.cmap, a.smap, a.H, a.Mw, a.Aw, a.Gw, a.dh0, a.Yw, a.dRw);
+  a.stage("intra_bwd");
   if (a.ncmax > 0)
     k_intra_bwd<Tin, DK, DV><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
         q, k, v, dO, beta, a.d, a.cmap, a.H, a.Gw, a.Xw, a.Dw, a.Yw, a.dRw, a.dq, a.dk_, a.dv_,
         a.dbeta, a.dg, a.ddp);
+  a.stage("reduce_dd");
   k_reduce_dd<<<a.H, NTHR, 0, st>>>(a.ddp, a.ncmax, a.H, a.dd);
+  a.stage(nullptr);
   return hipGetLastError();
 }
 

@@ -16,6 +16,13 @@ struct SeqInfo {
   int32_t chunk0, nchunks, tok0, len;
 };
 
+// Optional per-stage timing hook: mark() is called before every kernel stage
+// with its name and once after the last stage with name == nullptr.
+struct StageHook {
+  void (*mark)(void* ctx, hipStream_t stream, const char* name);
+  void* ctx;
+};
+
 struct LaunchArgs {
   bool bf16;
   int dk, dv, H, N, Tseq, Ttot, ncmax;
@@ -31,6 +38,10 @@ struct LaunchArgs {
   float *Xw, *Dw, *Yw, *dRw;      // per chunk-head: X (dk x dv), D (64 x dv), Y, dR
   float* ddp;                     // per chunk-head partial dd
   hipStream_t stream;
+  StageHook hook;
+  void stage(const char* name) const {
+    if (hook.mark) hook.mark(hook.ctx, stream, name);
+  }
 };
 
 hipError_t launch_fwd(const LaunchArgs& a);

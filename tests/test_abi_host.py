@@ -47,13 +47,20 @@ def bwd(shp, ws_bytes=1 << 40, **over):
 def test_library_exports_every_declared_symbol():
     declared = comba.exported_symbols()
     assert set(declared) == {"comba_fwd_workspace_bytes", "comba_bwd_workspace_bytes",
-                             "comba_chunk_fwd", "comba_chunk_bwd", "comba_status_string"}
+                             "comba_chunk_fwd", "comba_chunk_bwd", "comba_status_string",
+                             "comba_profile_enable", "comba_profile_read"}
     out = subprocess.run(["nm", "-D", "--defined-only", comba.library_path()],
                          capture_output=True, text=True, check=True).stdout
     exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
     for name in declared:
         assert name in exported, name
         assert hasattr(comba.load_library(), name)
+
+
+def test_profile_read_without_calls_is_empty():
+    comba.profile_enable(True)
+    assert comba.profile_read() == []
+    comba.profile_enable(False)
 
 
 def test_status_strings():
