@@ -79,21 +79,23 @@ def kernel_source_sha():
     return h.hexdigest()[:16]
 
 
-def measured_traffic(kernel, launches_per_step=1):
-    """HBM bytes per launch from committed rocprofv3 counter summaries, if they
-    were taken on the current kernel source (else None)."""
-    path = os.path.join(ROOT, "profiles", "traffic.json")
+def measured_traffic(kernel):
+    """HBM bytes per launch of a kernel stage from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE summary (scaled by a plain copy of known size), if
+    the counters were taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic_counters_l1p3b_fwdbwd.md")
     try:
         with open(path) as f:
-            rec = json.load(f)
-    except (OSError, ValueError):
+            text = f.read()
+        rec = json.loads(text.split("```json", 1)[1].split("```", 1)[0])
+    except (OSError, ValueError, IndexError):
         return None
     if rec.get("source_sha") != kernel_source_sha():
         return None
     k = rec.get("kernels", {}).get(kernel)
     if not k:
         return None
-    return float(k["bytes_per_launch"])
+    return round(float(k["bytes_per_launch"]))
 
 
 def cpu_baseline(w, heads_sample, threads):
@@ -116,6 +118,9 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-bytes", type=int, default=0,
+                    help="after the timed steps, run one plain device-to-device copy of this "
+                         "many bytes (calibrates HBM traffic counters against a known size)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -219,6 +224,14 @@ def main():
         "stages_ms": {n: round(x, 4) for n, x in tot.items()},
         "roofline": roof,
     }
+    if args.copy_bytes > 0:
+        n = args.copy_bytes // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        result["copy_bytes"] = n * 4
     if not args.no_cpu_baseline:
         try:
             threads = len(os.sched_getaffinity(0))
