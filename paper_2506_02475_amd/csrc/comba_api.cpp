@@ -59,7 +59,7 @@ comba_status check_shape(const comba_shape* s, Dims* out) {
 }
 
 struct Layout {
-  size_t cmap, smap, M, A, G, X, D, Y, dR, ddp, total;
+  size_t cmap, smap, M, A, G, X, D, Y, dR, ddp, MT, AT, KT, QT, Xfin, sink, total;
 };
 
 Layout layout(const Dims& d, bool bwd) {
@@ -71,11 +71,23 @@ Layout layout(const Dims& d, bool bwd) {
     off += round_up(bytes);
     return at;
   };
+  L.sink = take(1024);
   L.cmap = take((size_t)d.ncmax * sizeof(comba::ChunkInfo));
   L.smap = take((size_t)(d.N > 0 ? d.N : 1) * sizeof(comba::SeqInfo));
   L.M = take(chh * kChunk * kChunk * sizeof(float));
   L.A = take(chh * kChunk * kChunk * sizeof(float));
   L.G = take(chh * kChunk * sizeof(float));
+  if (d.bf16) {
+    // bf16 path: M and A regions hold (hi, lo) bf16 pairs; K^T per chunk;
+    // the backward also keeps M^T, A^T (hi, lo) and Q^T
+    L.KT = take(chh * d.dk * kChunk * sizeof(uint16_t));
+    if (bwd) {
+      L.MT = take(chh * 2 * kChunk * kChunk * sizeof(uint16_t));
+      L.AT = take(chh * 2 * kChunk * kChunk * sizeof(uint16_t));
+      L.QT = take(chh * d.dk * kChunk * sizeof(uint16_t));
+      L.Xfin = take((size_t)(d.N > 0 ? d.N : 1) * d.H * d.dk * d.dv * sizeof(float));
+    }
+  }
   if (bwd) {
     L.X = take(chh * d.dk * d.dv * sizeof(float));
     L.D = take(chh * kChunk * d.dv * sizeof(float));
@@ -131,6 +143,14 @@ void carve(comba::LaunchArgs& a, const Layout& L, void* ws, bool bwd) {
   a.Mw = reinterpret_cast<float*>(base + L.M);
   a.Aw = reinterpret_cast<float*>(base + L.A);
   a.Gw = reinterpret_cast<float*>(base + L.G);
+  a.sink = reinterpret_cast<float*>(base + L.sink);
+  if (L.Xfin) a.Xfin = reinterpret_cast<float*>(base + L.Xfin);
+  a.Mp = reinterpret_cast<uint16_t*>(base + L.M);
+  a.Ap = reinterpret_cast<uint16_t*>(base + L.A);
+  if (L.KT) a.KTp = reinterpret_cast<uint16_t*>(base + L.KT);
+  if (L.MT) a.MTp = reinterpret_cast<uint16_t*>(base + L.MT);
+  if (L.AT) a.ATp = reinterpret_cast<uint16_t*>(base + L.AT);
+  if (L.QT) a.QTp = reinterpret_cast<uint16_t*>(base + L.QT);
   if (bwd) {
     a.Xw = reinterpret_cast<float*>(base + L.X);
     a.Dw = reinterpret_cast<float*>(base + L.D);

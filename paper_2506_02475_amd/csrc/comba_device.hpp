@@ -161,38 +161,65 @@ __device__ __forceinline__ float wave_sum(float x) {
   return sum_groups(sum16(x));
 }
 
-// ---- global -> LDS tile copies ---------------------------------------------
+// ---- global -> register -> LDS tile copies ---------------------------------
 
-// Copy `rows` rows of `cols` elements (row stride gs in global memory) into LDS
-// row-major with stride ld; rows in [rows, nrows) are zero-filled.  cols must
-// be a multiple of 16 bytes' worth of elements; all threads participate.
+// A NROWS x COLS tile of T held in registers, 16 bytes per slot, slots spread
+// over the workgroup's threads.  load() issues every global load of the tile
+// back to back (rows >= `rows` read as zero) so their latencies overlap; the
+// store functions then write LDS.  Keeping load() and store() apart lets a
+// kernel issue the next chunk's loads before computing on the current one.
+template <typename T, int NROWS, int COLS>
+struct TileRegs {
+  static constexpr int V = 16 / sizeof(T);
+  static constexpr int PER_ROW = COLS / V;
+  static constexpr int TOTAL = NROWS * PER_ROW;
+  static constexpr int ITER = (TOTAL + NTHR - 1) / NTHR;
+  static_assert(COLS % V == 0, "tile rows must be whole 16-byte units");
+  uint4 r[ITER];
+
+  __device__ __forceinline__ void load(const T* __restrict__ g, long gs, int rows) {
+#pragma unroll
+    for (int it = 0; it < ITER; ++it) {
+      const int idx = threadIdx.x + it * NTHR;
+      const int rr = idx / PER_ROW, cc = (idx % PER_ROW) * V;
+      uint4 val = make_uint4(0, 0, 0, 0);
+      if ((TOTAL % NTHR == 0 || idx < TOTAL) && rr < rows)
+        val = *reinterpret_cast<const uint4*>(g + (long)rr * gs + cc);
+      r[it] = val;
+    }
+  }
+  __device__ __forceinline__ void store(T* s, int ld) const {
+#pragma unroll
+    for (int it = 0; it < ITER; ++it) {
+      const int idx = threadIdx.x + it * NTHR;
+      if (TOTAL % NTHR == 0 || idx < TOTAL) {
+        const int rr = idx / PER_ROW, cc = (idx % PER_ROW) * V;
+        *reinterpret_cast<uint4*>(s + rr * ld + cc) = r[it];
+      }
+    }
+  }
+  // st[c * ldt + r] = tile[r][c]
+  __device__ __forceinline__ void store_t(T* st, int ldt) const {
+#pragma unroll
+    for (int it = 0; it < ITER; ++it) {
+      const int idx = threadIdx.x + it * NTHR;
+      if (TOTAL % NTHR == 0 || idx < TOTAL) {
+        const int rr = idx / PER_ROW, cc = (idx % PER_ROW) * V;
+        union { uint4 u; T e[V]; } val;
+        val.u = r[it];
+#pragma unroll
+        for (int e = 0; e < V; ++e) st[(cc + e) * ldt + rr] = val.e[e];
+      }
+    }
+  }
+};
+
+// One-shot copies (load then store) for tiles that are not prefetched.
 template <typename T, int NROWS, int COLS>
 __device__ __forceinline__ void tile_to_lds(const T* __restrict__ g, long gs, int rows, T* s, int ld) {
-  constexpr int V = 16 / sizeof(T);
-  constexpr int PER_ROW = COLS / V;
-  for (int idx = threadIdx.x; idx < NROWS * PER_ROW; idx += NTHR) {
-    const int rr = idx / PER_ROW, cc = (idx % PER_ROW) * V;
-    uint4 val = make_uint4(0, 0, 0, 0);
-    if (rr < rows) val = *reinterpret_cast<const uint4*>(g + (long)rr * gs + cc);
-    *reinterpret_cast<uint4*>(s + rr * ld + cc) = val;
-  }
-}
-
-// Same copy, also (or only) writing the transpose: st[c * ldt + r] = tile[r][c].
-template <typename T, int NROWS, int COLS, bool ROWMAJOR>
-__device__ __forceinline__ void tile_to_lds_t(const T* __restrict__ g, long gs, int rows, T* s, int ld,
-                                              T* st, int ldt) {
-  constexpr int V = 16 / sizeof(T);
-  constexpr int PER_ROW = COLS / V;
-  for (int idx = threadIdx.x; idx < NROWS * PER_ROW; idx += NTHR) {
-    const int rr = idx / PER_ROW, cc = (idx % PER_ROW) * V;
-    union { uint4 u; T e[V]; } val;
-    val.u = make_uint4(0, 0, 0, 0);
-    if (rr < rows) val.u = *reinterpret_cast<const uint4*>(g + (long)rr * gs + cc);
-    if constexpr (ROWMAJOR) *reinterpret_cast<uint4*>(s + rr * ld + cc) = val.u;
-#pragma unroll
-    for (int e = 0; e < V; ++e) st[(cc + e) * ldt + rr] = val.e[e];
-  }
+  TileRegs<T, NROWS, COLS> t;
+  t.load(g, gs, rows);
+  t.store(s, ld);
 }
 
 // Inclusive prefix sum across the 64 lanes of a wavefront.

@@ -141,8 +141,13 @@ __global__ __launch_bounds__(NTHR) void k_prep(const Tin* __restrict__ q, const 
   const long tok = (long)ci.tok0 * H + h;
   const int w = wave_id(), lane = lane_id();
 
-  tile_to_lds<Tin, CH, DK>(k + tok * DK, (long)H * DK, ci.len, Ks, LDK);
-  tile_to_lds<Tin, CH, DK>(q + tok * DK, (long)H * DK, ci.len, Qs, LDK);
+  {
+    TileRegs<Tin, CH, DK> kr, qr;
+    kr.load(k + tok * DK, (long)H * DK, ci.len);
+    qr.load(q + tok * DK, (long)H * DK, ci.len);
+    kr.store(Ks, LDK);
+    qr.store(Qs, LDK);
+  }
   if (w == 0) {
     const float gr = lane < ci.len ? g[tok + (long)lane * H] : 0.f;
     const float G = wave_prefix_sum(gr);
@@ -250,21 +255,43 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd(
         XT[jj * LDX + i] = X[mt][nt][e];
       }
 
-  for (int cc = 0; cc < si.nchunks; ++cc) {
-    const int c = si.chunk0 + cc;
-    const ChunkInfo ci = cmap[c];
-    const long chh = (long)c * H + h;
-    const long tok = (long)ci.tok0 * H + h;
-    __syncthreads();
-    tile_to_lds_t<Tin, CH, DK, true>(k + tok * DK, (long)H * DK, ci.len, Ks, LDK, KsT, LDC);
-    if constexpr (OUT) tile_to_lds<Tin, CH, DK>(q + tok * DK, (long)H * DK, ci.len, Qs, LDK);
-    tile_to_lds<Tin, CH, BV>(v + tok * DV + j0, (long)H * DV, ci.len, Vs, LDV);
-    tile_to_lds<float, CH, CH>(Mw + chh * CH * CH, CH, CH, Ms, LDF);
-    if constexpr (OUT) tile_to_lds<float, CH, CH>(Aw + chh * CH * CH, CH, CH, As, LDF);
+  // registers holding the next chunk's tiles (loaded one chunk ahead)
+  TileRegs<Tin, CH, DK> pk, pq;
+  TileRegs<Tin, CH, BV> pv;
+  TileRegs<float, CH, CH> pm, pa;
+  float pg = 0.f, pb = 0.f;
+  auto issue = [&](int cc) {
+    const int len = min(CH, si.len - cc * CH);
+    const long chh = (long)(si.chunk0 + cc) * H + h;
+    const long tok = (long)(si.tok0 + cc * CH) * H + h;
+    pk.load(k + tok * DK, (long)H * DK, len);
+    if constexpr (OUT) pq.load(q + tok * DK, (long)H * DK, len);
+    pv.load(v + tok * DV + j0, (long)H * DV, len);
+    pm.load(Mw + chh * CH * CH, CH, CH);
+    if constexpr (OUT) pa.load(Aw + chh * CH * CH, CH, CH);
     if (threadIdx.x < CH) {
       const int r = threadIdx.x;
-      Gs[r] = Gw[chh * CH + r];
-      Bs[r] = r < ci.len ? to_f(beta[tok + (long)r * H]) : 0.f;
+      pg = Gw[chh * CH + r];
+      pb = r < len ? to_f(beta[tok + (long)r * H]) : 0.f;
+    }
+  };
+  if (si.nchunks > 0) issue(0);
+
+  for (int cc = 0; cc < si.nchunks; ++cc) {
+    const long chh = (long)(si.chunk0 + cc) * H + h;
+    const long tok = (long)(si.tok0 + cc * CH) * H + h;
+    ChunkInfo ci;
+    ci.len = min(CH, si.len - cc * CH);
+    __syncthreads();
+    pk.store(Ks, LDK);
+    pk.store_t(KsT, LDC);
+    if constexpr (OUT) pq.store(Qs, LDK);
+    pv.store(Vs, LDV);
+    pm.store(Ms, LDF);
+    if constexpr (OUT) pa.store(As, LDF);
+    if (threadIdx.x < CH) {
+      Gs[threadIdx.x] = pg;
+      Bs[threadIdx.x] = pb;
     }
     if constexpr (STORE) {
 #pragma unroll
@@ -278,6 +305,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd(
           }
     }
     __syncthreads();
+    if (cc + 1 < si.nchunks) issue(cc + 1);
     const float Glast = Gs[CH - 1];
 
     // K X and Q X for rows 16w..16w+15; R = Diag(beta)(V - Diag(exp Gm) K X)
@@ -403,21 +431,39 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd(
         YT[jj * LDX + i] = Y[mt][nt][e];
       }
 
-  for (int cc = si.nchunks - 1; cc >= 0; --cc) {
-    const int c = si.chunk0 + cc;
-    const ChunkInfo ci = cmap[c];
-    const long chh = (long)c * H + h;
-    const long tok = (long)ci.tok0 * H + h;
-    __syncthreads();
-    tile_to_lds_t<Tin, CH, DK, true>(k + tok * DK, (long)H * DK, ci.len, Ks, LDK, KsT, LDC);
-    tile_to_lds_t<Tin, CH, DK, false>(q + tok * DK, (long)H * DK, ci.len, nullptr, 0, QsT, LDC);
-    tile_to_lds_t<Tin, CH, BV, false>(dO + tok * DV + j0, (long)H * DV, ci.len, nullptr, 0, dOT, LDC);
-    tile_to_lds_t<float, CH, CH, false>(Aw + chh * CH * CH, CH, CH, nullptr, 0, AsT, LDF);
-    tile_to_lds_t<float, CH, CH, false>(Mw + chh * CH * CH, CH, CH, nullptr, 0, MsT, LDF);
+  TileRegs<Tin, CH, DK> pk, pq;
+  TileRegs<Tin, CH, BV> pdo;
+  TileRegs<float, CH, CH> pm, pa;
+  float pg = 0.f, pb = 0.f;
+  auto issue = [&](int cc) {
+    const int len = min(CH, si.len - cc * CH);
+    const long chh = (long)(si.chunk0 + cc) * H + h;
+    const long tok = (long)(si.tok0 + cc * CH) * H + h;
+    pk.load(k + tok * DK, (long)H * DK, len);
+    pq.load(q + tok * DK, (long)H * DK, len);
+    pdo.load(dO + tok * DV + j0, (long)H * DV, len);
+    pa.load(Aw + chh * CH * CH, CH, CH);
+    pm.load(Mw + chh * CH * CH, CH, CH);
     if (threadIdx.x < CH) {
       const int r = threadIdx.x;
-      Gs[r] = Gw[chh * CH + r];
-      Bs[r] = r < ci.len ? to_f(beta[tok + (long)r * H]) : 0.f;
+      pg = Gw[chh * CH + r];
+      pb = r < len ? to_f(beta[tok + (long)r * H]) : 0.f;
+    }
+  };
+  if (si.nchunks > 0) issue(si.nchunks - 1);
+
+  for (int cc = si.nchunks - 1; cc >= 0; --cc) {
+    const long chh = (long)(si.chunk0 + cc) * H + h;
+    __syncthreads();
+    pk.store(Ks, LDK);
+    pk.store_t(KsT, LDC);
+    pq.store_t(QsT, LDC);
+    pdo.store_t(dOT, LDC);
+    pa.store_t(AsT, LDF);
+    pm.store_t(MsT, LDF);
+    if (threadIdx.x < CH) {
+      Gs[threadIdx.x] = pg;
+      Bs[threadIdx.x] = pb;
     }
 #pragma unroll
     for (int mt = 0; mt < XMT; ++mt)
@@ -429,6 +475,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd(
           Yw[chh * DK * DV + (long)i * DV + j0 + jj] = Y[mt][nt][e];
         }
     __syncthreads();
+    if (cc > 0) issue(cc - 1);
     const float Glast = Gs[CH - 1];
 
     // dD = A^T dO + Diag(exp(G_63 - G)) K Y
@@ -570,15 +617,28 @@ __global__ __launch_bounds__(NTHR, 1) void k_intra_bwd(
   zero_acc(dLr);
   float Fpart = 0.f, bv = 0.f;
   const int er = tid >> 2, ec = (tid & 3) * 8;  // elementwise ownership: row er, 8 columns
+  TileRegs<Tin, CH, VB> rdo, rv;
+  TileRegs<float, CH, VB> rdr, rdl;
+  TileRegs<float, DK, VB> rx, ry;
+  auto issue = [&](int vb) {
+    rdo.load(dO + tok * DV + vb * VB, (long)H * DV, len);
+    rv.load(v + tok * DV + vb * VB, (long)H * DV, len);
+    rdr.load(dRw + chh * CH * DV + vb * VB, DV, CH);
+    rdl.load(Dw + chh * CH * DV + vb * VB, DV, CH);
+    rx.load(Xw + chh * DK * DV + vb * VB, DV, DK);
+    ry.load(Yw + chh * DK * DV + vb * VB, DV, DK);
+  };
+  issue(0);
   for (int vb = 0; vb < DV / VB; ++vb) {
     __syncthreads();
-    tile_to_lds<Tin, CH, VB>(dO + tok * DV + vb * VB, (long)H * DV, len, dOb, LDVB);
-    tile_to_lds<Tin, CH, VB>(v + tok * DV + vb * VB, (long)H * DV, len, Vb, LDVB);
-    tile_to_lds<float, CH, VB>(dRw + chh * CH * DV + vb * VB, DV, CH, dRb, LDFB);
-    tile_to_lds<float, CH, VB>(Dw + chh * CH * DV + vb * VB, DV, CH, Dlb, LDFB);
-    tile_to_lds<float, DK, VB>(Xw + chh * DK * DV + vb * VB, DV, DK, Xb, LDFB);
-    tile_to_lds<float, DK, VB>(Yw + chh * DK * DV + vb * VB, DV, DK, Yb, LDFB);
+    rdo.store(dOb, LDVB);
+    rv.store(Vb, LDVB);
+    rdr.store(dRb, LDFB);
+    rdl.store(Dlb, LDFB);
+    rx.store(Xb, LDFB);
+    ry.store(Yb, LDFB);
     __syncthreads();
+    if (vb + 1 < DV / VB) issue(vb + 1);
     mma<F32, 1, NTK, VB>(T1, dOb + 16 * w * LDVB, LDVB, Xb, LDFB);
     mma<F32, 1, NTK, VB>(T3, dRb + 16 * w * LDFB, LDFB, Xb, LDFB);
     mma<F32, 1, NTK, VB>(T2, Dlb + 16 * w * LDFB, LDFB, Yb, LDFB);
@@ -611,8 +671,15 @@ __global__ __launch_bounds__(NTHR, 1) void k_intra_bwd(
   float* dAGT = dAG + CH * LDF;
   float* Bsym = dAGT + CH * LDF;
   float* dAkk = Bsym + CH * LDF;
-  tile_to_lds_t<Tin, CH, DK, true>(k + tok * DK, (long)H * DK, len, Ks, LDK, KsT, LDC);
-  tile_to_lds_t<Tin, CH, DK, true>(q + tok * DK, (long)H * DK, len, Qs, LDK, QsT, LDC);
+  {
+    TileRegs<Tin, CH, DK> kr, qr;
+    kr.load(k + tok * DK, (long)H * DK, len);
+    qr.load(q + tok * DK, (long)H * DK, len);
+    kr.store(Ks, LDK);
+    kr.store_t(KsT, LDC);
+    qr.store(Qs, LDK);
+    qr.store_t(QsT, LDC);
+  }
   __syncthreads();
   const float Glast = Gs[CH - 1];
 
@@ -786,6 +853,721 @@ __global__ __launch_bounds__(NTHR) void k_reduce_dd(const float* __restrict__ dd
   if (threadIdx.x == 0) dd[h] = part[0];
 }
 
+// ===========================================================================
+// bf16 path.  k_prep_bf writes every per-chunk operand the scans need in the
+// form the MFMA consumes: M, A (and for the backward M^T, A^T) as bf16 (hi, lo)
+// pairs, K^T (and Q^T) as bf16.  In the scans each wave then loads the
+// A-operand fragments of its own rows straight from global memory into
+// registers, one chunk ahead, and LDS only carries what the four waves
+// exchange (state, R, D and their backward counterparts), already split.
+// ===========================================================================
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// dv columns per scan workgroup: a chain (sequence, head) is split into
+// dv / SCAN_BV independent workgroups
+#ifndef COMBA_SCAN_BV
+#define COMBA_SCAN_BV 32
+#endif
+constexpr int SCAN_BV = COMBA_SCAN_BV;
+
+__device__ __forceinline__ floatx4 mfma16(const bf16x8& a, const bf16x8& b, const floatx4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ bf16x8 ld8(const bf16_t* p) { return *reinterpret_cast<const bf16x8*>(p); }
+__device__ __forceinline__ bf16x8 zero8() { return __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u}); }
+
+// four fp32 values -> bf16 (hi, lo) with hi + lo ~ x to ~16 significant bits
+__device__ __forceinline__ void split4(const float (&x)[4], bf16x4& hi, bf16x4& lo) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const __bf16 h = (__bf16)x[e];
+    hi[e] = h;
+    lo[e] = (__bf16)(x[e] - (float)h);
+  }
+}
+// store the 4 values a lane holds in one accumulator column (rows 4g..4g+3)
+// into a transposed, split LDS buffer: dst[col * ld + row0 + e]
+__device__ __forceinline__ void put_t4(bf16_t* hi, bf16_t* lo, int off, const float (&x)[4]) {
+  bf16x4 h, l;
+  split4(x, h, l);
+  *reinterpret_cast<bf16x4*>(hi + off) = h;
+  *reinterpret_cast<bf16x4*>(lo + off) = l;
+}
+
+template <int DK, bool BWD>
+__global__ __launch_bounds__(NTHR) void k_prep_bf(
+    const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const float* __restrict__ g,
+    const bf16_t* __restrict__ beta, const float* __restrict__ d, const ChunkInfo* __restrict__ cmap,
+    int H, bf16_t* __restrict__ Mp, bf16_t* __restrict__ Ap, bf16_t* __restrict__ MTp,
+    bf16_t* __restrict__ ATp, bf16_t* __restrict__ KTp, bf16_t* __restrict__ QTp,
+    float* __restrict__ Gw) {
+  constexpr int LDK = DK + 8;
+  constexpr int LDL = CH + 4;
+  constexpr int CC = CH * CH;
+  __shared__ __align__(16) bf16_t Ks[CH * LDK];
+  __shared__ __align__(16) bf16_t Qs[CH * LDK];
+  __shared__ __align__(16) float Ls[CH * LDL];
+  __shared__ float Gs[CH], Bs[CH];
+
+  const ChunkInfo ci = cmap[blockIdx.x];
+  if (ci.len <= 0) return;
+  const int h = blockIdx.y;
+  const long chh = (long)blockIdx.x * H + h;
+  const long tok = (long)ci.tok0 * H + h;
+  const int w = wave_id(), lane = lane_id(), g4 = lane >> 4;
+  {
+    TileRegs<bf16_t, CH, DK> kr, qr;
+    kr.load(k + tok * DK, (long)H * DK, ci.len);
+    qr.load(q + tok * DK, (long)H * DK, ci.len);
+    kr.store(Ks, LDK);
+    qr.store(Qs, LDK);
+  }
+  if (w == 0) {
+    const float gr = lane < ci.len ? g[tok + (long)lane * H] : 0.f;
+    const float G = wave_prefix_sum(gr);
+    Gs[lane] = G;
+    Bs[lane] = lane < ci.len ? bf2f(beta[tok + (long)lane * H]) : 0.f;
+    Gw[chh * CH + lane] = G;
+  }
+  __syncthreads();
+
+  floatx4 akk[1][4], aqk[1][4];
+  zero_acc(akk);
+  zero_acc(aqk);
+  mma<false, 1, 4, DK>(akk, Ks + 16 * w * LDK, LDK, Ks, LDK);
+  mma<false, 1, 4, DK>(aqk, Qs + 16 * w * LDK, LDK, Ks, LDK);
+  const float dh = d[h];
+  bf16_t* Ao = Ap + chh * 2 * CC;
+#pragma unroll
+  for (int nt = 0; nt < 4; ++nt) {
+    float av[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int r = 16 * w + acc_row(0, e), c = acc_col(nt);
+      const float kk = akk[0][nt][e];
+      float a = 0.f, l = 0.f;
+      if (r >= c) a = (aqk[0][nt][e] - dh * kk) * __expf(Gs[r] - Gs[c]);
+      if (r > c) l = Bs[r] * __expf(Gs[r - 1] - Gs[c]) * kk;
+      av[e] = a;
+      const __bf16 ah = (__bf16)a;
+      Ao[r * CH + c] = __builtin_bit_cast(bf16_t, ah);
+      Ao[CC + r * CH + c] = __builtin_bit_cast(bf16_t, (__bf16)(a - (float)ah));
+      Ls[r * LDL + c] = l;
+    }
+    if constexpr (BWD) {
+      // A^T: this lane's column c, rows 16w + 4g .. +3
+      bf16_t* At = ATp + chh * 2 * CC;
+      put_t4(At, At + CC, acc_col(nt) * CH + 16 * w + 4 * g4, av);
+    }
+  }
+  __syncthreads();
+
+  if (w == 0) {
+    // M = (I + L)^{-1}: lane j solves column j by forward substitution in fp32,
+    // x_i = -sum_{m < i} L_im x_m (x_j = 1, x_i = 0 for i < j); four partial
+    // sums per row shorten the dependency chain.
+    const int j = lane;
+    float x[CH];
+#pragma unroll
+    for (int i = 0; i < CH; ++i) x[i] = (i == j) ? 1.f : 0.f;
+#pragma unroll
+    for (int i = 1; i < CH; ++i) {
+      float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+#pragma unroll
+      for (int m = 0; m < i; m += 4) {
+        const float4 lv = *reinterpret_cast<const float4*>(Ls + i * LDL + m);
+        s0 += lv.x * x[m];
+        if (m + 1 < i) s1 += lv.y * x[m + 1];
+        if (m + 2 < i) s2 += lv.z * x[m + 2];
+        if (m + 3 < i) s3 += lv.w * x[m + 3];
+      }
+      const float sum = (s0 + s1) + (s2 + s3);
+      if (i > j) x[i] = -sum;
+    }
+    bf16_t* Mo = Mp + chh * 2 * CC;
+#pragma unroll
+    for (int i = 0; i < CH; ++i) {
+      const __bf16 hh = (__bf16)x[i];
+      Mo[i * CH + j] = __builtin_bit_cast(bf16_t, hh);
+      Mo[CC + i * CH + j] = __builtin_bit_cast(bf16_t, (__bf16)(x[i] - (float)hh));
+    }
+    if constexpr (BWD) {
+      bf16_t* Mt = MTp + chh * 2 * CC + j * CH;
+#pragma unroll
+      for (int i = 0; i < CH; i += 8) {
+        bf16x8 hv, lv;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const __bf16 hh = (__bf16)x[i + e];
+          hv[e] = hh;
+          lv[e] = (__bf16)(x[i + e] - (float)hh);
+        }
+        *reinterpret_cast<bf16x8*>(Mt + i) = hv;
+        *reinterpret_cast<bf16x8*>(Mt + CC + i) = lv;
+      }
+    }
+  } else {
+    // waves 1..3: K^T (and Q^T) per chunk-head, [dk][64] bf16
+    bf16_t* Kt = KTp + chh * DK * CH;
+    bf16_t* Qt = BWD ? QTp + chh * DK * CH : nullptr;
+    for (int idx = threadIdx.x - 64; idx < DK * (CH / 8); idx += NTHR - 64) {
+      const int i = idx / (CH / 8), t0 = (idx % (CH / 8)) * 8;
+      bf16x8 kv, qv;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        kv[e] = __builtin_bit_cast(__bf16, Ks[(t0 + e) * LDK + i]);
+        if constexpr (BWD) qv[e] = __builtin_bit_cast(__bf16, Qs[(t0 + e) * LDK + i]);
+      }
+      *reinterpret_cast<bf16x8*>(Kt + i * CH + t0) = kv;
+      if constexpr (BWD) *reinterpret_cast<bf16x8*>(Qt + i * CH + t0) = qv;
+    }
+  }
+}
+
+// Forward state scan (bf16 inputs).  One workgroup per (sequence, head,
+// 32-wide dv slice); wave w owns rows 16w..16w+15 of the chunk products and
+// rows (dk/4)w.. of the state slice.
+template <int DK, int DV, int BV, bool OUT, bool STORE>
+__global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
+    const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
+    const bf16_t* __restrict__ beta, const float* __restrict__ d, const float* __restrict__ h0,
+    const SeqInfo* __restrict__ smap, int H, const bf16_t* __restrict__ Mp,
+    const bf16_t* __restrict__ Ap, const bf16_t* __restrict__ KTp, const float* __restrict__ Gw,
+    float* __restrict__ o, float* __restrict__ ht, float* __restrict__ Xw, float* __restrict__ Dw,
+    float* __restrict__ Xfin, float* __restrict__ sink) {
+  // Every global load and store inside the chunk loop is issued unconditionally
+  // (clamped rows and chunk indices, masked values applied at use, padded-row
+  // stores sent to `sink`), so the memory-counter waits stay exact and the
+  // next chunk's loads overlap the current chunk's work.
+  constexpr int NTV = BV / 16, XMT = DK / 64, KS = DK / 32, CC = CH * CH;
+  constexpr int LDX = DK + 8, LDR = CH + 8;
+  __shared__ __align__(16) bf16_t XTh[BV * LDX];
+  __shared__ __align__(16) bf16_t XTl[BV * LDX];
+  __shared__ __align__(16) bf16_t RTh[BV * LDR];
+  __shared__ __align__(16) bf16_t RTl[BV * LDR];
+  __shared__ __align__(16) bf16_t DgTh[BV * LDR];
+  __shared__ __align__(16) bf16_t DgTl[BV * LDR];
+  __shared__ __align__(16) bf16_t DTh[OUT ? BV * LDR : 8];
+  __shared__ __align__(16) bf16_t DTl[OUT ? BV * LDR : 8];
+
+  const int s = blockIdx.x, h = blockIdx.y, j0 = blockIdx.z * BV;
+  const SeqInfo si = smap[s];
+  const int w = wave_id(), lane = lane_id(), r16 = lane & 15, g4 = lane >> 4;
+  const long soff = ((long)s * H + h) * DK * DV;
+  const float dh = d[h];
+  const int n = si.nchunks;
+  const int xrow0 = (DK / 4) * w + 4 * g4;  // state rows of this lane: xrow0 + 16 mt + e
+
+  floatx4 X[XMT][NTV];
+#pragma unroll
+  for (int mt = 0; mt < XMT; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < NTV; ++nt)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        X[mt][nt][e] = h0 ? h0[soff + (long)(xrow0 + 16 * mt + e) * DV + j0 + 16 * nt + r16] : 0.f;
+  auto put_state = [&]() {
+#pragma unroll
+    for (int mt = 0; mt < XMT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < NTV; ++nt) {
+        const float xv[4] = {X[mt][nt][0], X[mt][nt][1], X[mt][nt][2], X[mt][nt][3]};
+        put_t4(XTh, XTl, (16 * nt + r16) * LDX + xrow0 + 16 * mt, xv);
+      }
+  };
+  auto store_state = [&](float* dst) {
+#pragma unroll
+    for (int mt = 0; mt < XMT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < NTV; ++nt)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          dst[(long)(xrow0 + 16 * mt + e) * DV + j0 + 16 * nt + r16] = X[mt][nt][e];
+  };
+  put_state();
+
+  auto c_len = [&](int cc) { return min(CH, si.len - cc * CH); };
+  auto c_tok = [&](int cc) { return (long)(si.tok0 + cc * CH) * H + h; };
+  auto c_chh = [&](int cc) { return (long)(si.chunk0 + cc) * H + h; };
+
+  // per-chunk operands, loaded one chunk ahead
+  bf16x8 kf[KS], qf[KS], ktf[XMT][2], mh[2], ml[2], ah[2], al[2];
+  // per-row values of the chunk (cumulative gates G, beta, the V slice) are
+  // loaded one chunk ahead into registers and staged through a double-buffered
+  // LDS area at the end of each chunk
+  __shared__ float Grow[2][CH], Brow[2][CH];
+  __shared__ __align__(16) bf16_t Vrow[2][CH * (BV + 8)];
+  constexpr int VPR = BV / 8;                  // 16-byte pieces per V row
+  const int vr = threadIdx.x / VPR, vc = (threadIdx.x % VPR) * 8;
+  const int vr_ld = min(vr, CH - 1);
+  float pgv = 0.f;
+  bf16_t pbv = 0;
+  uint4 pvv = make_uint4(0, 0, 0, 0);
+  int plen = 0;
+  auto load_rows = [&](int cc) {
+    plen = c_len(cc);
+    const long tok = c_tok(cc), chh = c_chh(cc);
+    const int t = threadIdx.x & (CH - 1);
+    pgv = Gw[chh * CH + t];
+    pbv = beta[tok + (long)min(t, plen - 1) * H];
+    pvv = *reinterpret_cast<const uint4*>(v + (tok + (long)min(vr_ld, plen - 1) * H) * DV + j0 + vc);
+  };
+  auto put_rows = [&](int buf) {
+    const int t = threadIdx.x & (CH - 1);
+    Grow[buf][t] = pgv;
+    Brow[buf][t] = t < plen ? bf2f(pbv) : 0.f;
+    if (CH * VPR >= NTHR || threadIdx.x < CH * VPR)
+      *reinterpret_cast<uint4*>(&Vrow[buf][vr * (BV + 8) + vc]) =
+          vr < plen ? pvv : make_uint4(0, 0, 0, 0);
+  };
+  const int prow = 16 * w + r16;  // operand row of this lane
+  // rows past the chunk end load a valid row; their K X / Q X results are
+  // never used (beta = 0 zeroes R there and such outputs are not stored)
+  auto load_kq = [&](int cc) {
+    const long rb = (c_tok(cc) + (long)min(prow, c_len(cc) - 1) * H) * DK + 8 * g4;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      kf[ks] = ld8(k + rb + 32 * ks);
+      if constexpr (OUT) qf[ks] = ld8(q + rb + 32 * ks);
+    }
+  };
+  auto load_kt = [&](int cc) {
+    const bf16_t* p = KTp + c_chh(cc) * DK * CH + ((DK / 4) * w + r16) * CH + 8 * g4;
+#pragma unroll
+    for (int mt = 0; mt < XMT; ++mt)
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) ktf[mt][ks] = ld8(p + 16 * mt * CH + 32 * ks);
+  };
+  auto load_m = [&](int cc) {
+    const bf16_t* p = Mp + c_chh(cc) * 2 * CC + prow * CH + 8 * g4;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      mh[ks] = ld8(p + 32 * ks);
+      ml[ks] = ld8(p + CC + 32 * ks);
+    }
+  };
+  auto load_a = [&](int cc) {
+    const bf16_t* p = Ap + c_chh(cc) * 2 * CC + prow * CH + 8 * g4;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      ah[ks] = ld8(p + 32 * ks);
+      al[ks] = ld8(p + CC + 32 * ks);
+    }
+  };
+  if (n > 0) {
+    load_kq(0);
+    load_kt(0);
+    load_m(0);
+    if constexpr (OUT) load_a(0);
+    load_rows(0);
+    put_rows(0);
+    if constexpr (STORE) store_state(Xw + c_chh(0) * DK * DV);
+  }
+  __syncthreads();
+
+  for (int cc = 0; cc < n; ++cc) {
+    const bool more = cc + 1 < n;
+    const int nx = more ? cc + 1 : cc;  // chunk prefetched during this one
+    const int len = c_len(cc);
+    const long tok = c_tok(cc), chh = c_chh(cc);
+    const int buf = cc & 1;
+    load_rows(nx);
+    const float glast = Grow[buf][CH - 1];
+    float gg[4], gm[4], bb[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int r = 16 * w + 4 * g4 + e;
+      gg[e] = Grow[buf][r];
+      gm[e] = r > 0 ? Grow[buf][r - 1] : 0.f;
+      bb[e] = Brow[buf][r];
+    }
+
+    // K X and Q X (rows 16w..), R = Diag(beta)(V - Diag(exp Gm) K X)
+    floatx4 kx[NTV], qx[NTV];
+#pragma unroll
+    for (int nt = 0; nt < NTV; ++nt) {
+      kx[nt] = zero4();
+      qx[nt] = zero4();
+    }
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int nt = 0; nt < NTV; ++nt) {
+        const int off = (16 * nt + r16) * LDX + 32 * ks + 8 * g4;
+        const bf16x8 xh = ld8(XTh + off), xl = ld8(XTl + off);
+        kx[nt] = mfma16(kf[ks], xh, kx[nt]);
+        kx[nt] = mfma16(kf[ks], xl, kx[nt]);
+        if constexpr (OUT) {
+          qx[nt] = mfma16(qf[ks], xh, qx[nt]);
+          qx[nt] = mfma16(qf[ks], xl, qx[nt]);
+        }
+      }
+    load_kq(nx);
+    floatx4 oacc[NTV];
+#pragma unroll
+    for (int nt = 0; nt < NTV; ++nt) {
+      float rv[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = 16 * w + 4 * g4 + e;
+        const float vval = bf2f(Vrow[buf][r * (BV + 8) + 16 * nt + r16]);
+        rv[e] = bb[e] * (vval - __expf(gm[e]) * kx[nt][e]);
+        if constexpr (OUT) oacc[nt][e] = __expf(gg[e]) * (qx[nt][e] - dh * kx[nt][e]);
+      }
+      put_t4(RTh, RTl, (16 * nt + r16) * LDR + 16 * w + 4 * g4, rv);
+    }
+    __syncthreads();
+
+    // D = M R
+    floatx4 dl[NTV];
+#pragma unroll
+    for (int nt = 0; nt < NTV; ++nt) dl[nt] = zero4();
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int nt = 0; nt < NTV; ++nt) {
+        const int off = (16 * nt + r16) * LDR + 32 * ks + 8 * g4;
+        const bf16x8 rh = ld8(RTh + off), rl = ld8(RTl + off);
+        dl[nt] = mfma16(mh[ks], rh, dl[nt]);
+        dl[nt] = mfma16(mh[ks], rl, dl[nt]);
+        dl[nt] = mfma16(ml[ks], rh, dl[nt]);
+      }
+    load_m(nx);
+#pragma unroll
+    for (int nt = 0; nt < NTV; ++nt) {
+      float dv[4], dgv[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        dv[e] = dl[nt][e];
+        dgv[e] = __expf(glast - gg[e]) * dv[e];
+        if constexpr (STORE)
+          Dw[chh * CH * DV + (long)(16 * w + 4 * g4 + e) * DV + j0 + 16 * nt + r16] = dv[e];
+      }
+      const int off = (16 * nt + r16) * LDR + 16 * w + 4 * g4;
+      put_t4(DgTh, DgTl, off, dgv);
+      if constexpr (OUT) put_t4(DTh, DTl, off, dv);
+    }
+    __syncthreads();
+
+    // X' = exp(G_63) X + K^T Diag(exp(G_63 - G)) D
+    const float gC = __expf(glast);
+#pragma unroll
+    for (int mt = 0; mt < XMT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < NTV; ++nt) X[mt][nt] *= gC;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int nt = 0; nt < NTV; ++nt) {
+        const int off = (16 * nt + r16) * LDR + 32 * ks + 8 * g4;
+        const bf16x8 dh_ = ld8(DgTh + off), dl_ = ld8(DgTl + off);
+#pragma unroll
+        for (int mt = 0; mt < XMT; ++mt) {
+          X[mt][nt] = mfma16(ktf[mt][ks], dh_, X[mt][nt]);
+          X[mt][nt] = mfma16(ktf[mt][ks], dl_, X[mt][nt]);
+        }
+      }
+    load_kt(nx);
+
+    // O = Diag(exp G)(Q - d K) X + A D
+    if constexpr (OUT) {
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+        for (int nt = 0; nt < NTV; ++nt) {
+          const int off = (16 * nt + r16) * LDR + 32 * ks + 8 * g4;
+          const bf16x8 dh_ = ld8(DTh + off), dl_ = ld8(DTl + off);
+          oacc[nt] = mfma16(ah[ks], dh_, oacc[nt]);
+          oacc[nt] = mfma16(ah[ks], dl_, oacc[nt]);
+          oacc[nt] = mfma16(al[ks], dh_, oacc[nt]);
+        }
+      load_a(nx);
+#pragma unroll
+      for (int nt = 0; nt < NTV; ++nt)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = 16 * w + 4 * g4 + e;
+          float* dst = r < len ? o + (tok + (long)r * H) * DV + j0 + 16 * nt + r16
+                               : sink + (threadIdx.x & 255);
+          *dst = oacc[nt][e];
+        }
+    }
+    put_state();
+    // state entering the next chunk (after the last chunk: the final state)
+    if constexpr (STORE)
+      store_state(more ? Xw + c_chh(cc + 1) * DK * DV : Xfin + soff);
+    put_rows(buf ^ 1);
+    __syncthreads();
+  }
+  if (ht) store_state(ht + soff);
+}
+
+// Reverse state scan (bf16 inputs): Y = gradient of the state leaving the chunk.
+template <int DK, int DV, int BV>
+__global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
+    const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ dO,
+    const bf16_t* __restrict__ beta, const float* __restrict__ d, const float* __restrict__ dht,
+    const SeqInfo* __restrict__ smap, int H, const bf16_t* __restrict__ MTp,
+    const bf16_t* __restrict__ ATp, const bf16_t* __restrict__ KTp, const bf16_t* __restrict__ QTp,
+    const float* __restrict__ Gw, float* __restrict__ dh0, float* __restrict__ Yw,
+    float* __restrict__ dRw) {
+  // as in the forward scan, all loop memory operations are unconditional
+  constexpr int NTV = BV / 16, XMT = DK / 64, KS = DK / 32, CC = CH * CH;
+  constexpr int LDX = DK + 8, LDR = CH + 8;
+  __shared__ __align__(16) bf16_t YTh[BV * LDX];
+  __shared__ __align__(16) bf16_t YTl[BV * LDX];
+  __shared__ __align__(16) bf16_t dOT[2][BV * LDR];
+  __shared__ __align__(16) bf16_t dDTh[BV * LDR];
+  __shared__ __align__(16) bf16_t dDTl[BV * LDR];
+  __shared__ __align__(16) bf16_t PgTh[BV * LDR];
+  __shared__ __align__(16) bf16_t PgTl[BV * LDR];
+  __shared__ __align__(16) bf16_t W2Th[BV * LDR];
+  __shared__ __align__(16) bf16_t W2Tl[BV * LDR];
+
+  const int s = blockIdx.x, h = blockIdx.y, j0 = blockIdx.z * BV;
+  const SeqInfo si = smap[s];
+  const int w = wave_id(), lane = lane_id(), r16 = lane & 15, g4 = lane >> 4;
+  const long soff = ((long)s * H + h) * DK * DV;
+  const float dh = d[h];
+  const int n = si.nchunks;
+  const int yrow0 = (DK / 4) * w + 4 * g4;
+
+  floatx4 Y[XMT][NTV];
+#pragma unroll
+  for (int mt = 0; mt < XMT; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < NTV; ++nt)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        Y[mt][nt][e] = dht ? dht[soff + (long)(yrow0 + 16 * mt + e) * DV + j0 + 16 * nt + r16] : 0.f;
+  auto put_state = [&]() {
+#pragma unroll
+    for (int mt = 0; mt < XMT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < NTV; ++nt) {
+        const float yv[4] = {Y[mt][nt][0], Y[mt][nt][1], Y[mt][nt][2], Y[mt][nt][3]};
+        put_t4(YTh, YTl, (16 * nt + r16) * LDX + yrow0 + 16 * mt, yv);
+      }
+  };
+  auto store_state = [&](float* dst) {
+#pragma unroll
+    for (int mt = 0; mt < XMT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < NTV; ++nt)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          dst[(long)(yrow0 + 16 * mt + e) * DV + j0 + 16 * nt + r16] = Y[mt][nt][e];
+  };
+  put_state();
+
+  auto c_len = [&](int cc) { return min(CH, si.len - cc * CH); };
+  auto c_tok = [&](int cc) { return (long)(si.tok0 + cc * CH) * H + h; };
+  auto c_chh = [&](int cc) { return (long)(si.chunk0 + cc) * H + h; };
+
+  bf16x8 kf[KS], ath[2], atl[2], mth[2], mtl[2], qtf[XMT][2], ktf[XMT][2];
+  // per-row values (G, beta) and the dO slice are loaded one chunk ahead into
+  // registers and staged through double-buffered LDS at the end of each chunk
+  __shared__ float Grow[2][CH], Brow[2][CH];
+  float pgv = 0.f;
+  bf16_t pbv = 0;
+  int plen = 0;
+  uint4 pdo = make_uint4(0, 0, 0, 0);  // next chunk's dO slice, 16 bytes per thread
+  const int prow = 16 * w + r16;
+  // rows past the chunk end load a valid row; dD is zeroed there at use
+  auto load_k = [&](int cc) {
+    const long rb = (c_tok(cc) + (long)min(prow, c_len(cc) - 1) * H) * DK + 8 * g4;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) kf[ks] = ld8(k + rb + 32 * ks);
+  };
+  auto load_at = [&](int cc) {
+    const bf16_t* p = ATp + c_chh(cc) * 2 * CC + prow * CH + 8 * g4;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      ath[ks] = ld8(p + 32 * ks);
+      atl[ks] = ld8(p + CC + 32 * ks);
+    }
+  };
+  auto load_mt = [&](int cc) {
+    const bf16_t* p = MTp + c_chh(cc) * 2 * CC + prow * CH + 8 * g4;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      mth[ks] = ld8(p + 32 * ks);
+      mtl[ks] = ld8(p + CC + 32 * ks);
+    }
+  };
+  auto load_qkt = [&](int cc) {
+    const long base = c_chh(cc) * DK * CH + ((DK / 4) * w + r16) * CH + 8 * g4;
+#pragma unroll
+    for (int mt = 0; mt < XMT; ++mt)
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        qtf[mt][ks] = ld8(QTp + base + 16 * mt * CH + 32 * ks);
+        ktf[mt][ks] = ld8(KTp + base + 16 * mt * CH + 32 * ks);
+      }
+  };
+  auto load_rows = [&](int cc) {
+    plen = c_len(cc);
+    const long tok = c_tok(cc), chh = c_chh(cc);
+    const int t = threadIdx.x & (CH - 1);
+    pgv = Gw[chh * CH + t];
+    pbv = beta[tok + (long)min(t, plen - 1) * H];
+  };
+  auto put_rows = [&](int buf) {
+    const int t = threadIdx.x & (CH - 1);
+    Grow[buf][t] = pgv;
+    Brow[buf][t] = t < plen ? bf2f(pbv) : 0.f;
+  };
+  // dO slice of a chunk: 64 tokens x BV columns in 16-byte pieces; thread t
+  // (t < 8 BV) holds token t / (BV/8), columns 8 (t % (BV/8)) .. +7
+  constexpr int DPR = BV / 8;
+  const int dr = threadIdx.x / DPR, dc = (threadIdx.x % DPR) * 8;
+  const bool do_thr = CH * DPR >= NTHR || threadIdx.x < CH * DPR;
+  const int dr_ld = min(dr, CH - 1);
+  int do_ok = 0;
+  auto load_do = [&](int cc) {
+    const int len = c_len(cc);
+    do_ok = do_thr && dr < len;
+    pdo = *reinterpret_cast<const uint4*>(dO + (c_tok(cc) + (long)min(dr_ld, len - 1) * H) * DV + j0 + dc);
+  };
+  auto put_do = [&](int buf) {
+    union { uint4 u; bf16_t e[8]; } val;
+    val.u = do_ok ? pdo : make_uint4(0, 0, 0, 0);
+    if (do_thr) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) dOT[buf][(dc + e) * LDR + dr] = val.e[e];
+    }
+  };
+
+  if (n > 0) {
+    load_do(n - 1);
+    load_k(n - 1);
+    load_at(n - 1);
+    load_mt(n - 1);
+    load_qkt(n - 1);
+    load_rows(n - 1);
+    put_rows((n - 1) & 1);
+    put_do((n - 1) & 1);
+  }
+  __syncthreads();
+
+  for (int cc = n - 1; cc >= 0; --cc) {
+    const bool more = cc > 0;
+    const int nx = more ? cc - 1 : cc;  // chunk prefetched during this one
+    const long chh = c_chh(cc);
+    const int buf = cc & 1;
+    const int clen = c_len(cc);
+    store_state(Yw + chh * DK * DV);
+    load_rows(nx);
+    load_do(nx);
+    const float glast = Grow[buf][CH - 1];
+    float gg[4], gm[4], bb[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int r = 16 * w + 4 * g4 + e;
+      gg[e] = Grow[buf][r];
+      gm[e] = r > 0 ? Grow[buf][r - 1] : 0.f;
+      bb[e] = Brow[buf][r];
+    }
+
+    // dD = A^T dO + Diag(exp(G_63 - G)) K Y
+    floatx4 ky[NTV], ad[NTV];
+#pragma unroll
+    for (int nt = 0; nt < NTV; ++nt) {
+      ky[nt] = zero4();
+      ad[nt] = zero4();
+    }
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int nt = 0; nt < NTV; ++nt) {
+        const int off = (16 * nt + r16) * LDX + 32 * ks + 8 * g4;
+        const bf16x8 yh = ld8(YTh + off), yl = ld8(YTl + off);
+        ky[nt] = mfma16(kf[ks], yh, ky[nt]);
+        ky[nt] = mfma16(kf[ks], yl, ky[nt]);
+      }
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int nt = 0; nt < NTV; ++nt) {
+        const bf16x8 dov = ld8(dOT[buf] + (16 * nt + r16) * LDR + 32 * ks + 8 * g4);
+        ad[nt] = mfma16(ath[ks], dov, ad[nt]);
+        ad[nt] = mfma16(atl[ks], dov, ad[nt]);
+      }
+    load_k(nx);
+    load_at(nx);
+#pragma unroll
+    for (int nt = 0; nt < NTV; ++nt) {
+      float dd_[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        dd_[e] = 16 * w + 4 * g4 + e < clen ? ad[nt][e] + __expf(glast - gg[e]) * ky[nt][e] : 0.f;
+      put_t4(dDTh, dDTl, (16 * nt + r16) * LDR + 16 * w + 4 * g4, dd_);
+    }
+    __syncthreads();
+
+    // dR = M^T dD;  Pg = Diag(exp G) dO;  W2 = -d Pg - Diag(beta exp Gm) dR
+    floatx4 drr[NTV];
+#pragma unroll
+    for (int nt = 0; nt < NTV; ++nt) drr[nt] = zero4();
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int nt = 0; nt < NTV; ++nt) {
+        const int off = (16 * nt + r16) * LDR + 32 * ks + 8 * g4;
+        const bf16x8 xh = ld8(dDTh + off), xl = ld8(dDTl + off);
+        drr[nt] = mfma16(mth[ks], xh, drr[nt]);
+        drr[nt] = mfma16(mth[ks], xl, drr[nt]);
+        drr[nt] = mfma16(mtl[ks], xh, drr[nt]);
+      }
+    load_mt(nx);
+#pragma unroll
+    for (int nt = 0; nt < NTV; ++nt) {
+      const int off = (16 * nt + r16) * LDR + 16 * w + 4 * g4;
+      const bf16x4 dov = *reinterpret_cast<const bf16x4*>(dOT[buf] + off);
+      float pg[4], w2[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float drv = drr[nt][e];
+        dRw[chh * CH * DV + (long)(16 * w + 4 * g4 + e) * DV + j0 + 16 * nt + r16] = drv;
+        pg[e] = __expf(gg[e]) * (float)dov[e];
+        w2[e] = -dh * pg[e] - bb[e] * __expf(gm[e]) * drv;
+      }
+      put_t4(PgTh, PgTl, off, pg);
+      put_t4(W2Th, W2Tl, off, w2);
+    }
+    __syncthreads();
+
+    // Y <- exp(G_63) Y + Q^T Pg + K^T W2
+    const float gC = __expf(glast);
+#pragma unroll
+    for (int mt = 0; mt < XMT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < NTV; ++nt) Y[mt][nt] *= gC;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int nt = 0; nt < NTV; ++nt) {
+        const int off = (16 * nt + r16) * LDR + 32 * ks + 8 * g4;
+        const bf16x8 ph = ld8(PgTh + off), pl = ld8(PgTl + off);
+        const bf16x8 wh = ld8(W2Th + off), wl = ld8(W2Tl + off);
+#pragma unroll
+        for (int mt = 0; mt < XMT; ++mt) {
+          Y[mt][nt] = mfma16(qtf[mt][ks], ph, Y[mt][nt]);
+          Y[mt][nt] = mfma16(qtf[mt][ks], pl, Y[mt][nt]);
+          Y[mt][nt] = mfma16(ktf[mt][ks], wh, Y[mt][nt]);
+          Y[mt][nt] = mfma16(ktf[mt][ks], wl, Y[mt][nt]);
+        }
+      }
+    load_qkt(nx);
+    put_do(buf ^ 1);
+    put_rows(buf ^ 1);
+    put_state();
+    __syncthreads();
+  }
+  if (dh0) store_state(dh0 + soff);
+}
+
 // ---------------------------------------------------------------------------
 // host launchers
 // ---------------------------------------------------------------------------
@@ -846,23 +1628,85 @@ static hipError_t run_bwd(const LaunchArgs& a) {
   return hipGetLastError();
 }
 
+template <int DK, int DV>
+static hipError_t run_fwd_bf(const LaunchArgs& a) {
+  hipStream_t st = a.stream;
+  const bf16_t* q = static_cast<const bf16_t*>(a.q);
+  const bf16_t* k = static_cast<const bf16_t*>(a.k);
+  const bf16_t* v = static_cast<const bf16_t*>(a.v);
+  const bf16_t* beta = static_cast<const bf16_t*>(a.beta);
+  a.stage("chunk_map");
+  k_chunk_map<<<1, NTHR, 0, st>>>(a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.ncmax, a.cmap, a.smap);
+  a.stage("prep");
+  if (a.ncmax > 0)
+    k_prep_bf<DK, false><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
+        q, k, a.g, beta, a.d, a.cmap, a.H, a.Mp, a.Ap, nullptr, nullptr, a.KTp, nullptr, a.Gw);
+  a.stage("scan_fwd");
+  k_scan_fwd_bf<DK, DV, SCAN_BV, true, false><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
+      q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mp, a.Ap, a.KTp, a.Gw, a.o, a.ht, nullptr, nullptr,
+      nullptr, a.sink);
+  a.stage(nullptr);
+  return hipGetLastError();
+}
+
+template <int DK, int DV>
+static hipError_t run_bwd_bf(const LaunchArgs& a) {
+  hipStream_t st = a.stream;
+  const bf16_t* q = static_cast<const bf16_t*>(a.q);
+  const bf16_t* k = static_cast<const bf16_t*>(a.k);
+  const bf16_t* v = static_cast<const bf16_t*>(a.v);
+  const bf16_t* beta = static_cast<const bf16_t*>(a.beta);
+  const bf16_t* dO = static_cast<const bf16_t*>(a.dO);
+  if (a.N == 0) {
+    k_reduce_dd<<<a.H, NTHR, 0, st>>>(a.ddp, 0, a.H, a.dd);
+    return hipGetLastError();
+  }
+  a.stage("chunk_map");
+  k_chunk_map<<<1, NTHR, 0, st>>>(a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.ncmax, a.cmap, a.smap);
+  a.stage("prep");
+  if (a.ncmax > 0)
+    k_prep_bf<DK, true><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
+        q, k, a.g, beta, a.d, a.cmap, a.H, a.Mp, a.Ap, a.MTp, a.ATp, a.KTp, a.QTp, a.Gw);
+  a.stage("scan_fwd_store");
+  k_scan_fwd_bf<DK, DV, SCAN_BV, false, true><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
+      q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mp, a.Ap, a.KTp, a.Gw, nullptr, nullptr, a.Xw,
+      a.Dw, a.Xfin, a.sink);
+  a.stage("scan_bwd");
+  k_scan_bwd_bf<DK, DV, SCAN_BV><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
+      q, k, dO, beta, a.d, a.dht, a.smap, a.H, a.MTp, a.ATp, a.KTp, a.QTp, a.Gw, a.dh0, a.Yw,
+      a.dRw);
+  a.stage("intra_bwd");
+  if (a.ncmax > 0)
+    k_intra_bwd<bf16_t, DK, DV><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
+        q, k, v, dO, beta, a.d, a.cmap, a.H, a.Gw, a.Xw, a.Dw, a.Yw, a.dRw, a.dq, a.dk_, a.dv_,
+        a.dbeta, a.dg, a.ddp);
+  a.stage("reduce_dd");
+  k_reduce_dd<<<a.H, NTHR, 0, st>>>(a.ddp, a.ncmax, a.H, a.dd);
+  a.stage(nullptr);
+  return hipGetLastError();
+}
+
+template <bool BWD>
+static hipError_t dispatch_bf(const LaunchArgs& a) {
+  if (a.dk == 64 && a.dv == 64) return BWD ? run_bwd_bf<64, 64>(a) : run_fwd_bf<64, 64>(a);
+  if (a.dk == 128 && a.dv == 128) return BWD ? run_bwd_bf<128, 128>(a) : run_fwd_bf<128, 128>(a);
+  if (a.dk == 64 && a.dv == 128) return BWD ? run_bwd_bf<64, 128>(a) : run_fwd_bf<64, 128>(a);
+  if (a.dk == 128 && a.dv == 64) return BWD ? run_bwd_bf<128, 64>(a) : run_fwd_bf<128, 64>(a);
+  return hipErrorInvalidValue;
+}
+
 template <bool BWD, typename Tin>
 static hipError_t dispatch_dims(const LaunchArgs& a) {
   if (a.dk == 64 && a.dv == 64) return BWD ? run_bwd<Tin, 64, 64>(a) : run_fwd<Tin, 64, 64>(a);
-  if constexpr (!is_f32<Tin>::value) {
-    if (a.dk == 128 && a.dv == 128) return BWD ? run_bwd<Tin, 128, 128>(a) : run_fwd<Tin, 128, 128>(a);
-    if (a.dk == 64 && a.dv == 128) return BWD ? run_bwd<Tin, 64, 128>(a) : run_fwd<Tin, 64, 128>(a);
-    if (a.dk == 128 && a.dv == 64) return BWD ? run_bwd<Tin, 128, 64>(a) : run_fwd<Tin, 128, 64>(a);
-  }
   return hipErrorInvalidValue;
 }
 
 hipError_t launch_fwd(const LaunchArgs& a) {
-  return a.bf16 ? dispatch_dims<false, bf16_t>(a) : dispatch_dims<false, float>(a);
+  return a.bf16 ? dispatch_bf<false>(a) : dispatch_dims<false, float>(a);
 }
 
 hipError_t launch_bwd(const LaunchArgs& a) {
-  return a.bf16 ? dispatch_dims<true, bf16_t>(a) : dispatch_dims<true, float>(a);
+  return a.bf16 ? dispatch_bf<true>(a) : dispatch_dims<true, float>(a);
 }
 
 }  // namespace comba

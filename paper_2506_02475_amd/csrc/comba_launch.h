@@ -37,6 +37,11 @@ struct LaunchArgs {
   float *Mw, *Aw, *Gw;            // per chunk-head: M, A (64 x 64), G (64)
   float *Xw, *Dw, *Yw, *dRw;      // per chunk-head: X (dk x dv), D (64 x dv), Y, dR
   float* ddp;                     // per chunk-head partial dd
+  // bf16 path, per chunk-head: M, A as (hi, lo) bf16 pairs [2][64][64] (in the
+  // M, A regions), M^T, A^T likewise, K^T and Q^T as [dk][64] bf16
+  uint16_t *Mp, *Ap, *MTp, *ATp, *KTp, *QTp;
+  float* Xfin;  // backward: final state of the recomputed forward [N,H,dk,dv]
+  float* sink;  // 1 KiB that absorbs stores of padded rows (never read)
   hipStream_t stream;
   StageHook hook;
   void stage(const char* name) const {
