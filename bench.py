@@ -1,10 +1,12 @@
 #!/usr/bin/env python3
 """Benchmark of the chunk-wise Comba forward + backward on one MI355X.
 
-One step = one pass of the whole hot path over one batch: comba_chunk_fwd
-(chunk tables, gates/score matrix/UT inverse, state scan fused with the
-output) followed by comba_chunk_bwd (which recomputes the forward states, runs
-the reverse state scan and the intra-chunk gradients).  Workload: the 1.3B-model
+One step = one pass of the whole hot path over one batch, as a training step
+runs it: comba_chunk_fwd_save (chunk tables, gates/score matrix/UT inverse,
+state scan fused with the output, keeping the chunk states for the backward)
+followed by comba_chunk_bwd_saved (reverse state scan and intra-chunk
+gradients).  The stateless pair comba_chunk_fwd + comba_chunk_bwd (whose
+backward recomputes the forward) is timed as well and reported beside it.  Workload: the 1.3B-model
 layer shape, B=4, H=16, T=4096, dk=dv=128, chunk 64, bf16 inputs, fp32 state and
 outputs, seeded synthetic inputs (comba_inputs, PCG64).
 
@@ -36,28 +38,41 @@ WORKLOAD_INDEX = 3             # l1p3b_fwdbwd
 def stage_model(name, B, T, H, dk, dv, C=64, in_bytes=2):
     """Algorithmic (flops, bytes) of one launch of a kernel stage.
 
-    Per chunk-head (C tokens of one head) the dense products the stage performs
+    Per chunk-head (C tokens of one head): the dense products the stage performs
     (2 m n k flops each) and the HBM bytes it must move at minimum (each operand
-    read once, each result written once; L2 re-reads excluded).
+    read once, each result written once; L2 re-reads excluded).  fp32
+    intermediates are counted at 4 bytes per element (the bf16 path stores them
+    as (hi, lo) bf16 pairs, the same size); K^T and Q^T copies made by the prep
+    stage are counted where they are written and read.
     """
     nch = B * math.ceil(T / C) * H
     f4 = 4
-    if name == "prep":            # K K^T, Q K^T; read q, k, g, beta; write M, A, G
+    qk = C * dk * in_bytes          # one of q, k (or its transpose)
+    vv = C * dv * in_bytes          # one of v, dO
+    gb = C * (f4 + in_bytes)        # g (or G) and beta
+    cc = C * C * f4                 # one C x C fp32 matrix
+    st = dk * dv * f4               # one state
+    cd = C * dv * f4                # one C x dv fp32 matrix
+    if name in ("prep", "prep_save"):    # K K^T, Q K^T; q, k, g, beta -> M, A, K^T, G
         fl = 4 * C * C * dk
-        by = C * 2 * dk * in_bytes + C * (f4 + in_bytes) + 2 * C * C * f4 + C * f4
-    elif name == "scan_fwd":      # K X, Q X, M R, A D, K^T D; read q,k,v,M,A,G,beta; write o
+        by = 2 * qk + gb + 2 * cc + qk + C * f4
+        if name == "prep_save":           # + M^T, A^T, Q^T for the backward
+            by += 2 * cc + qk
+    elif name in ("scan_fwd", "scan_fwd_save"):  # K X, Q X, M R, A D, K^T D
         fl = 6 * C * dk * dv + 4 * C * C * dv
-        by = C * (2 * dk + dv) * in_bytes + 2 * C * C * f4 + C * (f4 + in_bytes) + C * dv * f4
-    elif name == "scan_fwd_store":  # K X, M R, K^T D; read k,v,M,G,beta; write X, D
+        by = 3 * qk + vv + 2 * cc + gb + cd
+        if name == "scan_fwd_save":       # + chunk states X and D for the backward
+            by += st + cd
+    elif name == "scan_fwd_store":  # K X, M R, K^T D; -> X, D
         fl = 4 * C * dk * dv + 2 * C * C * dv
-        by = C * (dk + dv) * in_bytes + C * C * f4 + C * (f4 + in_bytes) + dk * dv * f4 + C * dv * f4
-    elif name == "scan_bwd":      # K Y, A^T dO, M^T dD, Q^T Pg, K^T W2; read q,k,dO,A,M,G,beta; write Y, dR
+        by = 2 * qk + vv + cc + gb + st + cd
+    elif name == "scan_bwd":      # K Y, A^T dO, M^T dD, Q^T Pg, K^T W2; -> Y, dR
         fl = 6 * C * dk * dv + 4 * C * C * dv
-        by = C * (2 * dk + dv) * in_bytes + 2 * C * C * f4 + C * (f4 + in_bytes) + dk * dv * f4 + C * dv * f4
+        by = 3 * qk + vv + 2 * cc + gb + st + cd
     elif name == "intra_bwd":     # 3 C x dk x dv, 2 C x C x dv, 5 C x C x dk products
         fl = 6 * C * dk * dv + 4 * C * C * dv + 10 * C * C * dk
-        by = (C * (2 * dk + 2 * dv) * in_bytes + 2 * dk * dv * f4 + 2 * C * dv * f4 + C * (f4 + in_bytes)
-              + C * (2 * dk + dv) * f4 + 2 * C * f4)
+        by = (4 * qk + 2 * vv + 2 * st + 2 * cd + gb          # q,k,K^T,Q^T,v,dO,X,Y,D,dR
+              + C * (2 * dk + dv) * f4 + 2 * C * f4)           # dq, dk, dv, dg, dbeta
     else:
         return 0.0, 0.0
     return float(fl * nch), float(by * nch)
@@ -152,9 +167,24 @@ def main():
     ws_b = torch.empty(comba.bwd_workspace_bytes(B, T, H, dk, dv), dtype=torch.uint8, device=dev)
 
     def step():
+        # training pair: the forward leaves the backward's state in ws_b
+        o, ht, _ = comba.comba_chunk_fwd_save(q, k, v, g, beta, d, h0, workspace=ws_b)
+        gr = comba.comba_chunk_bwd_saved(q, k, v, g, beta, d, h0, dO, None, workspace=ws_b)
+        return o, gr
+
+    def step_stateless():
         o, ht = comba.comba_chunk_fwd(q, k, v, g, beta, d, h0, workspace=ws_f)
         gr = comba.comba_chunk_bwd(q, k, v, g, beta, d, h0, dO, None, workspace=ws_b)
         return o, gr
+
+    for _ in range(args.warmup):
+        step_stateless()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step_stateless()
+    torch.cuda.synchronize()
+    ms_stateless = (time.perf_counter() - t0) * 1e3 / args.steps
 
     for _ in range(args.warmup):
         step()
@@ -219,6 +249,8 @@ def main():
                 "beta=sigmoid(N(0,1)), d~U(0,1))",
         "config": {"workload": spec.name, "B": B, "T": T, "H": H, "dk": dk, "dv": dv,
                    "chunk": 64, "in_dtype": "bf16", "out_dtype": "f32"},
+        "step": "comba_chunk_fwd_save + comba_chunk_bwd_saved",
+        "ms_per_step_stateless": round(ms_stateless, 4),
         "mfma_pct_peak_op": round(100.0 * mfma_frac_op, 3),
         "op_algorithmic_tflops": round(op_fl / (ms_per_step * 1e-3) / 1e12, 2),
         "stages_ms": {n: round(x, 4) for n, x in tot.items()},

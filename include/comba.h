@@ -110,6 +110,28 @@ comba_status comba_chunk_bwd(const comba_shape *shape, const void *q, const void
                              float *dh0, void *ws, size_t ws_bytes, void *stream);
 
 /*
+ * Training pair.  comba_chunk_fwd_save computes exactly what comba_chunk_fwd
+ * computes and, in addition, leaves in `ws` everything the backward would
+ * otherwise recompute (chunk tables, the per-chunk UT-transform operands and
+ * the chunk-boundary states); `ws` must hold comba_bwd_workspace_bytes(shape).
+ * comba_chunk_bwd_saved then returns the same gradients as comba_chunk_bwd
+ * while skipping that recomputation.  The caller must pass the same shape and
+ * inputs (q, k, v, g, beta, d, h0) and the same, unmodified `ws` to both calls,
+ * with the backward ordered after the forward (same stream, or synchronised);
+ * otherwise the results are undefined (never out of bounds).
+ */
+comba_status comba_chunk_fwd_save(const comba_shape *shape, const void *q, const void *k,
+                                  const void *v, const float *g, const void *beta, const float *d,
+                                  const float *h0, float *o, float *ht, void *ws,
+                                  size_t ws_bytes, void *stream);
+comba_status comba_chunk_bwd_saved(const comba_shape *shape, const void *q, const void *k,
+                                   const void *v, const float *g, const void *beta,
+                                   const float *d, const float *h0, const void *dO,
+                                   const float *dht, float *dq, float *dk, float *dv, float *dg,
+                                   float *dbeta, float *dd, float *dh0, void *ws,
+                                   size_t ws_bytes, void *stream);
+
+/*
  * Stage timing, for benchmarks (not part of the method).  comba_profile_enable(1)
  * starts a recording session on the calling host thread: every following
  * comba_chunk_fwd / comba_chunk_bwd call on this thread records a HIP event on

@@ -23,7 +23,8 @@ import os
 import re
 import threading
 
-__all__ = ["comba_chunk_fwd", "comba_chunk_bwd", "load_library", "library_path",
+__all__ = ["comba_chunk_fwd", "comba_chunk_bwd", "comba_chunk_fwd_save", "comba_chunk_bwd_saved",
+           "load_library", "library_path",
            "profile_enable", "profile_read",
            "fwd_workspace_bytes", "bwd_workspace_bytes", "exported_symbols", "CombaError",
            "CombaShape", "COMBA_F32", "COMBA_BF16", "CHUNK"]
@@ -73,6 +74,10 @@ def load_library():
             lib.comba_chunk_fwd.restype = I
             lib.comba_chunk_bwd.argtypes = [SP] + [P] * 16 + [P, Z, P]
             lib.comba_chunk_bwd.restype = I
+            lib.comba_chunk_fwd_save.argtypes = [SP] + [P] * 9 + [P, Z, P]
+            lib.comba_chunk_fwd_save.restype = I
+            lib.comba_chunk_bwd_saved.argtypes = [SP] + [P] * 16 + [P, Z, P]
+            lib.comba_chunk_bwd_saved.restype = I
             lib.comba_profile_enable.argtypes = [I]
             lib.comba_profile_enable.restype = I
             lib.comba_profile_read.argtypes = [P, P, I]
@@ -175,9 +180,7 @@ def _prepare(q, k, v, g, beta, d, h0, cu_seqlens, extra=()):
     return shp, (B, T, H, dk, dv, N)
 
 
-def comba_chunk_fwd(q, k, v, g, beta, d, h0=None, *, cu_seqlens=None, output_final_state=True,
-                    workspace=None, stream=None):
-    """Chunk-wise forward.  Returns (o [B,T,H,dv] fp32, ht [N,H,dk,dv] fp32 or None)."""
+def _fwd(save, q, k, v, g, beta, d, h0, cu_seqlens, output_final_state, workspace, stream):
     import torch
 
     lib = load_library()
@@ -185,22 +188,39 @@ def comba_chunk_fwd(q, k, v, g, beta, d, h0=None, *, cu_seqlens=None, output_fin
     o = torch.empty((B, T, H, dv), dtype=torch.float32, device=q.device)
     ht = torch.empty((N, H, dk, dv), dtype=torch.float32, device=q.device) \
         if output_final_state else None
-    nbytes = lib.comba_fwd_workspace_bytes(ctypes.byref(shp))
+    size_fn = lib.comba_bwd_workspace_bytes if save else lib.comba_fwd_workspace_bytes
+    nbytes = size_fn(ctypes.byref(shp))
     if nbytes == 0:
         _check(2)
     if workspace is None or workspace.numel() < nbytes:
         workspace = torch.empty(nbytes, dtype=torch.uint8, device=q.device)
     st = torch.cuda.current_stream(q.device).cuda_stream if stream is None else stream
-    _check(lib.comba_chunk_fwd(ctypes.byref(shp), _ptr(q), _ptr(k), _ptr(v), _ptr(g),
-                               _ptr(beta), _ptr(d), _ptr(h0), _ptr(o), _ptr(ht),
-                               _ptr(workspace), ctypes.c_size_t(workspace.numel()),
-                               ctypes.c_void_p(st)))
+    fn = lib.comba_chunk_fwd_save if save else lib.comba_chunk_fwd
+    _check(fn(ctypes.byref(shp), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(d),
+              _ptr(h0), _ptr(o), _ptr(ht), _ptr(workspace), ctypes.c_size_t(workspace.numel()),
+              ctypes.c_void_p(st)))
+    return o, ht, workspace
+
+
+def comba_chunk_fwd(q, k, v, g, beta, d, h0=None, *, cu_seqlens=None, output_final_state=True,
+                    workspace=None, stream=None):
+    """Chunk-wise forward.  Returns (o [B,T,H,dv] fp32, ht [N,H,dk,dv] fp32 or None)."""
+    o, ht, _ = _fwd(False, q, k, v, g, beta, d, h0, cu_seqlens, output_final_state, workspace,
+                    stream)
     return o, ht
 
 
-def comba_chunk_bwd(q, k, v, g, beta, d, h0, dO, dht=None, *, cu_seqlens=None,
-                    need_dh0=True, workspace=None, stream=None):
-    """Chunk-wise backward.  Returns dict dq, dk, dv, dg, dbeta, dd, dh0 (fp32)."""
+def comba_chunk_fwd_save(q, k, v, g, beta, d, h0=None, *, cu_seqlens=None,
+                         output_final_state=True, workspace=None, stream=None):
+    """Forward that also keeps the backward's state in a backward-sized workspace.
+
+    Returns (o, ht, workspace); pass the same inputs and `workspace` to
+    comba_chunk_bwd_saved."""
+    return _fwd(True, q, k, v, g, beta, d, h0, cu_seqlens, output_final_state, workspace,
+                stream)
+
+
+def _bwd(saved, q, k, v, g, beta, d, h0, dO, dht, cu_seqlens, need_dh0, workspace, stream):
     import torch
 
     lib = load_library()
@@ -226,12 +246,27 @@ def comba_chunk_bwd(q, k, v, g, beta, d, h0, dO, dht=None, *, cu_seqlens=None,
     if nbytes == 0:
         _check(2)
     if workspace is None or workspace.numel() < nbytes:
+        if saved:
+            raise CombaError("comba: comba_chunk_bwd_saved needs the workspace filled by "
+                             "comba_chunk_fwd_save")
         workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
     st = torch.cuda.current_stream(dev).cuda_stream if stream is None else stream
-    _check(lib.comba_chunk_bwd(ctypes.byref(shp), _ptr(q), _ptr(k), _ptr(v), _ptr(g),
-                               _ptr(beta), _ptr(d), _ptr(h0), _ptr(dO), _ptr(dht),
-                               _ptr(out["dq"]), _ptr(out["dk"]), _ptr(out["dv"]),
-                               _ptr(out["dg"]), _ptr(out["dbeta"]), _ptr(out["dd"]),
-                               _ptr(out["dh0"]), _ptr(workspace),
-                               ctypes.c_size_t(workspace.numel()), ctypes.c_void_p(st)))
+    fn = lib.comba_chunk_bwd_saved if saved else lib.comba_chunk_bwd
+    _check(fn(ctypes.byref(shp), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(d),
+              _ptr(h0), _ptr(dO), _ptr(dht), _ptr(out["dq"]), _ptr(out["dk"]), _ptr(out["dv"]),
+              _ptr(out["dg"]), _ptr(out["dbeta"]), _ptr(out["dd"]), _ptr(out["dh0"]),
+              _ptr(workspace), ctypes.c_size_t(workspace.numel()), ctypes.c_void_p(st)))
     return out
+
+
+def comba_chunk_bwd(q, k, v, g, beta, d, h0, dO, dht=None, *, cu_seqlens=None,
+                    need_dh0=True, workspace=None, stream=None):
+    """Chunk-wise backward (recomputes the forward).  Returns dict dq, dk, dv, dg, dbeta, dd,
+    dh0 (fp32)."""
+    return _bwd(False, q, k, v, g, beta, d, h0, dO, dht, cu_seqlens, need_dh0, workspace, stream)
+
+
+def comba_chunk_bwd_saved(q, k, v, g, beta, d, h0, dO, dht=None, *, workspace, cu_seqlens=None,
+                          need_dh0=True, stream=None):
+    """Backward reusing the state left by comba_chunk_fwd_save in `workspace`."""
+    return _bwd(True, q, k, v, g, beta, d, h0, dO, dht, cu_seqlens, need_dh0, workspace, stream)

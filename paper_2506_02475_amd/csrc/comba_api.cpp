@@ -172,25 +172,10 @@ void fill_common(comba::LaunchArgs& a, const Dims& d, const comba_shape* s) {
   a.cu_seqlens = s->cu_seqlens;
 }
 
-}  // namespace
-
-extern "C" {
-
-size_t comba_fwd_workspace_bytes(const comba_shape* shape) {
-  Dims d;
-  if (check_shape(shape, &d) != COMBA_OK) return 0;
-  return layout(d, false).total;
-}
-
-size_t comba_bwd_workspace_bytes(const comba_shape* shape) {
-  Dims d;
-  if (check_shape(shape, &d) != COMBA_OK) return 0;
-  return layout(d, true).total;
-}
-
-comba_status comba_chunk_fwd(const comba_shape* shape, const void* q, const void* k, const void* v,
-                             const float* g, const void* beta, const float* d, const float* h0,
-                             float* o, float* ht, void* ws, size_t ws_bytes, void* stream) {
+comba_status chunk_fwd(bool save, const comba_shape* shape, const void* q, const void* k,
+                              const void* v, const float* g, const void* beta, const float* d,
+                              const float* h0, float* o, float* ht, void* ws, size_t ws_bytes,
+                              void* stream) {
   Dims dm;
   comba_status st = check_shape(shape, &dm);
   if (st != COMBA_OK) return st;
@@ -199,10 +184,11 @@ comba_status comba_chunk_fwd(const comba_shape* shape, const void* q, const void
       !aligned(g, 4) || !aligned(d, 4) || !aligned(o, 4) || (h0 && !aligned(h0, 4)) ||
       (ht && !aligned(ht, 4)) || !aligned(beta, dm.bf16 ? 2 : 4))
     return COMBA_ERR_ALIGN;
-  const Layout L = layout(dm, false);
+  const Layout L = layout(dm, save);
   if (ws_bytes < L.total) return COMBA_ERR_WORKSPACE;
   comba::LaunchArgs a{};
   fill_common(a, dm, shape);
+  a.saved = save;
   a.q = q;
   a.k = k;
   a.v = v;
@@ -213,17 +199,17 @@ comba_status comba_chunk_fwd(const comba_shape* shape, const void* q, const void
   a.o = o;
   a.ht = ht;
   a.stream = static_cast<hipStream_t>(stream);
-  carve(a, L, ws, false);
+  carve(a, L, ws, save);
   attach_profile(a);
   if (dm.N == 0) return COMBA_OK;
   return comba::launch_fwd(a) == hipSuccess ? COMBA_OK : COMBA_ERR_HIP;
 }
 
-comba_status comba_chunk_bwd(const comba_shape* shape, const void* q, const void* k, const void* v,
-                             const float* g, const void* beta, const float* d, const float* h0,
-                             const void* dO, const float* dht, float* dq, float* dk, float* dv,
-                             float* dg, float* dbeta, float* dd, float* dh0, void* ws,
-                             size_t ws_bytes, void* stream) {
+comba_status chunk_bwd(bool saved, const comba_shape* shape, const void* q, const void* k,
+                              const void* v, const float* g, const void* beta, const float* d,
+                              const float* h0, const void* dO, const float* dht, float* dq,
+                              float* dk, float* dv, float* dg, float* dbeta, float* dd,
+                              float* dh0, void* ws, size_t ws_bytes, void* stream) {
   Dims dm;
   comba_status st = check_shape(shape, &dm);
   if (st != COMBA_OK) return st;
@@ -240,6 +226,7 @@ comba_status comba_chunk_bwd(const comba_shape* shape, const void* q, const void
   if (ws_bytes < L.total) return COMBA_ERR_WORKSPACE;
   comba::LaunchArgs a{};
   fill_common(a, dm, shape);
+  a.saved = saved;
   a.q = q;
   a.k = k;
   a.v = v;
@@ -262,6 +249,22 @@ comba_status comba_chunk_bwd(const comba_shape* shape, const void* q, const void
   return comba::launch_bwd(a) == hipSuccess ? COMBA_OK : COMBA_ERR_HIP;
 }
 
+}  // namespace
+
+extern "C" {
+
+size_t comba_fwd_workspace_bytes(const comba_shape* shape) {
+  Dims d;
+  if (check_shape(shape, &d) != COMBA_OK) return 0;
+  return layout(d, false).total;
+}
+
+size_t comba_bwd_workspace_bytes(const comba_shape* shape) {
+  Dims d;
+  if (check_shape(shape, &d) != COMBA_OK) return 0;
+  return layout(d, true).total;
+}
+
 comba_status comba_profile_enable(int enable) {
   g_prof.on = enable != 0;
   g_prof.n = 0;
@@ -281,6 +284,38 @@ int comba_profile_read(float* ms, const char** names, int capacity) {
     ++out;
   }
   return out;
+}
+
+comba_status comba_chunk_fwd(const comba_shape* shape, const void* q, const void* k, const void* v,
+                             const float* g, const void* beta, const float* d, const float* h0,
+                             float* o, float* ht, void* ws, size_t ws_bytes, void* stream) {
+  return chunk_fwd(false, shape, q, k, v, g, beta, d, h0, o, ht, ws, ws_bytes, stream);
+}
+
+comba_status comba_chunk_fwd_save(const comba_shape* shape, const void* q, const void* k,
+                                  const void* v, const float* g, const void* beta, const float* d,
+                                  const float* h0, float* o, float* ht, void* ws, size_t ws_bytes,
+                                  void* stream) {
+  return chunk_fwd(true, shape, q, k, v, g, beta, d, h0, o, ht, ws, ws_bytes, stream);
+}
+
+comba_status comba_chunk_bwd(const comba_shape* shape, const void* q, const void* k, const void* v,
+                             const float* g, const void* beta, const float* d, const float* h0,
+                             const void* dO, const float* dht, float* dq, float* dk, float* dv,
+                             float* dg, float* dbeta, float* dd, float* dh0, void* ws,
+                             size_t ws_bytes, void* stream) {
+  return chunk_bwd(false, shape, q, k, v, g, beta, d, h0, dO, dht, dq, dk, dv, dg, dbeta, dd, dh0,
+                   ws, ws_bytes, stream);
+}
+
+comba_status comba_chunk_bwd_saved(const comba_shape* shape, const void* q, const void* k,
+                                   const void* v, const float* g, const void* beta,
+                                   const float* d, const float* h0, const void* dO,
+                                   const float* dht, float* dq, float* dk, float* dv, float* dg,
+                                   float* dbeta, float* dd, float* dh0, void* ws, size_t ws_bytes,
+                                   void* stream) {
+  return chunk_bwd(true, shape, q, k, v, g, beta, d, h0, dO, dht, dq, dk, dv, dg, dbeta, dd, dh0,
+                   ws, ws_bytes, stream);
 }
 
 const char* comba_status_string(comba_status s) {

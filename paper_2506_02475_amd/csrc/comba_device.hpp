@@ -168,7 +168,7 @@ __device__ __forceinline__ float wave_sum(float x) {
 // back to back (rows >= `rows` read as zero) so their latencies overlap; the
 // store functions then write LDS.  Keeping load() and store() apart lets a
 // kernel issue the next chunk's loads before computing on the current one.
-template <typename T, int NROWS, int COLS>
+template <typename T, int NROWS, int COLS, int NTHR = comba::NTHR>
 struct TileRegs {
   static constexpr int V = 16 / sizeof(T);
   static constexpr int PER_ROW = COLS / V;

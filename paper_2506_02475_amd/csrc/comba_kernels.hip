@@ -1569,6 +1569,377 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
 }
 
 // ---------------------------------------------------------------------------
+// k_intra_bwd_bf: per chunk-head gradients for bf16 inputs, 8 wavefronts.
+// Wave w works on row tile rt = w % 4 (rows 16 rt .. 16 rt + 15) and column
+// half ch = w / 4 of every chunk product.  Phase 1 streams dv in blocks of 32
+// (prefetched one block ahead; fp32 operands are split into bf16 hi/lo once,
+// when staged into LDS) and accumulates T1 = dO X^T, T3 = dR X^T, T2 = D Y^T,
+// dA = dO D^T, dL = dR D^T.  Phase 2 forms dQ~ and dK, with the K^T and Q^T
+// B-operands read straight from the prep output.
+// ---------------------------------------------------------------------------
+constexpr int IB_THR = 512;
+
+template <int DK>
+struct IntraBwdBfSmem {
+  static constexpr int VB = 32, LDB = VB + 8;
+  static constexpr int LDK = DK + 8, LDC = CH + 8;
+  static constexpr int P1 = (5 * CH * LDB + 4 * DK * LDB) * 2;
+  static constexpr int P2 = (2 * CH * LDK + 6 * CH * LDC) * 2;
+  static constexpr int BYTES = P1 > P2 ? P1 : P2;
+};
+
+__device__ __forceinline__ void split4v(const float4& x, bf16x4& hi, bf16x4& lo) {
+  const float a[4] = {x.x, x.y, x.z, x.w};
+  split4(a, hi, lo);
+}
+__device__ __forceinline__ void put_split(bf16_t* hi, bf16_t* lo, float x) {
+  const __bf16 h = (__bf16)x;
+  *hi = __builtin_bit_cast(bf16_t, h);
+  *lo = __builtin_bit_cast(bf16_t, (__bf16)(x - (float)h));
+}
+
+template <int DK, int DV>
+__global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
+    const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
+    const bf16_t* __restrict__ dO, const bf16_t* __restrict__ beta, const float* __restrict__ d,
+    const ChunkInfo* __restrict__ cmap, int H, const float* __restrict__ Gw,
+    const float* __restrict__ Xw, const float* __restrict__ Dw, const float* __restrict__ Yw,
+    const float* __restrict__ dRw, const bf16_t* __restrict__ KTp,
+    const bf16_t* __restrict__ QTp, float* __restrict__ dq, float* __restrict__ dk,
+    float* __restrict__ dv, float* __restrict__ dbeta, float* __restrict__ dg,
+    float* __restrict__ ddp, float* __restrict__ sink) {
+  using SM = IntraBwdBfSmem<DK>;
+  constexpr int VB = SM::VB, LDB = SM::LDB, LDK = SM::LDK, LDC = SM::LDC;
+  constexpr int NTW = DK / 32;          // dk column tiles per wave
+  constexpr int NW = IB_THR / 64;       // wavefronts
+  constexpr int NVB = DV / VB;
+  constexpr int XP = DK * (VB / 4) / IB_THR;  // X / Y 16-byte pieces per thread
+  __shared__ __align__(16) char smem[SM::BYTES];
+  __shared__ float Gs[CH], Bs[CH], rowB[CH];
+  __shared__ float colpart[4][CH];      // per row tile: column sums of E1 + E2
+  __shared__ float rowacc[2][6][CH];    // per column half: E1, E2, BL, p1, p2, p3 row sums
+  __shared__ float scal[NW][2];         // per wave: <X, Y>_F, sum k . dQ~
+
+  const int h = blockIdx.y;
+  const long chh = (long)blockIdx.x * H + h;
+  const ChunkInfo ci = cmap[blockIdx.x];
+  if (ci.len <= 0) {
+    if (threadIdx.x == 0) ddp[chh] = 0.f;
+    return;
+  }
+  const long tok = (long)ci.tok0 * H + h;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r16 = lane & 15, g4 = lane >> 4;
+  const int rt = w & 3, ch = w >> 2;
+  const int len = ci.len;
+  const float dh = d[h];
+  if (tid < CH) {
+    Gs[tid] = Gw[chh * CH + tid];
+    Bs[tid] = tid < len ? bf2f(beta[tok + (long)tid * H]) : 0.f;
+  }
+
+  // ---------------- phase 1 ----------------
+  bf16_t* dOb = reinterpret_cast<bf16_t*>(smem);
+  bf16_t* dRh = dOb + CH * LDB;
+  bf16_t* dRl = dRh + CH * LDB;
+  bf16_t* Dh = dRl + CH * LDB;
+  bf16_t* Dl = Dh + CH * LDB;
+  bf16_t* Xh = Dl + CH * LDB;
+  bf16_t* Xl = Xh + DK * LDB;
+  bf16_t* Yh = Xl + DK * LDB;
+  bf16_t* Yl = Yh + DK * LDB;
+
+  const int po = tid & 255, po_r = po >> 2, po_c = (po & 3) * 8;  // dO piece (dup. above 256)
+  const int pf_r = tid >> 3, pf_c = (tid & 7) * 4;                 // dR / D / v piece
+  uint4 r_do;
+  float4 r_dr, r_d, r_x[XP], r_y[XP];
+  uint2 r_v;
+  auto issue = [&](int vb) {
+    const int j = vb * VB;
+    r_do = *reinterpret_cast<const uint4*>(dO + (tok + (long)min(po_r, len - 1) * H) * DV + j + po_c);
+    r_v = *reinterpret_cast<const uint2*>(v + (tok + (long)min(pf_r, len - 1) * H) * DV + j + pf_c);
+    r_dr = *reinterpret_cast<const float4*>(dRw + chh * CH * DV + (long)pf_r * DV + j + pf_c);
+    r_d = *reinterpret_cast<const float4*>(Dw + chh * CH * DV + (long)pf_r * DV + j + pf_c);
+#pragma unroll
+    for (int p = 0; p < XP; ++p) {
+      const int pc = tid + p * IB_THR, xr = pc >> 3, xc = (pc & 7) * 4;
+      r_x[p] = *reinterpret_cast<const float4*>(Xw + chh * DK * DV + (long)xr * DV + j + xc);
+      r_y[p] = *reinterpret_cast<const float4*>(Yw + chh * DK * DV + (long)xr * DV + j + xc);
+    }
+  };
+  float Fpart = 0.f, bv = 0.f;
+  auto put = [&](int vb) {
+    const int j = vb * VB;
+    *reinterpret_cast<uint4*>(dOb + po_r * LDB + po_c) = po_r < len ? r_do : make_uint4(0, 0, 0, 0);
+    bf16x4 hh, ll;
+    split4v(r_dr, hh, ll);
+    *reinterpret_cast<bf16x4*>(dRh + pf_r * LDB + pf_c) = hh;
+    *reinterpret_cast<bf16x4*>(dRl + pf_r * LDB + pf_c) = ll;
+    split4v(r_d, hh, ll);
+    *reinterpret_cast<bf16x4*>(Dh + pf_r * LDB + pf_c) = hh;
+    *reinterpret_cast<bf16x4*>(Dl + pf_r * LDB + pf_c) = ll;
+#pragma unroll
+    for (int p = 0; p < XP; ++p) {
+      const int pc = tid + p * IB_THR, xr = pc >> 3, xc = (pc & 7) * 4;
+      split4v(r_x[p], hh, ll);
+      *reinterpret_cast<bf16x4*>(Xh + xr * LDB + xc) = hh;
+      *reinterpret_cast<bf16x4*>(Xl + xr * LDB + xc) = ll;
+      split4v(r_y[p], hh, ll);
+      *reinterpret_cast<bf16x4*>(Yh + xr * LDB + xc) = hh;
+      *reinterpret_cast<bf16x4*>(Yl + xr * LDB + xc) = ll;
+      Fpart += r_x[p].x * r_y[p].x + r_x[p].y * r_y[p].y + r_x[p].z * r_y[p].z + r_x[p].w * r_y[p].w;
+    }
+    // dv = Diag(beta) dR and <v_r, dR_r>
+    const float b = Bs[pf_r];
+    const float4 dvv = make_float4(b * r_dr.x, b * r_dr.y, b * r_dr.z, b * r_dr.w);
+    float* dst = pf_r < len ? dv + (tok + (long)pf_r * H) * DV + j + pf_c : sink + (tid & 63) * 4;
+    *reinterpret_cast<float4*>(dst) = dvv;
+    union { uint2 u; bf16_t e[4]; } vv;
+    vv.u = r_v;
+    bv += bf2f(vv.e[0]) * r_dr.x + bf2f(vv.e[1]) * r_dr.y + bf2f(vv.e[2]) * r_dr.z +
+          bf2f(vv.e[3]) * r_dr.w;
+  };
+
+  floatx4 T1[NTW], T2[NTW], T3[NTW], dA[2], dL[2];
+#pragma unroll
+  for (int j = 0; j < NTW; ++j) {
+    T1[j] = zero4();
+    T2[j] = zero4();
+    T3[j] = zero4();
+  }
+  dA[0] = dA[1] = dL[0] = dL[1] = zero4();
+  TileRegs<bf16_t, CH, DK, IB_THR> kr, qr;
+  issue(0);
+  for (int vb = 0; vb < NVB; ++vb) {
+    __syncthreads();
+    put(vb);
+    __syncthreads();
+    if (vb + 1 < NVB) {
+      issue(vb + 1);
+    } else {
+      kr.load(k + tok * DK, (long)H * DK, len);
+      qr.load(q + tok * DK, (long)H * DK, len);
+    }
+    const int arow = (16 * rt + r16) * LDB + 8 * g4;
+    const bf16x8 a_do = ld8(dOb + arow), a_drh = ld8(dRh + arow), a_drl = ld8(dRl + arow);
+    const bf16x8 a_dh = ld8(Dh + arow), a_dl = ld8(Dl + arow);
+#pragma unroll
+    for (int j = 0; j < NTW; ++j) {
+      const int brow = (16 * (ch * NTW + j) + r16) * LDB + 8 * g4;
+      const bf16x8 xh = ld8(Xh + brow), xl = ld8(Xl + brow);
+      const bf16x8 yh = ld8(Yh + brow), yl = ld8(Yl + brow);
+      T1[j] = mfma16(a_do, xh, T1[j]);
+      T1[j] = mfma16(a_do, xl, T1[j]);
+      T3[j] = mfma16(a_drh, xh, T3[j]);
+      T3[j] = mfma16(a_drh, xl, T3[j]);
+      T3[j] = mfma16(a_drl, xh, T3[j]);
+      T2[j] = mfma16(a_dh, yh, T2[j]);
+      T2[j] = mfma16(a_dh, yl, T2[j]);
+      T2[j] = mfma16(a_dl, yh, T2[j]);
+    }
+#pragma unroll
+    for (int j2 = 0; j2 < 2; ++j2) {
+      const int brow = (16 * (2 * ch + j2) + r16) * LDB + 8 * g4;
+      const bf16x8 bh = ld8(Dh + brow), bl = ld8(Dl + brow);
+      dA[j2] = mfma16(a_do, bh, dA[j2]);
+      dA[j2] = mfma16(a_do, bl, dA[j2]);
+      dL[j2] = mfma16(a_drh, bh, dL[j2]);
+      dL[j2] = mfma16(a_drh, bl, dL[j2]);
+      dL[j2] = mfma16(a_drl, bh, dL[j2]);
+    }
+  }
+  bv += __shfl_xor(bv, 1);
+  bv += __shfl_xor(bv, 2);
+  bv += __shfl_xor(bv, 4);
+  if ((tid & 7) == 0) rowB[pf_r] = bv;
+  Fpart = wave_sum(Fpart);
+  if (lane == 0) scal[w][0] = Fpart;
+  __syncthreads();
+
+  // ---------------- phase 2 ----------------
+  bf16_t* Ks = reinterpret_cast<bf16_t*>(smem);
+  bf16_t* Qs = Ks + CH * LDK;
+  bf16_t* Gh = Qs + CH * LDK;   // dA o Gamma (hi, lo), row-major
+  bf16_t* Gl = Gh + CH * LDC;
+  bf16_t* GTh = Gl + CH * LDC;  // its transpose
+  bf16_t* GTl = GTh + CH * LDC;
+  bf16_t* Sh = GTl + CH * LDC;  // dAkk + dAkk^T - d (dA o Gamma)^T
+  bf16_t* Sl = Sh + CH * LDC;
+  kr.store(Ks, LDK);
+  qr.store(Qs, LDK);
+  // B operands K^T, Q^T of this wave's dk columns: B(k = t, n = c) = K[t][c]
+  bf16x8 ktb[NTW][2], qtb[NTW][2];
+#pragma unroll
+  for (int j = 0; j < NTW; ++j)
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const long off = chh * DK * CH + (long)(16 * (ch * NTW + j) + r16) * CH + 32 * ks + 8 * g4;
+      ktb[j][ks] = ld8(KTp + off);
+      qtb[j][ks] = ld8(QTp + off);
+    }
+  __syncthreads();
+  const float Glast = Gs[CH - 1];
+  {
+    floatx4 akk[2], aqk[2];
+    akk[0] = akk[1] = aqk[0] = aqk[1] = zero4();
+#pragma unroll
+    for (int ks = 0; ks < DK / 32; ++ks) {
+      const int ar = (16 * rt + r16) * LDK + 32 * ks + 8 * g4;
+      const bf16x8 a_k = ld8(Ks + ar), a_q = ld8(Qs + ar);
+#pragma unroll
+      for (int j2 = 0; j2 < 2; ++j2) {
+        const bf16x8 b = ld8(Ks + (16 * (2 * ch + j2) + r16) * LDK + 32 * ks + 8 * g4);
+        akk[j2] = mfma16(a_k, b, akk[j2]);
+        aqk[j2] = mfma16(a_q, b, aqk[j2]);
+      }
+    }
+    float rE1[4] = {0.f, 0.f, 0.f, 0.f}, rE2[4] = {0.f, 0.f, 0.f, 0.f}, rBL[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j2 = 0; j2 < 2; ++j2) {
+      const int c = 16 * (2 * ch + j2) + r16;
+      float cE = 0.f, dagv[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = 16 * rt + 4 * g4 + e;
+        const float kk = akk[j2][e];
+        float dag = 0.f, e1 = 0.f, e2 = 0.f, dakk = 0.f;
+        if (r >= c) {
+          const float gam = __expf(Gs[r] - Gs[c]);
+          const float a = (aqk[j2][e] - dh * kk) * gam;
+          const float da = dA[j2][e];
+          e1 = da * a;
+          dag = da * gam;
+        }
+        if (r > c) {
+          const float lc = __expf(Gs[r - 1] - Gs[c]);
+          const float dl = -dL[j2][e];
+          const float lck = lc * kk;
+          e2 = dl * Bs[r] * lck;
+          rBL[e] += dl * lck;
+          dakk = dl * Bs[r] * lc;
+          put_split(Sh + r * LDC + c, Sl + r * LDC + c, dakk);
+        }
+        if (r >= c) put_split(Sh + c * LDC + r, Sl + c * LDC + r, dakk - dh * dag);
+        put_split(Gh + r * LDC + c, Gl + r * LDC + c, dag);
+        dagv[e] = dag;
+        rE1[e] += e1;
+        rE2[e] += e2;
+        cE += e1 + e2;
+      }
+      put_t4(GTh, GTl, c * LDC + 16 * rt + 4 * g4, dagv);
+      cE = sum_groups(cE);
+      if (g4 == 0) colpart[rt][c] = cE;
+    }
+    // row dot products of T1, T2, T3 with q~ and k over this wave's columns
+    float p1[4] = {0.f, 0.f, 0.f, 0.f}, p2[4] = {0.f, 0.f, 0.f, 0.f}, p3[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < NTW; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = 16 * rt + 4 * g4 + e, c = 16 * (ch * NTW + j) + r16;
+        const float kv = bf2f(Ks[r * LDK + c]);
+        const float qv = bf2f(Qs[r * LDK + c]) - dh * kv;
+        p1[e] += T1[j][e] * qv;
+        p2[e] += T2[j][e] * kv;
+        p3[e] += T3[j][e] * kv;
+      }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float s0 = sum16(rE1[e]), s1 = sum16(rE2[e]), s2 = sum16(rBL[e]);
+      const float s3 = sum16(p1[e]), s4 = sum16(p2[e]), s5 = sum16(p3[e]);
+      if (r16 == 0) {
+        const int r = 16 * rt + 4 * g4 + e;
+        rowacc[ch][0][r] = s0;
+        rowacc[ch][1][r] = s1;
+        rowacc[ch][2][r] = s2;
+        rowacc[ch][3][r] = s3;
+        rowacc[ch][4][r] = s4;
+        rowacc[ch][5][r] = s5;
+      }
+    }
+  }
+  __syncthreads();
+
+  // dQ~ (in T1) and dK (in T2)
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int r = 16 * rt + 4 * g4 + e;
+    const float gr = __expf(Gs[r]), dec = __expf(Glast - Gs[r]);
+    const float sr = Bs[r] * __expf(r > 0 ? Gs[r - 1] : 0.f);
+#pragma unroll
+    for (int j = 0; j < NTW; ++j) {
+      T1[j][e] *= gr;
+      T2[j][e] = dec * T2[j][e] - sr * T3[j][e];
+    }
+  }
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) {
+    const int ar = (16 * rt + r16) * LDC + 32 * ks + 8 * g4;
+    const bf16x8 agh = ld8(Gh + ar), agl = ld8(Gl + ar);
+    const bf16x8 ath = ld8(GTh + ar), atl = ld8(GTl + ar);
+    const bf16x8 ash = ld8(Sh + ar), asl = ld8(Sl + ar);
+#pragma unroll
+    for (int j = 0; j < NTW; ++j) {
+      T1[j] = mfma16(agh, ktb[j][ks], T1[j]);
+      T1[j] = mfma16(agl, ktb[j][ks], T1[j]);
+      T2[j] = mfma16(ath, qtb[j][ks], T2[j]);
+      T2[j] = mfma16(atl, qtb[j][ks], T2[j]);
+      T2[j] = mfma16(ash, ktb[j][ks], T2[j]);
+      T2[j] = mfma16(asl, ktb[j][ks], T2[j]);
+    }
+  }
+  float ddpart = 0.f;
+#pragma unroll
+  for (int j = 0; j < NTW; ++j)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int r = 16 * rt + 4 * g4 + e, c = 16 * (ch * NTW + j) + r16;
+      const float dqt = T1[j][e];
+      ddpart += bf2f(Ks[r * LDK + c]) * dqt;
+      const bool ok = r < len;
+      const long off = (tok + (long)r * H) * DK + c;
+      *(ok ? dq + off : sink + lane) = dqt;
+      *(ok ? dk + off : sink + 64 + lane) = T2[j][e] - dh * dqt;
+    }
+  ddpart = wave_sum(ddpart);
+  if (lane == 0) scal[w][1] = ddpart;
+  __syncthreads();
+
+  if (w == 0) {
+    const int r = lane;
+    float F = 0.f, dds = 0.f;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      F += scal[i][0];
+      dds += scal[i][1];
+    }
+    const float e1 = rowacc[0][0][r] + rowacc[1][0][r];
+    const float e2 = rowacc[0][1][r] + rowacc[1][1][r];
+    const float bl = rowacc[0][2][r] + rowacc[1][2][r];
+    const float p1 = rowacc[0][3][r] + rowacc[1][3][r];
+    const float p2 = rowacc[0][4][r] + rowacc[1][4][r];
+    const float p3 = rowacc[0][5][r] + rowacc[1][5][r];
+    const float col = colpart[0][r] + colpart[1][r] + colpart[2][r] + colpart[3][r];
+    const float egm = __expf(r > 0 ? Gs[r - 1] : 0.f);
+    const float cr = __expf(Glast - Gs[r]) * p2;
+    const float rowg = e1 + __expf(Gs[r]) * p1 - cr;
+    const float rowgm = e2 - Bs[r] * egm * p3;
+    const float rowb = rowB[r] + bl - egm * p3;
+    const float gcs = wave_sum(cr);
+    const float rowgm_next = __shfl_down(rowgm, 1);
+    float dG = rowg - col + (r + 1 < CH ? rowgm_next : 0.f);
+    if (r == CH - 1) dG += gcs + __expf(Glast) * F;
+    float x = __shfl(dG, 63 - lane);
+    x = wave_prefix_sum(x);
+    const float dgr = __shfl(x, 63 - lane);
+    if (r < len) {
+      dg[tok + (long)r * H] = dgr;
+      dbeta[tok + (long)r * H] = rowb;
+    }
+    if (lane == 0) ddp[chh] = -dds;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // host launchers
 // ---------------------------------------------------------------------------
 template <typename Tin, int DK, int DV>
@@ -1585,8 +1956,13 @@ static hipError_t run_fwd(const LaunchArgs& a) {
     k_prep<Tin, DK><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(q, k, a.g, beta, a.d, a.cmap, a.H, a.Mw,
                                                          a.Aw, a.Gw);
   a.stage("scan_fwd");
-  k_scan_fwd<Tin, DK, DV, true, false><<<dim3(a.N, a.H, DV / 32), NTHR, 0, st>>>(
-      q, k, v, beta, a.d, a.h0, a.cmap, a.smap, a.H, a.Mw, a.Aw, a.Gw, a.o, a.ht, nullptr, nullptr);
+  if (a.saved)
+    k_scan_fwd<Tin, DK, DV, true, true><<<dim3(a.N, a.H, DV / 32), NTHR, 0, st>>>(
+        q, k, v, beta, a.d, a.h0, a.cmap, a.smap, a.H, a.Mw, a.Aw, a.Gw, a.o, a.ht, a.Xw, a.Dw);
+  else
+    k_scan_fwd<Tin, DK, DV, true, false><<<dim3(a.N, a.H, DV / 32), NTHR, 0, st>>>(
+        q, k, v, beta, a.d, a.h0, a.cmap, a.smap, a.H, a.Mw, a.Aw, a.Gw, a.o, a.ht, nullptr,
+        nullptr);
   a.stage(nullptr);
   return hipGetLastError();
 }
@@ -1604,16 +1980,18 @@ static hipError_t run_bwd(const LaunchArgs& a) {
     k_reduce_dd<<<a.H, NTHR, 0, st>>>(a.ddp, 0, a.H, a.dd);
     return hipGetLastError();
   }
-  a.stage("chunk_map");
-  k_chunk_map<<<1, NTHR, 0, st>>>(a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.ncmax, a.cmap, a.smap);
-  a.stage("prep");
-  if (a.ncmax > 0)
-    k_prep<Tin, DK><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(q, k, a.g, beta, a.d, a.cmap, a.H, a.Mw,
-                                                         a.Aw, a.Gw);
-  a.stage("scan_fwd_store");
-  k_scan_fwd<Tin, DK, DV, false, true><<<dim3(a.N, a.H, DV / 32), NTHR, 0, st>>>(
-      q, k, v, beta, a.d, a.h0, a.cmap, a.smap, a.H, a.Mw, a.Aw, a.Gw, nullptr, nullptr, a.Xw,
-      a.Dw);
+  if (!a.saved) {
+    a.stage("chunk_map");
+    k_chunk_map<<<1, NTHR, 0, st>>>(a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.ncmax, a.cmap, a.smap);
+    a.stage("prep");
+    if (a.ncmax > 0)
+      k_prep<Tin, DK><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(q, k, a.g, beta, a.d, a.cmap, a.H,
+                                                           a.Mw, a.Aw, a.Gw);
+    a.stage("scan_fwd_store");
+    k_scan_fwd<Tin, DK, DV, false, true><<<dim3(a.N, a.H, DV / 32), NTHR, 0, st>>>(
+        q, k, v, beta, a.d, a.h0, a.cmap, a.smap, a.H, a.Mw, a.Aw, a.Gw, nullptr, nullptr, a.Xw,
+        a.Dw);
+  }
   a.stage("scan_bwd");
   k_scan_bwd<Tin, DK, DV><<<dim3(a.N, a.H, DV / 32), NTHR, 0, st>>>(
       q, k, dO, beta, a.d, a.dht, a.cmap, a.smap, a.H, a.Mw, a.Aw, a.Gw, a.dh0, a.Yw, a.dRw);
@@ -1637,14 +2015,24 @@ static hipError_t run_fwd_bf(const LaunchArgs& a) {
   const bf16_t* beta = static_cast<const bf16_t*>(a.beta);
   a.stage("chunk_map");
   k_chunk_map<<<1, NTHR, 0, st>>>(a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.ncmax, a.cmap, a.smap);
-  a.stage("prep");
-  if (a.ncmax > 0)
-    k_prep_bf<DK, false><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
-        q, k, a.g, beta, a.d, a.cmap, a.H, a.Mp, a.Ap, nullptr, nullptr, a.KTp, nullptr, a.Gw);
-  a.stage("scan_fwd");
-  k_scan_fwd_bf<DK, DV, SCAN_BV, true, false><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-      q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mp, a.Ap, a.KTp, a.Gw, a.o, a.ht, nullptr, nullptr,
-      nullptr, a.sink);
+  a.stage(a.saved ? "prep_save" : "prep");
+  if (a.ncmax > 0) {
+    if (a.saved)
+      k_prep_bf<DK, true><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
+          q, k, a.g, beta, a.d, a.cmap, a.H, a.Mp, a.Ap, a.MTp, a.ATp, a.KTp, a.QTp, a.Gw);
+    else
+      k_prep_bf<DK, false><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
+          q, k, a.g, beta, a.d, a.cmap, a.H, a.Mp, a.Ap, nullptr, nullptr, a.KTp, nullptr, a.Gw);
+  }
+  a.stage(a.saved ? "scan_fwd_save" : "scan_fwd");
+  if (a.saved)
+    k_scan_fwd_bf<DK, DV, SCAN_BV, true, true><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
+        q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mp, a.Ap, a.KTp, a.Gw, a.o, a.ht, a.Xw, a.Dw,
+        a.Xfin, a.sink);
+  else
+    k_scan_fwd_bf<DK, DV, SCAN_BV, true, false><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
+        q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mp, a.Ap, a.KTp, a.Gw, a.o, a.ht, nullptr,
+        nullptr, nullptr, a.sink);
   a.stage(nullptr);
   return hipGetLastError();
 }
@@ -1661,25 +2049,27 @@ static hipError_t run_bwd_bf(const LaunchArgs& a) {
     k_reduce_dd<<<a.H, NTHR, 0, st>>>(a.ddp, 0, a.H, a.dd);
     return hipGetLastError();
   }
-  a.stage("chunk_map");
-  k_chunk_map<<<1, NTHR, 0, st>>>(a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.ncmax, a.cmap, a.smap);
-  a.stage("prep");
-  if (a.ncmax > 0)
-    k_prep_bf<DK, true><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
-        q, k, a.g, beta, a.d, a.cmap, a.H, a.Mp, a.Ap, a.MTp, a.ATp, a.KTp, a.QTp, a.Gw);
-  a.stage("scan_fwd_store");
-  k_scan_fwd_bf<DK, DV, SCAN_BV, false, true><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-      q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mp, a.Ap, a.KTp, a.Gw, nullptr, nullptr, a.Xw,
-      a.Dw, a.Xfin, a.sink);
+  if (!a.saved) {
+    a.stage("chunk_map");
+    k_chunk_map<<<1, NTHR, 0, st>>>(a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.ncmax, a.cmap, a.smap);
+    a.stage("prep");
+    if (a.ncmax > 0)
+      k_prep_bf<DK, true><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
+          q, k, a.g, beta, a.d, a.cmap, a.H, a.Mp, a.Ap, a.MTp, a.ATp, a.KTp, a.QTp, a.Gw);
+    a.stage("scan_fwd_store");
+    k_scan_fwd_bf<DK, DV, SCAN_BV, false, true><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
+        q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mp, a.Ap, a.KTp, a.Gw, nullptr, nullptr, a.Xw,
+        a.Dw, a.Xfin, a.sink);
+  }
   a.stage("scan_bwd");
   k_scan_bwd_bf<DK, DV, SCAN_BV><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
       q, k, dO, beta, a.d, a.dht, a.smap, a.H, a.MTp, a.ATp, a.KTp, a.QTp, a.Gw, a.dh0, a.Yw,
       a.dRw);
   a.stage("intra_bwd");
   if (a.ncmax > 0)
-    k_intra_bwd<bf16_t, DK, DV><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
-        q, k, v, dO, beta, a.d, a.cmap, a.H, a.Gw, a.Xw, a.Dw, a.Yw, a.dRw, a.dq, a.dk_, a.dv_,
-        a.dbeta, a.dg, a.ddp);
+    k_intra_bwd_bf<DK, DV><<<dim3(a.ncmax, a.H), IB_THR, 0, st>>>(
+        q, k, v, dO, beta, a.d, a.cmap, a.H, a.Gw, a.Xw, a.Dw, a.Yw, a.dRw, a.KTp, a.QTp, a.dq,
+        a.dk_, a.dv_, a.dbeta, a.dg, a.ddp, a.sink);
   a.stage("reduce_dd");
   k_reduce_dd<<<a.H, NTHR, 0, st>>>(a.ddp, a.ncmax, a.H, a.dd);
   a.stage(nullptr);

@@ -25,6 +25,10 @@ struct StageHook {
 
 struct LaunchArgs {
   bool bf16;
+  // forward: also leave the backward's state (tables, per-chunk operands,
+  // chunk states X and D) in the backward-sized workspace;
+  // backward: reuse that state instead of recomputing the forward
+  bool saved;
   int dk, dv, H, N, Tseq, Ttot, ncmax;
   const int32_t* cu_seqlens;
   const void *q, *k, *v, *beta, *dO;

@@ -48,7 +48,8 @@ def test_library_exports_every_declared_symbol():
     declared = comba.exported_symbols()
     assert set(declared) == {"comba_fwd_workspace_bytes", "comba_bwd_workspace_bytes",
                              "comba_chunk_fwd", "comba_chunk_bwd", "comba_status_string",
-                             "comba_profile_enable", "comba_profile_read"}
+                             "comba_profile_enable", "comba_profile_read",
+                             "comba_chunk_fwd_save", "comba_chunk_bwd_saved"}
     out = subprocess.run(["nm", "-D", "--defined-only", comba.library_path()],
                          capture_output=True, text=True, check=True).stdout
     exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
@@ -113,6 +114,28 @@ def test_rejects_null_and_misaligned_pointers():
     lib = comba.load_library()
     assert lib.comba_chunk_fwd(None, *[ctypes.c_void_p(FAKE)] * 9, ctypes.c_void_p(FAKE),
                                ctypes.c_size_t(1 << 40), None) == ENULL
+
+
+def test_saved_pair_validates_like_the_plain_calls():
+    lib = comba.load_library()
+    P = ctypes.c_void_p
+    s = shape(chunk=32)
+    args = [P(FAKE)] * 9
+    assert lib.comba_chunk_fwd_save(ctypes.byref(s), *args, P(FAKE), ctypes.c_size_t(1 << 40),
+                                    None) == ESHAPE
+    s = shape()
+    # the forward-with-save needs the backward-sized workspace
+    need_f = lib.comba_fwd_workspace_bytes(ctypes.byref(s))
+    need_b = lib.comba_bwd_workspace_bytes(ctypes.byref(s))
+    assert need_b > need_f
+    assert lib.comba_chunk_fwd_save(ctypes.byref(s), *args, P(FAKE), ctypes.c_size_t(need_f),
+                                    None) == EWS
+    bargs = [P(FAKE)] * 16
+    assert lib.comba_chunk_bwd_saved(ctypes.byref(s), *bargs, P(FAKE),
+                                     ctypes.c_size_t(need_b - 1), None) == EWS
+    bargs[7] = None  # dO
+    assert lib.comba_chunk_bwd_saved(ctypes.byref(s), *bargs, P(FAKE),
+                                     ctypes.c_size_t(need_b), None) == ENULL
 
 
 def test_rejects_small_workspace():

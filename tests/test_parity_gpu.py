@@ -110,6 +110,43 @@ def test_segment_chaining_matches_one_pass():
     assert maxrel(h2, ht) < 1e-5
 
 
+# ------------------------------------------------------------ saved-state pair
+SAVED = [
+    ("bf16_B2_T300", dict(B=2, T=300, H=2, dk=128, dv=128, in_dtype="bf16")),
+    ("bf16_varlen", dict(T=0, H=2, dk=128, dv=128, in_dtype="bf16", seqlens=[1, 70, 0, 200])),
+    ("bf16_d64", dict(B=1, T=130, H=3, dk=64, dv=64, in_dtype="bf16")),
+    ("f32_ragged", dict(B=2, T=130, H=2, dk=64, dv=64, in_dtype="f32")),
+]
+
+
+@pytest.mark.parametrize("name,kw", SAVED, ids=[s_[0] for s_ in SAVED])
+def test_saved_pair_matches_stateless_and_oracle(name, kw):
+    import torch
+    import oracle
+    import paper_2506_02475_amd as comba
+    from gpu_helpers import to_device
+
+    w = random_case(seed=zlib.crc32(name.encode()) % 1000 + 7, dht=True, **kw)
+    a = to_device(w)
+    args = (a["q"], a["k"], a["v"], a["g"], a["beta"], a["d"], a["h0"])
+    o_s, ht_s, ws = comba.comba_chunk_fwd_save(*args, cu_seqlens=a["cu_seqlens"])
+    gr_s = comba.comba_chunk_bwd_saved(*args, a["dO"], a["dht"], workspace=ws,
+                                       cu_seqlens=a["cu_seqlens"])
+    o, ht = comba.comba_chunk_fwd(*args, cu_seqlens=a["cu_seqlens"])
+    gr = comba.comba_chunk_bwd(*args, a["dO"], a["dht"], cu_seqlens=a["cu_seqlens"])
+    torch.cuda.synchronize()
+    # same kernels and arithmetic: bitwise equal to the stateless calls
+    assert torch.equal(o_s, o) and torch.equal(ht_s, ht)
+    for key in gr:
+        assert torch.equal(gr_s[key], gr[key]), key
+    ro, rht = oracle.workload_fwd(w)
+    ref = oracle.workload_bwd(w)
+    tol = 1e-5 if w.in_dtype == "f32" else 2e-3
+    assert maxrel(o_s.cpu().numpy(), ro) <= tol
+    for key in ("dq", "dk", "dv", "dg", "dbeta", "dd", "dh0"):
+        assert maxrel(gr_s[key].cpu().numpy(), ref[key]) <= tol, key
+
+
 # ----------------------------------------------------- the five workload shapes
 def test_workload_tiny_f32_fwd():
     w = generate(0)
