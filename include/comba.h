@@ -35,7 +35,11 @@
  *  - Calls are asynchronous on `stream` (a hipStream_t passed as void*; NULL is
  *    the default stream).  Argument errors are detected before any launch and
  *    then nothing is written.  A failed launch returns COMBA_ERR_HIP.
- *  - Outputs must not alias inputs; outputs are overwritten, never accumulated.
+ *  - Alignment: q, k, v, dO and every fp32 tensor whose last dimension is dk
+    or dv (h0, ht, o, dht, dh0, dq, dk, dv) need 16 bytes, the workspace 256
+    bytes, the other fp32 tensors 4 bytes and beta its element size; any other
+    pointer is rejected with COMBA_ERR_ALIGN.
+  - Outputs must not alias inputs; outputs are overwritten, never accumulated.
  *  - Calls on different streams with distinct workspaces may run concurrently;
  *    a workspace must not be shared by calls that overlap in time.
  */
@@ -54,7 +58,7 @@ typedef enum {
   COMBA_ERR_NULL = 1,      /* a required pointer is NULL                         */
   COMBA_ERR_SHAPE = 2,     /* unsupported or inconsistent sizes                  */
   COMBA_ERR_DTYPE = 3,     /* unknown dtype                                      */
-  COMBA_ERR_ALIGN = 4,     /* q/k/v/dO not 16-byte aligned, workspace not 256    */
+  COMBA_ERR_ALIGN = 4,     /* a pointer breaks the alignment rules above         */
   COMBA_ERR_WORKSPACE = 5, /* workspace smaller than the *_workspace_bytes value */
   COMBA_ERR_HIP = 6        /* a kernel launch failed                             */
 } comba_status;

@@ -181,8 +181,8 @@ comba_status chunk_fwd(bool save, const comba_shape* shape, const void* q, const
   if (st != COMBA_OK) return st;
   if (!q || !k || !v || !g || !beta || !d || !o || !ws) return COMBA_ERR_NULL;
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(ws, kAlign) ||
-      !aligned(g, 4) || !aligned(d, 4) || !aligned(o, 4) || (h0 && !aligned(h0, 4)) ||
-      (ht && !aligned(ht, 4)) || !aligned(beta, dm.bf16 ? 2 : 4))
+      !aligned(g, 4) || !aligned(d, 4) || !aligned(o, 16) || (h0 && !aligned(h0, 16)) ||
+      (ht && !aligned(ht, 16)) || !aligned(beta, dm.bf16 ? 2 : 4))
     return COMBA_ERR_ALIGN;
   const Layout L = layout(dm, save);
   if (ws_bytes < L.total) return COMBA_ERR_WORKSPACE;
@@ -217,10 +217,10 @@ comba_status chunk_bwd(bool saved, const comba_shape* shape, const void* q, cons
       !ws)
     return COMBA_ERR_NULL;
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(dO, 16) ||
-      !aligned(ws, kAlign) || !aligned(g, 4) || !aligned(d, 4) || !aligned(dq, 4) ||
-      !aligned(dk, 4) || !aligned(dv, 4) || !aligned(dg, 4) || !aligned(dbeta, 4) ||
-      !aligned(dd, 4) || (h0 && !aligned(h0, 4)) || (dht && !aligned(dht, 4)) ||
-      (dh0 && !aligned(dh0, 4)) || !aligned(beta, dm.bf16 ? 2 : 4))
+      !aligned(ws, kAlign) || !aligned(g, 4) || !aligned(d, 4) || !aligned(dq, 16) ||
+      !aligned(dk, 16) || !aligned(dv, 16) || !aligned(dg, 4) || !aligned(dbeta, 4) ||
+      !aligned(dd, 4) || (h0 && !aligned(h0, 16)) || (dht && !aligned(dht, 16)) ||
+      (dh0 && !aligned(dh0, 16)) || !aligned(beta, dm.bf16 ? 2 : 4))
     return COMBA_ERR_ALIGN;
   const Layout L = layout(dm, true);
   if (ws_bytes < L.total) return COMBA_ERR_WORKSPACE;
@@ -324,7 +324,7 @@ const char* comba_status_string(comba_status s) {
     case COMBA_ERR_NULL: return "a required pointer is NULL";
     case COMBA_ERR_SHAPE: return "unsupported or inconsistent shape";
     case COMBA_ERR_DTYPE: return "unknown dtype";
-    case COMBA_ERR_ALIGN: return "misaligned pointer (q/k/v/dO need 16 B, workspace 256 B)";
+    case COMBA_ERR_ALIGN: return "misaligned pointer (q/k/v/dO and the [.., dk|dv] fp32 tensors need 16 B, workspace 256 B)";
     case COMBA_ERR_WORKSPACE: return "workspace too small";
     case COMBA_ERR_HIP: return "HIP kernel launch failed";
   }

@@ -143,6 +143,49 @@ __device__ __forceinline__ void mma(floatx4 (&acc)[MT][NT], const TA* __restrict
 __device__ __forceinline__ int acc_row(int mt, int e) { return 16 * mt + 4 * (lane_id() >> 4) + e; }
 __device__ __forceinline__ int acc_col(int nt) { return 16 * nt + (lane_id() & 15); }
 
+// ---- accumulator row stores --------------------------------------------------
+// An accumulator tile gives lane l the rows 4 (l / 16) + e (e = 0..3) of
+// column l % 16, so a plain store writes 4 bytes per lane.  quad_transpose
+// exchanges values inside each group of four lanes (DPP quad permutations, no
+// LDS) so that lane l instead holds row 4 (l / 16) + (l % 4), columns
+// (l & 12) + e: four consecutive columns of one row, written with one 16-byte
+// store.  Two butterfly rounds: exchange with lane ^ 1, then with lane ^ 2.
+template <int CTRL>
+__device__ __forceinline__ float dpp_quad(float x) {
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), CTRL, 0xF, 0xF, true));
+}
+__device__ __forceinline__ floatx4 quad_transpose(floatx4 a) {
+  constexpr int XOR1 = 0xB1;  // quad_perm [1, 0, 3, 2]
+  constexpr int XOR2 = 0x4E;  // quad_perm [2, 3, 0, 1]
+  const int i = lane_id() & 3;
+  const bool odd = i & 1, hi = i & 2;
+  {
+    const float r0 = dpp_quad<XOR1>(odd ? a[0] : a[1]);
+    const float r1 = dpp_quad<XOR1>(odd ? a[2] : a[3]);
+    a[0] = odd ? r0 : a[0];
+    a[1] = odd ? a[1] : r0;
+    a[2] = odd ? r1 : a[2];
+    a[3] = odd ? a[3] : r1;
+  }
+  {
+    const float r0 = dpp_quad<XOR2>(hi ? a[0] : a[2]);
+    const float r1 = dpp_quad<XOR2>(hi ? a[1] : a[3]);
+    a[0] = hi ? r0 : a[0];
+    a[2] = hi ? a[2] : r0;
+    a[1] = hi ? r1 : a[1];
+    a[3] = hi ? a[3] : r1;
+  }
+  return a;
+}
+// Row and first column (relative to the tile origin) of the four values a lane
+// holds after quad_transpose.
+__device__ __forceinline__ int qt_row() { return 4 * (lane_id() >> 4) + (lane_id() & 3); }
+__device__ __forceinline__ int qt_col() { return lane_id() & 12; }
+__device__ __forceinline__ void store4(float* p, const floatx4& x) {
+  *reinterpret_cast<float4*>(p) = make_float4(x[0], x[1], x[2], x[3]);
+}
+
 // Sum over the 16 lanes that hold one accumulator row (same lane / 16 group).
 __device__ __forceinline__ float sum16(float x) {
   x += __shfl_xor(x, 1);

@@ -1076,14 +1076,14 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
         put_t4(XTh, XTl, (16 * nt + r16) * LDX + xrow0 + 16 * mt, xv);
       }
   };
+  // state rows leave as 16-byte row pieces (see quad_transpose)
+  const int xrow_q = (DK / 4) * w + qt_row(), xcol_q = j0 + qt_col();
   auto store_state = [&](float* dst) {
 #pragma unroll
     for (int mt = 0; mt < XMT; ++mt)
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt)
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          dst[(long)(xrow0 + 16 * mt + e) * DV + j0 + 16 * nt + r16] = X[mt][nt][e];
+        store4(dst + (long)(xrow_q + 16 * mt) * DV + xcol_q + 16 * nt, quad_transpose(X[mt][nt]));
   };
   put_state();
 
@@ -1241,9 +1241,10 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
       for (int e = 0; e < 4; ++e) {
         dv[e] = dl[nt][e];
         dgv[e] = __expf(glast - gg[e]) * dv[e];
-        if constexpr (STORE)
-          Dw[chh * CH * DV + (long)(16 * w + 4 * g4 + e) * DV + j0 + 16 * nt + r16] = dv[e];
       }
+      if constexpr (STORE)
+        store4(Dw + chh * CH * DV + (long)(16 * w + qt_row()) * DV + xcol_q + 16 * nt,
+               quad_transpose(dl[nt]));
       const int off = (16 * nt + r16) * LDR + 16 * w + 4 * g4;
       put_t4(DgTh, DgTl, off, dgv);
       if constexpr (OUT) put_t4(DTh, DTl, off, dv);
@@ -1283,15 +1284,13 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
           oacc[nt] = mfma16(al[ks], dh_, oacc[nt]);
         }
       load_a(nx);
+      const int orow = 16 * w + qt_row();
 #pragma unroll
-      for (int nt = 0; nt < NTV; ++nt)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = 16 * w + 4 * g4 + e;
-          float* dst = r < len ? o + (tok + (long)r * H) * DV + j0 + 16 * nt + r16
-                               : sink + (threadIdx.x & 255);
-          *dst = oacc[nt][e];
-        }
+      for (int nt = 0; nt < NTV; ++nt) {
+        float* dst = orow < len ? o + (tok + (long)orow * H) * DV + xcol_q + 16 * nt
+                                : sink + 4 * lane;
+        store4(dst, quad_transpose(oacc[nt]));
+      }
     }
     put_state();
     // state entering the next chunk (after the last chunk: the final state)
@@ -1350,14 +1349,14 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
         put_t4(YTh, YTl, (16 * nt + r16) * LDX + yrow0 + 16 * mt, yv);
       }
   };
+  // state rows leave as 16-byte row pieces (see quad_transpose)
+  const int yrow_q = (DK / 4) * w + qt_row(), ycol_q = j0 + qt_col();
   auto store_state = [&](float* dst) {
 #pragma unroll
     for (int mt = 0; mt < XMT; ++mt)
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt)
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          dst[(long)(yrow0 + 16 * mt + e) * DV + j0 + 16 * nt + r16] = Y[mt][nt][e];
+        store4(dst + (long)(yrow_q + 16 * mt) * DV + ycol_q + 16 * nt, quad_transpose(Y[mt][nt]));
   };
   put_state();
 
@@ -1526,10 +1525,11 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
       const int off = (16 * nt + r16) * LDR + 16 * w + 4 * g4;
       const bf16x4 dov = *reinterpret_cast<const bf16x4*>(dOT[buf] + off);
       float pg[4], w2[4];
+      store4(dRw + chh * CH * DV + (long)(16 * w + qt_row()) * DV + ycol_q + 16 * nt,
+             quad_transpose(drr[nt]));
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const float drv = drr[nt][e];
-        dRw[chh * CH * DV + (long)(16 * w + 4 * g4 + e) * DV + j0 + 16 * nt + r16] = drv;
         pg[e] = __expf(gg[e]) * (float)dov[e];
         w2[e] = -dh * pg[e] - bb[e] * __expf(gm[e]) * drv;
       }
@@ -1888,18 +1888,22 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     }
   }
   float ddpart = 0.f;
+  const int qrow = 16 * rt + qt_row();
+  const bool qok = qrow < len;
 #pragma unroll
-  for (int j = 0; j < NTW; ++j)
+  for (int j = 0; j < NTW; ++j) {
+    floatx4 dkv;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int r = 16 * rt + 4 * g4 + e, c = 16 * (ch * NTW + j) + r16;
       const float dqt = T1[j][e];
       ddpart += bf2f(Ks[r * LDK + c]) * dqt;
-      const bool ok = r < len;
-      const long off = (tok + (long)r * H) * DK + c;
-      *(ok ? dq + off : sink + lane) = dqt;
-      *(ok ? dk + off : sink + 64 + lane) = T2[j][e] - dh * dqt;
+      dkv[e] = T2[j][e] - dh * dqt;
     }
+    const long off = (tok + (long)qrow * H) * DK + 16 * (ch * NTW + j) + qt_col();
+    store4(qok ? dq + off : sink + 4 * lane, quad_transpose(T1[j]));
+    store4(qok ? dk + off : sink + 4 * lane, quad_transpose(dkv));
+  }
   ddpart = wave_sum(ddpart);
   if (lane == 0) scal[w][1] = ddpart;
   __syncthreads();

@@ -111,6 +111,17 @@ def test_rejects_null_and_misaligned_pointers():
     assert fwd(s, ws=FAKE + 16) == EALIGN
     assert fwd(s, o=FAKE + 2) == EALIGN
     assert bwd(s, dO=FAKE + 4) == EALIGN
+    # fp32 tensors with a dk / dv last dimension are written 16 bytes at a time
+    for name in ("o", "h0", "ht"):
+        assert fwd(s, **{name: FAKE + 4}) == EALIGN, name
+    for name in ("dq", "dk", "dv", "h0", "dht", "dh0"):
+        assert bwd(s, **{name: FAKE + 8}) == EALIGN, name
+    # per-token / per-head fp32 tensors need only 4 bytes: with a too-small
+    # workspace the next check fails instead (and nothing is launched)
+    for name in ("g", "d"):
+        assert fwd(s, ws_bytes=1, **{name: FAKE + 4}) == EWS, name
+    for name in ("dg", "dbeta", "dd"):
+        assert bwd(s, ws_bytes=1, **{name: FAKE + 4}) == EWS, name
     lib = comba.load_library()
     assert lib.comba_chunk_fwd(None, *[ctypes.c_void_p(FAKE)] * 9, ctypes.c_void_p(FAKE),
                                ctypes.c_size_t(1 << 40), None) == ENULL
