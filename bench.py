@@ -71,7 +71,7 @@ def stage_model(name, B, T, H, dk, dv, C=64, in_bytes=2):
         by = 3 * qk + vv + 2 * cc + gb + st + cd
     elif name == "intra_bwd":     # 3 C x dk x dv, 2 C x C x dv, 5 C x C x dk products
         fl = 6 * C * dk * dv + 4 * C * C * dv + 10 * C * C * dk
-        by = (4 * qk + 2 * vv + 2 * st + 2 * cd + gb          # q,k,K^T,Q^T,v,dO,X,Y,D,dR
+        by = (2 * qk + 2 * vv + 2 * st + 2 * cd + gb          # q,k,v,dO,X,Y,D,dR
               + C * (2 * dk + dv) * f4 + 2 * C * f4)           # dq, dk, dv, dg, dbeta
     else:
         return 0.0, 0.0

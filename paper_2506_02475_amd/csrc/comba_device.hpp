@@ -186,6 +186,28 @@ __device__ __forceinline__ void store4(float* p, const floatx4& x) {
   *reinterpret_cast<float4*>(p) = make_float4(x[0], x[1], x[2], x[3]);
 }
 
+// ---- transposed operand fragments from LDS --------------------------------
+// ds_read_b64_tr_b16 (gfx950): inside each 16-lane group the 16 lanes' 8-byte
+// reads form S[s][p] (lane s, element p), and lane i receives S[4e + i/4][i%4]
+// for e = 0..3.  So when lane s of the group addresses row r0 + s/4, columns
+// c0 + 4 (s%4) .. +3 of a row-major bf16 tile, lane i receives the column
+// c0 + i at rows r0 .. r0 + 3: an MFMA operand fragment whose reduction index
+// runs down the tile's rows.  (Layout established by an in-bounds probe.)
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ bf16x4_t ld_tr4(const bf16_t* tile, int ld, int r0, int c0) {
+  const int s = lane_id() & 15;
+  const bf16_t* p = tile + (r0 + (s >> 2)) * ld + c0 + 4 * (s & 3);
+  const i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) i16x4*)(p));
+  return __builtin_bit_cast(bf16x4_t, v);
+}
+// Eight consecutive rows r0 .. r0 + 7 of column c0 + (lane % 16).
+__device__ __forceinline__ bf16x8 ld_tr8(const bf16_t* tile, int ld, int r0, int c0) {
+  const bf16x4_t a = ld_tr4(tile, ld, r0, c0), b = ld_tr4(tile, ld, r0 + 4, c0);
+  return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
 // Sum over the 16 lanes that hold one accumulator row (same lane / 16 group).
 __device__ __forceinline__ float sum16(float x) {
   x += __shfl_xor(x, 1);

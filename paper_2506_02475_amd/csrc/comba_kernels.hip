@@ -1604,8 +1604,7 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     const bf16_t* __restrict__ dO, const bf16_t* __restrict__ beta, const float* __restrict__ d,
     const ChunkInfo* __restrict__ cmap, int H, const float* __restrict__ Gw,
     const float* __restrict__ Xw, const float* __restrict__ Dw, const float* __restrict__ Yw,
-    const float* __restrict__ dRw, const bf16_t* __restrict__ KTp,
-    const bf16_t* __restrict__ QTp, float* __restrict__ dq, float* __restrict__ dk,
+    const float* __restrict__ dRw, int touch_ahead, float* __restrict__ dq, float* __restrict__ dk,
     float* __restrict__ dv, float* __restrict__ dbeta, float* __restrict__ dg,
     float* __restrict__ ddp, float* __restrict__ sink) {
   using SM = IntraBwdBfSmem<DK>;
@@ -1766,16 +1765,36 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
   bf16_t* Sl = Sh + CH * LDC;
   kr.store(Ks, LDK);
   qr.store(Qs, LDK);
-  // B operands K^T, Q^T of this wave's dk columns: B(k = t, n = c) = K[t][c]
-  bf16x8 ktb[NTW][2], qtb[NTW][2];
-#pragma unroll
-  for (int j = 0; j < NTW; ++j)
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      const long off = chh * DK * CH + (long)(16 * (ch * NTW + j) + r16) * CH + 32 * ks + 8 * g4;
-      ktb[j][ks] = ld8(KTp + off);
-      qtb[j][ks] = ld8(QTp + off);
+  // Phase 2 reads nothing else from memory: warm L2 with the first phase-1
+  // block of the workgroup that runs touch_ahead workgroups later (dispatch is
+  // in linear order, round-robin over the XCDs, so with touch_ahead a multiple
+  // of their count it shares this L2).  One 4-byte load per 128-byte line, one
+  // line per thread; the value is consumed only at the very end, so no wait
+  // for it falls inside this workgroup's work.
+  uint32_t touched = 0;
+  {
+    const int lin2 = blockIdx.x + blockIdx.y * gridDim.x + touch_ahead;
+    const int c2 = lin2 % gridDim.x, h2 = lin2 / gridDim.x;
+    if (touch_ahead > 0 && h2 < (int)gridDim.y) {
+      const ChunkInfo ci2 = cmap[c2];
+      if (ci2.len > 0) {
+        const long chh2 = (long)c2 * H + h2, tok2 = (long)ci2.tok0 * H + h2;
+        // lines: X rows (DK), Y rows (DK), dR, D, dO, v rows (64 each); the
+        // first 32 columns of each row are the block
+        static_assert(2 * DK + 4 * CH <= IB_THR, "one line per thread");
+        int t = tid;
+        const int rr = min(t & (CH - 1), ci2.len - 1);
+        const char* a = reinterpret_cast<const char*>(Xw + chh2 * DK * DV);
+        if (t < DK) a = reinterpret_cast<const char*>(Xw + chh2 * DK * DV + (long)t * DV);
+        else if ((t -= DK) < DK) a = reinterpret_cast<const char*>(Yw + chh2 * DK * DV + (long)t * DV);
+        else if ((t -= DK) < CH) a = reinterpret_cast<const char*>(dRw + (chh2 * CH + t) * DV);
+        else if ((t -= CH) < CH) a = reinterpret_cast<const char*>(Dw + (chh2 * CH + t) * DV);
+        else if ((t -= CH) < CH) a = reinterpret_cast<const char*>(dO + (tok2 + (long)rr * H) * DV);
+        else if ((t -= CH) < CH) a = reinterpret_cast<const char*>(v + (tok2 + (long)rr * H) * DV);
+        touched = *reinterpret_cast<const uint32_t*>(a);
+      }
     }
+  }
   __syncthreads();
   const float Glast = Gs[CH - 1];
   {
@@ -1879,12 +1898,16 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     const bf16x8 ash = ld8(Sh + ar), asl = ld8(Sl + ar);
 #pragma unroll
     for (int j = 0; j < NTW; ++j) {
-      T1[j] = mfma16(agh, ktb[j][ks], T1[j]);
-      T1[j] = mfma16(agl, ktb[j][ks], T1[j]);
-      T2[j] = mfma16(ath, qtb[j][ks], T2[j]);
-      T2[j] = mfma16(atl, qtb[j][ks], T2[j]);
-      T2[j] = mfma16(ash, ktb[j][ks], T2[j]);
-      T2[j] = mfma16(asl, ktb[j][ks], T2[j]);
+      // B operands K^T, Q^T of this wave's dk columns, B(k = t, n = c) = K[t][c],
+      // read transposed from the row-major LDS tiles
+      const bf16x8 ktb = ld_tr8(Ks, LDK, 32 * ks + 8 * g4, 16 * (ch * NTW + j));
+      const bf16x8 qtb = ld_tr8(Qs, LDK, 32 * ks + 8 * g4, 16 * (ch * NTW + j));
+      T1[j] = mfma16(agh, ktb, T1[j]);
+      T1[j] = mfma16(agl, ktb, T1[j]);
+      T2[j] = mfma16(ath, qtb, T2[j]);
+      T2[j] = mfma16(atl, qtb, T2[j]);
+      T2[j] = mfma16(ash, ktb, T2[j]);
+      T2[j] = mfma16(asl, ktb, T2[j]);
     }
   }
   float ddpart = 0.f;
@@ -1941,11 +1964,22 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     }
     if (lane == 0) ddp[chh] = -dds;
   }
+  // keeps the warm-up load alive; a matching value only writes the sink
+  if (touched == 0x7fbfffffu) sink[tid & 255] = 0.f;
 }
 
 // ---------------------------------------------------------------------------
 // host launchers
 // ---------------------------------------------------------------------------
+// Compute units of the current device (0 when the query fails).
+static int device_cus() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return 0;
+  return cus > 0 ? cus : 0;
+}
+
 template <typename Tin, int DK, int DV>
 static hipError_t run_fwd(const LaunchArgs& a) {
   hipStream_t st = a.stream;
@@ -2072,7 +2106,7 @@ static hipError_t run_bwd_bf(const LaunchArgs& a) {
   a.stage("intra_bwd");
   if (a.ncmax > 0)
     k_intra_bwd_bf<DK, DV><<<dim3(a.ncmax, a.H), IB_THR, 0, st>>>(
-        q, k, v, dO, beta, a.d, a.cmap, a.H, a.Gw, a.Xw, a.Dw, a.Yw, a.dRw, a.KTp, a.QTp, a.dq,
+        q, k, v, dO, beta, a.d, a.cmap, a.H, a.Gw, a.Xw, a.Dw, a.Yw, a.dRw, device_cus(), a.dq,
         a.dk_, a.dv_, a.dbeta, a.dg, a.ddp, a.sink);
   a.stage("reduce_dd");
   k_reduce_dd<<<a.H, NTHR, 0, st>>>(a.ddp, a.ncmax, a.H, a.dd);
