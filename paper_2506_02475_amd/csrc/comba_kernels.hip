@@ -950,10 +950,17 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
       if (r >= c) a = (aqk[0][nt][e] - dh * kk) * __expf(Gs[r] - Gs[c]);
       if (r > c) l = Bs[r] * __expf(Gs[r - 1] - Gs[c]) * kk;
       av[e] = a;
-      const __bf16 ah = (__bf16)a;
-      Ao[r * CH + c] = __builtin_bit_cast(bf16_t, ah);
-      Ao[CC + r * CH + c] = __builtin_bit_cast(bf16_t, (__bf16)(a - (float)ah));
       Ls[r * LDL + c] = l;
+    }
+    // A rows (hi, lo) leave as 8-byte pieces of four columns (see quad_transpose)
+    {
+      const floatx4 aq = quad_transpose(floatx4{av[0], av[1], av[2], av[3]});
+      const float aa[4] = {aq[0], aq[1], aq[2], aq[3]};
+      bf16x4 hh, ll;
+      split4(aa, hh, ll);
+      const int off = (16 * w + qt_row()) * CH + 16 * nt + qt_col();
+      *reinterpret_cast<bf16x4*>(Ao + off) = hh;
+      *reinterpret_cast<bf16x4*>(Ao + CC + off) = ll;
     }
     if constexpr (BWD) {
       // A^T: this lane's column c, rows 16w + 4g .. +3
@@ -985,13 +992,10 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
       const float sum = (s0 + s1) + (s2 + s3);
       if (i > j) x[i] = -sum;
     }
-    bf16_t* Mo = Mp + chh * 2 * CC;
+    // column j of M into LDS (wave 0 is the only reader of L and is done with
+    // it); the rows are written out below by the whole workgroup
 #pragma unroll
-    for (int i = 0; i < CH; ++i) {
-      const __bf16 hh = (__bf16)x[i];
-      Mo[i * CH + j] = __builtin_bit_cast(bf16_t, hh);
-      Mo[CC + i * CH + j] = __builtin_bit_cast(bf16_t, (__bf16)(x[i] - (float)hh));
-    }
+    for (int i = 0; i < CH; ++i) Ls[i * LDL + j] = x[i];
     if constexpr (BWD) {
       bf16_t* Mt = MTp + chh * 2 * CC + j * CH;
 #pragma unroll
@@ -1008,20 +1012,35 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
       }
     }
   } else {
-    // waves 1..3: K^T (and Q^T) per chunk-head, [dk][64] bf16
+    // waves 1..3: K^T (and Q^T) per chunk-head, [dk][64] bf16.  One transposing
+    // LDS read pair gives lane (g, i) the 8 rows 32 tb + 8 g .. of column c0 + i,
+    // i.e. one 16-byte piece of row c0 + i of K^T.
     bf16_t* Kt = KTp + chh * DK * CH;
     bf16_t* Qt = BWD ? QTp + chh * DK * CH : nullptr;
-    for (int idx = threadIdx.x - 64; idx < DK * (CH / 8); idx += NTHR - 64) {
-      const int i = idx / (CH / 8), t0 = (idx % (CH / 8)) * 8;
-      bf16x8 kv, qv;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        kv[e] = __builtin_bit_cast(__bf16, Ks[(t0 + e) * LDK + i]);
-        if constexpr (BWD) qv[e] = __builtin_bit_cast(__bf16, Qs[(t0 + e) * LDK + i]);
-      }
-      *reinterpret_cast<bf16x8*>(Kt + i * CH + t0) = kv;
-      if constexpr (BWD) *reinterpret_cast<bf16x8*>(Qt + i * CH + t0) = qv;
+    for (int ci = w - 1; ci < 2 * (DK / 16); ci += NWAVE - 1) {
+      const int c0 = 16 * (ci % (DK / 16)), r0 = 32 * (ci / (DK / 16)) + 8 * g4;
+      const long off = (long)(c0 + (lane & 15)) * CH + r0;
+      *reinterpret_cast<bf16x8*>(Kt + off) = ld_tr8(Ks, LDK, r0, c0);
+      if constexpr (BWD) *reinterpret_cast<bf16x8*>(Qt + off) = ld_tr8(Qs, LDK, r0, c0);
     }
+  }
+  __syncthreads();
+  // M rows (hi, lo) from LDS, 16-byte pieces of eight columns
+  bf16_t* Mo = Mp + chh * 2 * CC;
+  for (int idx = threadIdx.x; idx < CC / 8; idx += NTHR) {
+    const int r = idx / (CH / 8), c8 = (idx % (CH / 8)) * 8;
+    const float4 m0 = *reinterpret_cast<const float4*>(Ls + r * LDL + c8);
+    const float4 m1 = *reinterpret_cast<const float4*>(Ls + r * LDL + c8 + 4);
+    const float mv[8] = {m0.x, m0.y, m0.z, m0.w, m1.x, m1.y, m1.z, m1.w};
+    bf16x8 hv, lv;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const __bf16 hh = (__bf16)mv[e];
+      hv[e] = hh;
+      lv[e] = (__bf16)(mv[e] - (float)hh);
+    }
+    *reinterpret_cast<bf16x8*>(Mo + r * CH + c8) = hv;
+    *reinterpret_cast<bf16x8*>(Mo + CC + r * CH + c8) = lv;
   }
 }
 
