@@ -133,6 +133,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--skip-stateless", action="store_true",
+                    help="time only the training pair (profiling runs: one stage per kernel)")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="after the timed steps, run one plain device-to-device copy of this "
                          "many bytes (calibrates HBM traffic counters against a known size)")
@@ -177,14 +179,16 @@ def main():
         gr = comba.comba_chunk_bwd(q, k, v, g, beta, d, h0, dO, None, workspace=ws_b)
         return o, gr
 
-    for _ in range(args.warmup):
-        step_stateless()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step_stateless()
-    torch.cuda.synchronize()
-    ms_stateless = (time.perf_counter() - t0) * 1e3 / args.steps
+    ms_stateless = None
+    if not args.skip_stateless:
+        for _ in range(args.warmup):
+            step_stateless()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            step_stateless()
+        torch.cuda.synchronize()
+        ms_stateless = round((time.perf_counter() - t0) * 1e3 / args.steps, 4)
 
     for _ in range(args.warmup):
         step()
@@ -250,7 +254,7 @@ def main():
         "config": {"workload": spec.name, "B": B, "T": T, "H": H, "dk": dk, "dv": dv,
                    "chunk": 64, "in_dtype": "bf16", "out_dtype": "f32"},
         "step": "comba_chunk_fwd_save + comba_chunk_bwd_saved",
-        "ms_per_step_stateless": round(ms_stateless, 4),
+        "ms_per_step_stateless": ms_stateless,
         "mfma_pct_peak_op": round(100.0 * mfma_frac_op, 3),
         "op_algorithmic_tflops": round(op_fl / (ms_per_step * 1e-3) / 1e12, 2),
         "stages_ms": {n: round(x, 4) for n, x in tot.items()},
