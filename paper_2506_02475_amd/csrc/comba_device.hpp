@@ -208,12 +208,31 @@ __device__ __forceinline__ bf16x8 ld_tr8(const bf16_t* tile, int ld, int r0, int
   return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
 }
 
-// Sum over the 16 lanes that hold one accumulator row (same lane / 16 group).
+// ---- cross-lane reductions and scans (DPP: VALU only, no LDS round trip) ----
+// DPP controls used (gfx9 encodings; a "row" is 16 lanes): quad_perm xor 1 /
+// xor 2, row_half_mirror (lane i of an 8-lane half reads lane 7 - i), row_mirror
+// (lane i reads 15 - i), row_shr:n (lane i reads i - n inside its row, old value
+// at the row start), row_bcast15 / row_bcast31 (last lane of a row, resp. of
+// the lower half, to the following rows selected by the row mask), wave_shl:1
+// (lane i reads lane i + 1).  Directions were checked with an in-bounds probe.
+template <int CTRL, int ROWMASK = 0xF>
+__device__ __forceinline__ float dpp_upd(float old, float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, old),
+                                                               __builtin_bit_cast(int, x), CTRL,
+                                                               ROWMASK, 0xF, false));
+}
+// Sum over each group of 8 lanes (every lane of the group gets the same value).
+__device__ __forceinline__ float sum8(float x) {
+  x += dpp_upd<0xB1>(0.f, x);   // quad_perm [1,0,3,2]
+  x += dpp_upd<0x4E>(0.f, x);   // quad_perm [2,3,0,1]
+  x += dpp_upd<0x141>(0.f, x);  // row_half_mirror
+  return x;
+}
+// Sum over the 16 lanes that hold one accumulator row (same lane / 16 group);
+// a symmetric butterfly, so every lane of the row gets the same value.
 __device__ __forceinline__ float sum16(float x) {
-  x += __shfl_xor(x, 1);
-  x += __shfl_xor(x, 2);
-  x += __shfl_xor(x, 4);
-  x += __shfl_xor(x, 8);
+  x = sum8(x);
+  x += dpp_upd<0x140>(0.f, x);  // row_mirror
   return x;
 }
 // Sum over the 4 lane groups (lanes l, l^16, l^32, l^48).
@@ -222,9 +241,17 @@ __device__ __forceinline__ float sum_groups(float x) {
   x += __shfl_xor(x, 32);
   return x;
 }
-__device__ __forceinline__ float wave_sum(float x) {
-  return sum_groups(sum16(x));
+// Value of `lane` (the readlane builtin moves 32-bit integers).
+__device__ __forceinline__ float read_lane(float x, int lane) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), lane));
 }
+// Sum over the wavefront, uniform result.
+__device__ __forceinline__ float wave_sum(float x) {
+  x = sum16(x);
+  return (read_lane(x, 0) + read_lane(x, 16)) + (read_lane(x, 32) + read_lane(x, 48));
+}
+// Value of lane + 1 (0 for the last lane).
+__device__ __forceinline__ float shift_down1(float x) { return dpp_upd<0x130>(0.f, x); }
 
 // ---- global -> register -> LDS tile copies ---------------------------------
 
@@ -287,14 +314,15 @@ __device__ __forceinline__ void tile_to_lds(const T* __restrict__ g, long gs, in
   t.store(s, ld);
 }
 
-// Inclusive prefix sum across the 64 lanes of a wavefront.
+// Inclusive prefix sum across the 64 lanes of a wavefront: within each row by
+// shifts of 1, 2, 4, 8, then the row totals carried upward by row broadcasts.
 __device__ __forceinline__ float wave_prefix_sum(float x) {
-  const int lane = lane_id();
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const float y = __shfl_up(x, off);
-    if (lane >= off) x += y;
-  }
+  x += dpp_upd<0x111>(0.f, x);       // row_shr:1
+  x += dpp_upd<0x112>(0.f, x);       // row_shr:2
+  x += dpp_upd<0x114>(0.f, x);       // row_shr:4
+  x += dpp_upd<0x118>(0.f, x);       // row_shr:8
+  x += dpp_upd<0x142, 0xA>(0.f, x);  // row_bcast15 into rows 1, 3
+  x += dpp_upd<0x143, 0xC>(0.f, x);  // row_bcast31 into rows 2, 3
   return x;
 }
 

@@ -1611,11 +1611,6 @@ __device__ __forceinline__ void split4v(const float4& x, bf16x4& hi, bf16x4& lo)
   const float a[4] = {x.x, x.y, x.z, x.w};
   split4(a, hi, lo);
 }
-__device__ __forceinline__ void put_split(bf16_t* hi, bf16_t* lo, float x) {
-  const __bf16 h = (__bf16)x;
-  *hi = __builtin_bit_cast(bf16_t, h);
-  *lo = __builtin_bit_cast(bf16_t, (__bf16)(x - (float)h));
-}
 
 template <int DK, int DV>
 __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
@@ -1765,9 +1760,7 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
       dL[j2] = mfma16(a_drl, bh, dL[j2]);
     }
   }
-  bv += __shfl_xor(bv, 1);
-  bv += __shfl_xor(bv, 2);
-  bv += __shfl_xor(bv, 4);
+  bv = sum8(bv);
   if ((tid & 7) == 0) rowB[pf_r] = bv;
   Fpart = wave_sum(Fpart);
   if (lane == 0) scal[w][0] = Fpart;
@@ -1776,12 +1769,18 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
   // ---------------- phase 2 ----------------
   bf16_t* Ks = reinterpret_cast<bf16_t*>(smem);
   bf16_t* Qs = Ks + CH * LDK;
-  bf16_t* Gh = Qs + CH * LDK;   // dA o Gamma (hi, lo), row-major
-  bf16_t* Gl = Gh + CH * LDC;
-  bf16_t* GTh = Gl + CH * LDC;  // its transpose
+  // The 64 x 64 gate-term matrices, each (hi, lo), stored in the orientation in
+  // which a lane's four accumulator values (rows r .. r+3 of one column c) are
+  // contiguous, i.e. at [c][r]; the row-major operands are read back with
+  // transposing LDS reads.  With G = dA o Gamma (lower incl. diagonal),
+  // P = dAkk (strictly lower) and U = P^T - d G^T (upper incl. diagonal):
+  //   GT[c][r] = G[r][c],  PT[c][r] = P[r][c],  Ub[c][r] = U[c][r].
+  bf16_t* GTh = Qs + CH * LDK;
   bf16_t* GTl = GTh + CH * LDC;
-  bf16_t* Sh = GTl + CH * LDC;  // dAkk + dAkk^T - d (dA o Gamma)^T
-  bf16_t* Sl = Sh + CH * LDC;
+  bf16_t* PTh = GTl + CH * LDC;
+  bf16_t* PTl = PTh + CH * LDC;
+  bf16_t* Ubh = PTl + CH * LDC;
+  bf16_t* Ubl = Ubh + CH * LDC;
   kr.store(Ks, LDK);
   qr.store(Qs, LDK);
   // Phase 2 reads nothing else from memory: warm L2 with the first phase-1
@@ -1834,7 +1833,7 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
 #pragma unroll
     for (int j2 = 0; j2 < 2; ++j2) {
       const int c = 16 * (2 * ch + j2) + r16;
-      float cE = 0.f, dagv[4];
+      float cE = 0.f, dagv[4], pv[4], uv[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int r = 16 * rt + 4 * g4 + e;
@@ -1854,16 +1853,18 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
           e2 = dl * Bs[r] * lck;
           rBL[e] += dl * lck;
           dakk = dl * Bs[r] * lc;
-          put_split(Sh + r * LDC + c, Sl + r * LDC + c, dakk);
         }
-        if (r >= c) put_split(Sh + c * LDC + r, Sl + c * LDC + r, dakk - dh * dag);
-        put_split(Gh + r * LDC + c, Gl + r * LDC + c, dag);
         dagv[e] = dag;
+        pv[e] = dakk;
+        uv[e] = dakk - dh * dag;  // zero above the diagonal like the others
         rE1[e] += e1;
         rE2[e] += e2;
         cE += e1 + e2;
       }
-      put_t4(GTh, GTl, c * LDC + 16 * rt + 4 * g4, dagv);
+      const int toff = c * LDC + 16 * rt + 4 * g4;
+      put_t4(GTh, GTl, toff, dagv);
+      put_t4(PTh, PTl, toff, pv);
+      put_t4(Ubh, Ubl, toff, uv);
       cE = sum_groups(cE);
       if (g4 == 0) colpart[rt][c] = cE;
     }
@@ -1911,10 +1912,15 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
   }
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks) {
+    // A operands of this wave's rows x = 16 rt + r16: G and P rows via
+    // transposing reads of GT, PT; G^T and U rows directly
     const int ar = (16 * rt + r16) * LDC + 32 * ks + 8 * g4;
-    const bf16x8 agh = ld8(Gh + ar), agl = ld8(Gl + ar);
+    const bf16x8 agh = ld_tr8(GTh, LDC, 32 * ks + 8 * g4, 16 * rt);
+    const bf16x8 agl = ld_tr8(GTl, LDC, 32 * ks + 8 * g4, 16 * rt);
+    const bf16x8 aph = ld_tr8(PTh, LDC, 32 * ks + 8 * g4, 16 * rt);
+    const bf16x8 apl = ld_tr8(PTl, LDC, 32 * ks + 8 * g4, 16 * rt);
     const bf16x8 ath = ld8(GTh + ar), atl = ld8(GTl + ar);
-    const bf16x8 ash = ld8(Sh + ar), asl = ld8(Sl + ar);
+    const bf16x8 auh = ld8(Ubh + ar), aul = ld8(Ubl + ar);
 #pragma unroll
     for (int j = 0; j < NTW; ++j) {
       // B operands K^T, Q^T of this wave's dk columns, B(k = t, n = c) = K[t][c],
@@ -1925,8 +1931,10 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
       T1[j] = mfma16(agl, ktb, T1[j]);
       T2[j] = mfma16(ath, qtb, T2[j]);
       T2[j] = mfma16(atl, qtb, T2[j]);
-      T2[j] = mfma16(ash, ktb, T2[j]);
-      T2[j] = mfma16(asl, ktb, T2[j]);
+      T2[j] = mfma16(aph, ktb, T2[j]);
+      T2[j] = mfma16(apl, ktb, T2[j]);
+      T2[j] = mfma16(auh, ktb, T2[j]);
+      T2[j] = mfma16(aul, ktb, T2[j]);
     }
   }
   float ddpart = 0.f;
@@ -1971,7 +1979,7 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     const float rowgm = e2 - Bs[r] * egm * p3;
     const float rowb = rowB[r] + bl - egm * p3;
     const float gcs = wave_sum(cr);
-    const float rowgm_next = __shfl_down(rowgm, 1);
+    const float rowgm_next = shift_down1(rowgm);
     float dG = rowg - col + (r + 1 < CH ? rowgm_next : 0.f);
     if (r == CH - 1) dG += gcs + __expf(Glast) * F;
     float x = __shfl(dG, 63 - lane);
