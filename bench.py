@@ -40,10 +40,12 @@ def stage_model(name, B, T, H, dk, dv, C=64, in_bytes=2):
 
     Per chunk-head (C tokens of one head): the dense products the stage performs
     (2 m n k flops each) and the HBM bytes it must move at minimum (each operand
-    read once, each result written once; L2 re-reads excluded).  fp32
-    intermediates are counted at 4 bytes per element (the bf16 path stores them
-    as (hi, lo) bf16 pairs, the same size); K^T and Q^T copies made by the prep
-    stage are counted where they are written and read.
+    read once, each result written once; L2 re-reads excluded).  M, A and their
+    transposes count 4 bytes per element (stored as (hi, lo) bf16 pairs); the
+    chunk states X, Y and pseudo-values D, dR handed from the scans to the
+    backward gradient kernel count 2 bytes per element plus one 4-byte scale per
+    32 elements (their int16 storage); K^T and Q^T copies made by the prep stage
+    are counted where they are written and read.
     """
     nch = B * math.ceil(T / C) * H
     f4 = 4
@@ -51,8 +53,8 @@ def stage_model(name, B, T, H, dk, dv, C=64, in_bytes=2):
     vv = C * dv * in_bytes          # one of v, dO
     gb = C * (f4 + in_bytes)        # g (or G) and beta
     cc = C * C * f4                 # one C x C fp32 matrix
-    st = dk * dv * f4               # one state
-    cd = C * dv * f4                # one C x dv fp32 matrix
+    st = dk * dv * 2 + dk * (dv // 32) * f4     # one stored state (int16 + scales)
+    cd = C * dv * 2 + C * (dv // 32) * f4       # one stored C x dv matrix
     if name in ("prep", "prep_save"):    # K K^T, Q K^T; q, k, g, beta -> M, A, K^T, G
         fl = 4 * C * C * dk
         by = 2 * qk + gb + 2 * cc + qk + C * f4
@@ -60,7 +62,7 @@ def stage_model(name, B, T, H, dk, dv, C=64, in_bytes=2):
             by += 2 * cc + qk
     elif name in ("scan_fwd", "scan_fwd_save"):  # K X, Q X, M R, A D, K^T D
         fl = 6 * C * dk * dv + 4 * C * C * dv
-        by = 3 * qk + vv + 2 * cc + gb + cd
+        by = 3 * qk + vv + 2 * cc + gb + C * dv * f4   # ... -> o (fp32)
         if name == "scan_fwd_save":       # + chunk states X and D for the backward
             by += st + cd
     elif name == "scan_fwd_store":  # K X, M R, K^T D; -> X, D

@@ -60,6 +60,7 @@ comba_status check_shape(const comba_shape* s, Dims* out) {
 
 struct Layout {
   size_t cmap, smap, M, A, G, X, D, Y, dR, ddp, MT, AT, KT, QT, Xfin, sink, total;
+  size_t Xs, Ds, Ys, dRs, Xfs;  // bf16 path: scales of the int16 X, D, Y, dR, final-state sink
 };
 
 Layout layout(const Dims& d, bool bwd) {
@@ -82,13 +83,25 @@ Layout layout(const Dims& d, bool bwd) {
     // the backward also keeps M^T, A^T (hi, lo) and Q^T
     L.KT = take(chh * d.dk * kChunk * sizeof(uint16_t));
     if (bwd) {
+      // M^T, A^T, Q^T; X, D, Y, dR as int16 + one fp32 scale per 32 values
+      const size_t nf = (size_t)(d.N > 0 ? d.N : 1) * d.H;
+      const size_t nb = d.dv / 32;
       L.MT = take(chh * 2 * kChunk * kChunk * sizeof(uint16_t));
       L.AT = take(chh * 2 * kChunk * kChunk * sizeof(uint16_t));
       L.QT = take(chh * d.dk * kChunk * sizeof(uint16_t));
-      L.Xfin = take((size_t)(d.N > 0 ? d.N : 1) * d.H * d.dk * d.dv * sizeof(float));
+      L.Xfin = take(nf * d.dk * d.dv * sizeof(int16_t));
+      L.Xfs = take(nf * d.dk * nb * sizeof(float));
+      L.X = take(chh * d.dk * d.dv * sizeof(int16_t));
+      L.Xs = take(chh * d.dk * nb * sizeof(float));
+      L.D = take(chh * kChunk * d.dv * sizeof(int16_t));
+      L.Ds = take(chh * kChunk * nb * sizeof(float));
+      L.Y = take(chh * d.dk * d.dv * sizeof(int16_t));
+      L.Ys = take(chh * d.dk * nb * sizeof(float));
+      L.dR = take(chh * kChunk * d.dv * sizeof(int16_t));
+      L.dRs = take(chh * kChunk * nb * sizeof(float));
+      L.ddp = take(chh * sizeof(float));
     }
-  }
-  if (bwd) {
+  } else if (bwd) {
     L.X = take(chh * d.dk * d.dv * sizeof(float));
     L.D = take(chh * kChunk * d.dv * sizeof(float));
     L.Y = take(chh * d.dk * d.dv * sizeof(float));
@@ -144,14 +157,25 @@ void carve(comba::LaunchArgs& a, const Layout& L, void* ws, bool bwd) {
   a.Aw = reinterpret_cast<float*>(base + L.A);
   a.Gw = reinterpret_cast<float*>(base + L.G);
   a.sink = reinterpret_cast<float*>(base + L.sink);
-  if (L.Xfin) a.Xfin = reinterpret_cast<float*>(base + L.Xfin);
   a.Mp = reinterpret_cast<uint16_t*>(base + L.M);
   a.Ap = reinterpret_cast<uint16_t*>(base + L.A);
   if (L.KT) a.KTp = reinterpret_cast<uint16_t*>(base + L.KT);
   if (L.MT) a.MTp = reinterpret_cast<uint16_t*>(base + L.MT);
   if (L.AT) a.ATp = reinterpret_cast<uint16_t*>(base + L.AT);
   if (L.QT) a.QTp = reinterpret_cast<uint16_t*>(base + L.QT);
-  if (bwd) {
+  if (bwd && a.bf16) {
+    a.Xfq = reinterpret_cast<int16_t*>(base + L.Xfin);
+    a.Xfs = reinterpret_cast<float*>(base + L.Xfs);
+    a.Xq = reinterpret_cast<int16_t*>(base + L.X);
+    a.Xs = reinterpret_cast<float*>(base + L.Xs);
+    a.Dq = reinterpret_cast<int16_t*>(base + L.D);
+    a.Ds = reinterpret_cast<float*>(base + L.Ds);
+    a.Yq = reinterpret_cast<int16_t*>(base + L.Y);
+    a.Ys = reinterpret_cast<float*>(base + L.Ys);
+    a.dRq = reinterpret_cast<int16_t*>(base + L.dR);
+    a.dRs = reinterpret_cast<float*>(base + L.dRs);
+    a.ddp = reinterpret_cast<float*>(base + L.ddp);
+  } else if (bwd) {
     a.Xw = reinterpret_cast<float*>(base + L.X);
     a.Dw = reinterpret_cast<float*>(base + L.D);
     a.Yw = reinterpret_cast<float*>(base + L.Y);

@@ -186,6 +186,37 @@ __device__ __forceinline__ void store4(float* p, const floatx4& x) {
   *reinterpret_cast<float4*>(p) = make_float4(x[0], x[1], x[2], x[3]);
 }
 
+// ---- int16 fixed-point row blocks -----------------------------------------
+// The chunk states and pseudo-values that the scans hand to the backward
+// gradient kernel are stored as int16 q with one power-of-two scale s per
+// (row, 32-column block): x = q * s, s = 2^(e - 15) where the block's max |x| is
+// below 2^e, so |q| <= 32767 and the rounding error is at most s / 2, i.e. at
+// most 2^-15 of the block's max.  q * s splits exactly into the bf16 (hi, lo)
+// pair the consumer's MFMA products use, so no further rounding is added there.
+// (Zero, tiny and non-finite maxima give a scale in [2^-115, 2^114].)
+__device__ __forceinline__ int q_exponent(float m) {  // e with m < 2^e, m >= 0
+  return max(((__float_as_int(m) >> 23) & 0xFF) - 126, -100);
+}
+__device__ __forceinline__ float q_scale(float m) { return __int_as_float((q_exponent(m) + 112) << 23); }
+__device__ __forceinline__ float q_inv_scale(float m) {
+  return __int_as_float((142 - q_exponent(m)) << 23);
+}
+// four values (times the inverse scale) -> four int16, nearest, saturated
+__device__ __forceinline__ uint2 q_pack4(const floatx4& x, float inv) {
+  uint32_t w[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int a = min(max((int)__builtin_rintf(x[2 * h] * inv), -32767), 32767);
+    const int b = min(max((int)__builtin_rintf(x[2 * h + 1] * inv), -32767), 32767);
+    w[h] = ((uint32_t)a & 0xFFFFu) | ((uint32_t)b << 16);
+  }
+  return make_uint2(w[0], w[1]);
+}
+__device__ __forceinline__ float4 q_unpack4(uint2 u, float s) {
+  return make_float4((float)(int)(int16_t)(u.x & 0xFFFFu) * s, (float)((int)u.x >> 16) * s,
+                     (float)(int)(int16_t)(u.y & 0xFFFFu) * s, (float)((int)u.y >> 16) * s);
+}
+
 // ---- transposed operand fragments from LDS --------------------------------
 // ds_read_b64_tr_b16 (gfx950): inside each 16-lane group the 16 lanes' 8-byte
 // reads form S[s][p] (lane s, element p), and lane i receives S[4e + i/4][i%4]
@@ -252,6 +283,13 @@ __device__ __forceinline__ float wave_sum(float x) {
 }
 // Value of lane + 1 (0 for the last lane).
 __device__ __forceinline__ float shift_down1(float x) { return dpp_upd<0x130>(0.f, x); }
+// Max over lanes l, l ^ 4, l ^ 8, l ^ 12 (the four lanes that hold one row
+// after quad_transpose), every one of them gets the result.
+__device__ __forceinline__ float row4_max(float m) {
+  m = fmaxf(m, dpp_upd<0x124>(0.f, m));  // row_ror:4
+  m = fmaxf(m, dpp_upd<0x128>(0.f, m));  // row_ror:8
+  return m;
+}
 
 // ---- global -> register -> LDS tile copies ---------------------------------
 

@@ -1053,14 +1053,16 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     const bf16_t* __restrict__ beta, const float* __restrict__ d, const float* __restrict__ h0,
     const SeqInfo* __restrict__ smap, int H, const bf16_t* __restrict__ Mp,
     const bf16_t* __restrict__ Ap, const bf16_t* __restrict__ KTp, const float* __restrict__ Gw,
-    float* __restrict__ o, float* __restrict__ ht, float* __restrict__ Xw, float* __restrict__ Dw,
-    float* __restrict__ Xfin, float* __restrict__ sink) {
+    float* __restrict__ o, float* __restrict__ ht, int16_t* __restrict__ Xq,
+    float* __restrict__ Xs, int16_t* __restrict__ Dq, float* __restrict__ Ds,
+    int16_t* __restrict__ Xfq, float* __restrict__ Xfs, float* __restrict__ sink) {
   // Every global load and store inside the chunk loop is issued unconditionally
   // (clamped rows and chunk indices, masked values applied at use, padded-row
   // stores sent to `sink`), so the memory-counter waits stay exact and the
   // next chunk's loads overlap the current chunk's work.
   constexpr int NTV = BV / 16, XMT = DK / 64, KS = DK / 32, CC = CH * CH;
-  constexpr int LDX = DK + 8, LDR = CH + 8;
+  constexpr int LDX = DK + 8, LDR = CH + 8, NB = DV / 32;
+  static_assert(BV == 32, "stored states use one scale per 32-column block = one dv slice");
   __shared__ __align__(16) bf16_t XTh[BV * LDX];
   __shared__ __align__(16) bf16_t XTl[BV * LDX];
   __shared__ __align__(16) bf16_t RTh[BV * LDR];
@@ -1103,6 +1105,27 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt)
         store4(dst + (long)(xrow_q + 16 * mt) * DV + xcol_q + 16 * nt, quad_transpose(X[mt][nt]));
+  };
+  // The same rows as int16 with one scale per row of the slice (see q_pack4).
+  auto store_state_q = [&](int16_t* dq, float* ds) {
+#pragma unroll
+    for (int mt = 0; mt < XMT; ++mt) {
+      floatx4 t[NTV];
+      float m = 0.f;
+#pragma unroll
+      for (int nt = 0; nt < NTV; ++nt) {
+        t[nt] = quad_transpose(X[mt][nt]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) m = fmaxf(m, fabsf(t[nt][e]));
+      }
+      m = row4_max(m);
+      const float inv = q_inv_scale(m);
+      const long row = xrow_q + 16 * mt;
+#pragma unroll
+      for (int nt = 0; nt < NTV; ++nt)
+        *reinterpret_cast<uint2*>(dq + row * DV + xcol_q + 16 * nt) = q_pack4(t[nt], inv);
+      *(qt_col() == 0 ? ds + row * NB + blockIdx.z : sink + lane) = q_scale(m);
+    }
   };
   put_state();
 
@@ -1181,7 +1204,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     if constexpr (OUT) load_a(0);
     load_rows(0);
     put_rows(0);
-    if constexpr (STORE) store_state(Xw + c_chh(0) * DK * DV);
+    if constexpr (STORE) store_state_q(Xq + c_chh(0) * DK * DV, Xs + c_chh(0) * DK * NB);
   }
   __syncthreads();
 
@@ -1253,6 +1276,24 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
         dl[nt] = mfma16(ml[ks], rh, dl[nt]);
       }
     load_m(nx);
+    if constexpr (STORE) {
+      // D rows as int16 with one scale per row of the slice
+      floatx4 t[NTV];
+      float m = 0.f;
+#pragma unroll
+      for (int nt = 0; nt < NTV; ++nt) {
+        t[nt] = quad_transpose(dl[nt]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) m = fmaxf(m, fabsf(t[nt][e]));
+      }
+      m = row4_max(m);
+      const float inv = q_inv_scale(m);
+      const long row = chh * CH + 16 * w + qt_row();
+#pragma unroll
+      for (int nt = 0; nt < NTV; ++nt)
+        *reinterpret_cast<uint2*>(Dq + row * DV + xcol_q + 16 * nt) = q_pack4(t[nt], inv);
+      *(qt_col() == 0 ? Ds + row * NB + blockIdx.z : sink + lane) = q_scale(m);
+    }
 #pragma unroll
     for (int nt = 0; nt < NTV; ++nt) {
       float dv[4], dgv[4];
@@ -1261,9 +1302,6 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
         dv[e] = dl[nt][e];
         dgv[e] = __expf(glast - gg[e]) * dv[e];
       }
-      if constexpr (STORE)
-        store4(Dw + chh * CH * DV + (long)(16 * w + qt_row()) * DV + xcol_q + 16 * nt,
-               quad_transpose(dl[nt]));
       const int off = (16 * nt + r16) * LDR + 16 * w + 4 * g4;
       put_t4(DgTh, DgTl, off, dgv);
       if constexpr (OUT) put_t4(DTh, DTl, off, dv);
@@ -1313,8 +1351,10 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     }
     put_state();
     // state entering the next chunk (after the last chunk: the final state)
-    if constexpr (STORE)
-      store_state(more ? Xw + c_chh(cc + 1) * DK * DV : Xfin + soff);
+    if constexpr (STORE) {
+      const long sb = more ? c_chh(cc + 1) * DK * DV : soff;
+      store_state_q((more ? Xq : Xfq) + sb, (more ? Xs : Xfs) + sb / 32);
+    }
     put_rows(buf ^ 1);
     __syncthreads();
   }
@@ -1328,11 +1368,13 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     const bf16_t* __restrict__ beta, const float* __restrict__ d, const float* __restrict__ dht,
     const SeqInfo* __restrict__ smap, int H, const bf16_t* __restrict__ MTp,
     const bf16_t* __restrict__ ATp, const bf16_t* __restrict__ KTp, const bf16_t* __restrict__ QTp,
-    const float* __restrict__ Gw, float* __restrict__ dh0, float* __restrict__ Yw,
-    float* __restrict__ dRw) {
+    const float* __restrict__ Gw, float* __restrict__ dh0, int16_t* __restrict__ Yq,
+    float* __restrict__ Ys, int16_t* __restrict__ dRq, float* __restrict__ dRs,
+    float* __restrict__ sink) {
   // as in the forward scan, all loop memory operations are unconditional
   constexpr int NTV = BV / 16, XMT = DK / 64, KS = DK / 32, CC = CH * CH;
-  constexpr int LDX = DK + 8, LDR = CH + 8;
+  constexpr int LDX = DK + 8, LDR = CH + 8, NB = DV / 32;
+  static_assert(BV == 32, "stored states use one scale per 32-column block = one dv slice");
   __shared__ __align__(16) bf16_t YTh[BV * LDX];
   __shared__ __align__(16) bf16_t YTl[BV * LDX];
   __shared__ __align__(16) bf16_t dOT[2][BV * LDR];
@@ -1376,6 +1418,27 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt)
         store4(dst + (long)(yrow_q + 16 * mt) * DV + ycol_q + 16 * nt, quad_transpose(Y[mt][nt]));
+  };
+  // the same rows as int16 with one scale per row of the slice (see q_pack4)
+  auto store_state_q = [&](int16_t* dq, float* ds) {
+#pragma unroll
+    for (int mt = 0; mt < XMT; ++mt) {
+      floatx4 t[NTV];
+      float m = 0.f;
+#pragma unroll
+      for (int nt = 0; nt < NTV; ++nt) {
+        t[nt] = quad_transpose(Y[mt][nt]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) m = fmaxf(m, fabsf(t[nt][e]));
+      }
+      m = row4_max(m);
+      const float inv = q_inv_scale(m);
+      const long row = yrow_q + 16 * mt;
+#pragma unroll
+      for (int nt = 0; nt < NTV; ++nt)
+        *reinterpret_cast<uint2*>(dq + row * DV + ycol_q + 16 * nt) = q_pack4(t[nt], inv);
+      *(qt_col() == 0 ? ds + row * NB + blockIdx.z : sink + lane) = q_scale(m);
+    }
   };
   put_state();
 
@@ -1475,7 +1538,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     const long chh = c_chh(cc);
     const int buf = cc & 1;
     const int clen = c_len(cc);
-    store_state(Yw + chh * DK * DV);
+    store_state_q(Yq + chh * DK * DV, Ys + chh * DK * NB);
     load_rows(nx);
     load_do(nx);
     const float glast = Grow[buf][CH - 1];
@@ -1539,13 +1602,29 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
         drr[nt] = mfma16(mtl[ks], xh, drr[nt]);
       }
     load_mt(nx);
+    {
+      // dR rows as int16 with one scale per row of the slice
+      floatx4 t[NTV];
+      float m = 0.f;
+#pragma unroll
+      for (int nt = 0; nt < NTV; ++nt) {
+        t[nt] = quad_transpose(drr[nt]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) m = fmaxf(m, fabsf(t[nt][e]));
+      }
+      m = row4_max(m);
+      const float inv = q_inv_scale(m);
+      const long row = chh * CH + 16 * w + qt_row();
+#pragma unroll
+      for (int nt = 0; nt < NTV; ++nt)
+        *reinterpret_cast<uint2*>(dRq + row * DV + ycol_q + 16 * nt) = q_pack4(t[nt], inv);
+      *(qt_col() == 0 ? dRs + row * NB + blockIdx.z : sink + lane) = q_scale(m);
+    }
 #pragma unroll
     for (int nt = 0; nt < NTV; ++nt) {
       const int off = (16 * nt + r16) * LDR + 16 * w + 4 * g4;
       const bf16x4 dov = *reinterpret_cast<const bf16x4*>(dOT[buf] + off);
       float pg[4], w2[4];
-      store4(dRw + chh * CH * DV + (long)(16 * w + qt_row()) * DV + ycol_q + 16 * nt,
-             quad_transpose(drr[nt]));
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const float drv = drr[nt][e];
@@ -1617,8 +1696,9 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
     const bf16_t* __restrict__ dO, const bf16_t* __restrict__ beta, const float* __restrict__ d,
     const ChunkInfo* __restrict__ cmap, int H, const float* __restrict__ Gw,
-    const float* __restrict__ Xw, const float* __restrict__ Dw, const float* __restrict__ Yw,
-    const float* __restrict__ dRw, int touch_ahead, float* __restrict__ dq, float* __restrict__ dk,
+    const int16_t* __restrict__ Xq, const float* __restrict__ Xs, const int16_t* __restrict__ Dq,
+    const float* __restrict__ Ds, const int16_t* __restrict__ Yq, const float* __restrict__ Ys,
+    const int16_t* __restrict__ dRq, const float* __restrict__ dRs, int touch_ahead, float* __restrict__ dq, float* __restrict__ dk,
     float* __restrict__ dv, float* __restrict__ dbeta, float* __restrict__ dg,
     float* __restrict__ ddp, float* __restrict__ sink) {
   using SM = IntraBwdBfSmem<DK>;
@@ -1663,20 +1743,31 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
 
   const int po = tid & 255, po_r = po >> 2, po_c = (po & 3) * 8;  // dO piece (dup. above 256)
   const int pf_r = tid >> 3, pf_c = (tid & 7) * 4;                 // dR / D / v piece
+  // X, Y, D, dR arrive as int16 with one scale per (row, 32-column block): the
+  // block is exactly one VB-wide column block (see q_pack4)
+  static_assert(VB == 32, "column blocks must match the stored scale blocks");
+  constexpr int NB = DV / 32;
   uint4 r_do;
-  float4 r_dr, r_d, r_x[XP], r_y[XP];
+  uint2 r_dr, r_d, r_x[XP], r_y[XP];
+  float s_dr, s_d, s_x[XP], s_y[XP];
   uint2 r_v;
   auto issue = [&](int vb) {
     const int j = vb * VB;
     r_do = *reinterpret_cast<const uint4*>(dO + (tok + (long)min(po_r, len - 1) * H) * DV + j + po_c);
     r_v = *reinterpret_cast<const uint2*>(v + (tok + (long)min(pf_r, len - 1) * H) * DV + j + pf_c);
-    r_dr = *reinterpret_cast<const float4*>(dRw + chh * CH * DV + (long)pf_r * DV + j + pf_c);
-    r_d = *reinterpret_cast<const float4*>(Dw + chh * CH * DV + (long)pf_r * DV + j + pf_c);
+    const long rr = chh * CH + pf_r;
+    r_dr = *reinterpret_cast<const uint2*>(dRq + rr * DV + j + pf_c);
+    r_d = *reinterpret_cast<const uint2*>(Dq + rr * DV + j + pf_c);
+    s_dr = dRs[rr * NB + vb];
+    s_d = Ds[rr * NB + vb];
 #pragma unroll
     for (int p = 0; p < XP; ++p) {
       const int pc = tid + p * IB_THR, xr = pc >> 3, xc = (pc & 7) * 4;
-      r_x[p] = *reinterpret_cast<const float4*>(Xw + chh * DK * DV + (long)xr * DV + j + xc);
-      r_y[p] = *reinterpret_cast<const float4*>(Yw + chh * DK * DV + (long)xr * DV + j + xc);
+      const long xrow = chh * DK + xr;
+      r_x[p] = *reinterpret_cast<const uint2*>(Xq + xrow * DV + j + xc);
+      r_y[p] = *reinterpret_cast<const uint2*>(Yq + xrow * DV + j + xc);
+      s_x[p] = Xs[xrow * NB + vb];
+      s_y[p] = Ys[xrow * NB + vb];
     }
   };
   float Fpart = 0.f, bv = 0.f;
@@ -1684,32 +1775,34 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     const int j = vb * VB;
     *reinterpret_cast<uint4*>(dOb + po_r * LDB + po_c) = po_r < len ? r_do : make_uint4(0, 0, 0, 0);
     bf16x4 hh, ll;
-    split4v(r_dr, hh, ll);
+    const float4 fdr = q_unpack4(r_dr, s_dr);
+    split4v(fdr, hh, ll);
     *reinterpret_cast<bf16x4*>(dRh + pf_r * LDB + pf_c) = hh;
     *reinterpret_cast<bf16x4*>(dRl + pf_r * LDB + pf_c) = ll;
-    split4v(r_d, hh, ll);
+    split4v(q_unpack4(r_d, s_d), hh, ll);
     *reinterpret_cast<bf16x4*>(Dh + pf_r * LDB + pf_c) = hh;
     *reinterpret_cast<bf16x4*>(Dl + pf_r * LDB + pf_c) = ll;
 #pragma unroll
     for (int p = 0; p < XP; ++p) {
       const int pc = tid + p * IB_THR, xr = pc >> 3, xc = (pc & 7) * 4;
-      split4v(r_x[p], hh, ll);
+      const float4 fx = q_unpack4(r_x[p], s_x[p]), fy = q_unpack4(r_y[p], s_y[p]);
+      split4v(fx, hh, ll);
       *reinterpret_cast<bf16x4*>(Xh + xr * LDB + xc) = hh;
       *reinterpret_cast<bf16x4*>(Xl + xr * LDB + xc) = ll;
-      split4v(r_y[p], hh, ll);
+      split4v(fy, hh, ll);
       *reinterpret_cast<bf16x4*>(Yh + xr * LDB + xc) = hh;
       *reinterpret_cast<bf16x4*>(Yl + xr * LDB + xc) = ll;
-      Fpart += r_x[p].x * r_y[p].x + r_x[p].y * r_y[p].y + r_x[p].z * r_y[p].z + r_x[p].w * r_y[p].w;
+      Fpart += fx.x * fy.x + fx.y * fy.y + fx.z * fy.z + fx.w * fy.w;
     }
     // dv = Diag(beta) dR and <v_r, dR_r>
     const float b = Bs[pf_r];
-    const float4 dvv = make_float4(b * r_dr.x, b * r_dr.y, b * r_dr.z, b * r_dr.w);
+    const float4 dvv = make_float4(b * fdr.x, b * fdr.y, b * fdr.z, b * fdr.w);
     float* dst = pf_r < len ? dv + (tok + (long)pf_r * H) * DV + j + pf_c : sink + (tid & 63) * 4;
     *reinterpret_cast<float4*>(dst) = dvv;
     union { uint2 u; bf16_t e[4]; } vv;
     vv.u = r_v;
-    bv += bf2f(vv.e[0]) * r_dr.x + bf2f(vv.e[1]) * r_dr.y + bf2f(vv.e[2]) * r_dr.z +
-          bf2f(vv.e[3]) * r_dr.w;
+    bv += bf2f(vv.e[0]) * fdr.x + bf2f(vv.e[1]) * fdr.y + bf2f(vv.e[2]) * fdr.z +
+          bf2f(vv.e[3]) * fdr.w;
   };
 
   floatx4 T1[NTW], T2[NTW], T3[NTW], dA[2], dL[2];
@@ -1802,11 +1895,11 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
         static_assert(2 * DK + 4 * CH <= IB_THR, "one line per thread");
         int t = tid;
         const int rr = min(t & (CH - 1), ci2.len - 1);
-        const char* a = reinterpret_cast<const char*>(Xw + chh2 * DK * DV);
-        if (t < DK) a = reinterpret_cast<const char*>(Xw + chh2 * DK * DV + (long)t * DV);
-        else if ((t -= DK) < DK) a = reinterpret_cast<const char*>(Yw + chh2 * DK * DV + (long)t * DV);
-        else if ((t -= DK) < CH) a = reinterpret_cast<const char*>(dRw + (chh2 * CH + t) * DV);
-        else if ((t -= CH) < CH) a = reinterpret_cast<const char*>(Dw + (chh2 * CH + t) * DV);
+        const char* a = reinterpret_cast<const char*>(Xq + chh2 * DK * DV);
+        if (t < DK) a = reinterpret_cast<const char*>(Xq + (chh2 * DK + t) * DV);
+        else if ((t -= DK) < DK) a = reinterpret_cast<const char*>(Yq + (chh2 * DK + t) * DV);
+        else if ((t -= DK) < CH) a = reinterpret_cast<const char*>(dRq + (chh2 * CH + t) * DV);
+        else if ((t -= CH) < CH) a = reinterpret_cast<const char*>(Dq + (chh2 * CH + t) * DV);
         else if ((t -= CH) < CH) a = reinterpret_cast<const char*>(dO + (tok2 + (long)rr * H) * DV);
         else if ((t -= CH) < CH) a = reinterpret_cast<const char*>(v + (tok2 + (long)rr * H) * DV);
         touched = *reinterpret_cast<const uint32_t*>(a);
@@ -2092,12 +2185,12 @@ static hipError_t run_fwd_bf(const LaunchArgs& a) {
   a.stage(a.saved ? "scan_fwd_save" : "scan_fwd");
   if (a.saved)
     k_scan_fwd_bf<DK, DV, SCAN_BV, true, true><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-        q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mp, a.Ap, a.KTp, a.Gw, a.o, a.ht, a.Xw, a.Dw,
-        a.Xfin, a.sink);
+        q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mp, a.Ap, a.KTp, a.Gw, a.o, a.ht, a.Xq, a.Xs,
+        a.Dq, a.Ds, a.Xfq, a.Xfs, a.sink);
   else
     k_scan_fwd_bf<DK, DV, SCAN_BV, true, false><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
         q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mp, a.Ap, a.KTp, a.Gw, a.o, a.ht, nullptr,
-        nullptr, nullptr, a.sink);
+        nullptr, nullptr, nullptr, nullptr, nullptr, a.sink);
   a.stage(nullptr);
   return hipGetLastError();
 }
@@ -2123,18 +2216,18 @@ static hipError_t run_bwd_bf(const LaunchArgs& a) {
           q, k, a.g, beta, a.d, a.cmap, a.H, a.Mp, a.Ap, a.MTp, a.ATp, a.KTp, a.QTp, a.Gw);
     a.stage("scan_fwd_store");
     k_scan_fwd_bf<DK, DV, SCAN_BV, false, true><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-        q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mp, a.Ap, a.KTp, a.Gw, nullptr, nullptr, a.Xw,
-        a.Dw, a.Xfin, a.sink);
+        q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mp, a.Ap, a.KTp, a.Gw, nullptr, nullptr, a.Xq,
+        a.Xs, a.Dq, a.Ds, a.Xfq, a.Xfs, a.sink);
   }
   a.stage("scan_bwd");
   k_scan_bwd_bf<DK, DV, SCAN_BV><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-      q, k, dO, beta, a.d, a.dht, a.smap, a.H, a.MTp, a.ATp, a.KTp, a.QTp, a.Gw, a.dh0, a.Yw,
-      a.dRw);
+      q, k, dO, beta, a.d, a.dht, a.smap, a.H, a.MTp, a.ATp, a.KTp, a.QTp, a.Gw, a.dh0, a.Yq,
+      a.Ys, a.dRq, a.dRs, a.sink);
   a.stage("intra_bwd");
   if (a.ncmax > 0)
     k_intra_bwd_bf<DK, DV><<<dim3(a.ncmax, a.H), IB_THR, 0, st>>>(
-        q, k, v, dO, beta, a.d, a.cmap, a.H, a.Gw, a.Xw, a.Dw, a.Yw, a.dRw, device_cus(), a.dq,
-        a.dk_, a.dv_, a.dbeta, a.dg, a.ddp, a.sink);
+        q, k, v, dO, beta, a.d, a.cmap, a.H, a.Gw, a.Xq, a.Xs, a.Dq, a.Ds, a.Yq, a.Ys, a.dRq, a.dRs,
+        device_cus(), a.dq, a.dk_, a.dv_, a.dbeta, a.dg, a.ddp, a.sink);
   a.stage("reduce_dd");
   k_reduce_dd<<<a.H, NTHR, 0, st>>>(a.ddp, a.ncmax, a.H, a.dd);
   a.stage(nullptr);

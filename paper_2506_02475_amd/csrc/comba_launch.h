@@ -44,7 +44,12 @@ struct LaunchArgs {
   // bf16 path, per chunk-head: M, A as (hi, lo) bf16 pairs [2][64][64] (in the
   // M, A regions), M^T, A^T likewise, K^T and Q^T as [dk][64] bf16
   uint16_t *Mp, *Ap, *MTp, *ATp, *KTp, *QTp;
-  float* Xfin;  // backward: final state of the recomputed forward [N,H,dk,dv]
+  // bf16 path, per chunk-head: X, Y (dk x dv), D, dR (64 x dv) as int16 with one
+  // power-of-two scale per (row, 32-column block) in the matching *s array
+  int16_t *Xq, *Dq, *Yq, *dRq;
+  float *Xs, *Ds, *Ys, *dRs;
+  int16_t* Xfq;  // bf16 path: sink for the state after the last chunk [N,H,dk,dv]
+  float* Xfs;    //   and its scales
   float* sink;  // 1 KiB that absorbs stores of padded rows (never read)
   hipStream_t stream;
   StageHook hook;
