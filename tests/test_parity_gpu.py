@@ -80,6 +80,21 @@ def test_strong_decay_gates_stay_finite():
     check_bwd(w)
 
 
+@pytest.mark.parametrize("v_exp,do_exp", [(12, -24), (-20, 10)])
+def test_far_from_unit_magnitudes(v_exp, do_exp):
+    # values, states and gradients many binades away from 1 (powers of two keep
+    # the bf16 inputs exact): the per-block scales of the stored chunk states
+    # must keep the relative error of the unit-scale case
+    w = random_case(B=1, T=200, H=2, dk=128, dv=128, in_dtype="bf16", dht=True)
+    w.v *= np.float32(2.0 ** v_exp)
+    w.h0 *= np.float32(2.0 ** v_exp)
+    w.dO *= np.float32(2.0 ** do_exp)
+    w.dht *= np.float32(2.0 ** do_exp)
+    errs = check_bwd(w)
+    _log("far-from-unit v 2^%d, dO 2^%d: %s" % (v_exp, do_exp, errs))
+    assert max(errs.values()) < 2e-4
+
+
 def test_deterministic_bitwise():
     w = random_case(B=2, T=300, H=2, dk=128, dv=128, in_dtype="bf16", dht=True)
     a = gpu_bwd(w)
