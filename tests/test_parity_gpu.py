@@ -185,6 +185,39 @@ def test_workload_1p3b_fwdbwd():
     _log("l1p3b_fwdbwd bwd %s" % check_bwd(w, heads=[0, 9]))
 
 
+def test_workload_1p3b_training_pair():
+    # the launch configuration the benchmark times: comba_chunk_fwd_save +
+    # comba_chunk_bwd_saved at the full 1.3B-layer shape, sampled heads against
+    # the oracle and every output bitwise against the stateless pair
+    import torch
+    import oracle
+    import paper_2506_02475_amd as comba
+    from gpu_helpers import to_device
+
+    w = generate(3)
+    a = to_device(w)
+    args = (a["q"], a["k"], a["v"], a["g"], a["beta"], a["d"], a["h0"])
+    o_s, ht_s, ws = comba.comba_chunk_fwd_save(*args)
+    gr_s = comba.comba_chunk_bwd_saved(*args, a["dO"], a["dht"], workspace=ws)
+    o, ht = comba.comba_chunk_fwd(*args)
+    gr = comba.comba_chunk_bwd(*args, a["dO"], a["dht"])
+    torch.cuda.synchronize()
+    assert torch.equal(o_s, o) and torch.equal(ht_s, ht)
+    for key in gr:
+        assert torch.equal(gr_s[key], gr[key]), key
+    heads = [4, 13]
+    ro, rht = oracle.workload_fwd(w, heads=heads)
+    ref = oracle.workload_bwd(w, heads=heads)
+    errs = {"o": maxrel(o_s.cpu().numpy()[:, :, heads], ro),
+            "ht": maxrel(ht_s.cpu().numpy()[:, heads], rht)}
+    for key in ("dq", "dk", "dv", "dg", "dbeta"):
+        errs[key] = maxrel(gr_s[key].cpu().numpy()[:, :, heads], ref[key])
+    errs["dd"] = maxrel(gr_s["dd"].cpu().numpy()[heads], ref["dd"])
+    _log("l1p3b training pair %s" % errs)
+    for key, e in errs.items():
+        assert np.isfinite(e) and e <= 2e-3, (key, e)
+
+
 def test_workload_varlen_512k_fwd():
     w = generate(4)
     _log("varlen_512k_fwd %s" % check_fwd(w, heads=[5]))
