@@ -61,6 +61,7 @@ comba_status check_shape(const comba_shape* s, Dims* out) {
 struct Layout {
   size_t cmap, smap, M, A, G, X, D, Y, dR, ddp, MT, AT, KT, QT, Xfin, sink, total;
   size_t Xs, Ds, Ys, dRs, Xfs;  // bf16 path: scales of the int16 X, D, Y, dR, final-state sink
+  size_t Ms, As, MTs, ATs;       // bf16 path: row scales of the int16 M, A, M^T, A^T
 };
 
 Layout layout(const Dims& d, bool bwd) {
@@ -75,19 +76,23 @@ Layout layout(const Dims& d, bool bwd) {
   L.sink = take(1024);
   L.cmap = take((size_t)d.ncmax * sizeof(comba::ChunkInfo));
   L.smap = take((size_t)(d.N > 0 ? d.N : 1) * sizeof(comba::SeqInfo));
-  L.M = take(chh * kChunk * kChunk * sizeof(float));
-  L.A = take(chh * kChunk * kChunk * sizeof(float));
   L.G = take(chh * kChunk * sizeof(float));
   if (d.bf16) {
-    // bf16 path: M and A regions hold (hi, lo) bf16 pairs; K^T per chunk;
-    // the backward also keeps M^T, A^T (hi, lo) and Q^T
+    // bf16 path: M, A as int16 with row scales; K^T per chunk; the backward
+    // also keeps M^T, A^T (int16 + row scales) and Q^T
+    L.M = take(chh * kChunk * kChunk * sizeof(int16_t));
+    L.Ms = take(chh * kChunk * sizeof(float));
+    L.A = take(chh * kChunk * kChunk * sizeof(int16_t));
+    L.As = take(chh * kChunk * sizeof(float));
     L.KT = take(chh * d.dk * kChunk * sizeof(uint16_t));
     if (bwd) {
       // M^T, A^T, Q^T; X, D, Y, dR as int16 + one fp32 scale per 32 values
       const size_t nf = (size_t)(d.N > 0 ? d.N : 1) * d.H;
       const size_t nb = d.dv / 32;
-      L.MT = take(chh * 2 * kChunk * kChunk * sizeof(uint16_t));
-      L.AT = take(chh * 2 * kChunk * kChunk * sizeof(uint16_t));
+      L.MT = take(chh * kChunk * kChunk * sizeof(int16_t));
+      L.MTs = take(chh * kChunk * sizeof(float));
+      L.AT = take(chh * kChunk * kChunk * sizeof(int16_t));
+      L.ATs = take(chh * kChunk * sizeof(float));
       L.QT = take(chh * d.dk * kChunk * sizeof(uint16_t));
       L.Xfin = take(nf * d.dk * d.dv * sizeof(int16_t));
       L.Xfs = take(nf * d.dk * nb * sizeof(float));
@@ -101,7 +106,11 @@ Layout layout(const Dims& d, bool bwd) {
       L.dRs = take(chh * kChunk * nb * sizeof(float));
       L.ddp = take(chh * sizeof(float));
     }
-  } else if (bwd) {
+  } else {
+    L.M = take(chh * kChunk * kChunk * sizeof(float));
+    L.A = take(chh * kChunk * kChunk * sizeof(float));
+  }
+  if (!d.bf16 && bwd) {
     L.X = take(chh * d.dk * d.dv * sizeof(float));
     L.D = take(chh * kChunk * d.dv * sizeof(float));
     L.Y = take(chh * d.dk * d.dv * sizeof(float));
@@ -157,12 +166,20 @@ void carve(comba::LaunchArgs& a, const Layout& L, void* ws, bool bwd) {
   a.Aw = reinterpret_cast<float*>(base + L.A);
   a.Gw = reinterpret_cast<float*>(base + L.G);
   a.sink = reinterpret_cast<float*>(base + L.sink);
-  a.Mp = reinterpret_cast<uint16_t*>(base + L.M);
-  a.Ap = reinterpret_cast<uint16_t*>(base + L.A);
-  if (L.KT) a.KTp = reinterpret_cast<uint16_t*>(base + L.KT);
-  if (L.MT) a.MTp = reinterpret_cast<uint16_t*>(base + L.MT);
-  if (L.AT) a.ATp = reinterpret_cast<uint16_t*>(base + L.AT);
-  if (L.QT) a.QTp = reinterpret_cast<uint16_t*>(base + L.QT);
+  if (a.bf16) {
+    a.Mq = reinterpret_cast<int16_t*>(base + L.M);
+    a.Ms = reinterpret_cast<float*>(base + L.Ms);
+    a.Aq = reinterpret_cast<int16_t*>(base + L.A);
+    a.As = reinterpret_cast<float*>(base + L.As);
+    a.KTp = reinterpret_cast<uint16_t*>(base + L.KT);
+    if (bwd) {
+      a.MTq = reinterpret_cast<int16_t*>(base + L.MT);
+      a.MTs = reinterpret_cast<float*>(base + L.MTs);
+      a.ATq = reinterpret_cast<int16_t*>(base + L.AT);
+      a.ATs = reinterpret_cast<float*>(base + L.ATs);
+      a.QTp = reinterpret_cast<uint16_t*>(base + L.QT);
+    }
+  }
   if (bwd && a.bf16) {
     a.Xfq = reinterpret_cast<int16_t*>(base + L.Xfin);
     a.Xfs = reinterpret_cast<float*>(base + L.Xfs);

@@ -217,6 +217,28 @@ __device__ __forceinline__ float4 q_unpack4(uint2 u, float s) {
                      (float)(int)(int16_t)(u.y & 0xFFFFu) * s, (float)((int)u.y >> 16) * s);
 }
 
+// Eight int16 (one 16-byte piece of a stored row) as the exact bf16 pair
+// hi + lo of each value: |q| < 2^15, hi keeps 8 significant bits, q - hi is an
+// integer below 2^7 in magnitude and so exact in bf16.
+__device__ __forceinline__ void q_split8(const uint4& u, bf16x8& hi, bf16x8& lo) {
+  const uint32_t wd[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float a = (float)(int)(int16_t)(wd[i] & 0xFFFFu), b = (float)((int)wd[i] >> 16);
+    const __bf16 ah = (__bf16)a, bh = (__bf16)b;
+    hi[2 * i] = ah;
+    lo[2 * i] = (__bf16)(a - (float)ah);
+    hi[2 * i + 1] = bh;
+    lo[2 * i + 1] = (__bf16)(b - (float)bh);
+  }
+}
+// Eight values (times the inverse scale) -> eight int16, nearest, saturated.
+__device__ __forceinline__ uint4 q_pack8(const float (&x)[8], float inv) {
+  const uint2 a = q_pack4(floatx4{x[0], x[1], x[2], x[3]}, inv);
+  const uint2 b = q_pack4(floatx4{x[4], x[5], x[6], x[7]}, inv);
+  return make_uint4(a.x, a.y, b.x, b.y);
+}
+
 // ---- transposed operand fragments from LDS --------------------------------
 // ds_read_b64_tr_b16 (gfx950): inside each 16-lane group the 16 lanes' 8-byte
 // reads form S[s][p] (lane s, element p), and lane i receives S[4e + i/4][i%4]
@@ -283,6 +305,18 @@ __device__ __forceinline__ float wave_sum(float x) {
 }
 // Value of lane + 1 (0 for the last lane).
 __device__ __forceinline__ float shift_down1(float x) { return dpp_upd<0x130>(0.f, x); }
+// Max over each group of 8 lanes, resp. the 16 lanes of a row (symmetric
+// butterflies, every lane gets the result).
+__device__ __forceinline__ float max8(float m) {
+  m = fmaxf(m, dpp_upd<0xB1>(0.f, m));   // quad_perm [1,0,3,2]
+  m = fmaxf(m, dpp_upd<0x4E>(0.f, m));   // quad_perm [2,3,0,1]
+  m = fmaxf(m, dpp_upd<0x141>(0.f, m));  // row_half_mirror
+  return m;
+}
+__device__ __forceinline__ float max16(float m) {
+  m = max8(m);
+  return fmaxf(m, dpp_upd<0x140>(0.f, m));  // row_mirror
+}
 // Max over lanes l, l ^ 4, l ^ 8, l ^ 12 (the four lanes that hold one row
 // after quad_transpose), every one of them gets the result.
 __device__ __forceinline__ float row4_max(float m) {

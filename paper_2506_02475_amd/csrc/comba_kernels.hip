@@ -899,9 +899,12 @@ template <int DK, bool BWD>
 __global__ __launch_bounds__(NTHR) void k_prep_bf(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const float* __restrict__ g,
     const bf16_t* __restrict__ beta, const float* __restrict__ d, const ChunkInfo* __restrict__ cmap,
-    int H, bf16_t* __restrict__ Mp, bf16_t* __restrict__ Ap, bf16_t* __restrict__ MTp,
-    bf16_t* __restrict__ ATp, bf16_t* __restrict__ KTp, bf16_t* __restrict__ QTp,
-    float* __restrict__ Gw) {
+    int H, int16_t* __restrict__ Mq, float* __restrict__ Ms, int16_t* __restrict__ Aq,
+    float* __restrict__ As, int16_t* __restrict__ MTq, float* __restrict__ MTs,
+    int16_t* __restrict__ ATq, float* __restrict__ ATs, bf16_t* __restrict__ KTp,
+    bf16_t* __restrict__ QTp, float* __restrict__ Gw, float* __restrict__ sink) {
+  // M, A (and M^T, A^T) leave as int16 rows with one power-of-two scale per row
+  // (see q_pack4): the scans fold the scale into their accumulator rows
   constexpr int LDK = DK + 8;
   constexpr int LDL = CH + 4;
   constexpr int CC = CH * CH;
@@ -909,13 +912,14 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
   __shared__ __align__(16) bf16_t Qs[CH * LDK];
   __shared__ __align__(16) float Ls[CH * LDL];
   __shared__ float Gs[CH], Bs[CH];
+  __shared__ float colmax[BWD ? NWAVE : 1][CH];  // per-wave column maxima of |A|
 
   const ChunkInfo ci = cmap[blockIdx.x];
   if (ci.len <= 0) return;
   const int h = blockIdx.y;
   const long chh = (long)blockIdx.x * H + h;
   const long tok = (long)ci.tok0 * H + h;
-  const int w = wave_id(), lane = lane_id(), g4 = lane >> 4;
+  const int w = wave_id(), lane = lane_id(), g4 = lane >> 4, r16 = lane & 15;
   {
     TileRegs<bf16_t, CH, DK> kr, qr;
     kr.load(k + tok * DK, (long)H * DK, ci.len);
@@ -938,10 +942,10 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
   mma<false, 1, 4, DK>(akk, Ks + 16 * w * LDK, LDK, Ks, LDK);
   mma<false, 1, 4, DK>(aqk, Qs + 16 * w * LDK, LDK, Ks, LDK);
   const float dh = d[h];
-  bf16_t* Ao = Ap + chh * 2 * CC;
+  // A in the accumulator layout: av[nt][e] = A[16w + 4g4 + e][16nt + r16]
+  float av[4][4], rmax[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int nt = 0; nt < 4; ++nt) {
-    float av[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int r = 16 * w + acc_row(0, e), c = acc_col(nt);
@@ -949,26 +953,52 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
       float a = 0.f, l = 0.f;
       if (r >= c) a = (aqk[0][nt][e] - dh * kk) * __expf(Gs[r] - Gs[c]);
       if (r > c) l = Bs[r] * __expf(Gs[r - 1] - Gs[c]) * kk;
-      av[e] = a;
+      av[nt][e] = a;
+      rmax[e] = fmaxf(rmax[e], fabsf(a));
       Ls[r * LDL + c] = l;
     }
-    // A rows (hi, lo) leave as 8-byte pieces of four columns (see quad_transpose)
-    {
-      const floatx4 aq = quad_transpose(floatx4{av[0], av[1], av[2], av[3]});
-      const float aa[4] = {aq[0], aq[1], aq[2], aq[3]};
-      bf16x4 hh, ll;
-      split4(aa, hh, ll);
-      const int off = (16 * w + qt_row()) * CH + 16 * nt + qt_col();
-      *reinterpret_cast<bf16x4*>(Ao + off) = hh;
-      *reinterpret_cast<bf16x4*>(Ao + CC + off) = ll;
-    }
-    if constexpr (BWD) {
-      // A^T: this lane's column c, rows 16w + 4g .. +3
-      bf16_t* At = ATp + chh * 2 * CC;
-      put_t4(At, At + CC, acc_col(nt) * CH + 16 * w + 4 * g4, av);
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) rmax[e] = max16(rmax[e]);  // over the row's 64 columns
+  {
+    // A rows leave as 8-byte pieces of four columns (see quad_transpose); the
+    // lane's row after the transpose is 16w + 4g4 + (lane & 3)
+    const int i = lane & 3;
+    const float mrow = i == 0 ? rmax[0] : i == 1 ? rmax[1] : i == 2 ? rmax[2] : rmax[3];
+    const float inv = q_inv_scale(mrow);
+    const long rowoff = chh * CC + (long)(16 * w + qt_row()) * CH;
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt)
+      *reinterpret_cast<uint2*>(Aq + rowoff + 16 * nt + qt_col()) =
+          q_pack4(quad_transpose(floatx4{av[nt][0], av[nt][1], av[nt][2], av[nt][3]}), inv);
+    const float4 sc = make_float4(q_scale(rmax[0]), q_scale(rmax[1]), q_scale(rmax[2]),
+                                  q_scale(rmax[3]));
+    *reinterpret_cast<float4*>(r16 == 0 ? As + chh * CH + 16 * w + 4 * g4 : sink + 4 * lane) = sc;
+  }
+  if constexpr (BWD) {
+    // column maxima of this wave's 16 rows, combined over the waves below
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) {
+      float m = fmaxf(fmaxf(fabsf(av[nt][0]), fabsf(av[nt][1])), fmaxf(fabsf(av[nt][2]), fabsf(av[nt][3])));
+      m = fmaxf(m, __shfl_xor(m, 16));
+      m = fmaxf(m, __shfl_xor(m, 32));
+      if (g4 == 0) colmax[w][16 * nt + r16] = m;
     }
   }
   __syncthreads();
+
+  if constexpr (BWD) {
+    // A^T rows (= columns c of A) as 8-byte pieces: this lane's column c, rows
+    // 16w + 4g4 .. +3
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) {
+      const int c = 16 * nt + r16;
+      const float m = fmaxf(fmaxf(colmax[0][c], colmax[1][c]), fmaxf(colmax[2][c], colmax[3][c]));
+      *reinterpret_cast<uint2*>(ATq + chh * CC + (long)c * CH + 16 * w + 4 * g4) =
+          q_pack4(floatx4{av[nt][0], av[nt][1], av[nt][2], av[nt][3]}, q_inv_scale(m));
+      *(w == 0 && g4 == 0 ? ATs + chh * CH + c : sink + lane) = q_scale(m);
+    }
+  }
 
   if (w == 0) {
     // M = (I + L)^{-1}: lane j solves column j by forward substitution in fp32,
@@ -997,19 +1027,18 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
 #pragma unroll
     for (int i = 0; i < CH; ++i) Ls[i * LDL + j] = x[i];
     if constexpr (BWD) {
-      bf16_t* Mt = MTp + chh * 2 * CC + j * CH;
+      // M^T row j = column j of M, straight from registers
+      float m = 0.f;
+#pragma unroll
+      for (int i = 0; i < CH; ++i) m = fmaxf(m, fabsf(x[i]));
+      const float inv = q_inv_scale(m);
+      int16_t* Mt = MTq + chh * CC + (long)j * CH;
 #pragma unroll
       for (int i = 0; i < CH; i += 8) {
-        bf16x8 hv, lv;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const __bf16 hh = (__bf16)x[i + e];
-          hv[e] = hh;
-          lv[e] = (__bf16)(x[i + e] - (float)hh);
-        }
-        *reinterpret_cast<bf16x8*>(Mt + i) = hv;
-        *reinterpret_cast<bf16x8*>(Mt + CC + i) = lv;
+        const float xv[8] = {x[i], x[i + 1], x[i + 2], x[i + 3], x[i + 4], x[i + 5], x[i + 6], x[i + 7]};
+        *reinterpret_cast<uint4*>(Mt + i) = q_pack8(xv, inv);
       }
+      MTs[chh * CH + j] = q_scale(m);
     }
   } else {
     // waves 1..3: K^T (and Q^T) per chunk-head, [dk][64] bf16.  One transposing
@@ -1025,22 +1054,20 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
     }
   }
   __syncthreads();
-  // M rows (hi, lo) from LDS, 16-byte pieces of eight columns
-  bf16_t* Mo = Mp + chh * 2 * CC;
+  // M rows from LDS as 16-byte pieces of eight columns; the 8 threads of a row
+  // are one 8-lane group, which reduces the row maximum
+  static_assert(CC / 8 % NTHR == 0, "every thread takes whole passes");
   for (int idx = threadIdx.x; idx < CC / 8; idx += NTHR) {
     const int r = idx / (CH / 8), c8 = (idx % (CH / 8)) * 8;
     const float4 m0 = *reinterpret_cast<const float4*>(Ls + r * LDL + c8);
     const float4 m1 = *reinterpret_cast<const float4*>(Ls + r * LDL + c8 + 4);
     const float mv[8] = {m0.x, m0.y, m0.z, m0.w, m1.x, m1.y, m1.z, m1.w};
-    bf16x8 hv, lv;
+    float m = 0.f;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const __bf16 hh = (__bf16)mv[e];
-      hv[e] = hh;
-      lv[e] = (__bf16)(mv[e] - (float)hh);
-    }
-    *reinterpret_cast<bf16x8*>(Mo + r * CH + c8) = hv;
-    *reinterpret_cast<bf16x8*>(Mo + CC + r * CH + c8) = lv;
+    for (int e = 0; e < 8; ++e) m = fmaxf(m, fabsf(mv[e]));
+    m = max8(m);
+    *reinterpret_cast<uint4*>(Mq + chh * CC + (long)r * CH + c8) = q_pack8(mv, q_inv_scale(m));
+    *(c8 == 0 ? Ms + chh * CH + r : sink + lane) = q_scale(m);
   }
 }
 
@@ -1051,8 +1078,9 @@ template <int DK, int DV, int BV, bool OUT, bool STORE>
 __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
     const bf16_t* __restrict__ beta, const float* __restrict__ d, const float* __restrict__ h0,
-    const SeqInfo* __restrict__ smap, int H, const bf16_t* __restrict__ Mp,
-    const bf16_t* __restrict__ Ap, const bf16_t* __restrict__ KTp, const float* __restrict__ Gw,
+    const SeqInfo* __restrict__ smap, int H, const int16_t* __restrict__ Mq,
+    const float* __restrict__ Ms, const int16_t* __restrict__ Aq, const float* __restrict__ As,
+    const bf16_t* __restrict__ KTp, const float* __restrict__ Gw,
     float* __restrict__ o, float* __restrict__ ht, int16_t* __restrict__ Xq,
     float* __restrict__ Xs, int16_t* __restrict__ Dq, float* __restrict__ Ds,
     int16_t* __restrict__ Xfq, float* __restrict__ Xfs, float* __restrict__ sink) {
@@ -1133,8 +1161,12 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
   auto c_tok = [&](int cc) { return (long)(si.tok0 + cc * CH) * H + h; };
   auto c_chh = [&](int cc) { return (long)(si.chunk0 + cc) * H + h; };
 
-  // per-chunk operands, loaded one chunk ahead
-  bf16x8 kf[KS], qf[KS], ktf[XMT][2], mh[2], ml[2], ah[2], al[2];
+  // per-chunk operands, loaded one chunk ahead: K, Q rows and K^T as bf16, the
+  // rows of M and A as int16 with their row scales (applied to the accumulator
+  // rows: (M R)[r] = s_r sum_i q[r][i] R[i])
+  bf16x8 kf[KS], qf[KS], ktf[XMT][2];
+  uint4 mq[2], aq[2];
+  float4 msc, asc;
   // per-row values of the chunk (cumulative gates G, beta, the V slice) are
   // loaded one chunk ahead into registers and staged through a double-buffered
   // LDS area at the end of each chunk
@@ -1182,20 +1214,16 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
       for (int ks = 0; ks < 2; ++ks) ktf[mt][ks] = ld8(p + 16 * mt * CH + 32 * ks);
   };
   auto load_m = [&](int cc) {
-    const bf16_t* p = Mp + c_chh(cc) * 2 * CC + prow * CH + 8 * g4;
+    const int16_t* p = Mq + c_chh(cc) * CC + prow * CH + 8 * g4;
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      mh[ks] = ld8(p + 32 * ks);
-      ml[ks] = ld8(p + CC + 32 * ks);
-    }
+    for (int ks = 0; ks < 2; ++ks) mq[ks] = *reinterpret_cast<const uint4*>(p + 32 * ks);
+    msc = *reinterpret_cast<const float4*>(Ms + c_chh(cc) * CH + 16 * w + 4 * g4);
   };
   auto load_a = [&](int cc) {
-    const bf16_t* p = Ap + c_chh(cc) * 2 * CC + prow * CH + 8 * g4;
+    const int16_t* p = Aq + c_chh(cc) * CC + prow * CH + 8 * g4;
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      ah[ks] = ld8(p + 32 * ks);
-      al[ks] = ld8(p + CC + 32 * ks);
-    }
+    for (int ks = 0; ks < 2; ++ks) aq[ks] = *reinterpret_cast<const uint4*>(p + 32 * ks);
+    asc = *reinterpret_cast<const float4*>(As + c_chh(cc) * CH + 16 * w + 4 * g4);
   };
   if (n > 0) {
     load_kq(0);
@@ -1266,16 +1294,27 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
 #pragma unroll
     for (int nt = 0; nt < NTV; ++nt) dl[nt] = zero4();
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
+    for (int ks = 0; ks < 2; ++ks) {
+      bf16x8 mh, ml;
+      q_split8(mq[ks], mh, ml);
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt) {
         const int off = (16 * nt + r16) * LDR + 32 * ks + 8 * g4;
         const bf16x8 rh = ld8(RTh + off), rl = ld8(RTl + off);
-        dl[nt] = mfma16(mh[ks], rh, dl[nt]);
-        dl[nt] = mfma16(mh[ks], rl, dl[nt]);
-        dl[nt] = mfma16(ml[ks], rh, dl[nt]);
+        dl[nt] = mfma16(mh, rh, dl[nt]);
+        dl[nt] = mfma16(mh, rl, dl[nt]);
+        dl[nt] = mfma16(ml, rh, dl[nt]);
       }
+    }
+    const float4 ms_cur = msc;
     load_m(nx);
+#pragma unroll
+    for (int nt = 0; nt < NTV; ++nt) {
+      dl[nt][0] *= ms_cur.x;
+      dl[nt][1] *= ms_cur.y;
+      dl[nt][2] *= ms_cur.z;
+      dl[nt][3] *= ms_cur.w;
+    }
     if constexpr (STORE) {
       // D rows as int16 with one scale per row of the slice
       floatx4 t[NTV];
@@ -1330,17 +1369,31 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
 
     // O = Diag(exp G)(Q - d K) X + A D
     if constexpr (OUT) {
+      floatx4 adc[NTV];
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks)
+      for (int nt = 0; nt < NTV; ++nt) adc[nt] = zero4();
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        bf16x8 ah, al;
+        q_split8(aq[ks], ah, al);
 #pragma unroll
         for (int nt = 0; nt < NTV; ++nt) {
           const int off = (16 * nt + r16) * LDR + 32 * ks + 8 * g4;
           const bf16x8 dh_ = ld8(DTh + off), dl_ = ld8(DTl + off);
-          oacc[nt] = mfma16(ah[ks], dh_, oacc[nt]);
-          oacc[nt] = mfma16(ah[ks], dl_, oacc[nt]);
-          oacc[nt] = mfma16(al[ks], dh_, oacc[nt]);
+          adc[nt] = mfma16(ah, dh_, adc[nt]);
+          adc[nt] = mfma16(ah, dl_, adc[nt]);
+          adc[nt] = mfma16(al, dh_, adc[nt]);
         }
+      }
+      const float4 as_cur = asc;
       load_a(nx);
+#pragma unroll
+      for (int nt = 0; nt < NTV; ++nt) {
+        oacc[nt][0] += as_cur.x * adc[nt][0];
+        oacc[nt][1] += as_cur.y * adc[nt][1];
+        oacc[nt][2] += as_cur.z * adc[nt][2];
+        oacc[nt][3] += as_cur.w * adc[nt][3];
+      }
       const int orow = 16 * w + qt_row();
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt) {
@@ -1366,8 +1419,9 @@ template <int DK, int DV, int BV>
 __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ dO,
     const bf16_t* __restrict__ beta, const float* __restrict__ d, const float* __restrict__ dht,
-    const SeqInfo* __restrict__ smap, int H, const bf16_t* __restrict__ MTp,
-    const bf16_t* __restrict__ ATp, const bf16_t* __restrict__ KTp, const bf16_t* __restrict__ QTp,
+    const SeqInfo* __restrict__ smap, int H, const int16_t* __restrict__ MTq,
+    const float* __restrict__ MTs, const int16_t* __restrict__ ATq, const float* __restrict__ ATs,
+    const bf16_t* __restrict__ KTp, const bf16_t* __restrict__ QTp,
     const float* __restrict__ Gw, float* __restrict__ dh0, int16_t* __restrict__ Yq,
     float* __restrict__ Ys, int16_t* __restrict__ dRq, float* __restrict__ dRs,
     float* __restrict__ sink) {
@@ -1446,7 +1500,10 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
   auto c_tok = [&](int cc) { return (long)(si.tok0 + cc * CH) * H + h; };
   auto c_chh = [&](int cc) { return (long)(si.chunk0 + cc) * H + h; };
 
-  bf16x8 kf[KS], ath[2], atl[2], mth[2], mtl[2], qtf[XMT][2], ktf[XMT][2];
+  // A^T, M^T rows as int16 with their row scales (applied to the accumulator rows)
+  bf16x8 kf[KS], qtf[XMT][2], ktf[XMT][2];
+  uint4 atq[2], mtq[2];
+  float4 atsc, mtsc;
   // per-row values (G, beta) and the dO slice are loaded one chunk ahead into
   // registers and staged through double-buffered LDS at the end of each chunk
   __shared__ float Grow[2][CH], Brow[2][CH];
@@ -1462,20 +1519,16 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     for (int ks = 0; ks < KS; ++ks) kf[ks] = ld8(k + rb + 32 * ks);
   };
   auto load_at = [&](int cc) {
-    const bf16_t* p = ATp + c_chh(cc) * 2 * CC + prow * CH + 8 * g4;
+    const int16_t* p = ATq + c_chh(cc) * CC + prow * CH + 8 * g4;
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      ath[ks] = ld8(p + 32 * ks);
-      atl[ks] = ld8(p + CC + 32 * ks);
-    }
+    for (int ks = 0; ks < 2; ++ks) atq[ks] = *reinterpret_cast<const uint4*>(p + 32 * ks);
+    atsc = *reinterpret_cast<const float4*>(ATs + c_chh(cc) * CH + 16 * w + 4 * g4);
   };
   auto load_mt = [&](int cc) {
-    const bf16_t* p = MTp + c_chh(cc) * 2 * CC + prow * CH + 8 * g4;
+    const int16_t* p = MTq + c_chh(cc) * CC + prow * CH + 8 * g4;
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      mth[ks] = ld8(p + 32 * ks);
-      mtl[ks] = ld8(p + CC + 32 * ks);
-    }
+    for (int ks = 0; ks < 2; ++ks) mtq[ks] = *reinterpret_cast<const uint4*>(p + 32 * ks);
+    mtsc = *reinterpret_cast<const float4*>(MTs + c_chh(cc) * CH + 16 * w + 4 * g4);
   };
   auto load_qkt = [&](int cc) {
     const long base = c_chh(cc) * DK * CH + ((DK / 4) * w + r16) * CH + 8 * g4;
@@ -1568,15 +1621,26 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
         ky[nt] = mfma16(kf[ks], yl, ky[nt]);
       }
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
+    for (int ks = 0; ks < 2; ++ks) {
+      bf16x8 ath, atl;
+      q_split8(atq[ks], ath, atl);
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt) {
         const bf16x8 dov = ld8(dOT[buf] + (16 * nt + r16) * LDR + 32 * ks + 8 * g4);
-        ad[nt] = mfma16(ath[ks], dov, ad[nt]);
-        ad[nt] = mfma16(atl[ks], dov, ad[nt]);
+        ad[nt] = mfma16(ath, dov, ad[nt]);
+        ad[nt] = mfma16(atl, dov, ad[nt]);
       }
+    }
+    const float4 at_cur = atsc;
     load_k(nx);
     load_at(nx);
+#pragma unroll
+    for (int nt = 0; nt < NTV; ++nt) {
+      ad[nt][0] *= at_cur.x;
+      ad[nt][1] *= at_cur.y;
+      ad[nt][2] *= at_cur.z;
+      ad[nt][3] *= at_cur.w;
+    }
 #pragma unroll
     for (int nt = 0; nt < NTV; ++nt) {
       float dd_[4];
@@ -1592,16 +1656,27 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
 #pragma unroll
     for (int nt = 0; nt < NTV; ++nt) drr[nt] = zero4();
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
+    for (int ks = 0; ks < 2; ++ks) {
+      bf16x8 mth, mtl;
+      q_split8(mtq[ks], mth, mtl);
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt) {
         const int off = (16 * nt + r16) * LDR + 32 * ks + 8 * g4;
         const bf16x8 xh = ld8(dDTh + off), xl = ld8(dDTl + off);
-        drr[nt] = mfma16(mth[ks], xh, drr[nt]);
-        drr[nt] = mfma16(mth[ks], xl, drr[nt]);
-        drr[nt] = mfma16(mtl[ks], xh, drr[nt]);
+        drr[nt] = mfma16(mth, xh, drr[nt]);
+        drr[nt] = mfma16(mth, xl, drr[nt]);
+        drr[nt] = mfma16(mtl, xh, drr[nt]);
       }
+    }
+    const float4 mt_cur = mtsc;
     load_mt(nx);
+#pragma unroll
+    for (int nt = 0; nt < NTV; ++nt) {
+      drr[nt][0] *= mt_cur.x;
+      drr[nt][1] *= mt_cur.y;
+      drr[nt][2] *= mt_cur.z;
+      drr[nt][3] *= mt_cur.w;
+    }
     {
       // dR rows as int16 with one scale per row of the slice
       floatx4 t[NTV];
@@ -2177,19 +2252,21 @@ static hipError_t run_fwd_bf(const LaunchArgs& a) {
   if (a.ncmax > 0) {
     if (a.saved)
       k_prep_bf<DK, true><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
-          q, k, a.g, beta, a.d, a.cmap, a.H, a.Mp, a.Ap, a.MTp, a.ATp, a.KTp, a.QTp, a.Gw);
+          q, k, a.g, beta, a.d, a.cmap, a.H, a.Mq, a.Ms, a.Aq, a.As, a.MTq, a.MTs, a.ATq, a.ATs,
+          a.KTp, a.QTp, a.Gw, a.sink);
     else
       k_prep_bf<DK, false><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
-          q, k, a.g, beta, a.d, a.cmap, a.H, a.Mp, a.Ap, nullptr, nullptr, a.KTp, nullptr, a.Gw);
+          q, k, a.g, beta, a.d, a.cmap, a.H, a.Mq, a.Ms, a.Aq, a.As, nullptr, nullptr, nullptr,
+          nullptr, a.KTp, nullptr, a.Gw, a.sink);
   }
   a.stage(a.saved ? "scan_fwd_save" : "scan_fwd");
   if (a.saved)
     k_scan_fwd_bf<DK, DV, SCAN_BV, true, true><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-        q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mp, a.Ap, a.KTp, a.Gw, a.o, a.ht, a.Xq, a.Xs,
+        q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mq, a.Ms, a.Aq, a.As, a.KTp, a.Gw, a.o, a.ht, a.Xq, a.Xs,
         a.Dq, a.Ds, a.Xfq, a.Xfs, a.sink);
   else
     k_scan_fwd_bf<DK, DV, SCAN_BV, true, false><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-        q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mp, a.Ap, a.KTp, a.Gw, a.o, a.ht, nullptr,
+        q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mq, a.Ms, a.Aq, a.As, a.KTp, a.Gw, a.o, a.ht, nullptr,
         nullptr, nullptr, nullptr, nullptr, nullptr, a.sink);
   a.stage(nullptr);
   return hipGetLastError();
@@ -2213,15 +2290,16 @@ static hipError_t run_bwd_bf(const LaunchArgs& a) {
     a.stage("prep");
     if (a.ncmax > 0)
       k_prep_bf<DK, true><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
-          q, k, a.g, beta, a.d, a.cmap, a.H, a.Mp, a.Ap, a.MTp, a.ATp, a.KTp, a.QTp, a.Gw);
+          q, k, a.g, beta, a.d, a.cmap, a.H, a.Mq, a.Ms, a.Aq, a.As, a.MTq, a.MTs, a.ATq, a.ATs,
+          a.KTp, a.QTp, a.Gw, a.sink);
     a.stage("scan_fwd_store");
     k_scan_fwd_bf<DK, DV, SCAN_BV, false, true><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-        q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mp, a.Ap, a.KTp, a.Gw, nullptr, nullptr, a.Xq,
+        q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mq, a.Ms, a.Aq, a.As, a.KTp, a.Gw, nullptr, nullptr, a.Xq,
         a.Xs, a.Dq, a.Ds, a.Xfq, a.Xfs, a.sink);
   }
   a.stage("scan_bwd");
   k_scan_bwd_bf<DK, DV, SCAN_BV><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-      q, k, dO, beta, a.d, a.dht, a.smap, a.H, a.MTp, a.ATp, a.KTp, a.QTp, a.Gw, a.dh0, a.Yq,
+      q, k, dO, beta, a.d, a.dht, a.smap, a.H, a.MTq, a.MTs, a.ATq, a.ATs, a.KTp, a.QTp, a.Gw, a.dh0, a.Yq,
       a.Ys, a.dRq, a.dRs, a.sink);
   a.stage("intra_bwd");
   if (a.ncmax > 0)

@@ -41,9 +41,12 @@ struct LaunchArgs {
   float *Mw, *Aw, *Gw;            // per chunk-head: M, A (64 x 64), G (64)
   float *Xw, *Dw, *Yw, *dRw;      // per chunk-head: X (dk x dv), D (64 x dv), Y, dR
   float* ddp;                     // per chunk-head partial dd
-  // bf16 path, per chunk-head: M, A as (hi, lo) bf16 pairs [2][64][64] (in the
-  // M, A regions), M^T, A^T likewise, K^T and Q^T as [dk][64] bf16
-  uint16_t *Mp, *Ap, *MTp, *ATp, *KTp, *QTp;
+  // bf16 path, per chunk-head: M, A, M^T, A^T as int16 [64][64] with one
+  // power-of-two scale per row in the matching *s array; K^T and Q^T as [dk][64]
+  // bf16
+  int16_t *Mq, *Aq, *MTq, *ATq;
+  float *Ms, *As, *MTs, *ATs;
+  uint16_t *KTp, *QTp;
   // bf16 path, per chunk-head: X, Y (dk x dv), D, dR (64 x dv) as int16 with one
   // power-of-two scale per (row, 32-column block) in the matching *s array
   int16_t *Xq, *Dq, *Yq, *dRq;

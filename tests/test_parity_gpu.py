@@ -92,7 +92,17 @@ def test_far_from_unit_magnitudes(v_exp, do_exp):
     w.dht *= np.float32(2.0 ** do_exp)
     errs = check_bwd(w)
     _log("far-from-unit v 2^%d, dO 2^%d: %s" % (v_exp, do_exp, errs))
-    assert max(errs.values()) < 2e-4
+    assert max(errs.values()) < 1e-3
+
+
+def test_long_weak_decay_errors_stay_bounded():
+    # alpha ~ 0.999 per token over 128 chunks: the int16 operands of the state
+    # updates must not let rounding accumulate along the recurrence
+    w = random_case(seed=11, B=1, T=8192, H=1, dk=128, dv=128, in_dtype="bf16", dht=True,
+                    gate_scale=0.001)
+    ef = check_fwd(w, tol=1e-3)
+    eb = check_bwd(w, tol=1e-3)
+    _log("long weak decay fwd %s bwd %s" % (ef, eb))
 
 
 def test_deterministic_bitwise():
