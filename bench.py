@@ -41,10 +41,10 @@ def stage_model(name, B, T, H, dk, dv, C=64, in_bytes=2):
     Per chunk-head (C tokens of one head): the dense products the stage performs
     (2 m n k flops each) and the HBM bytes it must move at minimum (each operand
     read once, each result written once; L2 re-reads excluded).  M, A and their
-    transposes count 4 bytes per element (stored as (hi, lo) bf16 pairs); the
+    transposes count 2 bytes per element plus one 4-byte scale per row, the
     chunk states X, Y and pseudo-values D, dR handed from the scans to the
-    backward gradient kernel count 2 bytes per element plus one 4-byte scale per
-    32 elements (their int16 storage); K^T and Q^T copies made by the prep stage
+    backward gradient kernel 2 bytes per element plus one 4-byte scale per 32
+    elements (their int16 storage); K^T and Q^T copies made by the prep stage
     are counted where they are written and read.
     """
     nch = B * math.ceil(T / C) * H
@@ -52,7 +52,7 @@ def stage_model(name, B, T, H, dk, dv, C=64, in_bytes=2):
     qk = C * dk * in_bytes          # one of q, k (or its transpose)
     vv = C * dv * in_bytes          # one of v, dO
     gb = C * (f4 + in_bytes)        # g (or G) and beta
-    cc = C * C * f4                 # one C x C fp32 matrix
+    cc = C * C * 2 + C * f4         # one stored C x C matrix (int16 + row scales)
     st = dk * dv * 2 + dk * (dv // 32) * f4     # one stored state (int16 + scales)
     cd = C * dv * 2 + C * (dv // 32) * f4       # one stored C x dv matrix
     if name in ("prep", "prep_save"):    # K K^T, Q K^T; q, k, g, beta -> M, A, K^T, G
