@@ -895,6 +895,64 @@ __device__ __forceinline__ void put_t4(bf16_t* hi, bf16_t* lo, int off, const fl
   *reinterpret_cast<bf16x4*>(lo + off) = l;
 }
 
+// Block column J of M = (I + L)^{-1} below the diagonal, in the accumulator
+// layout of the 16x16 fp32 MFMA: on entry mb[J] = D_J; on exit mb[i] = M_iJ for
+// i > J.  The L_ik and D_i blocks come from LDS (row-major, stride LDL, D_i in
+// the diagonal blocks).  Each product runs its k index in the order
+// 4 (lane / 16) + e at step e, so that an accumulator is directly the B operand
+// of the next product and the A operand of a step is one 16-byte LDS read.
+template <int J, int LDL>
+__device__ __forceinline__ void solve_block_column(const float* Ls, floatx4 (&mb)[4]) {
+  const int lane = lane_id(), r16 = lane & 15, g4 = lane >> 4;
+#pragma unroll
+  for (int i = J + 1; i < 4; ++i) {
+    floatx4 t = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = J; kb < i; ++kb) {
+      const float4 a = *reinterpret_cast<const float4*>(Ls + (16 * i + r16) * LDL + 16 * kb + 4 * g4);
+      t = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, mb[kb][0], t, 0, 0, 0);
+      t = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, mb[kb][1], t, 0, 0, 0);
+      t = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, mb[kb][2], t, 0, 0, 0);
+      t = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, mb[kb][3], t, 0, 0, 0);
+    }
+    const float4 dd = *reinterpret_cast<const float4*>(Ls + (16 * i + r16) * LDL + 16 * i + 4 * g4);
+    floatx4 u = {0.f, 0.f, 0.f, 0.f};
+    u = __builtin_amdgcn_mfma_f32_16x16x4f32(dd.x, t[0], u, 0, 0, 0);
+    u = __builtin_amdgcn_mfma_f32_16x16x4f32(dd.y, t[1], u, 0, 0, 0);
+    u = __builtin_amdgcn_mfma_f32_16x16x4f32(dd.z, t[2], u, 0, 0, 0);
+    u = __builtin_amdgcn_mfma_f32_16x16x4f32(dd.w, t[3], u, 0, 0, 0);
+    mb[i] = -u;
+  }
+}
+
+// Block column J of M (mb as left by solve_block_column) into LDS over L, and
+// with BWD the rows 16 J .. 16 J + 15 of M^T (= columns of M) as int16 with
+// one scale per row: lane (g4, r16) holds rows 4 g4 .. 4 g4 + 3 of every
+// block of column 16 J + r16, i.e. 8-byte pieces of row 16 J + r16 of M^T.
+template <int J, int LDL, bool BWD>
+__device__ __forceinline__ void put_block_column(float* Ls, const floatx4 (&mb)[4], int16_t* Mt,
+                                                 float* MTs, float* sink) {
+  const int lane = lane_id(), r16 = lane & 15, g4 = lane >> 4;
+#pragma unroll
+  for (int i = J + 1; i < 4; ++i)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) Ls[(16 * i + 4 * g4 + e) * LDL + 16 * J + r16] = mb[i][e];
+  if constexpr (BWD) {
+    float m = 0.f;
+#pragma unroll
+    for (int i = J; i < 4; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) m = fmaxf(m, fabsf(mb[i][e]));
+    m = fmaxf(m, __shfl_xor(m, 16));
+    m = fmaxf(m, __shfl_xor(m, 32));
+    const float inv = q_inv_scale(m);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      *reinterpret_cast<uint2*>(Mt + 16 * i + 4 * g4) = i < J ? make_uint2(0u, 0u) : q_pack4(mb[i], inv);
+    *(g4 == 0 ? MTs + 16 * J + r16 : sink + lane) = q_scale(m);
+  }
+}
+
 template <int DK, bool BWD>
 __global__ __launch_bounds__(NTHR) void k_prep_bf(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const float* __restrict__ g,
@@ -1000,57 +1058,73 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
     }
   }
 
-  if (w == 0) {
-    // M = (I + L)^{-1}: lane j solves column j by forward substitution in fp32,
-    // x_i = -sum_{m < i} L_im x_m (x_j = 1, x_i = 0 for i < j); four partial
-    // sums per row shorten the dependency chain.
-    const int j = lane;
-    float x[CH];
+  // M = (I + L)^{-1} by 16x16 blocks (L is strictly lower triangular, so M is
+  // unit lower triangular).  Wave w owns block column jb: it inverts the
+  // diagonal block, D_jb = (I + L_jb,jb)^{-1}, then walks down its block column
+  // with M_ij = -D_i sum_{j <= k < i} L_ik M_kj.  Block columns do not depend
+  // on one another; the rotation spreads the longest column (jb = 0) over the
+  // SIMDs of workgroups that share a CU.
+  const int jb = (w + blockIdx.x + blockIdx.y) & (NWAVE - 1);
+  floatx4 mb[4];
+  {
+    // lane (g4, r16) solves column r16 of the diagonal block by forward
+    // substitution in fp32 (the four 16-lane groups redundantly)
+    float* Lb = Ls + 16 * jb * LDL + 16 * jb;
+    float x[16];
 #pragma unroll
-    for (int i = 0; i < CH; ++i) x[i] = (i == j) ? 1.f : 0.f;
+    for (int i = 0; i < 16; ++i) x[i] = (i == r16) ? 1.f : 0.f;
 #pragma unroll
-    for (int i = 1; i < CH; ++i) {
+    for (int i = 1; i < 16; ++i) {
       float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
 #pragma unroll
       for (int m = 0; m < i; m += 4) {
-        const float4 lv = *reinterpret_cast<const float4*>(Ls + i * LDL + m);
+        const float4 lv = *reinterpret_cast<const float4*>(Lb + i * LDL + m);
         s0 += lv.x * x[m];
         if (m + 1 < i) s1 += lv.y * x[m + 1];
         if (m + 2 < i) s2 += lv.z * x[m + 2];
         if (m + 3 < i) s3 += lv.w * x[m + 3];
       }
-      const float sum = (s0 + s1) + (s2 + s3);
-      if (i > j) x[i] = -sum;
+      if (i > r16) x[i] = -((s0 + s1) + (s2 + s3));
     }
-    // column j of M into LDS (wave 0 is the only reader of L and is done with
-    // it); the rows are written out below by the whole workgroup
+    // D_jb in the accumulator layout (rows 4 g4 + e of column r16) replaces
+    // L_jb,jb in LDS; only this wave reads that block, and its reads are done
+    floatx4 dm;
 #pragma unroll
-    for (int i = 0; i < CH; ++i) Ls[i * LDL + j] = x[i];
-    if constexpr (BWD) {
-      // M^T row j = column j of M, straight from registers
-      float m = 0.f;
-#pragma unroll
-      for (int i = 0; i < CH; ++i) m = fmaxf(m, fabsf(x[i]));
-      const float inv = q_inv_scale(m);
-      int16_t* Mt = MTq + chh * CC + (long)j * CH;
-#pragma unroll
-      for (int i = 0; i < CH; i += 8) {
-        const float xv[8] = {x[i], x[i + 1], x[i + 2], x[i + 3], x[i + 4], x[i + 5], x[i + 6], x[i + 7]};
-        *reinterpret_cast<uint4*>(Mt + i) = q_pack8(xv, inv);
-      }
-      MTs[chh * CH + j] = q_scale(m);
+    for (int e = 0; e < 4; ++e) {
+      dm[e] = g4 == 0 ? x[e] : g4 == 1 ? x[4 + e] : g4 == 2 ? x[8 + e] : x[12 + e];
+      Lb[(4 * g4 + e) * LDL + r16] = dm[e];
     }
-  } else {
-    // waves 1..3: K^T (and Q^T) per chunk-head, [dk][64] bf16.  One transposing
-    // LDS read pair gives lane (g, i) the 8 rows 32 tb + 8 g .. of column c0 + i,
-    // i.e. one 16-byte piece of row c0 + i of K^T.
+    mb[0] = mb[1] = mb[2] = mb[3] = dm;
+  }
+  __syncthreads();
+  switch (jb) {
+    case 0: solve_block_column<0, LDL>(Ls, mb); break;
+    case 1: solve_block_column<1, LDL>(Ls, mb); break;
+    case 2: solve_block_column<2, LDL>(Ls, mb); break;
+    default: break;
+  }
+  if (jb != 0) {
+    // the waves with shorter block columns: K^T (and Q^T) per chunk-head,
+    // [dk][64] bf16.  One transposing LDS read pair gives lane (g, i) the 8 rows
+    // 32 tb + 8 g .. of column c0 + i, i.e. one 16-byte piece of row c0 + i of K^T.
     bf16_t* Kt = KTp + chh * DK * CH;
     bf16_t* Qt = BWD ? QTp + chh * DK * CH : nullptr;
-    for (int ci = w - 1; ci < 2 * (DK / 16); ci += NWAVE - 1) {
+    for (int ci = NWAVE - 1 - jb; ci < 2 * (DK / 16); ci += NWAVE - 1) {
       const int c0 = 16 * (ci % (DK / 16)), r0 = 32 * (ci / (DK / 16)) + 8 * g4;
       const long off = (long)(c0 + (lane & 15)) * CH + r0;
       *reinterpret_cast<bf16x8*>(Kt + off) = ld_tr8(Ks, LDK, r0, c0);
       if constexpr (BWD) *reinterpret_cast<bf16x8*>(Qt + off) = ld_tr8(Qs, LDK, r0, c0);
+    }
+  }
+  __syncthreads();  // every read of L is done
+  {
+    int16_t* Mt = BWD ? MTq + chh * CC + (long)(16 * jb + r16) * CH : nullptr;
+    float* Mts = BWD ? MTs + chh * CH : nullptr;
+    switch (jb) {
+      case 0: put_block_column<0, LDL, BWD>(Ls, mb, Mt, Mts, sink); break;
+      case 1: put_block_column<1, LDL, BWD>(Ls, mb, Mt, Mts, sink); break;
+      case 2: put_block_column<2, LDL, BWD>(Ls, mb, Mt, Mts, sink); break;
+      default: put_block_column<3, LDL, BWD>(Ls, mb, Mt, Mts, sink); break;
     }
   }
   __syncthreads();
