@@ -966,9 +966,13 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
   constexpr int LDK = DK + 8;
   constexpr int LDL = CH + 4;
   constexpr int CC = CH * CH;
+  // the Q tile is dead once K^T, Q^T and Q K^T are taken: L (then M) reuses
+  // its LDS, which keeps four workgroups on a CU
+  constexpr int QLB = CH * LDL * 4 > CH * LDK * 2 ? CH * LDL * 4 : CH * LDK * 2;
   __shared__ __align__(16) bf16_t Ks[CH * LDK];
-  __shared__ __align__(16) bf16_t Qs[CH * LDK];
-  __shared__ __align__(16) float Ls[CH * LDL];
+  __shared__ __align__(16) unsigned char QLbuf[QLB];
+  bf16_t* Qs = reinterpret_cast<bf16_t*>(QLbuf);
+  float* Ls = reinterpret_cast<float*>(QLbuf);
   __shared__ float Gs[CH], Bs[CH];
   __shared__ float colmax[BWD ? NWAVE : 1][CH];  // per-wave column maxima of |A|
 
@@ -978,6 +982,7 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
   const long chh = (long)blockIdx.x * H + h;
   const long tok = (long)ci.tok0 * H + h;
   const int w = wave_id(), lane = lane_id(), g4 = lane >> 4, r16 = lane & 15;
+  const float dh = d[h];
   {
     TileRegs<bf16_t, CH, DK> kr, qr;
     kr.load(k + tok * DK, (long)H * DK, ci.len);
@@ -993,13 +998,26 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
     Gw[chh * CH + lane] = G;
   }
   __syncthreads();
+  {
+    // K^T (and Q^T) per chunk-head, [dk][64] bf16.  One transposing LDS read
+    // pair gives lane (g, i) the 8 rows 32 tb + 8 g .. of column c0 + i, i.e.
+    // one 16-byte piece of row c0 + i of K^T.
+    bf16_t* Kt = KTp + chh * DK * CH;
+    bf16_t* Qt = BWD ? QTp + chh * DK * CH : nullptr;
+    for (int pc = w; pc < 2 * (DK / 16); pc += NWAVE) {
+      const int c0 = 16 * (pc % (DK / 16)), r0 = 32 * (pc / (DK / 16)) + 8 * g4;
+      const long off = (long)(c0 + (lane & 15)) * CH + r0;
+      *reinterpret_cast<bf16x8*>(Kt + off) = ld_tr8(Ks, LDK, r0, c0);
+      if constexpr (BWD) *reinterpret_cast<bf16x8*>(Qt + off) = ld_tr8(Qs, LDK, r0, c0);
+    }
+  }
 
   floatx4 akk[1][4], aqk[1][4];
   zero_acc(akk);
   zero_acc(aqk);
   mma<false, 1, 4, DK>(akk, Ks + 16 * w * LDK, LDK, Ks, LDK);
   mma<false, 1, 4, DK>(aqk, Qs + 16 * w * LDK, LDK, Ks, LDK);
-  const float dh = d[h];
+  __syncthreads();  // every read of the Q tile is done: L overwrites it
   // A in the accumulator layout: av[nt][e] = A[16w + 4g4 + e][16nt + r16]
   float av[4][4], rmax[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -1102,19 +1120,6 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
     case 1: solve_block_column<1, LDL>(Ls, mb); break;
     case 2: solve_block_column<2, LDL>(Ls, mb); break;
     default: break;
-  }
-  if (jb != 0) {
-    // the waves with shorter block columns: K^T (and Q^T) per chunk-head,
-    // [dk][64] bf16.  One transposing LDS read pair gives lane (g, i) the 8 rows
-    // 32 tb + 8 g .. of column c0 + i, i.e. one 16-byte piece of row c0 + i of K^T.
-    bf16_t* Kt = KTp + chh * DK * CH;
-    bf16_t* Qt = BWD ? QTp + chh * DK * CH : nullptr;
-    for (int ci = NWAVE - 1 - jb; ci < 2 * (DK / 16); ci += NWAVE - 1) {
-      const int c0 = 16 * (ci % (DK / 16)), r0 = 32 * (ci / (DK / 16)) + 8 * g4;
-      const long off = (long)(c0 + (lane & 15)) * CH + r0;
-      *reinterpret_cast<bf16x8*>(Kt + off) = ld_tr8(Ks, LDK, r0, c0);
-      if constexpr (BWD) *reinterpret_cast<bf16x8*>(Qt + off) = ld_tr8(Qs, LDK, r0, c0);
-    }
   }
   __syncthreads();  // every read of L is done
   {
