@@ -352,6 +352,23 @@ struct TileRegs {
       r[it] = val;
     }
   }
+  // The same tile through raw buffer loads whose record count ends at row
+  // rows - 1: the hardware returns zeros past it, so there is no per-row branch
+  // (a branch around a load leaves a copy of its result that waits for it at
+  // once).  g is 4-byte aligned; the tile's byte extent fits in 32 bits.
+  __device__ __forceinline__ void load_clip(const T* __restrict__ g, long gs, int rows) {
+    const int nbytes = rows > 0 ? (int)(((long)(rows - 1) * gs + COLS) * (long)sizeof(T)) : 0;
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(g), 0, nbytes, 0x00020000);
+#pragma unroll
+    for (int it = 0; it < ITER; ++it) {
+      const int idx = threadIdx.x + it * NTHR;
+      const int rr = idx / PER_ROW, cc = (idx % PER_ROW) * V;
+      // rows at or past NROWS (idx >= TOTAL) fall past the record count too (gs >= COLS)
+      const unsigned off = (unsigned)(((long)rr * gs + cc) * (long)sizeof(T));
+      r[it] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
+    }
+  }
   __device__ __forceinline__ void store(T* s, int ld) const {
 #pragma unroll
     for (int it = 0; it < ITER; ++it) {

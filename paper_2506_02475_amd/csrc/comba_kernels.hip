@@ -984,18 +984,20 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
   const int w = wave_id(), lane = lane_id(), g4 = lane >> 4, r16 = lane & 15;
   const float dh = d[h];
   {
+    // every load is unconditional (clamped rows, zeroed where used): a branch
+    // around a load makes the wave wait for it on the spot
+    const long grow = tok + (long)min(lane, ci.len - 1) * H;
+    const float g_in = g[grow], b_in = bf2f(beta[grow]);
     TileRegs<bf16_t, CH, DK> kr, qr;
-    kr.load(k + tok * DK, (long)H * DK, ci.len);
-    qr.load(q + tok * DK, (long)H * DK, ci.len);
+    kr.load_clip(k + tok * DK, (long)H * DK, ci.len);
+    qr.load_clip(q + tok * DK, (long)H * DK, ci.len);
+    // every wave forms G and writes the same Gs, Bs (no branch around the uses)
+    const float G = wave_prefix_sum(lane < ci.len ? g_in : 0.f);
+    Gs[lane] = G;
+    Bs[lane] = lane < ci.len ? b_in : 0.f;
+    if (w == 0) Gw[chh * CH + lane] = G;
     kr.store(Ks, LDK);
     qr.store(Qs, LDK);
-  }
-  if (w == 0) {
-    const float gr = lane < ci.len ? g[tok + (long)lane * H] : 0.f;
-    const float G = wave_prefix_sum(gr);
-    Gs[lane] = G;
-    Bs[lane] = lane < ci.len ? bf2f(beta[tok + (long)lane * H]) : 0.f;
-    Gw[chh * CH + lane] = G;
   }
   __syncthreads();
   {
@@ -1879,10 +1881,6 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
   const int rt = w & 3, ch = w >> 2;
   const int len = ci.len;
   const float dh = d[h];
-  if (tid < CH) {
-    Gs[tid] = Gw[chh * CH + tid];
-    Bs[tid] = tid < len ? bf2f(beta[tok + (long)tid * H]) : 0.f;
-  }
 
   // ---------------- phase 1 ----------------
   bf16_t* dOb = reinterpret_cast<bf16_t*>(smem);
@@ -1923,11 +1921,14 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
       s_x[p] = Xs[xrow * NB + vb];
       s_y[p] = Ys[xrow * NB + vb];
     }
+    // keep the loads here: the scheduler otherwise sinks some of them to their
+    // use one block later, where they are waited for at once
+    __builtin_amdgcn_sched_barrier(0);
   };
   float Fpart = 0.f, bv = 0.f;
   auto put = [&](int vb) {
     const int j = vb * VB;
-    *reinterpret_cast<uint4*>(dOb + po_r * LDB + po_c) = po_r < len ? r_do : make_uint4(0, 0, 0, 0);
+    *reinterpret_cast<uint4*>(dOb + po_r * LDB + po_c) = r_do;
     bf16x4 hh, ll;
     const float4 fdr = q_unpack4(r_dr, s_dr);
     split4v(fdr, hh, ll);
@@ -1969,18 +1970,35 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
   dA[0] = dA[1] = dL[0] = dL[1] = zero4();
   TileRegs<bf16_t, CH, DK, IB_THR> kr, qr;
   issue(0);
+  // gates and beta after the first block's loads, unconditional (clamped rows)
+  const float g_in = Gw[chh * CH + (tid & (CH - 1))];
+  const float b_in = bf2f(beta[tok + (long)min(tid & (CH - 1), len - 1) * H]);
+  // unrolled: a rolled loop carries the prefetched registers through copies at
+  // the back edge, which wait for the loads just issued
+#pragma unroll
   for (int vb = 0; vb < NVB; ++vb) {
+    // the scheduler would hoist put's dequantisation across the barrier into
+    // the previous block's MFMAs, waiting there for the loads just issued
+    __builtin_amdgcn_sched_barrier(0);
+    if (vb == 0 && tid < CH) {
+      Gs[tid] = g_in;
+      Bs[tid] = tid < len ? b_in : 0.f;
+    }
     __syncthreads();
     put(vb);
     __syncthreads();
     if (vb + 1 < NVB) {
       issue(vb + 1);
     } else {
-      kr.load(k + tok * DK, (long)H * DK, len);
-      qr.load(q + tok * DK, (long)H * DK, len);
+      kr.load_clip(k + tok * DK, (long)H * DK, len);
+      qr.load_clip(q + tok * DK, (long)H * DK, len);
     }
     const int arow = (16 * rt + r16) * LDB + 8 * g4;
-    const bf16x8 a_do = ld8(dOb + arow), a_drh = ld8(dRh + arow), a_drl = ld8(dRl + arow);
+    // dO rows past the chunk end hold row len - 1 (clamped loads): zero them
+    // here, where dO is an MFMA A operand, not on the load's path
+    bf16x8 a_do = ld8(dOb + arow);
+    if (16 * rt + r16 >= len) a_do = bf16x8{};
+    const bf16x8 a_drh = ld8(dRh + arow), a_drl = ld8(dRl + arow);
     const bf16x8 a_dh = ld8(Dh + arow), a_dl = ld8(Dl + arow);
 #pragma unroll
     for (int j = 0; j < NTW; ++j) {
