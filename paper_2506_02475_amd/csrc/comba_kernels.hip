@@ -1826,10 +1826,11 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
 // k_intra_bwd_bf: per chunk-head gradients for bf16 inputs, 8 wavefronts.
 // Wave w works on row tile rt = w % 4 (rows 16 rt .. 16 rt + 15) and column
 // half ch = w / 4 of every chunk product.  Phase 1 streams dv in blocks of 32
-// (prefetched one block ahead; fp32 operands are split into bf16 hi/lo once,
-// when staged into LDS) and accumulates T1 = dO X^T, T3 = dR X^T, T2 = D Y^T,
-// dA = dO D^T, dL = dR D^T.  Phase 2 forms dQ~ and dK, with the K^T and Q^T
-// B-operands read straight from the prep output.
+// (prefetched one block ahead; the int16 operands are dequantised and split
+// into bf16 hi/lo once, when staged into LDS) and accumulates T1 = dO X^T,
+// T3 = dR X^T, T2 = D Y^T, dA = dO D^T, dL = dR D^T.  The K and Q tiles are
+// loaded with the first block into LDS of their own; phase 2 forms dQ~ and dK
+// from them (K^T, Q^T B-operands by transposing LDS reads).
 // ---------------------------------------------------------------------------
 constexpr int IB_THR = 512;
 
