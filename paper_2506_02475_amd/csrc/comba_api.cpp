@@ -59,7 +59,7 @@ comba_status check_shape(const comba_shape* s, Dims* out) {
 }
 
 struct Layout {
-  size_t cmap, smap, M, A, G, X, D, Y, dR, ddp, MT, AT, KT, QT, Xfin, sink, total;
+  size_t cmap, smap, M, A, G, X, D, Y, dR, ddp, MT, AT, QT, Xfin, sink, total;
   size_t Xs, Ds, Ys, dRs, Xfs;  // bf16 path: scales of the int16 X, D, Y, dR, final-state sink
   size_t Ms, As, MTs, ATs;       // bf16 path: row scales of the int16 M, A, M^T, A^T
 };
@@ -78,13 +78,12 @@ Layout layout(const Dims& d, bool bwd) {
   L.smap = take((size_t)(d.N > 0 ? d.N : 1) * sizeof(comba::SeqInfo));
   L.G = take(chh * kChunk * sizeof(float));
   if (d.bf16) {
-    // bf16 path: M, A as int16 with row scales; K^T per chunk; the backward
+    // bf16 path: M, A as int16 with row scales; the backward
     // also keeps M^T, A^T (int16 + row scales) and Q^T
     L.M = take(chh * kChunk * kChunk * sizeof(int16_t));
     L.Ms = take(chh * kChunk * sizeof(float));
     L.A = take(chh * kChunk * kChunk * sizeof(int16_t));
     L.As = take(chh * kChunk * sizeof(float));
-    L.KT = take(chh * d.dk * kChunk * sizeof(uint16_t));
     if (bwd) {
       // M^T, A^T, Q^T; X, D, Y, dR as int16 + one fp32 scale per 32 values
       const size_t nf = (size_t)(d.N > 0 ? d.N : 1) * d.H;
@@ -171,7 +170,6 @@ void carve(comba::LaunchArgs& a, const Layout& L, void* ws, bool bwd) {
     a.Ms = reinterpret_cast<float*>(base + L.Ms);
     a.Aq = reinterpret_cast<int16_t*>(base + L.A);
     a.As = reinterpret_cast<float*>(base + L.As);
-    a.KTp = reinterpret_cast<uint16_t*>(base + L.KT);
     if (bwd) {
       a.MTq = reinterpret_cast<int16_t*>(base + L.MT);
       a.MTs = reinterpret_cast<float*>(base + L.MTs);

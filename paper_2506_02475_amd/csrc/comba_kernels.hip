@@ -959,8 +959,8 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
     const bf16_t* __restrict__ beta, const float* __restrict__ d, const ChunkInfo* __restrict__ cmap,
     int H, int16_t* __restrict__ Mq, float* __restrict__ Ms, int16_t* __restrict__ Aq,
     float* __restrict__ As, int16_t* __restrict__ MTq, float* __restrict__ MTs,
-    int16_t* __restrict__ ATq, float* __restrict__ ATs, bf16_t* __restrict__ KTp,
-    bf16_t* __restrict__ QTp, float* __restrict__ Gw, float* __restrict__ sink) {
+    int16_t* __restrict__ ATq, float* __restrict__ ATs, bf16_t* __restrict__ QTp,
+    float* __restrict__ Gw, float* __restrict__ sink) {
   // M, A (and M^T, A^T) leave as int16 rows with one power-of-two scale per row
   // (see q_pack4): the scans fold the scale into their accumulator rows
   constexpr int LDK = DK + 8;
@@ -1000,17 +1000,14 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
     qr.store(Qs, LDK);
   }
   __syncthreads();
-  {
-    // K^T (and Q^T) per chunk-head, [dk][64] bf16.  One transposing LDS read
-    // pair gives lane (g, i) the 8 rows 32 tb + 8 g .. of column c0 + i, i.e.
-    // one 16-byte piece of row c0 + i of K^T.
-    bf16_t* Kt = KTp + chh * DK * CH;
-    bf16_t* Qt = BWD ? QTp + chh * DK * CH : nullptr;
+  if constexpr (BWD) {
+    // Q^T per chunk-head, [dk][64] bf16, for the reverse scan.  One transposing
+    // LDS read pair gives lane (g, i) the 8 rows 32 tb + 8 g .. of column c0 + i,
+    // i.e. one 16-byte piece of row c0 + i of Q^T.
+    bf16_t* Qt = QTp + chh * DK * CH;
     for (int pc = w; pc < 2 * (DK / 16); pc += NWAVE) {
       const int c0 = 16 * (pc % (DK / 16)), r0 = 32 * (pc / (DK / 16)) + 8 * g4;
-      const long off = (long)(c0 + (lane & 15)) * CH + r0;
-      *reinterpret_cast<bf16x8*>(Kt + off) = ld_tr8(Ks, LDK, r0, c0);
-      if constexpr (BWD) *reinterpret_cast<bf16x8*>(Qt + off) = ld_tr8(Qs, LDK, r0, c0);
+      *reinterpret_cast<bf16x8*>(Qt + (long)(c0 + (lane & 15)) * CH + r0) = ld_tr8(Qs, LDK, r0, c0);
     }
   }
 
@@ -1161,8 +1158,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     const bf16_t* __restrict__ beta, const float* __restrict__ d, const float* __restrict__ h0,
     const SeqInfo* __restrict__ smap, int H, const int16_t* __restrict__ Mq,
     const float* __restrict__ Ms, const int16_t* __restrict__ Aq, const float* __restrict__ As,
-    const bf16_t* __restrict__ KTp, const float* __restrict__ Gw,
-    float* __restrict__ o, float* __restrict__ ht, int16_t* __restrict__ Xq,
+    const float* __restrict__ Gw, float* __restrict__ o, float* __restrict__ ht, int16_t* __restrict__ Xq,
     float* __restrict__ Xs, int16_t* __restrict__ Dq, float* __restrict__ Ds,
     int16_t* __restrict__ Xfq, float* __restrict__ Xfs, float* __restrict__ sink) {
   // Every global load and store inside the chunk loop is issued unconditionally
@@ -1180,6 +1176,10 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
   __shared__ __align__(16) bf16_t DgTl[BV * LDR];
   __shared__ __align__(16) bf16_t DTh[OUT ? BV * LDR : 8];
   __shared__ __align__(16) bf16_t DTl[OUT ? BV * LDR : 8];
+  // the chunk's K rows, staged from the K operand registers: the state update
+  // takes its K^T operand from here with transposing reads
+  constexpr int LDKC = DK + 8;
+  __shared__ __align__(16) bf16_t Kc[CH * LDKC];
 
   const int s = blockIdx.x, h = blockIdx.y, j0 = blockIdx.z * BV;
   const SeqInfo si = smap[s];
@@ -1242,10 +1242,10 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
   auto c_tok = [&](int cc) { return (long)(si.tok0 + cc * CH) * H + h; };
   auto c_chh = [&](int cc) { return (long)(si.chunk0 + cc) * H + h; };
 
-  // per-chunk operands, loaded one chunk ahead: K, Q rows and K^T as bf16, the
-  // rows of M and A as int16 with their row scales (applied to the accumulator
-  // rows: (M R)[r] = s_r sum_i q[r][i] R[i])
-  bf16x8 kf[KS], qf[KS], ktf[XMT][2];
+  // per-chunk operands, loaded one chunk ahead: K, Q rows as bf16, the rows of
+  // M and A as int16 with their row scales (applied to the accumulator rows:
+  // (M R)[r] = s_r sum_i q[r][i] R[i])
+  bf16x8 kf[KS], qf[KS];
   uint4 mq[2], aq[2];
   float4 msc, asc;
   // per-row values of the chunk (cumulative gates G, beta, the V slice) are
@@ -1287,13 +1287,6 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
       if constexpr (OUT) qf[ks] = ld8(q + rb + 32 * ks);
     }
   };
-  auto load_kt = [&](int cc) {
-    const bf16_t* p = KTp + c_chh(cc) * DK * CH + ((DK / 4) * w + r16) * CH + 8 * g4;
-#pragma unroll
-    for (int mt = 0; mt < XMT; ++mt)
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks) ktf[mt][ks] = ld8(p + 16 * mt * CH + 32 * ks);
-  };
   auto load_m = [&](int cc) {
     const int16_t* p = Mq + c_chh(cc) * CC + prow * CH + 8 * g4;
 #pragma unroll
@@ -1308,7 +1301,6 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
   };
   if (n > 0) {
     load_kq(0);
-    load_kt(0);
     load_m(0);
     if constexpr (OUT) load_a(0);
     load_rows(0);
@@ -1354,6 +1346,9 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
           qx[nt] = mfma16(qf[ks], xl, qx[nt]);
         }
       }
+    // K rows past the chunk end repeat row len - 1; D is zero there
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) *reinterpret_cast<bf16x8*>(Kc + prow * LDKC + 32 * ks + 8 * g4) = kf[ks];
     load_kq(nx);
     floatx4 oacc[NTV];
 #pragma unroll
@@ -1435,18 +1430,22 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt) X[mt][nt] *= gC;
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
+    for (int ks = 0; ks < 2; ++ks) {
+      // K^T rows (DK/4) w + 16 mt + i, chunk rows 32 ks + 8 g4 ..
+      bf16x8 ktf[XMT];
+#pragma unroll
+      for (int mt = 0; mt < XMT; ++mt) ktf[mt] = ld_tr8(Kc, LDKC, 32 * ks + 8 * g4, (DK / 4) * w + 16 * mt);
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt) {
         const int off = (16 * nt + r16) * LDR + 32 * ks + 8 * g4;
         const bf16x8 dh_ = ld8(DgTh + off), dl_ = ld8(DgTl + off);
 #pragma unroll
         for (int mt = 0; mt < XMT; ++mt) {
-          X[mt][nt] = mfma16(ktf[mt][ks], dh_, X[mt][nt]);
-          X[mt][nt] = mfma16(ktf[mt][ks], dl_, X[mt][nt]);
+          X[mt][nt] = mfma16(ktf[mt], dh_, X[mt][nt]);
+          X[mt][nt] = mfma16(ktf[mt], dl_, X[mt][nt]);
         }
       }
-    load_kt(nx);
+    }
 
     // O = Diag(exp G)(Q - d K) X + A D
     if constexpr (OUT) {
@@ -1502,7 +1501,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     const bf16_t* __restrict__ beta, const float* __restrict__ d, const float* __restrict__ dht,
     const SeqInfo* __restrict__ smap, int H, const int16_t* __restrict__ MTq,
     const float* __restrict__ MTs, const int16_t* __restrict__ ATq, const float* __restrict__ ATs,
-    const bf16_t* __restrict__ KTp, const bf16_t* __restrict__ QTp,
+    const bf16_t* __restrict__ QTp,
     const float* __restrict__ Gw, float* __restrict__ dh0, int16_t* __restrict__ Yq,
     float* __restrict__ Ys, int16_t* __restrict__ dRq, float* __restrict__ dRs,
     float* __restrict__ sink) {
@@ -1582,7 +1581,11 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
   auto c_chh = [&](int cc) { return (long)(si.chunk0 + cc) * H + h; };
 
   // A^T, M^T rows as int16 with their row scales (applied to the accumulator rows)
-  bf16x8 kf[KS], qtf[XMT][2], ktf[XMT][2];
+  bf16x8 kf[KS], qtf[XMT][2];
+  // the chunk's K rows, staged from the K operand registers: the state update
+  // takes its K^T operand from here with transposing reads
+  constexpr int LDKC = DK + 8;
+  __shared__ __align__(16) bf16_t Kc[CH * LDKC];
   uint4 atq[2], mtq[2];
   float4 atsc, mtsc;
   // per-row values (G, beta) and the dO slice are loaded one chunk ahead into
@@ -1611,15 +1614,12 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     for (int ks = 0; ks < 2; ++ks) mtq[ks] = *reinterpret_cast<const uint4*>(p + 32 * ks);
     mtsc = *reinterpret_cast<const float4*>(MTs + c_chh(cc) * CH + 16 * w + 4 * g4);
   };
-  auto load_qkt = [&](int cc) {
+  auto load_qt = [&](int cc) {
     const long base = c_chh(cc) * DK * CH + ((DK / 4) * w + r16) * CH + 8 * g4;
 #pragma unroll
     for (int mt = 0; mt < XMT; ++mt)
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        qtf[mt][ks] = ld8(QTp + base + 16 * mt * CH + 32 * ks);
-        ktf[mt][ks] = ld8(KTp + base + 16 * mt * CH + 32 * ks);
-      }
+      for (int ks = 0; ks < 2; ++ks) qtf[mt][ks] = ld8(QTp + base + 16 * mt * CH + 32 * ks);
   };
   auto load_rows = [&](int cc) {
     plen = c_len(cc);
@@ -1659,7 +1659,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     load_k(n - 1);
     load_at(n - 1);
     load_mt(n - 1);
-    load_qkt(n - 1);
+    load_qt(n - 1);
     load_rows(n - 1);
     put_rows((n - 1) & 1);
     put_do((n - 1) & 1);
@@ -1713,6 +1713,9 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
       }
     }
     const float4 at_cur = atsc;
+    // K rows past the chunk end repeat row len - 1; W2 is zero there
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) *reinterpret_cast<bf16x8*>(Kc + prow * LDKC + 32 * ks + 8 * g4) = kf[ks];
     load_k(nx);
     load_at(nx);
 #pragma unroll
@@ -1799,7 +1802,11 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt) Y[mt][nt] *= gC;
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
+    for (int ks = 0; ks < 2; ++ks) {
+      // K^T rows (DK/4) w + 16 mt + i, chunk rows 32 ks + 8 g4 ..
+      bf16x8 ktf[XMT];
+#pragma unroll
+      for (int mt = 0; mt < XMT; ++mt) ktf[mt] = ld_tr8(Kc, LDKC, 32 * ks + 8 * g4, (DK / 4) * w + 16 * mt);
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt) {
         const int off = (16 * nt + r16) * LDR + 32 * ks + 8 * g4;
@@ -1809,11 +1816,12 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
         for (int mt = 0; mt < XMT; ++mt) {
           Y[mt][nt] = mfma16(qtf[mt][ks], ph, Y[mt][nt]);
           Y[mt][nt] = mfma16(qtf[mt][ks], pl, Y[mt][nt]);
-          Y[mt][nt] = mfma16(ktf[mt][ks], wh, Y[mt][nt]);
-          Y[mt][nt] = mfma16(ktf[mt][ks], wl, Y[mt][nt]);
+          Y[mt][nt] = mfma16(ktf[mt], wh, Y[mt][nt]);
+          Y[mt][nt] = mfma16(ktf[mt], wl, Y[mt][nt]);
         }
       }
-    load_qkt(nx);
+    }
+    load_qt(nx);
     put_do(buf ^ 1);
     put_rows(buf ^ 1);
     put_state();
@@ -2351,20 +2359,20 @@ static hipError_t run_fwd_bf(const LaunchArgs& a) {
     if (a.saved)
       k_prep_bf<DK, true><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
           q, k, a.g, beta, a.d, a.cmap, a.H, a.Mq, a.Ms, a.Aq, a.As, a.MTq, a.MTs, a.ATq, a.ATs,
-          a.KTp, a.QTp, a.Gw, a.sink);
+          a.QTp, a.Gw, a.sink);
     else
       k_prep_bf<DK, false><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
           q, k, a.g, beta, a.d, a.cmap, a.H, a.Mq, a.Ms, a.Aq, a.As, nullptr, nullptr, nullptr,
-          nullptr, a.KTp, nullptr, a.Gw, a.sink);
+          nullptr, nullptr, a.Gw, a.sink);
   }
   a.stage(a.saved ? "scan_fwd_save" : "scan_fwd");
   if (a.saved)
     k_scan_fwd_bf<DK, DV, SCAN_BV, true, true><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-        q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mq, a.Ms, a.Aq, a.As, a.KTp, a.Gw, a.o, a.ht, a.Xq, a.Xs,
+        q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, a.o, a.ht, a.Xq, a.Xs,
         a.Dq, a.Ds, a.Xfq, a.Xfs, a.sink);
   else
     k_scan_fwd_bf<DK, DV, SCAN_BV, true, false><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-        q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mq, a.Ms, a.Aq, a.As, a.KTp, a.Gw, a.o, a.ht, nullptr,
+        q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, a.o, a.ht, nullptr,
         nullptr, nullptr, nullptr, nullptr, nullptr, a.sink);
   a.stage(nullptr);
   return hipGetLastError();
@@ -2389,15 +2397,15 @@ static hipError_t run_bwd_bf(const LaunchArgs& a) {
     if (a.ncmax > 0)
       k_prep_bf<DK, true><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
           q, k, a.g, beta, a.d, a.cmap, a.H, a.Mq, a.Ms, a.Aq, a.As, a.MTq, a.MTs, a.ATq, a.ATs,
-          a.KTp, a.QTp, a.Gw, a.sink);
+          a.QTp, a.Gw, a.sink);
     a.stage("scan_fwd_store");
     k_scan_fwd_bf<DK, DV, SCAN_BV, false, true><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-        q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mq, a.Ms, a.Aq, a.As, a.KTp, a.Gw, nullptr, nullptr, a.Xq,
+        q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, nullptr, nullptr, a.Xq,
         a.Xs, a.Dq, a.Ds, a.Xfq, a.Xfs, a.sink);
   }
   a.stage("scan_bwd");
   k_scan_bwd_bf<DK, DV, SCAN_BV><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-      q, k, dO, beta, a.d, a.dht, a.smap, a.H, a.MTq, a.MTs, a.ATq, a.ATs, a.KTp, a.QTp, a.Gw, a.dh0, a.Yq,
+      q, k, dO, beta, a.d, a.dht, a.smap, a.H, a.MTq, a.MTs, a.ATq, a.ATs, a.QTp, a.Gw, a.dh0, a.Yq,
       a.Ys, a.dRq, a.dRs, a.sink);
   a.stage("intra_bwd");
   if (a.ncmax > 0)

@@ -42,11 +42,10 @@ struct LaunchArgs {
   float *Xw, *Dw, *Yw, *dRw;      // per chunk-head: X (dk x dv), D (64 x dv), Y, dR
   float* ddp;                     // per chunk-head partial dd
   // bf16 path, per chunk-head: M, A, M^T, A^T as int16 [64][64] with one
-  // power-of-two scale per row in the matching *s array; K^T and Q^T as [dk][64]
-  // bf16
+  // power-of-two scale per row in the matching *s array; Q^T as [dk][64] bf16
   int16_t *Mq, *Aq, *MTq, *ATq;
   float *Ms, *As, *MTs, *ATs;
-  uint16_t *KTp, *QTp;
+  uint16_t* QTp;
   // bf16 path, per chunk-head: X, Y (dk x dv), D, dR (64 x dv) as int16 with one
   // power-of-two scale per (row, 32-column block) in the matching *s array
   int16_t *Xq, *Dq, *Yq, *dRq;
