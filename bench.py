@@ -44,8 +44,8 @@ def stage_model(name, B, T, H, dk, dv, C=64, in_bytes=2):
     transposes count 2 bytes per element plus one 4-byte scale per row, the
     chunk states X, Y and pseudo-values D, dR handed from the scans to the
     backward gradient kernel 2 bytes per element plus one 4-byte scale per 32
-    elements (their int16 storage); K^T and Q^T copies made by the prep stage
-    are counted where they are written and read.
+    elements (their int16 storage); the Q^T copy made by the prep stage is
+    counted where it is written and read (K^T is formed on chip from K).
     """
     nch = B * math.ceil(T / C) * H
     f4 = 4
@@ -55,22 +55,22 @@ def stage_model(name, B, T, H, dk, dv, C=64, in_bytes=2):
     cc = C * C * 2 + C * f4         # one stored C x C matrix (int16 + row scales)
     st = dk * dv * 2 + dk * (dv // 32) * f4     # one stored state (int16 + scales)
     cd = C * dv * 2 + C * (dv // 32) * f4       # one stored C x dv matrix
-    if name in ("prep", "prep_save"):    # K K^T, Q K^T; q, k, g, beta -> M, A, K^T, G
+    if name in ("prep", "prep_save"):    # K K^T, Q K^T; q, k, g, beta -> M, A, G
         fl = 4 * C * C * dk
-        by = 2 * qk + gb + 2 * cc + qk + C * f4
+        by = 2 * qk + gb + 2 * cc + C * f4
         if name == "prep_save":           # + M^T, A^T, Q^T for the backward
             by += 2 * cc + qk
     elif name in ("scan_fwd", "scan_fwd_save"):  # K X, Q X, M R, A D, K^T D
         fl = 6 * C * dk * dv + 4 * C * C * dv
-        by = 3 * qk + vv + 2 * cc + gb + C * dv * f4   # ... -> o (fp32)
+        by = 2 * qk + vv + 2 * cc + gb + C * dv * f4   # q, k, v, M, A, g, beta -> o (fp32)
         if name == "scan_fwd_save":       # + chunk states X and D for the backward
             by += st + cd
     elif name == "scan_fwd_store":  # K X, M R, K^T D; -> X, D
         fl = 4 * C * dk * dv + 2 * C * C * dv
-        by = 2 * qk + vv + cc + gb + st + cd
+        by = qk + vv + cc + gb + st + cd
     elif name == "scan_bwd":      # K Y, A^T dO, M^T dD, Q^T Pg, K^T W2; -> Y, dR
         fl = 6 * C * dk * dv + 4 * C * C * dv
-        by = 3 * qk + vv + 2 * cc + gb + st + cd
+        by = 2 * qk + vv + 2 * cc + gb + st + cd      # k, Q^T, dO, M^T, A^T, g, beta
     elif name == "intra_bwd":     # 3 C x dk x dv, 2 C x C x dv, 5 C x C x dk products
         fl = 6 * C * dk * dv + 4 * C * C * dv + 10 * C * C * dk
         by = (2 * qk + 2 * vv + 2 * st + 2 * cd + gb          # q,k,v,dO,X,Y,D,dR
