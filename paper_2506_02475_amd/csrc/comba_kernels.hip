@@ -931,7 +931,7 @@ __device__ __forceinline__ void solve_block_column(const float* Ls, floatx4 (&mb
 // block of column 16 J + r16, i.e. 8-byte pieces of row 16 J + r16 of M^T.
 template <int J, int LDL, bool BWD>
 __device__ __forceinline__ void put_block_column(float* Ls, const floatx4 (&mb)[4], int16_t* Mt,
-                                                 float* MTs, float* sink) {
+                                                 float* MTs) {
   const int lane = lane_id(), r16 = lane & 15, g4 = lane >> 4;
 #pragma unroll
   for (int i = J + 1; i < 4; ++i)
@@ -949,7 +949,7 @@ __device__ __forceinline__ void put_block_column(float* Ls, const floatx4 (&mb)[
 #pragma unroll
     for (int i = 0; i < 4; ++i)
       *reinterpret_cast<uint2*>(Mt + 16 * i + 4 * g4) = i < J ? make_uint2(0u, 0u) : q_pack4(mb[i], inv);
-    *(g4 == 0 ? MTs + 16 * J + r16 : sink + lane) = q_scale(m);
+    MTs[16 * J + r16] = q_scale(m);  // the four lanes of a row store the same value
   }
 }
 
@@ -1048,7 +1048,8 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
           q_pack4(quad_transpose(floatx4{av[nt][0], av[nt][1], av[nt][2], av[nt][3]}), inv);
     const float4 sc = make_float4(q_scale(rmax[0]), q_scale(rmax[1]), q_scale(rmax[2]),
                                   q_scale(rmax[3]));
-    *reinterpret_cast<float4*>(r16 == 0 ? As + chh * CH + 16 * w + 4 * g4 : sink + 4 * lane) = sc;
+    // the 16 lanes of a group hold the same four scales and store them alike
+    *reinterpret_cast<float4*>(As + chh * CH + 16 * w + 4 * g4) = sc;
   }
   if constexpr (BWD) {
     // column maxima of this wave's 16 rows, combined over the waves below
@@ -1071,7 +1072,7 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
       const float m = fmaxf(fmaxf(colmax[0][c], colmax[1][c]), fmaxf(colmax[2][c], colmax[3][c]));
       *reinterpret_cast<uint2*>(ATq + chh * CC + (long)c * CH + 16 * w + 4 * g4) =
           q_pack4(floatx4{av[nt][0], av[nt][1], av[nt][2], av[nt][3]}, q_inv_scale(m));
-      *(w == 0 && g4 == 0 ? ATs + chh * CH + c : sink + lane) = q_scale(m);
+      if (w == 0) ATs[chh * CH + c] = q_scale(m);  // equal in the four lane groups
     }
   }
 
@@ -1125,10 +1126,10 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
     int16_t* Mt = BWD ? MTq + chh * CC + (long)(16 * jb + r16) * CH : nullptr;
     float* Mts = BWD ? MTs + chh * CH : nullptr;
     switch (jb) {
-      case 0: put_block_column<0, LDL, BWD>(Ls, mb, Mt, Mts, sink); break;
-      case 1: put_block_column<1, LDL, BWD>(Ls, mb, Mt, Mts, sink); break;
-      case 2: put_block_column<2, LDL, BWD>(Ls, mb, Mt, Mts, sink); break;
-      default: put_block_column<3, LDL, BWD>(Ls, mb, Mt, Mts, sink); break;
+      case 0: put_block_column<0, LDL, BWD>(Ls, mb, Mt, Mts); break;
+      case 1: put_block_column<1, LDL, BWD>(Ls, mb, Mt, Mts); break;
+      case 2: put_block_column<2, LDL, BWD>(Ls, mb, Mt, Mts); break;
+      default: put_block_column<3, LDL, BWD>(Ls, mb, Mt, Mts); break;
     }
   }
   __syncthreads();
@@ -1145,7 +1146,7 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
     for (int e = 0; e < 8; ++e) m = fmaxf(m, fabsf(mv[e]));
     m = max8(m);
     *reinterpret_cast<uint4*>(Mq + chh * CC + (long)r * CH + c8) = q_pack8(mv, q_inv_scale(m));
-    *(c8 == 0 ? Ms + chh * CH + r : sink + lane) = q_scale(m);
+    Ms[chh * CH + r] = q_scale(m);  // the eight threads of a row store the same value
   }
 }
 
@@ -1233,7 +1234,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt)
         *reinterpret_cast<uint2*>(dq + row * DV + xcol_q + 16 * nt) = q_pack4(t[nt], inv);
-      *(qt_col() == 0 ? ds + row * NB + blockIdx.z : sink + lane) = q_scale(m);
+      ds[row * NB + blockIdx.z] = q_scale(m);  // the four lanes of a row store the same value
     }
   };
   put_state();
@@ -1407,7 +1408,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt)
         *reinterpret_cast<uint2*>(Dq + row * DV + xcol_q + 16 * nt) = q_pack4(t[nt], inv);
-      *(qt_col() == 0 ? Ds + row * NB + blockIdx.z : sink + lane) = q_scale(m);
+      Ds[row * NB + blockIdx.z] = q_scale(m);  // the four lanes of a row store the same value
     }
 #pragma unroll
     for (int nt = 0; nt < NTV; ++nt) {
@@ -1571,7 +1572,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt)
         *reinterpret_cast<uint2*>(dq + row * DV + ycol_q + 16 * nt) = q_pack4(t[nt], inv);
-      *(qt_col() == 0 ? ds + row * NB + blockIdx.z : sink + lane) = q_scale(m);
+      ds[row * NB + blockIdx.z] = q_scale(m);  // the four lanes of a row store the same value
     }
   };
   put_state();
@@ -1777,7 +1778,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt)
         *reinterpret_cast<uint2*>(dRq + row * DV + ycol_q + 16 * nt) = q_pack4(t[nt], inv);
-      *(qt_col() == 0 ? dRs + row * NB + blockIdx.z : sink + lane) = q_scale(m);
+      dRs[row * NB + blockIdx.z] = q_scale(m);  // the four lanes of a row store the same value
     }
 #pragma unroll
     for (int nt = 0; nt < NTV; ++nt) {
