@@ -1216,7 +1216,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
       for (int nt = 0; nt < NTV; ++nt)
         store4(dst + (long)(xrow_q + 16 * mt) * DV + xcol_q + 16 * nt, quad_transpose(X[mt][nt]));
   };
-  // The same rows as int16 with one scale per row of the slice (see q_pack4).
+  // The same rows as int16 with one scale per row of the slice (see q_pack4),
+  // into the slice's own block: dq = block base, [DK][BV]; ds = its row scales.
   auto store_state_q = [&](int16_t* dq, float* ds) {
 #pragma unroll
     for (int mt = 0; mt < XMT; ++mt) {
@@ -1233,8 +1234,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
       const long row = xrow_q + 16 * mt;
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt)
-        *reinterpret_cast<uint2*>(dq + row * DV + xcol_q + 16 * nt) = q_pack4(t[nt], inv);
-      ds[row * NB + blockIdx.z] = q_scale(m);  // the four lanes of a row store the same value
+        *reinterpret_cast<uint2*>(dq + row * BV + qt_col() + 16 * nt) = q_pack4(t[nt], inv);
+      ds[row] = q_scale(m);  // the four lanes of a row store the same value
     }
   };
   put_state();
@@ -1306,7 +1307,10 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     if constexpr (OUT) load_a(0);
     load_rows(0);
     put_rows(0);
-    if constexpr (STORE) store_state_q(Xq + c_chh(0) * DK * DV, Xs + c_chh(0) * DK * NB);
+    if constexpr (STORE) {
+      const long xb = (c_chh(0) * NB + blockIdx.z) * DK;
+      store_state_q(Xq + xb * BV, Xs + xb);
+    }
   }
   __syncthreads();
 
@@ -1404,11 +1408,11 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
       }
       m = row4_max(m);
       const float inv = q_inv_scale(m);
-      const long row = chh * CH + 16 * w + qt_row();
+      const long row = (chh * NB + blockIdx.z) * CH + 16 * w + qt_row();  // the slice's block
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt)
-        *reinterpret_cast<uint2*>(Dq + row * DV + xcol_q + 16 * nt) = q_pack4(t[nt], inv);
-      Ds[row * NB + blockIdx.z] = q_scale(m);  // the four lanes of a row store the same value
+        *reinterpret_cast<uint2*>(Dq + row * BV + qt_col() + 16 * nt) = q_pack4(t[nt], inv);
+      Ds[row] = q_scale(m);  // the four lanes of a row store the same value
     }
 #pragma unroll
     for (int nt = 0; nt < NTV; ++nt) {
@@ -1486,8 +1490,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     put_state();
     // state entering the next chunk (after the last chunk: the final state)
     if constexpr (STORE) {
-      const long sb = more ? c_chh(cc + 1) * DK * DV : soff;
-      store_state_q((more ? Xq : Xfq) + sb, (more ? Xs : Xfs) + sb / 32);
+      const long xb = ((more ? c_chh(cc + 1) : (long)s * H + h) * NB + blockIdx.z) * DK;
+      store_state_q((more ? Xq : Xfq) + xb * BV, (more ? Xs : Xfs) + xb);
     }
     put_rows(buf ^ 1);
     __syncthreads();
@@ -1554,7 +1558,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
       for (int nt = 0; nt < NTV; ++nt)
         store4(dst + (long)(yrow_q + 16 * mt) * DV + ycol_q + 16 * nt, quad_transpose(Y[mt][nt]));
   };
-  // the same rows as int16 with one scale per row of the slice (see q_pack4)
+  // the same rows as int16 with one scale per row of the slice (see q_pack4),
+  // into the slice's own block: dq = block base, [DK][BV]; ds = its row scales
   auto store_state_q = [&](int16_t* dq, float* ds) {
 #pragma unroll
     for (int mt = 0; mt < XMT; ++mt) {
@@ -1571,8 +1576,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
       const long row = yrow_q + 16 * mt;
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt)
-        *reinterpret_cast<uint2*>(dq + row * DV + ycol_q + 16 * nt) = q_pack4(t[nt], inv);
-      ds[row * NB + blockIdx.z] = q_scale(m);  // the four lanes of a row store the same value
+        *reinterpret_cast<uint2*>(dq + row * BV + qt_col() + 16 * nt) = q_pack4(t[nt], inv);
+      ds[row] = q_scale(m);  // the four lanes of a row store the same value
     }
   };
   put_state();
@@ -1673,7 +1678,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     const long chh = c_chh(cc);
     const int buf = cc & 1;
     const int clen = c_len(cc);
-    store_state_q(Yq + chh * DK * DV, Ys + chh * DK * NB);
+    store_state_q(Yq + (chh * NB + blockIdx.z) * DK * BV, Ys + (chh * NB + blockIdx.z) * DK);
     load_rows(nx);
     load_do(nx);
     const float glast = Grow[buf][CH - 1];
@@ -1774,11 +1779,11 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
       }
       m = row4_max(m);
       const float inv = q_inv_scale(m);
-      const long row = chh * CH + 16 * w + qt_row();
+      const long row = (chh * NB + blockIdx.z) * CH + 16 * w + qt_row();  // the slice's block
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt)
-        *reinterpret_cast<uint2*>(dRq + row * DV + ycol_q + 16 * nt) = q_pack4(t[nt], inv);
-      dRs[row * NB + blockIdx.z] = q_scale(m);  // the four lanes of a row store the same value
+        *reinterpret_cast<uint2*>(dRq + row * BV + qt_col() + 16 * nt) = q_pack4(t[nt], inv);
+      dRs[row] = q_scale(m);  // the four lanes of a row store the same value
     }
 #pragma unroll
     for (int nt = 0; nt < NTV; ++nt) {
@@ -1905,8 +1910,9 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
 
   const int po = tid & 255, po_r = po >> 2, po_c = (po & 3) * 8;  // dO piece (dup. above 256)
   const int pf_r = tid >> 3, pf_c = (tid & 7) * 4;                 // dR / D / v piece
-  // X, Y, D, dR arrive as int16 with one scale per (row, 32-column block): the
-  // block is exactly one VB-wide column block (see q_pack4)
+  // X, Y, D, dR arrive as int16 with one scale per (row, 32-column block), each
+  // 32-column block stored on its own ([chunk-head][block][row][32]): the block
+  // is exactly one VB-wide phase-1 step (see q_pack4)
   static_assert(VB == 32, "column blocks must match the stored scale blocks");
   constexpr int NB = DV / 32;
   uint4 r_do;
@@ -1917,19 +1923,19 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     const int j = vb * VB;
     r_do = *reinterpret_cast<const uint4*>(dO + (tok + (long)min(po_r, len - 1) * H) * DV + j + po_c);
     r_v = *reinterpret_cast<const uint2*>(v + (tok + (long)min(pf_r, len - 1) * H) * DV + j + pf_c);
-    const long rr = chh * CH + pf_r;
-    r_dr = *reinterpret_cast<const uint2*>(dRq + rr * DV + j + pf_c);
-    r_d = *reinterpret_cast<const uint2*>(Dq + rr * DV + j + pf_c);
-    s_dr = dRs[rr * NB + vb];
-    s_d = Ds[rr * NB + vb];
+    const long rr = (chh * NB + vb) * CH + pf_r;
+    r_dr = *reinterpret_cast<const uint2*>(dRq + rr * VB + pf_c);
+    r_d = *reinterpret_cast<const uint2*>(Dq + rr * VB + pf_c);
+    s_dr = dRs[rr];
+    s_d = Ds[rr];
 #pragma unroll
     for (int p = 0; p < XP; ++p) {
       const int pc = tid + p * IB_THR, xr = pc >> 3, xc = (pc & 7) * 4;
-      const long xrow = chh * DK + xr;
-      r_x[p] = *reinterpret_cast<const uint2*>(Xq + xrow * DV + j + xc);
-      r_y[p] = *reinterpret_cast<const uint2*>(Yq + xrow * DV + j + xc);
-      s_x[p] = Xs[xrow * NB + vb];
-      s_y[p] = Ys[xrow * NB + vb];
+      const long xrow = (chh * NB + vb) * DK + xr;
+      r_x[p] = *reinterpret_cast<const uint2*>(Xq + xrow * VB + xc);
+      r_y[p] = *reinterpret_cast<const uint2*>(Yq + xrow * VB + xc);
+      s_x[p] = Xs[xrow];
+      s_y[p] = Ys[xrow];
     }
     // keep the loads here: the scheduler otherwise sinks some of them to their
     // use one block later, where they are waited for at once
@@ -2072,17 +2078,20 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
       const ChunkInfo ci2 = cmap[c2];
       if (ci2.len > 0) {
         const long chh2 = (long)c2 * H + h2, tok2 = (long)ci2.tok0 * H + h2;
-        // lines: X rows (DK), Y rows (DK), dR, D, dO, v rows (64 each); the
-        // first 32 columns of each row are the block
-        static_assert(2 * DK + 4 * CH <= IB_THR, "one line per thread");
+        // lines: the first blocks of X, Y (DK rows x 64 bytes: DK / 2 lines
+        // each) and of dR, D (CH / 2 lines each), then the dO and v rows (one
+        // line each; their first 32 columns are the block)
+        static_assert(DK + 3 * CH <= IB_THR, "one line per thread");
+        static_assert((DK + CH) % CH == 0, "the dO and v rows start at a multiple of CH");
         int t = tid;
         const int rr = min(t & (CH - 1), ci2.len - 1);
-        const char* a = reinterpret_cast<const char*>(Xq + chh2 * DK * DV);
-        if (t < DK) a = reinterpret_cast<const char*>(Xq + (chh2 * DK + t) * DV);
-        else if ((t -= DK) < DK) a = reinterpret_cast<const char*>(Yq + (chh2 * DK + t) * DV);
-        else if ((t -= DK) < CH) a = reinterpret_cast<const char*>(dRq + (chh2 * CH + t) * DV);
-        else if ((t -= CH) < CH) a = reinterpret_cast<const char*>(Dq + (chh2 * CH + t) * DV);
-        else if ((t -= CH) < CH) a = reinterpret_cast<const char*>(dO + (tok2 + (long)rr * H) * DV);
+        const long b2 = chh2 * NB;  // block (chh2, 0)
+        const char* a = reinterpret_cast<const char*>(Xq + b2 * DK * VB);
+        if (t < DK / 2) a = reinterpret_cast<const char*>(Xq + b2 * DK * VB) + 128 * t;
+        else if ((t -= DK / 2) < DK / 2) a = reinterpret_cast<const char*>(Yq + b2 * DK * VB) + 128 * t;
+        else if ((t -= DK / 2) < CH / 2) a = reinterpret_cast<const char*>(dRq + b2 * CH * VB) + 128 * t;
+        else if ((t -= CH / 2) < CH / 2) a = reinterpret_cast<const char*>(Dq + b2 * CH * VB) + 128 * t;
+        else if ((t -= CH / 2) < CH) a = reinterpret_cast<const char*>(dO + (tok2 + (long)rr * H) * DV);
         else if ((t -= CH) < CH) a = reinterpret_cast<const char*>(v + (tok2 + (long)rr * H) * DV);
         touched = *reinterpret_cast<const uint32_t*>(a);
       }

@@ -47,10 +47,12 @@ struct LaunchArgs {
   float *Ms, *As, *MTs, *ATs;
   uint16_t* QTp;
   // bf16 path, per chunk-head: X, Y (dk x dv), D, dR (64 x dv) as int16 with one
-  // power-of-two scale per (row, 32-column block) in the matching *s array
+  // power-of-two scale per (row, 32-column block) in the matching *s array;
+  // each 32-column block is stored on its own: [chunk-head][dv/32][rows][32],
+  // scales [chunk-head][dv/32][rows]
   int16_t *Xq, *Dq, *Yq, *dRq;
   float *Xs, *Ds, *Ys, *dRs;
-  int16_t* Xfq;  // bf16 path: sink for the state after the last chunk [N,H,dk,dv]
+  int16_t* Xfq;  // bf16 path: sink for the state after the last chunk (same layout)
   float* Xfs;    //   and its scales
   float* sink;  // 1 KiB that absorbs stores of padded rows (never read)
   hipStream_t stream;
