@@ -4,7 +4,8 @@
 //   G_r   in-chunk cumulative log-gate sum_{j<=r} g_j; Gm_r = G_{r-1} (Gm_0 = 0)
 //   X     state entering the chunk, H = S^T in R^{dk x dv} (the paper's S_[t])
 //   L     strictly lower, L_ri = beta_r exp(Gm_r - G_i) k_r.k_i       (Eq. prepare-WY_M)
-//   M     (I + L)^{-1}, by forward substitution in fp32           (Section 3.3)
+//   M     (I + L)^{-1} in fp32 (Section 3.3): forward substitution (fp32 path);
+//         blocked, substitution in the 16x16 diagonal blocks and MFMA for the rest (bf16 path)
 //   A     (Q - d K) K^T masked to r >= i and scaled by exp(G_r - G_i)
 //   R     Diag(beta) V - Diag(beta exp(Gm)) K X
 //   D     M R = U - W X, the pseudo-value term of the matrix form
@@ -854,12 +855,13 @@ __global__ __launch_bounds__(NTHR) void k_reduce_dd(const float* __restrict__ dd
 }
 
 // ===========================================================================
-// bf16 path.  k_prep_bf writes every per-chunk operand the scans need in the
-// form the MFMA consumes: M, A (and for the backward M^T, A^T) as bf16 (hi, lo)
-// pairs, K^T (and Q^T) as bf16.  In the scans each wave then loads the
-// A-operand fragments of its own rows straight from global memory into
-// registers, one chunk ahead, and LDS only carries what the four waves
-// exchange (state, R, D and their backward counterparts), already split.
+// bf16 path.  k_prep_bf writes the per-chunk operands the scans need in the
+// order the MFMA consumes them: M, A (and for the backward M^T, A^T) as int16
+// rows with one power-of-two scale per row, Q^T as bf16.  In the scans each
+// wave loads the A-operand fragments of its own rows straight from global
+// memory into registers, one chunk ahead; LDS carries what the four waves
+// exchange (state, R, D and their backward counterparts, already split) and
+// the chunk's K rows, whose transposing reads give the K^T operand.
 // ===========================================================================
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
