@@ -2157,16 +2157,20 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     // row dot products of T1, T2, T3 with q~ and k over this wave's columns
     float p1[4] = {0.f, 0.f, 0.f, 0.f}, p2[4] = {0.f, 0.f, 0.f, 0.f}, p3[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int j = 0; j < NTW; ++j)
+    for (int j = 0; j < NTW; ++j) {
+      // K, Q at this lane's accumulator rows 16 rt + 4 g4 + e of column
+      // 16 (ch NTW + j) + r16: one transposing read each
+      const bf16x4_t k4 = ld_tr4(Ks, LDK, 16 * rt + 4 * g4, 16 * (ch * NTW + j));
+      const bf16x4_t q4 = ld_tr4(Qs, LDK, 16 * rt + 4 * g4, 16 * (ch * NTW + j));
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int r = 16 * rt + 4 * g4 + e, c = 16 * (ch * NTW + j) + r16;
-        const float kv = bf2f(Ks[r * LDK + c]);
-        const float qv = bf2f(Qs[r * LDK + c]) - dh * kv;
+        const float kv = (float)k4[e];
+        const float qv = (float)q4[e] - dh * kv;
         p1[e] += T1[j][e] * qv;
         p2[e] += T2[j][e] * kv;
         p3[e] += T3[j][e] * kv;
       }
+    }
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const float s0 = sum16(rE1[e]), s1 = sum16(rE2[e]), s2 = sum16(rBL[e]);
@@ -2229,11 +2233,11 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
 #pragma unroll
   for (int j = 0; j < NTW; ++j) {
     floatx4 dkv;
+    const bf16x4_t k4 = ld_tr4(Ks, LDK, 16 * rt + 4 * g4, 16 * (ch * NTW + j));
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const int r = 16 * rt + 4 * g4 + e, c = 16 * (ch * NTW + j) + r16;
       const float dqt = T1[j][e];
-      ddpart += bf2f(Ks[r * LDK + c]) * dqt;
+      ddpart += (float)k4[e] * dqt;
       dkv[e] = T2[j][e] - dh * dqt;
     }
     const long off = (tok + (long)qrow * H) * DK + 16 * (ch * NTW + j) + qt_col();
