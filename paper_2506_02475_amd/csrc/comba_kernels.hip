@@ -879,6 +879,15 @@ __device__ __forceinline__ floatx4 mfma16(const bf16x8& a, const bf16x8& b, cons
 __device__ __forceinline__ bf16x8 ld8(const bf16_t* p) { return *reinterpret_cast<const bf16x8*>(p); }
 __device__ __forceinline__ bf16x8 zero8() { return __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u}); }
 
+// Element (row, col) of a 64-column operand tile that prep stores in MFMA
+// fragment order (M, A, M^T, A^T, Q^T): the 16 bytes lane (g, i) of wave w
+// loads for k-step ks (row 16 w + i, columns 32 ks + 8 g .. +7) sit at
+// ((2 (row / 16) + ks) 64 + 16 g + i) * 8, so one k-step load of a wave reads
+// 1 KiB of whole lines (a row-major fragment would touch 16 half lines).
+__device__ __forceinline__ int frag_off(int row, int col) {
+  return (((row >> 4) * 2 + (col >> 5)) * 64 + ((col >> 3) & 3) * 16 + (row & 15)) * 8 + (col & 7);
+}
+
 // four fp32 values -> bf16 (hi, lo) with hi + lo ~ x to ~16 significant bits
 __device__ __forceinline__ void split4(const float (&x)[4], bf16x4& hi, bf16x4& lo) {
 #pragma unroll
@@ -929,8 +938,9 @@ __device__ __forceinline__ void solve_block_column(const float* Ls, floatx4 (&mb
 
 // Block column J of M (mb as left by solve_block_column) into LDS over L, and
 // with BWD the rows 16 J .. 16 J + 15 of M^T (= columns of M) as int16 with
-// one scale per row: lane (g4, r16) holds rows 4 g4 .. 4 g4 + 3 of every
-// block of column 16 J + r16, i.e. 8-byte pieces of row 16 J + r16 of M^T.
+// one scale per row, in fragment order (Mt = the chunk-head's M^T): lane
+// (g4, r16) holds rows 4 g4 .. 4 g4 + 3 of every block of column 16 J + r16,
+// i.e. 8-byte pieces of row 16 J + r16 of M^T.
 template <int J, int LDL, bool BWD>
 __device__ __forceinline__ void put_block_column(float* Ls, const floatx4 (&mb)[4], int16_t* Mt,
                                                  float* MTs) {
@@ -950,7 +960,8 @@ __device__ __forceinline__ void put_block_column(float* Ls, const floatx4 (&mb)[
     const float inv = q_inv_scale(m);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      *reinterpret_cast<uint2*>(Mt + 16 * i + 4 * g4) = i < J ? make_uint2(0u, 0u) : q_pack4(mb[i], inv);
+      *reinterpret_cast<uint2*>(Mt + frag_off(16 * J + r16, 16 * i + 4 * g4)) =
+          i < J ? make_uint2(0u, 0u) : q_pack4(mb[i], inv);
     MTs[16 * J + r16] = q_scale(m);  // the four lanes of a row store the same value
   }
 }
@@ -1003,13 +1014,13 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
   }
   __syncthreads();
   if constexpr (BWD) {
-    // Q^T per chunk-head, [dk][64] bf16, for the reverse scan.  One transposing
+    // Q^T per chunk-head, dk x 64 bf16 in fragment order, for the reverse scan.  One transposing
     // LDS read pair gives lane (g, i) the 8 rows 32 tb + 8 g .. of column c0 + i,
     // i.e. one 16-byte piece of row c0 + i of Q^T.
     bf16_t* Qt = QTp + chh * DK * CH;
     for (int pc = w; pc < 2 * (DK / 16); pc += NWAVE) {
       const int c0 = 16 * (pc % (DK / 16)), r0 = 32 * (pc / (DK / 16)) + 8 * g4;
-      *reinterpret_cast<bf16x8*>(Qt + (long)(c0 + (lane & 15)) * CH + r0) = ld_tr8(Qs, LDK, r0, c0);
+      *reinterpret_cast<bf16x8*>(Qt + frag_off(c0 + (lane & 15), r0)) = ld_tr8(Qs, LDK, r0, c0);
     }
   }
 
@@ -1043,10 +1054,9 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
     const int i = lane & 3;
     const float mrow = i == 0 ? rmax[0] : i == 1 ? rmax[1] : i == 2 ? rmax[2] : rmax[3];
     const float inv = q_inv_scale(mrow);
-    const long rowoff = chh * CC + (long)(16 * w + qt_row()) * CH;
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt)
-      *reinterpret_cast<uint2*>(Aq + rowoff + 16 * nt + qt_col()) =
+      *reinterpret_cast<uint2*>(Aq + chh * CC + frag_off(16 * w + qt_row(), 16 * nt + qt_col())) =
           q_pack4(quad_transpose(floatx4{av[nt][0], av[nt][1], av[nt][2], av[nt][3]}), inv);
     const float4 sc = make_float4(q_scale(rmax[0]), q_scale(rmax[1]), q_scale(rmax[2]),
                                   q_scale(rmax[3]));
@@ -1072,7 +1082,7 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
     for (int nt = 0; nt < 4; ++nt) {
       const int c = 16 * nt + r16;
       const float m = fmaxf(fmaxf(colmax[0][c], colmax[1][c]), fmaxf(colmax[2][c], colmax[3][c]));
-      *reinterpret_cast<uint2*>(ATq + chh * CC + (long)c * CH + 16 * w + 4 * g4) =
+      *reinterpret_cast<uint2*>(ATq + chh * CC + frag_off(c, 16 * w + 4 * g4)) =
           q_pack4(floatx4{av[nt][0], av[nt][1], av[nt][2], av[nt][3]}, q_inv_scale(m));
       if (w == 0) ATs[chh * CH + c] = q_scale(m);  // equal in the four lane groups
     }
@@ -1125,7 +1135,7 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
   }
   __syncthreads();  // every read of L is done
   {
-    int16_t* Mt = BWD ? MTq + chh * CC + (long)(16 * jb + r16) * CH : nullptr;
+    int16_t* Mt = BWD ? MTq + chh * CC : nullptr;
     float* Mts = BWD ? MTs + chh * CH : nullptr;
     switch (jb) {
       case 0: put_block_column<0, LDL, BWD>(Ls, mb, Mt, Mts); break;
@@ -1147,7 +1157,7 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
 #pragma unroll
     for (int e = 0; e < 8; ++e) m = fmaxf(m, fabsf(mv[e]));
     m = max8(m);
-    *reinterpret_cast<uint4*>(Mq + chh * CC + (long)r * CH + c8) = q_pack8(mv, q_inv_scale(m));
+    *reinterpret_cast<uint4*>(Mq + chh * CC + frag_off(r, c8)) = q_pack8(mv, q_inv_scale(m));
     Ms[chh * CH + r] = q_scale(m);  // the eight threads of a row store the same value
   }
 }
@@ -1292,15 +1302,15 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     }
   };
   auto load_m = [&](int cc) {
-    const int16_t* p = Mq + c_chh(cc) * CC + prow * CH + 8 * g4;
+    const int16_t* p = Mq + c_chh(cc) * CC + (2 * w * 64 + lane) * 8;  // fragment order
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) mq[ks] = *reinterpret_cast<const uint4*>(p + 32 * ks);
+    for (int ks = 0; ks < 2; ++ks) mq[ks] = *reinterpret_cast<const uint4*>(p + ks * 512);
     msc = *reinterpret_cast<const float4*>(Ms + c_chh(cc) * CH + 16 * w + 4 * g4);
   };
   auto load_a = [&](int cc) {
-    const int16_t* p = Aq + c_chh(cc) * CC + prow * CH + 8 * g4;
+    const int16_t* p = Aq + c_chh(cc) * CC + (2 * w * 64 + lane) * 8;  // fragment order
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) aq[ks] = *reinterpret_cast<const uint4*>(p + 32 * ks);
+    for (int ks = 0; ks < 2; ++ks) aq[ks] = *reinterpret_cast<const uint4*>(p + ks * 512);
     asc = *reinterpret_cast<const float4*>(As + c_chh(cc) * CH + 16 * w + 4 * g4);
   };
   if (n > 0) {
@@ -1611,23 +1621,24 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     for (int ks = 0; ks < KS; ++ks) kf[ks] = ld8(k + rb + 32 * ks);
   };
   auto load_at = [&](int cc) {
-    const int16_t* p = ATq + c_chh(cc) * CC + prow * CH + 8 * g4;
+    const int16_t* p = ATq + c_chh(cc) * CC + (2 * w * 64 + lane) * 8;  // fragment order
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) atq[ks] = *reinterpret_cast<const uint4*>(p + 32 * ks);
+    for (int ks = 0; ks < 2; ++ks) atq[ks] = *reinterpret_cast<const uint4*>(p + ks * 512);
     atsc = *reinterpret_cast<const float4*>(ATs + c_chh(cc) * CH + 16 * w + 4 * g4);
   };
   auto load_mt = [&](int cc) {
-    const int16_t* p = MTq + c_chh(cc) * CC + prow * CH + 8 * g4;
+    const int16_t* p = MTq + c_chh(cc) * CC + (2 * w * 64 + lane) * 8;  // fragment order
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) mtq[ks] = *reinterpret_cast<const uint4*>(p + 32 * ks);
+    for (int ks = 0; ks < 2; ++ks) mtq[ks] = *reinterpret_cast<const uint4*>(p + ks * 512);
     mtsc = *reinterpret_cast<const float4*>(MTs + c_chh(cc) * CH + 16 * w + 4 * g4);
   };
   auto load_qt = [&](int cc) {
-    const long base = c_chh(cc) * DK * CH + ((DK / 4) * w + r16) * CH + 8 * g4;
+    // fragment order: rows (DK/4) w + 16 mt + i are row block w XMT + mt
+    const long base = c_chh(cc) * DK * CH + (2 * XMT * w * 64 + lane) * 8;
 #pragma unroll
     for (int mt = 0; mt < XMT; ++mt)
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) qtf[mt][ks] = ld8(QTp + base + 16 * mt * CH + 32 * ks);
+      for (int ks = 0; ks < 2; ++ks) qtf[mt][ks] = ld8(QTp + base + (2 * mt + ks) * 512);
   };
   auto load_rows = [&](int cc) {
     plen = c_len(cc);
