@@ -1865,7 +1865,7 @@ template <int DK>
 struct IntraBwdBfSmem {
   static constexpr int VB = 32, LDB = VB + 8;
   static constexpr int LDK = DK + 8, LDC = CH + 8;
-  static constexpr int P1 = (5 * CH * LDB + 4 * DK * LDB) * 2;
+  static constexpr int P1 = (6 * CH * LDB + 4 * DK * LDB) * 2;
   static constexpr int P2 = (2 * CH * LDK + 6 * CH * LDC) * 2;
   static constexpr int BYTES = P1 > P2 ? P1 : P2;
 };
@@ -1920,22 +1920,28 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
   bf16_t* Xl = Xh + DK * LDB;
   bf16_t* Yh = Xl + DK * LDB;
   bf16_t* Yl = Yh + DK * LDB;
+  bf16_t* Vb = Yl + DK * LDB;
 
-  const int po = tid & 255, po_r = po >> 2, po_c = (po & 3) * 8;  // dO piece (dup. above 256)
-  const int pf_r = tid >> 3, pf_c = (tid & 7) * 4;                 // dR / D / v piece
+  // dO and v arrive two blocks at a time, whole 128-byte lines: thread t holds
+  // row t / 8, columns 8 (t % 8) .. +7 of the 64 columns of blocks (2p, 2p+1),
+  // i.e. a piece of block 2p + pb; it stages the piece when that block comes up
+  const int pr = tid >> 3, pc = (tid & 7) * 8, pb = (tid & 7) >> 2;
+  const int pf_r = tid >> 3, pf_c = (tid & 7) * 4;                 // dR / D piece
   // X, Y, D, dR arrive as int16 with one scale per (row, 32-column block), each
   // 32-column block stored on its own ([chunk-head][block][row][32]): the block
   // is exactly one VB-wide phase-1 step (see q_pack4)
   static_assert(VB == 32, "column blocks must match the stored scale blocks");
   constexpr int NB = DV / 32;
-  uint4 r_do;
+  uint4 r_do, r_v;
   uint2 r_dr, r_d, r_x[XP], r_y[XP];
   float s_dr, s_d, s_x[XP], s_y[XP];
-  uint2 r_v;
+  static_assert(NVB % 2 == 0 && CH * 8 == IB_THR, "dO / v pairs: one 16-byte piece per thread");
   auto issue = [&](int vb) {
-    const int j = vb * VB;
-    r_do = *reinterpret_cast<const uint4*>(dO + (tok + (long)min(po_r, len - 1) * H) * DV + j + po_c);
-    r_v = *reinterpret_cast<const uint2*>(v + (tok + (long)min(pf_r, len - 1) * H) * DV + j + pf_c);
+    if (vb % 2 == 0) {
+      const long rb = (tok + (long)min(pr, len - 1) * H) * DV + vb * VB + pc;
+      r_do = *reinterpret_cast<const uint4*>(dO + rb);
+      r_v = *reinterpret_cast<const uint4*>(v + rb);
+    }
     const long rr = (chh * NB + vb) * CH + pf_r;
     r_dr = *reinterpret_cast<const uint2*>(dRq + rr * VB + pf_c);
     r_d = *reinterpret_cast<const uint2*>(Dq + rr * VB + pf_c);
@@ -1955,11 +1961,15 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     __builtin_amdgcn_sched_barrier(0);
   };
   float Fpart = 0.f, bv = 0.f;
+  float4 fdr;  // this thread's dR piece, kept for <v_r, dR_r> after the barrier
   auto put = [&](int vb) {
     const int j = vb * VB;
-    *reinterpret_cast<uint4*>(dOb + po_r * LDB + po_c) = r_do;
+    if (pb == (vb & 1)) {
+      *reinterpret_cast<uint4*>(dOb + pr * LDB + (pc & 31)) = r_do;
+      *reinterpret_cast<uint4*>(Vb + pr * LDB + (pc & 31)) = r_v;
+    }
     bf16x4 hh, ll;
-    const float4 fdr = q_unpack4(r_dr, s_dr);
+    fdr = q_unpack4(r_dr, s_dr);
     split4v(fdr, hh, ll);
     *reinterpret_cast<bf16x4*>(dRh + pf_r * LDB + pf_c) = hh;
     *reinterpret_cast<bf16x4*>(dRl + pf_r * LDB + pf_c) = ll;
@@ -1978,15 +1988,11 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
       *reinterpret_cast<bf16x4*>(Yl + xr * LDB + xc) = ll;
       Fpart += fx.x * fy.x + fx.y * fy.y + fx.z * fy.z + fx.w * fy.w;
     }
-    // dv = Diag(beta) dR and <v_r, dR_r>
+    // dv = Diag(beta) dR
     const float b = Bs[pf_r];
     const float4 dvv = make_float4(b * fdr.x, b * fdr.y, b * fdr.z, b * fdr.w);
     float* dst = pf_r < len ? dv + (tok + (long)pf_r * H) * DV + j + pf_c : sink + (tid & 63) * 4;
     *reinterpret_cast<float4*>(dst) = dvv;
-    union { uint2 u; bf16_t e[4]; } vv;
-    vv.u = r_v;
-    bv += bf2f(vv.e[0]) * fdr.x + bf2f(vv.e[1]) * fdr.y + bf2f(vv.e[2]) * fdr.z +
-          bf2f(vv.e[3]) * fdr.w;
   };
 
   floatx4 T1[NTW], T2[NTW], T3[NTW], dA[2], dL[2];
@@ -2021,6 +2027,11 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     } else {
       kr.load_clip(k + tok * DK, (long)H * DK, len);
       qr.load_clip(q + tok * DK, (long)H * DK, len);
+    }
+    {
+      // <v_r, dR_r> for this thread's piece (v staged by the piece's owner)
+      const bf16x4 vv = *reinterpret_cast<const bf16x4*>(Vb + pf_r * LDB + pf_c);
+      bv += (float)vv[0] * fdr.x + (float)vv[1] * fdr.y + (float)vv[2] * fdr.z + (float)vv[3] * fdr.w;
     }
     const int arow = (16 * rt + r16) * LDB + 8 * g4;
     // dO rows past the chunk end hold row len - 1 (clamped loads): zero them
