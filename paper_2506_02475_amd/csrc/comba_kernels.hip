@@ -2250,8 +2250,6 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     }
   }
   float ddpart = 0.f;
-  const int qrow = 16 * rt + qt_row();
-  const bool qok = qrow < len;
 #pragma unroll
   for (int j = 0; j < NTW; ++j) {
     floatx4 dkv;
@@ -2262,9 +2260,17 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
       ddpart += (float)k4[e] * dqt;
       dkv[e] = T2[j][e] - dh * dqt;
     }
-    const long off = (tok + (long)qrow * H) * DK + 16 * (ch * NTW + j) + qt_col();
-    store4(qok ? dq + off : sink + 4 * lane, quad_transpose(T1[j]));
-    store4(qok ? dk + off : sink + 4 * lane, quad_transpose(dkv));
+    // straight from the accumulators (16 lanes write 64 contiguous bytes of a
+    // row): transposing to 16-byte pieces first costs more VALU than it saves
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int r = 16 * rt + 4 * g4 + e;
+      const long off = (tok + (long)r * H) * DK + 16 * (ch * NTW + j) + r16;
+      if (r < len) {
+        dq[off] = T1[j][e];
+        dk[off] = dkv[e];
+      }
+    }
   }
   ddpart = wave_sum(ddpart);
   if (lane == 0) scal[w][1] = ddpart;
