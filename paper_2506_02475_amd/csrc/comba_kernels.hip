@@ -879,6 +879,24 @@ __device__ __forceinline__ floatx4 mfma16(const bf16x8& a, const bf16x8& b, cons
 __device__ __forceinline__ bf16x8 ld8(const bf16_t* p) { return *reinterpret_cast<const bf16x8*>(p); }
 __device__ __forceinline__ bf16x8 zero8() { return __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u}); }
 
+// Chunk and sequence tables of the bf16 kernels: for fixed-length rows
+// (Tfix >= 0 tokens each) in closed form, for packed sequences (Tfix < 0) from
+// k_chunk_map's tables.
+__device__ __forceinline__ ChunkInfo chunk_at(const ChunkInfo* cmap, int c, int Tfix) {
+  if (Tfix >= 0) {
+    const int ncs = max(1, (Tfix + CH - 1) / CH), s = c / ncs, i = c - s * ncs;
+    return ChunkInfo{s * Tfix + i * CH, min(CH, Tfix - i * CH), s, 0};
+  }
+  return cmap[c];
+}
+__device__ __forceinline__ SeqInfo seq_at(const SeqInfo* smap, int s, int Tfix) {
+  if (Tfix >= 0) {
+    const int ncs = (Tfix + CH - 1) / CH;
+    return SeqInfo{s * ncs, ncs, s * Tfix, Tfix};
+  }
+  return smap[s];
+}
+
 // Element (row, col) of a 64-column operand tile that prep stores in MFMA
 // fragment order (M, A, M^T, A^T, Q^T): the 16 bytes lane (g, i) of wave w
 // loads for k-step ks (row 16 w + i, columns 32 ks + 8 g .. +7) sit at
@@ -970,7 +988,7 @@ template <int DK, bool BWD>
 __global__ __launch_bounds__(NTHR) void k_prep_bf(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const float* __restrict__ g,
     const bf16_t* __restrict__ beta, const float* __restrict__ d, const ChunkInfo* __restrict__ cmap,
-    int H, int16_t* __restrict__ Mq, float* __restrict__ Ms, int16_t* __restrict__ Aq,
+    int Tfix, int H, int16_t* __restrict__ Mq, float* __restrict__ Ms, int16_t* __restrict__ Aq,
     float* __restrict__ As, int16_t* __restrict__ MTq, float* __restrict__ MTs,
     int16_t* __restrict__ ATq, float* __restrict__ ATs, bf16_t* __restrict__ QTp,
     float* __restrict__ Gw, float* __restrict__ sink) {
@@ -989,7 +1007,7 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
   __shared__ float Gs[CH], Bs[CH];
   __shared__ float colmax[BWD ? NWAVE : 1][CH];  // per-wave column maxima of |A|
 
-  const ChunkInfo ci = cmap[blockIdx.x];
+  const ChunkInfo ci = chunk_at(cmap, blockIdx.x, Tfix);
   if (ci.len <= 0) return;
   const int h = blockIdx.y;
   const long chh = (long)blockIdx.x * H + h;
@@ -1169,7 +1187,7 @@ template <int DK, int DV, int BV, bool OUT, bool STORE>
 __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
     const bf16_t* __restrict__ beta, const float* __restrict__ d, const float* __restrict__ h0,
-    const SeqInfo* __restrict__ smap, int H, const int16_t* __restrict__ Mq,
+    const SeqInfo* __restrict__ smap, int Tfix, int H, const int16_t* __restrict__ Mq,
     const float* __restrict__ Ms, const int16_t* __restrict__ Aq, const float* __restrict__ As,
     const float* __restrict__ Gw, float* __restrict__ o, float* __restrict__ ht, int16_t* __restrict__ Xq,
     float* __restrict__ Xs, int16_t* __restrict__ Dq, float* __restrict__ Ds,
@@ -1195,7 +1213,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
   __shared__ __align__(16) bf16_t Kc[CH * LDKC];
 
   const int s = blockIdx.x, h = blockIdx.y, j0 = blockIdx.z * BV;
-  const SeqInfo si = smap[s];
+  const SeqInfo si = seq_at(smap, s, Tfix);
   const int w = wave_id(), lane = lane_id(), r16 = lane & 15, g4 = lane >> 4;
   const long soff = ((long)s * H + h) * DK * DV;
   const float dh = d[h];
@@ -1516,7 +1534,7 @@ template <int DK, int DV, int BV>
 __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ dO,
     const bf16_t* __restrict__ beta, const float* __restrict__ d, const float* __restrict__ dht,
-    const SeqInfo* __restrict__ smap, int H, const int16_t* __restrict__ MTq,
+    const SeqInfo* __restrict__ smap, int Tfix, int H, const int16_t* __restrict__ MTq,
     const float* __restrict__ MTs, const int16_t* __restrict__ ATq, const float* __restrict__ ATs,
     const bf16_t* __restrict__ QTp,
     const float* __restrict__ Gw, float* __restrict__ dh0, int16_t* __restrict__ Yq,
@@ -1537,7 +1555,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
   __shared__ __align__(16) bf16_t W2Tl[BV * LDR];
 
   const int s = blockIdx.x, h = blockIdx.y, j0 = blockIdx.z * BV;
-  const SeqInfo si = smap[s];
+  const SeqInfo si = seq_at(smap, s, Tfix);
   const int w = wave_id(), lane = lane_id(), r16 = lane & 15, g4 = lane >> 4;
   const long soff = ((long)s * H + h) * DK * DV;
   const float dh = d[h];
@@ -1879,7 +1897,7 @@ template <int DK, int DV>
 __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
     const bf16_t* __restrict__ dO, const bf16_t* __restrict__ beta, const float* __restrict__ d,
-    const ChunkInfo* __restrict__ cmap, int H, const float* __restrict__ Gw,
+    const ChunkInfo* __restrict__ cmap, int Tfix, int H, const float* __restrict__ Gw,
     const int16_t* __restrict__ Xq, const float* __restrict__ Xs, const int16_t* __restrict__ Dq,
     const float* __restrict__ Ds, const int16_t* __restrict__ Yq, const float* __restrict__ Ys,
     const int16_t* __restrict__ dRq, const float* __restrict__ dRs, int touch_ahead, float* __restrict__ dq, float* __restrict__ dk,
@@ -1899,7 +1917,7 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
 
   const int h = blockIdx.y;
   const long chh = (long)blockIdx.x * H + h;
-  const ChunkInfo ci = cmap[blockIdx.x];
+  const ChunkInfo ci = chunk_at(cmap, blockIdx.x, Tfix);
   if (ci.len <= 0) {
     if (threadIdx.x == 0) ddp[chh] = 0.f;
     return;
@@ -2099,7 +2117,7 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     const int lin2 = blockIdx.x + blockIdx.y * gridDim.x + touch_ahead;
     const int c2 = lin2 % gridDim.x, h2 = lin2 / gridDim.x;
     if (touch_ahead > 0 && h2 < (int)gridDim.y) {
-      const ChunkInfo ci2 = cmap[c2];
+      const ChunkInfo ci2 = chunk_at(cmap, c2, Tfix);
       if (ci2.len > 0) {
         const long chh2 = (long)c2 * H + h2, tok2 = (long)ci2.tok0 * H + h2;
         // lines: the first blocks of X, Y (DK rows x 64 bytes: DK / 2 lines
@@ -2396,27 +2414,31 @@ static hipError_t run_fwd_bf(const LaunchArgs& a) {
   const bf16_t* k = static_cast<const bf16_t*>(a.k);
   const bf16_t* v = static_cast<const bf16_t*>(a.v);
   const bf16_t* beta = static_cast<const bf16_t*>(a.beta);
-  a.stage("chunk_map");
-  k_chunk_map<<<1, NTHR, 0, st>>>(a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.ncmax, a.cmap, a.smap);
+  // fixed-length rows need no tables (closed form in the kernels)
+  const int Tfix = a.cu_seqlens ? -1 : a.Tseq;
+  if (Tfix < 0) {
+    a.stage("chunk_map");
+    k_chunk_map<<<1, NTHR, 0, st>>>(a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.ncmax, a.cmap, a.smap);
+  }
   a.stage(a.saved ? "prep_save" : "prep");
   if (a.ncmax > 0) {
     if (a.saved)
       k_prep_bf<DK, true><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
-          q, k, a.g, beta, a.d, a.cmap, a.H, a.Mq, a.Ms, a.Aq, a.As, a.MTq, a.MTs, a.ATq, a.ATs,
+          q, k, a.g, beta, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.MTq, a.MTs, a.ATq, a.ATs,
           a.QTp, a.Gw, a.sink);
     else
       k_prep_bf<DK, false><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
-          q, k, a.g, beta, a.d, a.cmap, a.H, a.Mq, a.Ms, a.Aq, a.As, nullptr, nullptr, nullptr,
+          q, k, a.g, beta, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, nullptr, nullptr, nullptr,
           nullptr, nullptr, a.Gw, a.sink);
   }
   a.stage(a.saved ? "scan_fwd_save" : "scan_fwd");
   if (a.saved)
     k_scan_fwd_bf<DK, DV, SCAN_BV, true, true><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-        q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, a.o, a.ht, a.Xq, a.Xs,
+        q, k, v, beta, a.d, a.h0, a.smap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, a.o, a.ht, a.Xq, a.Xs,
         a.Dq, a.Ds, a.Xfq, a.Xfs, a.sink);
   else
     k_scan_fwd_bf<DK, DV, SCAN_BV, true, false><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-        q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, a.o, a.ht, nullptr,
+        q, k, v, beta, a.d, a.h0, a.smap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, a.o, a.ht, nullptr,
         nullptr, nullptr, nullptr, nullptr, nullptr, a.sink);
   a.stage(nullptr);
   return hipGetLastError();
@@ -2434,27 +2456,31 @@ static hipError_t run_bwd_bf(const LaunchArgs& a) {
     k_reduce_dd<<<a.H, NTHR, 0, st>>>(a.ddp, 0, a.H, a.dd);
     return hipGetLastError();
   }
+  // fixed-length rows need no tables (closed form in the kernels)
+  const int Tfix = a.cu_seqlens ? -1 : a.Tseq;
   if (!a.saved) {
-    a.stage("chunk_map");
-    k_chunk_map<<<1, NTHR, 0, st>>>(a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.ncmax, a.cmap, a.smap);
+    if (Tfix < 0) {
+      a.stage("chunk_map");
+      k_chunk_map<<<1, NTHR, 0, st>>>(a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.ncmax, a.cmap, a.smap);
+    }
     a.stage("prep");
     if (a.ncmax > 0)
       k_prep_bf<DK, true><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
-          q, k, a.g, beta, a.d, a.cmap, a.H, a.Mq, a.Ms, a.Aq, a.As, a.MTq, a.MTs, a.ATq, a.ATs,
+          q, k, a.g, beta, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.MTq, a.MTs, a.ATq, a.ATs,
           a.QTp, a.Gw, a.sink);
     a.stage("scan_fwd_store");
     k_scan_fwd_bf<DK, DV, SCAN_BV, false, true><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-        q, k, v, beta, a.d, a.h0, a.smap, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, nullptr, nullptr, a.Xq,
+        q, k, v, beta, a.d, a.h0, a.smap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, nullptr, nullptr, a.Xq,
         a.Xs, a.Dq, a.Ds, a.Xfq, a.Xfs, a.sink);
   }
   a.stage("scan_bwd");
   k_scan_bwd_bf<DK, DV, SCAN_BV><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-      q, k, dO, beta, a.d, a.dht, a.smap, a.H, a.MTq, a.MTs, a.ATq, a.ATs, a.QTp, a.Gw, a.dh0, a.Yq,
+      q, k, dO, beta, a.d, a.dht, a.smap, Tfix, a.H, a.MTq, a.MTs, a.ATq, a.ATs, a.QTp, a.Gw, a.dh0, a.Yq,
       a.Ys, a.dRq, a.dRs, a.sink);
   a.stage("intra_bwd");
   if (a.ncmax > 0)
     k_intra_bwd_bf<DK, DV><<<dim3(a.ncmax, a.H), IB_THR, 0, st>>>(
-        q, k, v, dO, beta, a.d, a.cmap, a.H, a.Gw, a.Xq, a.Xs, a.Dq, a.Ds, a.Yq, a.Ys, a.dRq, a.dRs,
+        q, k, v, dO, beta, a.d, a.cmap, Tfix, a.H, a.Gw, a.Xq, a.Xs, a.Dq, a.Ds, a.Yq, a.Ys, a.dRq, a.dRs,
         device_cus(), a.dq, a.dk_, a.dv_, a.dbeta, a.dg, a.ddp, a.sink);
   a.stage("reduce_dd");
   k_reduce_dd<<<a.H, NTHR, 0, st>>>(a.ddp, a.ncmax, a.H, a.dd);
