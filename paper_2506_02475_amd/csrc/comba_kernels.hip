@@ -1900,7 +1900,7 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     const ChunkInfo* __restrict__ cmap, int Tfix, int H, const float* __restrict__ Gw,
     const int16_t* __restrict__ Xq, const float* __restrict__ Xs, const int16_t* __restrict__ Dq,
     const float* __restrict__ Ds, const int16_t* __restrict__ Yq, const float* __restrict__ Ys,
-    const int16_t* __restrict__ dRq, const float* __restrict__ dRs, int touch_ahead, float* __restrict__ dq, float* __restrict__ dk,
+    const int16_t* __restrict__ dRq, const float* __restrict__ dRs, int ncmax, float* __restrict__ dq, float* __restrict__ dk,
     float* __restrict__ dv, float* __restrict__ dbeta, float* __restrict__ dg,
     float* __restrict__ ddp, float* __restrict__ sink) {
   using SM = IntraBwdBfSmem<DK>;
@@ -1914,17 +1914,40 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
   __shared__ float colpart[4][CH];      // per row tile: column sums of E1 + E2
   __shared__ float rowacc[2][6][CH];    // per column half: E1, E2, BL, p1, p2, p3 row sums
   __shared__ float scal[NW][2];         // per wave: <X, Y>_F, sum k . dQ~
+  // The next item's first phase-1 block, copied from memory straight into LDS
+  // while this item is in phase 2 (which loads nothing else): the X, Y, dR, D
+  // blocks as stored, the dO and v rows of the first block pair, their scales.
+  // Every region is a whole number of 1 KiB pieces, one wave-wide 16-byte copy
+  // each.
+  constexpr int RX = 64 * DK, RD = 64 * CH, RP = 128 * CH;  // bytes: X or Y, dR or D, dO or v pair
+  constexpr int O_Y = RX, O_DR = 2 * RX, O_D = O_DR + RD, O_DO = O_D + RD, O_V = O_DO + RP;
+  constexpr int O_XS = O_V + RP, O_RS = O_XS + 1024, RAW = O_RS + 1024;
+  constexpr int NPIECE = RAW / 1024;
+  static_assert(RX % 1024 == 0 && RD % 1024 == 0 && 8 * DK <= 1024 && 8 * CH <= 1024, "1 KiB pieces");
+  __shared__ __align__(16) char R0[RAW];
 
-  const int h = blockIdx.y;
-  const long chh = (long)blockIdx.x * H + h;
-  const ChunkInfo ci = chunk_at(cmap, blockIdx.x, Tfix);
+  // Persistent: workgroup b takes items b, b + gridDim.x, ... (item = chunk +
+  // ncmax * head).
+  const int nitems = ncmax * H;
+  bool have = false;            // the item's first block is waiting in R0
+  float g_nx = 0.f, b_nx = 0.f;  // and its gates and beta, in registers
+  for (int item = blockIdx.x; item < nitems; item += gridDim.x) {
+  // The thread index passes through an opaque copy every item, so that the
+  // values derived from it are formed inside the loop instead of being held
+  // in registers across it.
+  int tid;
+  asm volatile("v_mov_b32 %0, %1" : "=v"(tid) : "v"((int)threadIdx.x));
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, r16 = lane & 15, g4 = lane >> 4;
+  const int rt = w & 3, ch = w >> 2;
+  const int h = item / ncmax;
+  const long chh = (long)(item % ncmax) * H + h;
+  const ChunkInfo ci = chunk_at(cmap, item % ncmax, Tfix);
   if (ci.len <= 0) {
-    if (threadIdx.x == 0) ddp[chh] = 0.f;
-    return;
+    if (tid == 0) ddp[chh] = 0.f;
+    have = false;
+    continue;
   }
   const long tok = (long)ci.tok0 * H + h;
-  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r16 = lane & 15, g4 = lane >> 4;
-  const int rt = w & 3, ch = w >> 2;
   const int len = ci.len;
   const float dh = d[h];
 
@@ -2022,10 +2045,34 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
   }
   dA[0] = dA[1] = dL[0] = dL[1] = zero4();
   TileRegs<bf16_t, CH, DK, IB_THR> kr, qr;
-  issue(0);
-  // gates and beta after the first block's loads, unconditional (clamped rows)
-  const float g_in = Gw[chh * CH + (tid & (CH - 1))];
-  const float b_in = bf2f(beta[tok + (long)min(tid & (CH - 1), len - 1) * H]);
+  float g_in, b_in;
+  if (have) {
+    // the copies into R0 were issued by this thread's wave; after the wait
+    // and the barrier every wave's copies are in place
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    r_do = *reinterpret_cast<const uint4*>(R0 + O_DO + pr * 128 + pc * 2);
+    r_v = *reinterpret_cast<const uint4*>(R0 + O_V + pr * 128 + pc * 2);
+    r_dr = *reinterpret_cast<const uint2*>(R0 + O_DR + pf_r * 64 + pf_c * 2);
+    r_d = *reinterpret_cast<const uint2*>(R0 + O_D + pf_r * 64 + pf_c * 2);
+    s_dr = *reinterpret_cast<const float*>(R0 + O_RS + 4 * pf_r);
+    s_d = *reinterpret_cast<const float*>(R0 + O_RS + 4 * CH + 4 * pf_r);
+#pragma unroll
+    for (int p = 0; p < XP; ++p) {
+      const int pc2 = tid + p * IB_THR, xr = pc2 >> 3, xc = (pc2 & 7) * 4;
+      r_x[p] = *reinterpret_cast<const uint2*>(R0 + xr * 64 + xc * 2);
+      r_y[p] = *reinterpret_cast<const uint2*>(R0 + O_Y + xr * 64 + xc * 2);
+      s_x[p] = *reinterpret_cast<const float*>(R0 + O_XS + 4 * xr);
+      s_y[p] = *reinterpret_cast<const float*>(R0 + O_XS + 4 * DK + 4 * xr);
+    }
+    g_in = g_nx;
+    b_in = b_nx;
+  } else {
+    issue(0);
+    // gates and beta after the first block's loads, unconditional (clamped rows)
+    g_in = Gw[chh * CH + (tid & (CH - 1))];
+    b_in = bf2f(beta[tok + (long)min(tid & (CH - 1), len - 1) * H]);
+  }
   // unrolled: a rolled loop carries the prefetched registers through copies at
   // the back edge, which wait for the loads just issued
 #pragma unroll
@@ -2106,36 +2153,53 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
   bf16_t* Ubl = Ubh + CH * LDC;
   kr.store(Ks, LDK);
   qr.store(Qs, LDK);
-  // Phase 2 reads nothing else from memory: warm L2 with the first phase-1
-  // block of the workgroup that runs touch_ahead workgroups later (dispatch is
-  // in linear order, round-robin over the XCDs, so with touch_ahead a multiple
-  // of their count it shares this L2).  One 4-byte load per 128-byte line, one
-  // line per thread; the value is consumed only at the very end, so no wait
-  // for it falls inside this workgroup's work.
-  uint32_t touched = 0;
+  // Phase 2 reads nothing else from memory: copy the next item's first block
+  // into R0 now (one wave-wide 16-byte copy per 1 KiB piece; rows past a chunk
+  // end repeat its last row).  The copies are invisible to the compiler's
+  // memory-counter bookkeeping: the next item waits for them explicitly.
   {
-    const int lin2 = blockIdx.x + blockIdx.y * gridDim.x + touch_ahead;
-    const int c2 = lin2 % gridDim.x, h2 = lin2 / gridDim.x;
-    if (touch_ahead > 0 && h2 < (int)gridDim.y) {
-      const ChunkInfo ci2 = chunk_at(cmap, c2, Tfix);
+    const int nx = item + gridDim.x;
+    have = false;
+    if (nx < nitems) {
+      const ChunkInfo ci2 = chunk_at(cmap, nx % ncmax, Tfix);
       if (ci2.len > 0) {
-        const long chh2 = (long)c2 * H + h2, tok2 = (long)ci2.tok0 * H + h2;
-        // lines: the first blocks of X, Y (DK rows x 64 bytes: DK / 2 lines
-        // each) and of dR, D (CH / 2 lines each), then the dO and v rows (one
-        // line each; their first 32 columns are the block)
-        static_assert(DK + 3 * CH <= IB_THR, "one line per thread");
-        static_assert((DK + CH) % CH == 0, "the dO and v rows start at a multiple of CH");
-        int t = tid;
-        const int rr = min(t & (CH - 1), ci2.len - 1);
-        const long b2 = chh2 * NB;  // block (chh2, 0)
-        const char* a = reinterpret_cast<const char*>(Xq + b2 * DK * VB);
-        if (t < DK / 2) a = reinterpret_cast<const char*>(Xq + b2 * DK * VB) + 128 * t;
-        else if ((t -= DK / 2) < DK / 2) a = reinterpret_cast<const char*>(Yq + b2 * DK * VB) + 128 * t;
-        else if ((t -= DK / 2) < CH / 2) a = reinterpret_cast<const char*>(dRq + b2 * CH * VB) + 128 * t;
-        else if ((t -= CH / 2) < CH / 2) a = reinterpret_cast<const char*>(Dq + b2 * CH * VB) + 128 * t;
-        else if ((t -= CH / 2) < CH) a = reinterpret_cast<const char*>(dO + (tok2 + (long)rr * H) * DV);
-        else if ((t -= CH) < CH) a = reinterpret_cast<const char*>(v + (tok2 + (long)rr * H) * DV);
-        touched = *reinterpret_cast<const uint32_t*>(a);
+        const int h2 = nx / ncmax;
+        const long chh2 = (long)(nx % ncmax) * H + h2, tok2 = (long)ci2.tok0 * H + h2;
+        const int len2 = ci2.len;
+        g_nx = Gw[chh2 * CH + (tid & (CH - 1))];
+        b_nx = bf2f(beta[tok2 + (long)min(tid & (CH - 1), len2 - 1) * H]);
+        const unsigned r0 = (unsigned)(size_t)(__attribute__((address_space(3))) void*)R0;
+        const char* xb = reinterpret_cast<const char*>(Xq + chh2 * NB * DK * VB);
+        const char* yb = reinterpret_cast<const char*>(Yq + chh2 * NB * DK * VB);
+        const char* rb = reinterpret_cast<const char*>(dRq + chh2 * NB * CH * VB);
+        const char* db = reinterpret_cast<const char*>(Dq + chh2 * NB * CH * VB);
+        for (int j = w; j < NPIECE; j += NW) {
+          const int o = 1024 * j;  // byte offset of the piece in R0
+          const char* src;
+          if (o < O_Y) src = xb + o + 16 * lane;
+          else if (o < O_DR) src = yb + (o - O_Y) + 16 * lane;
+          else if (o < O_D) src = rb + (o - O_DR) + 16 * lane;
+          else if (o < O_DO) src = db + (o - O_D) + 16 * lane;
+          else if (o < O_XS) {
+            const bf16_t* base = o < O_V ? dO : v;
+            const int row = min(8 * ((o - (o < O_V ? O_DO : O_V)) / 1024) + (lane >> 3), len2 - 1);
+            src = reinterpret_cast<const char*>(base + (tok2 + (long)row * H) * DV) + 16 * (lane & 7);
+          } else if (o < O_RS) {
+            // X then Y scales of block 0 (DK floats each); the rest repeats
+            const int l = lane < DK / 2 ? lane : lane & (DK / 4 - 1);
+            src = l < DK / 4 ? reinterpret_cast<const char*>(Xs + chh2 * NB * DK) + 16 * l
+                             : reinterpret_cast<const char*>(Ys + chh2 * NB * DK) + 16 * (l - DK / 4);
+          } else {
+            // dR then D scales of block 0 (CH floats each); the rest repeats
+            const int l = lane < CH / 2 ? lane : lane & (CH / 4 - 1);
+            src = l < CH / 4 ? reinterpret_cast<const char*>(dRs + chh2 * NB * CH) + 16 * l
+                             : reinterpret_cast<const char*>(Ds + chh2 * NB * CH) + 16 * (l - CH / 4);
+          }
+          const unsigned m0 = __builtin_amdgcn_readfirstlane(r0 + o);
+          asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                       :: "v"(src), "s"(m0) : "memory", "m0");
+        }
+        have = true;
       }
     }
   }
@@ -2327,8 +2391,10 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     }
     if (lane == 0) ddp[chh] = -dds;
   }
-  // keeps the warm-up load alive; a matching value only writes the sink
-  if (touched == 0x7fbfffffu) sink[tid & 255] = 0.f;
+  __syncthreads();  // the next item rewrites Gs, Bs
+  }
+  // no copy into R0 may still be in flight when the workgroup ends
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
 // ---------------------------------------------------------------------------
@@ -2341,6 +2407,13 @@ static int device_cus() {
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
     return 0;
   return cus > 0 ? cus : 0;
+}
+
+// Workgroups of the persistent k_intra_bwd_bf: one per CU (all items when the
+// CU count is unavailable).
+static unsigned intra_bwd_grid(long items) {
+  const int cus = device_cus();
+  return (unsigned)(cus > 0 && cus < items ? cus : items);
 }
 
 template <typename Tin, int DK, int DV>
@@ -2479,9 +2552,9 @@ static hipError_t run_bwd_bf(const LaunchArgs& a) {
       a.Ys, a.dRq, a.dRs, a.sink);
   a.stage("intra_bwd");
   if (a.ncmax > 0)
-    k_intra_bwd_bf<DK, DV><<<dim3(a.ncmax, a.H), IB_THR, 0, st>>>(
+    k_intra_bwd_bf<DK, DV><<<dim3(intra_bwd_grid((long)a.ncmax * a.H)), IB_THR, 0, st>>>(
         q, k, v, dO, beta, a.d, a.cmap, Tfix, a.H, a.Gw, a.Xq, a.Xs, a.Dq, a.Ds, a.Yq, a.Ys, a.dRq, a.dRs,
-        device_cus(), a.dq, a.dk_, a.dv_, a.dbeta, a.dg, a.ddp, a.sink);
+        a.ncmax, a.dq, a.dk_, a.dv_, a.dbeta, a.dg, a.ddp, a.sink);
   a.stage("reduce_dd");
   k_reduce_dd<<<a.H, NTHR, 0, st>>>(a.ddp, a.ncmax, a.H, a.dd);
   a.stage(nullptr);
