@@ -2195,9 +2195,13 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
             src = l < CH / 4 ? reinterpret_cast<const char*>(dRs + chh2 * NB * CH) + 16 * l
                              : reinterpret_cast<const char*>(Ds + chh2 * NB * CH) + 16 * (l - CH / 4);
           }
+          // M0 carries the LDS address; the instruction takes it at issue, and
+          // the previous M0 is restored (the compiler does not track M0 here)
           const unsigned m0 = __builtin_amdgcn_readfirstlane(r0 + o);
-          asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-                       :: "v"(src), "s"(m0) : "memory", "m0");
+          unsigned m0_saved;
+          asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\t"
+                       "global_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
+                       : "=&s"(m0_saved) : "v"(src), "s"(m0) : "memory");
         }
         have = true;
       }
