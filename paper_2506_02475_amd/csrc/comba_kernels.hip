@@ -1930,7 +1930,8 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
   // ncmax * head).
   const int nitems = ncmax * H;
   bool have = false;            // the item's first block is waiting in R0
-  float g_nx = 0.f, b_nx = 0.f;  // and its gates and beta, in registers
+  float g_nx = 0.f;              // and its gates
+  bf16_t b_nx = 0;               // and beta (raw: converted only when the item starts)
   for (int item = blockIdx.x; item < nitems; item += gridDim.x) {
   // The thread index passes through an opaque copy every item, so that the
   // values derived from it are formed inside the loop instead of being held
@@ -2066,7 +2067,7 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
       s_y[p] = *reinterpret_cast<const float*>(R0 + O_XS + 4 * DK + 4 * xr);
     }
     g_in = g_nx;
-    b_in = b_nx;
+    b_in = bf2f(b_nx);
   } else {
     issue(0);
     // gates and beta after the first block's loads, unconditional (clamped rows)
@@ -2158,52 +2159,46 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
   // end repeat its last row).  The copies are invisible to the compiler's
   // memory-counter bookkeeping: the next item waits for them explicitly.
   {
-    const int nx = item + gridDim.x;
-    have = false;
-    if (nx < nitems) {
-      const ChunkInfo ci2 = chunk_at(cmap, nx % ncmax, Tfix);
-      if (ci2.len > 0) {
-        const int h2 = nx / ncmax;
-        const long chh2 = (long)(nx % ncmax) * H + h2, tok2 = (long)ci2.tok0 * H + h2;
-        const int len2 = ci2.len;
-        g_nx = Gw[chh2 * CH + (tid & (CH - 1))];
-        b_nx = bf2f(beta[tok2 + (long)min(tid & (CH - 1), len2 - 1) * H]);
-        const unsigned r0 = (unsigned)(size_t)(__attribute__((address_space(3))) void*)R0;
-        const char* xb = reinterpret_cast<const char*>(Xq + chh2 * NB * DK * VB);
-        const char* yb = reinterpret_cast<const char*>(Yq + chh2 * NB * DK * VB);
-        const char* rb = reinterpret_cast<const char*>(dRq + chh2 * NB * CH * VB);
-        const char* db = reinterpret_cast<const char*>(Dq + chh2 * NB * CH * VB);
-        for (int j = w; j < NPIECE; j += NW) {
-          const int o = 1024 * j;  // byte offset of the piece in R0
-          const char* src;
-          if (o < O_Y) src = xb + o + 16 * lane;
-          else if (o < O_DR) src = yb + (o - O_Y) + 16 * lane;
-          else if (o < O_D) src = rb + (o - O_DR) + 16 * lane;
-          else if (o < O_DO) src = db + (o - O_D) + 16 * lane;
-          else if (o < O_XS) {
-            const bf16_t* base = o < O_V ? dO : v;
-            const int row = min(8 * ((o - (o < O_V ? O_DO : O_V)) / 1024) + (lane >> 3), len2 - 1);
-            src = reinterpret_cast<const char*>(base + (tok2 + (long)row * H) * DV) + 16 * (lane & 7);
-          } else if (o < O_RS) {
-            // X then Y scales of block 0 (DK floats each); the rest repeats
-            const int l = lane < DK / 2 ? lane : lane & (DK / 4 - 1);
-            src = l < DK / 4 ? reinterpret_cast<const char*>(Xs + chh2 * NB * DK) + 16 * l
-                             : reinterpret_cast<const char*>(Ys + chh2 * NB * DK) + 16 * (l - DK / 4);
-          } else {
-            // dR then D scales of block 0 (CH floats each); the rest repeats
-            const int l = lane < CH / 2 ? lane : lane & (CH / 4 - 1);
-            src = l < CH / 4 ? reinterpret_cast<const char*>(dRs + chh2 * NB * CH) + 16 * l
-                             : reinterpret_cast<const char*>(Ds + chh2 * NB * CH) + 16 * (l - CH / 4);
-          }
-          // M0 carries the LDS address; the instruction takes it at issue, and
-          // the previous M0 is restored (the compiler does not track M0 here)
-          const unsigned m0 = __builtin_amdgcn_readfirstlane(r0 + o);
-          unsigned m0_saved;
-          asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\t"
-                       "global_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
-                       : "=&s"(m0_saved) : "v"(src), "s"(m0) : "memory");
+    const int nx = item + gridDim.x, nxc = min(nx, nitems - 1);
+    const ChunkInfo ci2 = chunk_at(cmap, nxc % ncmax, Tfix);
+    const int h2 = nxc / ncmax, len2 = ci2.len;
+    const long chh2 = (long)(nxc % ncmax) * H + h2, tok2 = (long)ci2.tok0 * H + h2;
+    have = nx < nitems && len2 > 0;
+    if (have) {
+      const unsigned r0 = (unsigned)(size_t)(__attribute__((address_space(3))) void*)R0;
+      const char* xb = reinterpret_cast<const char*>(Xq + chh2 * NB * DK * VB);
+      const char* yb = reinterpret_cast<const char*>(Yq + chh2 * NB * DK * VB);
+      const char* rb = reinterpret_cast<const char*>(dRq + chh2 * NB * CH * VB);
+      const char* db = reinterpret_cast<const char*>(Dq + chh2 * NB * CH * VB);
+      for (int j = w; j < NPIECE; j += NW) {
+        const int o = 1024 * j;  // byte offset of the piece in R0
+        const char* src;
+        if (o < O_Y) src = xb + o + 16 * lane;
+        else if (o < O_DR) src = yb + (o - O_Y) + 16 * lane;
+        else if (o < O_D) src = rb + (o - O_DR) + 16 * lane;
+        else if (o < O_DO) src = db + (o - O_D) + 16 * lane;
+        else if (o < O_XS) {
+          const bf16_t* base = o < O_V ? dO : v;
+          const int row = min(8 * ((o - (o < O_V ? O_DO : O_V)) / 1024) + (lane >> 3), len2 - 1);
+          src = reinterpret_cast<const char*>(base + (tok2 + (long)row * H) * DV) + 16 * (lane & 7);
+        } else if (o < O_RS) {
+          // X then Y scales of block 0 (DK floats each); the rest repeats
+          const int l = lane < DK / 2 ? lane : lane & (DK / 4 - 1);
+          src = l < DK / 4 ? reinterpret_cast<const char*>(Xs + chh2 * NB * DK) + 16 * l
+                           : reinterpret_cast<const char*>(Ys + chh2 * NB * DK) + 16 * (l - DK / 4);
+        } else {
+          // dR then D scales of block 0 (CH floats each); the rest repeats
+          const int l = lane < CH / 2 ? lane : lane & (CH / 4 - 1);
+          src = l < CH / 4 ? reinterpret_cast<const char*>(dRs + chh2 * NB * CH) + 16 * l
+                           : reinterpret_cast<const char*>(Ds + chh2 * NB * CH) + 16 * (l - CH / 4);
         }
-        have = true;
+        // M0 carries the LDS address; the instruction takes it at issue, and
+        // the previous M0 is restored (the compiler does not track M0 here)
+        const unsigned m0 = __builtin_amdgcn_readfirstlane(r0 + o);
+        unsigned m0_saved;
+        asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\t"
+                     "global_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
+                     : "=&s"(m0_saved) : "v"(src), "s"(m0) : "memory");
       }
     }
   }
@@ -2357,6 +2352,19 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
         dk[off] = dkv[e];
       }
     }
+  }
+  {
+    // The next item's gates and beta, after this item's last loads and stores:
+    // a wait for them (in-order counters) is then a wait for everything, so
+    // they must not be needed earlier.  Unconditional, from a clamped item and
+    // row (this item has tokens, so every such address is valid): behind a
+    // branch, the merge would copy them and wait right there.
+    const int nxc = min(item + (int)gridDim.x, nitems - 1);
+    const ChunkInfo ci2 = chunk_at(cmap, nxc % ncmax, Tfix);
+    const int h2 = nxc / ncmax;
+    const long chh2 = (long)(nxc % ncmax) * H + h2, tok2 = (long)ci2.tok0 * H + h2;
+    g_nx = Gw[chh2 * CH + (tid & (CH - 1))];
+    b_nx = beta[tok2 + (long)min(tid & (CH - 1), max(ci2.len, 1) - 1) * H];
   }
   ddpart = wave_sum(ddpart);
   if (lane == 0) scal[w][1] = ddpart;
