@@ -1922,8 +1922,9 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
   constexpr int RX = 64 * DK, RD = 64 * CH, RP = 128 * CH;  // bytes: X or Y, dR or D, dO or v pair
   constexpr int O_Y = RX, O_DR = 2 * RX, O_D = O_DR + RD, O_DO = O_D + RD, O_V = O_DO + RP;
   constexpr int O_XS = O_V + RP, O_RS = O_XS + 1024, RAW = O_RS + 1024;
-  constexpr int NPIECE = RAW / 1024;
   static_assert(RX % 1024 == 0 && RD % 1024 == 0 && 8 * DK <= 1024 && 8 * CH <= 1024, "1 KiB pieces");
+  static_assert(2 * (RX / 1024) % NW == 0 && 2 * (RD / 1024) == NW && RP / 1024 == NW,
+                "the copies take whole rounds of one piece per wave");
   __shared__ __align__(16) char R0[RAW];
 
   // Persistent: workgroup b takes items b, b + gridDim.x, ... (item = chunk +
@@ -2165,40 +2166,52 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     const long chh2 = (long)(nxc % ncmax) * H + h2, tok2 = (long)ci2.tok0 * H + h2;
     have = nx < nitems && len2 > 0;
     if (have) {
+      // Straight-line rounds of one 1 KiB piece per wave: every wave would
+      // otherwise run the same per-piece selection on the CU's one scalar unit.
       const unsigned r0 = (unsigned)(size_t)(__attribute__((address_space(3))) void*)R0;
-      const char* xb = reinterpret_cast<const char*>(Xq + chh2 * NB * DK * VB);
-      const char* yb = reinterpret_cast<const char*>(Yq + chh2 * NB * DK * VB);
-      const char* rb = reinterpret_cast<const char*>(dRq + chh2 * NB * CH * VB);
-      const char* db = reinterpret_cast<const char*>(Dq + chh2 * NB * CH * VB);
-      for (int j = w; j < NPIECE; j += NW) {
-        const int o = 1024 * j;  // byte offset of the piece in R0
-        const char* src;
-        if (o < O_Y) src = xb + o + 16 * lane;
-        else if (o < O_DR) src = yb + (o - O_Y) + 16 * lane;
-        else if (o < O_D) src = rb + (o - O_DR) + 16 * lane;
-        else if (o < O_DO) src = db + (o - O_D) + 16 * lane;
-        else if (o < O_XS) {
-          const bf16_t* base = o < O_V ? dO : v;
-          const int row = min(8 * ((o - (o < O_V ? O_DO : O_V)) / 1024) + (lane >> 3), len2 - 1);
-          src = reinterpret_cast<const char*>(base + (tok2 + (long)row * H) * DV) + 16 * (lane & 7);
-        } else if (o < O_RS) {
-          // X then Y scales of block 0 (DK floats each); the rest repeats
-          const int l = lane < DK / 2 ? lane : lane & (DK / 4 - 1);
-          src = l < DK / 4 ? reinterpret_cast<const char*>(Xs + chh2 * NB * DK) + 16 * l
-                           : reinterpret_cast<const char*>(Ys + chh2 * NB * DK) + 16 * (l - DK / 4);
-        } else {
-          // dR then D scales of block 0 (CH floats each); the rest repeats
-          const int l = lane < CH / 2 ? lane : lane & (CH / 4 - 1);
-          src = l < CH / 4 ? reinterpret_cast<const char*>(dRs + chh2 * NB * CH) + 16 * l
-                           : reinterpret_cast<const char*>(Ds + chh2 * NB * CH) + 16 * (l - CH / 4);
-        }
+      auto copy = [&](int off, const char* src) {
         // M0 carries the LDS address; the instruction takes it at issue, and
         // the previous M0 is restored (the compiler does not track M0 here)
-        const unsigned m0 = __builtin_amdgcn_readfirstlane(r0 + o);
+        const unsigned m0 = __builtin_amdgcn_readfirstlane(r0 + off);
         unsigned m0_saved;
         asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\t"
                      "global_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
                      : "=&s"(m0_saved) : "v"(src), "s"(m0) : "memory");
+      };
+      const char* xb = reinterpret_cast<const char*>(Xq + chh2 * NB * DK * VB);
+      const char* yb = reinterpret_cast<const char*>(Yq + chh2 * NB * DK * VB);
+      const char* rb = reinterpret_cast<const char*>(dRq + chh2 * NB * CH * VB);
+      const char* db = reinterpret_cast<const char*>(Dq + chh2 * NB * CH * VB);
+      // X then Y blocks (RX / 1024 pieces each)
+#pragma unroll
+      for (int i = 0; i < 2 * (RX / 1024) / NW; ++i) {
+        const int j = i * NW + w;
+        const char* src = j < RX / 1024 ? xb + 1024 * j : yb + 1024 * (j - RX / 1024);
+        copy(1024 * j, src + 16 * lane);
+      }
+      // dR then D blocks, one round
+      {
+        const char* src = w < RD / 1024 ? rb + 1024 * w : db + 1024 * (w - RD / 1024);
+        copy(O_DR + 1024 * w, src + 16 * lane);
+      }
+      // dO and v rows of the first block pair, 8 rows per piece (rows past the
+      // chunk end repeat its last row)
+      {
+        const long row = min(8 * w + (lane >> 3), len2 - 1);
+        const long e = (tok2 + row * H) * DV + 8 * (lane & 7);
+        copy(O_DO + 1024 * w, reinterpret_cast<const char*>(dO + e));
+        copy(O_V + 1024 * w, reinterpret_cast<const char*>(v + e));
+      }
+      if (w == 0) {
+        // X then Y scales of block 0 (DK floats each); the rest repeats
+        const int l = lane < DK / 2 ? lane : lane & (DK / 4 - 1);
+        copy(O_XS, l < DK / 4 ? reinterpret_cast<const char*>(Xs + chh2 * NB * DK) + 16 * l
+                              : reinterpret_cast<const char*>(Ys + chh2 * NB * DK) + 16 * (l - DK / 4));
+      } else if (w == 1) {
+        // dR then D scales of block 0 (CH floats each); the rest repeats
+        const int l = lane < CH / 2 ? lane : lane & (CH / 4 - 1);
+        copy(O_RS, l < CH / 4 ? reinterpret_cast<const char*>(dRs + chh2 * NB * CH) + 16 * l
+                              : reinterpret_cast<const char*>(Ds + chh2 * NB * CH) + 16 * (l - CH / 4));
       }
     }
   }
