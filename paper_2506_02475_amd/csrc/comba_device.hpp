@@ -185,6 +185,19 @@ __device__ __forceinline__ int qt_col() { return lane_id() & 12; }
 __device__ __forceinline__ void store4(float* p, const floatx4& x) {
   *reinterpret_cast<float4*>(p) = make_float4(x[0], x[1], x[2], x[3]);
 }
+// An element at a per-lane byte offset from a wave-uniform base pointer: the
+// compiler keeps the base in SGPRs and the offset in one VGPR (global
+// addressing with a scalar base), instead of 64-bit per-lane address arithmetic.
+// The offset is unsigned 32-bit: callers keep it below 2^32 (offsets inside one
+// chunk or chunk-head).
+template <typename T>
+__device__ __forceinline__ T& at(T* base, unsigned byte_off) {
+  return *reinterpret_cast<T*>(reinterpret_cast<char*>(base) + byte_off);
+}
+template <typename T>
+__device__ __forceinline__ const T& at(const T* base, unsigned byte_off) {
+  return *reinterpret_cast<const T*>(reinterpret_cast<const char*>(base) + byte_off);
+}
 
 // ---- int16 fixed-point row blocks -----------------------------------------
 // The chunk states and pseudo-values that the scans hand to the backward

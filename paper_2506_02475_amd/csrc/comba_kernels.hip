@@ -1979,25 +1979,36 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
   uint2 r_dr, r_d, r_x[XP], r_y[XP];
   float s_dr, s_d, s_x[XP], s_y[XP];
   static_assert(NVB % 2 == 0 && CH * 8 == IB_THR, "dO / v pairs: one 16-byte piece per thread");
+  // this chunk-head's operands: scalar bases, 32-bit per-lane byte offsets
+  const bf16_t* dO_i = dO + tok * DV;  // row r at r H DV
+  const bf16_t* v_i = v + tok * DV;
+  const int16_t* dRq_i = dRq + chh * NB * CH * VB;  // [block][row][32]
+  const int16_t* Dq_i = Dq + chh * NB * CH * VB;
+  const float* dRs_i = dRs + chh * NB * CH;         // [block][row]
+  const float* Ds_i = Ds + chh * NB * CH;
+  const int16_t* Xq_i = Xq + chh * NB * DK * VB;
+  const int16_t* Yq_i = Yq + chh * NB * DK * VB;
+  const float* Xs_i = Xs + chh * NB * DK;
+  const float* Ys_i = Ys + chh * NB * DK;
   auto issue = [&](int vb) {
     if (vb % 2 == 0) {
-      const long rb = (tok + (long)min(pr, len - 1) * H) * DV + vb * VB + pc;
-      r_do = *reinterpret_cast<const uint4*>(dO + rb);
-      r_v = *reinterpret_cast<const uint4*>(v + rb);
+      const unsigned rb = 2u * ((unsigned)min(pr, len - 1) * (H * DV) + vb * VB + pc);
+      r_do = at(reinterpret_cast<const uint4*>(dO_i), rb);
+      r_v = at(reinterpret_cast<const uint4*>(v_i), rb);
     }
-    const long rr = (chh * NB + vb) * CH + pf_r;
-    r_dr = *reinterpret_cast<const uint2*>(dRq + rr * VB + pf_c);
-    r_d = *reinterpret_cast<const uint2*>(Dq + rr * VB + pf_c);
-    s_dr = dRs[rr];
-    s_d = Ds[rr];
+    const unsigned rr = vb * CH + pf_r;
+    r_dr = at(reinterpret_cast<const uint2*>(dRq_i), 2u * (rr * VB + pf_c));
+    r_d = at(reinterpret_cast<const uint2*>(Dq_i), 2u * (rr * VB + pf_c));
+    s_dr = at(dRs_i, 4u * rr);
+    s_d = at(Ds_i, 4u * rr);
 #pragma unroll
     for (int p = 0; p < XP; ++p) {
       const int pc = tid + p * IB_THR, xr = pc >> 3, xc = (pc & 7) * 4;
-      const long xrow = (chh * NB + vb) * DK + xr;
-      r_x[p] = *reinterpret_cast<const uint2*>(Xq + xrow * VB + xc);
-      r_y[p] = *reinterpret_cast<const uint2*>(Yq + xrow * VB + xc);
-      s_x[p] = Xs[xrow];
-      s_y[p] = Ys[xrow];
+      const unsigned xrow = vb * DK + xr;
+      r_x[p] = at(reinterpret_cast<const uint2*>(Xq_i), 2u * (xrow * VB + xc));
+      r_y[p] = at(reinterpret_cast<const uint2*>(Yq_i), 2u * (xrow * VB + xc));
+      s_x[p] = at(Xs_i, 4u * xrow);
+      s_y[p] = at(Ys_i, 4u * xrow);
     }
     // keep the loads here: the scheduler otherwise sinks some of them to their
     // use one block later, where they are waited for at once
@@ -2005,6 +2016,7 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
   };
   float Fpart = 0.f, bv = 0.f;
   float4 fdr;  // this thread's dR piece, kept for <v_r, dR_r> after the barrier
+  float* dv_i = dv + tok * DV;
   auto put = [&](int vb) {
     const int j = vb * VB;
     if (pb == (vb & 1)) {
@@ -2034,7 +2046,7 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     // dv = Diag(beta) dR
     const float b = Bs[pf_r];
     const float4 dvv = make_float4(b * fdr.x, b * fdr.y, b * fdr.z, b * fdr.w);
-    float* dst = pf_r < len ? dv + (tok + (long)pf_r * H) * DV + j + pf_c : sink + (tid & 63) * 4;
+    float* dst = pf_r < len ? &at(dv_i, 4u * ((unsigned)pf_r * (H * DV) + j + pf_c)) : sink + (tid & 63) * 4;
     *reinterpret_cast<float4*>(dst) = dvv;
   };
 
@@ -2344,6 +2356,8 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     }
   }
   float ddpart = 0.f;
+  float* dq_i = dq + tok * DK;  // this chunk's rows: row r at r H DK
+  float* dk_i = dk + tok * DK;
 #pragma unroll
   for (int j = 0; j < NTW; ++j) {
     floatx4 dkv;
@@ -2359,10 +2373,10 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int r = 16 * rt + 4 * g4 + e;
-      const long off = (tok + (long)r * H) * DK + 16 * (ch * NTW + j) + r16;
+      const unsigned off = 4u * ((unsigned)r * (H * DK) + 16 * (ch * NTW + j) + r16);
       if (r < len) {
-        dq[off] = T1[j][e];
-        dk[off] = dkv[e];
+        at(dq_i, off) = T1[j][e];
+        at(dk_i, off) = dkv[e];
       }
     }
   }
@@ -2411,8 +2425,8 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     x = wave_prefix_sum(x);
     const float dgr = __shfl(x, 63 - lane);
     if (r < len) {
-      dg[tok + (long)r * H] = dgr;
-      dbeta[tok + (long)r * H] = rowb;
+      at(dg + tok, 4u * (r * H)) = dgr;
+      at(dbeta + tok, 4u * (r * H)) = rowb;
     }
     if (lane == 0) ddp[chh] = -dds;
   }
