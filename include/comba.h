@@ -40,6 +40,10 @@
     bytes, the other fp32 tensors 4 bytes and beta its element size; any other
     pointer is rejected with COMBA_ERR_ALIGN.
   - Outputs must not alias inputs; outputs are overwritten, never accumulated.
+  - A call without tokens (T == 0 or B == 0) is valid: the per-token tensors
+    (q, k, v, g, beta, o, dO, dq, dk, dv, dg, dbeta) may then be NULL, and the
+    states pass through (ht = h0, dh0 = dht, dd = 0).  Empty sequences inside a
+    packed batch behave the same way for their own states.
  *  - Calls on different streams with distinct workspaces may run concurrently;
  *    a workspace must not be shared by calls that overlap in time.
  */

@@ -218,7 +218,9 @@ comba_status chunk_fwd(bool save, const comba_shape* shape, const void* q, const
   Dims dm;
   comba_status st = check_shape(shape, &dm);
   if (st != COMBA_OK) return st;
-  if (!q || !k || !v || !g || !beta || !d || !o || !ws) return COMBA_ERR_NULL;
+  // token tensors may be NULL when the call has no tokens (states pass through)
+  const bool tok = dm.Ttot > 0;
+  if ((tok && (!q || !k || !v || !g || !beta || !o)) || !d || !ws) return COMBA_ERR_NULL;
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(ws, kAlign) ||
       !aligned(g, 4) || !aligned(d, 4) || !aligned(o, 16) || (h0 && !aligned(h0, 16)) ||
       (ht && !aligned(ht, 16)) || !aligned(beta, dm.bf16 ? 2 : 4))
@@ -252,8 +254,10 @@ comba_status chunk_bwd(bool saved, const comba_shape* shape, const void* q, cons
   Dims dm;
   comba_status st = check_shape(shape, &dm);
   if (st != COMBA_OK) return st;
-  if (!q || !k || !v || !g || !beta || !d || !dO || !dq || !dk || !dv || !dg || !dbeta || !dd ||
-      !ws)
+  // token tensors may be NULL when the call has no tokens (states pass through)
+  const bool tok = dm.Ttot > 0;
+  if ((tok && (!q || !k || !v || !g || !beta || !dO || !dq || !dk || !dv || !dg || !dbeta)) ||
+      !d || !dd || !ws)
     return COMBA_ERR_NULL;
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(dO, 16) ||
       !aligned(ws, kAlign) || !aligned(g, 4) || !aligned(d, 4) || !aligned(dq, 16) ||

@@ -127,6 +127,23 @@ def test_rejects_null_and_misaligned_pointers():
                                ctypes.c_size_t(1 << 40), None) == ENULL
 
 
+def test_token_free_calls_accept_null_token_tensors():
+    # no tokens (T == 0 or B == 0): the per-token tensors may be NULL and the
+    # states pass through; d, dd and the workspace stay required.  A one-byte
+    # workspace makes the next check fail, so nothing is launched.
+    token_fwd = ("q", "k", "v", "g", "beta", "o")
+    token_bwd = ("q", "k", "v", "g", "beta", "dO", "dq", "dk", "dv", "dg", "dbeta")
+    for s in (shape(T=0), shape(B=0), shape(T=0, cu=FAKE, N=3)):
+        assert fwd(s, ws_bytes=1, **{n: None for n in token_fwd}) == EWS
+        assert bwd(s, ws_bytes=1, **{n: None for n in token_bwd}) == EWS
+        assert fwd(s, ws_bytes=1, d=None) == ENULL
+        assert fwd(s, ws_bytes=1, ws=None) == ENULL
+        assert bwd(s, ws_bytes=1, dd=None) == ENULL
+    # with tokens they are required as before
+    assert fwd(shape(T=1), ws_bytes=1, q=None) == ENULL
+    assert bwd(shape(T=1), ws_bytes=1, dbeta=None) == ENULL
+
+
 def test_saved_pair_validates_like_the_plain_calls():
     lib = comba.load_library()
     P = ctypes.c_void_p

@@ -105,6 +105,43 @@ def test_long_weak_decay_errors_stay_bounded():
     _log("long weak decay fwd %s bwd %s" % (ef, eb))
 
 
+@pytest.mark.parametrize("kw", [dict(B=2, T=0), dict(B=0, T=64), dict(B=1, T=0, seqlens=[0, 0, 0])],
+                         ids=["T0", "B0", "all_empty_varlen"])
+def test_token_free_calls_pass_states_through(kw):
+    # no tokens: the token tensors are empty (NULL data pointers), ht = h0,
+    # dh0 = dht and dd = 0 exactly
+    w = random_case(seed=5, H=2, dk=128, dv=128, in_dtype="bf16", dht=True, **kw)
+    o, ht = gpu_fwd(w)
+    assert o.size == 0 and np.array_equal(ht, w.h0)
+    gr = gpu_bwd(w)
+    assert np.array_equal(gr["dh0"], w.dht) and np.all(gr["dd"] == 0)
+    for name in ("dq", "dk", "dv", "dg", "dbeta"):
+        assert gr[name].size == 0, name
+
+
+@pytest.mark.parametrize("which", ["beta0", "g0", "d0", "k0"])
+def test_degenerate_parameters(which):
+    # beta = 0: nothing is written (the state only decays); g = 0: no decay;
+    # d = 0: no output correction; k = 0: every key is zero (L = 0, M = I)
+    w = random_case(seed=7, B=1, T=200, H=2, dk=128, dv=128, in_dtype="bf16", dht=True)
+    if which == "beta0":
+        w.beta[:] = 0.0
+    elif which == "g0":
+        w.g[:] = 0.0
+    elif which == "d0":
+        w.d[:] = 0.0
+    else:
+        w.k[:] = 0.0
+    if which in ("beta0", "k0"):
+        # weak decay: with nothing written, the state is h0 decayed by every
+        # gate; at the usual gates that is ~exp(-140) after 200 tokens, below
+        # the fp32 range (the oracle's fp64 value would be the only nonzero)
+        w.g *= np.float32(0.02)
+    ef = check_fwd(w)
+    eb = check_bwd(w)
+    _log("degenerate %s fwd %s bwd %s" % (which, ef, eb))
+
+
 def test_deterministic_bitwise():
     w = random_case(B=2, T=300, H=2, dk=128, dv=128, in_dtype="bf16", dht=True)
     a = gpu_bwd(w)
