@@ -211,19 +211,20 @@ __device__ __forceinline__ int q_exponent(float m) {  // e with m < 2^e, m >= 0
   return max(((__float_as_int(m) >> 23) & 0xFF) - 126, -100);
 }
 __device__ __forceinline__ float q_scale(float m) { return __int_as_float((q_exponent(m) + 112) << 23); }
+// 1 / s, divided by 32767 for the snorm16 conversion in q_pack4
 __device__ __forceinline__ float q_inv_scale(float m) {
-  return __int_as_float((142 - q_exponent(m)) << 23);
+  return __int_as_float((142 - q_exponent(m)) << 23) * (1.0f / 32767.0f);
 }
-// four values (times the inverse scale) -> four int16, nearest, saturated
+// four values (times the inverse scale) -> four int16 q = round(x / s),
+// saturated to +-32767: v_cvt_pknorm_i16_f32 rounds 32767 y to the nearest
+// integer after clamping y to [-1, 1] and packs two results (first argument in
+// the low half; checked on the device with an in-bounds probe).  The factor
+// 1/32767 in the inverse scale is rounded, so q can differ from round(x / s)
+// by one only where x / s lies within 2^-9 of a half-integer.
 __device__ __forceinline__ uint2 q_pack4(const floatx4& x, float inv) {
-  uint32_t w[2];
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int a = min(max((int)__builtin_rintf(x[2 * h] * inv), -32767), 32767);
-    const int b = min(max((int)__builtin_rintf(x[2 * h + 1] * inv), -32767), 32767);
-    w[h] = ((uint32_t)a & 0xFFFFu) | ((uint32_t)b << 16);
-  }
-  return make_uint2(w[0], w[1]);
+  const auto a = __builtin_amdgcn_cvt_pknorm_i16(x[0] * inv, x[1] * inv);
+  const auto b = __builtin_amdgcn_cvt_pknorm_i16(x[2] * inv, x[3] * inv);
+  return make_uint2(__builtin_bit_cast(uint32_t, a), __builtin_bit_cast(uint32_t, b));
 }
 __device__ __forceinline__ float4 q_unpack4(uint2 u, float s) {
   return make_float4((float)(int)(int16_t)(u.x & 0xFFFFu) * s, (float)((int)u.x >> 16) * s,
