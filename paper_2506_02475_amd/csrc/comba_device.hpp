@@ -199,6 +199,19 @@ __device__ __forceinline__ const T& at(const T* base, unsigned byte_off) {
   return *reinterpret_cast<const T*>(reinterpret_cast<const char*>(base) + byte_off);
 }
 
+// Max over the four lanes r16, r16 + 16, r16 + 32, r16 + 48 (the lanes that
+// hold one row of a transposed MFMA accumulator) of values >= 0:
+// v_permlane16_swap / v_permlane32_swap with both operands x hand lane l the
+// values of lanes l & ~16 and l | 16 (resp. 32) (checked with an in-bounds
+// probe); non-negative floats order like their bit patterns.
+__device__ __forceinline__ float rowgroup_max(float m) {
+  const unsigned x = __float_as_uint(m);
+  const auto a = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+  const unsigned y = max(a[0], a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(y, y, false, false);
+  return __uint_as_float(max(b[0], b[1]));
+}
+
 // ---- int16 fixed-point row blocks -----------------------------------------
 // The chunk states and pseudo-values that the scans hand to the backward
 // gradient kernel are stored as int16 q with one power-of-two scale s per

@@ -1182,7 +1182,12 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
 
 // Forward state scan (bf16 inputs).  One workgroup per (sequence, head,
 // 32-wide dv slice); wave w owns rows 16w..16w+15 of the chunk products and
-// rows (dk/4)w.. of the state slice.
+// rows (dk/4)w.. of the state slice.  Every product is formed transposed (the
+// MFMA operands swapped), so that an accumulator gives a lane one row and four
+// consecutive columns: rows leave for memory as they are (no transposes), a
+// lane needs the gates and beta of one row only, and the intermediate tiles
+// (state, R, D, Dg) sit row-major in LDS, read as operands with transposing
+// reads.
 template <int DK, int DV, int BV, bool OUT, bool STORE>
 __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
@@ -1197,18 +1202,22 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
   // stores sent to `sink`), so the memory-counter waits stay exact and the
   // next chunk's loads overlap the current chunk's work.
   constexpr int NTV = BV / 16, XMT = DK / 64, KS = DK / 32, CC = CH * CH;
-  constexpr int LDX = DK + 8, LDR = CH + 8, NB = DV / 32;
+  constexpr int NB = DV / 32;
+  // row-major BV-wide tiles: 72-byte rows put the four rows of a transposing
+  // read on disjoint banks
+  constexpr int LDT = BV + 4;
   static_assert(BV == 32, "stored states use one scale per 32-column block = one dv slice");
-  __shared__ __align__(16) bf16_t XTh[BV * LDX];
-  __shared__ __align__(16) bf16_t XTl[BV * LDX];
-  __shared__ __align__(16) bf16_t RTh[BV * LDR];
-  __shared__ __align__(16) bf16_t RTl[BV * LDR];
-  __shared__ __align__(16) bf16_t DgTh[BV * LDR];
-  __shared__ __align__(16) bf16_t DgTl[BV * LDR];
-  __shared__ __align__(16) bf16_t DTh[OUT ? BV * LDR : 8];
-  __shared__ __align__(16) bf16_t DTl[OUT ? BV * LDR : 8];
+  __shared__ __align__(16) bf16_t Xh[DK * LDT];
+  __shared__ __align__(16) bf16_t Xl[DK * LDT];
+  __shared__ __align__(16) bf16_t Rh[CH * LDT];
+  __shared__ __align__(16) bf16_t Rl[CH * LDT];
+  __shared__ __align__(16) bf16_t Dgh[CH * LDT];
+  __shared__ __align__(16) bf16_t Dgl[CH * LDT];
+  __shared__ __align__(16) bf16_t Dh[OUT ? CH * LDT : 8];
+  __shared__ __align__(16) bf16_t Dl[OUT ? CH * LDT : 8];
   // the chunk's K rows, staged from the K operand registers: the state update
-  // takes its K^T operand from here with transposing reads
+  // takes its K operand (reduction down the chunk rows) from here with
+  // transposing reads
   constexpr int LDKC = DK + 8;
   __shared__ __align__(16) bf16_t Kc[CH * LDKC];
 
@@ -1218,53 +1227,57 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
   const long soff = ((long)s * H + h) * DK * DV;
   const float dh = d[h];
   const int n = si.nchunks;
-  const int xrow0 = (DK / 4) * w + 4 * g4;  // state rows of this lane: xrow0 + 16 mt + e
+  const int prow = 16 * w + r16;            // chunk row of this lane
+  const int xrow0 = (DK / 4) * w + r16;     // state rows of this lane: xrow0 + 16 mt
+  const int col0 = 4 * g4;                  // columns of this lane: 16 nt + col0 .. +3
 
+  // state, accumulator layout of the transposed products: row xrow0 + 16 mt,
+  // columns 16 nt + col0 .. +3 of the slice
   floatx4 X[XMT][NTV];
 #pragma unroll
   for (int mt = 0; mt < XMT; ++mt)
 #pragma unroll
-    for (int nt = 0; nt < NTV; ++nt)
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        X[mt][nt][e] = h0 ? h0[soff + (long)(xrow0 + 16 * mt + e) * DV + j0 + 16 * nt + r16] : 0.f;
+    for (int nt = 0; nt < NTV; ++nt) {
+      if (h0) {
+        const float4 x4 = *reinterpret_cast<const float4*>(h0 + soff + (long)(xrow0 + 16 * mt) * DV + j0 + 16 * nt + col0);
+        X[mt][nt] = floatx4{x4.x, x4.y, x4.z, x4.w};
+      } else {
+        X[mt][nt] = zero4();
+      }
+    }
   auto put_state = [&]() {
 #pragma unroll
     for (int mt = 0; mt < XMT; ++mt)
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt) {
         const float xv[4] = {X[mt][nt][0], X[mt][nt][1], X[mt][nt][2], X[mt][nt][3]};
-        put_t4(XTh, XTl, (16 * nt + r16) * LDX + xrow0 + 16 * mt, xv);
+        put_t4(Xh, Xl, (xrow0 + 16 * mt) * LDT + 16 * nt + col0, xv);
       }
   };
-  // state rows leave as 16-byte row pieces (see quad_transpose)
-  const int xrow_q = (DK / 4) * w + qt_row(), xcol_q = j0 + qt_col();
   auto store_state = [&](float* dst) {
 #pragma unroll
     for (int mt = 0; mt < XMT; ++mt)
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt)
-        store4(dst + (long)(xrow_q + 16 * mt) * DV + xcol_q + 16 * nt, quad_transpose(X[mt][nt]));
+        store4(dst + (long)(xrow0 + 16 * mt) * DV + j0 + 16 * nt + col0, X[mt][nt]);
   };
   // The same rows as int16 with one scale per row of the slice (see q_pack4),
   // into the slice's own block: dq = block base, [DK][BV]; ds = its row scales.
+  // A row's 32 columns are spread over the four lanes r16 + 16 g4.
   auto store_state_q = [&](int16_t* dq, float* ds) {
 #pragma unroll
     for (int mt = 0; mt < XMT; ++mt) {
-      floatx4 t[NTV];
       float m = 0.f;
 #pragma unroll
-      for (int nt = 0; nt < NTV; ++nt) {
-        t[nt] = quad_transpose(X[mt][nt]);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) m = fmaxf(m, fabsf(t[nt][e]));
-      }
-      m = row4_max(m);
+      for (int nt = 0; nt < NTV; ++nt)
+        m = fmaxf(m, fmaxf(fmaxf(fabsf(X[mt][nt][0]), fabsf(X[mt][nt][1])),
+                           fmaxf(fabsf(X[mt][nt][2]), fabsf(X[mt][nt][3]))));
+      m = rowgroup_max(m);
       const float inv = q_inv_scale(m);
-      const long row = xrow_q + 16 * mt;
+      const long row = xrow0 + 16 * mt;
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt)
-        *reinterpret_cast<uint2*>(dq + row * BV + qt_col() + 16 * nt) = q_pack4(t[nt], inv);
+        *reinterpret_cast<uint2*>(dq + row * BV + 16 * nt + col0) = q_pack4(X[mt][nt], inv);
       ds[row] = q_scale(m);  // the four lanes of a row store the same value
     }
   };
@@ -1279,7 +1292,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
   // (M R)[r] = s_r sum_i q[r][i] R[i])
   bf16x8 kf[KS], qf[KS];
   uint4 mq[2], aq[2];
-  float4 msc, asc;
+  float msc, asc;
   // per-row values of the chunk (cumulative gates G, beta, the V slice) are
   // loaded one chunk ahead into registers and staged through a double-buffered
   // LDS area at the end of each chunk
@@ -1308,7 +1321,6 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
       *reinterpret_cast<uint4*>(&Vrow[buf][vr * (BV + 8) + vc]) =
           vr < plen ? pvv : make_uint4(0, 0, 0, 0);
   };
-  const int prow = 16 * w + r16;  // operand row of this lane
   // rows past the chunk end load a valid row; their K X / Q X results are
   // never used (beta = 0 zeroes R there and such outputs are not stored)
   auto load_kq = [&](int cc) {
@@ -1323,13 +1335,13 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     const int16_t* p = Mq + c_chh(cc) * CC + (2 * w * 64 + lane) * 8;  // fragment order
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) mq[ks] = *reinterpret_cast<const uint4*>(p + ks * 512);
-    msc = *reinterpret_cast<const float4*>(Ms + c_chh(cc) * CH + 16 * w + 4 * g4);
+    msc = Ms[c_chh(cc) * CH + prow];
   };
   auto load_a = [&](int cc) {
     const int16_t* p = Aq + c_chh(cc) * CC + (2 * w * 64 + lane) * 8;  // fragment order
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) aq[ks] = *reinterpret_cast<const uint4*>(p + ks * 512);
-    asc = *reinterpret_cast<const float4*>(As + c_chh(cc) * CH + 16 * w + 4 * g4);
+    asc = As[c_chh(cc) * CH + prow];
   };
   if (n > 0) {
     load_kq(0);
@@ -1352,16 +1364,10 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     const int buf = cc & 1;
     load_rows(nx);
     const float glast = Grow[buf][CH - 1];
-    float gg[4], gm[4], bb[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int r = 16 * w + 4 * g4 + e;
-      gg[e] = Grow[buf][r];
-      gm[e] = r > 0 ? Grow[buf][r - 1] : 0.f;
-      bb[e] = Brow[buf][r];
-    }
+    const float gg = Grow[buf][prow], gm = prow > 0 ? Grow[buf][prow - 1] : 0.f, bb = Brow[buf][prow];
 
-    // K X and Q X (rows 16w..), R = Diag(beta)(V - Diag(exp Gm) K X)
+    // (K X)^T and (Q X)^T: this lane holds row prow, columns 16 nt + col0 ..;
+    // R = Diag(beta)(V - Diag(exp Gm) K X)
     floatx4 kx[NTV], qx[NTV];
 #pragma unroll
     for (int nt = 0; nt < NTV; ++nt) {
@@ -1372,13 +1378,13 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt) {
-        const int off = (16 * nt + r16) * LDX + 32 * ks + 8 * g4;
-        const bf16x8 xh = ld8(XTh + off), xl = ld8(XTl + off);
-        kx[nt] = mfma16(kf[ks], xh, kx[nt]);
-        kx[nt] = mfma16(kf[ks], xl, kx[nt]);
+        const bf16x8 xh = ld_tr8(Xh, LDT, 32 * ks + 8 * g4, 16 * nt);
+        const bf16x8 xl = ld_tr8(Xl, LDT, 32 * ks + 8 * g4, 16 * nt);
+        kx[nt] = mfma16(xh, kf[ks], kx[nt]);
+        kx[nt] = mfma16(xl, kf[ks], kx[nt]);
         if constexpr (OUT) {
-          qx[nt] = mfma16(qf[ks], xh, qx[nt]);
-          qx[nt] = mfma16(qf[ks], xl, qx[nt]);
+          qx[nt] = mfma16(xh, qf[ks], qx[nt]);
+          qx[nt] = mfma16(xl, qf[ks], qx[nt]);
         }
       }
     // K rows past the chunk end repeat row len - 1; D is zero there
@@ -1386,21 +1392,25 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     for (int ks = 0; ks < KS; ++ks) *reinterpret_cast<bf16x8*>(Kc + prow * LDKC + 32 * ks + 8 * g4) = kf[ks];
     load_kq(nx);
     floatx4 oacc[NTV];
+    {
+      const float egm = __expf(gm), eg = __expf(gg);
 #pragma unroll
-    for (int nt = 0; nt < NTV; ++nt) {
-      float rv[4];
+      for (int nt = 0; nt < NTV; ++nt) {
+        const uint2 v4 = *reinterpret_cast<const uint2*>(&Vrow[buf][prow * (BV + 8) + 16 * nt + col0]);
+        const float vv[4] = {__uint_as_float(v4.x << 16), __uint_as_float(v4.x & 0xFFFF0000u),
+                             __uint_as_float(v4.y << 16), __uint_as_float(v4.y & 0xFFFF0000u)};
+        float rv[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int r = 16 * w + 4 * g4 + e;
-        const float vval = bf2f(Vrow[buf][r * (BV + 8) + 16 * nt + r16]);
-        rv[e] = bb[e] * (vval - __expf(gm[e]) * kx[nt][e]);
-        if constexpr (OUT) oacc[nt][e] = __expf(gg[e]) * (qx[nt][e] - dh * kx[nt][e]);
+        for (int e = 0; e < 4; ++e) {
+          rv[e] = bb * (vv[e] - egm * kx[nt][e]);
+          if constexpr (OUT) oacc[nt][e] = eg * (qx[nt][e] - dh * kx[nt][e]);
+        }
+        put_t4(Rh, Rl, prow * LDT + 16 * nt + col0, rv);
       }
-      put_t4(RTh, RTl, (16 * nt + r16) * LDR + 16 * w + 4 * g4, rv);
     }
     __syncthreads();
 
-    // D = M R
+    // (M R)^T
     floatx4 dl[NTV];
 #pragma unroll
     for (int nt = 0; nt < NTV; ++nt) dl[nt] = zero4();
@@ -1410,55 +1420,45 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
       q_split8(mq[ks], mh, ml);
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt) {
-        const int off = (16 * nt + r16) * LDR + 32 * ks + 8 * g4;
-        const bf16x8 rh = ld8(RTh + off), rl = ld8(RTl + off);
-        dl[nt] = mfma16(mh, rh, dl[nt]);
-        dl[nt] = mfma16(mh, rl, dl[nt]);
-        dl[nt] = mfma16(ml, rh, dl[nt]);
+        const bf16x8 rh = ld_tr8(Rh, LDT, 32 * ks + 8 * g4, 16 * nt);
+        const bf16x8 rl = ld_tr8(Rl, LDT, 32 * ks + 8 * g4, 16 * nt);
+        dl[nt] = mfma16(rh, mh, dl[nt]);
+        dl[nt] = mfma16(rl, mh, dl[nt]);
+        dl[nt] = mfma16(rh, ml, dl[nt]);
       }
     }
-    const float4 ms_cur = msc;
+    const float ms_cur = msc;
     load_m(nx);
 #pragma unroll
-    for (int nt = 0; nt < NTV; ++nt) {
-      dl[nt][0] *= ms_cur.x;
-      dl[nt][1] *= ms_cur.y;
-      dl[nt][2] *= ms_cur.z;
-      dl[nt][3] *= ms_cur.w;
-    }
+    for (int nt = 0; nt < NTV; ++nt) dl[nt] *= ms_cur;
     if constexpr (STORE) {
       // D rows as int16 with one scale per row of the slice
-      floatx4 t[NTV];
       float m = 0.f;
 #pragma unroll
-      for (int nt = 0; nt < NTV; ++nt) {
-        t[nt] = quad_transpose(dl[nt]);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) m = fmaxf(m, fabsf(t[nt][e]));
-      }
-      m = row4_max(m);
+      for (int nt = 0; nt < NTV; ++nt)
+        m = fmaxf(m, fmaxf(fmaxf(fabsf(dl[nt][0]), fabsf(dl[nt][1])), fmaxf(fabsf(dl[nt][2]), fabsf(dl[nt][3]))));
+      m = rowgroup_max(m);
       const float inv = q_inv_scale(m);
-      const long row = (chh * NB + blockIdx.z) * CH + 16 * w + qt_row();  // the slice's block
+      const long row = (chh * NB + blockIdx.z) * CH + prow;  // the slice's block
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt)
-        *reinterpret_cast<uint2*>(Dq + row * BV + qt_col() + 16 * nt) = q_pack4(t[nt], inv);
+        *reinterpret_cast<uint2*>(Dq + row * BV + 16 * nt + col0) = q_pack4(dl[nt], inv);
       Ds[row] = q_scale(m);  // the four lanes of a row store the same value
     }
+    {
+      const float edec = __expf(glast - gg);
 #pragma unroll
-    for (int nt = 0; nt < NTV; ++nt) {
-      float dv[4], dgv[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        dv[e] = dl[nt][e];
-        dgv[e] = __expf(glast - gg[e]) * dv[e];
+      for (int nt = 0; nt < NTV; ++nt) {
+        const float dv[4] = {dl[nt][0], dl[nt][1], dl[nt][2], dl[nt][3]};
+        const float dgv[4] = {edec * dv[0], edec * dv[1], edec * dv[2], edec * dv[3]};
+        const int off = prow * LDT + 16 * nt + col0;
+        put_t4(Dgh, Dgl, off, dgv);
+        if constexpr (OUT) put_t4(Dh, Dl, off, dv);
       }
-      const int off = (16 * nt + r16) * LDR + 16 * w + 4 * g4;
-      put_t4(DgTh, DgTl, off, dgv);
-      if constexpr (OUT) put_t4(DTh, DTl, off, dv);
     }
     __syncthreads();
 
-    // X' = exp(G_63) X + K^T Diag(exp(G_63 - G)) D
+    // X'^T = exp(G_63) X^T + (Diag(exp(G_63 - G)) D)^T K
     const float gC = __expf(glast);
 #pragma unroll
     for (int mt = 0; mt < XMT; ++mt)
@@ -1466,23 +1466,23 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
       for (int nt = 0; nt < NTV; ++nt) X[mt][nt] *= gC;
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
-      // K^T rows (DK/4) w + 16 mt + i, chunk rows 32 ks + 8 g4 ..
+      // K fragments for state rows (dk/4) w + 16 mt + r16, chunk rows 32 ks + 8 g4 ..
       bf16x8 ktf[XMT];
 #pragma unroll
       for (int mt = 0; mt < XMT; ++mt) ktf[mt] = ld_tr8(Kc, LDKC, 32 * ks + 8 * g4, (DK / 4) * w + 16 * mt);
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt) {
-        const int off = (16 * nt + r16) * LDR + 32 * ks + 8 * g4;
-        const bf16x8 dh_ = ld8(DgTh + off), dl_ = ld8(DgTl + off);
+        const bf16x8 dgh = ld_tr8(Dgh, LDT, 32 * ks + 8 * g4, 16 * nt);
+        const bf16x8 dgl = ld_tr8(Dgl, LDT, 32 * ks + 8 * g4, 16 * nt);
 #pragma unroll
         for (int mt = 0; mt < XMT; ++mt) {
-          X[mt][nt] = mfma16(ktf[mt], dh_, X[mt][nt]);
-          X[mt][nt] = mfma16(ktf[mt], dl_, X[mt][nt]);
+          X[mt][nt] = mfma16(dgh, ktf[mt], X[mt][nt]);
+          X[mt][nt] = mfma16(dgl, ktf[mt], X[mt][nt]);
         }
       }
     }
 
-    // O = Diag(exp G)(Q - d K) X + A D
+    // O = Diag(exp G)(Q - d K) X + A D, formed as (A D)^T = D^T A^T
     if constexpr (OUT) {
       floatx4 adc[NTV];
 #pragma unroll
@@ -1493,28 +1493,23 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
         q_split8(aq[ks], ah, al);
 #pragma unroll
         for (int nt = 0; nt < NTV; ++nt) {
-          const int off = (16 * nt + r16) * LDR + 32 * ks + 8 * g4;
-          const bf16x8 dh_ = ld8(DTh + off), dl_ = ld8(DTl + off);
-          adc[nt] = mfma16(ah, dh_, adc[nt]);
-          adc[nt] = mfma16(ah, dl_, adc[nt]);
-          adc[nt] = mfma16(al, dh_, adc[nt]);
+          const bf16x8 dh_ = ld_tr8(Dh, LDT, 32 * ks + 8 * g4, 16 * nt);
+          const bf16x8 dl_ = ld_tr8(Dl, LDT, 32 * ks + 8 * g4, 16 * nt);
+          adc[nt] = mfma16(dh_, ah, adc[nt]);
+          adc[nt] = mfma16(dl_, ah, adc[nt]);
+          adc[nt] = mfma16(dh_, al, adc[nt]);
         }
       }
-      const float4 as_cur = asc;
+      const float as_cur = asc;
       load_a(nx);
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt) {
-        oacc[nt][0] += as_cur.x * adc[nt][0];
-        oacc[nt][1] += as_cur.y * adc[nt][1];
-        oacc[nt][2] += as_cur.z * adc[nt][2];
-        oacc[nt][3] += as_cur.w * adc[nt][3];
-      }
-      const int orow = 16 * w + qt_row();
+        floatx4 ov;
 #pragma unroll
-      for (int nt = 0; nt < NTV; ++nt) {
-        float* dst = orow < len ? o + (tok + (long)orow * H) * DV + xcol_q + 16 * nt
+        for (int e = 0; e < 4; ++e) ov[e] = oacc[nt][e] + as_cur * adc[nt][e];
+        float* dst = prow < len ? o + (tok + (long)prow * H) * DV + j0 + 16 * nt + col0
                                 : sink + 4 * lane;
-        store4(dst, quad_transpose(oacc[nt]));
+        store4(dst, ov);
       }
     }
     put_state();
