@@ -1525,6 +1525,10 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
 }
 
 // Reverse state scan (bf16 inputs): Y = gradient of the state leaving the chunk.
+// As in the forward scan, every product is formed transposed, so that a lane
+// holds one row and four consecutive columns; the intermediate tiles (Y, dO,
+// dD, Pg, W2) sit row-major in LDS and are read as operands with transposing
+// reads.
 template <int DK, int DV, int BV>
 __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ dO,
@@ -1537,17 +1541,18 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     float* __restrict__ sink) {
   // as in the forward scan, all loop memory operations are unconditional
   constexpr int NTV = BV / 16, XMT = DK / 64, KS = DK / 32, CC = CH * CH;
-  constexpr int LDX = DK + 8, LDR = CH + 8, NB = DV / 32;
+  constexpr int NB = DV / 32;
+  constexpr int LDT = BV + 4;  // row-major BV-wide tiles (see the forward scan)
   static_assert(BV == 32, "stored states use one scale per 32-column block = one dv slice");
-  __shared__ __align__(16) bf16_t YTh[BV * LDX];
-  __shared__ __align__(16) bf16_t YTl[BV * LDX];
-  __shared__ __align__(16) bf16_t dOT[2][BV * LDR];
-  __shared__ __align__(16) bf16_t dDTh[BV * LDR];
-  __shared__ __align__(16) bf16_t dDTl[BV * LDR];
-  __shared__ __align__(16) bf16_t PgTh[BV * LDR];
-  __shared__ __align__(16) bf16_t PgTl[BV * LDR];
-  __shared__ __align__(16) bf16_t W2Th[BV * LDR];
-  __shared__ __align__(16) bf16_t W2Tl[BV * LDR];
+  __shared__ __align__(16) bf16_t Yh[DK * LDT];
+  __shared__ __align__(16) bf16_t Yl[DK * LDT];
+  __shared__ __align__(16) bf16_t dOs[2][CH * LDT];
+  __shared__ __align__(16) bf16_t dDh[CH * LDT];
+  __shared__ __align__(16) bf16_t dDl[CH * LDT];
+  __shared__ __align__(16) bf16_t Pgh[CH * LDT];
+  __shared__ __align__(16) bf16_t Pgl[CH * LDT];
+  __shared__ __align__(16) bf16_t W2h[CH * LDT];
+  __shared__ __align__(16) bf16_t W2l[CH * LDT];
 
   const int s = blockIdx.x, h = blockIdx.y, j0 = blockIdx.z * BV;
   const SeqInfo si = seq_at(smap, s, Tfix);
@@ -1555,53 +1560,54 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
   const long soff = ((long)s * H + h) * DK * DV;
   const float dh = d[h];
   const int n = si.nchunks;
-  const int yrow0 = (DK / 4) * w + 4 * g4;
+  const int prow = 16 * w + r16;            // chunk row of this lane
+  const int yrow0 = (DK / 4) * w + r16;     // state rows of this lane: yrow0 + 16 mt
+  const int col0 = 4 * g4;                  // columns of this lane: 16 nt + col0 .. +3
 
   floatx4 Y[XMT][NTV];
 #pragma unroll
   for (int mt = 0; mt < XMT; ++mt)
 #pragma unroll
-    for (int nt = 0; nt < NTV; ++nt)
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        Y[mt][nt][e] = dht ? dht[soff + (long)(yrow0 + 16 * mt + e) * DV + j0 + 16 * nt + r16] : 0.f;
+    for (int nt = 0; nt < NTV; ++nt) {
+      if (dht) {
+        const float4 y4 = *reinterpret_cast<const float4*>(dht + soff + (long)(yrow0 + 16 * mt) * DV + j0 + 16 * nt + col0);
+        Y[mt][nt] = floatx4{y4.x, y4.y, y4.z, y4.w};
+      } else {
+        Y[mt][nt] = zero4();
+      }
+    }
   auto put_state = [&]() {
 #pragma unroll
     for (int mt = 0; mt < XMT; ++mt)
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt) {
         const float yv[4] = {Y[mt][nt][0], Y[mt][nt][1], Y[mt][nt][2], Y[mt][nt][3]};
-        put_t4(YTh, YTl, (16 * nt + r16) * LDX + yrow0 + 16 * mt, yv);
+        put_t4(Yh, Yl, (yrow0 + 16 * mt) * LDT + 16 * nt + col0, yv);
       }
   };
-  // state rows leave as 16-byte row pieces (see quad_transpose)
-  const int yrow_q = (DK / 4) * w + qt_row(), ycol_q = j0 + qt_col();
   auto store_state = [&](float* dst) {
 #pragma unroll
     for (int mt = 0; mt < XMT; ++mt)
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt)
-        store4(dst + (long)(yrow_q + 16 * mt) * DV + ycol_q + 16 * nt, quad_transpose(Y[mt][nt]));
+        store4(dst + (long)(yrow0 + 16 * mt) * DV + j0 + 16 * nt + col0, Y[mt][nt]);
   };
   // the same rows as int16 with one scale per row of the slice (see q_pack4),
   // into the slice's own block: dq = block base, [DK][BV]; ds = its row scales
   auto store_state_q = [&](int16_t* dq, float* ds) {
 #pragma unroll
     for (int mt = 0; mt < XMT; ++mt) {
-      floatx4 t[NTV];
       float m = 0.f;
 #pragma unroll
-      for (int nt = 0; nt < NTV; ++nt) {
-        t[nt] = quad_transpose(Y[mt][nt]);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) m = fmaxf(m, fabsf(t[nt][e]));
-      }
-      m = row4_max(m);
+      for (int nt = 0; nt < NTV; ++nt)
+        m = fmaxf(m, fmaxf(fmaxf(fabsf(Y[mt][nt][0]), fabsf(Y[mt][nt][1])),
+                           fmaxf(fabsf(Y[mt][nt][2]), fabsf(Y[mt][nt][3]))));
+      m = rowgroup_max(m);
       const float inv = q_inv_scale(m);
-      const long row = yrow_q + 16 * mt;
+      const long row = yrow0 + 16 * mt;
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt)
-        *reinterpret_cast<uint2*>(dq + row * BV + qt_col() + 16 * nt) = q_pack4(t[nt], inv);
+        *reinterpret_cast<uint2*>(dq + row * BV + 16 * nt + col0) = q_pack4(Y[mt][nt], inv);
       ds[row] = q_scale(m);  // the four lanes of a row store the same value
     }
   };
@@ -1614,11 +1620,12 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
   // A^T, M^T rows as int16 with their row scales (applied to the accumulator rows)
   bf16x8 kf[KS], qtf[XMT][2];
   // the chunk's K rows, staged from the K operand registers: the state update
-  // takes its K^T operand from here with transposing reads
+  // takes its K operand (reduction down the chunk rows) from here with
+  // transposing reads
   constexpr int LDKC = DK + 8;
   __shared__ __align__(16) bf16_t Kc[CH * LDKC];
   uint4 atq[2], mtq[2];
-  float4 atsc, mtsc;
+  float atsc, mtsc;
   // per-row values (G, beta) and the dO slice are loaded one chunk ahead into
   // registers and staged through double-buffered LDS at the end of each chunk
   __shared__ float Grow[2][CH], Brow[2][CH];
@@ -1626,7 +1633,6 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
   bf16_t pbv = 0;
   int plen = 0;
   uint4 pdo = make_uint4(0, 0, 0, 0);  // next chunk's dO slice, 16 bytes per thread
-  const int prow = 16 * w + r16;
   // rows past the chunk end load a valid row; dD is zeroed there at use
   auto load_k = [&](int cc) {
     const long rb = (c_tok(cc) + (long)min(prow, c_len(cc) - 1) * H) * DK + 8 * g4;
@@ -1637,13 +1643,13 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     const int16_t* p = ATq + c_chh(cc) * CC + (2 * w * 64 + lane) * 8;  // fragment order
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) atq[ks] = *reinterpret_cast<const uint4*>(p + ks * 512);
-    atsc = *reinterpret_cast<const float4*>(ATs + c_chh(cc) * CH + 16 * w + 4 * g4);
+    atsc = ATs[c_chh(cc) * CH + prow];
   };
   auto load_mt = [&](int cc) {
     const int16_t* p = MTq + c_chh(cc) * CC + (2 * w * 64 + lane) * 8;  // fragment order
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) mtq[ks] = *reinterpret_cast<const uint4*>(p + ks * 512);
-    mtsc = *reinterpret_cast<const float4*>(MTs + c_chh(cc) * CH + 16 * w + 4 * g4);
+    mtsc = MTs[c_chh(cc) * CH + prow];
   };
   auto load_qt = [&](int cc) {
     // fragment order: rows (DK/4) w + 16 mt + i are row block w XMT + mt
@@ -1666,7 +1672,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     Brow[buf][t] = t < plen ? bf2f(pbv) : 0.f;
   };
   // dO slice of a chunk: 64 tokens x BV columns in 16-byte pieces; thread t
-  // (t < 8 BV) holds token t / (BV/8), columns 8 (t % (BV/8)) .. +7
+  // (t < 8 BV) holds token t / (BV/8), columns 8 (t % (BV/8)) .. +7; staged
+  // row-major (rows past the chunk end zero)
   constexpr int DPR = BV / 8;
   const int dr = threadIdx.x / DPR, dc = (threadIdx.x % DPR) * 8;
   const bool do_thr = CH * DPR >= NTHR || threadIdx.x < CH * DPR;
@@ -1678,11 +1685,11 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     pdo = *reinterpret_cast<const uint4*>(dO + (c_tok(cc) + (long)min(dr_ld, len - 1) * H) * DV + j0 + dc);
   };
   auto put_do = [&](int buf) {
-    union { uint4 u; bf16_t e[8]; } val;
-    val.u = do_ok ? pdo : make_uint4(0, 0, 0, 0);
+    const uint4 val = do_ok ? pdo : make_uint4(0, 0, 0, 0);
     if (do_thr) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) dOT[buf][(dc + e) * LDR + dr] = val.e[e];
+      // two 8-byte writes: the 72-byte rows keep only 8-byte alignment
+      *reinterpret_cast<uint2*>(dOs[buf] + dr * LDT + dc) = make_uint2(val.x, val.y);
+      *reinterpret_cast<uint2*>(dOs[buf] + dr * LDT + dc + 4) = make_uint2(val.z, val.w);
     }
   };
 
@@ -1708,16 +1715,9 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     load_rows(nx);
     load_do(nx);
     const float glast = Grow[buf][CH - 1];
-    float gg[4], gm[4], bb[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int r = 16 * w + 4 * g4 + e;
-      gg[e] = Grow[buf][r];
-      gm[e] = r > 0 ? Grow[buf][r - 1] : 0.f;
-      bb[e] = Brow[buf][r];
-    }
+    const float gg = Grow[buf][prow], gm = prow > 0 ? Grow[buf][prow - 1] : 0.f, bb = Brow[buf][prow];
 
-    // dD = A^T dO + Diag(exp(G_63 - G)) K Y
+    // dD = A^T dO + Diag(exp(G_63 - G)) K Y, formed transposed
     floatx4 ky[NTV], ad[NTV];
 #pragma unroll
     for (int nt = 0; nt < NTV; ++nt) {
@@ -1728,10 +1728,10 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt) {
-        const int off = (16 * nt + r16) * LDX + 32 * ks + 8 * g4;
-        const bf16x8 yh = ld8(YTh + off), yl = ld8(YTl + off);
-        ky[nt] = mfma16(kf[ks], yh, ky[nt]);
-        ky[nt] = mfma16(kf[ks], yl, ky[nt]);
+        const bf16x8 yh = ld_tr8(Yh, LDT, 32 * ks + 8 * g4, 16 * nt);
+        const bf16x8 yl = ld_tr8(Yl, LDT, 32 * ks + 8 * g4, 16 * nt);
+        ky[nt] = mfma16(yh, kf[ks], ky[nt]);
+        ky[nt] = mfma16(yl, kf[ks], ky[nt]);
       }
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
@@ -1739,31 +1739,26 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
       q_split8(atq[ks], ath, atl);
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt) {
-        const bf16x8 dov = ld8(dOT[buf] + (16 * nt + r16) * LDR + 32 * ks + 8 * g4);
-        ad[nt] = mfma16(ath, dov, ad[nt]);
-        ad[nt] = mfma16(atl, dov, ad[nt]);
+        const bf16x8 dov = ld_tr8(dOs[buf], LDT, 32 * ks + 8 * g4, 16 * nt);
+        ad[nt] = mfma16(dov, ath, ad[nt]);
+        ad[nt] = mfma16(dov, atl, ad[nt]);
       }
     }
-    const float4 at_cur = atsc;
+    const float at_cur = atsc;
     // K rows past the chunk end repeat row len - 1; W2 is zero there
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) *reinterpret_cast<bf16x8*>(Kc + prow * LDKC + 32 * ks + 8 * g4) = kf[ks];
     load_k(nx);
     load_at(nx);
+    {
+      const float edec = prow < clen ? __expf(glast - gg) : 0.f, atm = prow < clen ? at_cur : 0.f;
 #pragma unroll
-    for (int nt = 0; nt < NTV; ++nt) {
-      ad[nt][0] *= at_cur.x;
-      ad[nt][1] *= at_cur.y;
-      ad[nt][2] *= at_cur.z;
-      ad[nt][3] *= at_cur.w;
-    }
+      for (int nt = 0; nt < NTV; ++nt) {
+        float dd_[4];
 #pragma unroll
-    for (int nt = 0; nt < NTV; ++nt) {
-      float dd_[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        dd_[e] = 16 * w + 4 * g4 + e < clen ? ad[nt][e] + __expf(glast - gg[e]) * ky[nt][e] : 0.f;
-      put_t4(dDTh, dDTl, (16 * nt + r16) * LDR + 16 * w + 4 * g4, dd_);
+        for (int e = 0; e < 4; ++e) dd_[e] = atm * ad[nt][e] + edec * ky[nt][e];
+        put_t4(dDh, dDl, prow * LDT + 16 * nt + col0, dd_);
+      }
     }
     __syncthreads();
 
@@ -1777,57 +1772,52 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
       q_split8(mtq[ks], mth, mtl);
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt) {
-        const int off = (16 * nt + r16) * LDR + 32 * ks + 8 * g4;
-        const bf16x8 xh = ld8(dDTh + off), xl = ld8(dDTl + off);
-        drr[nt] = mfma16(mth, xh, drr[nt]);
-        drr[nt] = mfma16(mth, xl, drr[nt]);
-        drr[nt] = mfma16(mtl, xh, drr[nt]);
+        const bf16x8 xh = ld_tr8(dDh, LDT, 32 * ks + 8 * g4, 16 * nt);
+        const bf16x8 xl = ld_tr8(dDl, LDT, 32 * ks + 8 * g4, 16 * nt);
+        drr[nt] = mfma16(xh, mth, drr[nt]);
+        drr[nt] = mfma16(xl, mth, drr[nt]);
+        drr[nt] = mfma16(xh, mtl, drr[nt]);
       }
     }
-    const float4 mt_cur = mtsc;
+    const float mt_cur = mtsc;
     load_mt(nx);
 #pragma unroll
-    for (int nt = 0; nt < NTV; ++nt) {
-      drr[nt][0] *= mt_cur.x;
-      drr[nt][1] *= mt_cur.y;
-      drr[nt][2] *= mt_cur.z;
-      drr[nt][3] *= mt_cur.w;
-    }
+    for (int nt = 0; nt < NTV; ++nt) drr[nt] *= mt_cur;
     {
       // dR rows as int16 with one scale per row of the slice
-      floatx4 t[NTV];
       float m = 0.f;
 #pragma unroll
-      for (int nt = 0; nt < NTV; ++nt) {
-        t[nt] = quad_transpose(drr[nt]);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) m = fmaxf(m, fabsf(t[nt][e]));
-      }
-      m = row4_max(m);
+      for (int nt = 0; nt < NTV; ++nt)
+        m = fmaxf(m, fmaxf(fmaxf(fabsf(drr[nt][0]), fabsf(drr[nt][1])), fmaxf(fabsf(drr[nt][2]), fabsf(drr[nt][3]))));
+      m = rowgroup_max(m);
       const float inv = q_inv_scale(m);
-      const long row = (chh * NB + blockIdx.z) * CH + 16 * w + qt_row();  // the slice's block
+      const long row = (chh * NB + blockIdx.z) * CH + prow;  // the slice's block
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt)
-        *reinterpret_cast<uint2*>(dRq + row * BV + qt_col() + 16 * nt) = q_pack4(t[nt], inv);
+        *reinterpret_cast<uint2*>(dRq + row * BV + 16 * nt + col0) = q_pack4(drr[nt], inv);
       dRs[row] = q_scale(m);  // the four lanes of a row store the same value
     }
+    {
+      const float eg = __expf(gg), begm = bb * __expf(gm);
 #pragma unroll
-    for (int nt = 0; nt < NTV; ++nt) {
-      const int off = (16 * nt + r16) * LDR + 16 * w + 4 * g4;
-      const bf16x4 dov = *reinterpret_cast<const bf16x4*>(dOT[buf] + off);
-      float pg[4], w2[4];
+      for (int nt = 0; nt < NTV; ++nt) {
+        const int off = prow * LDT + 16 * nt + col0;
+        const uint2 d4 = *reinterpret_cast<const uint2*>(dOs[buf] + off);
+        const float dov[4] = {__uint_as_float(d4.x << 16), __uint_as_float(d4.x & 0xFFFF0000u),
+                              __uint_as_float(d4.y << 16), __uint_as_float(d4.y & 0xFFFF0000u)};
+        float pg[4], w2[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float drv = drr[nt][e];
-        pg[e] = __expf(gg[e]) * (float)dov[e];
-        w2[e] = -dh * pg[e] - bb[e] * __expf(gm[e]) * drv;
+        for (int e = 0; e < 4; ++e) {
+          pg[e] = eg * dov[e];
+          w2[e] = -dh * pg[e] - begm * drr[nt][e];
+        }
+        put_t4(Pgh, Pgl, off, pg);
+        put_t4(W2h, W2l, off, w2);
       }
-      put_t4(PgTh, PgTl, off, pg);
-      put_t4(W2Th, W2Tl, off, w2);
     }
     __syncthreads();
 
-    // Y <- exp(G_63) Y + Q^T Pg + K^T W2
+    // Y^T <- exp(G_63) Y^T + Pg^T Q + W2^T K
     const float gC = __expf(glast);
 #pragma unroll
     for (int mt = 0; mt < XMT; ++mt)
@@ -1835,21 +1825,22 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
       for (int nt = 0; nt < NTV; ++nt) Y[mt][nt] *= gC;
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
-      // K^T rows (DK/4) w + 16 mt + i, chunk rows 32 ks + 8 g4 ..
+      // K fragments for state rows (dk/4) w + 16 mt + r16, chunk rows 32 ks + 8 g4 ..
       bf16x8 ktf[XMT];
 #pragma unroll
       for (int mt = 0; mt < XMT; ++mt) ktf[mt] = ld_tr8(Kc, LDKC, 32 * ks + 8 * g4, (DK / 4) * w + 16 * mt);
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt) {
-        const int off = (16 * nt + r16) * LDR + 32 * ks + 8 * g4;
-        const bf16x8 ph = ld8(PgTh + off), pl = ld8(PgTl + off);
-        const bf16x8 wh = ld8(W2Th + off), wl = ld8(W2Tl + off);
+        const bf16x8 ph = ld_tr8(Pgh, LDT, 32 * ks + 8 * g4, 16 * nt);
+        const bf16x8 pl = ld_tr8(Pgl, LDT, 32 * ks + 8 * g4, 16 * nt);
+        const bf16x8 wh = ld_tr8(W2h, LDT, 32 * ks + 8 * g4, 16 * nt);
+        const bf16x8 wl = ld_tr8(W2l, LDT, 32 * ks + 8 * g4, 16 * nt);
 #pragma unroll
         for (int mt = 0; mt < XMT; ++mt) {
-          Y[mt][nt] = mfma16(qtf[mt][ks], ph, Y[mt][nt]);
-          Y[mt][nt] = mfma16(qtf[mt][ks], pl, Y[mt][nt]);
-          Y[mt][nt] = mfma16(ktf[mt], wh, Y[mt][nt]);
-          Y[mt][nt] = mfma16(ktf[mt], wl, Y[mt][nt]);
+          Y[mt][nt] = mfma16(ph, qtf[mt][ks], Y[mt][nt]);
+          Y[mt][nt] = mfma16(pl, qtf[mt][ks], Y[mt][nt]);
+          Y[mt][nt] = mfma16(wh, ktf[mt], Y[mt][nt]);
+          Y[mt][nt] = mfma16(wl, ktf[mt], Y[mt][nt]);
         }
       }
     }
