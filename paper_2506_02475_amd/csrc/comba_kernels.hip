@@ -994,7 +994,7 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
     float* __restrict__ Gw, float* __restrict__ sink) {
   // M, A (and M^T, A^T) leave as int16 rows with one power-of-two scale per row
   // (see q_pack4): the scans fold the scale into their accumulator rows
-  constexpr int LDK = DK + 8;
+  constexpr int LDK = DK + 24;  // 304-byte rows: conflict-free 16-byte and transposing reads
   constexpr int LDL = CH + 4;
   constexpr int CC = CH * CH;
   // the Q tile is dead once K^T, Q^T and Q K^T are taken: L (then M) reuses
@@ -1218,7 +1218,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
   // the chunk's K rows, staged from the K operand registers: the state update
   // takes its K operand (reduction down the chunk rows) from here with
   // transposing reads
-  constexpr int LDKC = DK + 8;
+  constexpr int LDKC = DK + 24;  // 304-byte rows: conflict-free transposing reads
   __shared__ __align__(16) bf16_t Kc[CH * LDKC];
 
   const int s = blockIdx.x, h = blockIdx.y, j0 = blockIdx.z * BV;
@@ -1622,7 +1622,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
   // the chunk's K rows, staged from the K operand registers: the state update
   // takes its K operand (reduction down the chunk rows) from here with
   // transposing reads
-  constexpr int LDKC = DK + 8;
+  constexpr int LDKC = DK + 24;  // 304-byte rows: conflict-free transposing reads
   __shared__ __align__(16) bf16_t Kc[CH * LDKC];
   uint4 atq[2], mtq[2];
   float atsc, mtsc;
@@ -1868,7 +1868,7 @@ constexpr int IB_THR = 512;
 template <int DK>
 struct IntraBwdBfSmem {
   static constexpr int VB = 32, LDB = VB + 8;
-  static constexpr int LDK = DK + 8, LDC = CH + 8;
+  static constexpr int LDK = DK + 24, LDC = CH + 8;  // K, Q: conflict-free 16-byte and transposing reads
   static constexpr int P1 = (6 * CH * LDB + 4 * DK * LDB) * 2;
   static constexpr int P2 = (2 * CH * LDK + 6 * CH * LDC) * 2;
   static constexpr int BYTES = P1 > P2 ? P1 : P2;
