@@ -244,20 +244,28 @@ __device__ __forceinline__ float4 q_unpack4(uint2 u, float s) {
                      (float)(int)(int16_t)(u.y & 0xFFFFu) * s, (float)((int)u.y >> 16) * s);
 }
 
+// Two fp32 values as packed bf16 (hi, lo): hi = bf16(x) (nearest), lo =
+// bf16(x - hi), each pair converted by one v_cvt_pk_bf16_f32 (3 VALU per value).
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ void split2(float a, float b, uint32_t& hi, uint32_t& lo) {
+  const uint32_t h = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
+  const float ah = __uint_as_float(h << 16), bh = __uint_as_float(h & 0xFFFF0000u);
+  hi = h;
+  lo = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a - ah, b - bh}, bf16x2_t));
+}
+
 // Eight int16 (one 16-byte piece of a stored row) as the exact bf16 pair
 // hi + lo of each value: |q| < 2^15, hi keeps 8 significant bits, q - hi is an
 // integer below 2^7 in magnitude and so exact in bf16.
 __device__ __forceinline__ void q_split8(const uint4& u, bf16x8& hi, bf16x8& lo) {
   const uint32_t wd[4] = {u.x, u.y, u.z, u.w};
+  uint32_t h[4], l[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const float a = (float)(int)(int16_t)(wd[i] & 0xFFFFu), b = (float)((int)wd[i] >> 16);
-    const __bf16 ah = (__bf16)a, bh = (__bf16)b;
-    hi[2 * i] = ah;
-    lo[2 * i] = (__bf16)(a - (float)ah);
-    hi[2 * i + 1] = bh;
-    lo[2 * i + 1] = (__bf16)(b - (float)bh);
-  }
+  for (int i = 0; i < 4; ++i)
+    split2((float)(int)(int16_t)(wd[i] & 0xFFFFu), (float)((int)wd[i] >> 16), h[i], l[i]);
+  hi = __builtin_bit_cast(bf16x8, make_uint4(h[0], h[1], h[2], h[3]));
+  lo = __builtin_bit_cast(bf16x8, make_uint4(l[0], l[1], l[2], l[3]));
 }
 // Eight values (times the inverse scale) -> eight int16, nearest, saturated.
 __device__ __forceinline__ uint4 q_pack8(const float (&x)[8], float inv) {

@@ -908,12 +908,11 @@ __device__ __forceinline__ int frag_off(int row, int col) {
 
 // four fp32 values -> bf16 (hi, lo) with hi + lo ~ x to ~16 significant bits
 __device__ __forceinline__ void split4(const float (&x)[4], bf16x4& hi, bf16x4& lo) {
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const __bf16 h = (__bf16)x[e];
-    hi[e] = h;
-    lo[e] = (__bf16)(x[e] - (float)h);
-  }
+  uint32_t h0, h1, l0, l1;
+  split2(x[0], x[1], h0, l0);
+  split2(x[2], x[3], h1, l1);
+  hi = __builtin_bit_cast(bf16x4, make_uint2(h0, h1));
+  lo = __builtin_bit_cast(bf16x4, make_uint2(l0, l1));
 }
 // store the 4 values a lane holds in one accumulator column (rows 4g..4g+3)
 // into a transposed, split LDS buffer: dst[col * ld + row0 + e]
