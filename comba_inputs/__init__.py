@@ -34,6 +34,7 @@ __all__ = [
     "WorkloadSpec",
     "Workload",
     "WORKLOADS",
+    "attach_beta_tilde",
     "bf16_round",
     "generate",
     "random_case",
@@ -211,6 +212,36 @@ def _fill_head(child_seed, h, arrays, in_dtype):
         dO[:, :, h, :] = x
 
 
+def attach_beta_tilde(w: Workload, form: str = "b_beta", seed: int = 0) -> Workload:
+    """Give ``w`` a separate state-feedback strength in ``w.extra['beta_tilde']``.
+
+    Forms (Section 3.2 and the SPLR/IPLR comparison of Section 3):
+      "b_beta"       beta~ = b_h * beta with one b_h = sigmoid(N(0,1)) per head
+                     (the paper's default parameterisation, b in (0, 1));
+      "independent"  beta~ = sigmoid(N(0,1)) per token, independent of beta;
+      "iplr"         beta~ = 2 alpha c with c = sigmoid(N(0,1)) per token: the
+                     IPLR transition alpha (I - 2 c k k^T) written in SPLR form
+                     (beta~ up to 2, transition eigenvalues down to -alpha).
+    The draws come from a PCG64 stream seeded with ``seed``; the result is
+    rounded to the storage dtype like beta.
+    """
+    rng = np.random.default_rng(seed)
+    shp = w.beta.shape
+    if form == "b_beta":
+        b = _sigmoid(rng.standard_normal(w.H, dtype=np.float32))
+        bt = w.beta * b[None, None, :]
+    elif form == "independent":
+        bt = _sigmoid(rng.standard_normal(shp, dtype=np.float32))
+    elif form == "iplr":
+        c = _sigmoid(rng.standard_normal(shp, dtype=np.float32))
+        bt = np.float32(2.0) * np.exp(w.g) * c
+    else:
+        raise ValueError(form)
+    bt = np.ascontiguousarray(bt, dtype=np.float32)
+    w.extra["beta_tilde"] = bf16_round(bt) if w.in_dtype == "bf16" else bt
+    return w
+
+
 def generate(spec, *, with_grad: Optional[bool] = None, threads: Optional[int] = None) -> Workload:
     """Draw the seeded inputs of one workload.
 
@@ -271,7 +302,8 @@ def random_case(*, B=1, T=64, H=1, dk=16, dv=16, seed=0, in_dtype="f32", seqlens
     ``seqlens`` (list of ints) builds a packed variable-length batch (B must be 1).
     ``gate_scale`` scales the softplus argument noise's magnitude so tests can
     reach strong and weak decay.  ``beta_tilde`` adds an independent feedback
-    strength in ``extra['beta_tilde']`` (oracle-only tests).
+    strength in ``extra['beta_tilde']`` (stored like beta: bf16-representable
+    for bf16 inputs).
     """
     rng = np.random.default_rng(seed)
     cu = None
@@ -299,6 +331,8 @@ def random_case(*, B=1, T=64, H=1, dk=16, dv=16, seed=0, in_dtype="f32", seqlens
         q, k, v, beta = bf16_round(q), bf16_round(k), bf16_round(v), bf16_round(beta)
         if dO is not None:
             dO = bf16_round(dO)
+        if beta_tilde:
+            extra["beta_tilde"] = bf16_round(extra["beta_tilde"])
     spec = WorkloadSpec("random", H=H, dk=dk, dv=dv, B=B, T=T, in_dtype=in_dtype,
                         work="fwdbwd" if grad else "fwd", seed=seed)
     return Workload(spec=spec, B=B, T=T, H=H, dk=dk, dv=dv, chunk=64, in_dtype=in_dtype,

@@ -4,13 +4,16 @@
  * Comba (arXiv 2506.02475) is a bilinear RNN whose per-head state S_t (dv x dk)
  * follows, for tokens t = 1..T of one sequence (Eq. comba-S, Section 3):
  *
- *     S_t = S_{t-1} (alpha_t I - beta_t k_t k_t^T) + beta_t v_t k_t^T
+ *     S_t = S_{t-1} (alpha_t I - beta~_t k_t k_t^T) + beta_t v_t k_t^T
  *     o_t = S_t (q_t - d k_t)
  *
- * with forget gate alpha_t = exp(g_t) in (0, 1], input gate beta_t, and a
- * per-head output-feedback scalar d.  The state-feedback strength (tilde beta
- * of Section 3.2) is taken equal to beta_t (the paper's ablation without the
- * extra factor b).  The library evaluates this recurrence with the chunk-wise
+ * with forget gate alpha_t = exp(g_t) in (0, 1], input gate beta_t, state
+ * feedback strength beta~_t, and a per-head output-feedback scalar d.  beta~ is
+ * an optional per-token input (Section 3.2 forms it as b * beta with a learned
+ * b in (0, 1); Comba-iplr, alpha (I - 2 beta~ k k^T), is the same recurrence
+ * with beta~' = 2 alpha beta~, Section 3 SPLR/IPLR); when it is omitted
+ * (NULL) it is tied to beta, the paper's ablation without the factor b
+ * (Section 4).  The library evaluates this recurrence with the chunk-wise
  * parallel algorithm of Section 3.3 (chunks of 64 tokens, WY/UT transform with
  * one unit-lower-triangular inverse per chunk, inter-chunk state passing), and
  * its reverse-mode derivative (derived from the same chunk form; the paper
@@ -28,8 +31,14 @@
  *  - The recurrent state is stored transposed, H = S^T, as [N, H, dk, dv] fp32
  *    (N = number of sequences), the orientation of the paper's recurrent
  *    pseudocode (Appendix B.1).
- *  - q, k, v, beta and dO have dtype shape->in_dtype (bf16 or fp32); g (log
- *    alpha), d, states and every output are fp32.
+ *  - q, k, v, beta, beta_tilde and dO have dtype shape->in_dtype (bf16 or
+ *    fp32); g (log alpha), d, states and every output are fp32.
+ *  - beta_tilde [B,T,H] may be NULL: beta~ = beta.  The backward's dbeta_tilde
+ *    [B,T,H] fp32 may be NULL only when beta_tilde is: dbeta then holds the
+ *    total derivative through both roles of beta.  When dbeta_tilde is given,
+ *    dbeta holds the derivative through the write strength only and
+ *    dbeta_tilde that through the feedback strength (the per-head b of Section
+ *    3.2 then gets db_h = sum over tokens of beta * dbeta_tilde).
  *  - g must be <= 0 (alpha in (0, 1]); other values are outside the contract
  *    (results may overflow) but never cause out-of-bounds accesses.
  *  - Calls are asynchronous on `stream` (a hipStream_t passed as void*; NULL is
@@ -37,11 +46,11 @@
  *    then nothing is written.  A failed launch returns COMBA_ERR_HIP.
  *  - Alignment: q, k, v, dO and every fp32 tensor whose last dimension is dk
     or dv (h0, ht, o, dht, dh0, dq, dk, dv) need 16 bytes, the workspace 256
-    bytes, the other fp32 tensors 4 bytes and beta its element size; any other
+    bytes, the other fp32 tensors 4 bytes and beta, beta_tilde their element size; any other
     pointer is rejected with COMBA_ERR_ALIGN.
   - Outputs must not alias inputs; outputs are overwritten, never accumulated.
   - A call without tokens (T == 0 or B == 0) is valid: the per-token tensors
-    (q, k, v, g, beta, o, dO, dq, dk, dv, dg, dbeta) may then be NULL, and the
+    (q, k, v, g, beta, o, dO, dq, dk, dv, dg, dbeta, dbeta_tilde) may then be NULL, and the
     states pass through (ht = h0, dh0 = dht, dd = 0).  Empty sequences inside a
     packed batch behave the same way for their own states.
  *  - Calls on different streams with distinct workspaces may run concurrently;
@@ -79,7 +88,7 @@ typedef struct {
   int32_t num_seqs;           /* N: sequences; must equal B when cu_seqlens == NULL     */
   const int32_t *cu_seqlens;  /* device [N+1] offsets (0 = cu[0] <= ... <= cu[N] = T),
                                  or NULL for fixed-length rows                           */
-  comba_dtype in_dtype;       /* dtype of q, k, v, beta, dO                             */
+  comba_dtype in_dtype;       /* dtype of q, k, v, beta, beta_tilde, dO                 */
 } comba_shape;
 
 /* Workspace sizes in bytes for one call of the matching entry point. */
@@ -92,14 +101,15 @@ size_t comba_bwd_workspace_bytes(const comba_shape *shape);
  * the closing matrix form).
  *   q, k  [B,T,H,dk] in_dtype      v   [B,T,H,dv] in_dtype
  *   g     [B,T,H] fp32 (log alpha) beta [B,T,H] in_dtype    d [H] fp32
+ *   beta_tilde [B,T,H] in_dtype feedback strength, or NULL (tied to beta)
  *   h0    [N,H,dk,dv] fp32 initial states, or NULL for zero states
  *   o     [B,T,H,dv] fp32 output   ht  [N,H,dk,dv] fp32 final states, or NULL
  *   ws    device workspace of at least comba_fwd_workspace_bytes(shape), 256-B aligned
  */
 comba_status comba_chunk_fwd(const comba_shape *shape, const void *q, const void *k,
-                             const void *v, const float *g, const void *beta, const float *d,
-                             const float *h0, float *o, float *ht, void *ws, size_t ws_bytes,
-                             void *stream);
+                             const void *v, const float *g, const void *beta,
+                             const void *beta_tilde, const float *d, const float *h0, float *o,
+                             float *ht, void *ws, size_t ws_bytes, void *stream);
 
 /*
  * Backward: gradients of L = <dO, o> + <dht, ht> with respect to every input.
@@ -107,15 +117,15 @@ comba_status comba_chunk_fwd(const comba_shape *shape, const void *q, const void
  * call).  Inputs as comba_chunk_fwd plus
  *   dO    [B,T,H,dv] in_dtype     dht [N,H,dk,dv] fp32 or NULL (zero)
  * Outputs (fp32): dq, dk [B,T,H,dk]; dv [B,T,H,dv]; dg, dbeta [B,T,H];
+ *   dbeta_tilde [B,T,H] (see the conventions: NULL only with beta_tilde NULL);
  *   dd [H] (summed over all sequences and tokens); dh0 [N,H,dk,dv] or NULL.
- * dbeta is the total derivative through both roles of beta (write strength
- * and state-feedback strength).
  */
 comba_status comba_chunk_bwd(const comba_shape *shape, const void *q, const void *k,
-                             const void *v, const float *g, const void *beta, const float *d,
-                             const float *h0, const void *dO, const float *dht, float *dq,
-                             float *dk, float *dv, float *dg, float *dbeta, float *dd,
-                             float *dh0, void *ws, size_t ws_bytes, void *stream);
+                             const void *v, const float *g, const void *beta,
+                             const void *beta_tilde, const float *d, const float *h0,
+                             const void *dO, const float *dht, float *dq, float *dk, float *dv,
+                             float *dg, float *dbeta, float *dbeta_tilde, float *dd, float *dh0,
+                             void *ws, size_t ws_bytes, void *stream);
 
 /*
  * Training pair.  comba_chunk_fwd_save computes exactly what comba_chunk_fwd
@@ -124,20 +134,21 @@ comba_status comba_chunk_bwd(const comba_shape *shape, const void *q, const void
  * the chunk-boundary states); `ws` must hold comba_bwd_workspace_bytes(shape).
  * comba_chunk_bwd_saved then returns the same gradients as comba_chunk_bwd
  * while skipping that recomputation.  The caller must pass the same shape and
- * inputs (q, k, v, g, beta, d, h0) and the same, unmodified `ws` to both calls,
+ * inputs (q, k, v, g, beta, beta_tilde, d, h0) and the same, unmodified `ws` to both calls,
  * with the backward ordered after the forward (same stream, or synchronised);
  * otherwise the results are undefined (never out of bounds).
  */
 comba_status comba_chunk_fwd_save(const comba_shape *shape, const void *q, const void *k,
-                                  const void *v, const float *g, const void *beta, const float *d,
-                                  const float *h0, float *o, float *ht, void *ws,
-                                  size_t ws_bytes, void *stream);
+                                  const void *v, const float *g, const void *beta,
+                                  const void *beta_tilde, const float *d, const float *h0,
+                                  float *o, float *ht, void *ws, size_t ws_bytes, void *stream);
 comba_status comba_chunk_bwd_saved(const comba_shape *shape, const void *q, const void *k,
                                    const void *v, const float *g, const void *beta,
-                                   const float *d, const float *h0, const void *dO,
-                                   const float *dht, float *dq, float *dk, float *dv, float *dg,
-                                   float *dbeta, float *dd, float *dh0, void *ws,
-                                   size_t ws_bytes, void *stream);
+                                   const void *beta_tilde, const float *d, const float *h0,
+                                   const void *dO, const float *dht, float *dq, float *dk,
+                                   float *dv, float *dg, float *dbeta, float *dbeta_tilde,
+                                   float *dd, float *dh0, void *ws, size_t ws_bytes,
+                                   void *stream);
 
 /*
  * Stage timing, for benchmarks (not part of the method).  comba_profile_enable(1)

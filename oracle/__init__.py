@@ -169,13 +169,19 @@ def step_bwd(q, k, v, g, beta, d, h0, dO, dht=None, *, cu_seqlens=None, beta_til
     return res
 
 
+def _workload_beta_tilde(w, sel):
+    bt = w.extra.get("beta_tilde")
+    return None if bt is None else bt[:, :, sel]
+
+
 def workload_fwd(w, *, heads=None, nthreads=None):
-    """Oracle forward on a comba_inputs.Workload (optionally a subset of heads)."""
+    """Oracle forward on a comba_inputs.Workload (optionally a subset of heads);
+    a separate feedback strength in ``w.extra['beta_tilde']`` is used when present."""
     sel = slice(None) if heads is None else list(heads)
     h0 = None if w.h0 is None else w.h0[:, sel]
     return step_fwd(w.q[:, :, sel], w.k[:, :, sel], w.v[:, :, sel], w.g[:, :, sel],
                     w.beta[:, :, sel], w.d[sel], h0, cu_seqlens=w.cu_seqlens,
-                    nthreads=nthreads)
+                    beta_tilde=_workload_beta_tilde(w, sel), nthreads=nthreads)
 
 
 def workload_bwd(w, *, heads=None, nthreads=None):
@@ -185,4 +191,5 @@ def workload_bwd(w, *, heads=None, nthreads=None):
     dht = None if w.dht is None else w.dht[:, sel]
     return step_bwd(w.q[:, :, sel], w.k[:, :, sel], w.v[:, :, sel], w.g[:, :, sel],
                     w.beta[:, :, sel], w.d[sel], h0, w.dO[:, :, sel], dht,
-                    cu_seqlens=w.cu_seqlens, nthreads=nthreads)
+                    cu_seqlens=w.cu_seqlens, beta_tilde=_workload_beta_tilde(w, sel),
+                    nthreads=nthreads)

@@ -14,7 +14,10 @@ Shapes (see include/comba.h): q, k [B,T,H,dk]; v, dO [B,T,H,dv]; g, beta [B,T,H]
 d [H]; h0, dht [N,H,dk,dv].  q, k, v, beta, dO share one dtype (bfloat16 or
 float32); g, d and states are float32; all outputs are float32.  Pass
 ``cu_seqlens`` (int32 [N+1] on the device) for a packed variable-length batch
-with B == 1.
+with B == 1.  ``beta_tilde=`` ([B,T,H], the dtype of q) gives the state
+feedback strength its own value (Section 3.2; omitted: tied to beta); the
+backward then also returns ``dbeta_tilde`` and ``dbeta`` covers the write
+strength only.
 """
 from __future__ import annotations
 
@@ -70,13 +73,13 @@ def load_library():
             lib.comba_fwd_workspace_bytes.restype = Z
             lib.comba_bwd_workspace_bytes.argtypes = [SP]
             lib.comba_bwd_workspace_bytes.restype = Z
-            lib.comba_chunk_fwd.argtypes = [SP] + [P] * 9 + [P, Z, P]
+            lib.comba_chunk_fwd.argtypes = [SP] + [P] * 10 + [P, Z, P]
             lib.comba_chunk_fwd.restype = I
-            lib.comba_chunk_bwd.argtypes = [SP] + [P] * 16 + [P, Z, P]
+            lib.comba_chunk_bwd.argtypes = [SP] + [P] * 18 + [P, Z, P]
             lib.comba_chunk_bwd.restype = I
-            lib.comba_chunk_fwd_save.argtypes = [SP] + [P] * 9 + [P, Z, P]
+            lib.comba_chunk_fwd_save.argtypes = [SP] + [P] * 10 + [P, Z, P]
             lib.comba_chunk_fwd_save.restype = I
-            lib.comba_chunk_bwd_saved.argtypes = [SP] + [P] * 16 + [P, Z, P]
+            lib.comba_chunk_bwd_saved.argtypes = [SP] + [P] * 18 + [P, Z, P]
             lib.comba_chunk_bwd_saved.restype = I
             lib.comba_profile_enable.argtypes = [I]
             lib.comba_profile_enable.restype = I
@@ -180,11 +183,21 @@ def _prepare(q, k, v, g, beta, d, h0, cu_seqlens, extra=()):
     return shp, (B, T, H, dk, dv, N)
 
 
-def _fwd(save, q, k, v, g, beta, d, h0, cu_seqlens, output_final_state, workspace, stream):
+def _beta_tilde(beta_tilde, beta):
+    if beta_tilde is None:
+        return ()
+    if tuple(beta_tilde.shape) != tuple(beta.shape):
+        raise CombaError("comba: beta_tilde must have the shape of beta [B,T,H]")
+    return (("beta_tilde", beta_tilde),)
+
+
+def _fwd(save, q, k, v, g, beta, d, h0, cu_seqlens, output_final_state, workspace, stream,
+         beta_tilde):
     import torch
 
     lib = load_library()
-    shp, (B, T, H, dk, dv, N) = _prepare(q, k, v, g, beta, d, h0, cu_seqlens)
+    shp, (B, T, H, dk, dv, N) = _prepare(q, k, v, g, beta, d, h0, cu_seqlens,
+                                         extra=_beta_tilde(beta_tilde, beta))
     o = torch.empty((B, T, H, dv), dtype=torch.float32, device=q.device)
     ht = torch.empty((N, H, dk, dv), dtype=torch.float32, device=q.device) \
         if output_final_state else None
@@ -196,36 +209,37 @@ def _fwd(save, q, k, v, g, beta, d, h0, cu_seqlens, output_final_state, workspac
         workspace = torch.empty(nbytes, dtype=torch.uint8, device=q.device)
     st = torch.cuda.current_stream(q.device).cuda_stream if stream is None else stream
     fn = lib.comba_chunk_fwd_save if save else lib.comba_chunk_fwd
-    _check(fn(ctypes.byref(shp), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(d),
-              _ptr(h0), _ptr(o), _ptr(ht), _ptr(workspace), ctypes.c_size_t(workspace.numel()),
-              ctypes.c_void_p(st)))
+    _check(fn(ctypes.byref(shp), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta),
+              _ptr(beta_tilde), _ptr(d), _ptr(h0), _ptr(o), _ptr(ht), _ptr(workspace),
+              ctypes.c_size_t(workspace.numel()), ctypes.c_void_p(st)))
     return o, ht, workspace
 
 
-def comba_chunk_fwd(q, k, v, g, beta, d, h0=None, *, cu_seqlens=None, output_final_state=True,
-                    workspace=None, stream=None):
+def comba_chunk_fwd(q, k, v, g, beta, d, h0=None, *, beta_tilde=None, cu_seqlens=None,
+                    output_final_state=True, workspace=None, stream=None):
     """Chunk-wise forward.  Returns (o [B,T,H,dv] fp32, ht [N,H,dk,dv] fp32 or None)."""
     o, ht, _ = _fwd(False, q, k, v, g, beta, d, h0, cu_seqlens, output_final_state, workspace,
-                    stream)
+                    stream, beta_tilde)
     return o, ht
 
 
-def comba_chunk_fwd_save(q, k, v, g, beta, d, h0=None, *, cu_seqlens=None,
+def comba_chunk_fwd_save(q, k, v, g, beta, d, h0=None, *, beta_tilde=None, cu_seqlens=None,
                          output_final_state=True, workspace=None, stream=None):
     """Forward that also keeps the backward's state in a backward-sized workspace.
 
     Returns (o, ht, workspace); pass the same inputs and `workspace` to
     comba_chunk_bwd_saved."""
     return _fwd(True, q, k, v, g, beta, d, h0, cu_seqlens, output_final_state, workspace,
-                stream)
+                stream, beta_tilde)
 
 
-def _bwd(saved, q, k, v, g, beta, d, h0, dO, dht, cu_seqlens, need_dh0, workspace, stream):
+def _bwd(saved, q, k, v, g, beta, d, h0, dO, dht, cu_seqlens, need_dh0, workspace, stream,
+         beta_tilde):
     import torch
 
     lib = load_library()
     shp, (B, T, H, dk, dv, N) = _prepare(q, k, v, g, beta, d, h0, cu_seqlens,
-                                         extra=(("dO", dO),))
+                                         extra=(("dO", dO),) + _beta_tilde(beta_tilde, beta))
     if dht is not None and (dht.dtype != torch.float32 or tuple(dht.shape) != (N, H, dk, dv)
                             or not dht.is_contiguous()):
         raise CombaError("comba: dht must be contiguous float32 [N,H,dk,dv]")
@@ -239,6 +253,8 @@ def _bwd(saved, q, k, v, g, beta, d, h0, dO, dht, cu_seqlens, need_dh0, workspac
         "dv": torch.empty((B, T, H, dv), dtype=f32, device=dev),
         "dg": torch.empty((B, T, H), dtype=f32, device=dev),
         "dbeta": torch.empty((B, T, H), dtype=f32, device=dev),
+        "dbeta_tilde": None if beta_tilde is None else torch.empty((B, T, H), dtype=f32,
+                                                                   device=dev),
         "dd": torch.empty((H,), dtype=f32, device=dev),
         "dh0": torch.empty((N, H, dk, dv), dtype=f32, device=dev) if need_dh0 else None,
     }
@@ -252,21 +268,27 @@ def _bwd(saved, q, k, v, g, beta, d, h0, dO, dht, cu_seqlens, need_dh0, workspac
         workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
     st = torch.cuda.current_stream(dev).cuda_stream if stream is None else stream
     fn = lib.comba_chunk_bwd_saved if saved else lib.comba_chunk_bwd
-    _check(fn(ctypes.byref(shp), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(d),
-              _ptr(h0), _ptr(dO), _ptr(dht), _ptr(out["dq"]), _ptr(out["dk"]), _ptr(out["dv"]),
-              _ptr(out["dg"]), _ptr(out["dbeta"]), _ptr(out["dd"]), _ptr(out["dh0"]),
-              _ptr(workspace), ctypes.c_size_t(workspace.numel()), ctypes.c_void_p(st)))
+    _check(fn(ctypes.byref(shp), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta),
+              _ptr(beta_tilde), _ptr(d), _ptr(h0), _ptr(dO), _ptr(dht), _ptr(out["dq"]),
+              _ptr(out["dk"]), _ptr(out["dv"]), _ptr(out["dg"]), _ptr(out["dbeta"]),
+              _ptr(out["dbeta_tilde"]), _ptr(out["dd"]), _ptr(out["dh0"]), _ptr(workspace),
+              ctypes.c_size_t(workspace.numel()), ctypes.c_void_p(st)))
+    if beta_tilde is None:
+        del out["dbeta_tilde"]
     return out
 
 
-def comba_chunk_bwd(q, k, v, g, beta, d, h0, dO, dht=None, *, cu_seqlens=None,
+def comba_chunk_bwd(q, k, v, g, beta, d, h0, dO, dht=None, *, beta_tilde=None, cu_seqlens=None,
                     need_dh0=True, workspace=None, stream=None):
     """Chunk-wise backward (recomputes the forward).  Returns dict dq, dk, dv, dg, dbeta, dd,
-    dh0 (fp32)."""
-    return _bwd(False, q, k, v, g, beta, d, h0, dO, dht, cu_seqlens, need_dh0, workspace, stream)
+    dh0 (fp32), and dbeta_tilde when beta_tilde is given (dbeta is then the derivative
+    through the write strength only; otherwise it is the total derivative)."""
+    return _bwd(False, q, k, v, g, beta, d, h0, dO, dht, cu_seqlens, need_dh0, workspace, stream,
+                beta_tilde)
 
 
-def comba_chunk_bwd_saved(q, k, v, g, beta, d, h0, dO, dht=None, *, workspace, cu_seqlens=None,
-                          need_dh0=True, stream=None):
+def comba_chunk_bwd_saved(q, k, v, g, beta, d, h0, dO, dht=None, *, workspace, beta_tilde=None,
+                          cu_seqlens=None, need_dh0=True, stream=None):
     """Backward reusing the state left by comba_chunk_fwd_save in `workspace`."""
-    return _bwd(True, q, k, v, g, beta, d, h0, dO, dht, cu_seqlens, need_dh0, workspace, stream)
+    return _bwd(True, q, k, v, g, beta, d, h0, dO, dht, cu_seqlens, need_dh0, workspace, stream,
+                beta_tilde)

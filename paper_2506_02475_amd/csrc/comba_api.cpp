@@ -212,9 +212,9 @@ void fill_common(comba::LaunchArgs& a, const Dims& d, const comba_shape* s) {
 }
 
 comba_status chunk_fwd(bool save, const comba_shape* shape, const void* q, const void* k,
-                              const void* v, const float* g, const void* beta, const float* d,
-                              const float* h0, float* o, float* ht, void* ws, size_t ws_bytes,
-                              void* stream) {
+                       const void* v, const float* g, const void* beta, const void* beta_tilde,
+                       const float* d, const float* h0, float* o, float* ht, void* ws,
+                       size_t ws_bytes, void* stream) {
   Dims dm;
   comba_status st = check_shape(shape, &dm);
   if (st != COMBA_OK) return st;
@@ -223,7 +223,8 @@ comba_status chunk_fwd(bool save, const comba_shape* shape, const void* q, const
   if ((tok && (!q || !k || !v || !g || !beta || !o)) || !d || !ws) return COMBA_ERR_NULL;
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(ws, kAlign) ||
       !aligned(g, 4) || !aligned(d, 4) || !aligned(o, 16) || (h0 && !aligned(h0, 16)) ||
-      (ht && !aligned(ht, 16)) || !aligned(beta, dm.bf16 ? 2 : 4))
+      (ht && !aligned(ht, 16)) || !aligned(beta, dm.bf16 ? 2 : 4) ||
+      !aligned(beta_tilde, dm.bf16 ? 2 : 4))
     return COMBA_ERR_ALIGN;
   const Layout L = layout(dm, save);
   if (ws_bytes < L.total) return COMBA_ERR_WORKSPACE;
@@ -234,6 +235,7 @@ comba_status chunk_fwd(bool save, const comba_shape* shape, const void* q, const
   a.k = k;
   a.v = v;
   a.beta = beta;
+  a.beta_tilde = beta_tilde ? beta_tilde : beta;  // NULL: tied to beta
   a.g = g;
   a.d = d;
   a.h0 = h0;
@@ -247,23 +249,27 @@ comba_status chunk_fwd(bool save, const comba_shape* shape, const void* q, const
 }
 
 comba_status chunk_bwd(bool saved, const comba_shape* shape, const void* q, const void* k,
-                              const void* v, const float* g, const void* beta, const float* d,
-                              const float* h0, const void* dO, const float* dht, float* dq,
-                              float* dk, float* dv, float* dg, float* dbeta, float* dd,
-                              float* dh0, void* ws, size_t ws_bytes, void* stream) {
+                       const void* v, const float* g, const void* beta, const void* beta_tilde,
+                       const float* d, const float* h0, const void* dO, const float* dht,
+                       float* dq, float* dk, float* dv, float* dg, float* dbeta,
+                       float* dbeta_tilde, float* dd, float* dh0, void* ws, size_t ws_bytes,
+                       void* stream) {
   Dims dm;
   comba_status st = check_shape(shape, &dm);
   if (st != COMBA_OK) return st;
   // token tensors may be NULL when the call has no tokens (states pass through)
   const bool tok = dm.Ttot > 0;
-  if ((tok && (!q || !k || !v || !g || !beta || !dO || !dq || !dk || !dv || !dg || !dbeta)) ||
+  // a separate beta~ needs its own gradient
+  if ((tok && (!q || !k || !v || !g || !beta || !dO || !dq || !dk || !dv || !dg || !dbeta ||
+               (beta_tilde && !dbeta_tilde))) ||
       !d || !dd || !ws)
     return COMBA_ERR_NULL;
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(dO, 16) ||
       !aligned(ws, kAlign) || !aligned(g, 4) || !aligned(d, 4) || !aligned(dq, 16) ||
       !aligned(dk, 16) || !aligned(dv, 16) || !aligned(dg, 4) || !aligned(dbeta, 4) ||
       !aligned(dd, 4) || (h0 && !aligned(h0, 16)) || (dht && !aligned(dht, 16)) ||
-      (dh0 && !aligned(dh0, 16)) || !aligned(beta, dm.bf16 ? 2 : 4))
+      (dh0 && !aligned(dh0, 16)) || !aligned(beta, dm.bf16 ? 2 : 4) ||
+      !aligned(beta_tilde, dm.bf16 ? 2 : 4) || !aligned(dbeta_tilde, 4))
     return COMBA_ERR_ALIGN;
   const Layout L = layout(dm, true);
   if (ws_bytes < L.total) return COMBA_ERR_WORKSPACE;
@@ -274,6 +280,7 @@ comba_status chunk_bwd(bool saved, const comba_shape* shape, const void* q, cons
   a.k = k;
   a.v = v;
   a.beta = beta;
+  a.beta_tilde = beta_tilde ? beta_tilde : beta;  // NULL: tied to beta
   a.dO = dO;
   a.g = g;
   a.d = d;
@@ -284,6 +291,7 @@ comba_status chunk_bwd(bool saved, const comba_shape* shape, const void* q, cons
   a.dv_ = dv;
   a.dg = dg;
   a.dbeta = dbeta;
+  a.dbeta_tilde = dbeta_tilde;  // NULL: dbeta holds the total derivative
   a.dd = dd;
   a.dh0 = dh0;
   a.stream = static_cast<hipStream_t>(stream);
@@ -330,35 +338,38 @@ int comba_profile_read(float* ms, const char** names, int capacity) {
 }
 
 comba_status comba_chunk_fwd(const comba_shape* shape, const void* q, const void* k, const void* v,
-                             const float* g, const void* beta, const float* d, const float* h0,
-                             float* o, float* ht, void* ws, size_t ws_bytes, void* stream) {
-  return chunk_fwd(false, shape, q, k, v, g, beta, d, h0, o, ht, ws, ws_bytes, stream);
+                             const float* g, const void* beta, const void* beta_tilde,
+                             const float* d, const float* h0, float* o, float* ht, void* ws,
+                             size_t ws_bytes, void* stream) {
+  return chunk_fwd(false, shape, q, k, v, g, beta, beta_tilde, d, h0, o, ht, ws, ws_bytes, stream);
 }
 
 comba_status comba_chunk_fwd_save(const comba_shape* shape, const void* q, const void* k,
-                                  const void* v, const float* g, const void* beta, const float* d,
-                                  const float* h0, float* o, float* ht, void* ws, size_t ws_bytes,
-                                  void* stream) {
-  return chunk_fwd(true, shape, q, k, v, g, beta, d, h0, o, ht, ws, ws_bytes, stream);
+                                  const void* v, const float* g, const void* beta,
+                                  const void* beta_tilde, const float* d, const float* h0, float* o,
+                                  float* ht, void* ws, size_t ws_bytes, void* stream) {
+  return chunk_fwd(true, shape, q, k, v, g, beta, beta_tilde, d, h0, o, ht, ws, ws_bytes, stream);
 }
 
 comba_status comba_chunk_bwd(const comba_shape* shape, const void* q, const void* k, const void* v,
-                             const float* g, const void* beta, const float* d, const float* h0,
-                             const void* dO, const float* dht, float* dq, float* dk, float* dv,
-                             float* dg, float* dbeta, float* dd, float* dh0, void* ws,
-                             size_t ws_bytes, void* stream) {
-  return chunk_bwd(false, shape, q, k, v, g, beta, d, h0, dO, dht, dq, dk, dv, dg, dbeta, dd, dh0,
-                   ws, ws_bytes, stream);
+                             const float* g, const void* beta, const void* beta_tilde,
+                             const float* d, const float* h0, const void* dO, const float* dht,
+                             float* dq, float* dk, float* dv, float* dg, float* dbeta,
+                             float* dbeta_tilde, float* dd, float* dh0, void* ws, size_t ws_bytes,
+                             void* stream) {
+  return chunk_bwd(false, shape, q, k, v, g, beta, beta_tilde, d, h0, dO, dht, dq, dk, dv, dg,
+                   dbeta, dbeta_tilde, dd, dh0, ws, ws_bytes, stream);
 }
 
 comba_status comba_chunk_bwd_saved(const comba_shape* shape, const void* q, const void* k,
                                    const void* v, const float* g, const void* beta,
-                                   const float* d, const float* h0, const void* dO,
-                                   const float* dht, float* dq, float* dk, float* dv, float* dg,
-                                   float* dbeta, float* dd, float* dh0, void* ws, size_t ws_bytes,
+                                   const void* beta_tilde, const float* d, const float* h0,
+                                   const void* dO, const float* dht, float* dq, float* dk,
+                                   float* dv, float* dg, float* dbeta, float* dbeta_tilde,
+                                   float* dd, float* dh0, void* ws, size_t ws_bytes,
                                    void* stream) {
-  return chunk_bwd(true, shape, q, k, v, g, beta, d, h0, dO, dht, dq, dk, dv, dg, dbeta, dd, dh0,
-                   ws, ws_bytes, stream);
+  return chunk_bwd(true, shape, q, k, v, g, beta, beta_tilde, d, h0, dO, dht, dq, dk, dv, dg,
+                   dbeta, dbeta_tilde, dd, dh0, ws, ws_bytes, stream);
 }
 
 const char* comba_status_string(comba_status s) {

@@ -28,7 +28,7 @@
 //   k_scan_fwd   per (sequence, head, 32-column slice of dv): the sequential
 //                state recurrence over chunks, fused with the output
 //   k_scan_bwd   the reverse recurrence of the state gradient
-//   k_intra_bwd  per chunk-head gradients dq, dk, dv, dbeta, dg, partial dd
+//   k_intra_bwd  per chunk-head gradients dq, dk, dv, dbeta (, dbeta~), dg, partial dd
 //   k_reduce_dd  deterministic sum of the partial dd over chunks
 #include <hip/hip_runtime.h>
 
@@ -122,7 +122,7 @@ __global__ __launch_bounds__(NTHR) void k_chunk_map(const int32_t* __restrict__ 
 template <typename Tin, int DK>
 __global__ __launch_bounds__(NTHR) void k_prep(const Tin* __restrict__ q, const Tin* __restrict__ k,
                                                const float* __restrict__ g,
-                                               const Tin* __restrict__ beta,
+                                               const Tin* __restrict__ beta_tilde,
                                                const float* __restrict__ d,
                                                const ChunkInfo* __restrict__ cmap, int H,
                                                float* __restrict__ Mw, float* __restrict__ Aw,
@@ -153,7 +153,7 @@ __global__ __launch_bounds__(NTHR) void k_prep(const Tin* __restrict__ q, const 
     const float gr = lane < ci.len ? g[tok + (long)lane * H] : 0.f;
     const float G = wave_prefix_sum(gr);
     Gs[lane] = G;
-    Bs[lane] = lane < ci.len ? to_f(beta[tok + (long)lane * H]) : 0.f;
+    Bs[lane] = lane < ci.len ? to_f(beta_tilde[tok + (long)lane * H]) : 0.f;  // feedback strength
     Gw[chh * CH + lane] = G;
   }
   __syncthreads();
@@ -217,10 +217,11 @@ __global__ __launch_bounds__(NTHR) void k_prep(const Tin* __restrict__ q, const 
 template <typename Tin, int DK, int DV, bool OUT, bool STORE>
 __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd(
     const Tin* __restrict__ q, const Tin* __restrict__ k, const Tin* __restrict__ v,
-    const Tin* __restrict__ beta, const float* __restrict__ d, const float* __restrict__ h0,
-    const ChunkInfo* __restrict__ cmap, const SeqInfo* __restrict__ smap, int H,
-    const float* __restrict__ Mw, const float* __restrict__ Aw, const float* __restrict__ Gw,
-    float* __restrict__ o, float* __restrict__ ht, float* __restrict__ Xw, float* __restrict__ Dw) {
+    const Tin* __restrict__ beta, const Tin* __restrict__ beta_tilde, const float* __restrict__ d,
+    const float* __restrict__ h0, const ChunkInfo* __restrict__ cmap,
+    const SeqInfo* __restrict__ smap, int H, const float* __restrict__ Mw,
+    const float* __restrict__ Aw, const float* __restrict__ Gw, float* __restrict__ o,
+    float* __restrict__ ht, float* __restrict__ Xw, float* __restrict__ Dw) {
   constexpr bool F32 = is_f32<Tin>::value;
   constexpr int BV = 32, NTV = BV / 16, XMT = DK / 64;
   constexpr int PI = Pad<Tin>::value;
@@ -236,7 +237,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd(
   __shared__ __align__(16) float RT[BV * LDF];
   __shared__ __align__(16) float DT[OUT ? BV * LDF : 4];
   __shared__ __align__(16) float DgT[BV * LDF];
-  __shared__ float Gs[CH], Bs[CH];
+  __shared__ float Gs[CH], Bs[CH], Bts[CH];
 
   const int s = blockIdx.x, h = blockIdx.y, j0 = blockIdx.z * BV;
   const SeqInfo si = smap[s];
@@ -260,7 +261,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd(
   TileRegs<Tin, CH, DK> pk, pq;
   TileRegs<Tin, CH, BV> pv;
   TileRegs<float, CH, CH> pm, pa;
-  float pg = 0.f, pb = 0.f;
+  float pg = 0.f, pb = 0.f, pbt = 0.f;
   auto issue = [&](int cc) {
     const int len = min(CH, si.len - cc * CH);
     const long chh = (long)(si.chunk0 + cc) * H + h;
@@ -274,6 +275,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd(
       const int r = threadIdx.x;
       pg = Gw[chh * CH + r];
       pb = r < len ? to_f(beta[tok + (long)r * H]) : 0.f;
+      pbt = r < len ? to_f(beta_tilde[tok + (long)r * H]) : 0.f;
     }
   };
   if (si.nchunks > 0) issue(0);
@@ -293,6 +295,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd(
     if (threadIdx.x < CH) {
       Gs[threadIdx.x] = pg;
       Bs[threadIdx.x] = pb;
+      Bts[threadIdx.x] = pbt;
     }
     if constexpr (STORE) {
 #pragma unroll
@@ -309,7 +312,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd(
     if (cc + 1 < si.nchunks) issue(cc + 1);
     const float Glast = Gs[CH - 1];
 
-    // K X and Q X for rows 16w..16w+15; R = Diag(beta)(V - Diag(exp Gm) K X)
+    // K X and Q X for rows 16w..16w+15; R = Diag(beta) V - Diag(beta~ exp Gm) K X
     floatx4 kx[1][NTV], qx[1][NTV];
     zero_acc(kx);
     mma<F32, 1, NTV, DK>(kx, Ks + 16 * w * LDK, LDK, XT, LDX);
@@ -325,7 +328,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd(
         const int r = 16 * w + acc_row(0, e), jj = acc_col(nt);
         const float kxv = kx[0][nt][e];
         const float gm = r > 0 ? Gs[r - 1] : 0.f;
-        RT[jj * LDF + r] = Bs[r] * (to_f(Vs[r * LDV + jj]) - __expf(gm) * kxv);
+        RT[jj * LDF + r] = Bs[r] * to_f(Vs[r * LDV + jj]) - Bts[r] * __expf(gm) * kxv;
         if constexpr (OUT) oacc[0][nt][e] = __expf(Gs[r]) * (qx[0][nt][e] - dh * kxv);
       }
     __syncthreads();
@@ -393,7 +396,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd(
 template <typename Tin, int DK, int DV>
 __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd(
     const Tin* __restrict__ q, const Tin* __restrict__ k, const Tin* __restrict__ dO,
-    const Tin* __restrict__ beta, const float* __restrict__ d, const float* __restrict__ dht,
+    const Tin* __restrict__ beta_tilde, const float* __restrict__ d, const float* __restrict__ dht,
     const ChunkInfo* __restrict__ cmap, const SeqInfo* __restrict__ smap, int H,
     const float* __restrict__ Mw, const float* __restrict__ Aw, const float* __restrict__ Gw,
     float* __restrict__ dh0, float* __restrict__ Yw, float* __restrict__ dRw) {
@@ -448,7 +451,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd(
     if (threadIdx.x < CH) {
       const int r = threadIdx.x;
       pg = Gw[chh * CH + r];
-      pb = r < len ? to_f(beta[tok + (long)r * H]) : 0.f;
+      pb = r < len ? to_f(beta_tilde[tok + (long)r * H]) : 0.f;
     }
   };
   if (si.nchunks > 0) issue(si.nchunks - 1);
@@ -494,7 +497,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd(
       }
     __syncthreads();
 
-    // dR = M^T dD;  Pg = Diag(exp G) dO;  W2 = -d Pg - Diag(beta exp Gm) dR
+    // dR = M^T dD;  Pg = Diag(exp G) dO;  W2 = -d Pg - Diag(beta~ exp Gm) dR
     floatx4 dr[1][NTV];
     zero_acc(dr);
     mma<F32, 1, NTV, CH>(dr, MsT + 16 * w * LDF, LDF, dDT, LDF);
@@ -567,19 +570,21 @@ struct IntraBwdSmem {
 template <typename Tin, int DK, int DV>
 __global__ __launch_bounds__(NTHR, 1) void k_intra_bwd(
     const Tin* __restrict__ q, const Tin* __restrict__ k, const Tin* __restrict__ v,
-    const Tin* __restrict__ dO, const Tin* __restrict__ beta, const float* __restrict__ d,
-    const ChunkInfo* __restrict__ cmap, int H, const float* __restrict__ Gw,
-    const float* __restrict__ Xw, const float* __restrict__ Dw, const float* __restrict__ Yw,
-    const float* __restrict__ dRw, float* __restrict__ dq, float* __restrict__ dk,
-    float* __restrict__ dv, float* __restrict__ dbeta, float* __restrict__ dg,
-    float* __restrict__ ddp) {
+    const Tin* __restrict__ dO, const Tin* __restrict__ beta, const Tin* __restrict__ beta_tilde,
+    const float* __restrict__ d, const ChunkInfo* __restrict__ cmap, int H,
+    const float* __restrict__ Gw, const float* __restrict__ Xw, const float* __restrict__ Dw,
+    const float* __restrict__ Yw, const float* __restrict__ dRw, float* __restrict__ dq,
+    float* __restrict__ dk, float* __restrict__ dv, float* __restrict__ dbeta,
+    float* __restrict__ dbeta_tilde, float* __restrict__ dg, float* __restrict__ ddp) {
   using SM = IntraBwdSmem<Tin, DK, DV>;
   constexpr bool F32 = is_f32<Tin>::value;
   constexpr int VB = SM::VB, LDK = SM::LDK, LDC = SM::LDC, LDVB = SM::LDVB, LDF = SM::LDF,
                 LDFB = SM::LDFB;
   constexpr int NTK = DK / 16;
   __shared__ __align__(16) char smem[SM::BYTES];
-  __shared__ float Gs[CH], Bs[CH], rowG[CH], rowGm[CH], rowB[CH];
+  // rowB: derivative through beta (write strength), rowBt: through beta~
+  // (feedback strength, in L and in R's K X term)
+  __shared__ float Gs[CH], Bs[CH], Bts[CH], rowG[CH], rowGm[CH], rowB[CH], rowBt[CH];
   __shared__ float colpart[NWAVE][CH];
   __shared__ float scal[NWAVE][3];
 
@@ -598,8 +603,10 @@ __global__ __launch_bounds__(NTHR, 1) void k_intra_bwd(
   if (tid < CH) {
     Gs[tid] = Gw[chh * CH + tid];
     Bs[tid] = tid < len ? to_f(beta[tok + (long)tid * H]) : 0.f;
+    Bts[tid] = tid < len ? to_f(beta_tilde[tok + (long)tid * H]) : 0.f;
     rowG[tid] = 0.f;
     rowGm[tid] = 0.f;
+    rowBt[tid] = 0.f;
   }
 
   // ---------------- phase 1: reductions over dv ----------------
@@ -710,9 +717,9 @@ __global__ __launch_bounds__(NTHR, 1) void k_intra_bwd(
           const float lc = __expf(Gs[r - 1] - Gs[c]);
           const float dl = -dLr[0][nt][e];
           const float lck = lc * kk;
-          e2 = dl * Bs[r] * lck;
+          e2 = dl * Bts[r] * lck;
           rBL[e] += dl * lck;
-          dakk = dl * Bs[r] * lc;
+          dakk = dl * Bts[r] * lc;
         }
         rE1[e] += e1;
         rE2[e] += e2;
@@ -738,7 +745,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_intra_bwd(
         const int r = 16 * w + acc_row(0, e);
         rowG[r] += rE1[e];
         rowGm[r] += rE2[e];
-        rowB[r] += rBL[e];
+        rowBt[r] += rBL[e];
       }
     }
   }
@@ -774,8 +781,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_intra_bwd(
         const float cr = __expf(Glast - Gs[r]) * p2[e];
         const float egm = __expf(r > 0 ? Gs[r - 1] : 0.f);
         rowG[r] += __expf(Gs[r]) * p1[e] - cr;
-        rowGm[r] -= Bs[r] * egm * p3[e];
-        rowB[r] -= egm * p3[e];
+        rowGm[r] -= Bts[r] * egm * p3[e];
+        rowBt[r] -= egm * p3[e];
         gcp += cr;
       }
     }
@@ -791,7 +798,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_intra_bwd(
       const int r = 16 * w + acc_row(0, e);
       const float egm = __expf(r > 0 ? Gs[r - 1] : 0.f);
       T1[0][nt][e] *= __expf(Gs[r]);
-      T2[0][nt][e] = __expf(Glast - Gs[r]) * T2[0][nt][e] - Bs[r] * egm * T3[0][nt][e];
+      T2[0][nt][e] = __expf(Glast - Gs[r]) * T2[0][nt][e] - Bts[r] * egm * T3[0][nt][e];
     }
   mma<F32, 1, NTK, CH>(T1, dAG + 16 * w * LDF, LDF, KsT, LDC);
   mma<F32, 1, NTK, CH>(T2, dAGT + 16 * w * LDF, LDF, QsT, LDC);
@@ -832,7 +839,12 @@ __global__ __launch_bounds__(NTHR, 1) void k_intra_bwd(
     const float dgr = __shfl(x, 63 - lane);
     if (r < len) {
       dg[tok + (long)r * H] = dgr;
-      dbeta[tok + (long)r * H] = rowB[r];
+      if (dbeta_tilde) {
+        dbeta[tok + (long)r * H] = rowB[r];
+        dbeta_tilde[tok + (long)r * H] = rowBt[r];
+      } else {
+        dbeta[tok + (long)r * H] = rowB[r] + rowBt[r];
+      }
     }
     if (lane == 0) ddp[chh] = -dds;
   }
@@ -986,8 +998,8 @@ __device__ __forceinline__ void put_block_column(float* Ls, const floatx4 (&mb)[
 template <int DK, bool BWD>
 __global__ __launch_bounds__(NTHR) void k_prep_bf(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const float* __restrict__ g,
-    const bf16_t* __restrict__ beta, const float* __restrict__ d, const ChunkInfo* __restrict__ cmap,
-    int Tfix, int H, int16_t* __restrict__ Mq, float* __restrict__ Ms, int16_t* __restrict__ Aq,
+    const bf16_t* __restrict__ beta_tilde, const float* __restrict__ d,
+    const ChunkInfo* __restrict__ cmap, int Tfix, int H, int16_t* __restrict__ Mq, float* __restrict__ Ms, int16_t* __restrict__ Aq,
     float* __restrict__ As, int16_t* __restrict__ MTq, float* __restrict__ MTs,
     int16_t* __restrict__ ATq, float* __restrict__ ATs, bf16_t* __restrict__ QTp,
     float* __restrict__ Gw, float* __restrict__ sink) {
@@ -1017,7 +1029,7 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
     // every load is unconditional (clamped rows, zeroed where used): a branch
     // around a load makes the wave wait for it on the spot
     const long grow = tok + (long)min(lane, ci.len - 1) * H;
-    const float g_in = g[grow], b_in = bf2f(beta[grow]);
+    const float g_in = g[grow], b_in = bf2f(beta_tilde[grow]);  // feedback strength (L only)
     TileRegs<bf16_t, CH, DK> kr, qr;
     kr.load_clip(k + tok * DK, (long)H * DK, ci.len);
     qr.load_clip(q + tok * DK, (long)H * DK, ci.len);
@@ -1190,7 +1202,8 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
 template <int DK, int DV, int BV, bool OUT, bool STORE>
 __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
-    const bf16_t* __restrict__ beta, const float* __restrict__ d, const float* __restrict__ h0,
+    const bf16_t* __restrict__ beta, const bf16_t* __restrict__ beta_tilde,
+    const float* __restrict__ d, const float* __restrict__ h0,
     const SeqInfo* __restrict__ smap, int Tfix, int H, const int16_t* __restrict__ Mq,
     const float* __restrict__ Ms, const int16_t* __restrict__ Aq, const float* __restrict__ As,
     const float* __restrict__ Gw, float* __restrict__ o, float* __restrict__ ht, int16_t* __restrict__ Xq,
@@ -1292,16 +1305,16 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
   bf16x8 kf[KS], qf[KS];
   uint4 mq[2], aq[2];
   float msc, asc;
-  // per-row values of the chunk (cumulative gates G, beta, the V slice) are
-  // loaded one chunk ahead into registers and staged through a double-buffered
-  // LDS area at the end of each chunk
-  __shared__ float Grow[2][CH], Brow[2][CH];
+  // per-row values of the chunk (cumulative gates G, beta, beta~, the V slice)
+  // are loaded one chunk ahead into registers and staged through a
+  // double-buffered LDS area at the end of each chunk
+  __shared__ float Grow[2][CH], Brow[2][CH], BTrow[2][CH];
   __shared__ __align__(16) bf16_t Vrow[2][CH * (BV + 8)];
   constexpr int VPR = BV / 8;                  // 16-byte pieces per V row
   const int vr = threadIdx.x / VPR, vc = (threadIdx.x % VPR) * 8;
   const int vr_ld = min(vr, CH - 1);
   float pgv = 0.f;
-  bf16_t pbv = 0;
+  bf16_t pbv = 0, pbtv = 0;
   uint4 pvv = make_uint4(0, 0, 0, 0);
   int plen = 0;
   auto load_rows = [&](int cc) {
@@ -1310,18 +1323,20 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     const int t = threadIdx.x & (CH - 1);
     pgv = Gw[chh * CH + t];
     pbv = beta[tok + (long)min(t, plen - 1) * H];
+    pbtv = beta_tilde[tok + (long)min(t, plen - 1) * H];
     pvv = *reinterpret_cast<const uint4*>(v + (tok + (long)min(vr_ld, plen - 1) * H) * DV + j0 + vc);
   };
   auto put_rows = [&](int buf) {
     const int t = threadIdx.x & (CH - 1);
     Grow[buf][t] = pgv;
     Brow[buf][t] = t < plen ? bf2f(pbv) : 0.f;
+    BTrow[buf][t] = t < plen ? bf2f(pbtv) : 0.f;
     if (CH * VPR >= NTHR || threadIdx.x < CH * VPR)
       *reinterpret_cast<uint4*>(&Vrow[buf][vr * (BV + 8) + vc]) =
           vr < plen ? pvv : make_uint4(0, 0, 0, 0);
   };
   // rows past the chunk end load a valid row; their K X / Q X results are
-  // never used (beta = 0 zeroes R there and such outputs are not stored)
+  // never used (beta = beta~ = 0 zeroes R there and such outputs are not stored)
   auto load_kq = [&](int cc) {
     const long rb = (c_tok(cc) + (long)min(prow, c_len(cc) - 1) * H) * DK + 8 * g4;
 #pragma unroll
@@ -1364,9 +1379,10 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     load_rows(nx);
     const float glast = Grow[buf][CH - 1];
     const float gg = Grow[buf][prow], gm = prow > 0 ? Grow[buf][prow - 1] : 0.f, bb = Brow[buf][prow];
+    const float bt = BTrow[buf][prow];
 
     // (K X)^T and (Q X)^T: this lane holds row prow, columns 16 nt + col0 ..;
-    // R = Diag(beta)(V - Diag(exp Gm) K X)
+    // R = Diag(beta) V - Diag(beta~ exp Gm) K X
     floatx4 kx[NTV], qx[NTV];
 #pragma unroll
     for (int nt = 0; nt < NTV; ++nt) {
@@ -1392,7 +1408,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     load_kq(nx);
     floatx4 oacc[NTV];
     {
-      const float egm = __expf(gm), eg = __expf(gg);
+      const float btegm = bt * __expf(gm), eg = __expf(gg);
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt) {
         const uint2 v4 = *reinterpret_cast<const uint2*>(&Vrow[buf][prow * (BV + 8) + 16 * nt + col0]);
@@ -1401,7 +1417,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
         float rv[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          rv[e] = bb * (vv[e] - egm * kx[nt][e]);
+          rv[e] = bb * vv[e] - btegm * kx[nt][e];
           if constexpr (OUT) oacc[nt][e] = eg * (qx[nt][e] - dh * kx[nt][e]);
         }
         put_t4(Rh, Rl, prow * LDT + 16 * nt + col0, rv);
@@ -1531,7 +1547,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
 template <int DK, int DV, int BV>
 __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ dO,
-    const bf16_t* __restrict__ beta, const float* __restrict__ d, const float* __restrict__ dht,
+    const bf16_t* __restrict__ beta_tilde, const float* __restrict__ d, const float* __restrict__ dht,
     const SeqInfo* __restrict__ smap, int Tfix, int H, const int16_t* __restrict__ MTq,
     const float* __restrict__ MTs, const int16_t* __restrict__ ATq, const float* __restrict__ ATs,
     const bf16_t* __restrict__ QTp,
@@ -1625,7 +1641,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
   __shared__ __align__(16) bf16_t Kc[CH * LDKC];
   uint4 atq[2], mtq[2];
   float atsc, mtsc;
-  // per-row values (G, beta) and the dO slice are loaded one chunk ahead into
+  // per-row values (G, beta~) and the dO slice are loaded one chunk ahead into
   // registers and staged through double-buffered LDS at the end of each chunk
   __shared__ float Grow[2][CH], Brow[2][CH];
   float pgv = 0.f;
@@ -1663,7 +1679,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     const long tok = c_tok(cc), chh = c_chh(cc);
     const int t = threadIdx.x & (CH - 1);
     pgv = Gw[chh * CH + t];
-    pbv = beta[tok + (long)min(t, plen - 1) * H];
+    pbv = beta_tilde[tok + (long)min(t, plen - 1) * H];
   };
   auto put_rows = [&](int buf) {
     const int t = threadIdx.x & (CH - 1);
@@ -1761,7 +1777,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     }
     __syncthreads();
 
-    // dR = M^T dD;  Pg = Diag(exp G) dO;  W2 = -d Pg - Diag(beta exp Gm) dR
+    // dR = M^T dD;  Pg = Diag(exp G) dO;  W2 = -d Pg - Diag(beta~ exp Gm) dR
     floatx4 drr[NTV];
 #pragma unroll
     for (int nt = 0; nt < NTV; ++nt) drr[nt] = zero4();
@@ -1881,13 +1897,14 @@ __device__ __forceinline__ void split4v(const float4& x, bf16x4& hi, bf16x4& lo)
 template <int DK, int DV>
 __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
-    const bf16_t* __restrict__ dO, const bf16_t* __restrict__ beta, const float* __restrict__ d,
+    const bf16_t* __restrict__ dO, const bf16_t* __restrict__ beta,
+    const bf16_t* __restrict__ beta_tilde, const float* __restrict__ d,
     const ChunkInfo* __restrict__ cmap, int Tfix, int H, const float* __restrict__ Gw,
     const int16_t* __restrict__ Xq, const float* __restrict__ Xs, const int16_t* __restrict__ Dq,
     const float* __restrict__ Ds, const int16_t* __restrict__ Yq, const float* __restrict__ Ys,
     const int16_t* __restrict__ dRq, const float* __restrict__ dRs, int ncmax, float* __restrict__ dq, float* __restrict__ dk,
-    float* __restrict__ dv, float* __restrict__ dbeta, float* __restrict__ dg,
-    float* __restrict__ ddp, float* __restrict__ sink) {
+    float* __restrict__ dv, float* __restrict__ dbeta, float* __restrict__ dbeta_tilde,
+    float* __restrict__ dg, float* __restrict__ ddp, float* __restrict__ sink) {
   using SM = IntraBwdBfSmem<DK>;
   constexpr int VB = SM::VB, LDB = SM::LDB, LDK = SM::LDK, LDC = SM::LDC;
   constexpr int NTW = DK / 32;          // dk column tiles per wave
@@ -1895,7 +1912,9 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
   constexpr int NVB = DV / VB;
   constexpr int XP = DK * (VB / 4) / IB_THR;  // X / Y 16-byte pieces per thread
   __shared__ __align__(16) char smem[SM::BYTES];
-  __shared__ float Gs[CH], Bs[CH], rowB[CH];
+  // Bs: beta (write strength: dv), Bts: beta~ (feedback strength: L and R's
+  // K X term); rowB: <v, dR> per row, the derivative through beta
+  __shared__ float Gs[CH], Bs[CH], Bts[CH], rowB[CH];
   __shared__ float colpart[4][CH];      // per row tile: column sums of E1 + E2
   __shared__ float rowacc[2][6][CH];    // per column half: E1, E2, BL, p1, p2, p3 row sums
   __shared__ float scal[NW][2];         // per wave: <X, Y>_F, sum k . dQ~
@@ -1917,7 +1936,7 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
   const int nitems = ncmax * H;
   bool have = false;            // the item's first block is waiting in R0
   float g_nx = 0.f;              // and its gates
-  bf16_t b_nx = 0;               // and beta (raw: converted only when the item starts)
+  bf16_t b_nx = 0, bt_nx = 0;    // and beta, beta~ (raw: converted only when the item starts)
   for (int item = blockIdx.x; item < nitems; item += gridDim.x) {
   // The thread index passes through an opaque copy every item, so that the
   // values derived from it are formed inside the loop instead of being held
@@ -2044,7 +2063,7 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
   }
   dA[0] = dA[1] = dL[0] = dL[1] = zero4();
   TileRegs<bf16_t, CH, DK, IB_THR> kr, qr;
-  float g_in, b_in;
+  float g_in, b_in, bt_in;
   if (have) {
     // the copies into R0 were issued by this thread's wave; after the wait
     // and the barrier every wave's copies are in place
@@ -2066,11 +2085,13 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     }
     g_in = g_nx;
     b_in = bf2f(b_nx);
+    bt_in = bf2f(bt_nx);
   } else {
     issue(0);
     // gates and beta after the first block's loads, unconditional (clamped rows)
     g_in = Gw[chh * CH + (tid & (CH - 1))];
     b_in = bf2f(beta[tok + (long)min(tid & (CH - 1), len - 1) * H]);
+    bt_in = bf2f(beta_tilde[tok + (long)min(tid & (CH - 1), len - 1) * H]);
   }
   // unrolled: a rolled loop carries the prefetched registers through copies at
   // the back edge, which wait for the loads just issued
@@ -2082,6 +2103,7 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     if (vb == 0 && tid < CH) {
       Gs[tid] = g_in;
       Bs[tid] = tid < len ? b_in : 0.f;
+      Bts[tid] = tid < len ? bt_in : 0.f;
     }
     __syncthreads();
     put(vb);
@@ -2249,9 +2271,9 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
           const float lc = __expf(Gs[r - 1] - Gs[c]);
           const float dl = -dL[j2][e];
           const float lck = lc * kk;
-          e2 = dl * Bs[r] * lck;
+          e2 = dl * Bts[r] * lck;
           rBL[e] += dl * lck;
-          dakk = dl * Bs[r] * lc;
+          dakk = dl * Bts[r] * lc;
         }
         dagv[e] = dag;
         pv[e] = dakk;
@@ -2306,7 +2328,7 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
   for (int e = 0; e < 4; ++e) {
     const int r = 16 * rt + 4 * g4 + e;
     const float gr = __expf(Gs[r]), dec = __expf(Glast - Gs[r]);
-    const float sr = Bs[r] * __expf(r > 0 ? Gs[r - 1] : 0.f);
+    const float sr = Bts[r] * __expf(r > 0 ? Gs[r - 1] : 0.f);
 #pragma unroll
     for (int j = 0; j < NTW; ++j) {
       T1[j][e] *= gr;
@@ -2376,7 +2398,9 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     const int h2 = nxc / ncmax;
     const long chh2 = (long)(nxc % ncmax) * H + h2, tok2 = (long)ci2.tok0 * H + h2;
     g_nx = Gw[chh2 * CH + (tid & (CH - 1))];
-    b_nx = beta[tok2 + (long)min(tid & (CH - 1), max(ci2.len, 1) - 1) * H];
+    const long brow2 = tok2 + (long)min(tid & (CH - 1), max(ci2.len, 1) - 1) * H;
+    b_nx = beta[brow2];
+    bt_nx = beta_tilde[brow2];
   }
   ddpart = wave_sum(ddpart);
   if (lane == 0) scal[w][1] = ddpart;
@@ -2400,8 +2424,8 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     const float egm = __expf(r > 0 ? Gs[r - 1] : 0.f);
     const float cr = __expf(Glast - Gs[r]) * p2;
     const float rowg = e1 + __expf(Gs[r]) * p1 - cr;
-    const float rowgm = e2 - Bs[r] * egm * p3;
-    const float rowb = rowB[r] + bl - egm * p3;
+    const float rowgm = e2 - Bts[r] * egm * p3;
+    const float rowbt = bl - egm * p3;  // through beta~
     const float gcs = wave_sum(cr);
     const float rowgm_next = shift_down1(rowgm);
     float dG = rowg - col + (r + 1 < CH ? rowgm_next : 0.f);
@@ -2411,7 +2435,12 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     const float dgr = __shfl(x, 63 - lane);
     if (r < len) {
       at(dg + tok, 4u * (r * H)) = dgr;
-      at(dbeta + tok, 4u * (r * H)) = rowb;
+      if (dbeta_tilde) {
+        at(dbeta + tok, 4u * (r * H)) = rowB[r];
+        at(dbeta_tilde + tok, 4u * (r * H)) = rowbt;
+      } else {
+        at(dbeta + tok, 4u * (r * H)) = rowB[r] + rowbt;
+      }
     }
     if (lane == 0) ddp[chh] = -dds;
   }
@@ -2447,19 +2476,20 @@ static hipError_t run_fwd(const LaunchArgs& a) {
   const Tin* k = static_cast<const Tin*>(a.k);
   const Tin* v = static_cast<const Tin*>(a.v);
   const Tin* beta = static_cast<const Tin*>(a.beta);
+  const Tin* bt = static_cast<const Tin*>(a.beta_tilde);
   a.stage("chunk_map");
   k_chunk_map<<<1, NTHR, 0, st>>>(a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.ncmax, a.cmap, a.smap);
   a.stage("prep");
   if (a.ncmax > 0)
-    k_prep<Tin, DK><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(q, k, a.g, beta, a.d, a.cmap, a.H, a.Mw,
+    k_prep<Tin, DK><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(q, k, a.g, bt, a.d, a.cmap, a.H, a.Mw,
                                                          a.Aw, a.Gw);
   a.stage("scan_fwd");
   if (a.saved)
     k_scan_fwd<Tin, DK, DV, true, true><<<dim3(a.N, a.H, DV / 32), NTHR, 0, st>>>(
-        q, k, v, beta, a.d, a.h0, a.cmap, a.smap, a.H, a.Mw, a.Aw, a.Gw, a.o, a.ht, a.Xw, a.Dw);
+        q, k, v, beta, bt, a.d, a.h0, a.cmap, a.smap, a.H, a.Mw, a.Aw, a.Gw, a.o, a.ht, a.Xw, a.Dw);
   else
     k_scan_fwd<Tin, DK, DV, true, false><<<dim3(a.N, a.H, DV / 32), NTHR, 0, st>>>(
-        q, k, v, beta, a.d, a.h0, a.cmap, a.smap, a.H, a.Mw, a.Aw, a.Gw, a.o, a.ht, nullptr,
+        q, k, v, beta, bt, a.d, a.h0, a.cmap, a.smap, a.H, a.Mw, a.Aw, a.Gw, a.o, a.ht, nullptr,
         nullptr);
   a.stage(nullptr);
   return hipGetLastError();
@@ -2472,6 +2502,7 @@ static hipError_t run_bwd(const LaunchArgs& a) {
   const Tin* k = static_cast<const Tin*>(a.k);
   const Tin* v = static_cast<const Tin*>(a.v);
   const Tin* beta = static_cast<const Tin*>(a.beta);
+  const Tin* bt = static_cast<const Tin*>(a.beta_tilde);
   const Tin* dO = static_cast<const Tin*>(a.dO);
   if (a.N == 0) {
     // no sequences: dd (one value per head) is zero
@@ -2483,21 +2514,21 @@ static hipError_t run_bwd(const LaunchArgs& a) {
     k_chunk_map<<<1, NTHR, 0, st>>>(a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.ncmax, a.cmap, a.smap);
     a.stage("prep");
     if (a.ncmax > 0)
-      k_prep<Tin, DK><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(q, k, a.g, beta, a.d, a.cmap, a.H,
+      k_prep<Tin, DK><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(q, k, a.g, bt, a.d, a.cmap, a.H,
                                                            a.Mw, a.Aw, a.Gw);
     a.stage("scan_fwd_store");
     k_scan_fwd<Tin, DK, DV, false, true><<<dim3(a.N, a.H, DV / 32), NTHR, 0, st>>>(
-        q, k, v, beta, a.d, a.h0, a.cmap, a.smap, a.H, a.Mw, a.Aw, a.Gw, nullptr, nullptr, a.Xw,
+        q, k, v, beta, bt, a.d, a.h0, a.cmap, a.smap, a.H, a.Mw, a.Aw, a.Gw, nullptr, nullptr, a.Xw,
         a.Dw);
   }
   a.stage("scan_bwd");
   k_scan_bwd<Tin, DK, DV><<<dim3(a.N, a.H, DV / 32), NTHR, 0, st>>>(
-      q, k, dO, beta, a.d, a.dht, a.cmap, a.smap, a.H, a.Mw, a.Aw, a.Gw, a.dh0, a.Yw, a.dRw);
+      q, k, dO, bt, a.d, a.dht, a.cmap, a.smap, a.H, a.Mw, a.Aw, a.Gw, a.dh0, a.Yw, a.dRw);
   a.stage("intra_bwd");
   if (a.ncmax > 0)
     k_intra_bwd<Tin, DK, DV><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
-        q, k, v, dO, beta, a.d, a.cmap, a.H, a.Gw, a.Xw, a.Dw, a.Yw, a.dRw, a.dq, a.dk_, a.dv_,
-        a.dbeta, a.dg, a.ddp);
+        q, k, v, dO, beta, bt, a.d, a.cmap, a.H, a.Gw, a.Xw, a.Dw, a.Yw, a.dRw, a.dq, a.dk_, a.dv_,
+        a.dbeta, a.dbeta_tilde, a.dg, a.ddp);
   a.stage("reduce_dd");
   k_reduce_dd<<<a.H, NTHR, 0, st>>>(a.ddp, a.ncmax, a.H, a.dd);
   a.stage(nullptr);
@@ -2511,6 +2542,7 @@ static hipError_t run_fwd_bf(const LaunchArgs& a) {
   const bf16_t* k = static_cast<const bf16_t*>(a.k);
   const bf16_t* v = static_cast<const bf16_t*>(a.v);
   const bf16_t* beta = static_cast<const bf16_t*>(a.beta);
+  const bf16_t* bt = static_cast<const bf16_t*>(a.beta_tilde);
   // fixed-length rows need no tables (closed form in the kernels)
   const int Tfix = a.cu_seqlens ? -1 : a.Tseq;
   if (Tfix < 0) {
@@ -2521,21 +2553,21 @@ static hipError_t run_fwd_bf(const LaunchArgs& a) {
   if (a.ncmax > 0) {
     if (a.saved)
       k_prep_bf<DK, true><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
-          q, k, a.g, beta, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.MTq, a.MTs, a.ATq, a.ATs,
+          q, k, a.g, bt, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.MTq, a.MTs, a.ATq, a.ATs,
           a.QTp, a.Gw, a.sink);
     else
       k_prep_bf<DK, false><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
-          q, k, a.g, beta, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, nullptr, nullptr, nullptr,
+          q, k, a.g, bt, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, nullptr, nullptr, nullptr,
           nullptr, nullptr, a.Gw, a.sink);
   }
   a.stage(a.saved ? "scan_fwd_save" : "scan_fwd");
   if (a.saved)
     k_scan_fwd_bf<DK, DV, SCAN_BV, true, true><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-        q, k, v, beta, a.d, a.h0, a.smap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, a.o, a.ht, a.Xq, a.Xs,
+        q, k, v, beta, bt, a.d, a.h0, a.smap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, a.o, a.ht, a.Xq, a.Xs,
         a.Dq, a.Ds, a.Xfq, a.Xfs, a.sink);
   else
     k_scan_fwd_bf<DK, DV, SCAN_BV, true, false><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-        q, k, v, beta, a.d, a.h0, a.smap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, a.o, a.ht, nullptr,
+        q, k, v, beta, bt, a.d, a.h0, a.smap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, a.o, a.ht, nullptr,
         nullptr, nullptr, nullptr, nullptr, nullptr, a.sink);
   a.stage(nullptr);
   return hipGetLastError();
@@ -2548,6 +2580,7 @@ static hipError_t run_bwd_bf(const LaunchArgs& a) {
   const bf16_t* k = static_cast<const bf16_t*>(a.k);
   const bf16_t* v = static_cast<const bf16_t*>(a.v);
   const bf16_t* beta = static_cast<const bf16_t*>(a.beta);
+  const bf16_t* bt = static_cast<const bf16_t*>(a.beta_tilde);
   const bf16_t* dO = static_cast<const bf16_t*>(a.dO);
   if (a.N == 0) {
     k_reduce_dd<<<a.H, NTHR, 0, st>>>(a.ddp, 0, a.H, a.dd);
@@ -2563,22 +2596,22 @@ static hipError_t run_bwd_bf(const LaunchArgs& a) {
     a.stage("prep");
     if (a.ncmax > 0)
       k_prep_bf<DK, true><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
-          q, k, a.g, beta, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.MTq, a.MTs, a.ATq, a.ATs,
+          q, k, a.g, bt, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.MTq, a.MTs, a.ATq, a.ATs,
           a.QTp, a.Gw, a.sink);
     a.stage("scan_fwd_store");
     k_scan_fwd_bf<DK, DV, SCAN_BV, false, true><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-        q, k, v, beta, a.d, a.h0, a.smap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, nullptr, nullptr, a.Xq,
+        q, k, v, beta, bt, a.d, a.h0, a.smap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, nullptr, nullptr, a.Xq,
         a.Xs, a.Dq, a.Ds, a.Xfq, a.Xfs, a.sink);
   }
   a.stage("scan_bwd");
   k_scan_bwd_bf<DK, DV, SCAN_BV><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-      q, k, dO, beta, a.d, a.dht, a.smap, Tfix, a.H, a.MTq, a.MTs, a.ATq, a.ATs, a.QTp, a.Gw, a.dh0, a.Yq,
+      q, k, dO, bt, a.d, a.dht, a.smap, Tfix, a.H, a.MTq, a.MTs, a.ATq, a.ATs, a.QTp, a.Gw, a.dh0, a.Yq,
       a.Ys, a.dRq, a.dRs, a.sink);
   a.stage("intra_bwd");
   if (a.ncmax > 0)
     k_intra_bwd_bf<DK, DV><<<dim3(intra_bwd_grid((long)a.ncmax * a.H)), IB_THR, 0, st>>>(
-        q, k, v, dO, beta, a.d, a.cmap, Tfix, a.H, a.Gw, a.Xq, a.Xs, a.Dq, a.Ds, a.Yq, a.Ys, a.dRq, a.dRs,
-        a.ncmax, a.dq, a.dk_, a.dv_, a.dbeta, a.dg, a.ddp, a.sink);
+        q, k, v, dO, beta, bt, a.d, a.cmap, Tfix, a.H, a.Gw, a.Xq, a.Xs, a.Dq, a.Ds, a.Yq, a.Ys, a.dRq,
+        a.dRs, a.ncmax, a.dq, a.dk_, a.dv_, a.dbeta, a.dbeta_tilde, a.dg, a.ddp, a.sink);
   a.stage("reduce_dd");
   k_reduce_dd<<<a.H, NTHR, 0, st>>>(a.ddp, a.ncmax, a.H, a.dd);
   a.stage(nullptr);

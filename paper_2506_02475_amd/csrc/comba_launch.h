@@ -31,10 +31,12 @@ struct LaunchArgs {
   bool saved;
   int dk, dv, H, N, Tseq, Ttot, ncmax;
   const int32_t* cu_seqlens;
-  const void *q, *k, *v, *beta, *dO;
+  // beta_tilde (feedback strength) is never NULL here: it points at beta when
+  // the two are tied; dbeta_tilde NULL means tied (dbeta then holds the sum)
+  const void *q, *k, *v, *beta, *beta_tilde, *dO;
   const float *g, *d, *h0, *dht;
   float *o, *ht;
-  float *dq, *dk_, *dv_, *dg, *dbeta, *dd, *dh0;
+  float *dq, *dk_, *dv_, *dg, *dbeta, *dbeta_tilde, *dd, *dh0;
   // workspace views
   ChunkInfo* cmap;
   SeqInfo* smap;

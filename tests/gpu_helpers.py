@@ -33,7 +33,8 @@ def to_device(w, device="cuda"):
         return torch.from_numpy(np.ascontiguousarray(x)).to(device=device, dtype=dtype or torch.float32)
 
     out = dict(q=t(w.q, dt), k=t(w.k, dt), v=t(w.v, dt), g=t(w.g), beta=t(w.beta, dt), d=t(w.d),
-               h0=t(w.h0), dO=t(w.dO, dt), dht=t(w.dht))
+               h0=t(w.h0), dO=t(w.dO, dt), dht=t(w.dht),
+               beta_tilde=t(w.extra.get("beta_tilde"), dt))
     out["cu_seqlens"] = None if w.cu_seqlens is None else \
         torch.from_numpy(w.cu_seqlens.astype(np.int32)).to(device)
     return out
@@ -45,7 +46,7 @@ def gpu_fwd(w, **kw):
 
     a = to_device(w)
     o, ht = comba.comba_chunk_fwd(a["q"], a["k"], a["v"], a["g"], a["beta"], a["d"], a["h0"],
-                                  cu_seqlens=a["cu_seqlens"], **kw)
+                                  beta_tilde=a["beta_tilde"], cu_seqlens=a["cu_seqlens"], **kw)
     torch.cuda.synchronize()
     return o.cpu().numpy(), (None if ht is None else ht.cpu().numpy())
 
@@ -56,7 +57,8 @@ def gpu_bwd(w, **kw):
 
     a = to_device(w)
     gr = comba.comba_chunk_bwd(a["q"], a["k"], a["v"], a["g"], a["beta"], a["d"], a["h0"],
-                               a["dO"], a["dht"], cu_seqlens=a["cu_seqlens"], **kw)
+                               a["dO"], a["dht"], beta_tilde=a["beta_tilde"],
+                               cu_seqlens=a["cu_seqlens"], **kw)
     torch.cuda.synchronize()
     return {k: (None if v is None else v.cpu().numpy()) for k, v in gr.items()}
 
@@ -79,7 +81,9 @@ def check_bwd(w, heads=None, tol=None):
     ref = oracle.workload_bwd(w, heads=heads)
     sel = slice(None) if heads is None else list(heads)
     errs = {}
-    for name in ("dq", "dk", "dv", "dg", "dbeta"):
+    names = ("dq", "dk", "dv", "dg", "dbeta") + (("dbeta_tilde",) if "dbeta_tilde" in ref else ())
+    assert ("dbeta_tilde" in gr) == ("dbeta_tilde" in ref)
+    for name in names:
         errs[name] = maxrel(gr[name][:, :, sel], ref[name])
     errs["dd"] = maxrel(gr["dd"][sel], ref["dd"])
     errs["dh0"] = maxrel(gr["dh0"][:, sel], ref["dh0"])

@@ -23,20 +23,21 @@ def shape(B=1, T=128, H=2, dk=128, dv=128, chunk=64, N=None, cu=None, dtype=comb
 
 def fwd(shp, ptrs=None, ws_bytes=1 << 40, **over):
     lib = comba.load_library()
-    p = dict(q=FAKE, k=FAKE, v=FAKE, g=FAKE, beta=FAKE, d=FAKE, h0=None, o=FAKE, ht=None, ws=FAKE)
+    p = dict(q=FAKE, k=FAKE, v=FAKE, g=FAKE, beta=FAKE, beta_tilde=None, d=FAKE, h0=None, o=FAKE,
+             ht=None, ws=FAKE)
     p.update(over)
     P = ctypes.c_void_p
     return lib.comba_chunk_fwd(ctypes.byref(shp), P(p["q"]), P(p["k"]), P(p["v"]), P(p["g"]),
-                               P(p["beta"]), P(p["d"]), P(p["h0"]), P(p["o"]), P(p["ht"]),
-                               P(p["ws"]), ctypes.c_size_t(ws_bytes), None)
+                               P(p["beta"]), P(p["beta_tilde"]), P(p["d"]), P(p["h0"]),
+                               P(p["o"]), P(p["ht"]), P(p["ws"]), ctypes.c_size_t(ws_bytes), None)
 
 
 def bwd(shp, ws_bytes=1 << 40, **over):
     lib = comba.load_library()
-    names = ["q", "k", "v", "g", "beta", "d", "h0", "dO", "dht", "dq", "dk", "dv", "dg",
-             "dbeta", "dd", "dh0", "ws"]
+    names = ["q", "k", "v", "g", "beta", "beta_tilde", "d", "h0", "dO", "dht", "dq", "dk", "dv",
+             "dg", "dbeta", "dbeta_tilde", "dd", "dh0", "ws"]
     p = {n: FAKE for n in names}
-    p.update(h0=None, dht=None, dh0=None)
+    p.update(beta_tilde=None, dbeta_tilde=None, h0=None, dht=None, dh0=None)
     p.update(over)
     P = ctypes.c_void_p
     args = [P(p[n]) for n in names]
@@ -123,8 +124,29 @@ def test_rejects_null_and_misaligned_pointers():
     for name in ("dg", "dbeta", "dd"):
         assert bwd(s, ws_bytes=1, **{name: FAKE + 4}) == EWS, name
     lib = comba.load_library()
-    assert lib.comba_chunk_fwd(None, *[ctypes.c_void_p(FAKE)] * 9, ctypes.c_void_p(FAKE),
+    assert lib.comba_chunk_fwd(None, *[ctypes.c_void_p(FAKE)] * 10, ctypes.c_void_p(FAKE),
                                ctypes.c_size_t(1 << 40), None) == ENULL
+
+
+def test_beta_tilde_arguments():
+    # beta_tilde is optional (NULL: tied to beta); when it is given, its
+    # gradient dbeta_tilde is required.  dbeta_tilde alone is allowed (the
+    # derivative split by role).  A one-byte workspace stops every call that
+    # passes validation before any launch.
+    s = shape()
+    assert fwd(s, ws_bytes=1, beta_tilde=FAKE) == EWS
+    assert bwd(s, ws_bytes=1, beta_tilde=FAKE, dbeta_tilde=FAKE) == EWS
+    assert bwd(s, ws_bytes=1, dbeta_tilde=FAKE) == EWS
+    assert bwd(s, ws_bytes=1, beta_tilde=FAKE) == ENULL
+    # element alignment: bf16 beta_tilde 2 bytes, fp32 dbeta_tilde 4 bytes
+    assert fwd(s, ws_bytes=1, beta_tilde=FAKE + 1) == EALIGN
+    assert fwd(s, ws_bytes=1, beta_tilde=FAKE + 2) == EWS
+    assert fwd(shape(dk=64, dv=64, dtype=comba.COMBA_F32), ws_bytes=1,
+               beta_tilde=FAKE + 2) == EALIGN
+    assert bwd(s, ws_bytes=1, beta_tilde=FAKE, dbeta_tilde=FAKE + 2) == EALIGN
+    assert bwd(s, ws_bytes=1, beta_tilde=FAKE, dbeta_tilde=FAKE + 4) == EWS
+    # without tokens both may be NULL
+    assert bwd(shape(T=0), ws_bytes=1, beta_tilde=FAKE) == EWS
 
 
 def test_token_free_calls_accept_null_token_tensors():
@@ -148,7 +170,7 @@ def test_saved_pair_validates_like_the_plain_calls():
     lib = comba.load_library()
     P = ctypes.c_void_p
     s = shape(chunk=32)
-    args = [P(FAKE)] * 9
+    args = [P(FAKE)] * 10
     assert lib.comba_chunk_fwd_save(ctypes.byref(s), *args, P(FAKE), ctypes.c_size_t(1 << 40),
                                     None) == ESHAPE
     s = shape()
@@ -158,10 +180,10 @@ def test_saved_pair_validates_like_the_plain_calls():
     assert need_b > need_f
     assert lib.comba_chunk_fwd_save(ctypes.byref(s), *args, P(FAKE), ctypes.c_size_t(need_f),
                                     None) == EWS
-    bargs = [P(FAKE)] * 16
+    bargs = [P(FAKE)] * 18
     assert lib.comba_chunk_bwd_saved(ctypes.byref(s), *bargs, P(FAKE),
                                      ctypes.c_size_t(need_b - 1), None) == EWS
-    bargs[7] = None  # dO
+    bargs[8] = None  # dO
     assert lib.comba_chunk_bwd_saved(ctypes.byref(s), *bargs, P(FAKE),
                                      ctypes.c_size_t(need_b), None) == ENULL
 

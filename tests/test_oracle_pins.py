@@ -344,3 +344,28 @@ def test_backward_segment_chaining():
         assert rel(np.concatenate([g1[key], g2[key]], axis=1), full[key]) < 1e-12
     assert rel(g1["dd"] + g2["dd"], full["dd"]) < 1e-12
     assert rel(g1["dh0"], full["dh0"]) < 1e-12
+
+
+def test_iplr_reflections_preserve_the_state_norm():
+    # Comba-iplr's transition alpha (I - 2 c k k^T) in SPLR form has beta~ =
+    # 2 alpha c.  With alpha = 1, c = 1, beta = 0 and |k| = 1 every transition
+    # is a Householder reflection (orthogonal, its own inverse): the state's
+    # Frobenius norm never changes, and a key repeated twice gives the state back.
+    w = random_case(B=1, T=24, H=2, dk=8, dv=5, seed=41, h0=True)
+    k = w.k.astype(np.float64)
+    k /= np.linalg.norm(k, axis=-1, keepdims=True)
+    g = np.zeros_like(w.g)
+    zero = np.zeros_like(w.beta)
+    two = np.full_like(w.beta, 2.0)
+    _, ht = oracle.step_fwd(w.q, k, w.v, g, zero, w.d, w.h0, beta_tilde=two)
+    h0 = w.h0.astype(np.float64)
+    for h in range(2):
+        assert abs(np.linalg.norm(ht[0, h]) / np.linalg.norm(h0[0, h]) - 1.0) < 1e-13
+    assert rel(ht, h0) > 0.1  # the reflections did act on the state
+    kk = k.copy()
+    kk[:, 1::2] = kk[:, 0::2]  # every key twice in a row
+    _, ht2 = oracle.step_fwd(w.q, kk, w.v, g, zero, w.d, w.h0, beta_tilde=two)
+    assert rel(ht2, w.h0) < 1e-13
+    # and the chunk form agrees across chunk boundaries
+    _, htc = chunk_fwd(w.q, kk, w.v, g, zero, w.d, w.h0, chunk=8, beta_tilde=two)
+    assert rel(htc, w.h0) < 1e-12
