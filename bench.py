@@ -13,11 +13,14 @@ outputs, seeded synthetic inputs (comba_inputs, PCG64).
 Prints one JSON line with the whole-job throughput in tokens/s, the roofline of
 the dominant kernel (timed live with HIP events on the library's stream over
 the timed region) and the fp64 CPU oracle timed on this host's cores on a
-bounded sample of the same workload.
+bounded sample of the same workload.  The training pair with a separate
+state-feedback strength beta~ = b * beta (Section 3.2, one b per head) is timed
+after the headline region and reported under "variants".
 """
 from __future__ import annotations
 
 import argparse
+import copy
 import hashlib
 import json
 import math
@@ -35,7 +38,7 @@ RIDGE = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)   # flop / byte
 WORKLOAD_INDEX = 3             # l1p3b_fwdbwd
 
 
-def stage_model(name, B, T, H, dk, dv, C=64, in_bytes=2):
+def stage_model(name, B, T, H, dk, dv, C=64, in_bytes=2, sep_bt=False):
     """Algorithmic (flops, bytes) of one launch of a kernel stage.
 
     Per chunk-head (C tokens of one head): the dense products the stage performs
@@ -46,6 +49,9 @@ def stage_model(name, B, T, H, dk, dv, C=64, in_bytes=2):
     backward gradient kernel 2 bytes per element plus one 4-byte scale per 32
     elements (their int16 storage); the Q^T copy made by the prep stage is
     counted where it is written and read (K^T is formed on chip from K).
+    ``sep_bt``: a separate feedback strength beta~ (read where beta and beta~
+    both act: the forward scan and the gradient kernel, which also writes
+    dbeta~; the prep and reverse scan read beta~ in place of beta).
     """
     nch = B * math.ceil(T / C) * H
     f4 = 4
@@ -65,6 +71,8 @@ def stage_model(name, B, T, H, dk, dv, C=64, in_bytes=2):
         by = 2 * qk + vv + 2 * cc + gb + C * dv * f4   # q, k, v, M, A, g, beta -> o (fp32)
         if name == "scan_fwd_save":       # + chunk states X and D for the backward
             by += st + cd
+        if sep_bt:
+            by += C * in_bytes
     elif name == "scan_fwd_store":  # K X, M R, K^T D; -> X, D
         fl = 4 * C * dk * dv + 2 * C * C * dv
         by = qk + vv + cc + gb + st + cd
@@ -75,6 +83,8 @@ def stage_model(name, B, T, H, dk, dv, C=64, in_bytes=2):
         fl = 6 * C * dk * dv + 4 * C * C * dv + 10 * C * C * dk
         by = (2 * qk + 2 * vv + 2 * st + 2 * cd + gb          # q,k,v,dO,X,Y,D,dR
               + C * (2 * dk + dv) * f4 + 2 * C * f4)           # dq, dk, dv, dg, dbeta
+        if sep_bt:
+            by += C * (in_bytes + f4)                           # beta~ in, dbeta~ out
     else:
         return 0.0, 0.0
     return float(fl * nch), float(by * nch)
@@ -137,6 +147,11 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--skip-stateless", action="store_true",
                     help="time only the training pair (profiling runs: one stage per kernel)")
+    ap.add_argument("--no-variants", action="store_true",
+                    help="skip the timed variant legs (separate feedback strength beta~)")
+    ap.add_argument("--beta-tilde", action="store_true",
+                    help="time the workload with beta~ = b * beta as the headline (profiling "
+                         "runs of that variant; implies --no-variants)")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="after the timed steps, run one plain device-to-device copy of this "
                          "many bytes (calibrates HBM traffic counters against a known size)")
@@ -152,7 +167,7 @@ def main():
     import torch
 
     import paper_2506_02475_amd as comba
-    from comba_inputs import WORKLOADS, generate
+    from comba_inputs import WORKLOADS, attach_beta_tilde, generate
 
     spec = WORKLOADS[WORKLOAD_INDEX]
     w = generate(WORKLOAD_INDEX)
@@ -169,16 +184,25 @@ def main():
     B, T, H, dk, dv = w.B, w.T, w.H, w.dk, w.dv
     ws_f = torch.empty(comba.fwd_workspace_bytes(B, T, H, dk, dv), dtype=torch.uint8, device=dev)
     ws_b = torch.empty(comba.bwd_workspace_bytes(B, T, H, dk, dv), dtype=torch.uint8, device=dev)
+    # the paper's separate feedback strength beta~ = b * beta (one b per head)
+    w_bt = copy.copy(w)
+    w_bt.extra = {}
+    attach_beta_tilde(w_bt, "b_beta", seed=31)
+    bt_var = t(w_bt.extra["beta_tilde"], bf)
+    bt_main = bt_var if args.beta_tilde else None
 
-    def step():
+    def step(bt=bt_main):
         # training pair: the forward leaves the backward's state in ws_b
-        o, ht, _ = comba.comba_chunk_fwd_save(q, k, v, g, beta, d, h0, workspace=ws_b)
-        gr = comba.comba_chunk_bwd_saved(q, k, v, g, beta, d, h0, dO, None, workspace=ws_b)
+        o, ht, _ = comba.comba_chunk_fwd_save(q, k, v, g, beta, d, h0, beta_tilde=bt,
+                                              workspace=ws_b)
+        gr = comba.comba_chunk_bwd_saved(q, k, v, g, beta, d, h0, dO, None, beta_tilde=bt,
+                                         workspace=ws_b)
         return o, gr
 
     def step_stateless():
-        o, ht = comba.comba_chunk_fwd(q, k, v, g, beta, d, h0, workspace=ws_f)
-        gr = comba.comba_chunk_bwd(q, k, v, g, beta, d, h0, dO, None, workspace=ws_b)
+        o, ht = comba.comba_chunk_fwd(q, k, v, g, beta, d, h0, beta_tilde=bt_main, workspace=ws_f)
+        gr = comba.comba_chunk_bwd(q, k, v, g, beta, d, h0, dO, None, beta_tilde=bt_main,
+                                   workspace=ws_b)
         return o, gr
 
     ms_stateless = None
@@ -219,10 +243,11 @@ def main():
     avg = {n: s[0] / s[1] for n, s in agg.items()}
     tot = {n: s[0] / args.steps for n, s in agg.items()}
     dom = max(tot, key=tot.get)
-    fl, by = stage_model(dom, B, T, H, dk, dv)
+    fl, by = stage_model(dom, B, T, H, dk, dv, sep_bt=args.beta_tilde)
     sec = avg[dom] * 1e-3
     intensity = fl / by if by else 0.0
-    traffic = measured_traffic(dom)
+    # the committed counters cover the headline workload only
+    traffic = None if args.beta_tilde else measured_traffic(dom)
     if intensity < RIDGE:
         achieved = by / sec / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
@@ -252,8 +277,10 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded PCG64; q,k L2-normalised, log alpha=-softplus(N(0,1)), "
-                "beta=sigmoid(N(0,1)), d~U(0,1))",
-        "config": {"workload": spec.name, "B": B, "T": T, "H": H, "dk": dk, "dv": dv,
+                "beta=sigmoid(N(0,1)), d~U(0,1)%s)" % (
+                    "; beta~=b*beta, b=sigmoid(N(0,1)) per head" if args.beta_tilde else ""),
+        "config": {"workload": spec.name + ("_beta_tilde" if args.beta_tilde else ""),
+                   "B": B, "T": T, "H": H, "dk": dk, "dv": dv,
                    "chunk": 64, "in_dtype": "bf16", "out_dtype": "f32"},
         "step": "comba_chunk_fwd_save + comba_chunk_bwd_saved",
         "ms_per_step_stateless": ms_stateless,
@@ -262,6 +289,26 @@ def main():
         "stages_ms": {n: round(x, 4) for n, x in tot.items()},
         "roofline": roof,
     }
+    if not (args.no_variants or args.beta_tilde):
+        # the same training pair with beta~ = b * beta, timed after the headline region
+        for _ in range(args.warmup):
+            step(bt_var)
+        torch.cuda.synchronize()
+        comba.profile_enable(True)
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            step(bt_var)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        st_bt = comba.profile_read()
+        comba.profile_enable(False)
+        agg_bt = {}
+        for name, ms in st_bt:
+            agg_bt[name] = agg_bt.get(name, 0.0) + ms / args.steps
+        result["variants"] = {"beta_tilde_b_beta": {
+            "value": round(tokens / ((t1 - t0) / args.steps), 1), "unit": "tokens/s",
+            "ms_per_step": round((t1 - t0) * 1e3 / args.steps, 4),
+            "stages_ms": {n: round(x, 4) for n, x in agg_bt.items()}}}
     if args.copy_bytes > 0:
         n = args.copy_bytes // 4
         src = torch.ones(n, dtype=torch.float32, device=dev)
@@ -277,7 +324,7 @@ def main():
             threads = os.cpu_count() or 1
         nh = min(H, max(1, math.ceil(2 * threads / B)))
         heads = list(range(0, H, max(1, H // nh)))[:nh]
-        result["cpu_baseline"] = cpu_baseline(w, heads, threads)
+        result["cpu_baseline"] = cpu_baseline(w_bt if args.beta_tilde else w, heads, threads)
     else:
         result["cpu_baseline"] = None
     print(json.dumps(result), flush=True)
