@@ -125,6 +125,84 @@ def measured_traffic(kernel):
     return round(float(k["bytes_per_launch"]))
 
 
+DECODE = dict(B=64, H=16, dk=128, dv=128, layers=8, seed=47)
+
+
+def decode_bytes(B, H, dk, dv, in_bytes=2):
+    """Algorithmic HBM bytes of one decoding call (T = 1, states updated in place):
+    every state read and written once (fp32), q, k, v, g, beta read, o written."""
+    per_head = 2 * dk * dv * 4 + (2 * dk + dv) * in_bytes + 4 + in_bytes + dv * 4
+    return float(B * H * per_head)
+
+
+def time_decode(comba, torch, steps, warmup, threads=None, with_cpu=False):
+    """Decoding step of one layer: one token for each of B sequences through
+    comba_recurrent_fwd, states updated in place.  The timed loop cycles over
+    the states of DECODE['layers'] layers (512 MiB at the default shape, more
+    than the 256 MB on-die cache), as a model's layers would."""
+    import numpy as np
+    import oracle
+    from comba_inputs import random_case
+
+    c = DECODE
+    w = random_case(seed=c["seed"], B=c["B"], T=1, H=c["H"], dk=c["dk"], dv=c["dv"],
+                    in_dtype="bf16", grad=False)
+    dev = torch.device("cuda:0")
+    bf = torch.bfloat16
+
+    def t(x, dt=torch.float32):
+        return torch.from_numpy(np.ascontiguousarray(x)).to(dev, dt)
+
+    q, k, v, g, beta, d = t(w.q, bf), t(w.k, bf), t(w.v, bf), t(w.g), t(w.beta, bf), t(w.d)
+    h0 = t(w.h0)
+    states = [h0.clone() for _ in range(c["layers"])]
+
+    def call(st):
+        return comba.comba_recurrent_fwd(q, k, v, g, beta, d, st, ht=st)
+
+    for _ in range(warmup):
+        for st in states:
+            call(st)
+    torch.cuda.synchronize()
+    comba.profile_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        for st in states:
+            call(st)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    marks = comba.profile_read()
+    comba.profile_enable(False)
+    ncalls = steps * len(states)
+    ms_call = (t1 - t0) * 1e3 / ncalls
+    kern = [ms for name, ms in marks if name == "recurrent"]
+    kms = sum(kern) / len(kern)
+    by = decode_bytes(c["B"], c["H"], c["dk"], c["dv"])
+    achieved = by / (kms * 1e-3) / 1e9
+    res = {"value": round(c["B"] / (ms_call * 1e-3), 1), "unit": "tokens/s (one layer)",
+           "ms_per_call": round(ms_call, 5), "config": {k_: c[k_] for k_ in ("B", "H", "dk", "dv",
+                                                                             "layers")},
+           "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                        "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
+                        "traffic": None, "kernel": "recurrent", "avg_launch_ms": round(kms, 5),
+                        "algorithmic_bytes": by}}
+    if with_cpu:
+        reps = 0
+        t0 = time.perf_counter()
+        while True:
+            oracle.workload_fwd(w, nthreads=threads)
+            reps += 1
+            if time.perf_counter() - t0 > 2.0:
+                break
+        dt = (time.perf_counter() - t0) / reps
+        res["cpu_baseline"] = {"value": c["B"] / dt, "unit": "tokens/s (one layer)",
+                               "cores": threads, "kind": "oracle",
+                               "sample": "fp64 step recurrence on the whole decoding call "
+                                         "(%d sequences x %d heads, T = 1), %d repetitions"
+                                         % (c["B"], c["H"], reps)}
+    return res
+
+
 def cpu_baseline(w, heads_sample, threads):
     import oracle
 
@@ -152,6 +230,9 @@ def main():
     ap.add_argument("--beta-tilde", action="store_true",
                     help="time the workload with beta~ = b * beta as the headline (profiling "
                          "runs of that variant; implies --no-variants)")
+    ap.add_argument("--decode", action="store_true",
+                    help="time the decoding step (comba_recurrent_fwd, T = 1, B = 64, H = 16, "
+                         "d = 128, in place) as the headline instead of the training pair")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="after the timed steps, run one plain device-to-device copy of this "
                          "many bytes (calibrates HBM traffic counters against a known size)")
@@ -168,6 +249,29 @@ def main():
 
     import paper_2506_02475_amd as comba
     from comba_inputs import WORKLOADS, attach_beta_tilde, generate
+
+    try:
+        threads = len(os.sched_getaffinity(0))
+    except Exception:
+        threads = os.cpu_count() or 1
+    if args.decode:
+        torch.cuda.set_device(0)
+        r = time_decode(comba, torch, args.steps, args.warmup, threads,
+                        with_cpu=not args.no_cpu_baseline)
+        c = DECODE
+        result = {
+            "metric": "Comba decoding tokens/s per layer (T=1, states in place) at B=64,H=16,d=128 "
+                      "bf16",
+            "value": r["value"], "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": round(r["ms_per_call"] * c["layers"], 4),
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+            "data": "synthetic (seeded PCG64, comba_inputs.random_case)",
+            "config": {"workload": "decode_b64_h16_d128", **r["config"]},
+            "step": "comba_recurrent_fwd on each of %d layers' states" % c["layers"],
+            "ms_per_call": r["ms_per_call"], "roofline": r["roofline"],
+            "cpu_baseline": r.get("cpu_baseline")}
+        print(json.dumps(result), flush=True)
+        return
 
     spec = WORKLOADS[WORKLOAD_INDEX]
     w = generate(WORKLOAD_INDEX)
@@ -309,6 +413,8 @@ def main():
             "value": round(tokens / ((t1 - t0) / args.steps), 1), "unit": "tokens/s",
             "ms_per_step": round((t1 - t0) * 1e3 / args.steps, 4),
             "stages_ms": {n: round(x, 4) for n, x in agg_bt.items()}}}
+        result["variants"]["decode_b64_h16_d128"] = time_decode(comba, torch, args.steps,
+                                                                args.warmup)
     if args.copy_bytes > 0:
         n = args.copy_bytes // 4
         src = torch.ones(n, dtype=torch.float32, device=dev)
@@ -318,10 +424,6 @@ def main():
         torch.cuda.synchronize()
         result["copy_bytes"] = n * 4
     if not args.no_cpu_baseline:
-        try:
-            threads = len(os.sched_getaffinity(0))
-        except Exception:
-            threads = os.cpu_count() or 1
         nh = min(H, max(1, math.ceil(2 * threads / B)))
         heads = list(range(0, H, max(1, H // nh)))[:nh]
         result["cpu_baseline"] = cpu_baseline(w_bt if args.beta_tilde else w, heads, threads)

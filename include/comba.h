@@ -48,7 +48,8 @@
     or dv (h0, ht, o, dht, dh0, dq, dk, dv) need 16 bytes, the workspace 256
     bytes, the other fp32 tensors 4 bytes and beta, beta_tilde their element size; any other
     pointer is rejected with COMBA_ERR_ALIGN.
-  - Outputs must not alias inputs; outputs are overwritten, never accumulated.
+  - Outputs must not alias inputs (the one exception: ht == h0 in comba_recurrent_fwd);
+    outputs are overwritten, never accumulated.
   - A call without tokens (T == 0 or B == 0) is valid: the per-token tensors
     (q, k, v, g, beta, o, dO, dq, dk, dv, dg, dbeta, dbeta_tilde) may then be NULL, and the
     states pass through (ht = h0, dh0 = dht, dd = 0).  Empty sequences inside a
@@ -149,6 +150,26 @@ comba_status comba_chunk_bwd_saved(const comba_shape *shape, const void *q, cons
                                    float *dv, float *dg, float *dbeta, float *dbeta_tilde,
                                    float *dd, float *dh0, void *ws, size_t ws_bytes,
                                    void *stream);
+
+/*
+ * Token-by-token recurrence (Eq. comba-S evaluated one token at a time: the
+ * constant-memory inference form of Section 3), for decoding and short
+ * segments.  Per sequence, head and token, with H = S^T:
+ *     u_t = beta_t v_t - beta~_t H_{t-1}^T k_t,  H_t = alpha_t H_{t-1} + k_t u_t^T,
+ *     o_t = H_t^T (q_t - d k_t).
+ * Arguments and layouts are those of comba_chunk_fwd (same shape struct; its
+ * `chunk` field is not used, and fp32 inputs also allow dk, dv = 128), without
+ * a workspace: the call needs no device memory of its own.  h0 may be NULL
+ * (zero states) and ht NULL (states not returned); ht may be the same buffer
+ * as h0, which updates the states in place (the usual decoding step, T = 1);
+ * any other overlap of ht with an input is undefined.  The work per token is a
+ * dependent chain, so long sequences belong to comba_chunk_fwd; results agree
+ * with it to rounding.
+ */
+comba_status comba_recurrent_fwd(const comba_shape *shape, const void *q, const void *k,
+                                 const void *v, const float *g, const void *beta,
+                                 const void *beta_tilde, const float *d, const float *h0,
+                                 float *o, float *ht, void *stream);
 
 /*
  * Stage timing, for benchmarks (not part of the method).  comba_profile_enable(1)

@@ -27,7 +27,7 @@ import re
 import threading
 
 __all__ = ["comba_chunk_fwd", "comba_chunk_bwd", "comba_chunk_fwd_save", "comba_chunk_bwd_saved",
-           "load_library", "library_path",
+           "comba_recurrent_fwd", "load_library", "library_path",
            "profile_enable", "profile_read",
            "fwd_workspace_bytes", "bwd_workspace_bytes", "exported_symbols", "CombaError",
            "CombaShape", "COMBA_F32", "COMBA_BF16", "CHUNK"]
@@ -81,6 +81,8 @@ def load_library():
             lib.comba_chunk_fwd_save.restype = I
             lib.comba_chunk_bwd_saved.argtypes = [SP] + [P] * 18 + [P, Z, P]
             lib.comba_chunk_bwd_saved.restype = I
+            lib.comba_recurrent_fwd.argtypes = [SP] + [P] * 10 + [P]
+            lib.comba_recurrent_fwd.restype = I
             lib.comba_profile_enable.argtypes = [I]
             lib.comba_profile_enable.restype = I
             lib.comba_profile_read.argtypes = [P, P, I]
@@ -231,6 +233,32 @@ def comba_chunk_fwd_save(q, k, v, g, beta, d, h0=None, *, beta_tilde=None, cu_se
     comba_chunk_bwd_saved."""
     return _fwd(True, q, k, v, g, beta, d, h0, cu_seqlens, output_final_state, workspace,
                 stream, beta_tilde)
+
+
+def comba_recurrent_fwd(q, k, v, g, beta, d, h0=None, *, beta_tilde=None, cu_seqlens=None,
+                        output_final_state=True, ht=None, stream=None):
+    """Token-by-token recurrence (decoding; short segments).  Returns (o, ht).
+
+    Same tensors as comba_chunk_fwd (fp32 inputs also allow d = 128) and no
+    workspace.  ``ht`` may be passed as the output state buffer; passing the
+    ``h0`` tensor itself updates the states in place."""
+    import torch
+
+    lib = load_library()
+    shp, (B, T, H, dk, dv, N) = _prepare(q, k, v, g, beta, d, h0, cu_seqlens,
+                                         extra=_beta_tilde(beta_tilde, beta))
+    o = torch.empty((B, T, H, dv), dtype=torch.float32, device=q.device)
+    if ht is not None:
+        if ht.dtype != torch.float32 or tuple(ht.shape) != (N, H, dk, dv) \
+                or not ht.is_contiguous() or ht.device != q.device:
+            raise CombaError("comba: ht must be contiguous float32 [N,H,dk,dv] on the device")
+    elif output_final_state:
+        ht = torch.empty((N, H, dk, dv), dtype=torch.float32, device=q.device)
+    st = torch.cuda.current_stream(q.device).cuda_stream if stream is None else stream
+    _check(lib.comba_recurrent_fwd(ctypes.byref(shp), _ptr(q), _ptr(k), _ptr(v), _ptr(g),
+                                   _ptr(beta), _ptr(beta_tilde), _ptr(d), _ptr(h0), _ptr(o),
+                                   _ptr(ht), ctypes.c_void_p(st)))
+    return o, ht
 
 
 def _bwd(saved, q, k, v, g, beta, d, h0, dO, dht, cu_seqlens, need_dh0, workspace, stream,

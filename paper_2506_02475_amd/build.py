@@ -9,7 +9,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libcomba.so")
-SOURCES = [os.path.join(CSRC, "comba_kernels.hip"), os.path.join(CSRC, "comba_api.cpp")]
+SOURCES = [os.path.join(CSRC, "comba_kernels.hip"), os.path.join(CSRC, "comba_recurrent.hip"),
+           os.path.join(CSRC, "comba_api.cpp")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

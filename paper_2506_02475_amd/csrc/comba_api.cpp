@@ -58,6 +58,19 @@ comba_status check_shape(const comba_shape* s, Dims* out) {
   return COMBA_OK;
 }
 
+// Shape rules of the token-by-token entry point: those of check_shape, except
+// that the chunk length is not used and fp32 inputs allow d = 128 as well.
+comba_status check_shape_recurrent(const comba_shape* s, Dims* out) {
+  if (!s) return COMBA_ERR_NULL;
+  comba_shape c = *s;
+  c.chunk = kChunk;
+  const bool f32 = c.in_dtype == COMBA_F32;
+  if (f32) c.in_dtype = COMBA_BF16;  // the head-size rule of the bf16 path
+  const comba_status st = check_shape(&c, out);
+  if (st == COMBA_OK) out->bf16 = !f32;
+  return st;
+}
+
 struct Layout {
   size_t cmap, smap, M, A, G, X, D, Y, dR, ddp, MT, AT, QT, Xfin, sink, total;
   size_t Xs, Ds, Ys, dRs, Xfs;  // bf16 path: scales of the int16 X, D, Y, dR, final-state sink
@@ -149,7 +162,8 @@ void prof_mark(void* ctx, hipStream_t st, const char* name) {
   ++p->n;
 }
 
-void attach_profile(comba::LaunchArgs& a) {
+template <typename Args>
+void attach_profile(Args& a) {
   // a call records at most kMaxMarksPerCall marks; stop at the pool limit so
   // that no call is recorded partially
   if (!g_prof.on || g_prof.n + kMaxMarksPerCall > kMaxEvents) return;
@@ -300,6 +314,43 @@ comba_status chunk_bwd(bool saved, const comba_shape* shape, const void* q, cons
   return comba::launch_bwd(a) == hipSuccess ? COMBA_OK : COMBA_ERR_HIP;
 }
 
+comba_status recurrent_fwd(const comba_shape* shape, const void* q, const void* k, const void* v,
+                           const float* g, const void* beta, const void* beta_tilde,
+                           const float* d, const float* h0, float* o, float* ht, void* stream) {
+  Dims dm;
+  comba_status st = check_shape_recurrent(shape, &dm);
+  if (st != COMBA_OK) return st;
+  const bool tok = dm.Ttot > 0;
+  if ((tok && (!q || !k || !v || !g || !beta || !o)) || !d) return COMBA_ERR_NULL;
+  const size_t eb = dm.bf16 ? 2 : 4;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(g, 4) ||
+      !aligned(d, 4) || !aligned(o, 16) || (h0 && !aligned(h0, 16)) || (ht && !aligned(ht, 16)) ||
+      !aligned(beta, eb) || !aligned(beta_tilde, eb))
+    return COMBA_ERR_ALIGN;
+  comba::RecurrentArgs a{};
+  a.bf16 = dm.bf16;
+  a.dk = dm.dk;
+  a.dv = dm.dv;
+  a.H = dm.H;
+  a.N = dm.N;
+  a.Tseq = dm.Tseq;
+  a.Ttot = dm.Ttot;
+  a.cu_seqlens = shape->cu_seqlens;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.beta = beta;
+  a.beta_tilde = beta_tilde ? beta_tilde : beta;  // NULL: tied to beta
+  a.g = g;
+  a.d = d;
+  a.h0 = h0;
+  a.o = o;
+  a.ht = ht;
+  a.stream = static_cast<hipStream_t>(stream);
+  attach_profile(a);
+  return comba::launch_recurrent(a) == hipSuccess ? COMBA_OK : COMBA_ERR_HIP;
+}
+
 }  // namespace
 
 extern "C" {
@@ -370,6 +421,13 @@ comba_status comba_chunk_bwd_saved(const comba_shape* shape, const void* q, cons
                                    void* stream) {
   return chunk_bwd(true, shape, q, k, v, g, beta, beta_tilde, d, h0, dO, dht, dq, dk, dv, dg,
                    dbeta, dbeta_tilde, dd, dh0, ws, ws_bytes, stream);
+}
+
+comba_status comba_recurrent_fwd(const comba_shape* shape, const void* q, const void* k,
+                                 const void* v, const float* g, const void* beta,
+                                 const void* beta_tilde, const float* d, const float* h0, float* o,
+                                 float* ht, void* stream) {
+  return recurrent_fwd(shape, q, k, v, g, beta, beta_tilde, d, h0, o, ht, stream);
 }
 
 const char* comba_status_string(comba_status s) {

@@ -68,4 +68,21 @@ struct LaunchArgs {
 hipError_t launch_fwd(const LaunchArgs& a);
 hipError_t launch_bwd(const LaunchArgs& a);
 
+// Token-by-token recurrence (comba_recurrent_fwd): no workspace.
+struct RecurrentArgs {
+  bool bf16;
+  int dk, dv, H, N, Tseq, Ttot;
+  const int32_t* cu_seqlens;
+  const void *q, *k, *v, *beta, *beta_tilde;  // beta_tilde never NULL (beta when tied)
+  const float *g, *d, *h0;
+  float *o, *ht;  // ht may equal h0
+  hipStream_t stream;
+  StageHook hook;
+  void stage(const char* name) const {
+    if (hook.mark) hook.mark(hook.ctx, stream, name);
+  }
+};
+
+hipError_t launch_recurrent(const RecurrentArgs& a);
+
 }  // namespace comba

@@ -50,7 +50,8 @@ def test_library_exports_every_declared_symbol():
     assert set(declared) == {"comba_fwd_workspace_bytes", "comba_bwd_workspace_bytes",
                              "comba_chunk_fwd", "comba_chunk_bwd", "comba_status_string",
                              "comba_profile_enable", "comba_profile_read",
-                             "comba_chunk_fwd_save", "comba_chunk_bwd_saved"}
+                             "comba_chunk_fwd_save", "comba_chunk_bwd_saved",
+                             "comba_recurrent_fwd"}
     out = subprocess.run(["nm", "-D", "--defined-only", comba.library_path()],
                          capture_output=True, text=True, check=True).stdout
     exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
@@ -164,6 +165,37 @@ def test_token_free_calls_accept_null_token_tensors():
     # with tokens they are required as before
     assert fwd(shape(T=1), ws_bytes=1, q=None) == ENULL
     assert bwd(shape(T=1), ws_bytes=1, dbeta=None) == ENULL
+
+
+def rec(shp, **over):
+    lib = comba.load_library()
+    p = dict(q=FAKE, k=FAKE, v=FAKE, g=FAKE, beta=FAKE, beta_tilde=None, d=FAKE, h0=None, o=FAKE,
+             ht=None)
+    p.update(over)
+    P = ctypes.c_void_p
+    names = ("q", "k", "v", "g", "beta", "beta_tilde", "d", "h0", "o", "ht")
+    return lib.comba_recurrent_fwd(ctypes.byref(shp), *[P(p[n]) for n in names], None)
+
+
+def test_recurrent_validates_before_launch():
+    # every call below stops at a check (a misaligned o or ht marks the ones
+    # whose shape passed), so nothing is launched
+    assert rec(shape(dk=96)) == ESHAPE
+    assert rec(shape(dv=256)) == ESHAPE
+    assert rec(shape(B=2, N=3)) == ESHAPE
+    assert rec(shape(dtype=7)) == EDTYPE
+    # the chunk length is not used; fp32 inputs allow d = 128 here
+    assert rec(shape(chunk=32), o=FAKE + 4) == EALIGN
+    assert rec(shape(dk=128, dv=128, dtype=comba.COMBA_F32), o=FAKE + 4) == EALIGN
+    for name in ("q", "k", "v", "g", "beta", "d", "o"):
+        assert rec(shape(), **{name: None}) == ENULL, name
+    assert rec(shape(), beta_tilde=FAKE + 1) == EALIGN
+    assert rec(shape(), h0=FAKE + 8) == EALIGN
+    assert rec(shape(), ht=FAKE + 8) == EALIGN
+    # without tokens the token tensors may be NULL (d stays required)
+    none = {n: None for n in ("q", "k", "v", "g", "beta", "o")}
+    assert rec(shape(T=0), ht=FAKE + 8, **none) == EALIGN
+    assert rec(shape(T=0), d=None, **none) == ENULL
 
 
 def test_saved_pair_validates_like_the_plain_calls():
