@@ -98,26 +98,30 @@ def op_flops(B, T, H, dk, dv, C=64):
     return float((fwd + bwd) * nch)
 
 
-def kernel_source_sha():
+def kernel_source_sha(files=("comba_kernels.hip", "comba_device.hpp")):
     h = hashlib.sha256()
-    for f in ("comba_kernels.hip", "comba_device.hpp"):
+    for f in files:
         with open(os.path.join(ROOT, "paper_2506_02475_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def measured_traffic(kernel):
+DECODE_SOURCES = ("comba_recurrent.hip", "comba_device.hpp")
+
+
+def measured_traffic(kernel, summary="traffic_counters_l1p3b_fwdbwd.md",
+                     sources=("comba_kernels.hip", "comba_device.hpp")):
     """HBM bytes per launch of a kernel stage from the committed rocprofv3
     FETCH_SIZE / WRITE_SIZE summary (scaled by a plain copy of known size), if
     the counters were taken on the current kernel source; else None."""
-    path = os.path.join(ROOT, "profiles", "traffic_counters_l1p3b_fwdbwd.md")
+    path = os.path.join(ROOT, "profiles", summary)
     try:
         with open(path) as f:
             text = f.read()
         rec = json.loads(text.split("```json", 1)[1].split("```", 1)[0])
     except (OSError, ValueError, IndexError):
         return None
-    if rec.get("source_sha") != kernel_source_sha():
+    if rec.get("source_sha") != kernel_source_sha(sources):
         return None
     k = rec.get("kernels", {}).get(kernel)
     if not k:
@@ -164,19 +168,37 @@ def time_decode(comba, torch, steps, warmup, threads=None, with_cpu=False):
         for st in states:
             call(st)
     torch.cuda.synchronize()
-    comba.profile_enable(True)
+    # the timed calls go straight through the C ABI with their arguments
+    # marshalled beforehand: a decoding call is shorter than the binding's
+    # per-call checks, which would otherwise leave the GPU waiting between calls
+    import ctypes
+    lib = comba.load_library()
+    shp = comba.CombaShape(c["B"], 1, c["H"], c["dk"], c["dv"], comba.CHUNK, c["B"], None,
+                           comba.COMBA_BF16)
+    o = torch.empty((c["B"], 1, c["H"], c["dv"]), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    P = ctypes.c_void_p
+    fixed = [P(x.data_ptr()) for x in (q, k, v, g, beta)] + [None, P(d.data_ptr())]
+    argv = [[ctypes.byref(shp)] + fixed + [P(st.data_ptr()), P(o.data_ptr()), P(st.data_ptr()),
+                                            P(stream.cuda_stream)] for st in states]
+    fn = lib.comba_recurrent_fwd
+    for a in argv:
+        assert fn(*a) == 0
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
+    e0.record(stream)
     for _ in range(steps):
-        for st in states:
-            call(st)
+        for a in argv:
+            fn(*a)
+    e1.record(stream)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    marks = comba.profile_read()
-    comba.profile_enable(False)
     ncalls = steps * len(states)
     ms_call = (t1 - t0) * 1e3 / ncalls
-    kern = [ms for name, ms in marks if name == "recurrent"]
-    kms = sum(kern) / len(kern)
+    # average launch duration: HIP events on the launch stream around the
+    # back-to-back calls (each launch is one kernel)
+    kms = e0.elapsed_time(e1) / ncalls
     by = decode_bytes(c["B"], c["H"], c["dk"], c["dv"])
     achieved = by / (kms * 1e-3) / 1e9
     res = {"value": round(c["B"] / (ms_call * 1e-3), 1), "unit": "tokens/s (one layer)",
@@ -184,7 +206,10 @@ def time_decode(comba, torch, steps, warmup, threads=None, with_cpu=False):
                                                                              "layers")},
            "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
                         "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
-                        "traffic": None, "kernel": "recurrent", "avg_launch_ms": round(kms, 5),
+                        "traffic": measured_traffic("recurrent",
+                                                    "traffic_counters_decode_b64_h16_d128.md",
+                                                    DECODE_SOURCES),
+                        "kernel": "recurrent", "avg_launch_ms": round(kms, 5),
                         "algorithmic_bytes": by}}
     if with_cpu:
         reps = 0
@@ -270,6 +295,14 @@ def main():
             "step": "comba_recurrent_fwd on each of %d layers' states" % c["layers"],
             "ms_per_call": r["ms_per_call"], "roofline": r["roofline"],
             "cpu_baseline": r.get("cpu_baseline")}
+        if args.copy_bytes > 0:
+            n = args.copy_bytes // 4
+            src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+            dst = torch.empty_like(src)
+            torch.cuda.synchronize()
+            dst.copy_(src)
+            torch.cuda.synchronize()
+            result["copy_bytes"] = n * 4
         print(json.dumps(result), flush=True)
         return
 
