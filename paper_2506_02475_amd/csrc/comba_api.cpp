@@ -59,15 +59,25 @@ comba_status check_shape(const comba_shape* s, Dims* out) {
 }
 
 // Shape rules of the token-by-token entry point: those of check_shape, except
-// that the chunk length is not used and fp32 inputs allow d = 128 as well.
+// that the chunk length is not used and dk, dv may each be 64, 128 or 256 for
+// either input dtype (pairs with 64 and 256 excepted).
 comba_status check_shape_recurrent(const comba_shape* s, Dims* out) {
   if (!s) return COMBA_ERR_NULL;
   comba_shape c = *s;
   c.chunk = kChunk;
   const bool f32 = c.in_dtype == COMBA_F32;
   if (f32) c.in_dtype = COMBA_BF16;  // the head-size rule of the bf16 path
+  const bool wide = c.dk == 256 || c.dv == 256;
+  if (wide) {
+    if ((c.dk != 128 && c.dk != 256) || (c.dv != 128 && c.dv != 256)) return COMBA_ERR_SHAPE;
+    c.dk = c.dv = 128;  // checked as d = 128, restored below
+  }
   const comba_status st = check_shape(&c, out);
-  if (st == COMBA_OK) out->bf16 = !f32;
+  if (st == COMBA_OK) {
+    out->bf16 = !f32;
+    out->dk = s->dk;
+    out->dv = s->dv;
+  }
   return st;
 }
 

@@ -213,7 +213,9 @@ __global__ __launch_bounds__(64 * NW) void k_recurrent(
 
 template <typename Tin, int DK, int DV>
 static hipError_t run_recurrent(const RecurrentArgs& a) {
-  constexpr int BV = DV, NW = 4;
+  // at most 128 columns per workgroup and 32 rows per wave: 64 state
+  // registers per lane (a d = 256 state takes two workgroups of 8 waves)
+  constexpr int BV = DV < 128 ? DV : 128, NW = DK <= 128 ? 4 : DK / 32;
   a.stage("recurrent");
   k_recurrent<Tin, DK, DV, BV, NW><<<dim3(a.N, a.H, DV / BV), 64 * NW, 0, a.stream>>>(
       static_cast<const Tin*>(a.q), static_cast<const Tin*>(a.k), static_cast<const Tin*>(a.v),
@@ -229,6 +231,9 @@ static hipError_t run_recurrent_t(const RecurrentArgs& a) {
   if (a.dk == 64 && a.dv == 128) return run_recurrent<Tin, 64, 128>(a);
   if (a.dk == 128 && a.dv == 64) return run_recurrent<Tin, 128, 64>(a);
   if (a.dk == 128 && a.dv == 128) return run_recurrent<Tin, 128, 128>(a);
+  if (a.dk == 256 && a.dv == 256) return run_recurrent<Tin, 256, 256>(a);
+  if (a.dk == 128 && a.dv == 256) return run_recurrent<Tin, 128, 256>(a);
+  if (a.dk == 256 && a.dv == 128) return run_recurrent<Tin, 256, 128>(a);
   return hipErrorInvalidValue;
 }
 

@@ -181,12 +181,17 @@ def test_recurrent_validates_before_launch():
     # every call below stops at a check (a misaligned o or ht marks the ones
     # whose shape passed), so nothing is launched
     assert rec(shape(dk=96)) == ESHAPE
-    assert rec(shape(dv=256)) == ESHAPE
+    assert rec(shape(dv=512)) == ESHAPE
     assert rec(shape(B=2, N=3)) == ESHAPE
     assert rec(shape(dtype=7)) == EDTYPE
     # the chunk length is not used; fp32 inputs allow d = 128 here
     assert rec(shape(chunk=32), o=FAKE + 4) == EALIGN
     assert rec(shape(dk=128, dv=128, dtype=comba.COMBA_F32), o=FAKE + 4) == EALIGN
+    # head dim 256 (the paper's models): with 128 or 256 on the other side
+    for dk, dv in ((256, 256), (128, 256), (256, 128)):
+        assert rec(shape(dk=dk, dv=dv), o=FAKE + 4) == EALIGN, (dk, dv)
+    assert rec(shape(dk=64, dv=256)) == ESHAPE
+    assert rec(shape(dk=256, dv=64)) == ESHAPE
     for name in ("q", "k", "v", "g", "beta", "d", "o"):
         assert rec(shape(), **{name: None}) == ENULL, name
     assert rec(shape(), beta_tilde=FAKE + 1) == EALIGN

@@ -64,6 +64,12 @@ CASES = [
     ("f32_T65_d128", dict(B=2, T=65, H=1, dk=128, dv=128, in_dtype="f32")),
     ("bf16_varlen", dict(T=0, H=2, dk=128, dv=128, in_dtype="bf16", seqlens=[1, 0, 5, 64, 3])),
     ("f32_varlen", dict(T=0, H=2, dk=64, dv=64, in_dtype="f32", seqlens=[0, 9, 1, 0])),
+    # head dim 256, the paper's model setting: two 128-column workgroups of 8 waves
+    ("decode_bf16_d256", dict(B=16, T=1, H=4, dk=256, dv=256, in_dtype="bf16")),
+    ("bf16_T45_d256", dict(B=2, T=45, H=2, dk=256, dv=256, in_dtype="bf16")),
+    ("f32_T20_dk128_dv256", dict(B=2, T=20, H=2, dk=128, dv=256, in_dtype="f32")),
+    ("bf16_varlen_dk256_dv128", dict(T=0, H=2, dk=256, dv=128, in_dtype="bf16",
+                                     seqlens=[3, 0, 40])),
 ]
 
 
