@@ -20,8 +20,9 @@ struct Dims {
   int dk, dv, H, N, Tseq, Ttot, ncmax;
 };
 
-// Validates the shape; fills dims on success.
-comba_status check_shape(const comba_shape* s, Dims* out) {
+// Validates the shape; fills dims on success.  `wide` also admits head dim 256
+// (bf16 inputs, with 128 or 256 on the other side): the stateless forward only.
+comba_status check_shape(const comba_shape* s, Dims* out, bool wide = false) {
   if (!s) return COMBA_ERR_NULL;
   if (s->in_dtype != COMBA_F32 && s->in_dtype != COMBA_BF16) return COMBA_ERR_DTYPE;
   const bool bf16 = s->in_dtype == COMBA_BF16;
@@ -29,7 +30,9 @@ comba_status check_shape(const comba_shape* s, Dims* out) {
   if (s->B < 0 || s->T < 0 || s->H <= 0 || s->H > 65535) return COMBA_ERR_SHAPE;
   const bool dk_ok = s->dk == 64 || (bf16 && s->dk == 128);
   const bool dv_ok = s->dv == 64 || (bf16 && s->dv == 128);
-  if (!dk_ok || !dv_ok) return COMBA_ERR_SHAPE;
+  const bool big = bf16 && wide && (s->dk == 256 || s->dv == 256) &&
+                   (s->dk == 128 || s->dk == 256) && (s->dv == 128 || s->dv == 256);
+  if (!big && (!dk_ok || !dv_ok)) return COMBA_ERR_SHAPE;
   Dims d;
   d.bf16 = bf16;
   d.dk = s->dk;
@@ -240,7 +243,7 @@ comba_status chunk_fwd(bool save, const comba_shape* shape, const void* q, const
                        const float* d, const float* h0, float* o, float* ht, void* ws,
                        size_t ws_bytes, void* stream) {
   Dims dm;
-  comba_status st = check_shape(shape, &dm);
+  comba_status st = check_shape(shape, &dm, !save);
   if (st != COMBA_OK) return st;
   // token tensors may be NULL when the call has no tokens (states pass through)
   const bool tok = dm.Ttot > 0;
@@ -367,7 +370,7 @@ extern "C" {
 
 size_t comba_fwd_workspace_bytes(const comba_shape* shape) {
   Dims d;
-  if (check_shape(shape, &d) != COMBA_OK) return 0;
+  if (check_shape(shape, &d, true) != COMBA_OK) return 0;
   return layout(d, false).total;
 }
 

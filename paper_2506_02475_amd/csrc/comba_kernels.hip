@@ -2624,6 +2624,15 @@ static hipError_t dispatch_bf(const LaunchArgs& a) {
   if (a.dk == 128 && a.dv == 128) return BWD ? run_bwd_bf<128, 128>(a) : run_fwd_bf<128, 128>(a);
   if (a.dk == 64 && a.dv == 128) return BWD ? run_bwd_bf<64, 128>(a) : run_fwd_bf<64, 128>(a);
   if (a.dk == 128 && a.dv == 64) return BWD ? run_bwd_bf<128, 64>(a) : run_fwd_bf<128, 64>(a);
+  if constexpr (!BWD) {
+    // head dim 256 (the paper's models): the stateless forward only (inference
+    // prefill); the host rejects the backward and the saved pair at this size
+    if (!a.saved) {
+      if (a.dk == 256 && a.dv == 256) return run_fwd_bf<256, 256>(a);
+      if (a.dk == 128 && a.dv == 256) return run_fwd_bf<128, 256>(a);
+      if (a.dk == 256 && a.dv == 128) return run_fwd_bf<256, 128>(a);
+    }
+  }
   return hipErrorInvalidValue;
 }
 

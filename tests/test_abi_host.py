@@ -90,7 +90,8 @@ def test_workspace_sizes_grow_with_problem():
 @pytest.mark.parametrize("kw,code", [
     (dict(chunk=32), ESHAPE),
     (dict(dk=96), ESHAPE),
-    (dict(dv=256), ESHAPE),
+    (dict(dv=512), ESHAPE),
+    (dict(dk=64, dv=256), ESHAPE),
     (dict(dk=128, dtype=comba.COMBA_F32), ESHAPE),   # fp32 path supports d = 64 only
     (dict(H=0), ESHAPE),
     (dict(T=-1), ESHAPE),
@@ -201,6 +202,23 @@ def test_recurrent_validates_before_launch():
     none = {n: None for n in ("q", "k", "v", "g", "beta", "o")}
     assert rec(shape(T=0), ht=FAKE + 8, **none) == EALIGN
     assert rec(shape(T=0), d=None, **none) == ENULL
+
+
+def test_head256_forward_only():
+    # head dim 256 (bf16): the stateless forward is accepted (a misaligned o
+    # shows the shape passed), the backward and the saved pair are not
+    for dk, dv in ((256, 256), (128, 256), (256, 128)):
+        s = shape(dk=dk, dv=dv)
+        assert comba.fwd_workspace_bytes(1, 128, 2, dk, dv) > 0
+        assert comba.bwd_workspace_bytes(1, 128, 2, dk, dv) == 0
+        assert fwd(s, o=FAKE + 4) == EALIGN
+        assert bwd(s) == ESHAPE
+        lib = comba.load_library()
+        P = ctypes.c_void_p
+        assert lib.comba_chunk_fwd_save(ctypes.byref(s), *[P(FAKE)] * 10, P(FAKE),
+                                        ctypes.c_size_t(1 << 40), None) == ESHAPE
+    assert fwd(shape(dk=64, dv=256)) == ESHAPE
+    assert fwd(shape(dk=256, dv=256, dtype=comba.COMBA_F32)) == ESHAPE
 
 
 def test_saved_pair_validates_like_the_plain_calls():
