@@ -35,6 +35,7 @@ __all__ = [
     "Workload",
     "WORKLOADS",
     "attach_beta_tilde",
+    "prologue_case",
     "bf16_round",
     "generate",
     "random_case",
@@ -240,6 +241,29 @@ def attach_beta_tilde(w: Workload, form: str = "b_beta", seed: int = 0) -> Workl
     bt = np.ascontiguousarray(bt, dtype=np.float32)
     w.extra["beta_tilde"] = bf16_round(bt) if w.in_dtype == "bf16" else bt
     return w
+
+
+def prologue_case(*, B=1, T=64, H=1, dk=64, dv=64, seed=0, in_dtype="bf16", seqlens=None,
+                  tap_scale=0.5) -> dict:
+    """Seeded inputs of the layer prologue: pre-activations xq, xk [B,T,H,dk] and xv
+    [B,T,H,dv] ~ N(0,1) (bf16-representable for bf16 inputs), taps wq, wk, wv
+    [H,d,4] ~ tap_scale * N(0,1) (fp32), output gradients gq, gk, gv ~ N(0,1)
+    (fp32), and cu_seqlens for packed sequences (then B = 1, T = sum)."""
+    rng = np.random.default_rng(seed)
+    cu = None
+    if seqlens is not None:
+        cu = np.zeros(len(seqlens) + 1, dtype=np.int32)
+        cu[1:] = np.cumsum(seqlens)
+        B, T = 1, int(cu[-1])
+    out = {"cu_seqlens": cu, "B": B, "T": T, "H": H, "dk": dk, "dv": dv, "in_dtype": in_dtype}
+    for n, dd in (("xq", dk), ("xk", dk), ("xv", dv)):
+        x = rng.standard_normal((B, T, H, dd), dtype=np.float32)
+        out[n] = bf16_round(x) if in_dtype == "bf16" else x
+    for n, dd in (("wq", dk), ("wk", dk), ("wv", dv)):
+        out[n] = (np.float32(tap_scale) * rng.standard_normal((H, dd, 4), dtype=np.float32))
+    for n, dd in (("gq", dk), ("gk", dk), ("gv", dv)):
+        out[n] = rng.standard_normal((B, T, H, dd), dtype=np.float32)
+    return out
 
 
 def generate(spec, *, with_grad: Optional[bool] = None, threads: Optional[int] = None) -> Workload:

@@ -172,6 +172,37 @@ comba_status comba_recurrent_fwd(const comba_shape *shape, const void *q, const 
                                  float *o, float *ht, void *stream);
 
 /*
+ * Layer input prologue (Section 3.4, Neural Architecture): turns the projected
+ * pre-activations xq, xk [B,T,H,dk] and xv [B,T,H,dv] (in_dtype) into the
+ * operator's q, k, v (in_dtype, same layouts):
+ *     u_t = sum_{j<4} w[h][c][j] x_{t-3+j}[c]   (causal depthwise conv, zero before
+ *                                               each sequence start)
+ *     s_t = SiLU(u_t);  q, k: y_t = s_t / sqrt(|s_t|^2 + 1e-6) over the head's
+ *     channels;  v: y_t = s_t.
+ * Taps wq, wk [H][dk][4] and wv [H][dv][4] fp32; the newest token takes tap 3.
+ * Shape rules of comba_recurrent_fwd (chunk not used; dk, dv in {64, 128, 256},
+ * 64 not paired with 256).  The forward needs no workspace.  bf16 outputs are
+ * rounded to nearest even.
+ */
+comba_status comba_prologue_fwd(const comba_shape *shape, const void *xq, const void *xk,
+                                const void *xv, const float *wq, const float *wk, const float *wv,
+                                void *q, void *k, void *v, void *stream);
+
+/*
+ * Backward of the prologue: given gq, gk, gv (fp32 gradients of q, k, v, same
+ * layouts), writes dxq, dxk, dxv (fp32, layouts of x) and dwq, dwk, dwv (fp32,
+ * layouts of w; summed over every token of every sequence in a fixed order).
+ * Recomputes the forward.  ws: device workspace of at least
+ * comba_prologue_workspace_bytes(shape) bytes, 256-byte aligned.
+ */
+size_t comba_prologue_workspace_bytes(const comba_shape *shape);
+comba_status comba_prologue_bwd(const comba_shape *shape, const void *xq, const void *xk,
+                                const void *xv, const float *wq, const float *wk, const float *wv,
+                                const float *gq, const float *gk, const float *gv, float *dxq,
+                                float *dxk, float *dxv, float *dwq, float *dwk, float *dwv,
+                                void *ws, size_t ws_bytes, void *stream);
+
+/*
  * Stage timing, for benchmarks (not part of the method).  comba_profile_enable(1)
  * starts a recording session on the calling host thread: every following
  * comba_chunk_fwd / comba_chunk_bwd call on this thread records a HIP event on

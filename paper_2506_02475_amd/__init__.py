@@ -27,7 +27,8 @@ import re
 import threading
 
 __all__ = ["comba_chunk_fwd", "comba_chunk_bwd", "comba_chunk_fwd_save", "comba_chunk_bwd_saved",
-           "comba_recurrent_fwd", "load_library", "library_path",
+           "comba_recurrent_fwd", "comba_prologue_fwd", "comba_prologue_bwd",
+           "load_library", "library_path",
            "profile_enable", "profile_read",
            "fwd_workspace_bytes", "bwd_workspace_bytes", "exported_symbols", "CombaError",
            "CombaShape", "COMBA_F32", "COMBA_BF16", "CHUNK"]
@@ -83,6 +84,12 @@ def load_library():
             lib.comba_chunk_bwd_saved.restype = I
             lib.comba_recurrent_fwd.argtypes = [SP] + [P] * 10 + [P]
             lib.comba_recurrent_fwd.restype = I
+            lib.comba_prologue_fwd.argtypes = [SP] + [P] * 9 + [P]
+            lib.comba_prologue_fwd.restype = I
+            lib.comba_prologue_bwd.argtypes = [SP] + [P] * 15 + [P, Z, P]
+            lib.comba_prologue_bwd.restype = I
+            lib.comba_prologue_workspace_bytes.argtypes = [SP]
+            lib.comba_prologue_workspace_bytes.restype = Z
             lib.comba_profile_enable.argtypes = [I]
             lib.comba_profile_enable.restype = I
             lib.comba_profile_read.argtypes = [P, P, I]
@@ -259,6 +266,81 @@ def comba_recurrent_fwd(q, k, v, g, beta, d, h0=None, *, beta_tilde=None, cu_seq
                                    _ptr(beta), _ptr(beta_tilde), _ptr(d), _ptr(h0), _ptr(o),
                                    _ptr(ht), ctypes.c_void_p(st)))
     return o, ht
+
+
+def _prologue_shape(xq, xk, xv, wq, wk, wv, cu_seqlens, extra=()):
+    import torch
+
+    if not xq.is_cuda:
+        raise CombaError("comba: tensors must be on a GPU device")
+    if xq.dtype not in (torch.bfloat16, torch.float32) or xk.dtype != xq.dtype \
+            or xv.dtype != xq.dtype:
+        raise CombaError("comba: xq, xk, xv must share one dtype (bfloat16 or float32)")
+    B, T, H, dk = xq.shape
+    dv = xv.shape[-1]
+    if xk.shape != xq.shape or tuple(xv.shape[:3]) != (B, T, H) or \
+            tuple(wq.shape) != (H, dk, 4) or tuple(wk.shape) != (H, dk, 4) or \
+            tuple(wv.shape) != (H, dv, 4):
+        raise CombaError("comba: inconsistent prologue shapes")
+    for t in (xq, xk, xv, wq, wk, wv) + tuple(extra):
+        if not t.is_contiguous() or t.device != xq.device:
+            raise CombaError("comba: all tensors must be contiguous and on one device")
+    for t in (wq, wk, wv) + tuple(extra):
+        if t.dtype != torch.float32:
+            raise CombaError("comba: taps and gradients must be float32")
+    if cu_seqlens is not None:
+        if cu_seqlens.dtype != torch.int32 or B != 1:
+            raise CombaError("comba: cu_seqlens must be int32 on the device, B == 1")
+        N = cu_seqlens.numel() - 1
+    else:
+        N = B
+    code = COMBA_BF16 if xq.dtype == torch.bfloat16 else COMBA_F32
+    return _make_shape(B, T, H, dk, dv, N, _ptr(cu_seqlens), code)
+
+
+def comba_prologue_fwd(xq, xk, xv, wq, wk, wv, *, cu_seqlens=None, stream=None):
+    """Layer input prologue: causal short conv (4 taps), SiLU, L2 norm of q and k.
+    Returns (q, k, v) in the dtype of x."""
+    import torch
+
+    lib = load_library()
+    shp = _prologue_shape(xq, xk, xv, wq, wk, wv, cu_seqlens)
+    q, k, v = torch.empty_like(xq), torch.empty_like(xk), torch.empty_like(xv)
+    st = torch.cuda.current_stream(xq.device).cuda_stream if stream is None else stream
+    _check(lib.comba_prologue_fwd(ctypes.byref(shp), _ptr(xq), _ptr(xk), _ptr(xv), _ptr(wq),
+                                  _ptr(wk), _ptr(wv), _ptr(q), _ptr(k), _ptr(v),
+                                  ctypes.c_void_p(st)))
+    return q, k, v
+
+
+def comba_prologue_bwd(xq, xk, xv, wq, wk, wv, gq, gk, gv, *, cu_seqlens=None, workspace=None,
+                       stream=None):
+    """Backward of the prologue from the fp32 gradients of q, k, v.  Returns dict
+    dxq, dxk, dxv, dwq, dwk, dwv (fp32)."""
+    import torch
+
+    lib = load_library()
+    shp = _prologue_shape(xq, xk, xv, wq, wk, wv, cu_seqlens, extra=(gq, gk, gv))
+    if gq.shape != xq.shape or gk.shape != xk.shape or gv.shape != xv.shape:
+        raise CombaError("comba: gradients must have the shapes of q, k, v")
+    f32 = torch.float32
+    out = {"dxq": torch.empty(xq.shape, dtype=f32, device=xq.device),
+           "dxk": torch.empty(xk.shape, dtype=f32, device=xq.device),
+           "dxv": torch.empty(xv.shape, dtype=f32, device=xq.device),
+           "dwq": torch.empty_like(wq), "dwk": torch.empty_like(wk), "dwv": torch.empty_like(wv)}
+    nbytes = lib.comba_prologue_workspace_bytes(ctypes.byref(shp))
+    if nbytes == 0:
+        _check(2)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=xq.device)
+    st = torch.cuda.current_stream(xq.device).cuda_stream if stream is None else stream
+    _check(lib.comba_prologue_bwd(ctypes.byref(shp), _ptr(xq), _ptr(xk), _ptr(xv), _ptr(wq),
+                                  _ptr(wk), _ptr(wv), _ptr(gq), _ptr(gk), _ptr(gv),
+                                  _ptr(out["dxq"]), _ptr(out["dxk"]), _ptr(out["dxv"]),
+                                  _ptr(out["dwq"]), _ptr(out["dwk"]), _ptr(out["dwv"]),
+                                  _ptr(workspace), ctypes.c_size_t(workspace.numel()),
+                                  ctypes.c_void_p(st)))
+    return out
 
 
 def _bwd(saved, q, k, v, g, beta, d, h0, dO, dht, cu_seqlens, need_dh0, workspace, stream,

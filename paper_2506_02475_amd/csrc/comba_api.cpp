@@ -364,9 +364,102 @@ comba_status recurrent_fwd(const comba_shape* shape, const void* q, const void* 
   return comba::launch_recurrent(a) == hipSuccess ? COMBA_OK : COMBA_ERR_HIP;
 }
 
+// Prologue: 64-token runs of the packed token axis and the per-run dw partials.
+constexpr int kRun = 64;
+constexpr float kPrologueEps = 1e-6f;
+
+size_t prologue_ws_bytes(const Dims& d) {
+  const size_t nruns = ((size_t)d.Ttot + kRun - 1) / kRun;
+  return round_up(nruns * d.H * (2 * d.dk + d.dv) * 4 * sizeof(float)) + kAlign;
+}
+
+comba_status prologue(bool bwd, const comba_shape* shape, const void* xq, const void* xk,
+                      const void* xv, const float* wq, const float* wk, const float* wv, void* q,
+                      void* k, void* v, const float* gq, const float* gk, const float* gv,
+                      float* dxq, float* dxk, float* dxv, float* dwq, float* dwk, float* dwv,
+                      void* ws, size_t ws_bytes, void* stream) {
+  Dims dm;
+  comba_status st = check_shape_recurrent(shape, &dm);
+  if (st != COMBA_OK) return st;
+  const bool tok = dm.Ttot > 0;
+  if (tok && dm.N == 0) return COMBA_ERR_SHAPE;  // tokens must belong to a sequence
+  if (tok && (!xq || !xk || !xv || !wq || !wk || !wv)) return COMBA_ERR_NULL;
+  if (!bwd && tok && (!q || !k || !v)) return COMBA_ERR_NULL;
+  if (bwd && ((tok && (!gq || !gk || !gv || !dxq || !dxk || !dxv)) || !dwq || !dwk || !dwv || !ws))
+    return COMBA_ERR_NULL;
+  if (!aligned(xq, 16) || !aligned(xk, 16) || !aligned(xv, 16) || !aligned(wq, 4) ||
+      !aligned(wk, 4) || !aligned(wv, 4) || !aligned(q, 16) || !aligned(k, 16) ||
+      !aligned(v, 16) || !aligned(gq, 16) || !aligned(gk, 16) || !aligned(gv, 16) ||
+      !aligned(dxq, 16) || !aligned(dxk, 16) || !aligned(dxv, 16) || !aligned(dwq, 4) ||
+      !aligned(dwk, 4) || !aligned(dwv, 4) || !aligned(ws, kAlign))
+    return COMBA_ERR_ALIGN;
+  if (bwd && ws_bytes < prologue_ws_bytes(dm)) return COMBA_ERR_WORKSPACE;
+  comba::PrologueArgs a{};
+  a.bf16 = dm.bf16;
+  a.dk = dm.dk;
+  a.dv = dm.dv;
+  a.H = dm.H;
+  a.N = dm.N;
+  a.Tseq = dm.Tseq;
+  a.Ttot = dm.Ttot;
+  a.nruns = (dm.Ttot + kRun - 1) / kRun;
+  a.eps = kPrologueEps;
+  a.cu_seqlens = shape->cu_seqlens;
+  a.xq = xq;
+  a.xk = xk;
+  a.xv = xv;
+  a.wq = wq;
+  a.wk = wk;
+  a.wv = wv;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.gq = gq;
+  a.gk = gk;
+  a.gv = gv;
+  a.dxq = dxq;
+  a.dxk = dxk;
+  a.dxv = dxv;
+  a.dwq = dwq;
+  a.dwk = dwk;
+  a.dwv = dwv;
+  if (bwd) {
+    const size_t nr = (size_t)a.nruns * a.H;
+    float* base = static_cast<float*>(ws);
+    a.dwpq = base;
+    a.dwpk = base + nr * a.dk * 4;
+    a.dwpv = base + 2 * nr * a.dk * 4;
+  }
+  a.stream = static_cast<hipStream_t>(stream);
+  attach_profile(a);
+  return comba::launch_prologue(a, bwd) == hipSuccess ? COMBA_OK : COMBA_ERR_HIP;
+}
+
 }  // namespace
 
 extern "C" {
+
+size_t comba_prologue_workspace_bytes(const comba_shape* shape) {
+  Dims d;
+  if (check_shape_recurrent(shape, &d) != COMBA_OK) return 0;
+  return prologue_ws_bytes(d);
+}
+
+comba_status comba_prologue_fwd(const comba_shape* shape, const void* xq, const void* xk,
+                                const void* xv, const float* wq, const float* wk, const float* wv,
+                                void* q, void* k, void* v, void* stream) {
+  return prologue(false, shape, xq, xk, xv, wq, wk, wv, q, k, v, nullptr, nullptr, nullptr,
+                  nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0, stream);
+}
+
+comba_status comba_prologue_bwd(const comba_shape* shape, const void* xq, const void* xk,
+                                const void* xv, const float* wq, const float* wk, const float* wv,
+                                const float* gq, const float* gk, const float* gv, float* dxq,
+                                float* dxk, float* dxv, float* dwq, float* dwk, float* dwv,
+                                void* ws, size_t ws_bytes, void* stream) {
+  return prologue(true, shape, xq, xk, xv, wq, wk, wv, nullptr, nullptr, nullptr, gq, gk, gv, dxq,
+                  dxk, dxv, dwq, dwk, dwv, ws, ws_bytes, stream);
+}
 
 size_t comba_fwd_workspace_bytes(const comba_shape* shape) {
   Dims d;

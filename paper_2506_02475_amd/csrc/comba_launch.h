@@ -85,4 +85,27 @@ struct RecurrentArgs {
 
 hipError_t launch_recurrent(const RecurrentArgs& a);
 
+// Layer input prologue (comba_prologue_fwd / comba_prologue_bwd).
+struct PrologueArgs {
+  bool bf16;
+  int dk, dv, H, N, Tseq, Ttot;
+  int nruns;  // 64-token runs of the packed token axis
+  float eps;
+  const int32_t* cu_seqlens;
+  const void *xq, *xk, *xv;     // pre-activations (in_dtype)
+  const float *wq, *wk, *wv;    // taps [H][d][4]
+  void *q, *k, *v;              // forward outputs (in_dtype)
+  const float *gq, *gk, *gv;    // backward: gradients of q, k, v
+  float *dxq, *dxk, *dxv;       // backward outputs
+  float *dwq, *dwk, *dwv;
+  float *dwpq, *dwpk, *dwpv;    // per-run dw partials (workspace)
+  hipStream_t stream;
+  StageHook hook;
+  void stage(const char* name) const {
+    if (hook.mark) hook.mark(hook.ctx, stream, name);
+  }
+};
+
+hipError_t launch_prologue(const PrologueArgs& a, bool bwd);
+
 }  // namespace comba

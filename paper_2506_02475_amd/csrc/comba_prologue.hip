@@ -1,0 +1,356 @@
+// Input prologue of the Comba layer (Section 3.4, Neural Architecture): the
+// projected q, k, v pre-activations pass through a short causal depthwise
+// convolution (K = 4 taps per channel, zero history at each sequence start),
+// the SiLU feature map and, for q and k, an L2 normalisation over the head's
+// channels; the results are the chunk operator's inputs.
+//
+//   u_t = sum_j w[j] x_{t-3+j},   s_t = u_t sigmoid(u_t),   y_t = s_t / sqrt(|s_t|^2 + eps)
+//
+// Both directions are streaming: one wavefront walks a run of 64 tokens of one
+// head along the sequence, its lanes holding D / 64 consecutive channels each,
+// with the convolution window in registers (every x row is read once, plus a
+// three-row halo per run).  The L2 norms are wave reductions.
+#include "comba_device.hpp"
+#include "comba_launch.h"
+
+namespace comba {
+
+constexpr int PRO_RUN = 64;   // tokens per wave
+constexpr int PRO_K = 4;      // taps
+constexpr int PRO_WAVES = 4;  // waves (runs) per workgroup
+
+template <typename Tin, int C>
+__device__ __forceinline__ void load_ch(const Tin* p, float (&v)[C]) {
+  if constexpr (is_f32<Tin>::value) {
+#pragma unroll
+    for (int i = 0; i < C; ++i) v[i] = p[i];
+  } else if constexpr (C == 1) {
+    v[0] = bf2f(*p);
+  } else if constexpr (C == 2) {
+    const uint32_t u = *reinterpret_cast<const uint32_t*>(p);
+    v[0] = __uint_as_float(u << 16);
+    v[1] = __uint_as_float(u & 0xFFFF0000u);
+  } else {
+    static_assert(C == 4, "channels per lane");
+    const uint2 u = *reinterpret_cast<const uint2*>(p);
+    v[0] = __uint_as_float(u.x << 16);
+    v[1] = __uint_as_float(u.x & 0xFFFF0000u);
+    v[2] = __uint_as_float(u.y << 16);
+    v[3] = __uint_as_float(u.y & 0xFFFF0000u);
+  }
+}
+
+__device__ __forceinline__ bf16_t f2bf(float x) {  // round to nearest even
+  const uint32_t u = __float_as_uint(x);
+  return (bf16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+
+template <typename Tin, int C>
+__device__ __forceinline__ void store_ch(Tin* p, const float (&v)[C]) {
+  if constexpr (is_f32<Tin>::value) {
+#pragma unroll
+    for (int i = 0; i < C; ++i) p[i] = v[i];
+  } else {
+#pragma unroll
+    for (int i = 0; i < C; ++i) p[i] = f2bf(v[i]);
+  }
+}
+
+__device__ __forceinline__ float sigm(float u) { return 1.f / (1.f + __expf(-u)); }
+
+// Sequence [sa, se) holding token t.
+__device__ __forceinline__ void seq_bounds(const int32_t* __restrict__ cu, int N, int Tseq, int Ttot,
+                                           int t, int& sa, int& se) {
+  if (!cu || N <= 0) {  // (the host rejects tokens without sequences)
+    sa = cu ? 0 : (t / Tseq) * Tseq;
+    se = cu ? Ttot : sa + Tseq;
+    return;
+  }
+  // largest s < N with cu[s] <= t (then cu[s + 1] > t: empty sequences skipped)
+  int lo = 0, hi = N - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (cu[mid] <= t) lo = mid; else hi = mid - 1;
+  }
+  sa = min(max(cu[lo], 0), t);
+  se = min(max(cu[lo + 1], t + 1), Ttot);
+}
+
+// Forward of one run of one head for one tensor.
+template <typename Tin, int D, bool NORM>
+__device__ __forceinline__ void prologue_fwd_run(const Tin* __restrict__ x, const float* __restrict__ w,
+                                                 Tin* __restrict__ y, const int32_t* __restrict__ cu,
+                                                 int N, int Tseq, int Ttot, int H, int run, float eps) {
+  constexpr int C = D / 64;
+  const int lane = lane_id(), h = blockIdx.y;
+  const int t0 = run * PRO_RUN, t1 = min(t0 + PRO_RUN, Ttot);
+  if (t0 >= Ttot) return;
+  const int c0 = lane * C;
+  float wt[C][PRO_K];
+#pragma unroll
+  for (int i = 0; i < C; ++i)
+#pragma unroll
+    for (int j = 0; j < PRO_K; ++j) wt[i][j] = w[((long)h * D + c0 + i) * PRO_K + j];
+  int sa, se;
+  seq_bounds(cu, N, Tseq, Ttot, t0, sa, se);
+  // window: x of tokens t-3, t-2, t-1 (zero before the sequence start)
+  float xw[PRO_K - 1][C];
+#pragma unroll
+  for (int m = 0; m < PRO_K - 1; ++m) {
+    const int tt = t0 - (PRO_K - 1) + m;
+    if (tt >= sa) {
+      load_ch<Tin, C>(x + ((long)tt * H + h) * D + c0, xw[m]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < C; ++i) xw[m][i] = 0.f;
+    }
+  }
+  for (int t = t0; t < t1; ++t) {
+    if (t >= se) {  // next (non-empty) sequence: no history
+      seq_bounds(cu, N, Tseq, Ttot, t, sa, se);
+#pragma unroll
+      for (int m = 0; m < PRO_K - 1; ++m)
+#pragma unroll
+        for (int i = 0; i < C; ++i) xw[m][i] = 0.f;
+    }
+    float xt[C], s[C];
+    load_ch<Tin, C>(x + ((long)t * H + h) * D + c0, xt);
+    float ss = 0.f;
+#pragma unroll
+    for (int i = 0; i < C; ++i) {
+      float u = wt[i][PRO_K - 1] * xt[i];
+#pragma unroll
+      for (int m = 0; m < PRO_K - 1; ++m) u = fmaf(wt[i][m], xw[m][i], u);
+      s[i] = u * sigm(u);
+      ss = fmaf(s[i], s[i], ss);
+    }
+    if constexpr (NORM) {
+      const float inv = rsqrtf(wave_sum(ss) + eps);
+#pragma unroll
+      for (int i = 0; i < C; ++i) s[i] *= inv;
+    }
+    store_ch<Tin, C>(y + ((long)t * H + h) * D + c0, s);
+#pragma unroll
+    for (int i = 0; i < C; ++i) {
+#pragma unroll
+      for (int m = 0; m < PRO_K - 2; ++m) xw[m][i] = xw[m + 1][i];
+      xw[PRO_K - 2][i] = xt[i];
+    }
+  }
+}
+
+template <typename Tin, int DK, int DV>
+__global__ __launch_bounds__(64 * PRO_WAVES) void k_prologue_fwd(PrologueArgs a) {
+  const int run = blockIdx.x * PRO_WAVES + wave_id();
+  const int z = blockIdx.z;
+  if (z == 0)
+    prologue_fwd_run<Tin, DK, true>(static_cast<const Tin*>(a.xq), a.wq, static_cast<Tin*>(a.q),
+                                    a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.H, run, a.eps);
+  else if (z == 1)
+    prologue_fwd_run<Tin, DK, true>(static_cast<const Tin*>(a.xk), a.wk, static_cast<Tin*>(a.k),
+                                    a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.H, run, a.eps);
+  else
+    prologue_fwd_run<Tin, DV, false>(static_cast<const Tin*>(a.xv), a.wv, static_cast<Tin*>(a.v),
+                                     a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.H, run, a.eps);
+}
+
+// Backward of one run: dx rows [t0, t1) and this run's share of dw.  du is
+// formed for tokens [t0, t1 + 3) (the last three belong to the next run but
+// feed this run's last rows); du_t adds w[j] du_t to dx row t - 3 + j, kept in
+// a four-row register accumulator whose oldest row is complete after each token.
+template <typename Tin, int D, bool NORM>
+__device__ __forceinline__ void prologue_bwd_run(const Tin* __restrict__ x, const float* __restrict__ w,
+                                                 const float* __restrict__ dy, float* __restrict__ dx,
+                                                 float* __restrict__ dwp, const int32_t* __restrict__ cu,
+                                                 int N, int Tseq, int Ttot, int H, int run, float eps) {
+  constexpr int C = D / 64;
+  const int lane = lane_id(), h = blockIdx.y;
+  const int t0 = run * PRO_RUN, t1 = min(t0 + PRO_RUN, Ttot);
+  if (t0 >= Ttot) return;
+  const int c0 = lane * C;
+  float wt[C][PRO_K], dw[C][PRO_K];
+#pragma unroll
+  for (int i = 0; i < C; ++i)
+#pragma unroll
+    for (int j = 0; j < PRO_K; ++j) {
+      wt[i][j] = w[((long)h * D + c0 + i) * PRO_K + j];
+      dw[i][j] = 0.f;
+    }
+  int sa, se;
+  seq_bounds(cu, N, Tseq, Ttot, t0, sa, se);
+  float xw[PRO_K - 1][C], acc[PRO_K][C];  // acc[m]: dx row t - 3 + m
+#pragma unroll
+  for (int m = 0; m < PRO_K - 1; ++m) {
+    const int tt = t0 - (PRO_K - 1) + m;
+    if (tt >= sa) {
+      load_ch<Tin, C>(x + ((long)tt * H + h) * D + c0, xw[m]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < C; ++i) xw[m][i] = 0.f;
+    }
+  }
+#pragma unroll
+  for (int m = 0; m < PRO_K; ++m)
+#pragma unroll
+    for (int i = 0; i < C; ++i) acc[m][i] = 0.f;
+  // store the pending rows t-3 .. t-3+cnt-1 that are this run's and in the sequence
+  auto flush = [&](int t, int cnt) {
+#pragma unroll
+    for (int m = 0; m < PRO_K - 1; ++m) {
+      const int r = t - (PRO_K - 1) + m;
+      if (m < cnt && r >= t0 && r < t1 && r >= sa) {
+        float* p = dx + ((long)r * H + h) * D + c0;
+#pragma unroll
+        for (int i = 0; i < C; ++i) p[i] = acc[m][i];
+      }
+    }
+  };
+  const int tstop = min(t1 + PRO_K - 1, Ttot);
+  int t = t0;
+  for (; t < tstop; ++t) {
+    if (t >= se) {
+      // sequence end: its last rows are complete
+      flush(t, PRO_K - 1);
+      if (t >= t1) break;  // the rest belongs to later runs
+      seq_bounds(cu, N, Tseq, Ttot, t, sa, se);
+#pragma unroll
+      for (int m = 0; m < PRO_K; ++m)
+#pragma unroll
+        for (int i = 0; i < C; ++i) acc[m][i] = 0.f;
+#pragma unroll
+      for (int m = 0; m < PRO_K - 1; ++m)
+#pragma unroll
+        for (int i = 0; i < C; ++i) xw[m][i] = 0.f;
+    }
+    float xt[C], g[C], u[C], sg[C], s[C];
+    load_ch<Tin, C>(x + ((long)t * H + h) * D + c0, xt);
+    const float* gp = dy + ((long)t * H + h) * D + c0;
+#pragma unroll
+    for (int i = 0; i < C; ++i) g[i] = gp[i];
+    float ss = 0.f;
+#pragma unroll
+    for (int i = 0; i < C; ++i) {
+      float uu = wt[i][PRO_K - 1] * xt[i];
+#pragma unroll
+      for (int m = 0; m < PRO_K - 1; ++m) uu = fmaf(wt[i][m], xw[m][i], uu);
+      u[i] = uu;
+      sg[i] = sigm(uu);
+      s[i] = uu * sg[i];
+      ss = fmaf(s[i], s[i], ss);
+    }
+    float ds[C];
+    if constexpr (NORM) {
+      const float inv = rsqrtf(wave_sum(ss) + eps);
+      float yg = 0.f;
+#pragma unroll
+      for (int i = 0; i < C; ++i) yg = fmaf(s[i] * inv, g[i], yg);
+      yg = wave_sum(yg);
+#pragma unroll
+      for (int i = 0; i < C; ++i) ds[i] = (g[i] - s[i] * inv * yg) * inv;
+    } else {
+#pragma unroll
+      for (int i = 0; i < C; ++i) ds[i] = g[i];
+    }
+    const bool own = t < t1;
+#pragma unroll
+    for (int i = 0; i < C; ++i) {
+      const float du = ds[i] * sg[i] * (1.f + u[i] * (1.f - sg[i]));
+#pragma unroll
+      for (int j = 0; j < PRO_K; ++j) acc[j][i] = fmaf(wt[i][j], du, acc[j][i]);
+      if (own) {
+#pragma unroll
+        for (int j = 0; j < PRO_K - 1; ++j) dw[i][j] = fmaf(du, xw[j][i], dw[i][j]);
+        dw[i][PRO_K - 1] = fmaf(du, xt[i], dw[i][PRO_K - 1]);
+      }
+    }
+    // row t - 3 has all its terms
+    {
+      const int r = t - (PRO_K - 1);
+      if (r >= t0 && r < t1 && r >= sa) {
+        float* p = dx + ((long)r * H + h) * D + c0;
+#pragma unroll
+        for (int i = 0; i < C; ++i) p[i] = acc[0][i];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < C; ++i) {
+#pragma unroll
+      for (int m = 0; m < PRO_K - 1; ++m) acc[m][i] = acc[m + 1][i];
+      acc[PRO_K - 1][i] = 0.f;
+#pragma unroll
+      for (int m = 0; m < PRO_K - 2; ++m) xw[m][i] = xw[m + 1][i];
+      xw[PRO_K - 2][i] = xt[i];
+    }
+  }
+  // loop ended at t1 + 3, at the end of the tokens, or at a sequence end past
+  // t1: every pending row of this run is complete
+  if (t == tstop) flush(t, PRO_K - 1);
+  // this run's dw share: [run][h][D][K]
+  float* q = dwp + (((long)run * H + h) * D + c0) * PRO_K;
+#pragma unroll
+  for (int i = 0; i < C; ++i)
+    *reinterpret_cast<float4*>(q + i * PRO_K) = make_float4(dw[i][0], dw[i][1], dw[i][2], dw[i][3]);
+}
+
+template <typename Tin, int DK, int DV>
+__global__ __launch_bounds__(64 * PRO_WAVES) void k_prologue_bwd(PrologueArgs a) {
+  const int run = blockIdx.x * PRO_WAVES + wave_id();
+  const int z = blockIdx.z;
+  if (run >= a.nruns) return;
+  if (z == 0)
+    prologue_bwd_run<Tin, DK, true>(static_cast<const Tin*>(a.xq), a.wq, a.gq, a.dxq, a.dwpq,
+                                    a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.H, run, a.eps);
+  else if (z == 1)
+    prologue_bwd_run<Tin, DK, true>(static_cast<const Tin*>(a.xk), a.wk, a.gk, a.dxk, a.dwpk,
+                                    a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.H, run, a.eps);
+  else
+    prologue_bwd_run<Tin, DV, false>(static_cast<const Tin*>(a.xv), a.wv, a.gv, a.dxv, a.dwpv,
+                                     a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.H, run, a.eps);
+}
+
+// dw[i] = sum over runs of the partials (fixed order), for q, k and v.
+__global__ __launch_bounds__(256) void k_prologue_dw(PrologueArgs a) {
+  const int z = blockIdx.y;
+  const long n = (long)a.H * (z == 2 ? a.dv : a.dk) * PRO_K;
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  const float* p = z == 0 ? a.dwpq : (z == 1 ? a.dwpk : a.dwpv);
+  float s = 0.f;
+  for (int r = 0; r < a.nruns; ++r) s += p[(long)r * n + i];
+  (z == 0 ? a.dwq : (z == 1 ? a.dwk : a.dwv))[i] = s;
+}
+
+template <typename Tin, int DK, int DV>
+static hipError_t run_prologue(const PrologueArgs& a, bool bwd) {
+  const dim3 grid((a.nruns + PRO_WAVES - 1) / PRO_WAVES, a.H, 3);
+  if (!bwd) {
+    a.stage("prologue_fwd");
+    if (a.nruns > 0) k_prologue_fwd<Tin, DK, DV><<<grid, 64 * PRO_WAVES, 0, a.stream>>>(a);
+  } else {
+    a.stage("prologue_bwd");
+    if (a.nruns > 0) k_prologue_bwd<Tin, DK, DV><<<grid, 64 * PRO_WAVES, 0, a.stream>>>(a);
+    a.stage("prologue_dw");
+    const int dmax = a.dk > a.dv ? a.dk : a.dv;
+    k_prologue_dw<<<dim3((a.H * dmax * PRO_K + 255) / 256, 3), 256, 0, a.stream>>>(a);
+  }
+  a.stage(nullptr);
+  return hipGetLastError();
+}
+
+template <typename Tin>
+static hipError_t dispatch_prologue(const PrologueArgs& a, bool bwd) {
+  if (a.dk == 64 && a.dv == 64) return run_prologue<Tin, 64, 64>(a, bwd);
+  if (a.dk == 64 && a.dv == 128) return run_prologue<Tin, 64, 128>(a, bwd);
+  if (a.dk == 128 && a.dv == 64) return run_prologue<Tin, 128, 64>(a, bwd);
+  if (a.dk == 128 && a.dv == 128) return run_prologue<Tin, 128, 128>(a, bwd);
+  if (a.dk == 256 && a.dv == 256) return run_prologue<Tin, 256, 256>(a, bwd);
+  if (a.dk == 128 && a.dv == 256) return run_prologue<Tin, 128, 256>(a, bwd);
+  if (a.dk == 256 && a.dv == 128) return run_prologue<Tin, 256, 128>(a, bwd);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_prologue(const PrologueArgs& a, bool bwd) {
+  return a.bf16 ? dispatch_prologue<bf16_t>(a, bwd) : dispatch_prologue<float>(a, bwd);
+}
+
+}  // namespace comba

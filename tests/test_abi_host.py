@@ -51,7 +51,8 @@ def test_library_exports_every_declared_symbol():
                              "comba_chunk_fwd", "comba_chunk_bwd", "comba_status_string",
                              "comba_profile_enable", "comba_profile_read",
                              "comba_chunk_fwd_save", "comba_chunk_bwd_saved",
-                             "comba_recurrent_fwd"}
+                             "comba_recurrent_fwd", "comba_prologue_fwd", "comba_prologue_bwd",
+                             "comba_prologue_workspace_bytes"}
     out = subprocess.run(["nm", "-D", "--defined-only", comba.library_path()],
                          capture_output=True, text=True, check=True).stdout
     exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
@@ -219,6 +220,42 @@ def test_head256_forward_only():
                                         ctypes.c_size_t(1 << 40), None) == ESHAPE
     assert fwd(shape(dk=64, dv=256)) == ESHAPE
     assert fwd(shape(dk=256, dv=256, dtype=comba.COMBA_F32)) == ESHAPE
+
+
+def pro(shp, bwd=False, ws_bytes=1 << 40, **over):
+    lib = comba.load_library()
+    P = ctypes.c_void_p
+    if not bwd:
+        names = ("xq", "xk", "xv", "wq", "wk", "wv", "q", "k", "v")
+        p = {n: FAKE for n in names}
+        p.update(over)
+        return lib.comba_prologue_fwd(ctypes.byref(shp), *[P(p[n]) for n in names], None)
+    names = ("xq", "xk", "xv", "wq", "wk", "wv", "gq", "gk", "gv", "dxq", "dxk", "dxv",
+             "dwq", "dwk", "dwv", "ws")
+    p = {n: FAKE for n in names}
+    p.update(over)
+    return lib.comba_prologue_bwd(ctypes.byref(shp), *[P(p[n]) for n in names],
+                                  ctypes.c_size_t(ws_bytes), None)
+
+
+def test_prologue_validates_before_launch():
+    lib = comba.load_library()
+    s = shape(B=2, T=130, H=3, dk=128, dv=64)
+    need = lib.comba_prologue_workspace_bytes(ctypes.byref(s))
+    # 3 runs x 3 heads x (2 x 128 + 64) channels x 4 taps of fp32 partials
+    assert need >= 3 * 3 * 320 * 4 * 4
+    assert pro(shape(dk=96)) == ESHAPE and pro(shape(dk=64, dv=256), bwd=True) == ESHAPE
+    assert pro(shape(dtype=7)) == EDTYPE
+    assert pro(shape(cu=FAKE, N=0)) == ESHAPE  # tokens without sequences
+    for name in ("xq", "xk", "xv", "wq", "wk", "wv", "q", "k", "v"):
+        assert pro(s, **{name: None}) == ENULL, name
+    for name in ("gq", "dxv", "dwk", "ws"):
+        assert pro(s, bwd=True, **{name: None}) == ENULL, name
+    assert pro(s, xq=FAKE + 8) == EALIGN
+    assert pro(s, bwd=True, dwq=FAKE + 2) == EALIGN
+    assert pro(s, bwd=True, ws_bytes=need - 1) == EWS
+    # the chunk length is not used; head dim 256 is accepted (stopped by the alignment check)
+    assert pro(shape(chunk=32, dk=256, dv=256), q=FAKE + 8) == EALIGN
 
 
 def test_saved_pair_validates_like_the_plain_calls():
