@@ -282,6 +282,73 @@ def time_prefill256(comba, torch, steps, warmup):
                          "algorithmic_bytes": by, "algorithmic_flops": fl}}
 
 
+PROLOGUE = dict(B=4, T=4096, H=16, dk=128, dv=128, seed=71)
+
+
+def prologue_bytes(stage, B, T, H, dk, dv, in_bytes=2):
+    """Algorithmic HBM bytes of one prologue launch: the forward reads x and
+    writes q, k, v (in_dtype); the backward reads x (in_dtype) and the fp32
+    gradients of q, k, v and writes fp32 dx (taps and dw are negligible)."""
+    n = B * T * H * (2 * dk + dv)
+    return float(n * 2 * in_bytes if stage == "prologue_fwd" else n * (in_bytes + 8))
+
+
+def time_prologue(comba, torch, steps, warmup):
+    """Layer input prologue (short conv, SiLU, L2 norm) forward + backward on the
+    1.3B layer's q, k, v (B4 T4096 H16 d128 bf16)."""
+    import numpy as np
+    from comba_inputs import prologue_case
+
+    c = PROLOGUE
+    pc = prologue_case(seed=c["seed"], B=c["B"], T=c["T"], H=c["H"], dk=c["dk"], dv=c["dv"],
+                       in_dtype="bf16")
+    dev = torch.device("cuda:0")
+
+    def t(x, dt=torch.float32):
+        return torch.from_numpy(np.ascontiguousarray(x)).to(dev, dt)
+
+    xs = [t(pc[n], torch.bfloat16) for n in ("xq", "xk", "xv")]
+    ws = [t(pc[n]) for n in ("wq", "wk", "wv")]
+    gs = [t(pc[n]) for n in ("gq", "gk", "gv")]
+    wsp = None
+
+    def step():
+        nonlocal wsp
+        comba.comba_prologue_fwd(*xs, *ws)
+        out = comba.comba_prologue_bwd(*xs, *ws, *gs, workspace=wsp)
+        return out
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    comba.profile_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    marks = comba.profile_read()
+    comba.profile_enable(False)
+    tot, cnt = {}, {}
+    for name, ms in marks:
+        tot[name] = tot.get(name, 0.0) + ms
+        cnt[name] = cnt.get(name, 0) + 1
+    roof = {}
+    for st in ("prologue_fwd", "prologue_bwd"):
+        avg = tot[st] / cnt[st]
+        by = prologue_bytes(st, c["B"], c["T"], c["H"], c["dk"], c["dv"])
+        ach = by / (avg * 1e-3) / 1e9
+        roof[st] = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
+                    "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None,
+                    "kernel": st, "avg_launch_ms": round(avg, 4), "algorithmic_bytes": by}
+    ms_step = (t1 - t0) * 1e3 / steps
+    return {"value": round(c["B"] * c["T"] / (ms_step * 1e-3), 1), "unit": "tokens/s",
+            "ms_per_step": round(ms_step, 4),
+            "config": {k_: c[k_] for k_ in ("B", "T", "H", "dk", "dv")},
+            "stages_ms": {n: round(x / steps, 4) for n, x in tot.items()},
+            "roofline": roof["prologue_bwd"], "roofline_fwd": roof["prologue_fwd"]}
+
+
 def cpu_baseline(w, heads_sample, threads):
     import oracle
 
@@ -315,6 +382,9 @@ def main():
     ap.add_argument("--prefill256", action="store_true",
                     help="time the inference prefill at head dim 256 (comba_chunk_fwd, B4 T4096 "
                          "H8 d256) as the headline")
+    ap.add_argument("--prologue", action="store_true",
+                    help="time the layer input prologue (short conv, SiLU, L2 norm; fwd + bwd) "
+                         "on the 1.3B layer's q, k, v as the headline")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="after the timed steps, run one plain device-to-device copy of this "
                          "many bytes (calibrates HBM traffic counters against a known size)")
@@ -336,6 +406,21 @@ def main():
         threads = len(os.sched_getaffinity(0))
     except Exception:
         threads = os.cpu_count() or 1
+    if args.prologue:
+        torch.cuda.set_device(0)
+        r = time_prologue(comba, torch, args.steps, args.warmup)
+        result = {
+            "metric": "Comba layer prologue (conv4, SiLU, L2 norm) fwd+bwd tokens/s at "
+                      "B=4,T=4096,H=16,d=128 bf16",
+            "value": r["value"], "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": r["ms_per_step"], "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+            "data": "synthetic (seeded PCG64, comba_inputs.prologue_case)",
+            "config": {"workload": "prologue_b4_t4096_h16_d128", **r["config"]},
+            "step": "comba_prologue_fwd + comba_prologue_bwd", "stages_ms": r["stages_ms"],
+            "roofline": r["roofline"], "roofline_fwd": r["roofline_fwd"], "cpu_baseline": None}
+        print(json.dumps(result), flush=True)
+        return
     if args.prefill256:
         torch.cuda.set_device(0)
         r = time_prefill256(comba, torch, args.steps, args.warmup)
@@ -520,6 +605,8 @@ def main():
         result["variants"]["decode_b64_h16_d128"] = time_decode(comba, torch, args.steps,
                                                                 args.warmup)
         result["variants"]["prefill_b4_t4096_h8_d256"] = time_prefill256(comba, torch,
+                                                                         args.steps, args.warmup)
+        result["variants"]["prologue_b4_t4096_h16_d128"] = time_prologue(comba, torch,
                                                                          args.steps, args.warmup)
     if args.copy_bytes > 0:
         n = args.copy_bytes // 4

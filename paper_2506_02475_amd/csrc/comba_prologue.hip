@@ -18,12 +18,24 @@ namespace comba {
 constexpr int PRO_RUN = 64;   // tokens per wave
 constexpr int PRO_K = 4;      // taps
 constexpr int PRO_WAVES = 4;  // waves (runs) per workgroup
+constexpr int PRO_PF = 8;     // token rows loaded ahead, together
 
 template <typename Tin, int C>
 __device__ __forceinline__ void load_ch(const Tin* p, float (&v)[C]) {
   if constexpr (is_f32<Tin>::value) {
-#pragma unroll
-    for (int i = 0; i < C; ++i) v[i] = p[i];
+    if constexpr (C == 1) {
+      v[0] = *p;
+    } else if constexpr (C == 2) {
+      const float2 f = *reinterpret_cast<const float2*>(p);
+      v[0] = f.x;
+      v[1] = f.y;
+    } else {
+      const float4 f = *reinterpret_cast<const float4*>(p);
+      v[0] = f.x;
+      v[1] = f.y;
+      v[2] = f.z;
+      v[3] = f.w;
+    }
   } else if constexpr (C == 1) {
     v[0] = bf2f(*p);
   } else if constexpr (C == 2) {
@@ -45,14 +57,31 @@ __device__ __forceinline__ bf16_t f2bf(float x) {  // round to nearest even
   return (bf16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
 }
 
+// One vector store per lane and row (element-wise stores would leave every
+// instruction writing only parts of each 4-byte word).
+template <int C>
+__device__ __forceinline__ void store_f32(float* p, const float (&v)[C]) {
+  if constexpr (C == 1) {
+    *p = v[0];
+  } else if constexpr (C == 2) {
+    *reinterpret_cast<float2*>(p) = make_float2(v[0], v[1]);
+  } else {
+    static_assert(C == 4, "channels per lane");
+    *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+  }
+}
+
 template <typename Tin, int C>
 __device__ __forceinline__ void store_ch(Tin* p, const float (&v)[C]) {
   if constexpr (is_f32<Tin>::value) {
-#pragma unroll
-    for (int i = 0; i < C; ++i) p[i] = v[i];
+    store_f32<C>(p, v);
+  } else if constexpr (C == 1) {
+    *p = f2bf(v[0]);
+  } else if constexpr (C == 2) {
+    *reinterpret_cast<uint32_t*>(p) = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
   } else {
-#pragma unroll
-    for (int i = 0; i < C; ++i) p[i] = f2bf(v[i]);
+    *reinterpret_cast<uint2*>(p) = make_uint2((uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16),
+                                              (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16));
   }
 }
 
@@ -105,7 +134,14 @@ __device__ __forceinline__ void prologue_fwd_run(const Tin* __restrict__ x, cons
       for (int i = 0; i < C; ++i) xw[m][i] = 0.f;
     }
   }
-  for (int t = t0; t < t1; ++t) {
+  for (int tb = t0; tb < t1; tb += PRO_PF) {
+  float xb[PRO_PF][C];
+#pragma unroll
+  for (int e = 0; e < PRO_PF; ++e) load_ch<Tin, C>(x + ((long)min(tb + e, t1 - 1) * H + h) * D + c0, xb[e]);
+#pragma unroll
+  for (int e = 0; e < PRO_PF; ++e) {
+    const int t = tb + e;
+    if (t >= t1) break;
     if (t >= se) {  // next (non-empty) sequence: no history
       seq_bounds(cu, N, Tseq, Ttot, t, sa, se);
 #pragma unroll
@@ -113,8 +149,8 @@ __device__ __forceinline__ void prologue_fwd_run(const Tin* __restrict__ x, cons
 #pragma unroll
         for (int i = 0; i < C; ++i) xw[m][i] = 0.f;
     }
-    float xt[C], s[C];
-    load_ch<Tin, C>(x + ((long)t * H + h) * D + c0, xt);
+    float s[C];
+    const float (&xt)[C] = xb[e];
     float ss = 0.f;
 #pragma unroll
     for (int i = 0; i < C; ++i) {
@@ -136,6 +172,7 @@ __device__ __forceinline__ void prologue_fwd_run(const Tin* __restrict__ x, cons
       for (int m = 0; m < PRO_K - 2; ++m) xw[m][i] = xw[m + 1][i];
       xw[PRO_K - 2][i] = xt[i];
     }
+  }
   }
 }
 
@@ -161,13 +198,17 @@ __global__ __launch_bounds__(64 * PRO_WAVES) void k_prologue_fwd(PrologueArgs a)
 template <typename Tin, int D, bool NORM>
 __device__ __forceinline__ void prologue_bwd_run(const Tin* __restrict__ x, const float* __restrict__ w,
                                                  const float* __restrict__ dy, float* __restrict__ dx,
-                                                 float* __restrict__ dwp, const int32_t* __restrict__ cu,
+                                                 float4* dwl, const int32_t* __restrict__ cu,
                                                  int N, int Tseq, int Ttot, int H, int run, float eps) {
   constexpr int C = D / 64;
   const int lane = lane_id(), h = blockIdx.y;
   const int t0 = run * PRO_RUN, t1 = min(t0 + PRO_RUN, Ttot);
-  if (t0 >= Ttot) return;
   const int c0 = lane * C;
+  if (t0 >= Ttot) {  // no run: a zero share of dw
+#pragma unroll
+    for (int i = 0; i < C; ++i) dwl[c0 + i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    return;
+  }
   float wt[C][PRO_K], dw[C][PRO_K];
 #pragma unroll
   for (int i = 0; i < C; ++i)
@@ -198,20 +239,30 @@ __device__ __forceinline__ void prologue_bwd_run(const Tin* __restrict__ x, cons
 #pragma unroll
     for (int m = 0; m < PRO_K - 1; ++m) {
       const int r = t - (PRO_K - 1) + m;
-      if (m < cnt && r >= t0 && r < t1 && r >= sa) {
-        float* p = dx + ((long)r * H + h) * D + c0;
-#pragma unroll
-        for (int i = 0; i < C; ++i) p[i] = acc[m][i];
-      }
+      if (m < cnt && r >= t0 && r < t1 && r >= sa) store_f32<C>(dx + ((long)r * H + h) * D + c0, acc[m]);
     }
   };
   const int tstop = min(t1 + PRO_K - 1, Ttot);
-  int t = t0;
-  for (; t < tstop; ++t) {
+  bool done = false;
+  for (int tb = t0; tb < tstop && !done; tb += PRO_PF) {
+  float xb[PRO_PF][C], gb[PRO_PF][C];
+#pragma unroll
+  for (int e = 0; e < PRO_PF; ++e) {
+    const long row = ((long)min(tb + e, tstop - 1) * H + h) * D + c0;
+    load_ch<Tin, C>(x + row, xb[e]);
+    load_ch<float, C>(dy + row, gb[e]);
+  }
+#pragma unroll
+  for (int e = 0; e < PRO_PF; ++e) {
+    const int t = tb + e;
+    if (t >= tstop) break;
     if (t >= se) {
       // sequence end: its last rows are complete
       flush(t, PRO_K - 1);
-      if (t >= t1) break;  // the rest belongs to later runs
+      if (t >= t1) {  // the rest belongs to later runs
+        done = true;
+        break;
+      }
       seq_bounds(cu, N, Tseq, Ttot, t, sa, se);
 #pragma unroll
       for (int m = 0; m < PRO_K; ++m)
@@ -222,11 +273,9 @@ __device__ __forceinline__ void prologue_bwd_run(const Tin* __restrict__ x, cons
 #pragma unroll
         for (int i = 0; i < C; ++i) xw[m][i] = 0.f;
     }
-    float xt[C], g[C], u[C], sg[C], s[C];
-    load_ch<Tin, C>(x + ((long)t * H + h) * D + c0, xt);
-    const float* gp = dy + ((long)t * H + h) * D + c0;
-#pragma unroll
-    for (int i = 0; i < C; ++i) g[i] = gp[i];
+    float u[C], sg[C], s[C];
+    const float (&xt)[C] = xb[e];
+    const float (&g)[C] = gb[e];
     float ss = 0.f;
 #pragma unroll
     for (int i = 0; i < C; ++i) {
@@ -266,11 +315,7 @@ __device__ __forceinline__ void prologue_bwd_run(const Tin* __restrict__ x, cons
     // row t - 3 has all its terms
     {
       const int r = t - (PRO_K - 1);
-      if (r >= t0 && r < t1 && r >= sa) {
-        float* p = dx + ((long)r * H + h) * D + c0;
-#pragma unroll
-        for (int i = 0; i < C; ++i) p[i] = acc[0][i];
-      }
+      if (r >= t0 && r < t1 && r >= sa) store_f32<C>(dx + ((long)r * H + h) * D + c0, acc[0]);
     }
 #pragma unroll
     for (int i = 0; i < C; ++i) {
@@ -282,41 +327,64 @@ __device__ __forceinline__ void prologue_bwd_run(const Tin* __restrict__ x, cons
       xw[PRO_K - 2][i] = xt[i];
     }
   }
-  // loop ended at t1 + 3, at the end of the tokens, or at a sequence end past
-  // t1: every pending row of this run is complete
-  if (t == tstop) flush(t, PRO_K - 1);
-  // this run's dw share: [run][h][D][K]
-  float* q = dwp + (((long)run * H + h) * D + c0) * PRO_K;
+  }
+  // the walk ended at t1 + 3 or at the end of the tokens (then flush here), or
+  // at a sequence end past t1 (flushed there): every pending row is complete
+  if (!done) flush(tstop, PRO_K - 1);
+  // this run's share of dw, combined with the other waves' in LDS
 #pragma unroll
-  for (int i = 0; i < C; ++i)
-    *reinterpret_cast<float4*>(q + i * PRO_K) = make_float4(dw[i][0], dw[i][1], dw[i][2], dw[i][3]);
+  for (int i = 0; i < C; ++i) dwl[c0 + i] = make_float4(dw[i][0], dw[i][1], dw[i][2], dw[i][3]);
+}
+
+// Sum of the workgroup's wave shares of dw (fixed order) into its partial
+// [block][h][D] (four taps per float4).
+template <int D>
+__device__ __forceinline__ void combine_dw(const float4 (*dws)[256], float* __restrict__ dwp, int H) {
+  float4* out = reinterpret_cast<float4*>(dwp) + ((long)blockIdx.x * H + blockIdx.y) * D;
+  for (int c = threadIdx.x; c < D; c += 64 * PRO_WAVES) {
+    float4 s = dws[0][c];
+#pragma unroll
+    for (int w = 1; w < PRO_WAVES; ++w) {
+      const float4 v = dws[w][c];
+      s = make_float4(s.x + v.x, s.y + v.y, s.z + v.z, s.w + v.w);
+    }
+    out[c] = s;
+  }
 }
 
 template <typename Tin, int DK, int DV>
 __global__ __launch_bounds__(64 * PRO_WAVES) void k_prologue_bwd(PrologueArgs a) {
+  static_assert(DK <= 256 && DV <= 256, "channels per share row");
+  __shared__ float4 dws[PRO_WAVES][256];  // per wave: the four tap sums of each channel
+  // every wave reaches the barrier below (runs past the tokens add zeros)
   const int run = blockIdx.x * PRO_WAVES + wave_id();
   const int z = blockIdx.z;
-  if (run >= a.nruns) return;
+  float4* dwl = dws[wave_id()];
   if (z == 0)
-    prologue_bwd_run<Tin, DK, true>(static_cast<const Tin*>(a.xq), a.wq, a.gq, a.dxq, a.dwpq,
+    prologue_bwd_run<Tin, DK, true>(static_cast<const Tin*>(a.xq), a.wq, a.gq, a.dxq, dwl,
                                     a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.H, run, a.eps);
   else if (z == 1)
-    prologue_bwd_run<Tin, DK, true>(static_cast<const Tin*>(a.xk), a.wk, a.gk, a.dxk, a.dwpk,
+    prologue_bwd_run<Tin, DK, true>(static_cast<const Tin*>(a.xk), a.wk, a.gk, a.dxk, dwl,
                                     a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.H, run, a.eps);
   else
-    prologue_bwd_run<Tin, DV, false>(static_cast<const Tin*>(a.xv), a.wv, a.gv, a.dxv, a.dwpv,
+    prologue_bwd_run<Tin, DV, false>(static_cast<const Tin*>(a.xv), a.wv, a.gv, a.dxv, dwl,
                                      a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.H, run, a.eps);
+  __syncthreads();
+  if (z == 0) combine_dw<DK>(dws, a.dwpq, a.H);
+  else if (z == 1) combine_dw<DK>(dws, a.dwpk, a.H);
+  else combine_dw<DV>(dws, a.dwpv, a.H);
 }
 
-// dw[i] = sum over runs of the partials (fixed order), for q, k and v.
+// dw[i] = sum over the workgroups' partials (fixed order), for q, k and v.
 __global__ __launch_bounds__(256) void k_prologue_dw(PrologueArgs a) {
   const int z = blockIdx.y;
   const long n = (long)a.H * (z == 2 ? a.dv : a.dk) * PRO_K;
   const long i = (long)blockIdx.x * 256 + threadIdx.x;
   if (i >= n) return;
   const float* p = z == 0 ? a.dwpq : (z == 1 ? a.dwpk : a.dwpv);
+  const int nblk = (a.nruns + PRO_WAVES - 1) / PRO_WAVES;
   float s = 0.f;
-  for (int r = 0; r < a.nruns; ++r) s += p[(long)r * n + i];
+  for (int r = 0; r < nblk; ++r) s += p[(long)r * n + i];
   (z == 0 ? a.dwq : (z == 1 ? a.dwk : a.dwv))[i] = s;
 }
 
