@@ -101,3 +101,19 @@ def prologue_bwd(x, w, normalize, dy, *, cu_seqlens=None, eps=EPS):
                     dx[b, a + src] += w[..., j] * du[t]
                     dw[..., j] += du[t] * seg[src]
     return dx, dw
+
+
+def gate_fwd(o, z):
+    """Output gate of the layer (Section 3.4: sigmoid gating): y = o * sigmoid(z), fp64."""
+    o = np.asarray(o, np.float64)
+    z = np.asarray(z, np.float64)
+    return o * _sigmoid(z)
+
+
+def gate_bwd(o, z, dy):
+    """(do, dz) of L = <dy, y>: do = dy sigmoid(z), dz = dy o sigmoid(z) (1 - sigmoid(z))."""
+    o = np.asarray(o, np.float64)
+    z = np.asarray(z, np.float64)
+    dy = np.asarray(dy, np.float64)
+    sg = _sigmoid(z)
+    return dy * sg, dy * o * sg * (1.0 - sg)

@@ -99,3 +99,26 @@ def test_backward_packed_matches_per_sequence():
         assert rel(dxs, dx[:, a:e]) < 1e-14
         dw_sum += dws
     assert rel(dw_sum, dw) < 1e-13
+
+
+def test_gate_matches_definition_and_finite_differences():
+    from oracle.prologue import gate_bwd, gate_fwd
+
+    rng = np.random.default_rng(9)
+    o, z, dy = (rng.standard_normal((2, 5, 3, 4)) for _ in range(3))
+    assert rel(gate_fwd(o, z), o * expit(z)) < 1e-15
+    assert np.all(gate_fwd(o, np.full_like(z, 0.0)) == 0.5 * o)   # sigmoid(0) = 1/2
+    do, dz = gate_bwd(o, z, dy)
+    h = 1e-6
+    fo = (np.sum(dy * gate_fwd(o + h, z)) - np.sum(dy * gate_fwd(o - h, z))) / (2 * h)
+    fz = (np.sum(dy * gate_fwd(o, z + h)) - np.sum(dy * gate_fwd(o, z - h))) / (2 * h)
+    # a uniform shift probes the sum of each gradient
+    assert abs(fo - np.sum(do)) < 1e-7 * max(1.0, abs(fo))
+    assert abs(fz - np.sum(dz)) < 1e-7 * max(1.0, abs(fz))
+    for idx in [(0, 0, 0, 0), (1, 4, 2, 3), (0, 2, 1, 1)]:
+        e = np.zeros_like(z)
+        e[idx] = h
+        fd = (np.sum(dy * gate_fwd(o, z + e)) - np.sum(dy * gate_fwd(o, z - e))) / (2 * h)
+        assert abs(fd - dz[idx]) < 1e-8
+        fd = (np.sum(dy * gate_fwd(o + e, z)) - np.sum(dy * gate_fwd(o - e, z))) / (2 * h)
+        assert abs(fd - do[idx]) < 1e-8
