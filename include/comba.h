@@ -203,6 +203,20 @@ comba_status comba_prologue_bwd(const comba_shape *shape, const void *xq, const 
                                 void *ws, size_t ws_bytes, void *stream);
 
 /*
+ * Output gate of the layer (Section 3.4, sigmoid gating), applied to the
+ * operator's output before the output projection: y = o * sigmoid(z), with o
+ * [B,T,H,dv] fp32 (as comba_chunk_fwd writes it), the gate pre-activation z and
+ * y [B,T,H,dv] in_dtype (bf16 y rounded to nearest even).  Backward from dy
+ * (fp32): do = dy sigmoid(z), dz = dy o sigmoid(z) (1 - sigmoid(z)), both
+ * fp32.  Shape rules of comba_recurrent_fwd (dk is checked but not used).  All
+ * pointers 16-byte aligned; no workspace.
+ */
+comba_status comba_gate_fwd(const comba_shape *shape, const float *o, const void *z, void *y,
+                            void *stream);
+comba_status comba_gate_bwd(const comba_shape *shape, const float *o, const void *z,
+                            const float *dy, float *dout, float *dz, void *stream);
+
+/*
  * Stage timing, for benchmarks (not part of the method).  comba_profile_enable(1)
  * starts a recording session on the calling host thread: every following
  * comba_chunk_fwd / comba_chunk_bwd call on this thread records a HIP event on

@@ -28,6 +28,7 @@ import threading
 
 __all__ = ["comba_chunk_fwd", "comba_chunk_bwd", "comba_chunk_fwd_save", "comba_chunk_bwd_saved",
            "comba_recurrent_fwd", "comba_prologue_fwd", "comba_prologue_bwd",
+           "comba_gate_fwd", "comba_gate_bwd",
            "load_library", "library_path",
            "profile_enable", "profile_read",
            "fwd_workspace_bytes", "bwd_workspace_bytes", "exported_symbols", "CombaError",
@@ -90,6 +91,10 @@ def load_library():
             lib.comba_prologue_bwd.restype = I
             lib.comba_prologue_workspace_bytes.argtypes = [SP]
             lib.comba_prologue_workspace_bytes.restype = Z
+            lib.comba_gate_fwd.argtypes = [SP, P, P, P, P]
+            lib.comba_gate_fwd.restype = I
+            lib.comba_gate_bwd.argtypes = [SP, P, P, P, P, P, P]
+            lib.comba_gate_bwd.restype = I
             lib.comba_profile_enable.argtypes = [I]
             lib.comba_profile_enable.restype = I
             lib.comba_profile_read.argtypes = [P, P, I]
@@ -341,6 +346,44 @@ def comba_prologue_bwd(xq, xk, xv, wq, wk, wv, gq, gk, gv, *, cu_seqlens=None, w
                                   _ptr(workspace), ctypes.c_size_t(workspace.numel()),
                                   ctypes.c_void_p(st)))
     return out
+
+
+def _gate_shape(o, z):
+    import torch
+
+    if not o.is_cuda or o.dtype != torch.float32 or z.shape != o.shape or not o.is_contiguous() \
+            or not z.is_contiguous() or z.device != o.device or \
+            z.dtype not in (torch.bfloat16, torch.float32):
+        raise CombaError("comba: gate takes o (float32) and z (bfloat16 or float32) of one shape")
+    B, T, H, dv = o.shape
+    code = COMBA_BF16 if z.dtype == torch.bfloat16 else COMBA_F32
+    return _make_shape(B, T, H, 64 if dv == 64 else 128, dv, B, None, code)
+
+
+def comba_gate_fwd(o, z, *, stream=None):
+    """Output gate y = o * sigmoid(z); y in the dtype of z."""
+    import torch
+
+    shp = _gate_shape(o, z)
+    y = torch.empty_like(z)
+    st = torch.cuda.current_stream(o.device).cuda_stream if stream is None else stream
+    _check(load_library().comba_gate_fwd(ctypes.byref(shp), _ptr(o), _ptr(z), _ptr(y),
+                                         ctypes.c_void_p(st)))
+    return y
+
+
+def comba_gate_bwd(o, z, dy, *, stream=None):
+    """Backward of the output gate from dy (float32).  Returns (do, dz), float32."""
+    import torch
+
+    shp = _gate_shape(o, z)
+    if dy.shape != o.shape or dy.dtype != torch.float32 or not dy.is_contiguous():
+        raise CombaError("comba: dy must be contiguous float32 of the shape of o")
+    do, dz = torch.empty_like(o), torch.empty(o.shape, dtype=torch.float32, device=o.device)
+    st = torch.cuda.current_stream(o.device).cuda_stream if stream is None else stream
+    _check(load_library().comba_gate_bwd(ctypes.byref(shp), _ptr(o), _ptr(z), _ptr(dy), _ptr(do),
+                                         _ptr(dz), ctypes.c_void_p(st)))
+    return do, dz
 
 
 def _bwd(saved, q, k, v, g, beta, d, h0, dO, dht, cu_seqlens, need_dh0, workspace, stream,

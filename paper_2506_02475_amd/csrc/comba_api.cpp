@@ -435,9 +435,39 @@ comba_status prologue(bool bwd, const comba_shape* shape, const void* xq, const 
   return comba::launch_prologue(a, bwd) == hipSuccess ? COMBA_OK : COMBA_ERR_HIP;
 }
 
+comba_status gate(const comba_shape* shape, const float* o, const void* z, void* y,
+                  const float* dy, float* dout, float* dz, void* stream) {
+  Dims dm;
+  comba_status st = check_shape_recurrent(shape, &dm);
+  if (st != COMBA_OK) return st;
+  const long n = (long)dm.Ttot * dm.H * dm.dv;
+  if (n > 0 && (!o || !z || (dy ? (!dout || !dz) : !y))) return COMBA_ERR_NULL;
+  if (!aligned(o, 16) || !aligned(z, 16) || !aligned(y, 16) || !aligned(dy, 16) ||
+      !aligned(dout, 16) || !aligned(dz, 16))
+    return COMBA_ERR_ALIGN;
+  return comba::launch_gate(dm.bf16, n, o, z, y, dy, dout, dz, static_cast<hipStream_t>(stream)) ==
+                 hipSuccess
+             ? COMBA_OK
+             : COMBA_ERR_HIP;
+}
+
 }  // namespace
 
 extern "C" {
+
+comba_status comba_gate_fwd(const comba_shape* shape, const float* o, const void* z, void* y,
+                            void* stream) {
+  return gate(shape, o, z, y, nullptr, nullptr, nullptr, stream);
+}
+
+comba_status comba_gate_bwd(const comba_shape* shape, const float* o, const void* z,
+                            const float* dy, float* dout, float* dz, void* stream) {
+  if (!dy && shape) {
+    Dims dm;
+    if (check_shape_recurrent(shape, &dm) == COMBA_OK && dm.Ttot > 0) return COMBA_ERR_NULL;
+  }
+  return gate(shape, o, z, nullptr, dy, dout, dz, stream);
+}
 
 size_t comba_prologue_workspace_bytes(const comba_shape* shape) {
   Dims d;

@@ -107,5 +107,8 @@ struct PrologueArgs {
 };
 
 hipError_t launch_prologue(const PrologueArgs& a, bool bwd);
+// Output gate over n elements (n a multiple of 4); forward when dy is NULL.
+hipError_t launch_gate(bool bf16, long n, const float* o, const void* z, void* y, const float* dy,
+                       float* dout, float* dz, hipStream_t st);
 
 }  // namespace comba

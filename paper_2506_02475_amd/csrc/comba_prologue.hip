@@ -417,6 +417,53 @@ static hipError_t dispatch_prologue(const PrologueArgs& a, bool bwd) {
   return hipErrorInvalidValue;
 }
 
+// Output gate (Section 3.4, sigmoid gating): y = o sigmoid(z); backward
+// do = dy sigmoid(z), dz = dy o sigmoid(z) (1 - sigmoid(z)).  Four elements per
+// thread, elementwise over the whole [B, T, H, dv] tensor.
+template <typename Tin>
+__global__ __launch_bounds__(256) void k_gate(const float* __restrict__ o, const Tin* __restrict__ z,
+                                              Tin* __restrict__ y, const float* __restrict__ dy,
+                                              float* __restrict__ dout, float* __restrict__ dz,
+                                              long n4) {
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n4) return;
+  float ov[4], zv[4], sg[4];
+  load_ch<float, 4>(o + 4 * i, ov);
+  load_ch<Tin, 4>(z + 4 * i, zv);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) sg[e] = sigm(zv[e]);
+  if (!dy) {
+    float yv[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) yv[e] = ov[e] * sg[e];
+    store_ch<Tin, 4>(y + 4 * i, yv);
+  } else {
+    float gv[4], a[4], b[4];
+    load_ch<float, 4>(dy + 4 * i, gv);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      a[e] = gv[e] * sg[e];
+      b[e] = a[e] * ov[e] * (1.f - sg[e]);
+    }
+    store_f32<4>(dout + 4 * i, a);
+    store_f32<4>(dz + 4 * i, b);
+  }
+}
+
+hipError_t launch_gate(bool bf16, long n, const float* o, const void* z, void* y, const float* dy,
+                       float* dout, float* dz, hipStream_t st) {
+  const long n4 = n / 4;
+  if (n4 == 0) return hipSuccess;
+  const dim3 grid((unsigned)((n4 + 255) / 256));
+  if (bf16)
+    k_gate<bf16_t><<<grid, 256, 0, st>>>(o, static_cast<const bf16_t*>(z), static_cast<bf16_t*>(y),
+                                         dy, dout, dz, n4);
+  else
+    k_gate<float><<<grid, 256, 0, st>>>(o, static_cast<const float*>(z), static_cast<float*>(y), dy,
+                                        dout, dz, n4);
+  return hipGetLastError();
+}
+
 hipError_t launch_prologue(const PrologueArgs& a, bool bwd) {
   return a.bf16 ? dispatch_prologue<bf16_t>(a, bwd) : dispatch_prologue<float>(a, bwd);
 }

@@ -52,7 +52,7 @@ def test_library_exports_every_declared_symbol():
                              "comba_profile_enable", "comba_profile_read",
                              "comba_chunk_fwd_save", "comba_chunk_bwd_saved",
                              "comba_recurrent_fwd", "comba_prologue_fwd", "comba_prologue_bwd",
-                             "comba_prologue_workspace_bytes"}
+                             "comba_prologue_workspace_bytes", "comba_gate_fwd", "comba_gate_bwd"}
     out = subprocess.run(["nm", "-D", "--defined-only", comba.library_path()],
                          capture_output=True, text=True, check=True).stdout
     exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
@@ -256,6 +256,19 @@ def test_prologue_validates_before_launch():
     assert pro(s, bwd=True, ws_bytes=need - 1) == EWS
     # the chunk length is not used; head dim 256 is accepted (stopped by the alignment check)
     assert pro(shape(chunk=32, dk=256, dv=256), q=FAKE + 8) == EALIGN
+
+
+def test_gate_validates_before_launch():
+    lib = comba.load_library()
+    P = ctypes.c_void_p
+    s = shape()
+    assert lib.comba_gate_fwd(ctypes.byref(s), P(FAKE), None, P(FAKE), None) == ENULL
+    assert lib.comba_gate_fwd(ctypes.byref(s), P(FAKE), P(FAKE), P(FAKE + 4), None) == EALIGN
+    assert lib.comba_gate_bwd(ctypes.byref(s), P(FAKE), P(FAKE), None, P(FAKE), P(FAKE),
+                              None) == ENULL
+    assert lib.comba_gate_bwd(ctypes.byref(s), P(FAKE), P(FAKE), P(FAKE), P(FAKE + 8), P(FAKE),
+                              None) == EALIGN
+    assert lib.comba_gate_fwd(ctypes.byref(shape(dv=96)), P(FAKE), P(FAKE), P(FAKE), None) == ESHAPE
 
 
 def test_saved_pair_validates_like_the_plain_calls():

@@ -104,3 +104,34 @@ def test_prologue_layer_shape():
         dx, dw = prologue_bwd(x, w, norm, g)
         assert maxrel(gr["dx" + n][:, :, heads], dx) <= 1e-5, n
         assert maxrel(gr["dw" + n][heads], dw) <= 1e-5, n
+
+
+@pytest.mark.parametrize("in_dtype,dv,shape", [("bf16", 128, (2, 100, 3)), ("f32", 256, (1, 70, 2)),
+                                               ("bf16", 64, (3, 5, 1)), ("bf16", 128, (4, 4096, 16))],
+                         ids=["bf16_d128", "f32_d256", "bf16_d64_T5", "bf16_layer"])
+def test_gate_parity(in_dtype, dv, shape):
+    import torch
+    import paper_2506_02475_amd as comba
+    from comba_inputs import bf16_round
+    from oracle.prologue import gate_bwd, gate_fwd
+
+    rng = np.random.default_rng(dv + shape[1])
+    B, T, H = shape
+    o = rng.standard_normal((B, T, H, dv), dtype=np.float32)
+    z = 2.0 * rng.standard_normal((B, T, H, dv), dtype=np.float32)
+    dy = rng.standard_normal((B, T, H, dv), dtype=np.float32)
+    if in_dtype == "bf16":
+        z = bf16_round(z)
+    dt = torch.bfloat16 if in_dtype == "bf16" else torch.float32
+    t = lambda x, d=torch.float32: torch.from_numpy(np.ascontiguousarray(x)).to("cuda", d)
+    y = comba.comba_gate_fwd(t(o), t(z, dt))
+    do, dz = comba.comba_gate_bwd(t(o), t(z, dt), t(dy))
+    torch.cuda.synchronize()
+    ref = gate_fwd(o, z)
+    y = y.float().cpu().numpy()
+    if in_dtype == "bf16":
+        assert np.all(np.abs(y - ref) <= 2.0 ** -8 * np.abs(ref) + 1e-6 * np.max(np.abs(ref)))
+    else:
+        assert maxrel(y, ref) <= 1e-5
+    rdo, rdz = gate_bwd(o, z, dy)
+    assert maxrel(do.cpu().numpy(), rdo) <= 1e-5 and maxrel(dz.cpu().numpy(), rdz) <= 1e-5
