@@ -342,11 +342,31 @@ def time_prologue(comba, torch, steps, warmup):
                     "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None,
                     "kernel": st, "avg_launch_ms": round(avg, 4), "algorithmic_bytes": by}
     ms_step = (t1 - t0) * 1e3 / steps
+    # the output gate on the operator's output shape (o fp32, z bf16): stream
+    # events around back-to-back calls
+    n = c["B"] * c["T"] * c["H"] * c["dv"]
+    o = torch.randn(c["B"], c["T"], c["H"], c["dv"], device=dev)
+    z = torch.randn(c["B"], c["T"], c["H"], c["dv"], device=dev).to(torch.bfloat16)
+    dy = torch.randn_like(o)
+    gate = {}
+    for name, fn, by in (("gate_fwd", lambda: comba.comba_gate_fwd(o, z), n * 8.0),
+                         ("gate_bwd", lambda: comba.comba_gate_bwd(o, z, dy), n * 18.0)):
+        for _ in range(warmup):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        gate[name] = {"ms": round(ms, 4), "achieved_GBs": round(by / (ms * 1e-3) / 1e9, 1),
+                      "frac": round(by / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4), "bytes": by}
     return {"value": round(c["B"] * c["T"] / (ms_step * 1e-3), 1), "unit": "tokens/s",
             "ms_per_step": round(ms_step, 4),
             "config": {k_: c[k_] for k_ in ("B", "T", "H", "dk", "dv")},
-            "stages_ms": {n: round(x / steps, 4) for n, x in tot.items()},
-            "roofline": roof["prologue_bwd"], "roofline_fwd": roof["prologue_fwd"]}
+            "stages_ms": {n_: round(x / steps, 4) for n_, x in tot.items()},
+            "roofline": roof["prologue_bwd"], "roofline_fwd": roof["prologue_fwd"], "gate": gate}
 
 
 def cpu_baseline(w, heads_sample, threads):
@@ -418,7 +438,8 @@ def main():
             "data": "synthetic (seeded PCG64, comba_inputs.prologue_case)",
             "config": {"workload": "prologue_b4_t4096_h16_d128", **r["config"]},
             "step": "comba_prologue_fwd + comba_prologue_bwd", "stages_ms": r["stages_ms"],
-            "roofline": r["roofline"], "roofline_fwd": r["roofline_fwd"], "cpu_baseline": None}
+            "roofline": r["roofline"], "roofline_fwd": r["roofline_fwd"], "gate": r["gate"],
+            "cpu_baseline": None}
         print(json.dumps(result), flush=True)
         return
     if args.prefill256:
