@@ -138,6 +138,44 @@ __device__ __forceinline__ void prologue_fwd_run(const Tin* __restrict__ x, cons
   float xb[PRO_PF][C];
 #pragma unroll
   for (int e = 0; e < PRO_PF; ++e) load_ch<Tin, C>(x + ((long)min(tb + e, t1 - 1) * H + h) * D + c0, xb[e]);
+  if (tb + PRO_PF <= t1 && tb + PRO_PF <= se) {
+    // the block lies inside one sequence (the usual case): straight-line code,
+    // so the tokens' independent norm reductions overlap
+    float hx[PRO_K - 1 + PRO_PF][C], sv[PRO_PF][C], ssv[PRO_PF];
+#pragma unroll
+    for (int i = 0; i < C; ++i) {
+#pragma unroll
+      for (int m = 0; m < PRO_K - 1; ++m) hx[m][i] = xw[m][i];
+#pragma unroll
+      for (int e = 0; e < PRO_PF; ++e) hx[PRO_K - 1 + e][i] = xb[e][i];
+    }
+#pragma unroll
+    for (int e = 0; e < PRO_PF; ++e) {
+      ssv[e] = 0.f;
+#pragma unroll
+      for (int i = 0; i < C; ++i) {
+        float u = wt[i][PRO_K - 1] * hx[e + PRO_K - 1][i];
+#pragma unroll
+        for (int m = 0; m < PRO_K - 1; ++m) u = fmaf(wt[i][m], hx[e + m][i], u);
+        sv[e][i] = u * sigm(u);
+        ssv[e] = fmaf(sv[e][i], sv[e][i], ssv[e]);
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < PRO_PF; ++e) {
+      if constexpr (NORM) {
+        const float inv = rsqrtf(wave_sum(ssv[e]) + eps);
+#pragma unroll
+        for (int i = 0; i < C; ++i) sv[e][i] *= inv;
+      }
+      store_ch<Tin, C>(y + ((long)(tb + e) * H + h) * D + c0, sv[e]);
+    }
+#pragma unroll
+    for (int m = 0; m < PRO_K - 1; ++m)
+#pragma unroll
+      for (int i = 0; i < C; ++i) xw[m][i] = hx[PRO_PF + m][i];
+    continue;
+  }
 #pragma unroll
   for (int e = 0; e < PRO_PF; ++e) {
     const int t = tb + e;
