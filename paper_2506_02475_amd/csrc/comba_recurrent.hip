@@ -211,18 +211,30 @@ __global__ __launch_bounds__(64 * NW) void k_recurrent(
   }
 }
 
+template <typename Tin, int DK, int DV, int BV, int NW>
+static hipError_t launch_rec(const RecurrentArgs& a) {
+  k_recurrent<Tin, DK, DV, BV, NW><<<dim3(a.N, a.H, DV / BV), 64 * NW, 0, a.stream>>>(
+      static_cast<const Tin*>(a.q), static_cast<const Tin*>(a.k), static_cast<const Tin*>(a.v),
+      a.g, static_cast<const Tin*>(a.beta), static_cast<const Tin*>(a.beta_tilde), a.d,
+      a.cu_seqlens, a.Tseq, a.Ttot, a.H, a.h0, a.o, a.ht);
+  return hipGetLastError();
+}
+
 template <typename Tin, int DK, int DV>
 static hipError_t run_recurrent(const RecurrentArgs& a) {
   // at most 128 columns per workgroup and 32 rows per wave: 64 state
   // registers per lane (a d = 256 state takes two workgroups of 8 waves)
   constexpr int BV = DV < 128 ? DV : 128, NW = DK <= 128 ? 4 : DK / 32;
   a.stage("recurrent");
-  k_recurrent<Tin, DK, DV, BV, NW><<<dim3(a.N, a.H, DV / BV), 64 * NW, 0, a.stream>>>(
-      static_cast<const Tin*>(a.q), static_cast<const Tin*>(a.k), static_cast<const Tin*>(a.v),
-      a.g, static_cast<const Tin*>(a.beta), static_cast<const Tin*>(a.beta_tilde), a.d,
-      a.cu_seqlens, a.Tseq, a.Ttot, a.H, a.h0, a.o, a.ht);
+  hipError_t e;
+  if ((long)a.N * a.H * (DV / BV) < 1024)
+    // few states (small decoding batches): 32-column slices give four times
+    // the workgroups, so more CUs stream the states
+    e = launch_rec<Tin, DK, DV, 32, DK / 32>(a);  // 32 rows per wave: 4 per lane
+  else
+    e = launch_rec<Tin, DK, DV, BV, NW>(a);
   a.stage(nullptr);
-  return hipGetLastError();
+  return e;
 }
 
 template <typename Tin>

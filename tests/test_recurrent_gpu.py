@@ -70,6 +70,10 @@ CASES = [
     ("f32_T20_dk128_dv256", dict(B=2, T=20, H=2, dk=128, dv=256, in_dtype="f32")),
     ("bf16_varlen_dk256_dv128", dict(T=0, H=2, dk=256, dv=128, in_dtype="bf16",
                                      seqlens=[3, 0, 40])),
+    # at least 1024 state slices: the full-width launch (fewer: 32-column slices)
+    ("decode_f32_d64_wide", dict(B=64, T=1, H=16, dk=64, dv=64, in_dtype="f32")),
+    ("decode_bf16_d256_wide", dict(B=32, T=1, H=16, dk=256, dv=256, in_dtype="bf16")),
+    ("decode_bf16_dk128_dv256_wide", dict(B=32, T=1, H=16, dk=128, dv=256, in_dtype="bf16")),
 ]
 
 
