@@ -33,6 +33,8 @@
  *    pseudocode (Appendix B.1).
  *  - q, k, v, beta, beta_tilde and dO have dtype shape->in_dtype (bf16 or
  *    fp32); g (log alpha), d, states and every output are fp32.
+ *  - Head sizes: dk, dv in {64, 128}; with bf16 inputs also dk, dv in {128, 256}
+ *    (256, the paper's models, for every chunk entry point).  fp32 inputs: 64.
  *  - beta_tilde [B,T,H] may be NULL: beta~ = beta.  The backward's dbeta_tilde
  *    [B,T,H] fp32 may be NULL only when beta_tilde is: dbeta then holds the
  *    total derivative through both roles of beta.  When dbeta_tilde is given,
@@ -83,8 +85,8 @@ typedef struct {
   int32_t B;                  /* batch rows (1 in variable-length mode)                 */
   int32_t T;                  /* tokens per row; packed total in variable-length mode   */
   int32_t H;                  /* heads                                                  */
-  int32_t dk;                 /* key/query head dim: 64 or 128 (64 only for COMBA_F32)  */
-  int32_t dv;                 /* value head dim: 64 or 128 (64 only for COMBA_F32)      */
+  int32_t dk;                 /* key/query head dim: 64, 128, 256 (see above)           */
+  int32_t dv;                 /* value head dim: 64, 128, 256 (see above)               */
   int32_t chunk;              /* chunk length; must be 64                               */
   int32_t num_seqs;           /* N: sequences; must equal B when cu_seqlens == NULL     */
   const int32_t *cu_seqlens;  /* device [N+1] offsets (0 = cu[0] <= ... <= cu[N] = T),

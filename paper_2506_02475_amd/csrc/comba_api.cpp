@@ -21,7 +21,7 @@ struct Dims {
 };
 
 // Validates the shape; fills dims on success.  `wide` also admits head dim 256
-// (bf16 inputs, with 128 or 256 on the other side): the stateless forward only.
+// (bf16 inputs, with 128 or 256 on the other side).
 comba_status check_shape(const comba_shape* s, Dims* out, bool wide = false) {
   if (!s) return COMBA_ERR_NULL;
   if (s->in_dtype != COMBA_F32 && s->in_dtype != COMBA_BF16) return COMBA_ERR_DTYPE;
@@ -243,7 +243,7 @@ comba_status chunk_fwd(bool save, const comba_shape* shape, const void* q, const
                        const float* d, const float* h0, float* o, float* ht, void* ws,
                        size_t ws_bytes, void* stream) {
   Dims dm;
-  comba_status st = check_shape(shape, &dm, !save);
+  comba_status st = check_shape(shape, &dm, true);
   if (st != COMBA_OK) return st;
   // token tensors may be NULL when the call has no tokens (states pass through)
   const bool tok = dm.Ttot > 0;
@@ -282,7 +282,7 @@ comba_status chunk_bwd(bool saved, const comba_shape* shape, const void* q, cons
                        float* dbeta_tilde, float* dd, float* dh0, void* ws, size_t ws_bytes,
                        void* stream) {
   Dims dm;
-  comba_status st = check_shape(shape, &dm);
+  comba_status st = check_shape(shape, &dm, true);
   if (st != COMBA_OK) return st;
   // token tensors may be NULL when the call has no tokens (states pass through)
   const bool tok = dm.Ttot > 0;
@@ -499,7 +499,7 @@ size_t comba_fwd_workspace_bytes(const comba_shape* shape) {
 
 size_t comba_bwd_workspace_bytes(const comba_shape* shape) {
   Dims d;
-  if (check_shape(shape, &d) != COMBA_OK) return 0;
+  if (check_shape(shape, &d, true) != COMBA_OK) return 0;
   return layout(d, true).total;
 }
 

@@ -2451,6 +2451,418 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
 }
 
 // ---------------------------------------------------------------------------
+// k_intra_bwd_wide: the intra-chunk gradients at head dim 256 (dk = 256).  The
+// work of k_intra_bwd_bf in dk / 128 passes over 128-wide slices of dk, so that
+// the LDS tiles and the T1, T2, T3 accumulators keep their dk = 128 size.  Every
+// quantity that spans dk enters the row and column sums linearly (the K K^T and
+// Q K^T terms of E1, E2, BL, the row dots p1, p2, p3, <X, Y>, <k, dQ~>), so each
+// pass adds its part and the sums are combined at the end; dA, dL, <v, dR> and
+// dv do not involve dk and are formed in the first pass.  One workgroup per
+// chunk-head (no persistent loop, no next-item copy).
+// ---------------------------------------------------------------------------
+template <int DK, int DV>
+__global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_wide(
+    const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
+    const bf16_t* __restrict__ dO, const bf16_t* __restrict__ beta,
+    const bf16_t* __restrict__ beta_tilde, const float* __restrict__ d,
+    const ChunkInfo* __restrict__ cmap, int Tfix, int H, const float* __restrict__ Gw,
+    const int16_t* __restrict__ Xq, const float* __restrict__ Xs, const int16_t* __restrict__ Dq,
+    const float* __restrict__ Ds, const int16_t* __restrict__ Yq, const float* __restrict__ Ys,
+    const int16_t* __restrict__ dRq, const float* __restrict__ dRs, float* __restrict__ dq,
+    float* __restrict__ dk, float* __restrict__ dv, float* __restrict__ dbeta,
+    float* __restrict__ dbeta_tilde, float* __restrict__ dg, float* __restrict__ ddp,
+    float* __restrict__ sink) {
+  constexpr int DKP = 128, KP = DK / DKP;
+  static_assert(DK % DKP == 0, "dk slices");
+  using SM = IntraBwdBfSmem<DKP>;
+  constexpr int VB = SM::VB, LDB = SM::LDB, LDK = SM::LDK, LDC = SM::LDC;
+  constexpr int NTW = DKP / 32;
+  constexpr int NW = IB_THR / 64;
+  constexpr int NVB = DV / VB;
+  constexpr int XP = DKP * (VB / 4) / IB_THR;
+  constexpr int NB = DV / 32;
+  static_assert(VB == 32 && NVB % 2 == 0 && CH * 8 == IB_THR, "blocks and pieces");
+  __shared__ __align__(16) char smem[SM::BYTES];
+  __shared__ float Gs[CH], Bs[CH], Bts[CH], rowB[CH];
+  __shared__ float colpart[KP][4][CH];
+  __shared__ float rowacc[KP][2][6][CH];
+  __shared__ float scal[KP][NW][2];
+
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, r16 = lane & 15, g4 = lane >> 4;
+  const int rt = w & 3, ch = w >> 2;
+  const int h = blockIdx.y;
+  const long chh = (long)blockIdx.x * H + h;
+  const ChunkInfo ci = chunk_at(cmap, blockIdx.x, Tfix);
+  if (ci.len <= 0) {
+    if (tid == 0) ddp[chh] = 0.f;
+    return;
+  }
+  const long tok = (long)ci.tok0 * H + h;
+  const int len = ci.len;
+  const float dh = d[h];
+  if (tid < CH) {
+    const long row = tok + (long)min(tid, len - 1) * H;
+    Gs[tid] = Gw[chh * CH + tid];
+    Bs[tid] = tid < len ? bf2f(beta[row]) : 0.f;
+    Bts[tid] = tid < len ? bf2f(beta_tilde[row]) : 0.f;
+  }
+
+  bf16_t* dOb = reinterpret_cast<bf16_t*>(smem);
+  bf16_t* dRh = dOb + CH * LDB;
+  bf16_t* dRl = dRh + CH * LDB;
+  bf16_t* Dh = dRl + CH * LDB;
+  bf16_t* Dl = Dh + CH * LDB;
+  bf16_t* Xh = Dl + CH * LDB;
+  bf16_t* Xl = Xh + DKP * LDB;
+  bf16_t* Yh = Xl + DKP * LDB;
+  bf16_t* Yl = Yh + DKP * LDB;
+  bf16_t* Vb = Yl + DKP * LDB;
+  const int pr = tid >> 3, pc = (tid & 7) * 8, pb = (tid & 7) >> 2;
+  const int pf_r = tid >> 3, pf_c = (tid & 7) * 4;
+  uint4 r_do, r_v;
+  uint2 r_dr, r_d, r_x[XP], r_y[XP];
+  float s_dr, s_d, s_x[XP], s_y[XP];
+  const bf16_t* dO_i = dO + tok * DV;
+  const bf16_t* v_i = v + tok * DV;
+  const int16_t* dRq_i = dRq + chh * NB * CH * VB;
+  const int16_t* Dq_i = Dq + chh * NB * CH * VB;
+  const float* dRs_i = dRs + chh * NB * CH;
+  const float* Ds_i = Ds + chh * NB * CH;
+  const int16_t* Xq_i = Xq + chh * NB * DK * VB;  // [block][dk rows][32]
+  const int16_t* Yq_i = Yq + chh * NB * DK * VB;
+  const float* Xs_i = Xs + chh * NB * DK;
+  const float* Ys_i = Ys + chh * NB * DK;
+  float* dv_i = dv + tok * DV;
+  float* dq_i = dq + tok * DK;
+  float* dk_i = dk + tok * DK;
+  floatx4 dA[2], dL[2];
+  dA[0] = dA[1] = dL[0] = dL[1] = zero4();
+  float bv = 0.f;
+  float4 fdr;
+
+  for (int kh = 0; kh < KP; ++kh) {
+    const int c0 = kh * DKP;  // this pass's dk columns c0 .. c0 + 127
+    auto issue = [&](int vb) {
+      if (vb % 2 == 0) {
+        const unsigned rb = 2u * ((unsigned)min(pr, len - 1) * (H * DV) + vb * VB + pc);
+        r_do = at(reinterpret_cast<const uint4*>(dO_i), rb);
+        r_v = at(reinterpret_cast<const uint4*>(v_i), rb);
+      }
+      const unsigned rr = vb * CH + pf_r;
+      r_dr = at(reinterpret_cast<const uint2*>(dRq_i), 2u * (rr * VB + pf_c));
+      r_d = at(reinterpret_cast<const uint2*>(Dq_i), 2u * (rr * VB + pf_c));
+      s_dr = at(dRs_i, 4u * rr);
+      s_d = at(Ds_i, 4u * rr);
+#pragma unroll
+      for (int p = 0; p < XP; ++p) {
+        const int pc2 = tid + p * IB_THR, xr = pc2 >> 3, xc = (pc2 & 7) * 4;
+        const unsigned xrow = vb * DK + c0 + xr;
+        r_x[p] = at(reinterpret_cast<const uint2*>(Xq_i), 2u * (xrow * VB + xc));
+        r_y[p] = at(reinterpret_cast<const uint2*>(Yq_i), 2u * (xrow * VB + xc));
+        s_x[p] = at(Xs_i, 4u * xrow);
+        s_y[p] = at(Ys_i, 4u * xrow);
+      }
+    };
+    float Fpart = 0.f;
+    auto put = [&](int vb) {
+      const int j = vb * VB;
+      if (pb == (vb & 1)) {
+        *reinterpret_cast<uint4*>(dOb + pr * LDB + (pc & 31)) = r_do;
+        *reinterpret_cast<uint4*>(Vb + pr * LDB + (pc & 31)) = r_v;
+      }
+      bf16x4 hh, ll;
+      fdr = q_unpack4(r_dr, s_dr);
+      split4v(fdr, hh, ll);
+      *reinterpret_cast<bf16x4*>(dRh + pf_r * LDB + pf_c) = hh;
+      *reinterpret_cast<bf16x4*>(dRl + pf_r * LDB + pf_c) = ll;
+      split4v(q_unpack4(r_d, s_d), hh, ll);
+      *reinterpret_cast<bf16x4*>(Dh + pf_r * LDB + pf_c) = hh;
+      *reinterpret_cast<bf16x4*>(Dl + pf_r * LDB + pf_c) = ll;
+#pragma unroll
+      for (int p = 0; p < XP; ++p) {
+        const int pc2 = tid + p * IB_THR, xr = pc2 >> 3, xc = (pc2 & 7) * 4;
+        const float4 fx = q_unpack4(r_x[p], s_x[p]), fy = q_unpack4(r_y[p], s_y[p]);
+        split4v(fx, hh, ll);
+        *reinterpret_cast<bf16x4*>(Xh + xr * LDB + xc) = hh;
+        *reinterpret_cast<bf16x4*>(Xl + xr * LDB + xc) = ll;
+        split4v(fy, hh, ll);
+        *reinterpret_cast<bf16x4*>(Yh + xr * LDB + xc) = hh;
+        *reinterpret_cast<bf16x4*>(Yl + xr * LDB + xc) = ll;
+        Fpart += fx.x * fy.x + fx.y * fy.y + fx.z * fy.z + fx.w * fy.w;
+      }
+      if (kh == 0) {  // dv = Diag(beta) dR, once
+        const float b = Bs[pf_r];
+        const float4 dvv = make_float4(b * fdr.x, b * fdr.y, b * fdr.z, b * fdr.w);
+        float* dst = pf_r < len ? &at(dv_i, 4u * ((unsigned)pf_r * (H * DV) + j + pf_c)) : sink + (tid & 63) * 4;
+        *reinterpret_cast<float4*>(dst) = dvv;
+      }
+    };
+
+    floatx4 T1[NTW], T2[NTW], T3[NTW];
+#pragma unroll
+    for (int j = 0; j < NTW; ++j) T1[j] = T2[j] = T3[j] = zero4();
+    TileRegs<bf16_t, CH, DKP, IB_THR> kr, qr;
+    issue(0);
+#pragma unroll
+    for (int vb = 0; vb < NVB; ++vb) {
+      __syncthreads();
+      put(vb);
+      __syncthreads();
+      if (vb + 1 < NVB) {
+        issue(vb + 1);
+      } else {
+        kr.load_clip(k + tok * DK + c0, (long)H * DK, len);
+        qr.load_clip(q + tok * DK + c0, (long)H * DK, len);
+      }
+      if (kh == 0) {
+        const bf16x4 vv = *reinterpret_cast<const bf16x4*>(Vb + pf_r * LDB + pf_c);
+        bv += (float)vv[0] * fdr.x + (float)vv[1] * fdr.y + (float)vv[2] * fdr.z + (float)vv[3] * fdr.w;
+      }
+      const int arow = (16 * rt + r16) * LDB + 8 * g4;
+      bf16x8 a_do = ld8(dOb + arow);
+      if (16 * rt + r16 >= len) a_do = bf16x8{};
+      const bf16x8 a_drh = ld8(dRh + arow), a_drl = ld8(dRl + arow);
+      const bf16x8 a_dh = ld8(Dh + arow), a_dl = ld8(Dl + arow);
+#pragma unroll
+      for (int j = 0; j < NTW; ++j) {
+        const int brow = (16 * (ch * NTW + j) + r16) * LDB + 8 * g4;
+        const bf16x8 xh = ld8(Xh + brow), xl = ld8(Xl + brow);
+        const bf16x8 yh = ld8(Yh + brow), yl = ld8(Yl + brow);
+        T1[j] = mfma16(a_do, xh, T1[j]);
+        T1[j] = mfma16(a_do, xl, T1[j]);
+        T3[j] = mfma16(a_drh, xh, T3[j]);
+        T3[j] = mfma16(a_drh, xl, T3[j]);
+        T3[j] = mfma16(a_drl, xh, T3[j]);
+        T2[j] = mfma16(a_dh, yh, T2[j]);
+        T2[j] = mfma16(a_dh, yl, T2[j]);
+        T2[j] = mfma16(a_dl, yh, T2[j]);
+      }
+      if (kh == 0) {
+#pragma unroll
+        for (int j2 = 0; j2 < 2; ++j2) {
+          const int brow = (16 * (2 * ch + j2) + r16) * LDB + 8 * g4;
+          const bf16x8 bh = ld8(Dh + brow), bl = ld8(Dl + brow);
+          dA[j2] = mfma16(a_do, bh, dA[j2]);
+          dA[j2] = mfma16(a_do, bl, dA[j2]);
+          dL[j2] = mfma16(a_drh, bh, dL[j2]);
+          dL[j2] = mfma16(a_drh, bl, dL[j2]);
+          dL[j2] = mfma16(a_drl, bh, dL[j2]);
+        }
+      }
+    }
+    if (kh == 0) {
+      bv = sum8(bv);
+      if ((tid & 7) == 0) rowB[pf_r] = bv;
+    }
+    Fpart = wave_sum(Fpart);
+    if (lane == 0) scal[kh][w][0] = Fpart;
+    __syncthreads();
+
+    // ---- phase 2 of the pass ----
+    bf16_t* Ks = reinterpret_cast<bf16_t*>(smem);
+    bf16_t* Qs = Ks + CH * LDK;
+    bf16_t* GTh = Qs + CH * LDK;
+    bf16_t* GTl = GTh + CH * LDC;
+    bf16_t* PTh = GTl + CH * LDC;
+    bf16_t* PTl = PTh + CH * LDC;
+    bf16_t* Ubh = PTl + CH * LDC;
+    bf16_t* Ubl = Ubh + CH * LDC;
+    kr.store(Ks, LDK);
+    qr.store(Qs, LDK);
+    __syncthreads();
+    const float Glast = Gs[CH - 1];
+    {
+      floatx4 akk[2], aqk[2];
+      akk[0] = akk[1] = aqk[0] = aqk[1] = zero4();
+#pragma unroll
+      for (int ks = 0; ks < DKP / 32; ++ks) {
+        const int ar = (16 * rt + r16) * LDK + 32 * ks + 8 * g4;
+        const bf16x8 a_k = ld8(Ks + ar), a_q = ld8(Qs + ar);
+#pragma unroll
+        for (int j2 = 0; j2 < 2; ++j2) {
+          const bf16x8 b = ld8(Ks + (16 * (2 * ch + j2) + r16) * LDK + 32 * ks + 8 * g4);
+          akk[j2] = mfma16(a_k, b, akk[j2]);
+          aqk[j2] = mfma16(a_q, b, aqk[j2]);
+        }
+      }
+      float rE1[4] = {0.f, 0.f, 0.f, 0.f}, rE2[4] = {0.f, 0.f, 0.f, 0.f}, rBL[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j2 = 0; j2 < 2; ++j2) {
+        const int c = 16 * (2 * ch + j2) + r16;
+        float cE = 0.f, dagv[4], pv[4], uv[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = 16 * rt + 4 * g4 + e;
+          const float kk = akk[j2][e];  // this pass's part of k_r . k_c
+          float dag = 0.f, e1 = 0.f, e2 = 0.f, dakk = 0.f;
+          if (r >= c) {
+            const float gam = __expf(Gs[r] - Gs[c]);
+            const float a = (aqk[j2][e] - dh * kk) * gam;
+            const float da = dA[j2][e];
+            e1 = da * a;
+            dag = da * gam;
+          }
+          if (r > c) {
+            const float lc = __expf(Gs[r - 1] - Gs[c]);
+            const float dl = -dL[j2][e];
+            const float lck = lc * kk;
+            e2 = dl * Bts[r] * lck;
+            rBL[e] += dl * lck;
+            dakk = dl * Bts[r] * lc;
+          }
+          dagv[e] = dag;
+          pv[e] = dakk;
+          uv[e] = dakk - dh * dag;
+          rE1[e] += e1;
+          rE2[e] += e2;
+          cE += e1 + e2;
+        }
+        const int toff = c * LDC + 16 * rt + 4 * g4;
+        put_t4(GTh, GTl, toff, dagv);
+        put_t4(PTh, PTl, toff, pv);
+        put_t4(Ubh, Ubl, toff, uv);
+        cE = sum_groups(cE);
+        if (g4 == 0) colpart[kh][rt][c] = cE;
+      }
+      float p1[4] = {0.f, 0.f, 0.f, 0.f}, p2[4] = {0.f, 0.f, 0.f, 0.f}, p3[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < NTW; ++j) {
+        const bf16x4_t k4 = ld_tr4(Ks, LDK, 16 * rt + 4 * g4, 16 * (ch * NTW + j));
+        const bf16x4_t q4 = ld_tr4(Qs, LDK, 16 * rt + 4 * g4, 16 * (ch * NTW + j));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float kv = (float)k4[e];
+          const float qv = (float)q4[e] - dh * kv;
+          p1[e] += T1[j][e] * qv;
+          p2[e] += T2[j][e] * kv;
+          p3[e] += T3[j][e] * kv;
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float s0 = sum16(rE1[e]), s1 = sum16(rE2[e]), s2 = sum16(rBL[e]);
+        const float s3 = sum16(p1[e]), s4 = sum16(p2[e]), s5 = sum16(p3[e]);
+        if (r16 == 0) {
+          const int r = 16 * rt + 4 * g4 + e;
+          rowacc[kh][ch][0][r] = s0;
+          rowacc[kh][ch][1][r] = s1;
+          rowacc[kh][ch][2][r] = s2;
+          rowacc[kh][ch][3][r] = s3;
+          rowacc[kh][ch][4][r] = s4;
+          rowacc[kh][ch][5][r] = s5;
+        }
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int r = 16 * rt + 4 * g4 + e;
+      const float gr = __expf(Gs[r]), dec = __expf(Glast - Gs[r]);
+      const float sr = Bts[r] * __expf(r > 0 ? Gs[r - 1] : 0.f);
+#pragma unroll
+      for (int j = 0; j < NTW; ++j) {
+        T1[j][e] *= gr;
+        T2[j][e] = dec * T2[j][e] - sr * T3[j][e];
+      }
+    }
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const int ar = (16 * rt + r16) * LDC + 32 * ks + 8 * g4;
+      const bf16x8 agh = ld_tr8(GTh, LDC, 32 * ks + 8 * g4, 16 * rt);
+      const bf16x8 agl = ld_tr8(GTl, LDC, 32 * ks + 8 * g4, 16 * rt);
+      const bf16x8 aph = ld_tr8(PTh, LDC, 32 * ks + 8 * g4, 16 * rt);
+      const bf16x8 apl = ld_tr8(PTl, LDC, 32 * ks + 8 * g4, 16 * rt);
+      const bf16x8 ath = ld8(GTh + ar), atl = ld8(GTl + ar);
+      const bf16x8 auh = ld8(Ubh + ar), aul = ld8(Ubl + ar);
+#pragma unroll
+      for (int j = 0; j < NTW; ++j) {
+        const bf16x8 ktb = ld_tr8(Ks, LDK, 32 * ks + 8 * g4, 16 * (ch * NTW + j));
+        const bf16x8 qtb = ld_tr8(Qs, LDK, 32 * ks + 8 * g4, 16 * (ch * NTW + j));
+        T1[j] = mfma16(agh, ktb, T1[j]);
+        T1[j] = mfma16(agl, ktb, T1[j]);
+        T2[j] = mfma16(ath, qtb, T2[j]);
+        T2[j] = mfma16(atl, qtb, T2[j]);
+        T2[j] = mfma16(aph, ktb, T2[j]);
+        T2[j] = mfma16(apl, ktb, T2[j]);
+        T2[j] = mfma16(auh, ktb, T2[j]);
+        T2[j] = mfma16(aul, ktb, T2[j]);
+      }
+    }
+    float ddpart = 0.f;
+#pragma unroll
+    for (int j = 0; j < NTW; ++j) {
+      floatx4 dkv;
+      const bf16x4_t k4 = ld_tr4(Ks, LDK, 16 * rt + 4 * g4, 16 * (ch * NTW + j));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float dqt = T1[j][e];
+        ddpart += (float)k4[e] * dqt;
+        dkv[e] = T2[j][e] - dh * dqt;
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = 16 * rt + 4 * g4 + e;
+        const unsigned off = 4u * ((unsigned)r * (H * DK) + c0 + 16 * (ch * NTW + j) + r16);
+        if (r < len) {
+          at(dq_i, off) = T1[j][e];
+          at(dk_i, off) = dkv[e];
+        }
+      }
+    }
+    ddpart = wave_sum(ddpart);
+    if (lane == 0) scal[kh][w][1] = ddpart;
+    __syncthreads();  // the next pass rewrites the LDS tiles
+  }
+
+  if (w == 0) {
+    const int r = lane;
+    float F = 0.f, dds = 0.f, e1 = 0.f, e2 = 0.f, bl = 0.f, p1 = 0.f, p2 = 0.f, p3 = 0.f, col = 0.f;
+#pragma unroll
+    for (int kh = 0; kh < KP; ++kh) {
+#pragma unroll
+      for (int i = 0; i < NW; ++i) {
+        F += scal[kh][i][0];
+        dds += scal[kh][i][1];
+      }
+#pragma unroll
+      for (int c2 = 0; c2 < 2; ++c2) {
+        e1 += rowacc[kh][c2][0][r];
+        e2 += rowacc[kh][c2][1][r];
+        bl += rowacc[kh][c2][2][r];
+        p1 += rowacc[kh][c2][3][r];
+        p2 += rowacc[kh][c2][4][r];
+        p3 += rowacc[kh][c2][5][r];
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) col += colpart[kh][i][r];
+    }
+    const float Glast = Gs[CH - 1];
+    const float egm = __expf(r > 0 ? Gs[r - 1] : 0.f);
+    const float cr = __expf(Glast - Gs[r]) * p2;
+    const float rowg = e1 + __expf(Gs[r]) * p1 - cr;
+    const float rowgm = e2 - Bts[r] * egm * p3;
+    const float rowbt = bl - egm * p3;
+    const float gcs = wave_sum(cr);
+    const float rowgm_next = shift_down1(rowgm);
+    float dG = rowg - col + (r + 1 < CH ? rowgm_next : 0.f);
+    if (r == CH - 1) dG += gcs + __expf(Glast) * F;
+    float x = __shfl(dG, 63 - lane);
+    x = wave_prefix_sum(x);
+    const float dgr = __shfl(x, 63 - lane);
+    if (r < len) {
+      at(dg + tok, 4u * (r * H)) = dgr;
+      if (dbeta_tilde) {
+        at(dbeta + tok, 4u * (r * H)) = rowB[r];
+        at(dbeta_tilde + tok, 4u * (r * H)) = rowbt;
+      } else {
+        at(dbeta + tok, 4u * (r * H)) = rowB[r] + rowbt;
+      }
+    }
+    if (lane == 0) ddp[chh] = -dds;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // host launchers
 // ---------------------------------------------------------------------------
 // Compute units of the current device (0 when the query fails).
@@ -2608,10 +3020,18 @@ static hipError_t run_bwd_bf(const LaunchArgs& a) {
       q, k, dO, bt, a.d, a.dht, a.smap, Tfix, a.H, a.MTq, a.MTs, a.ATq, a.ATs, a.QTp, a.Gw, a.dh0, a.Yq,
       a.Ys, a.dRq, a.dRs, a.sink);
   a.stage("intra_bwd");
-  if (a.ncmax > 0)
-    k_intra_bwd_bf<DK, DV><<<dim3(intra_bwd_grid((long)a.ncmax * a.H)), IB_THR, 0, st>>>(
-        q, k, v, dO, beta, bt, a.d, a.cmap, Tfix, a.H, a.Gw, a.Xq, a.Xs, a.Dq, a.Ds, a.Yq, a.Ys, a.dRq,
-        a.dRs, a.ncmax, a.dq, a.dk_, a.dv_, a.dbeta, a.dbeta_tilde, a.dg, a.ddp, a.sink);
+  if constexpr (DK > 128) {
+    // head dim 256: two passes of 128 dk columns, one workgroup per chunk-head
+    if (a.ncmax > 0)
+      k_intra_bwd_wide<DK, DV><<<dim3(a.ncmax, a.H), IB_THR, 0, st>>>(
+          q, k, v, dO, beta, bt, a.d, a.cmap, Tfix, a.H, a.Gw, a.Xq, a.Xs, a.Dq, a.Ds, a.Yq, a.Ys,
+          a.dRq, a.dRs, a.dq, a.dk_, a.dv_, a.dbeta, a.dbeta_tilde, a.dg, a.ddp, a.sink);
+  } else {
+    if (a.ncmax > 0)
+      k_intra_bwd_bf<DK, DV><<<dim3(intra_bwd_grid((long)a.ncmax * a.H)), IB_THR, 0, st>>>(
+          q, k, v, dO, beta, bt, a.d, a.cmap, Tfix, a.H, a.Gw, a.Xq, a.Xs, a.Dq, a.Ds, a.Yq, a.Ys, a.dRq,
+          a.dRs, a.ncmax, a.dq, a.dk_, a.dv_, a.dbeta, a.dbeta_tilde, a.dg, a.ddp, a.sink);
+  }
   a.stage("reduce_dd");
   k_reduce_dd<<<a.H, NTHR, 0, st>>>(a.ddp, a.ncmax, a.H, a.dd);
   a.stage(nullptr);
@@ -2624,15 +3044,10 @@ static hipError_t dispatch_bf(const LaunchArgs& a) {
   if (a.dk == 128 && a.dv == 128) return BWD ? run_bwd_bf<128, 128>(a) : run_fwd_bf<128, 128>(a);
   if (a.dk == 64 && a.dv == 128) return BWD ? run_bwd_bf<64, 128>(a) : run_fwd_bf<64, 128>(a);
   if (a.dk == 128 && a.dv == 64) return BWD ? run_bwd_bf<128, 64>(a) : run_fwd_bf<128, 64>(a);
-  if constexpr (!BWD) {
-    // head dim 256 (the paper's models): the stateless forward only (inference
-    // prefill); the host rejects the backward and the saved pair at this size
-    if (!a.saved) {
-      if (a.dk == 256 && a.dv == 256) return run_fwd_bf<256, 256>(a);
-      if (a.dk == 128 && a.dv == 256) return run_fwd_bf<128, 256>(a);
-      if (a.dk == 256 && a.dv == 128) return run_fwd_bf<256, 128>(a);
-    }
-  }
+  // head dim 256 (the paper's models)
+  if (a.dk == 256 && a.dv == 256) return BWD ? run_bwd_bf<256, 256>(a) : run_fwd_bf<256, 256>(a);
+  if (a.dk == 128 && a.dv == 256) return BWD ? run_bwd_bf<128, 256>(a) : run_fwd_bf<128, 256>(a);
+  if (a.dk == 256 && a.dv == 128) return BWD ? run_bwd_bf<256, 128>(a) : run_fwd_bf<256, 128>(a);
   return hipErrorInvalidValue;
 }
 

@@ -205,19 +205,21 @@ def test_recurrent_validates_before_launch():
     assert rec(shape(T=0), d=None, **none) == ENULL
 
 
-def test_head256_forward_only():
-    # head dim 256 (bf16): the stateless forward is accepted (a misaligned o
-    # shows the shape passed), the backward and the saved pair are not
+def test_head256_accepted_by_every_chunk_call():
+    # head dim 256 (bf16): every chunk entry point accepts it (a misaligned
+    # output shows the shape passed; nothing is launched)
     for dk, dv in ((256, 256), (128, 256), (256, 128)):
         s = shape(dk=dk, dv=dv)
         assert comba.fwd_workspace_bytes(1, 128, 2, dk, dv) > 0
-        assert comba.bwd_workspace_bytes(1, 128, 2, dk, dv) == 0
+        assert comba.bwd_workspace_bytes(1, 128, 2, dk, dv) > 0
         assert fwd(s, o=FAKE + 4) == EALIGN
-        assert bwd(s) == ESHAPE
+        assert bwd(s, dq=FAKE + 4) == EALIGN
         lib = comba.load_library()
         P = ctypes.c_void_p
-        assert lib.comba_chunk_fwd_save(ctypes.byref(s), *[P(FAKE)] * 10, P(FAKE),
-                                        ctypes.c_size_t(1 << 40), None) == ESHAPE
+        args = [P(FAKE)] * 10
+        args[8] = P(FAKE + 4)  # o
+        assert lib.comba_chunk_fwd_save(ctypes.byref(s), *args, P(FAKE),
+                                        ctypes.c_size_t(1 << 40), None) == EALIGN
     assert fwd(shape(dk=64, dv=256)) == ESHAPE
     assert fwd(shape(dk=256, dv=256, dtype=comba.COMBA_F32)) == ESHAPE
 

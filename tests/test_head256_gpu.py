@@ -59,16 +59,41 @@ def test_forward_head256_agrees_with_recurrent():
     assert maxrel(h_c.cpu().numpy(), h_r.cpu().numpy()) <= 2e-3
 
 
-def test_head256_backward_is_rejected():
-    import paper_2506_02475_amd as comba
+BWD_CASES = [
+    ("d256_T200", dict(B=1, T=200, H=2, dk=256, dv=256)),
+    ("dk128_dv256", dict(B=2, T=130, H=1, dk=128, dv=256)),
+    ("dk256_dv128", dict(B=1, T=129, H=2, dk=256, dv=128)),
+    ("d256_varlen", dict(T=0, H=2, dk=256, dv=256, seqlens=[1, 64, 0, 70])),
+]
 
-    w = random_case(seed=62, B=1, T=64, H=1, dk=256, dv=256, in_dtype="bf16")
+
+@pytest.mark.parametrize("name,kw", BWD_CASES, ids=[c[0] for c in BWD_CASES])
+def test_backward_head256(name, kw):
+    from gpu_helpers import check_bwd
+
+    w = random_case(seed=zlib.crc32(name.encode()) % 1000 + 19, dht=True, in_dtype="bf16", **kw)
+    _log("head256 bwd %s %s" % (name, check_bwd(w)))
+
+
+def test_head256_saved_pair_and_beta_tilde():
+    import torch
+    import paper_2506_02475_amd as comba
+    from comba_inputs import attach_beta_tilde
+
+    w = attach_beta_tilde(random_case(seed=62, B=2, T=150, H=2, dk=256, dv=256,
+                                      in_dtype="bf16", dht=True), "b_beta", seed=3)
     a = to_device(w)
     args = (a["q"], a["k"], a["v"], a["g"], a["beta"], a["d"], a["h0"])
-    with pytest.raises(comba.CombaError, match="shape"):
-        comba.comba_chunk_bwd(*args, a["dO"])
-    with pytest.raises(comba.CombaError, match="shape"):
-        comba.comba_chunk_fwd_save(*args)
+    o_s, ht_s, ws = comba.comba_chunk_fwd_save(*args, beta_tilde=a["beta_tilde"])
+    gr_s = comba.comba_chunk_bwd_saved(*args, a["dO"], a["dht"], workspace=ws,
+                                       beta_tilde=a["beta_tilde"])
+    gr = comba.comba_chunk_bwd(*args, a["dO"], a["dht"], beta_tilde=a["beta_tilde"])
+    torch.cuda.synchronize()
+    for key in gr:
+        assert torch.equal(gr_s[key], gr[key]), key
+    ref = oracle.workload_bwd(w)
+    for key in ("dq", "dk", "dv", "dg", "dbeta", "dbeta_tilde", "dd", "dh0"):
+        assert maxrel(gr_s[key].cpu().numpy(), ref[key]) <= 2e-3, key
 
 
 def test_prefill_head256_layer_shape():
