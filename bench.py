@@ -231,6 +231,60 @@ def time_decode(comba, torch, steps, warmup, threads=None, with_cpu=False):
 PREFILL256 = dict(B=4, T=4096, H=8, dk=256, dv=256, seed=63)
 
 
+def time_train256(comba, torch, steps, warmup):
+    """Training pair (comba_chunk_fwd_save + comba_chunk_bwd_saved) at head dim 256:
+    B4 T4096 H8 d256 bf16.  Per-stage live timing; roofline of the dominant stage."""
+    import numpy as np
+    from comba_inputs import random_case
+
+    c = PREFILL256
+    w = random_case(seed=c["seed"] + 1, B=c["B"], T=c["T"], H=c["H"], dk=c["dk"], dv=c["dv"],
+                    in_dtype="bf16", grad=True)
+    dev = torch.device("cuda:0")
+    bf = torch.bfloat16
+
+    def t(x, dt=torch.float32):
+        return torch.from_numpy(np.ascontiguousarray(x)).to(dev, dt)
+
+    q, k, v, g, beta, d, h0, dO = (t(w.q, bf), t(w.k, bf), t(w.v, bf), t(w.g), t(w.beta, bf),
+                                   t(w.d), t(w.h0), t(w.dO, bf))
+    B, T, H, dk, dv = c["B"], c["T"], c["H"], c["dk"], c["dv"]
+    ws = torch.empty(comba.bwd_workspace_bytes(B, T, H, dk, dv), dtype=torch.uint8, device=dev)
+
+    def step():
+        comba.comba_chunk_fwd_save(q, k, v, g, beta, d, h0, workspace=ws)
+        return comba.comba_chunk_bwd_saved(q, k, v, g, beta, d, h0, dO, None, workspace=ws)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    comba.profile_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    marks = comba.profile_read()
+    comba.profile_enable(False)
+    tot, cnt = {}, {}
+    for name, ms in marks:
+        tot[name] = tot.get(name, 0.0) + ms
+        cnt[name] = cnt.get(name, 0) + 1
+    dom = max(tot, key=tot.get)
+    fl, by = stage_model(dom, B, T, H, dk, dv)
+    avg = tot[dom] / cnt[dom]
+    ach = by / (avg * 1e-3) / 1e9
+    ms_step = (t1 - t0) * 1e3 / steps
+    return {"value": round(B * T / (ms_step * 1e-3), 1), "unit": "tokens/s",
+            "ms_per_step": round(ms_step, 4),
+            "config": {k_: c[k_] for k_ in ("B", "T", "H", "dk", "dv")},
+            "stages_ms": {n: round(x / steps, 4) for n, x in tot.items()},
+            "roofline": {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
+                         "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None,
+                         "kernel": dom, "avg_launch_ms": round(avg, 4), "algorithmic_bytes": by,
+                         "algorithmic_flops": fl}}
+
+
 def time_prefill256(comba, torch, steps, warmup):
     """Inference prefill at head dim 256 (the paper's models): the stateless
     comba_chunk_fwd over B4 T4096 with 8 heads of 256 (a 1.3B-model layer with
@@ -402,6 +456,8 @@ def main():
     ap.add_argument("--prefill256", action="store_true",
                     help="time the inference prefill at head dim 256 (comba_chunk_fwd, B4 T4096 "
                          "H8 d256) as the headline")
+    ap.add_argument("--train256", action="store_true",
+                    help="time the training pair at head dim 256 (B4 T4096 H8 d256) as the headline")
     ap.add_argument("--prologue", action="store_true",
                     help="time the layer input prologue (short conv, SiLU, L2 norm; fwd + bwd) "
                          "on the 1.3B layer's q, k, v as the headline")
@@ -426,6 +482,20 @@ def main():
         threads = len(os.sched_getaffinity(0))
     except Exception:
         threads = os.cpu_count() or 1
+    if args.train256:
+        torch.cuda.set_device(0)
+        r = time_train256(comba, torch, args.steps, args.warmup)
+        result = {
+            "metric": "Comba fwd+bwd tokens/s at B=4,T=4096,H=8,d=256 bf16 (training pair)",
+            "value": r["value"], "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": r["ms_per_step"], "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+            "data": "synthetic (seeded PCG64, comba_inputs.random_case)",
+            "config": {"workload": "train_b4_t4096_h8_d256", **r["config"]},
+            "step": "comba_chunk_fwd_save + comba_chunk_bwd_saved", "stages_ms": r["stages_ms"],
+            "roofline": r["roofline"], "cpu_baseline": None}
+        print(json.dumps(result), flush=True)
+        return
     if args.prologue:
         torch.cuda.set_device(0)
         r = time_prologue(comba, torch, args.steps, args.warmup)
@@ -629,6 +699,8 @@ def main():
                                                                          args.steps, args.warmup)
         result["variants"]["prologue_b4_t4096_h16_d128"] = time_prologue(comba, torch,
                                                                          args.steps, args.warmup)
+        result["variants"]["train_b4_t4096_h8_d256"] = time_train256(comba, torch, args.steps,
+                                                                     args.warmup)
     if args.copy_bytes > 0:
         n = args.copy_bytes // 4
         src = torch.ones(n, dtype=torch.float32, device=dev)

@@ -2603,7 +2603,9 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_wide(
     for (int j = 0; j < NTW; ++j) T1[j] = T2[j] = T3[j] = zero4();
     TileRegs<bf16_t, CH, DKP, IB_THR> kr, qr;
     issue(0);
-#pragma unroll
+    // one block per iteration: unrolled, the blocks of dv = 256 keep too many
+    // loaded pieces live and spill
+#pragma unroll 1
     for (int vb = 0; vb < NVB; ++vb) {
       __syncthreads();
       put(vb);

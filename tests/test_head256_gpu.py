@@ -112,3 +112,25 @@ def test_prefill_head256_layer_shape():
             "ht": maxrel(ht.cpu().numpy()[:, heads], rht)}
     _log("prefill B4 T4096 H8 d256 %s" % errs)
     assert max(errs.values()) <= 2e-3
+
+
+def test_train_head256_layer_shape():
+    # the training pair at B4 T4096 H8 d256 (the bench's d = 256 leg), sampled
+    # heads against the oracle
+    import torch
+    import paper_2506_02475_amd as comba
+
+    w = random_case(seed=64, B=4, T=4096, H=8, dk=256, dv=256, in_dtype="bf16", dht=True)
+    a = to_device(w)
+    args = (a["q"], a["k"], a["v"], a["g"], a["beta"], a["d"], a["h0"])
+    o, ht, ws = comba.comba_chunk_fwd_save(*args)
+    gr = comba.comba_chunk_bwd_saved(*args, a["dO"], a["dht"], workspace=ws)
+    torch.cuda.synchronize()
+    heads = [2, 5]
+    ref = oracle.workload_bwd(w, heads=heads)
+    errs = {n: maxrel(gr[n].cpu().numpy()[:, :, heads], ref[n])
+            for n in ("dq", "dk", "dv", "dg", "dbeta")}
+    errs["dd"] = maxrel(gr["dd"].cpu().numpy()[heads], ref["dd"])
+    errs["dh0"] = maxrel(gr["dh0"].cpu().numpy()[:, heads], ref["dh0"])
+    _log("train B4 T4096 H8 d256 %s" % errs)
+    assert max(errs.values()) <= 2e-3
