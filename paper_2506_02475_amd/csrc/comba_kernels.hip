@@ -3022,8 +3022,9 @@ static hipError_t run_bwd_bf(const LaunchArgs& a) {
       q, k, dO, bt, a.d, a.dht, a.smap, Tfix, a.H, a.MTq, a.MTs, a.ATq, a.ATs, a.QTp, a.Gw, a.dh0, a.Yq,
       a.Ys, a.dRq, a.dRs, a.sink);
   a.stage("intra_bwd");
-  if constexpr (DK > 128) {
-    // head dim 256: two passes of 128 dk columns, one workgroup per chunk-head
+  if constexpr (DK > 128 || DV > 128) {
+    // head dim 256: passes of 128 dk columns, one workgroup per chunk-head (at
+    // dv = 256 the persistent kernel spills; this one is 25% faster there)
     if (a.ncmax > 0)
       k_intra_bwd_wide<DK, DV><<<dim3(a.ncmax, a.H), IB_THR, 0, st>>>(
           q, k, v, dO, beta, bt, a.d, a.cmap, Tfix, a.H, a.Gw, a.Xq, a.Xs, a.Dq, a.Ds, a.Yq, a.Ys,
