@@ -1,11 +1,13 @@
-"""GPU parity of the chunk-wise forward at head dimension 256.
+"""GPU parity of the chunk-wise path at head dimension 256.
 
 The paper's models keep the head dimension at 256 (Section 2, to match the
-state size of Mamba2).  At that size the library serves inference: the
-stateless chunk forward (prefill; comba_chunk_fwd) and the token-by-token
-decoding step (comba_recurrent_fwd, covered with the other recurrent tests).
-Compared element by element with the fp64 oracle at the bf16 bar (2e-3,
-norm-wise max relative error)."""
+state size of Mamba2).  Covered here: the stateless forward (prefill), the
+backward (pass-wise intra-chunk kernel), the saved training pair with a
+separate beta~, mixed 128/256 head sizes, packed sequences, and the
+B4 T4096 H8 d256 layer on sampled heads; the token-by-token decoding step at
+d = 256 is covered with the other recurrent tests.  Compared element by
+element with the fp64 oracle at the bf16 bar (2e-3, norm-wise max relative
+error)."""
 import zlib
 
 import numpy as np
