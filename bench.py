@@ -173,7 +173,7 @@ def time_decode(comba, torch, steps, warmup, threads=None, with_cpu=False):
     # per-call checks, which would otherwise leave the GPU waiting between calls
     import ctypes
     lib = comba.load_library()
-    shp = comba.CombaShape(c["B"], 1, c["H"], c["dk"], c["dv"], comba.CHUNK, c["B"], None,
+    shp = comba.CombaShape(c["B"], 1, c["H"], c["dk"], c["dv"], comba.CHUNK, c["B"], None, None,
                            comba.COMBA_BF16)
     o = torch.empty((c["B"], 1, c["H"], c["dv"]), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream(dev)

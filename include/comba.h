@@ -20,10 +20,10 @@
  * states no backward).
  *
  * Conventions shared by every entry point
- *  - `shape` points to host memory; every other pointer (including
- *    shape->cu_seqlens) is a DEVICE pointer on the current HIP device.  The
- *    caller owns every buffer; the library allocates nothing and keeps no state
- *    between calls.
+ *  - `shape` (and shape->cu_seqlens_host) points to host memory; every other
+ *    pointer (including shape->cu_seqlens) is a DEVICE pointer on the current
+ *    HIP device.  The caller owns every buffer; the library allocates nothing
+ *    and keeps no state between calls.
  *  - Layouts are C-contiguous.  Token-major tensors are [B, T, H, D]; in the
  *    variable-length mode B == 1, T is the packed token count and sequence s
  *    covers tokens [cu_seqlens[s], cu_seqlens[s+1]).  A sequence's last chunk
@@ -47,15 +47,25 @@
  *    the default stream).  Argument errors are detected before any launch and
  *    then nothing is written.  A failed launch returns COMBA_ERR_HIP.
  *  - Alignment: q, k, v, dO and every fp32 tensor whose last dimension is dk
-    or dv (h0, ht, o, dht, dh0, dq, dk, dv) need 16 bytes, the workspace 256
-    bytes, the other fp32 tensors 4 bytes and beta, beta_tilde their element size; any other
-    pointer is rejected with COMBA_ERR_ALIGN.
-  - Outputs must not alias inputs (the one exception: ht == h0 in comba_recurrent_fwd);
-    outputs are overwritten, never accumulated.
-  - A call without tokens (T == 0 or B == 0) is valid: the per-token tensors
-    (q, k, v, g, beta, o, dO, dq, dk, dv, dg, dbeta, dbeta_tilde) may then be NULL, and the
-    states pass through (ht = h0, dh0 = dht, dd = 0).  Empty sequences inside a
-    packed batch behave the same way for their own states.
+ *    or dv (h0, ht, o, dht, dh0, dq, dk, dv) need 16 bytes, the workspace 256
+ *    bytes, the other fp32 tensors 4 bytes and beta, beta_tilde their element
+ *    size; any other pointer is rejected with COMBA_ERR_ALIGN.
+ *  - Outputs must not alias inputs (the one exception: ht == h0 in
+ *    comba_recurrent_fwd); outputs are overwritten, never accumulated.
+ *  - A call without tokens (T == 0 or B == 0) is valid: the per-token tensors
+ *    (q, k, v, g, beta, o, dO, dq, dk, dv, dg, dbeta, dbeta_tilde) may then be
+ *    NULL, and the states pass through (ht = h0, dh0 = dht, dd = 0).  Empty
+ *    sequences inside a packed batch behave the same way for their own states.
+ *  - Variable-length offsets: when shape->cu_seqlens_host (a HOST copy of the
+ *    same N + 1 offsets) is given, every entry point checks
+ *    0 = cu[0] <= cu[1] <= ... <= cu[N] = T on it and returns COMBA_ERR_SHAPE
+ *    before any launch when it fails.  Without the host copy the device
+ *    offsets are trusted: malformed ones are clamped into [0, T] on the device
+ *    (never an out-of-bounds access), and the outputs are then undefined.
+ *  - Non-finite inputs propagate: a NaN or Inf in q, k, v, dO (or the
+ *    states) makes the affected outputs and gradients of its sequence and
+ *    head non-finite; other sequences and heads are unaffected (dd sums over
+ *    all sequences of a head and so takes it up too).
  *  - Calls on different streams with distinct workspaces may run concurrently;
  *    a workspace must not be shared by calls that overlap in time.
  */
@@ -91,6 +101,9 @@ typedef struct {
   int32_t num_seqs;           /* N: sequences; must equal B when cu_seqlens == NULL     */
   const int32_t *cu_seqlens;  /* device [N+1] offsets (0 = cu[0] <= ... <= cu[N] = T),
                                  or NULL for fixed-length rows                           */
+  const int32_t *cu_seqlens_host; /* optional HOST copy of the same offsets, or NULL:
+                                 when given, checked before any launch (COMBA_ERR_SHAPE
+                                 on a malformed table; requires cu_seqlens)              */
   comba_dtype in_dtype;       /* dtype of q, k, v, beta, beta_tilde, dO                 */
 } comba_shape;
 

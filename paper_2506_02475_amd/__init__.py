@@ -53,7 +53,7 @@ class CombaShape(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int32), ("T", ctypes.c_int32), ("H", ctypes.c_int32),
                 ("dk", ctypes.c_int32), ("dv", ctypes.c_int32), ("chunk", ctypes.c_int32),
                 ("num_seqs", ctypes.c_int32), ("cu_seqlens", ctypes.c_void_p),
-                ("in_dtype", ctypes.c_int)]
+                ("cu_seqlens_host", ctypes.c_void_p), ("in_dtype", ctypes.c_int)]
 
 
 def library_path() -> str:
@@ -138,8 +138,33 @@ def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
-def _make_shape(B, T, H, dk, dv, N, cu_ptr, dtype_code, chunk=CHUNK):
-    return CombaShape(B, T, H, dk, dv, chunk, N, cu_ptr, dtype_code)
+def _make_shape(B, T, H, dk, dv, N, cu_ptr, dtype_code, chunk=CHUNK, cu_host=None):
+    """The C shape struct.  ``cu_host`` is a host int32 array of the offsets (a
+    numpy array or a CPU tensor, kept alive by the caller for the call); the
+    library then rejects a malformed offset table before any launch."""
+    hp = None
+    if cu_host is not None:
+        hp = ctypes.c_void_p(cu_host.ctypes.data if hasattr(cu_host, "ctypes")
+                             else cu_host.data_ptr())
+    shp = CombaShape(B, T, H, dk, dv, chunk, N, cu_ptr, hp, dtype_code)
+    shp._keep = cu_host  # the host offsets live as long as the struct
+    return shp
+
+
+def _host_offsets(cu_seqlens_host, n):
+    """A contiguous host int32 copy of the offsets (or None), checked for length."""
+    if cu_seqlens_host is None:
+        return None
+    import numpy as np
+
+    if hasattr(cu_seqlens_host, "detach"):  # torch tensor
+        if cu_seqlens_host.is_cuda:
+            raise CombaError("comba: cu_seqlens_host must be in host memory")
+        cu_seqlens_host = cu_seqlens_host.detach().numpy()
+    a = np.ascontiguousarray(np.asarray(cu_seqlens_host), dtype=np.int32)
+    if a.ndim != 1 or a.size != n:
+        raise CombaError("comba: cu_seqlens_host must hold the N + 1 offsets of cu_seqlens")
+    return a
 
 
 def fwd_workspace_bytes(B, T, H, dk, dv, *, num_seqs=None, varlen=False, bf16=True) -> int:
@@ -156,7 +181,7 @@ def bwd_workspace_bytes(B, T, H, dk, dv, *, num_seqs=None, varlen=False, bf16=Tr
     return int(load_library().comba_bwd_workspace_bytes(ctypes.byref(shp)))
 
 
-def _prepare(q, k, v, g, beta, d, h0, cu_seqlens, extra=()):
+def _prepare(q, k, v, g, beta, d, h0, cu_seqlens, extra=(), cu_seqlens_host=None):
     import torch
 
     if not q.is_cuda:
@@ -190,10 +215,13 @@ def _prepare(q, k, v, g, beta, d, h0, cu_seqlens, extra=()):
             raise CombaError("comba: cu_seqlens must be contiguous int32 on the device, B == 1")
         N = cu_seqlens.numel() - 1
     else:
+        if cu_seqlens_host is not None:
+            raise CombaError("comba: cu_seqlens_host needs cu_seqlens")
         N = B
     if h0 is not None and (h0.dtype != torch.float32 or tuple(h0.shape) != (N, H, dk, dv)):
         raise CombaError("comba: h0 must be float32 [N,H,dk,dv]")
-    shp = _make_shape(B, T, H, dk, dv, N, _ptr(cu_seqlens), code)
+    shp = _make_shape(B, T, H, dk, dv, N, _ptr(cu_seqlens), code,
+                      cu_host=_host_offsets(cu_seqlens_host, N + 1))
     return shp, (B, T, H, dk, dv, N)
 
 
@@ -206,12 +234,13 @@ def _beta_tilde(beta_tilde, beta):
 
 
 def _fwd(save, q, k, v, g, beta, d, h0, cu_seqlens, output_final_state, workspace, stream,
-         beta_tilde):
+         beta_tilde, cu_seqlens_host=None):
     import torch
 
     lib = load_library()
     shp, (B, T, H, dk, dv, N) = _prepare(q, k, v, g, beta, d, h0, cu_seqlens,
-                                         extra=_beta_tilde(beta_tilde, beta))
+                                         extra=_beta_tilde(beta_tilde, beta),
+                                         cu_seqlens_host=cu_seqlens_host)
     o = torch.empty((B, T, H, dv), dtype=torch.float32, device=q.device)
     ht = torch.empty((N, H, dk, dv), dtype=torch.float32, device=q.device) \
         if output_final_state else None
@@ -230,25 +259,30 @@ def _fwd(save, q, k, v, g, beta, d, h0, cu_seqlens, output_final_state, workspac
 
 
 def comba_chunk_fwd(q, k, v, g, beta, d, h0=None, *, beta_tilde=None, cu_seqlens=None,
-                    output_final_state=True, workspace=None, stream=None):
-    """Chunk-wise forward.  Returns (o [B,T,H,dv] fp32, ht [N,H,dk,dv] fp32 or None)."""
+                    cu_seqlens_host=None, output_final_state=True, workspace=None, stream=None):
+    """Chunk-wise forward.  Returns (o [B,T,H,dv] fp32, ht [N,H,dk,dv] fp32 or None).
+
+    ``cu_seqlens_host`` (optional, every entry point): a host copy of the
+    offsets (numpy array or CPU tensor); the library then rejects a malformed
+    table with a shape error before any launch."""
     o, ht, _ = _fwd(False, q, k, v, g, beta, d, h0, cu_seqlens, output_final_state, workspace,
-                    stream, beta_tilde)
+                    stream, beta_tilde, cu_seqlens_host)
     return o, ht
 
 
 def comba_chunk_fwd_save(q, k, v, g, beta, d, h0=None, *, beta_tilde=None, cu_seqlens=None,
-                         output_final_state=True, workspace=None, stream=None):
+                         cu_seqlens_host=None, output_final_state=True, workspace=None,
+                         stream=None):
     """Forward that also keeps the backward's state in a backward-sized workspace.
 
     Returns (o, ht, workspace); pass the same inputs and `workspace` to
     comba_chunk_bwd_saved."""
     return _fwd(True, q, k, v, g, beta, d, h0, cu_seqlens, output_final_state, workspace,
-                stream, beta_tilde)
+                stream, beta_tilde, cu_seqlens_host)
 
 
 def comba_recurrent_fwd(q, k, v, g, beta, d, h0=None, *, beta_tilde=None, cu_seqlens=None,
-                        output_final_state=True, ht=None, stream=None):
+                        cu_seqlens_host=None, output_final_state=True, ht=None, stream=None):
     """Token-by-token recurrence (decoding; short segments).  Returns (o, ht).
 
     Same tensors as comba_chunk_fwd (fp32 inputs also allow d = 128) and no
@@ -258,7 +292,8 @@ def comba_recurrent_fwd(q, k, v, g, beta, d, h0=None, *, beta_tilde=None, cu_seq
 
     lib = load_library()
     shp, (B, T, H, dk, dv, N) = _prepare(q, k, v, g, beta, d, h0, cu_seqlens,
-                                         extra=_beta_tilde(beta_tilde, beta))
+                                         extra=_beta_tilde(beta_tilde, beta),
+                                         cu_seqlens_host=cu_seqlens_host)
     o = torch.empty((B, T, H, dv), dtype=torch.float32, device=q.device)
     if ht is not None:
         if ht.dtype != torch.float32 or tuple(ht.shape) != (N, H, dk, dv) \
@@ -273,7 +308,7 @@ def comba_recurrent_fwd(q, k, v, g, beta, d, h0=None, *, beta_tilde=None, cu_seq
     return o, ht
 
 
-def _prologue_shape(xq, xk, xv, wq, wk, wv, cu_seqlens, extra=()):
+def _prologue_shape(xq, xk, xv, wq, wk, wv, cu_seqlens, extra=(), cu_seqlens_host=None):
     import torch
 
     if not xq.is_cuda:
@@ -298,18 +333,22 @@ def _prologue_shape(xq, xk, xv, wq, wk, wv, cu_seqlens, extra=()):
             raise CombaError("comba: cu_seqlens must be int32 on the device, B == 1")
         N = cu_seqlens.numel() - 1
     else:
+        if cu_seqlens_host is not None:
+            raise CombaError("comba: cu_seqlens_host needs cu_seqlens")
         N = B
     code = COMBA_BF16 if xq.dtype == torch.bfloat16 else COMBA_F32
-    return _make_shape(B, T, H, dk, dv, N, _ptr(cu_seqlens), code)
+    return _make_shape(B, T, H, dk, dv, N, _ptr(cu_seqlens), code,
+                       cu_host=_host_offsets(cu_seqlens_host, N + 1))
 
 
-def comba_prologue_fwd(xq, xk, xv, wq, wk, wv, *, cu_seqlens=None, stream=None):
+def comba_prologue_fwd(xq, xk, xv, wq, wk, wv, *, cu_seqlens=None, cu_seqlens_host=None,
+                       stream=None):
     """Layer input prologue: causal short conv (4 taps), SiLU, L2 norm of q and k.
     Returns (q, k, v) in the dtype of x."""
     import torch
 
     lib = load_library()
-    shp = _prologue_shape(xq, xk, xv, wq, wk, wv, cu_seqlens)
+    shp = _prologue_shape(xq, xk, xv, wq, wk, wv, cu_seqlens, cu_seqlens_host=cu_seqlens_host)
     q, k, v = torch.empty_like(xq), torch.empty_like(xk), torch.empty_like(xv)
     st = torch.cuda.current_stream(xq.device).cuda_stream if stream is None else stream
     _check(lib.comba_prologue_fwd(ctypes.byref(shp), _ptr(xq), _ptr(xk), _ptr(xv), _ptr(wq),
@@ -318,14 +357,15 @@ def comba_prologue_fwd(xq, xk, xv, wq, wk, wv, *, cu_seqlens=None, stream=None):
     return q, k, v
 
 
-def comba_prologue_bwd(xq, xk, xv, wq, wk, wv, gq, gk, gv, *, cu_seqlens=None, workspace=None,
-                       stream=None):
+def comba_prologue_bwd(xq, xk, xv, wq, wk, wv, gq, gk, gv, *, cu_seqlens=None,
+                       cu_seqlens_host=None, workspace=None, stream=None):
     """Backward of the prologue from the fp32 gradients of q, k, v.  Returns dict
     dxq, dxk, dxv, dwq, dwk, dwv (fp32)."""
     import torch
 
     lib = load_library()
-    shp = _prologue_shape(xq, xk, xv, wq, wk, wv, cu_seqlens, extra=(gq, gk, gv))
+    shp = _prologue_shape(xq, xk, xv, wq, wk, wv, cu_seqlens, extra=(gq, gk, gv),
+                          cu_seqlens_host=cu_seqlens_host)
     if gq.shape != xq.shape or gk.shape != xk.shape or gv.shape != xv.shape:
         raise CombaError("comba: gradients must have the shapes of q, k, v")
     f32 = torch.float32
@@ -387,12 +427,13 @@ def comba_gate_bwd(o, z, dy, *, stream=None):
 
 
 def _bwd(saved, q, k, v, g, beta, d, h0, dO, dht, cu_seqlens, need_dh0, workspace, stream,
-         beta_tilde):
+         beta_tilde, cu_seqlens_host=None):
     import torch
 
     lib = load_library()
     shp, (B, T, H, dk, dv, N) = _prepare(q, k, v, g, beta, d, h0, cu_seqlens,
-                                         extra=(("dO", dO),) + _beta_tilde(beta_tilde, beta))
+                                         extra=(("dO", dO),) + _beta_tilde(beta_tilde, beta),
+                                         cu_seqlens_host=cu_seqlens_host)
     if dht is not None and (dht.dtype != torch.float32 or tuple(dht.shape) != (N, H, dk, dv)
                             or not dht.is_contiguous()):
         raise CombaError("comba: dht must be contiguous float32 [N,H,dk,dv]")
@@ -432,16 +473,16 @@ def _bwd(saved, q, k, v, g, beta, d, h0, dO, dht, cu_seqlens, need_dh0, workspac
 
 
 def comba_chunk_bwd(q, k, v, g, beta, d, h0, dO, dht=None, *, beta_tilde=None, cu_seqlens=None,
-                    need_dh0=True, workspace=None, stream=None):
+                    cu_seqlens_host=None, need_dh0=True, workspace=None, stream=None):
     """Chunk-wise backward (recomputes the forward).  Returns dict dq, dk, dv, dg, dbeta, dd,
     dh0 (fp32), and dbeta_tilde when beta_tilde is given (dbeta is then the derivative
     through the write strength only; otherwise it is the total derivative)."""
     return _bwd(False, q, k, v, g, beta, d, h0, dO, dht, cu_seqlens, need_dh0, workspace, stream,
-                beta_tilde)
+                beta_tilde, cu_seqlens_host)
 
 
 def comba_chunk_bwd_saved(q, k, v, g, beta, d, h0, dO, dht=None, *, workspace, beta_tilde=None,
-                          cu_seqlens=None, need_dh0=True, stream=None):
+                          cu_seqlens=None, cu_seqlens_host=None, need_dh0=True, stream=None):
     """Backward reusing the state left by comba_chunk_fwd_save in `workspace`."""
     return _bwd(True, q, k, v, g, beta, d, h0, dO, dht, cu_seqlens, need_dh0, workspace, stream,
-                beta_tilde)
+                beta_tilde, cu_seqlens_host)

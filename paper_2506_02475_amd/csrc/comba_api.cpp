@@ -42,7 +42,15 @@ comba_status check_shape(const comba_shape* s, Dims* out, bool wide = false) {
     if (s->B != 1 || s->num_seqs < 0) return COMBA_ERR_SHAPE;
     d.N = s->num_seqs;
     d.Tseq = 0;
+    if (s->cu_seqlens_host) {
+      // the host copy of the offsets: 0 = cu[0] <= cu[1] <= ... <= cu[N] = T
+      const int32_t* cu = s->cu_seqlens_host;
+      if (cu[0] != 0 || cu[d.N] != s->T) return COMBA_ERR_SHAPE;
+      for (int i = 0; i < d.N; ++i)
+        if (cu[i + 1] < cu[i]) return COMBA_ERR_SHAPE;
+    }
   } else {
+    if (s->cu_seqlens_host) return COMBA_ERR_SHAPE;  // offsets without a packed batch
     if (s->num_seqs != s->B) return COMBA_ERR_SHAPE;
     d.N = s->B;
     d.Tseq = s->T;

@@ -48,6 +48,15 @@ __device__ __forceinline__ int wave_id() { return threadIdx.x >> 6; }
 
 __device__ __forceinline__ floatx4 zero4() { return floatx4{0.f, 0.f, 0.f, 0.f}; }
 
+// IEEE 754-2019 maximum: a NaN operand gives NaN (fmaxf would drop it).  The
+// block maxima behind every int16 scale use it, so that a non-finite value
+// turns its block's scale into NaN (see q_scale) instead of vanishing.  On
+// gfx950 it is v_maximum3_f32, which also folds |x| and a third operand.
+__device__ __forceinline__ float nmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+__device__ __forceinline__ float nmax_abs4(float m, const floatx4& x) {
+  return nmax(nmax(m, nmax(fabsf(x[0]), fabsf(x[1]))), nmax(fabsf(x[2]), fabsf(x[3])));
+}
+
 template <int MT, int NT>
 __device__ __forceinline__ void zero_acc(floatx4 (&acc)[MT][NT]) {
 #pragma unroll
@@ -200,10 +209,11 @@ __device__ __forceinline__ const T& at(const T* base, unsigned byte_off) {
 }
 
 // Max over the four lanes r16, r16 + 16, r16 + 32, r16 + 48 (the lanes that
-// hold one row of a transposed MFMA accumulator) of values >= 0:
+// hold one row of a transposed MFMA accumulator) of values >= 0 or NaN:
 // v_permlane16_swap / v_permlane32_swap with both operands x hand lane l the
 // values of lanes l & ~16 and l | 16 (resp. 32) (checked with an in-bounds
-// probe); non-negative floats order like their bit patterns.
+// probe); non-negative floats order like their bit patterns, and every NaN
+// pattern lies above +Inf, so a NaN wins.
 __device__ __forceinline__ float rowgroup_max(float m) {
   const unsigned x = __float_as_uint(m);
   const auto a = __builtin_amdgcn_permlane16_swap(x, x, false, false);
@@ -219,11 +229,17 @@ __device__ __forceinline__ float rowgroup_max(float m) {
 // below 2^e, so |q| <= 32767 and the rounding error is at most s / 2, i.e. at
 // most 2^-15 of the block's max.  q * s splits exactly into the bf16 (hi, lo)
 // pair the consumer's MFMA products use, so no further rounding is added there.
-// (Zero, tiny and non-finite maxima give a scale in [2^-115, 2^114].)
+// Zero and tiny maxima give a scale in [2^-115, 2^113].  A block whose max is
+// Inf or NaN (a non-finite value in the block, found by the NaN-propagating
+// maxima) gets the scale NaN: every value decoded from it is NaN, so
+// non-finite inputs stay visible downstream instead of saturating to +-32767.
 __device__ __forceinline__ int q_exponent(float m) {  // e with m < 2^e, m >= 0
   return max(((__float_as_int(m) >> 23) & 0xFF) - 126, -100);
 }
-__device__ __forceinline__ float q_scale(float m) { return __int_as_float((q_exponent(m) + 112) << 23); }
+__device__ __forceinline__ float q_scale(float m) {
+  const int e = q_exponent(m);  // 129: exponent field 255, m is Inf or NaN
+  return e > 128 ? __int_as_float(0x7FC00000) : __int_as_float((e + 112) << 23);
+}
 // 1 / s, divided by 32767 for the snorm16 conversion in q_pack4
 __device__ __forceinline__ float q_inv_scale(float m) {
   return __int_as_float((142 - q_exponent(m)) << 23) * (1.0f / 32767.0f);
@@ -342,21 +358,22 @@ __device__ __forceinline__ float wave_sum(float x) {
 __device__ __forceinline__ float shift_down1(float x) { return dpp_upd<0x130>(0.f, x); }
 // Max over each group of 8 lanes, resp. the 16 lanes of a row (symmetric
 // butterflies, every lane gets the result).
+// (NaN-propagating, see nmax.)
 __device__ __forceinline__ float max8(float m) {
-  m = fmaxf(m, dpp_upd<0xB1>(0.f, m));   // quad_perm [1,0,3,2]
-  m = fmaxf(m, dpp_upd<0x4E>(0.f, m));   // quad_perm [2,3,0,1]
-  m = fmaxf(m, dpp_upd<0x141>(0.f, m));  // row_half_mirror
+  m = nmax(m, dpp_upd<0xB1>(0.f, m));   // quad_perm [1,0,3,2]
+  m = nmax(m, dpp_upd<0x4E>(0.f, m));   // quad_perm [2,3,0,1]
+  m = nmax(m, dpp_upd<0x141>(0.f, m));  // row_half_mirror
   return m;
 }
 __device__ __forceinline__ float max16(float m) {
   m = max8(m);
-  return fmaxf(m, dpp_upd<0x140>(0.f, m));  // row_mirror
+  return nmax(m, dpp_upd<0x140>(0.f, m));  // row_mirror
 }
 // Max over lanes l, l ^ 4, l ^ 8, l ^ 12 (the four lanes that hold one row
 // after quad_transpose), every one of them gets the result.
 __device__ __forceinline__ float row4_max(float m) {
-  m = fmaxf(m, dpp_upd<0x124>(0.f, m));  // row_ror:4
-  m = fmaxf(m, dpp_upd<0x128>(0.f, m));  // row_ror:8
+  m = nmax(m, dpp_upd<0x124>(0.f, m));  // row_ror:4
+  m = nmax(m, dpp_upd<0x128>(0.f, m));  // row_ror:8
   return m;
 }
 

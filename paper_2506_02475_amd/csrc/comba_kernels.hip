@@ -981,11 +981,9 @@ __device__ __forceinline__ void put_block_column(float* Ls, const floatx4 (&mb)[
   if constexpr (BWD) {
     float m = 0.f;
 #pragma unroll
-    for (int i = J; i < 4; ++i)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) m = fmaxf(m, fabsf(mb[i][e]));
-    m = fmaxf(m, __shfl_xor(m, 16));
-    m = fmaxf(m, __shfl_xor(m, 32));
+    for (int i = J; i < 4; ++i) m = nmax_abs4(m, mb[i]);
+    m = nmax(m, __shfl_xor(m, 16));
+    m = nmax(m, __shfl_xor(m, 32));
     const float inv = q_inv_scale(m);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -1071,7 +1069,7 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
       if (r >= c) a = (aqk[0][nt][e] - dh * kk) * __expf(Gs[r] - Gs[c]);
       if (r > c) l = Bs[r] * __expf(Gs[r - 1] - Gs[c]) * kk;
       av[nt][e] = a;
-      rmax[e] = fmaxf(rmax[e], fabsf(a));
+      rmax[e] = nmax(rmax[e], fabsf(a));
       Ls[r * LDL + c] = l;
     }
   }
@@ -1096,9 +1094,9 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
     // column maxima of this wave's 16 rows, combined over the waves below
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt) {
-      float m = fmaxf(fmaxf(fabsf(av[nt][0]), fabsf(av[nt][1])), fmaxf(fabsf(av[nt][2]), fabsf(av[nt][3])));
-      m = fmaxf(m, __shfl_xor(m, 16));
-      m = fmaxf(m, __shfl_xor(m, 32));
+      float m = nmax_abs4(0.f, floatx4{av[nt][0], av[nt][1], av[nt][2], av[nt][3]});
+      m = nmax(m, __shfl_xor(m, 16));
+      m = nmax(m, __shfl_xor(m, 32));
       if (g4 == 0) colmax[w][16 * nt + r16] = m;
     }
   }
@@ -1110,7 +1108,7 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt) {
       const int c = 16 * nt + r16;
-      const float m = fmaxf(fmaxf(colmax[0][c], colmax[1][c]), fmaxf(colmax[2][c], colmax[3][c]));
+      const float m = nmax(nmax(colmax[0][c], colmax[1][c]), nmax(colmax[2][c], colmax[3][c]));
       *reinterpret_cast<uint2*>(ATq + chh * CC + frag_off(c, 16 * w + 4 * g4)) =
           q_pack4(floatx4{av[nt][0], av[nt][1], av[nt][2], av[nt][3]}, q_inv_scale(m));
       if (w == 0) ATs[chh * CH + c] = q_scale(m);  // equal in the four lane groups
@@ -1184,7 +1182,7 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
     const float mv[8] = {m0.x, m0.y, m0.z, m0.w, m1.x, m1.y, m1.z, m1.w};
     float m = 0.f;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) m = fmaxf(m, fabsf(mv[e]));
+    for (int e = 0; e < 8; ++e) m = nmax(m, fabsf(mv[e]));
     m = max8(m);
     *reinterpret_cast<uint4*>(Mq + chh * CC + frag_off(r, c8)) = q_pack8(mv, q_inv_scale(m));
     Ms[chh * CH + r] = q_scale(m);  // the eight threads of a row store the same value
@@ -1282,8 +1280,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
       float m = 0.f;
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt)
-        m = fmaxf(m, fmaxf(fmaxf(fabsf(X[mt][nt][0]), fabsf(X[mt][nt][1])),
-                           fmaxf(fabsf(X[mt][nt][2]), fabsf(X[mt][nt][3]))));
+        m = nmax_abs4(m, X[mt][nt]);
       m = rowgroup_max(m);
       const float inv = q_inv_scale(m);
       const long row = xrow0 + 16 * mt;
@@ -1451,7 +1448,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
       float m = 0.f;
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt)
-        m = fmaxf(m, fmaxf(fmaxf(fabsf(dl[nt][0]), fabsf(dl[nt][1])), fmaxf(fabsf(dl[nt][2]), fabsf(dl[nt][3]))));
+        m = nmax_abs4(m, dl[nt]);
       m = rowgroup_max(m);
       const float inv = q_inv_scale(m);
       const long row = (chh * NB + blockIdx.z) * CH + prow;  // the slice's block
@@ -1615,8 +1612,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
       float m = 0.f;
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt)
-        m = fmaxf(m, fmaxf(fmaxf(fabsf(Y[mt][nt][0]), fabsf(Y[mt][nt][1])),
-                           fmaxf(fabsf(Y[mt][nt][2]), fabsf(Y[mt][nt][3]))));
+        m = nmax_abs4(m, Y[mt][nt]);
       m = rowgroup_max(m);
       const float inv = q_inv_scale(m);
       const long row = yrow0 + 16 * mt;
@@ -1803,7 +1799,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
       float m = 0.f;
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt)
-        m = fmaxf(m, fmaxf(fmaxf(fabsf(drr[nt][0]), fabsf(drr[nt][1])), fmaxf(fabsf(drr[nt][2]), fabsf(drr[nt][3]))));
+        m = nmax_abs4(m, drr[nt]);
       m = rowgroup_max(m);
       const float inv = q_inv_scale(m);
       const long row = (chh * NB + blockIdx.z) * CH + prow;  // the slice's block

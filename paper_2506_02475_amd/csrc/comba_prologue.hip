@@ -52,9 +52,11 @@ __device__ __forceinline__ void load_ch(const Tin* p, float (&v)[C]) {
   }
 }
 
-__device__ __forceinline__ bf16_t f2bf(float x) {  // round to nearest even
-  const uint32_t u = __float_as_uint(x);
-  return (bf16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+// Round to nearest even with the hardware conversion (v_cvt_pk_bf16_f32),
+// which keeps NaN a NaN and Inf an Inf (adding a rounding bias to the bit
+// pattern would turn a NaN with a full payload into -0).
+__device__ __forceinline__ bf16_t f2bf(float x) {
+  return __builtin_bit_cast(bf16_t, (__bf16)x);
 }
 
 // One vector store per lane and row (element-wise stores would leave every

@@ -16,6 +16,39 @@ def maxrel(x, ref):
     return num / den
 
 
+def maxrel_by_slice(x, ref, offsets):
+    """Largest norm-wise relative error over the (sequence, head) slices of a
+    per-token tensor [B, T, H, ...] (ref = oracle); ``offsets`` are the
+    sequences' token offsets into the flattened B*T axis.  Every slice is
+    measured against its own largest reference value, so the small entries of
+    one sequence or head are not hidden behind another's."""
+    x = np.asarray(x, np.float64)
+    ref = np.asarray(ref, np.float64)
+    H = ref.shape[2]
+    xf = x.reshape((-1, H) + ref.shape[3:])
+    rf = ref.reshape((-1, H) + ref.shape[3:])
+    worst = 0.0
+    for s in range(len(offsets) - 1):
+        a, b = int(offsets[s]), int(offsets[s + 1])
+        if b <= a:
+            continue
+        for h in range(H):
+            worst = max(worst, maxrel(xf[a:b, h], rf[a:b, h]))
+    return worst
+
+
+def elementwise_floor(x, ref, floor=1e-2):
+    """Largest elementwise relative error |x - y| / max(|y|, floor * ||y||_inf),
+    for information: near zero a purely elementwise ratio is ill-posed."""
+    x = np.asarray(x, np.float64)
+    ref = np.asarray(ref, np.float64)
+    if ref.size == 0:
+        return 0.0
+    den = np.maximum(np.abs(ref), floor * np.max(np.abs(ref)))
+    den = np.where(den > 0, den, 1.0)
+    return float(np.max(np.abs(x - ref) / den))
+
+
 def tol_for(w):
     # tolerances stated for the operator: 1e-5 (fp32 inputs), 2e-3 (bf16 inputs,
     # fp32 accumulation), on the norm-wise max relative error
@@ -63,19 +96,34 @@ def gpu_bwd(w, **kw):
     return {k: (None if v is None else v.cpu().numpy()) for k, v in gr.items()}
 
 
+def _offsets(w):
+    return w.seq_offsets
+
+
 def check_fwd(w, heads=None, tol=None):
-    """GPU forward vs oracle; returns the error dict (asserts within tolerance)."""
+    """GPU forward vs oracle; returns the error dict (asserts within tolerance).
+
+    Norm-wise max relative error per output tensor (the stated metric) and per
+    (sequence, head) slice ("o@seq,head"), both held to ``tol``; the floored
+    elementwise error ("o~ew") is reported only."""
     tol = tol_for(w) if tol is None else tol
     o, ht = gpu_fwd(w)
     ro, rht = oracle.workload_fwd(w, heads=heads)
     sel = slice(None) if heads is None else list(heads)
-    errs = {"o": maxrel(o[:, :, sel], ro), "ht": maxrel(ht[:, sel], rht)}
+    assert np.all(np.isfinite(o)) and np.all(np.isfinite(ht)), w.spec.name
+    hts = ht[:, sel]
+    errs = {"o": maxrel(o[:, :, sel], ro), "ht": maxrel(hts, rht),
+            "o@seq,head": maxrel_by_slice(o[:, :, sel], ro, _offsets(w)),
+            "ht@seq,head": max((maxrel(hts[a, b], rht[a, b]) for a in range(rht.shape[0])
+                                for b in range(rht.shape[1])), default=0.0)}
     for name, e in errs.items():
-        assert np.all(np.isfinite(o)) and e <= tol, (w.spec.name, name, e, tol)
+        assert e <= tol, (w.spec.name, name, e, tol)
+    errs["o~ew"] = elementwise_floor(o[:, :, sel], ro)
     return errs
 
 
 def check_bwd(w, heads=None, tol=None):
+    """GPU backward vs oracle, metrics as in check_fwd; dd per head as well."""
     tol = tol_for(w) if tol is None else tol
     gr = gpu_bwd(w)
     ref = oracle.workload_bwd(w, heads=heads)
@@ -85,8 +133,14 @@ def check_bwd(w, heads=None, tol=None):
     assert ("dbeta_tilde" in gr) == ("dbeta_tilde" in ref)
     for name in names:
         errs[name] = maxrel(gr[name][:, :, sel], ref[name])
+        errs[name + "@seq,head"] = maxrel_by_slice(gr[name][:, :, sel], ref[name], _offsets(w))
     errs["dd"] = maxrel(gr["dd"][sel], ref["dd"])
+    rdd = np.abs(ref["dd"])
+    errs["dd@head"] = float(np.max(np.abs(gr["dd"][sel] - ref["dd"]) /
+                                   np.maximum(rdd, max(1e-7 * np.max(rdd), 1e-30))))
     errs["dh0"] = maxrel(gr["dh0"][:, sel], ref["dh0"])
     for name, e in errs.items():
         assert np.isfinite(e) and e <= tol, (w.spec.name, name, e, tol)
+    for name in names:
+        errs[name + "~ew"] = elementwise_floor(gr[name][:, :, sel], ref[name])
     return errs

@@ -16,9 +16,17 @@ OK, ENULL, ESHAPE, EDTYPE, EALIGN, EWS = 0, 1, 2, 3, 4, 5
 FAKE = 0x100000  # aligned, never dereferenced: validation fails before any launch
 
 
-def shape(B=1, T=128, H=2, dk=128, dv=128, chunk=64, N=None, cu=None, dtype=comba.COMBA_BF16):
-    return comba.CombaShape(B, T, H, dk, dv, chunk, B if N is None else N,
-                            None if cu is None else ctypes.c_void_p(cu), dtype)
+def shape(B=1, T=128, H=2, dk=128, dv=128, chunk=64, N=None, cu=None, dtype=comba.COMBA_BF16,
+          cu_host=None):
+    """The C shape struct; ``cu_host`` is a list of host offsets (kept alive on it)."""
+    hp = None
+    if cu_host is not None:
+        cu_host = (ctypes.c_int32 * len(cu_host))(*cu_host)
+        hp = ctypes.cast(cu_host, ctypes.c_void_p)
+    s = comba.CombaShape(B, T, H, dk, dv, chunk, B if N is None else N,
+                         None if cu is None else ctypes.c_void_p(cu), hp, dtype)
+    s._keep = cu_host
+    return s
 
 
 def fwd(shp, ptrs=None, ws_bytes=1 << 40, **over):
@@ -301,3 +309,46 @@ def test_rejects_small_workspace():
     assert fwd(s, ws_bytes=need - 1) == EWS
     needb = comba.load_library().comba_bwd_workspace_bytes(ctypes.byref(s))
     assert bwd(s, ws_bytes=needb - 1) == EWS
+
+
+@pytest.mark.parametrize("cu_host,ok", [
+    ([0, 40, 40, 128], True),
+    ([0, 128], True),
+    ([0, 0, 0, 128], True),
+    ([1, 40, 90, 128], False),     # cu[0] != 0
+    ([0, 40, 90, 127], False),     # cu[N] != T
+    ([0, 90, 40, 128], False),     # not monotone
+    ([0, 40, -5, 128], False),
+])
+def test_host_offsets_are_validated_before_any_launch(cu_host, ok):
+    # with a host copy of the offsets every entry point rejects a malformed
+    # table with a shape error; a well-formed one passes on to the next check
+    # (here the one-byte workspace, resp. a misaligned output), so nothing is
+    # launched either way
+    n = len(cu_host) - 1
+    s = shape(T=128, cu=FAKE, N=n, cu_host=cu_host)
+    assert fwd(s, ws_bytes=1) == (EWS if ok else ESHAPE)
+    assert bwd(s, ws_bytes=1) == (EWS if ok else ESHAPE)
+    assert rec(s, o=FAKE + 4) == (EALIGN if ok else ESHAPE)
+    assert pro(s, q=FAKE + 8) == (EALIGN if ok else ESHAPE)
+    lib = comba.load_library()
+    P = ctypes.c_void_p
+    args = [P(FAKE)] * 10
+    assert lib.comba_chunk_fwd_save(ctypes.byref(s), *args, P(FAKE), ctypes.c_size_t(1),
+                                    None) == (EWS if ok else ESHAPE)
+
+
+def test_host_offsets_need_a_packed_batch():
+    assert fwd(shape(B=2, T=64, cu_host=[0, 64, 128]), ws_bytes=1) == ESHAPE
+
+
+def test_binding_checks_host_offsets():
+    import numpy as np
+
+    with pytest.raises(comba.CombaError):
+        comba._host_offsets(np.array([0, 5, 9], dtype=np.int64), 4)
+    a = comba._host_offsets([0, 5, 9], 3)
+    assert a.dtype == np.int32 and a.flags.c_contiguous
+    shp = comba._make_shape(1, 9, 1, 64, 64, 2, ctypes.c_void_p(FAKE), comba.COMBA_BF16,
+                            cu_host=a)
+    assert shp.cu_seqlens_host == a.ctypes.data

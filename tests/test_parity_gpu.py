@@ -215,21 +215,24 @@ def test_workload_tiny_f32_fwd():
     _log("tiny_f32_fwd %s" % check_fwd(w))
 
 
+# Full-size workloads: four heads each, the last head among them; every sampled
+# head is compared in full (all sequences and tokens), per tensor and per
+# (sequence, head) slice.
 def test_workload_340m_fwd():
     w = generate(1)
-    _log("l340m_fwd %s" % check_fwd(w, heads=[0, 3, 7]))
+    _log("l340m_fwd %s" % check_fwd(w, heads=[0, 3, 5, 7]))
 
 
 def test_workload_340m_fwdbwd():
     w = generate(2)
-    _log("l340m_fwdbwd fwd %s" % check_fwd(w, heads=[1, 6]))
-    _log("l340m_fwdbwd bwd %s" % check_bwd(w, heads=[1, 6]))
+    _log("l340m_fwdbwd fwd %s" % check_fwd(w, heads=[1, 4, 6, 7]))
+    _log("l340m_fwdbwd bwd %s" % check_bwd(w, heads=[1, 4, 6, 7]))
 
 
 def test_workload_1p3b_fwdbwd():
     w = generate(3)
-    _log("l1p3b_fwdbwd fwd %s" % check_fwd(w, heads=[0, 9]))
-    _log("l1p3b_fwdbwd bwd %s" % check_bwd(w, heads=[0, 9]))
+    _log("l1p3b_fwdbwd fwd %s" % check_fwd(w, heads=[0, 5, 9, 15]))
+    _log("l1p3b_fwdbwd bwd %s" % check_bwd(w, heads=[0, 5, 9, 15]))
 
 
 def test_workload_1p3b_training_pair():
@@ -252,7 +255,7 @@ def test_workload_1p3b_training_pair():
     assert torch.equal(o_s, o) and torch.equal(ht_s, ht)
     for key in gr:
         assert torch.equal(gr_s[key], gr[key]), key
-    heads = [4, 13]
+    heads = [4, 8, 13, 15]
     ro, rht = oracle.workload_fwd(w, heads=heads)
     ref = oracle.workload_bwd(w, heads=heads)
     errs = {"o": maxrel(o_s.cpu().numpy()[:, :, heads], ro),
@@ -267,4 +270,4 @@ def test_workload_1p3b_training_pair():
 
 def test_workload_varlen_512k_fwd():
     w = generate(4)
-    _log("varlen_512k_fwd %s" % check_fwd(w, heads=[5]))
+    _log("varlen_512k_fwd %s" % check_fwd(w, heads=[0, 5, 10, 15]))
