@@ -11,7 +11,7 @@ import numpy as np
 import pytest
 
 from comba_inputs import WORKLOADS, generate, random_case
-from gpu_helpers import check_bwd, check_fwd, gpu_bwd, gpu_fwd, maxrel
+from gpu_helpers import bar_errors, check_bwd, check_fwd, gpu_bwd, gpu_fwd, maxrel
 
 pytestmark = pytest.mark.gpu
 
@@ -92,7 +92,7 @@ def test_far_from_unit_magnitudes(v_exp, do_exp):
     w.dht *= np.float32(2.0 ** do_exp)
     errs = check_bwd(w)
     _log("far-from-unit v 2^%d, dO 2^%d: %s" % (v_exp, do_exp, errs))
-    assert max(errs.values()) < 1e-3
+    assert max(bar_errors(errs).values()) < 1e-3
 
 
 def test_long_weak_decay_errors_stay_bounded():
