@@ -86,7 +86,9 @@ typedef enum {
   COMBA_ERR_DTYPE = 3,     /* unknown dtype                                      */
   COMBA_ERR_ALIGN = 4,     /* a pointer breaks the alignment rules above         */
   COMBA_ERR_WORKSPACE = 5, /* workspace smaller than the *_workspace_bytes value */
-  COMBA_ERR_HIP = 6        /* a kernel launch failed                             */
+  COMBA_ERR_HIP = 6,       /* a kernel launch failed                             */
+  COMBA_ERR_SCRATCH = 7    /* too large for the static scratch of the no-allocation
+                              entry point (comba_noalloc_scratch_bytes)           */
 } comba_status;
 
 typedef enum { COMBA_F32 = 0, COMBA_BF16 = 1 } comba_dtype;
@@ -165,6 +167,26 @@ comba_status comba_chunk_bwd_saved(const comba_shape *shape, const void *q, cons
                                    float *dv, float *dg, float *dbeta, float *dbeta_tilde,
                                    float *dd, float *dh0, void *ws, size_t ws_bytes,
                                    void *stream);
+
+/*
+ * Forward without any device allocation, for callers that cannot allocate:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  Computes exactly what comba_chunk_fwd computes (same kernels,
+ * bitwise-equal results), with its workspace in a static device array of
+ * comba_noalloc_scratch_bytes() bytes (80 MiB) that every device the library
+ * runs on holds until the process ends; the caller passes only inputs and
+ * outputs.  A shape whose comba_fwd_workspace_bytes exceeds it (more than about
+ * 4,900 chunk-heads, e.g. beyond the 1.3B layer's B4 T4096 H16 at d = 128) is
+ * rejected with COMBA_ERR_SCRATCH before any launch; invalid shapes with
+ * COMBA_ERR_SHAPE.  Calls that overlap in time on one device share the array
+ * and race: order them on one stream.  Nothing in it needs clearing between
+ * calls (each call writes every byte it reads).
+ */
+size_t comba_noalloc_scratch_bytes(void);
+comba_status comba_chunk_fwd_noalloc(const comba_shape *shape, const void *q, const void *k,
+                                     const void *v, const float *g, const void *beta,
+                                     const void *beta_tilde, const float *d, const float *h0,
+                                     float *o, float *ht, void *stream);
 
 /*
  * Token-by-token recurrence (Eq. comba-S evaluated one token at a time: the

@@ -27,6 +27,7 @@ import re
 import threading
 
 __all__ = ["comba_chunk_fwd", "comba_chunk_bwd", "comba_chunk_fwd_save", "comba_chunk_bwd_saved",
+           "comba_chunk_fwd_noalloc", "noalloc_scratch_bytes",
            "comba_recurrent_fwd", "comba_prologue_fwd", "comba_prologue_bwd",
            "comba_gate_fwd", "comba_gate_bwd",
            "load_library", "library_path",
@@ -83,6 +84,10 @@ def load_library():
             lib.comba_chunk_fwd_save.restype = I
             lib.comba_chunk_bwd_saved.argtypes = [SP] + [P] * 18 + [P, Z, P]
             lib.comba_chunk_bwd_saved.restype = I
+            lib.comba_chunk_fwd_noalloc.argtypes = [SP] + [P] * 10 + [P]
+            lib.comba_chunk_fwd_noalloc.restype = I
+            lib.comba_noalloc_scratch_bytes.argtypes = []
+            lib.comba_noalloc_scratch_bytes.restype = Z
             lib.comba_recurrent_fwd.argtypes = [SP] + [P] * 10 + [P]
             lib.comba_recurrent_fwd.restype = I
             lib.comba_prologue_fwd.argtypes = [SP] + [P] * 9 + [P]
@@ -279,6 +284,40 @@ def comba_chunk_fwd_save(q, k, v, g, beta, d, h0=None, *, beta_tilde=None, cu_se
     comba_chunk_bwd_saved."""
     return _fwd(True, q, k, v, g, beta, d, h0, cu_seqlens, output_final_state, workspace,
                 stream, beta_tilde, cu_seqlens_host)
+
+
+def noalloc_scratch_bytes() -> int:
+    """Size of the static device scratch behind comba_chunk_fwd_noalloc."""
+    return int(load_library().comba_noalloc_scratch_bytes())
+
+
+def comba_chunk_fwd_noalloc(q, k, v, g, beta, d, h0=None, *, beta_tilde=None, cu_seqlens=None,
+                            cu_seqlens_host=None, o=None, ht=None, output_final_state=True,
+                            stream=None):
+    """Chunk-wise forward whose library call allocates nothing (its workspace is
+    the library's static device scratch).  ``o`` [B,T,H,dv] and ``ht``
+    [N,H,dk,dv] (float32, contiguous) may be passed in so that the call
+    allocates nothing on the Python side either.  Returns (o, ht)."""
+    import torch
+
+    lib = load_library()
+    shp, (B, T, H, dk, dv, N) = _prepare(q, k, v, g, beta, d, h0, cu_seqlens,
+                                         extra=_beta_tilde(beta_tilde, beta),
+                                         cu_seqlens_host=cu_seqlens_host)
+    for name, t, shape in (("o", o, (B, T, H, dv)), ("ht", ht, (N, H, dk, dv))):
+        if t is not None and (t.dtype != torch.float32 or tuple(t.shape) != shape
+                              or not t.is_contiguous() or t.device != q.device):
+            raise CombaError("comba: %s must be contiguous float32 %s on the device"
+                             % (name, list(shape)))
+    if o is None:
+        o = torch.empty((B, T, H, dv), dtype=torch.float32, device=q.device)
+    if ht is None and output_final_state:
+        ht = torch.empty((N, H, dk, dv), dtype=torch.float32, device=q.device)
+    st = torch.cuda.current_stream(q.device).cuda_stream if stream is None else stream
+    _check(lib.comba_chunk_fwd_noalloc(ctypes.byref(shp), _ptr(q), _ptr(k), _ptr(v), _ptr(g),
+                                       _ptr(beta), _ptr(beta_tilde), _ptr(d), _ptr(h0), _ptr(o),
+                                       _ptr(ht), ctypes.c_void_p(st)))
+    return o, ht
 
 
 def comba_recurrent_fwd(q, k, v, g, beta, d, h0=None, *, beta_tilde=None, cu_seqlens=None,

@@ -10,7 +10,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libcomba.so")
 SOURCES = [os.path.join(CSRC, "comba_kernels.hip"), os.path.join(CSRC, "comba_recurrent.hip"),
-           os.path.join(CSRC, "comba_prologue.hip"),
+           os.path.join(CSRC, "comba_prologue.hip"), os.path.join(CSRC, "comba_noalloc.hip"),
            os.path.join(CSRC, "comba_api.cpp")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

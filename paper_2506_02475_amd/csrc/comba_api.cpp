@@ -583,6 +583,9 @@ const char* comba_status_string(comba_status s) {
     case COMBA_ERR_ALIGN: return "misaligned pointer (q/k/v/dO and the [.., dk|dv] fp32 tensors need 16 B, workspace 256 B)";
     case COMBA_ERR_WORKSPACE: return "workspace too small";
     case COMBA_ERR_HIP: return "HIP kernel launch failed";
+    case COMBA_ERR_SCRATCH:
+      return "problem too large for the static scratch of comba_chunk_fwd_noalloc (80 MiB; "
+             "use comba_chunk_fwd with a workspace)";
   }
   return "unknown status";
 }

@@ -60,7 +60,8 @@ def test_library_exports_every_declared_symbol():
                              "comba_profile_enable", "comba_profile_read",
                              "comba_chunk_fwd_save", "comba_chunk_bwd_saved",
                              "comba_recurrent_fwd", "comba_prologue_fwd", "comba_prologue_bwd",
-                             "comba_prologue_workspace_bytes", "comba_gate_fwd", "comba_gate_bwd"}
+                             "comba_prologue_workspace_bytes", "comba_gate_fwd", "comba_gate_bwd",
+                             "comba_chunk_fwd_noalloc", "comba_noalloc_scratch_bytes"}
     out = subprocess.run(["nm", "-D", "--defined-only", comba.library_path()],
                          capture_output=True, text=True, check=True).stdout
     exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
@@ -77,7 +78,7 @@ def test_profile_read_without_calls_is_empty():
 
 def test_status_strings():
     lib = comba.load_library()
-    for code in range(7):
+    for code in range(8):
         assert lib.comba_status_string(code)
     assert lib.comba_status_string(99) == b"unknown status"
 
