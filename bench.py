@@ -11,11 +11,20 @@ layer shape, B=4, H=16, T=4096, dk=dv=128, chunk 64, bf16 inputs, fp32 state and
 outputs, seeded synthetic inputs (comba_inputs, PCG64).
 
 Prints one JSON line with the whole-job throughput in tokens/s, the roofline of
-the dominant kernel (timed live with HIP events on the library's stream over
-the timed region) and the fp64 CPU oracle timed on this host's cores on a
-bounded sample of the same workload.  The training pair with a separate
-state-feedback strength beta~ = b * beta (Section 3.2, one b per head) is timed
-after the headline region and reported under "variants".
+the dominant kernel and the fp64 CPU oracle timed on this host's cores on a
+bounded sample of the same workload.  The roofline credits the dominant kernel
+with the method's minimal HBM bytes (and flops) of its direction: the
+backward's q, k, v, dO and one fp32 state per chunk in, fp32 dq, dk, dv out
+(method_model), divided by the kernel's average launch time (HIP events
+recorded by the library on its launch stream over the timed region); the
+bytes this design's own intermediates add are reported beside them
+("design_bytes"), and "step_roofline" holds the whole step's method bytes and
+flops over the step time.  Separate forward and backward times, per-kernel MFMA
+use (algorithmic, and counted by rocprofv3 where the committed counters match
+the kernel source) are reported too.  Further legs timed after the headline
+region under "variants": the training pair with a separate state-feedback
+strength beta~ = b * beta (Section 3.2, one b per head), decoding, the
+long-context packed forward, head dim 256 and the layer prologue.
 """
 from __future__ import annotations
 
@@ -98,6 +107,98 @@ def op_flops(B, T, H, dk, dv, C=64):
     return float((fwd + bwd) * nch)
 
 
+# Stages of the forward and of the backward direction (the names the library's
+# stage timing records)
+FWD_STAGES = ("chunk_map", "prep", "prep_save", "scan_fwd", "scan_fwd_save")
+BWD_STAGES = ("scan_fwd_store", "scan_bwd", "intra_bwd", "reduce_dd")
+
+
+def chunk_lengths(T, B=1, cu_seqlens=None, C=64):
+    """Token counts of every chunk of every sequence (one head)."""
+    import numpy as np
+
+    if cu_seqlens is None:
+        lens = [T] * B
+    else:
+        cu = np.asarray(cu_seqlens, dtype=np.int64)
+        lens = list(cu[1:] - cu[:-1])
+    out = []
+    for n in lens:
+        n = int(n)
+        out += [C] * (n // C) + ([n % C] if n % C else [])
+    return out
+
+
+def method_model(direction, B, T, H, dk, dv, C=64, in_bytes=2, cu_seqlens=None):
+    """Algorithmic (flops, bytes) of the chunk-wise method itself for one
+    direction over the whole batch, independent of how the kernels are split.
+
+    Bytes (minimal HBM traffic, fp32 outputs): the forward reads q, k, v and
+    writes o ("fwd", inference); "fwd_save" also writes one fp32 dk x dv state
+    per chunk for the backward; "bwd" reads q, k, v, dO and the per-chunk
+    states and writes dq, dk, dv.  Gates, beta and the gradients of per-token
+    scalars (4-6 bytes per token-head) and the h0/ht/dht/dh0 states of each
+    sequence are left out (below 0.3% at the 1.3B layer shape).
+    Flops, per chunk of L tokens (the dense products of the chunk form): forward
+    2 L^2 (3 dk + 2 dv) + 6 L dk dv (K K^T, Q K^T, W, U, the masked score
+    product; W H, Q H and the state update); backward 12 L^2 dk + 8 L^2 dv +
+    12 L dk dv + 4 L^3.
+    """
+    lens = chunk_lengths(T, B, cu_seqlens, C)
+    tok = sum(lens) * H
+    nch = len(lens) * H
+    if direction in ("fwd", "fwd_save"):
+        by = tok * ((2 * dk + dv) * in_bytes + dv * 4)
+        if direction == "fwd_save":
+            by += nch * dk * dv * 4
+        fl = sum(2 * L * L * (3 * dk + 2 * dv) + 6 * L * dk * dv for L in lens) * H
+    elif direction == "bwd":
+        by = tok * ((2 * dk + 2 * dv) * in_bytes + (2 * dk + dv) * 4) + nch * dk * dv * 4
+        fl = sum(12 * L * L * dk + 8 * L * L * dv + 12 * L * dk * dv + 4 * L ** 3
+                 for L in lens) * H
+    else:
+        raise ValueError(direction)
+    return float(fl), float(by)
+
+
+def stage_direction(name, saved=True):
+    if name in BWD_STAGES:
+        return "bwd"
+    if name in FWD_STAGES:
+        return "fwd_save" if saved else "fwd"
+    raise ValueError(name)
+
+
+def kernel_roofline(kernel, avg_ms, method, design=None, traffic=None, mfma_counted=None):
+    """Roofline of one kernel: the method's (flops, bytes) of the direction the
+    kernel belongs to, divided by the kernel's average launch time (each
+    launch covers the whole batch), against the MI355X peak of the bound it
+    falls under.  ``design`` (flops, bytes) are what the kernel itself moves and
+    computes in this design (its own intermediates included), kept beside the
+    method figures; ``traffic`` the HBM bytes per launch measured by counters."""
+    fl, by = method
+    sec = avg_ms * 1e-3
+    if fl / by < RIDGE:
+        ach = by / sec / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(ach / PEAK_HBM_GBS, 4)}
+    else:
+        ach = fl / sec / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4)}
+    roof.update({"traffic": traffic, "kernel": kernel, "avg_launch_ms": round(avg_ms, 4),
+                 "algorithmic_bytes": by, "algorithmic_flops": fl})
+    if design is not None:
+        dfl, dby = design
+        roof["design_bytes"] = dby
+        roof["design_flops"] = dfl
+        roof["design_frac_hbm"] = round(dby / sec / 1e9 / PEAK_HBM_GBS, 4)
+        roof["mfma_pct_algorithmic"] = round(100.0 * dfl / sec / (PEAK_BF16_TFLOPS * 1e12), 3)
+    if mfma_counted is not None:
+        roof["mfma_pct_counted"] = round(100.0 * mfma_counted / sec / (PEAK_BF16_TFLOPS * 1e12), 3)
+    return roof
+
+
 def kernel_source_sha(files=("comba_kernels.hip", "comba_device.hpp")):
     h = hashlib.sha256()
     for f in files:
@@ -127,6 +228,25 @@ def measured_traffic(kernel, summary="traffic_counters_l1p3b_fwdbwd.md",
     if not k:
         return None
     return round(float(k["bytes_per_launch"]))
+
+
+def measured_mfma(kernel, summary="mfma_counters_l1p3b_fwdbwd.md",
+                  sources=("comba_kernels.hip", "comba_device.hpp")):
+    """MFMA flops per launch of a kernel stage counted by rocprofv3
+    (SQ_INSTS_VALU_MFMA_MOPS_*, every MFMA the kernel issues, split products
+    and recomputation included), from the committed summary, if it was taken
+    on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", summary)
+    try:
+        with open(path) as f:
+            text = f.read()
+        rec = json.loads(text.split("```json", 1)[1].split("```", 1)[0])
+    except (OSError, ValueError, IndexError):
+        return None
+    if rec.get("source_sha") != kernel_source_sha(sources):
+        return None
+    k = rec.get("kernels", {}).get(kernel)
+    return None if not k else float(k["mfma_flops_per_launch"])
 
 
 DECODE = dict(B=64, H=16, dk=128, dv=128, layers=8, seed=47)
@@ -271,18 +391,22 @@ def time_train256(comba, torch, steps, warmup):
         tot[name] = tot.get(name, 0.0) + ms
         cnt[name] = cnt.get(name, 0) + 1
     dom = max(tot, key=tot.get)
-    fl, by = stage_model(dom, B, T, H, dk, dv)
     avg = tot[dom] / cnt[dom]
-    ach = by / (avg * 1e-3) / 1e9
     ms_step = (t1 - t0) * 1e3 / steps
+    roof = kernel_roofline(dom, avg, method_model(stage_direction(dom), B, T, H, dk, dv),
+                           design=stage_model(dom, B, T, H, dk, dv),
+                           traffic=measured_traffic(dom, TRAIN256_TRAFFIC))
     return {"value": round(B * T / (ms_step * 1e-3), 1), "unit": "tokens/s",
             "ms_per_step": round(ms_step, 4),
+            "ms_fwd": round(sum(x for n, x in tot.items() if n in FWD_STAGES) / steps, 4),
+            "ms_bwd": round(sum(x for n, x in tot.items() if n in BWD_STAGES) / steps, 4),
             "config": {k_: c[k_] for k_ in ("B", "T", "H", "dk", "dv")},
             "stages_ms": {n: round(x / steps, 4) for n, x in tot.items()},
-            "roofline": {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
-                         "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None,
-                         "kernel": dom, "avg_launch_ms": round(avg, 4), "algorithmic_bytes": by,
-                         "algorithmic_flops": fl}}
+            "roofline": roof}
+
+
+TRAIN256_TRAFFIC = "traffic_counters_train_b4_t4096_h8_d256.md"
+PREFILL256_TRAFFIC = "traffic_counters_prefill_b4_t4096_h8_d256.md"
 
 
 def time_prefill256(comba, torch, steps, warmup):
@@ -322,18 +446,86 @@ def time_prefill256(comba, torch, steps, warmup):
         tot[name] = tot.get(name, 0.0) + ms
         cnt[name] = cnt.get(name, 0) + 1
     dom = max(tot, key=tot.get)
-    fl, by = stage_model(dom, B, T, H, dk, dv)
     avg = tot[dom] / cnt[dom]
-    achieved = by / (avg * 1e-3) / 1e9
     ms_step = (t1 - t0) * 1e3 / steps
+    roof = kernel_roofline(dom, avg,
+                           method_model(stage_direction(dom, saved=False), B, T, H, dk, dv),
+                           design=stage_model(dom, B, T, H, dk, dv),
+                           traffic=measured_traffic(dom, PREFILL256_TRAFFIC))
     return {"value": round(B * T / (ms_step * 1e-3), 1), "unit": "tokens/s",
             "ms_per_step": round(ms_step, 4),
             "config": {k_: c[k_] for k_ in ("B", "T", "H", "dk", "dv")},
             "stages_ms": {n: round(x / steps, 4) for n, x in tot.items()},
-            "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
-                         "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
-                         "traffic": None, "kernel": dom, "avg_launch_ms": round(avg, 4),
-                         "algorithmic_bytes": by, "algorithmic_flops": fl}}
+            "roofline": roof}
+
+
+VARLEN_TRAFFIC = "traffic_counters_varlen_512k_fwd.md"
+
+
+def time_varlen(comba, torch, steps, warmup):
+    """Long-context packed forward: 16 sequences of U[1024, 65536] tokens
+    (525,868 in total) x 16 heads x d = 128, bf16 inputs, per-sequence fp32
+    initial and final states, through the stateless comba_chunk_fwd (the
+    inference form: no chunk states are kept).  Per-stage live timing; the
+    roofline is that of the dominant stage, credited the forward's method
+    bytes (q, k, v in, o out)."""
+    import numpy as np
+    from comba_inputs import WORKLOADS, generate
+
+    spec = WORKLOADS[4]
+    w = generate(4)
+    dev = torch.device("cuda:0")
+    bf = torch.bfloat16
+
+    def t(x, dt=torch.float32):
+        return torch.from_numpy(np.ascontiguousarray(x)).to(dev, dt)
+
+    q, k, v = t(w.q, bf), t(w.k, bf), t(w.v, bf)
+    g, beta, d, h0 = t(w.g), t(w.beta, bf), t(w.d), t(w.h0)
+    cu = torch.from_numpy(w.cu_seqlens.astype(np.int32)).to(dev)
+    cu_host = w.cu_seqlens.astype(np.int32)
+    N, T, H, dk, dv = w.nseq, w.T, w.H, w.dk, w.dv
+    del w
+    ws = torch.empty(comba.fwd_workspace_bytes(1, T, H, dk, dv, num_seqs=N, varlen=True),
+                     dtype=torch.uint8, device=dev)
+
+    def call():
+        return comba.comba_chunk_fwd(q, k, v, g, beta, d, h0, cu_seqlens=cu,
+                                     cu_seqlens_host=cu_host, workspace=ws)
+
+    for _ in range(warmup):
+        call()
+    torch.cuda.synchronize()
+    comba.profile_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        call()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    marks = comba.profile_read()
+    comba.profile_enable(False)
+    tot, cnt = {}, {}
+    for name, ms in marks:
+        tot[name] = tot.get(name, 0.0) + ms
+        cnt[name] = cnt.get(name, 0) + 1
+    dom = max(tot, key=tot.get)
+    avg = tot[dom] / cnt[dom]
+    ms_step = (t1 - t0) * 1e3 / steps
+    fwd = method_model("fwd", 1, T, H, dk, dv, cu_seqlens=cu_host)
+    roof = kernel_roofline(dom, avg, fwd, traffic=measured_traffic(dom, VARLEN_TRAFFIC))
+    lens = np.diff(cu_host)
+    return {"value": round(T / (ms_step * 1e-3), 1), "unit": "tokens/s",
+            "ms_per_step": round(ms_step, 4),
+            "config": {"N": int(N), "T_total": int(T), "H": H, "dk": dk, "dv": dv,
+                       "longest": int(lens.max()), "shortest": int(lens.min())},
+            "workload": spec.name,
+            "stages_ms": {n: round(x / steps, 4) for n, x in tot.items()},
+            "step_roofline": {"method_bytes": fwd[1],
+                              "frac_hbm": round(fwd[1] / (ms_step * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+                              "method_flops": fwd[0],
+                              "mfma_pct": round(100.0 * fwd[0] / (ms_step * 1e-3) /
+                                                (PEAK_BF16_TFLOPS * 1e12), 3)},
+            "roofline": roof}
 
 
 PROLOGUE = dict(B=4, T=4096, H=16, dk=128, dv=128, seed=71)
@@ -423,6 +615,18 @@ def time_prologue(comba, torch, steps, warmup):
             "roofline": roof["prologue_bwd"], "roofline_fwd": roof["prologue_fwd"], "gate": gate}
 
 
+def calibration_copy(torch, nbytes):
+    """One plain device-to-device copy of ``nbytes`` (its HBM traffic counters
+    calibrate those of the kernels in the same profiled run); returns the size."""
+    n = nbytes // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    return n * 4
+
+
 def cpu_baseline(w, heads_sample, threads):
     import oracle
 
@@ -453,6 +657,9 @@ def main():
     ap.add_argument("--decode", action="store_true",
                     help="time the decoding step (comba_recurrent_fwd, T = 1, B = 64, H = 16, "
                          "d = 128, in place) as the headline instead of the training pair")
+    ap.add_argument("--varlen", action="store_true",
+                    help="time the long-context packed forward (16 sequences, 525,868 tokens, "
+                         "H16 d128, comba_chunk_fwd) as the headline")
     ap.add_argument("--prefill256", action="store_true",
                     help="time the inference prefill at head dim 256 (comba_chunk_fwd, B4 T4096 "
                          "H8 d256) as the headline")
@@ -494,6 +701,8 @@ def main():
             "config": {"workload": "train_b4_t4096_h8_d256", **r["config"]},
             "step": "comba_chunk_fwd_save + comba_chunk_bwd_saved", "stages_ms": r["stages_ms"],
             "roofline": r["roofline"], "cpu_baseline": None}
+        if args.copy_bytes > 0:
+            result["copy_bytes"] = calibration_copy(torch, args.copy_bytes)
         print(json.dumps(result), flush=True)
         return
     if args.prologue:
@@ -510,6 +719,25 @@ def main():
             "step": "comba_prologue_fwd + comba_prologue_bwd", "stages_ms": r["stages_ms"],
             "roofline": r["roofline"], "roofline_fwd": r["roofline_fwd"], "gate": r["gate"],
             "cpu_baseline": None}
+        if args.copy_bytes > 0:
+            result["copy_bytes"] = calibration_copy(torch, args.copy_bytes)
+        print(json.dumps(result), flush=True)
+        return
+    if args.varlen:
+        torch.cuda.set_device(0)
+        r = time_varlen(comba, torch, args.steps, args.warmup)
+        result = {
+            "metric": "Comba long-context packed forward tokens/s (16 sequences, 525,868 tokens, "
+                      "H=16, d=128 bf16)",
+            "value": r["value"], "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": r["ms_per_step"], "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+            "data": "synthetic (seeded PCG64, comba_inputs.generate(4))",
+            "config": {"workload": r["workload"], **r["config"]}, "step": "comba_chunk_fwd",
+            "stages_ms": r["stages_ms"], "roofline": r["roofline"],
+            "step_roofline": r["step_roofline"], "cpu_baseline": None}
+        if args.copy_bytes > 0:
+            result["copy_bytes"] = calibration_copy(torch, args.copy_bytes)
         print(json.dumps(result), flush=True)
         return
     if args.prefill256:
@@ -524,6 +752,8 @@ def main():
             "config": {"workload": "prefill_b4_t4096_h8_d256", **r["config"]},
             "step": "comba_chunk_fwd", "stages_ms": r["stages_ms"], "roofline": r["roofline"],
             "cpu_baseline": None}
+        if args.copy_bytes > 0:
+            result["copy_bytes"] = calibration_copy(torch, args.copy_bytes)
         print(json.dumps(result), flush=True)
         return
     if args.decode:
@@ -543,13 +773,7 @@ def main():
             "ms_per_call": r["ms_per_call"], "roofline": r["roofline"],
             "cpu_baseline": r.get("cpu_baseline")}
         if args.copy_bytes > 0:
-            n = args.copy_bytes // 4
-            src = torch.ones(n, dtype=torch.float32, device="cuda:0")
-            dst = torch.empty_like(src)
-            torch.cuda.synchronize()
-            dst.copy_(src)
-            torch.cuda.synchronize()
-            result["copy_bytes"] = n * 4
+            result["copy_bytes"] = calibration_copy(torch, args.copy_bytes)
         print(json.dumps(result), flush=True)
         return
 
@@ -589,7 +813,7 @@ def main():
                                    workspace=ws_b)
         return o, gr
 
-    ms_stateless = None
+    ms_stateless = ms_fwd_stateless = ms_bwd_stateless = None
     if not args.skip_stateless:
         for _ in range(args.warmup):
             step_stateless()
@@ -599,6 +823,21 @@ def main():
             step_stateless()
         torch.cuda.synchronize()
         ms_stateless = round((time.perf_counter() - t0) * 1e3 / args.steps, 4)
+        # the operator's forward and backward calls on their own
+        for name, call in (("fwd", lambda: comba.comba_chunk_fwd(
+                q, k, v, g, beta, d, h0, beta_tilde=bt_main, workspace=ws_f)),
+                           ("bwd", lambda: comba.comba_chunk_bwd(
+                q, k, v, g, beta, d, h0, dO, None, beta_tilde=bt_main, workspace=ws_b))):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(args.steps):
+                call()
+            torch.cuda.synchronize()
+            ms = round((time.perf_counter() - t0) * 1e3 / args.steps, 4)
+            if name == "fwd":
+                ms_fwd_stateless = ms
+            else:
+                ms_bwd_stateless = ms
 
     for _ in range(args.warmup):
         step()
@@ -627,24 +866,33 @@ def main():
     avg = {n: s[0] / s[1] for n, s in agg.items()}
     tot = {n: s[0] / args.steps for n, s in agg.items()}
     dom = max(tot, key=tot.get)
-    fl, by = stage_model(dom, B, T, H, dk, dv, sep_bt=args.beta_tilde)
-    sec = avg[dom] * 1e-3
-    intensity = fl / by if by else 0.0
+    models = {dr: method_model(dr, B, T, H, dk, dv) for dr in ("fwd_save", "bwd")}
     # the committed counters cover the headline workload only
-    traffic = None if args.beta_tilde else measured_traffic(dom)
-    if intensity < RIDGE:
-        achieved = by / sec / 1e9
-        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
-    else:
-        achieved = fl / sec / 1e12
-        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4)}
-    roof["traffic"] = traffic
-    roof["kernel"] = dom
-    roof["avg_launch_ms"] = round(avg[dom], 4)
-    roof["algorithmic_bytes"] = by
-    roof["algorithmic_flops"] = fl
+    roof = kernel_roofline(dom, avg[dom], models[stage_direction(dom)],
+                           design=stage_model(dom, B, T, H, dk, dv, sep_bt=args.beta_tilde),
+                           traffic=None if args.beta_tilde else measured_traffic(dom),
+                           mfma_counted=None if args.beta_tilde else measured_mfma(dom))
+    mfma_by_kernel = {}
+    for n in tot:
+        dfl, _ = stage_model(n, B, T, H, dk, dv, sep_bt=args.beta_tilde)
+        if dfl > 0:
+            cnt = None if args.beta_tilde else measured_mfma(n)
+            mfma_by_kernel[n] = {
+                "avg_launch_ms": round(avg[n], 4),
+                "algorithmic_pct": round(100.0 * dfl / (avg[n] * 1e-3) /
+                                         (PEAK_BF16_TFLOPS * 1e12), 3),
+                "counted_pct": None if cnt is None else
+                round(100.0 * cnt / (avg[n] * 1e-3) / (PEAK_BF16_TFLOPS * 1e12), 3)}
+    ms_fwd = sum(x for n, x in tot.items() if n in FWD_STAGES)
+    ms_bwd = sum(x for n, x in tot.items() if n in BWD_STAGES)
+    step_fl = models["fwd_save"][0] + models["bwd"][0]
+    step_by = models["fwd_save"][1] + models["bwd"][1]
+    step_sec = ms_per_step * 1e-3
+    step_roof = {"method_bytes": step_by, "achieved_GBs": round(step_by / step_sec / 1e9, 1),
+                 "frac_hbm": round(step_by / step_sec / 1e9 / PEAK_HBM_GBS, 4),
+                 "method_flops": step_fl,
+                 "mfma_pct": round(100.0 * step_fl / step_sec / (PEAK_BF16_TFLOPS * 1e12), 3),
+                 "fwd_method_bytes": models["fwd_save"][1], "bwd_method_bytes": models["bwd"][1]}
     op_fl = op_flops(B, T, H, dk, dv)
     mfma_frac_op = op_fl / (ms_per_step * 1e-3) / (PEAK_BF16_TFLOPS * 1e12)
 
@@ -668,10 +916,16 @@ def main():
                    "chunk": 64, "in_dtype": "bf16", "out_dtype": "f32"},
         "step": "comba_chunk_fwd_save + comba_chunk_bwd_saved",
         "ms_per_step_stateless": ms_stateless,
+        "ms_fwd": round(ms_fwd, 4),
+        "ms_bwd": round(ms_bwd, 4),
+        "ms_fwd_stateless": ms_fwd_stateless,
+        "ms_bwd_stateless": ms_bwd_stateless,
         "mfma_pct_peak_op": round(100.0 * mfma_frac_op, 3),
         "op_algorithmic_tflops": round(op_fl / (ms_per_step * 1e-3) / 1e12, 2),
         "stages_ms": {n: round(x, 4) for n, x in tot.items()},
         "roofline": roof,
+        "step_roofline": step_roof,
+        "mfma_by_kernel": mfma_by_kernel,
     }
     if not (args.no_variants or args.beta_tilde):
         # the same training pair with beta~ = b * beta, timed after the headline region
@@ -699,16 +953,12 @@ def main():
                                                                          args.steps, args.warmup)
         result["variants"]["prologue_b4_t4096_h16_d128"] = time_prologue(comba, torch,
                                                                          args.steps, args.warmup)
+        result["variants"]["varlen_512k_fwd"] = time_varlen(comba, torch, args.steps,
+                                                           args.warmup)
         result["variants"]["train_b4_t4096_h8_d256"] = time_train256(comba, torch, args.steps,
                                                                      args.warmup)
     if args.copy_bytes > 0:
-        n = args.copy_bytes // 4
-        src = torch.ones(n, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        result["copy_bytes"] = n * 4
+        result["copy_bytes"] = calibration_copy(torch, args.copy_bytes)
     if not args.no_cpu_baseline:
         nh = min(H, max(1, math.ceil(2 * threads / B)))
         heads = list(range(0, H, max(1, H // nh)))[:nh]

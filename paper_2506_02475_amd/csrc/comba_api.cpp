@@ -58,6 +58,8 @@ comba_status check_shape(const comba_shape* s, Dims* out, bool wide = false) {
   const int64_t ttot = s->cu_seqlens ? (int64_t)s->T : (int64_t)s->B * s->T;
   if (ttot > INT32_MAX / 2) return COMBA_ERR_SHAPE;
   if (d.N > 65535 * 1024) return COMBA_ERR_SHAPE;
+  // the scans run one workgroup per (sequence, head, 32-column slice) in a 1-D grid
+  if ((int64_t)d.N * d.H * 8 > INT32_MAX) return COMBA_ERR_SHAPE;
   d.Ttot = (int)ttot;
   // fixed-length rows: ceil(T / 64) chunks each; packed sequences: each
   // sequence adds at most one partial chunk to ceil(Ttot / 64)
@@ -93,7 +95,7 @@ comba_status check_shape_recurrent(const comba_shape* s, Dims* out) {
 }
 
 struct Layout {
-  size_t cmap, smap, M, A, G, X, D, Y, dR, ddp, MT, AT, QT, Xfin, sink, total;
+  size_t cmap, smap, sord, M, A, G, X, D, Y, dR, ddp, MT, AT, QT, Xfin, sink, total;
   size_t Xs, Ds, Ys, dRs, Xfs;  // bf16 path: scales of the int16 X, D, Y, dR, final-state sink
   size_t Ms, As, MTs, ATs;       // bf16 path: row scales of the int16 M, A, M^T, A^T
 };
@@ -110,6 +112,7 @@ Layout layout(const Dims& d, bool bwd) {
   L.sink = take(1024);
   L.cmap = take((size_t)d.ncmax * sizeof(comba::ChunkInfo));
   L.smap = take((size_t)(d.N > 0 ? d.N : 1) * sizeof(comba::SeqInfo));
+  L.sord = take((size_t)(d.N > 0 ? d.N : 1) * sizeof(int));
   L.G = take(chh * kChunk * sizeof(float));
   if (d.bf16) {
     // bf16 path: M, A as int16 with row scales; the backward
@@ -196,6 +199,7 @@ void carve(comba::LaunchArgs& a, const Layout& L, void* ws, bool bwd) {
   char* base = static_cast<char*>(ws);
   a.cmap = reinterpret_cast<comba::ChunkInfo*>(base + L.cmap);
   a.smap = reinterpret_cast<comba::SeqInfo*>(base + L.smap);
+  a.sorder = reinterpret_cast<int*>(base + L.sord);
   a.Mw = reinterpret_cast<float*>(base + L.M);
   a.Aw = reinterpret_cast<float*>(base + L.A);
   a.Gw = reinterpret_cast<float*>(base + L.G);

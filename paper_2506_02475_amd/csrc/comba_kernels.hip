@@ -23,7 +23,7 @@
 //   dA  = tril(dO D^T) ...       (the intra-chunk kernel collects the rest)
 //
 // Kernels, in launch order:
-//   k_chunk_map  sequence/chunk tables from cu_seqlens (fixed-length rows too)
+//   k_seq_map, k_chunk_fill  sequence/chunk tables from cu_seqlens (fixed-length rows too)
 //   k_prep       per chunk-head: G, A, M                        (chunk-parallel)
 //   k_scan_fwd   per (sequence, head, 32-column slice of dv): the sequential
 //                state recurrence over chunks, fused with the output
@@ -40,11 +40,20 @@ namespace comba {
 // ---------------------------------------------------------------------------
 // sequence / chunk tables
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(NTHR) void k_chunk_map(const int32_t* __restrict__ cu, int N, int Tseq,
-                                                    int Ttot, int ncmax, ChunkInfo* __restrict__ cmap,
-                                                    SeqInfo* __restrict__ smap) {
+// k_seq_map: one workgroup; per sequence its token range (clamped into
+// [0, Ttot], so that malformed offsets cannot address memory outside the token
+// range) and its first chunk (exclusive scan of the chunk counts, NTHR
+// sequences per pass).
+// It also writes the order in which the scans take the sequences, sorder[r] =
+// the sequence of rank r: longest first (ties by index) for up to SORT_MAX
+// sequences, so that the longest chains start first; identity beyond that.
+constexpr int SORT_MAX = 1024;
+__global__ __launch_bounds__(NTHR) void k_seq_map(const int32_t* __restrict__ cu, int N, int Tseq,
+                                                  int Ttot, int ncmax, SeqInfo* __restrict__ smap,
+                                                  int* __restrict__ sorder) {
   __shared__ int wave_tot[NWAVE];
   __shared__ int carry;
+  __shared__ int nckS[SORT_MAX];
   const int tid = threadIdx.x, lane = lane_id(), w = wave_id();
   if (tid == 0) carry = 0;
   __syncthreads();
@@ -53,8 +62,6 @@ __global__ __launch_bounds__(NTHR) void k_chunk_map(const int32_t* __restrict__ 
     int tok0 = 0, len = 0, nck = 0;
     if (s < N) {
       if (cu) {
-        // clamp into [0, Ttot] so that malformed offsets cannot address memory
-        // outside the token range
         int a = cu[s], b = cu[s + 1];
         a = min(max(a, 0), Ttot);
         b = min(max(b, a), Ttot);
@@ -66,7 +73,6 @@ __global__ __launch_bounds__(NTHR) void k_chunk_map(const int32_t* __restrict__ 
       }
       nck = (len + CH - 1) / CH;
     }
-    // exclusive scan of nck over the workgroup
     int x = nck;
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
@@ -79,22 +85,14 @@ __global__ __launch_bounds__(NTHR) void k_chunk_map(const int32_t* __restrict__ 
     for (int i = 0; i < w; ++i) before += wave_tot[i];
     const int chunk0 = before + x - nck;
     if (s < N) {
-      const int room = max(0, ncmax - chunk0);
-      const int n = min(nck, room);
+      // a sequence never reaches past the ncmax chunk slots of the workspace
       SeqInfo si;
-      si.chunk0 = chunk0;
-      si.nchunks = n;
+      si.chunk0 = min(chunk0, ncmax);
+      si.nchunks = min(nck, max(0, ncmax - chunk0));
       si.tok0 = tok0;
       si.len = len;
       smap[s] = si;
-      for (int j = 0; j < n; ++j) {
-        ChunkInfo ci;
-        ci.tok0 = tok0 + j * CH;
-        ci.len = min(CH, len - j * CH);
-        ci.seq = s;
-        ci.pad = 0;
-        cmap[chunk0 + j] = ci;
-      }
+      if (N <= SORT_MAX) nckS[s] = nck;
     }
     __syncthreads();
     if (tid == 0) {
@@ -104,13 +102,47 @@ __global__ __launch_bounds__(NTHR) void k_chunk_map(const int32_t* __restrict__ 
     }
     __syncthreads();
   }
-  const int total = min(carry, ncmax);
-  for (int c = total + tid; c < ncmax; c += NTHR) {
+  for (int s = tid; s < N; s += NTHR) {
+    int r = s;
+    if (N <= SORT_MAX) {
+      const int n = nckS[s];
+      r = 0;
+      for (int j = 0; j < N; ++j) {
+        const int m = nckS[j];
+        r += (m > n || (m == n && j < s)) ? 1 : 0;
+      }
+    }
+    sorder[r] = s;
+  }
+}
+
+// k_chunk_fill: one thread per chunk slot c < ncmax.  Its sequence is the last
+// one whose first chunk is <= c (first chunks never decrease, and an empty
+// sequence shares its first chunk with the next one), found by binary search;
+// slots past the last chunk are marked empty (len 0, seq -1).
+__global__ __launch_bounds__(NTHR) void k_chunk_fill(const SeqInfo* __restrict__ smap, int N,
+                                                     int ncmax, ChunkInfo* __restrict__ cmap) {
+  for (int c = blockIdx.x * NTHR + threadIdx.x; c < ncmax; c += gridDim.x * NTHR) {
+    int lo = 0, hi = N;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (smap[mid].chunk0 <= c) lo = mid + 1;
+      else hi = mid;
+    }
     ChunkInfo ci;
     ci.tok0 = 0;
     ci.len = 0;
     ci.seq = -1;
     ci.pad = 0;
+    if (lo > 0) {
+      const SeqInfo si = smap[lo - 1];
+      const int j = c - si.chunk0;
+      if (j < si.nchunks) {
+        ci.tok0 = si.tok0 + j * CH;
+        ci.len = min(CH, si.len - j * CH);
+        ci.seq = lo - 1;
+      }
+    }
     cmap[c] = ci;
   }
 }
@@ -893,7 +925,7 @@ __device__ __forceinline__ bf16x8 zero8() { return __builtin_bit_cast(bf16x8, u3
 
 // Chunk and sequence tables of the bf16 kernels: for fixed-length rows
 // (Tfix >= 0 tokens each) in closed form, for packed sequences (Tfix < 0) from
-// k_chunk_map's tables.
+// the tables of k_seq_map and k_chunk_fill.
 __device__ __forceinline__ ChunkInfo chunk_at(const ChunkInfo* cmap, int c, int Tfix) {
   if (Tfix >= 0) {
     const int ncs = max(1, (Tfix + CH - 1) / CH), s = c / ncs, i = c - s * ncs;
@@ -916,6 +948,25 @@ __device__ __forceinline__ SeqInfo seq_at(const SeqInfo* smap, int s, int Tfix) 
 // 1 KiB of whole lines (a row-major fragment would touch 16 half lines).
 __device__ __forceinline__ int frag_off(int row, int col) {
   return (((row >> 4) * 2 + (col >> 5)) * 64 + ((col >> 3) & 3) * 16 + (row & 15)) * 8 + (col & 7);
+}
+
+// Workgroup -> (sequence s, head h, dv slice zb) of the bf16 scans (a 1-D grid of
+// scan_blocks workgroups).  The NSL slices of one (sequence, head) chain are
+// workgroups 8 NSL g + 8 zb + c8: their indices agree mod 8, so the round-robin
+// dispatch puts them on the same XCD, and they are dispatched together, so the
+// K, Q, M, A rows they all read are L2 hits for all but the first.  Chains are
+// taken rank-major (r = chain / H), with packed sequences in the order of
+// sorder (longest first); padding workgroups past the last chain return.
+template <int NSL>
+__device__ __forceinline__ bool scan_item(int N, int H, const int* sorder, int& s, int& h, int& zb) {
+  const int L = blockIdx.x;
+  zb = (L >> 3) % NSL;
+  const int chain = (L / (8 * NSL)) * 8 + (L & 7);
+  if (chain >= N * H) return false;
+  const int r = chain / H;
+  h = chain - r * H;
+  s = sorder ? sorder[r] : r;
+  return true;
 }
 
 // four fp32 values -> bf16 (hi, lo) with hi + lo ~ x to ~16 significant bits
@@ -1202,7 +1253,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
     const bf16_t* __restrict__ beta, const bf16_t* __restrict__ beta_tilde,
     const float* __restrict__ d, const float* __restrict__ h0,
-    const SeqInfo* __restrict__ smap, int Tfix, int H, const int16_t* __restrict__ Mq,
+    const SeqInfo* __restrict__ smap, const int* __restrict__ sorder, int N, int Tfix, int H,
+    const int16_t* __restrict__ Mq,
     const float* __restrict__ Ms, const int16_t* __restrict__ Aq, const float* __restrict__ As,
     const float* __restrict__ Gw, float* __restrict__ o, float* __restrict__ ht, int16_t* __restrict__ Xq,
     float* __restrict__ Xs, int16_t* __restrict__ Dq, float* __restrict__ Ds,
@@ -1231,7 +1283,9 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
   constexpr int LDKC = DK + 24;  // 304-byte rows: conflict-free transposing reads
   __shared__ __align__(16) bf16_t Kc[CH * LDKC];
 
-  const int s = blockIdx.x, h = blockIdx.y, j0 = blockIdx.z * BV;
+  int s, h, zb;
+  if (!scan_item<DV / BV>(N, H, sorder, s, h, zb)) return;
+  const int j0 = zb * BV;
   const SeqInfo si = seq_at(smap, s, Tfix);
   const int w = wave_id(), lane = lane_id(), r16 = lane & 15, g4 = lane >> 4;
   const long soff = ((long)s * H + h) * DK * DV;
@@ -1361,7 +1415,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     load_rows(0);
     put_rows(0);
     if constexpr (STORE) {
-      const long xb = (c_chh(0) * NB + blockIdx.z) * DK;
+      const long xb = (c_chh(0) * NB + zb) * DK;
       store_state_q(Xq + xb * BV, Xs + xb);
     }
   }
@@ -1451,7 +1505,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
         m = nmax_abs4(m, dl[nt]);
       m = rowgroup_max(m);
       const float inv = q_inv_scale(m);
-      const long row = (chh * NB + blockIdx.z) * CH + prow;  // the slice's block
+      const long row = (chh * NB + zb) * CH + prow;  // the slice's block
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt)
         *reinterpret_cast<uint2*>(Dq + row * BV + 16 * nt + col0) = q_pack4(dl[nt], inv);
@@ -1527,7 +1581,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     put_state();
     // state entering the next chunk (after the last chunk: the final state)
     if constexpr (STORE) {
-      const long xb = ((more ? c_chh(cc + 1) : (long)s * H + h) * NB + blockIdx.z) * DK;
+      const long xb = ((more ? c_chh(cc + 1) : (long)s * H + h) * NB + zb) * DK;
       store_state_q((more ? Xq : Xfq) + xb * BV, (more ? Xs : Xfs) + xb);
     }
     put_rows(buf ^ 1);
@@ -1545,7 +1599,8 @@ template <int DK, int DV, int BV>
 __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ dO,
     const bf16_t* __restrict__ beta_tilde, const float* __restrict__ d, const float* __restrict__ dht,
-    const SeqInfo* __restrict__ smap, int Tfix, int H, const int16_t* __restrict__ MTq,
+    const SeqInfo* __restrict__ smap, const int* __restrict__ sorder, int N, int Tfix, int H,
+    const int16_t* __restrict__ MTq,
     const float* __restrict__ MTs, const int16_t* __restrict__ ATq, const float* __restrict__ ATs,
     const bf16_t* __restrict__ QTp,
     const float* __restrict__ Gw, float* __restrict__ dh0, int16_t* __restrict__ Yq,
@@ -1566,7 +1621,9 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
   __shared__ __align__(16) bf16_t W2h[CH * LDT];
   __shared__ __align__(16) bf16_t W2l[CH * LDT];
 
-  const int s = blockIdx.x, h = blockIdx.y, j0 = blockIdx.z * BV;
+  int s, h, zb;
+  if (!scan_item<DV / BV>(N, H, sorder, s, h, zb)) return;
+  const int j0 = zb * BV;
   const SeqInfo si = seq_at(smap, s, Tfix);
   const int w = wave_id(), lane = lane_id(), r16 = lane & 15, g4 = lane >> 4;
   const long soff = ((long)s * H + h) * DK * DV;
@@ -1722,7 +1779,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     const long chh = c_chh(cc);
     const int buf = cc & 1;
     const int clen = c_len(cc);
-    store_state_q(Yq + (chh * NB + blockIdx.z) * DK * BV, Ys + (chh * NB + blockIdx.z) * DK);
+    store_state_q(Yq + (chh * NB + zb) * DK * BV, Ys + (chh * NB + zb) * DK);
     load_rows(nx);
     load_do(nx);
     const float glast = Grow[buf][CH - 1];
@@ -1802,7 +1859,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
         m = nmax_abs4(m, drr[nt]);
       m = rowgroup_max(m);
       const float inv = q_inv_scale(m);
-      const long row = (chh * NB + blockIdx.z) * CH + prow;  // the slice's block
+      const long row = (chh * NB + zb) * CH + prow;  // the slice's block
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt)
         *reinterpret_cast<uint2*>(dRq + row * BV + 16 * nt + col0) = q_pack4(drr[nt], inv);
@@ -2879,6 +2936,21 @@ static unsigned intra_bwd_grid(long items) {
   return (unsigned)(cus > 0 && cus < items ? cus : items);
 }
 
+// 1-D grid of the bf16 scans: whole groups of 8 chains (see scan_item).
+static unsigned scan_blocks(int N, int H, int nsl) {
+  return (unsigned)((((long)N * H + 7) / 8) * 8 * nsl);
+}
+
+// Sequence and chunk tables: the per-sequence scan (one workgroup), then one
+// thread per chunk slot.
+static void launch_chunk_map(const LaunchArgs& a, hipStream_t st) {
+  k_seq_map<<<1, NTHR, 0, st>>>(a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.ncmax, a.smap, a.sorder);
+  if (a.ncmax > 0) {
+    const int blocks = (a.ncmax + NTHR - 1) / NTHR;
+    k_chunk_fill<<<blocks < 1024 ? blocks : 1024, NTHR, 0, st>>>(a.smap, a.N, a.ncmax, a.cmap);
+  }
+}
+
 template <typename Tin, int DK, int DV>
 static hipError_t run_fwd(const LaunchArgs& a) {
   hipStream_t st = a.stream;
@@ -2888,7 +2960,7 @@ static hipError_t run_fwd(const LaunchArgs& a) {
   const Tin* beta = static_cast<const Tin*>(a.beta);
   const Tin* bt = static_cast<const Tin*>(a.beta_tilde);
   a.stage("chunk_map");
-  k_chunk_map<<<1, NTHR, 0, st>>>(a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.ncmax, a.cmap, a.smap);
+  launch_chunk_map(a, st);
   a.stage("prep");
   if (a.ncmax > 0)
     k_prep<Tin, DK><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(q, k, a.g, bt, a.d, a.cmap, a.H, a.Mw,
@@ -2921,7 +2993,7 @@ static hipError_t run_bwd(const LaunchArgs& a) {
   }
   if (!a.saved) {
     a.stage("chunk_map");
-    k_chunk_map<<<1, NTHR, 0, st>>>(a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.ncmax, a.cmap, a.smap);
+    launch_chunk_map(a, st);
     a.stage("prep");
     if (a.ncmax > 0)
       k_prep<Tin, DK><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(q, k, a.g, bt, a.d, a.cmap, a.H,
@@ -2955,9 +3027,10 @@ static hipError_t run_fwd_bf(const LaunchArgs& a) {
   const bf16_t* bt = static_cast<const bf16_t*>(a.beta_tilde);
   // fixed-length rows need no tables (closed form in the kernels)
   const int Tfix = a.cu_seqlens ? -1 : a.Tseq;
+  const int* sord = Tfix < 0 ? a.sorder : nullptr;
   if (Tfix < 0) {
     a.stage("chunk_map");
-    k_chunk_map<<<1, NTHR, 0, st>>>(a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.ncmax, a.cmap, a.smap);
+    launch_chunk_map(a, st);
   }
   a.stage(a.saved ? "prep_save" : "prep");
   if (a.ncmax > 0) {
@@ -2972,12 +3045,12 @@ static hipError_t run_fwd_bf(const LaunchArgs& a) {
   }
   a.stage(a.saved ? "scan_fwd_save" : "scan_fwd");
   if (a.saved)
-    k_scan_fwd_bf<DK, DV, SCAN_BV, true, true><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-        q, k, v, beta, bt, a.d, a.h0, a.smap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, a.o, a.ht, a.Xq, a.Xs,
+    k_scan_fwd_bf<DK, DV, SCAN_BV, true, true><<<scan_blocks(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
+        q, k, v, beta, bt, a.d, a.h0, a.smap, sord, a.N, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, a.o, a.ht, a.Xq, a.Xs,
         a.Dq, a.Ds, a.Xfq, a.Xfs, a.sink);
   else
-    k_scan_fwd_bf<DK, DV, SCAN_BV, true, false><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-        q, k, v, beta, bt, a.d, a.h0, a.smap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, a.o, a.ht, nullptr,
+    k_scan_fwd_bf<DK, DV, SCAN_BV, true, false><<<scan_blocks(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
+        q, k, v, beta, bt, a.d, a.h0, a.smap, sord, a.N, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, a.o, a.ht, nullptr,
         nullptr, nullptr, nullptr, nullptr, nullptr, a.sink);
   a.stage(nullptr);
   return hipGetLastError();
@@ -2998,10 +3071,11 @@ static hipError_t run_bwd_bf(const LaunchArgs& a) {
   }
   // fixed-length rows need no tables (closed form in the kernels)
   const int Tfix = a.cu_seqlens ? -1 : a.Tseq;
+  const int* sord = Tfix < 0 ? a.sorder : nullptr;
   if (!a.saved) {
     if (Tfix < 0) {
       a.stage("chunk_map");
-      k_chunk_map<<<1, NTHR, 0, st>>>(a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.ncmax, a.cmap, a.smap);
+      launch_chunk_map(a, st);
     }
     a.stage("prep");
     if (a.ncmax > 0)
@@ -3009,13 +3083,13 @@ static hipError_t run_bwd_bf(const LaunchArgs& a) {
           q, k, a.g, bt, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.MTq, a.MTs, a.ATq, a.ATs,
           a.QTp, a.Gw, a.sink);
     a.stage("scan_fwd_store");
-    k_scan_fwd_bf<DK, DV, SCAN_BV, false, true><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-        q, k, v, beta, bt, a.d, a.h0, a.smap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, nullptr, nullptr, a.Xq,
+    k_scan_fwd_bf<DK, DV, SCAN_BV, false, true><<<scan_blocks(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
+        q, k, v, beta, bt, a.d, a.h0, a.smap, sord, a.N, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, nullptr, nullptr, a.Xq,
         a.Xs, a.Dq, a.Ds, a.Xfq, a.Xfs, a.sink);
   }
   a.stage("scan_bwd");
-  k_scan_bwd_bf<DK, DV, SCAN_BV><<<dim3(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-      q, k, dO, bt, a.d, a.dht, a.smap, Tfix, a.H, a.MTq, a.MTs, a.ATq, a.ATs, a.QTp, a.Gw, a.dh0, a.Yq,
+  k_scan_bwd_bf<DK, DV, SCAN_BV><<<scan_blocks(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
+      q, k, dO, bt, a.d, a.dht, a.smap, sord, a.N, Tfix, a.H, a.MTq, a.MTs, a.ATq, a.ATs, a.QTp, a.Gw, a.dh0, a.Yq,
       a.Ys, a.dRq, a.dRs, a.sink);
   a.stage("intra_bwd");
   if constexpr (DK > 128 || DV > 128) {

@@ -40,6 +40,7 @@ struct LaunchArgs {
   // workspace views
   ChunkInfo* cmap;
   SeqInfo* smap;
+  int* sorder;  // packed sequences in the order the scans take them (longest first)
   float *Mw, *Aw, *Gw;            // per chunk-head: M, A (64 x 64), G (64)
   float *Xw, *Dw, *Yw, *dRw;      // per chunk-head: X (dk x dv), D (64 x dv), Y, dR
   float* ddp;                     // per chunk-head partial dd
