@@ -90,7 +90,8 @@ hipError_t launch_recurrent(const RecurrentArgs& a);
 struct PrologueArgs {
   bool bf16;
   int dk, dv, H, N, Tseq, Ttot;
-  int nruns;  // 64-token runs of the packed token axis
+  int nruns;  // 64-token runs of the packed token axis (backward)
+  int frun;   // tokens per run of the forward (set by its launcher)
   float eps;
   const int32_t* cu_seqlens;
   const void *xq, *xk, *xv;     // pre-activations (in_dtype)

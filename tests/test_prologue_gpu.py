@@ -76,6 +76,9 @@ CASES = [
     ("f32_d64", dict(B=2, T=70, H=2, dk=64, dv=64, in_dtype="f32")),
     ("f32_dk128_dv256", dict(B=1, T=66, H=1, dk=128, dv=256, in_dtype="f32")),
     ("bf16_T3", dict(B=3, T=3, H=2, dk=128, dv=128, in_dtype="bf16")),
+    # head counts that leave the forward's last group of heads partly empty
+    ("bf16_d128_H5", dict(B=2, T=333, H=5, dk=128, dv=128, in_dtype="bf16")),
+    ("bf16_d256_H3", dict(B=1, T=517, H=3, dk=256, dv=256, in_dtype="bf16")),
     # packed sequences: empty ones, sequences shorter than the taps, boundaries
     # inside a run and exactly at run edges
     ("bf16_varlen", dict(H=2, dk=128, dv=128, in_dtype="bf16",
