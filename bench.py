@@ -52,12 +52,13 @@ def stage_model(name, B, T, H, dk, dv, C=64, in_bytes=2, sep_bt=False):
 
     Per chunk-head (C tokens of one head): the dense products the stage performs
     (2 m n k flops each) and the HBM bytes it must move at minimum (each operand
-    read once, each result written once; L2 re-reads excluded).  M, A and their
-    transposes count 2 bytes per element plus one 4-byte scale per row, the
+    read once, each result written once; L2 re-reads excluded).  M and A count
+    2 bytes per element plus one 4-byte scale per row (M) or column (A), the
     chunk states X, Y and pseudo-values D, dR handed from the scans to the
     backward gradient kernel 2 bytes per element plus one 4-byte scale per 32
-    elements (their int16 storage); the Q^T copy made by the prep stage is
-    counted where it is written and read (K^T is formed on chip from K).
+    elements (their int16 storage).  The reverse scan transposes M, A and K on
+    chip; the Q^T copy made by the prep stage of the training pair is counted
+    where it is written and read.
     ``sep_bt``: a separate feedback strength beta~ (read where beta and beta~
     both act: the forward scan and the gradient kernel, which also writes
     dbeta~; the prep and reverse scan read beta~ in place of beta).
@@ -67,14 +68,14 @@ def stage_model(name, B, T, H, dk, dv, C=64, in_bytes=2, sep_bt=False):
     qk = C * dk * in_bytes          # one of q, k (or its transpose)
     vv = C * dv * in_bytes          # one of v, dO
     gb = C * (f4 + in_bytes)        # g (or G) and beta
-    cc = C * C * 2 + C * f4         # one stored C x C matrix (int16 + row scales)
+    cc = C * C * 2 + C * f4         # one stored C x C matrix (int16 + row / column scales)
     st = dk * dv * 2 + dk * (dv // 32) * f4     # one stored state (int16 + scales)
     cd = C * dv * 2 + C * (dv // 32) * f4       # one stored C x dv matrix
     if name in ("prep", "prep_save"):    # K K^T, Q K^T; q, k, g, beta -> M, A, G
         fl = 4 * C * C * dk
         by = 2 * qk + gb + 2 * cc + C * f4
-        if name == "prep_save":           # + M^T, A^T, Q^T for the backward
-            by += 2 * cc + qk
+        if name == "prep_save":           # + Q^T for the backward
+            by += qk
     elif name in ("scan_fwd", "scan_fwd_save"):  # K X, Q X, M R, A D, K^T D
         fl = 6 * C * dk * dv + 4 * C * C * dv
         by = 2 * qk + vv + 2 * cc + gb + C * dv * f4   # q, k, v, M, A, g, beta -> o (fp32)
@@ -87,7 +88,7 @@ def stage_model(name, B, T, H, dk, dv, C=64, in_bytes=2, sep_bt=False):
         by = qk + vv + cc + gb + st + cd
     elif name == "scan_bwd":      # K Y, A^T dO, M^T dD, Q^T Pg, K^T W2; -> Y, dR
         fl = 6 * C * dk * dv + 4 * C * C * dv
-        by = 2 * qk + vv + 2 * cc + gb + st + cd      # k, Q^T, dO, M^T, A^T, g, beta
+        by = 2 * qk + vv + 2 * cc + gb + st + cd      # k, Q^T, dO, M, A, g, beta
     elif name == "intra_bwd":     # 3 C x dk x dv, 2 C x C x dv, 5 C x C x dk products
         fl = 6 * C * dk * dv + 4 * C * C * dv + 10 * C * C * dk
         by = (2 * qk + 2 * vv + 2 * st + 2 * cd + gb          # q,k,v,dO,X,Y,D,dR

@@ -95,9 +95,9 @@ comba_status check_shape_recurrent(const comba_shape* s, Dims* out) {
 }
 
 struct Layout {
-  size_t cmap, smap, sord, M, A, G, X, D, Y, dR, ddp, MT, AT, QT, Xfin, sink, total;
+  size_t cmap, smap, sord, M, A, G, X, D, Y, dR, ddp, QT, Xfin, sink, total;
   size_t Xs, Ds, Ys, dRs, Xfs;  // bf16 path: scales of the int16 X, D, Y, dR, final-state sink
-  size_t Ms, As, MTs, ATs;       // bf16 path: row scales of the int16 M, A, M^T, A^T
+  size_t Ms, As;                // bf16 path: row scales of M, column scales of A
 };
 
 Layout layout(const Dims& d, bool bwd) {
@@ -115,20 +115,16 @@ Layout layout(const Dims& d, bool bwd) {
   L.sord = take((size_t)(d.N > 0 ? d.N : 1) * sizeof(int));
   L.G = take(chh * kChunk * sizeof(float));
   if (d.bf16) {
-    // bf16 path: M, A as int16 with row scales; the backward
-    // also keeps M^T, A^T (int16 + row scales) and Q^T
+    // bf16 path: M, A as int16 with row (M) and column (A) scales; the
+    // backward also keeps Q^T
     L.M = take(chh * kChunk * kChunk * sizeof(int16_t));
     L.Ms = take(chh * kChunk * sizeof(float));
     L.A = take(chh * kChunk * kChunk * sizeof(int16_t));
     L.As = take(chh * kChunk * sizeof(float));
     if (bwd) {
-      // M^T, A^T, Q^T; X, D, Y, dR as int16 + one fp32 scale per 32 values
+      // Q^T; X, D, Y, dR as int16 + one fp32 scale per 32 values
       const size_t nf = (size_t)(d.N > 0 ? d.N : 1) * d.H;
       const size_t nb = d.dv / 32;
-      L.MT = take(chh * kChunk * kChunk * sizeof(int16_t));
-      L.MTs = take(chh * kChunk * sizeof(float));
-      L.AT = take(chh * kChunk * kChunk * sizeof(int16_t));
-      L.ATs = take(chh * kChunk * sizeof(float));
       L.QT = take(chh * d.dk * kChunk * sizeof(uint16_t));
       L.Xfin = take(nf * d.dk * d.dv * sizeof(int16_t));
       L.Xfs = take(nf * d.dk * nb * sizeof(float));
@@ -209,13 +205,7 @@ void carve(comba::LaunchArgs& a, const Layout& L, void* ws, bool bwd) {
     a.Ms = reinterpret_cast<float*>(base + L.Ms);
     a.Aq = reinterpret_cast<int16_t*>(base + L.A);
     a.As = reinterpret_cast<float*>(base + L.As);
-    if (bwd) {
-      a.MTq = reinterpret_cast<int16_t*>(base + L.MT);
-      a.MTs = reinterpret_cast<float*>(base + L.MTs);
-      a.ATq = reinterpret_cast<int16_t*>(base + L.AT);
-      a.ATs = reinterpret_cast<float*>(base + L.ATs);
-      a.QTp = reinterpret_cast<uint16_t*>(base + L.QT);
-    }
+    if (bwd) a.QTp = reinterpret_cast<uint16_t*>(base + L.QT);
   }
   if (bwd && a.bf16) {
     a.Xfq = reinterpret_cast<int16_t*>(base + L.Xfin);

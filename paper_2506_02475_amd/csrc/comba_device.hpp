@@ -258,6 +258,12 @@ __device__ __forceinline__ uint2 q_pack4(const floatx4& x, float inv) {
   const auto b = __builtin_amdgcn_cvt_pknorm_i16(x[2] * inv, x[3] * inv);
   return make_uint2(__builtin_bit_cast(uint32_t, a), __builtin_bit_cast(uint32_t, b));
 }
+// The same with one inverse scale per value (four columns with column scales).
+__device__ __forceinline__ uint2 q_pack4v(const floatx4& x, const floatx4& inv) {
+  const auto a = __builtin_amdgcn_cvt_pknorm_i16(x[0] * inv[0], x[1] * inv[1]);
+  const auto b = __builtin_amdgcn_cvt_pknorm_i16(x[2] * inv[2], x[3] * inv[3]);
+  return make_uint2(__builtin_bit_cast(uint32_t, a), __builtin_bit_cast(uint32_t, b));
+}
 __device__ __forceinline__ float4 q_unpack4(uint2 u, float s) {
   return make_float4((float)(int)(int16_t)(u.x & 0xFFFFu) * s, (float)((int)u.x >> 16) * s,
                      (float)(int)(int16_t)(u.y & 0xFFFFu) * s, (float)((int)u.y >> 16) * s);

@@ -1016,32 +1016,14 @@ __device__ __forceinline__ void solve_block_column(const float* Ls, floatx4 (&mb
   }
 }
 
-// Block column J of M (mb as left by solve_block_column) into LDS over L, and
-// with BWD the rows 16 J .. 16 J + 15 of M^T (= columns of M) as int16 with
-// one scale per row, in fragment order (Mt = the chunk-head's M^T): lane
-// (g4, r16) holds rows 4 g4 .. 4 g4 + 3 of every block of column 16 J + r16,
-// i.e. 8-byte pieces of row 16 J + r16 of M^T.
-template <int J, int LDL, bool BWD>
-__device__ __forceinline__ void put_block_column(float* Ls, const floatx4 (&mb)[4], int16_t* Mt,
-                                                 float* MTs) {
+// Block column J of M (mb as left by solve_block_column) into LDS over L.
+template <int J, int LDL>
+__device__ __forceinline__ void put_block_column(float* Ls, const floatx4 (&mb)[4]) {
   const int lane = lane_id(), r16 = lane & 15, g4 = lane >> 4;
 #pragma unroll
   for (int i = J + 1; i < 4; ++i)
 #pragma unroll
     for (int e = 0; e < 4; ++e) Ls[(16 * i + 4 * g4 + e) * LDL + 16 * J + r16] = mb[i][e];
-  if constexpr (BWD) {
-    float m = 0.f;
-#pragma unroll
-    for (int i = J; i < 4; ++i) m = nmax_abs4(m, mb[i]);
-    m = nmax(m, __shfl_xor(m, 16));
-    m = nmax(m, __shfl_xor(m, 32));
-    const float inv = q_inv_scale(m);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      *reinterpret_cast<uint2*>(Mt + frag_off(16 * J + r16, 16 * i + 4 * g4)) =
-          i < J ? make_uint2(0u, 0u) : q_pack4(mb[i], inv);
-    MTs[16 * J + r16] = q_scale(m);  // the four lanes of a row store the same value
-  }
 }
 
 template <int DK, bool BWD>
@@ -1049,11 +1031,13 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const float* __restrict__ g,
     const bf16_t* __restrict__ beta_tilde, const float* __restrict__ d,
     const ChunkInfo* __restrict__ cmap, int Tfix, int H, int16_t* __restrict__ Mq, float* __restrict__ Ms, int16_t* __restrict__ Aq,
-    float* __restrict__ As, int16_t* __restrict__ MTq, float* __restrict__ MTs,
-    int16_t* __restrict__ ATq, float* __restrict__ ATs, bf16_t* __restrict__ QTp,
-    float* __restrict__ Gw, float* __restrict__ sink) {
-  // M, A (and M^T, A^T) leave as int16 rows with one power-of-two scale per row
-  // (see q_pack4): the scans fold the scale into their accumulator rows
+    float* __restrict__ As, bf16_t* __restrict__ QTp, float* __restrict__ Gw, float* __restrict__ sink) {
+  // M leaves as int16 with one power-of-two scale per row, A with one per
+  // column (see q_pack4).  The forward scan takes M's row scale out of the
+  // rows of M R and folds A's column scale into the matching rows of D before
+  // A D; the reverse scan reads both tiles transposed (M^T dD, A^T dO), folds
+  // M's row scale into the rows of dD and takes A's column scale out of the
+  // rows of A^T dO.  With BWD it also stores Q^T for the reverse scan.
   constexpr int LDK = DK + 24;  // 304-byte rows: conflict-free 16-byte and transposing reads
   constexpr int LDL = CH + 4;
   constexpr int CC = CH * CH;
@@ -1065,7 +1049,7 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
   bf16_t* Qs = reinterpret_cast<bf16_t*>(QLbuf);
   float* Ls = reinterpret_cast<float*>(QLbuf);
   __shared__ float Gs[CH], Bs[CH];
-  __shared__ float colmax[BWD ? NWAVE : 1][CH];  // per-wave column maxima of |A|
+  __shared__ float colmax[NWAVE][CH];  // per-wave column maxima of |A|
 
   const ChunkInfo ci = chunk_at(cmap, blockIdx.x, Tfix);
   if (ci.len <= 0) return;
@@ -1109,7 +1093,7 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
   mma<false, 1, 4, DK>(aqk, Qs + 16 * w * LDK, LDK, Ks, LDK);
   __syncthreads();  // every read of the Q tile is done: L overwrites it
   // A in the accumulator layout: av[nt][e] = A[16w + 4g4 + e][16nt + r16]
-  float av[4][4], rmax[4] = {0.f, 0.f, 0.f, 0.f};
+  float av[4][4];
 #pragma unroll
   for (int nt = 0; nt < 4; ++nt) {
 #pragma unroll
@@ -1120,50 +1104,34 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
       if (r >= c) a = (aqk[0][nt][e] - dh * kk) * __expf(Gs[r] - Gs[c]);
       if (r > c) l = Bs[r] * __expf(Gs[r - 1] - Gs[c]) * kk;
       av[nt][e] = a;
-      rmax[e] = nmax(rmax[e], fabsf(a));
       Ls[r * LDL + c] = l;
     }
   }
+  // column maxima of this wave's 16 rows, combined over the waves below
 #pragma unroll
-  for (int e = 0; e < 4; ++e) rmax[e] = max16(rmax[e]);  // over the row's 64 columns
-  {
-    // A rows leave as 8-byte pieces of four columns (see quad_transpose); the
-    // lane's row after the transpose is 16w + 4g4 + (lane & 3)
-    const int i = lane & 3;
-    const float mrow = i == 0 ? rmax[0] : i == 1 ? rmax[1] : i == 2 ? rmax[2] : rmax[3];
-    const float inv = q_inv_scale(mrow);
-#pragma unroll
-    for (int nt = 0; nt < 4; ++nt)
-      *reinterpret_cast<uint2*>(Aq + chh * CC + frag_off(16 * w + qt_row(), 16 * nt + qt_col())) =
-          q_pack4(quad_transpose(floatx4{av[nt][0], av[nt][1], av[nt][2], av[nt][3]}), inv);
-    const float4 sc = make_float4(q_scale(rmax[0]), q_scale(rmax[1]), q_scale(rmax[2]),
-                                  q_scale(rmax[3]));
-    // the 16 lanes of a group hold the same four scales and store them alike
-    *reinterpret_cast<float4*>(As + chh * CH + 16 * w + 4 * g4) = sc;
-  }
-  if constexpr (BWD) {
-    // column maxima of this wave's 16 rows, combined over the waves below
-#pragma unroll
-    for (int nt = 0; nt < 4; ++nt) {
-      float m = nmax_abs4(0.f, floatx4{av[nt][0], av[nt][1], av[nt][2], av[nt][3]});
-      m = nmax(m, __shfl_xor(m, 16));
-      m = nmax(m, __shfl_xor(m, 32));
-      if (g4 == 0) colmax[w][16 * nt + r16] = m;
-    }
+  for (int nt = 0; nt < 4; ++nt) {
+    float m = nmax_abs4(0.f, floatx4{av[nt][0], av[nt][1], av[nt][2], av[nt][3]});
+    m = nmax(m, __shfl_xor(m, 16));
+    m = nmax(m, __shfl_xor(m, 32));
+    if (g4 == 0) colmax[w][16 * nt + r16] = m;
   }
   __syncthreads();
-
-  if constexpr (BWD) {
-    // A^T rows (= columns c of A) as 8-byte pieces: this lane's column c, rows
-    // 16w + 4g4 .. +3
+  {
+    auto col_max = [&](int c) {
+      return nmax(nmax(colmax[0][c], colmax[1][c]), nmax(colmax[2][c], colmax[3][c]));
+    };
+    // A rows leave as 8-byte pieces of four columns (see quad_transpose): the
+    // lane's row after the transpose is 16w + qt_row(), its columns
+    // 16nt + qt_col() .. +3, each with its own column scale
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt) {
-      const int c = 16 * nt + r16;
-      const float m = nmax(nmax(colmax[0][c], colmax[1][c]), nmax(colmax[2][c], colmax[3][c]));
-      *reinterpret_cast<uint2*>(ATq + chh * CC + frag_off(c, 16 * w + 4 * g4)) =
-          q_pack4(floatx4{av[nt][0], av[nt][1], av[nt][2], av[nt][3]}, q_inv_scale(m));
-      if (w == 0) ATs[chh * CH + c] = q_scale(m);  // equal in the four lane groups
+      const int c0 = 16 * nt + qt_col();
+      const floatx4 inv = {q_inv_scale(col_max(c0)), q_inv_scale(col_max(c0 + 1)),
+                           q_inv_scale(col_max(c0 + 2)), q_inv_scale(col_max(c0 + 3))};
+      *reinterpret_cast<uint2*>(Aq + chh * CC + frag_off(16 * w + qt_row(), c0)) =
+          q_pack4v(quad_transpose(floatx4{av[nt][0], av[nt][1], av[nt][2], av[nt][3]}), inv);
     }
+    if (w == 0) As[chh * CH + lane] = q_scale(col_max(lane));
   }
 
   // M = (I + L)^{-1} by 16x16 blocks (L is strictly lower triangular, so M is
@@ -1212,15 +1180,11 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
     default: break;
   }
   __syncthreads();  // every read of L is done
-  {
-    int16_t* Mt = BWD ? MTq + chh * CC : nullptr;
-    float* Mts = BWD ? MTs + chh * CH : nullptr;
-    switch (jb) {
-      case 0: put_block_column<0, LDL, BWD>(Ls, mb, Mt, Mts); break;
-      case 1: put_block_column<1, LDL, BWD>(Ls, mb, Mt, Mts); break;
-      case 2: put_block_column<2, LDL, BWD>(Ls, mb, Mt, Mts); break;
-      default: put_block_column<3, LDL, BWD>(Ls, mb, Mt, Mts); break;
-    }
+  switch (jb) {
+    case 0: put_block_column<0, LDL>(Ls, mb); break;
+    case 1: put_block_column<1, LDL>(Ls, mb); break;
+    case 2: put_block_column<2, LDL>(Ls, mb); break;
+    default: put_block_column<3, LDL>(Ls, mb); break;
   }
   __syncthreads();
   // M rows from LDS as 16-byte pieces of eight columns; the 8 threads of a row
@@ -1351,8 +1315,9 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
   auto c_chh = [&](int cc) { return (long)(si.chunk0 + cc) * H + h; };
 
   // per-chunk operands, loaded one chunk ahead: K, Q rows as bf16, the rows of
-  // M and A as int16 with their row scales (applied to the accumulator rows:
-  // (M R)[r] = s_r sum_i q[r][i] R[i])
+  // M and A as int16 with M's row scale (applied to the accumulator rows:
+  // (M R)[r] = s_r sum_i q[r][i] R[i]) and A's column scale (applied to the
+  // rows of D before A D: (A D)[r] = sum_c q[r][c] (s_c D[c]))
   bf16x8 kf[KS], qf[KS];
   uint4 mq[2], aq[2];
   float msc, asc;
@@ -1519,7 +1484,11 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
         const float dgv[4] = {edec * dv[0], edec * dv[1], edec * dv[2], edec * dv[3]};
         const int off = prow * LDT + 16 * nt + col0;
         put_t4(Dgh, Dgl, off, dgv);
-        if constexpr (OUT) put_t4(Dh, Dl, off, dv);
+        if constexpr (OUT) {
+          // times A's column scale for column prow (a power of two: exact)
+          const float dav[4] = {asc * dv[0], asc * dv[1], asc * dv[2], asc * dv[3]};
+          put_t4(Dh, Dl, off, dav);
+        }
       }
     }
     __syncthreads();
@@ -1566,13 +1535,12 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
           adc[nt] = mfma16(dh_, al, adc[nt]);
         }
       }
-      const float as_cur = asc;
       load_a(nx);
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt) {
         floatx4 ov;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) ov[e] = oacc[nt][e] + as_cur * adc[nt][e];
+        for (int e = 0; e < 4; ++e) ov[e] = oacc[nt][e] + adc[nt][e];
         float* dst = prow < len ? o + (tok + (long)prow * H) * DV + j0 + 16 * nt + col0
                                 : sink + 4 * lane;
         store4(dst, ov);
@@ -1600,8 +1568,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ dO,
     const bf16_t* __restrict__ beta_tilde, const float* __restrict__ d, const float* __restrict__ dht,
     const SeqInfo* __restrict__ smap, const int* __restrict__ sorder, int N, int Tfix, int H,
-    const int16_t* __restrict__ MTq,
-    const float* __restrict__ MTs, const int16_t* __restrict__ ATq, const float* __restrict__ ATs,
+    const int16_t* __restrict__ Mq,
+    const float* __restrict__ Ms, const int16_t* __restrict__ Aq, const float* __restrict__ As,
     const bf16_t* __restrict__ QTp,
     const float* __restrict__ Gw, float* __restrict__ dh0, int16_t* __restrict__ Yq,
     float* __restrict__ Ys, int16_t* __restrict__ dRq, float* __restrict__ dRs,
@@ -1685,15 +1653,25 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
   auto c_tok = [&](int cc) { return (long)(si.tok0 + cc * CH) * H + h; };
   auto c_chh = [&](int cc) { return (long)(si.chunk0 + cc) * H + h; };
 
-  // A^T, M^T rows as int16 with their row scales (applied to the accumulator rows)
-  bf16x8 kf[KS], qtf[XMT][2];
-  // the chunk's K rows, staged from the K operand registers: the state update
+  // The chunk's K rows, staged from the K operand registers: the state update
   // takes its K operand (reduction down the chunk rows) from here with
-  // transposing reads
+  // transposing reads.  Q^T comes from prep in fragment order (staging Q rows
+  // like K cost this scan more than the copy saves).
+  bf16x8 kf[KS], qtf[XMT][2];
   constexpr int LDKC = DK + 24;  // 304-byte rows: conflict-free transposing reads
   __shared__ __align__(16) bf16_t Kc[CH * LDKC];
-  uint4 atq[2], mtq[2];
-  float atsc, mtsc;
+  // M and A of the chunk as int16, row-major: each lane stores the 16 bytes it
+  // loads in fragment order (8 consecutive columns of one row), and transposing
+  // reads return the B operands of M^T dD and A^T dO.  M's row scale is folded
+  // into the rows of dD (exact: a power of two), A's column scale taken out of
+  // the rows of A^T dO.  A is read at the start of a chunk, so the next
+  // chunk's A is staged at the end of the current one; M is staged in the
+  // chunk's first phase and read in its second.
+  constexpr int LDM = CH + 8;  // 144-byte rows: a transposing read's four rows on disjoint banks
+  __shared__ __align__(16) int16_t Mt_s[CH * LDM];
+  __shared__ __align__(16) int16_t At_s[CH * LDM];
+  uint4 aq[2], mq[2];
+  float asc, msc;
   // per-row values (G, beta~) and the dO slice are loaded one chunk ahead into
   // registers and staged through double-buffered LDS at the end of each chunk
   __shared__ float Grow[2][CH], Brow[2][CH];
@@ -1707,17 +1685,30 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) kf[ks] = ld8(k + rb + 32 * ks);
   };
-  auto load_at = [&](int cc) {
-    const int16_t* p = ATq + c_chh(cc) * CC + (2 * w * 64 + lane) * 8;  // fragment order
+  // A's fragments and the column scale of A's column prow
+  auto load_a = [&](int cc) {
+    const int16_t* p = Aq + c_chh(cc) * CC + (2 * w * 64 + lane) * 8;  // fragment order
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) atq[ks] = *reinterpret_cast<const uint4*>(p + ks * 512);
-    atsc = ATs[c_chh(cc) * CH + prow];
+    for (int ks = 0; ks < 2; ++ks) aq[ks] = *reinterpret_cast<const uint4*>(p + ks * 512);
+    asc = As[c_chh(cc) * CH + prow];
   };
-  auto load_mt = [&](int cc) {
-    const int16_t* p = MTq + c_chh(cc) * CC + (2 * w * 64 + lane) * 8;  // fragment order
+  // M's fragments and the scale of M's row prow
+  auto load_m = [&](int cc) {
+    const int16_t* p = Mq + c_chh(cc) * CC + (2 * w * 64 + lane) * 8;  // fragment order
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) mtq[ks] = *reinterpret_cast<const uint4*>(p + ks * 512);
-    mtsc = MTs[c_chh(cc) * CH + prow];
+    for (int ks = 0; ks < 2; ++ks) mq[ks] = *reinterpret_cast<const uint4*>(p + ks * 512);
+    msc = Ms[c_chh(cc) * CH + prow];
+  };
+  // fragment (row 16 w + r16, columns 32 ks + 8 g4 ..) to its row-major place
+  // (the fragments by value: a reference to the register arrays would keep
+  // them in memory)
+  auto put_frag = [&](int16_t* t, uint4 r0, uint4 r1) {
+    *reinterpret_cast<uint4*>(t + (16 * w + r16) * LDM + 8 * g4) = r0;
+    *reinterpret_cast<uint4*>(t + (16 * w + r16) * LDM + 32 + 8 * g4) = r1;
+  };
+  // lane (g4, r16): column 16 w + r16 of the tile at rows 32 ks + 8 g4 .. +7
+  auto get_tr = [&](const int16_t* t, int ks) {
+    return __builtin_bit_cast(uint4, ld_tr8(reinterpret_cast<const bf16_t*>(t), LDM, 32 * ks + 8 * g4, 16 * w));
   };
   auto load_qt = [&](int cc) {
     // fragment order: rows (DK/4) w + 16 mt + i are row block w XMT + mt
@@ -1764,12 +1755,13 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
   if (n > 0) {
     load_do(n - 1);
     load_k(n - 1);
-    load_at(n - 1);
-    load_mt(n - 1);
+    load_a(n - 1);
+    load_m(n - 1);
     load_qt(n - 1);
     load_rows(n - 1);
     put_rows((n - 1) & 1);
     put_do((n - 1) & 1);
+    put_frag(At_s, aq[0], aq[1]);  // the loop stages each next chunk's A
   }
   __syncthreads();
 
@@ -1804,7 +1796,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
       bf16x8 ath, atl;
-      q_split8(atq[ks], ath, atl);
+      q_split8(get_tr(At_s, ks), ath, atl);
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt) {
         const bf16x8 dov = ld_tr8(dOs[buf], LDT, 32 * ks + 8 * g4, 16 * nt);
@@ -1812,14 +1804,17 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
         ad[nt] = mfma16(dov, atl, ad[nt]);
       }
     }
-    const float at_cur = atsc;
+    const float at_cur = asc;
     // K rows past the chunk end repeat row len - 1; W2 is zero there
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) *reinterpret_cast<bf16x8*>(Kc + prow * LDKC + 32 * ks + 8 * g4) = kf[ks];
+    put_frag(Mt_s, mq[0], mq[1]);
     load_k(nx);
-    load_at(nx);
+    load_a(nx);
     {
-      const float edec = prow < clen ? __expf(glast - gg) : 0.f, atm = prow < clen ? at_cur : 0.f;
+      // dD rows times M's row scale (the reduction index of M^T dD)
+      const float edec = prow < clen ? __expf(glast - gg) * msc : 0.f,
+                  atm = prow < clen ? at_cur * msc : 0.f;
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt) {
         float dd_[4];
@@ -1837,7 +1832,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
       bf16x8 mth, mtl;
-      q_split8(mtq[ks], mth, mtl);
+      q_split8(get_tr(Mt_s, ks), mth, mtl);
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt) {
         const bf16x8 xh = ld_tr8(dDh, LDT, 32 * ks + 8 * g4, 16 * nt);
@@ -1847,10 +1842,15 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
         drr[nt] = mfma16(xh, mtl, drr[nt]);
       }
     }
-    const float mt_cur = mtsc;
-    load_mt(nx);
+    load_m(nx);
+    // the K fragments of the state update (state rows (dk/4) w + 16 mt + r16,
+    // chunk rows 32 ks + 8 g4 ..): the tile is complete since the first
+    // barrier, so they are read here, off the update's path
+    bf16x8 ktf[2][XMT];
 #pragma unroll
-    for (int nt = 0; nt < NTV; ++nt) drr[nt] *= mt_cur;
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int mt = 0; mt < XMT; ++mt) ktf[ks][mt] = ld_tr8(Kc, LDKC, 32 * ks + 8 * g4, (DK / 4) * w + 16 * mt);
     {
       // dR rows as int16 with one scale per row of the slice
       float m = 0.f;
@@ -1893,10 +1893,6 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
       for (int nt = 0; nt < NTV; ++nt) Y[mt][nt] *= gC;
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
-      // K fragments for state rows (dk/4) w + 16 mt + r16, chunk rows 32 ks + 8 g4 ..
-      bf16x8 ktf[XMT];
-#pragma unroll
-      for (int mt = 0; mt < XMT; ++mt) ktf[mt] = ld_tr8(Kc, LDKC, 32 * ks + 8 * g4, (DK / 4) * w + 16 * mt);
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt) {
         const bf16x8 ph = ld_tr8(Pgh, LDT, 32 * ks + 8 * g4, 16 * nt);
@@ -1907,12 +1903,14 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
         for (int mt = 0; mt < XMT; ++mt) {
           Y[mt][nt] = mfma16(ph, qtf[mt][ks], Y[mt][nt]);
           Y[mt][nt] = mfma16(pl, qtf[mt][ks], Y[mt][nt]);
-          Y[mt][nt] = mfma16(wh, ktf[mt], Y[mt][nt]);
-          Y[mt][nt] = mfma16(wl, ktf[mt], Y[mt][nt]);
+          Y[mt][nt] = mfma16(wh, ktf[ks][mt], Y[mt][nt]);
+          Y[mt][nt] = mfma16(wl, ktf[ks][mt], Y[mt][nt]);
         }
       }
     }
     load_qt(nx);
+    // the next chunk's A (this chunk's was read before the first barrier)
+    put_frag(At_s, aq[0], aq[1]);
     put_do(buf ^ 1);
     put_rows(buf ^ 1);
     put_state();
@@ -3036,12 +3034,10 @@ static hipError_t run_fwd_bf(const LaunchArgs& a) {
   if (a.ncmax > 0) {
     if (a.saved)
       k_prep_bf<DK, true><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
-          q, k, a.g, bt, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.MTq, a.MTs, a.ATq, a.ATs,
-          a.QTp, a.Gw, a.sink);
+          q, k, a.g, bt, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.QTp, a.Gw, a.sink);
     else
       k_prep_bf<DK, false><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
-          q, k, a.g, bt, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, nullptr, nullptr, nullptr,
-          nullptr, nullptr, a.Gw, a.sink);
+          q, k, a.g, bt, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, nullptr, a.Gw, a.sink);
   }
   a.stage(a.saved ? "scan_fwd_save" : "scan_fwd");
   if (a.saved)
@@ -3080,8 +3076,7 @@ static hipError_t run_bwd_bf(const LaunchArgs& a) {
     a.stage("prep");
     if (a.ncmax > 0)
       k_prep_bf<DK, true><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
-          q, k, a.g, bt, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.MTq, a.MTs, a.ATq, a.ATs,
-          a.QTp, a.Gw, a.sink);
+          q, k, a.g, bt, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.QTp, a.Gw, a.sink);
     a.stage("scan_fwd_store");
     k_scan_fwd_bf<DK, DV, SCAN_BV, false, true><<<scan_blocks(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
         q, k, v, beta, bt, a.d, a.h0, a.smap, sord, a.N, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, nullptr, nullptr, a.Xq,
@@ -3089,7 +3084,7 @@ static hipError_t run_bwd_bf(const LaunchArgs& a) {
   }
   a.stage("scan_bwd");
   k_scan_bwd_bf<DK, DV, SCAN_BV><<<scan_blocks(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-      q, k, dO, bt, a.d, a.dht, a.smap, sord, a.N, Tfix, a.H, a.MTq, a.MTs, a.ATq, a.ATs, a.QTp, a.Gw, a.dh0, a.Yq,
+      q, k, dO, bt, a.d, a.dht, a.smap, sord, a.N, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.QTp, a.Gw, a.dh0, a.Yq,
       a.Ys, a.dRq, a.dRs, a.sink);
   a.stage("intra_bwd");
   if constexpr (DK > 128 || DV > 128) {

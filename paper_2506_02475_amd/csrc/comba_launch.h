@@ -44,11 +44,11 @@ struct LaunchArgs {
   float *Mw, *Aw, *Gw;            // per chunk-head: M, A (64 x 64), G (64)
   float *Xw, *Dw, *Yw, *dRw;      // per chunk-head: X (dk x dv), D (64 x dv), Y, dR
   float* ddp;                     // per chunk-head partial dd
-  // bf16 path, per chunk-head: M, A, M^T, A^T as int16 64 x 64 with one
-  // power-of-two scale per row in the matching *s array, Q^T as dk x 64 bf16;
-  // the tiles are stored in MFMA fragment order (frag_off in the kernels)
-  int16_t *Mq, *Aq, *MTq, *ATq;
-  float *Ms, *As, *MTs, *ATs;
+  // bf16 path, per chunk-head: M, A as int16 64 x 64 with one power-of-two
+  // scale per row of M (Ms) and per column of A (As), in MFMA fragment order
+  // (frag_off in the kernels); the backward also keeps Q^T as dk x 64 bf16
+  int16_t *Mq, *Aq;
+  float *Ms, *As;
   uint16_t* QTp;
   // bf16 path, per chunk-head: X, Y (dk x dv), D, dR (64 x dv) as int16 with one
   // power-of-two scale per (row, 32-column block) in the matching *s array;
