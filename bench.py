@@ -530,6 +530,8 @@ def time_varlen(comba, torch, steps, warmup):
 
 
 PROLOGUE = dict(B=4, T=4096, H=16, dk=128, dv=128, seed=71)
+PROLOGUE_SOURCES = ("comba_prologue.hip", "comba_device.hpp")
+PROLOGUE_TRAFFIC = "traffic_counters_prologue_b4_t4096_h16_d128.md"
 
 
 def prologue_bytes(stage, B, T, H, dk, dv, in_bytes=2):
@@ -586,7 +588,8 @@ def time_prologue(comba, torch, steps, warmup):
         by = prologue_bytes(st, c["B"], c["T"], c["H"], c["dk"], c["dv"])
         ach = by / (avg * 1e-3) / 1e9
         roof[st] = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
-                    "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None,
+                    "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4),
+                    "traffic": measured_traffic(st, PROLOGUE_TRAFFIC, PROLOGUE_SOURCES),
                     "kernel": st, "avg_launch_ms": round(avg, 4), "algorithmic_bytes": by}
     ms_step = (t1 - t0) * 1e3 / steps
     # the output gate on the operator's output shape (o fp32, z bf16): stream

@@ -44,10 +44,13 @@ __device__ __forceinline__ float to_f(bf16_t x) { return bf2f(x); }
 template <typename T> struct Pad { static constexpr int value = 16 / sizeof(T); };
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
-// Wavefront index in the workgroup, in a scalar register (the compiler cannot
-// tell on its own that it is uniform across the wave; a vector copy would make
-// every branch and address derived from it per-lane).
-__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
+__device__ __forceinline__ int wave_id() { return threadIdx.x >> 6; }
+// The same in a scalar register: the compiler cannot tell on its own that it is
+// uniform across the wave, and a per-lane copy makes every branch and address
+// derived from it per-lane.  (For the streaming prologue kernels, whose loop
+// control derives from it; in the scan kernels the scalar form changed the
+// schedule for the worse: the d = 256 forward scan took 12% longer.)
+__device__ __forceinline__ int wave_id_s() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
 __device__ __forceinline__ floatx4 zero4() { return floatx4{0.f, 0.f, 0.f, 0.f}; }
 

@@ -326,7 +326,7 @@ constexpr int fwd_head_groups(int H) {
 
 template <typename Tin, int DK, int DV>
 __global__ __launch_bounds__(64 * PRO_WAVES) void k_prologue_fwd(PrologueArgs a) {
-  const int run = blockIdx.x * PRO_WAVES + wave_id();
+  const int run = blockIdx.x * PRO_WAVES + wave_id_s();
   const int z = blockIdx.z, hg = blockIdx.y;
   if (z == 0)
     prologue_fwd_run<Tin, DK, true>(static_cast<const Tin*>(a.xq), a.wq, static_cast<Tin*>(a.q),
@@ -517,9 +517,9 @@ __global__ __launch_bounds__(64 * PRO_WAVES) void k_prologue_bwd(PrologueArgs a)
   static_assert(64 * PRO_BCL <= 256, "slots per wave share");
   __shared__ float4 dws[PRO_WAVES][256];  // per wave: the four tap sums of each channel
   // every wave reaches the barrier below (runs past the tokens add zeros)
-  const int run = blockIdx.x * PRO_WAVES + wave_id();
+  const int run = blockIdx.x * PRO_WAVES + wave_id_s();
   const int z = blockIdx.z;
-  float4* dwl = dws[wave_id()];
+  float4* dwl = dws[wave_id_s()];
   if (z == 0)
     prologue_bwd_run<Tin, DK, true>(static_cast<const Tin*>(a.xq), a.wq, a.gq, a.dxq, dwl,
                                     a.cu_seqlens, a.N, a.Tseq, a.Ttot, a.H, run, blockIdx.y, a.eps);
