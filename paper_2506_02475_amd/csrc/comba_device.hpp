@@ -272,6 +272,25 @@ __device__ __forceinline__ float4 q_unpack4(uint2 u, float s) {
                      (float)(int)(int16_t)(u.y & 0xFFFFu) * s, (float)((int)u.y >> 16) * s);
 }
 
+// Wider stores of a 32-column int16 row block: a lane (group g = lane / 16)
+// holds the 4-column pieces a (columns 4g .. 4g+3) and b (16 + 4g ..) of its
+// row.  One v_permlane16_swap per dword exchanges b of the even groups with a
+// of the odd ones, after which groups 0, 1, 2, 3 hold the 8 consecutive
+// columns 0-7, 16-23, 8-15, 24-31 (checked with an in-bounds probe): one
+// 16-byte store per lane and row instead of two 8-byte ones.  (Each store
+// instruction costs the scans' single wave per SIMD about as much as the
+// arithmetic that produced it, whatever its width.)
+__device__ __forceinline__ uint4 row8_from_pieces(uint2 a, uint2 b) {
+  const auto x = __builtin_amdgcn_permlane16_swap(a.x, b.x, false, false);
+  const auto y = __builtin_amdgcn_permlane16_swap(a.y, b.y, false, false);
+  return make_uint4(x[0], y[0], x[1], y[1]);
+}
+// First column of the 8 a lane holds after row8_from_pieces.
+__device__ __forceinline__ int row8_col() {
+  const int g = lane_id() >> 4;
+  return 8 * (((g & 1) << 1) | (g >> 1));
+}
+
 // Two fp32 values as packed bf16 (hi, lo): hi = bf16(x) (nearest), lo =
 // bf16(x - hi), each pair converted by one v_cvt_pk_bf16_f32 (3 VALU per value).
 typedef float f32x2_t __attribute__((ext_vector_type(2)));

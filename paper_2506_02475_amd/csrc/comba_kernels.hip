@@ -900,12 +900,14 @@ __global__ __launch_bounds__(NTHR) void k_reduce_dd(const float* __restrict__ dd
 
 // ===========================================================================
 // bf16 path.  k_prep_bf writes the per-chunk operands the scans need in the
-// order the MFMA consumes them: M, A (and for the backward M^T, A^T) as int16
-// rows with one power-of-two scale per row, Q^T as bf16.  In the scans each
-// wave loads the A-operand fragments of its own rows straight from global
-// memory into registers, one chunk ahead; LDS carries what the four waves
-// exchange (state, R, D and their backward counterparts, already split) and
-// the chunk's K rows, whose transposing reads give the K^T operand.
+// order the MFMA consumes them: M and A as int16 with one power-of-two scale
+// per row of M and per column of A, and for the backward Q^T as bf16.  In the
+// forward scan each wave loads the fragments of its own rows straight from
+// global memory into registers, one chunk ahead; LDS carries what the four
+// waves exchange (state, R, D and their backward counterparts, already split)
+// and the chunk's K rows, whose transposing reads give the K^T operand.  The
+// reverse scan stages the same M and A fragments in LDS and reads M^T, A^T
+// back with transposing reads.
 // ===========================================================================
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -942,7 +944,7 @@ __device__ __forceinline__ SeqInfo seq_at(const SeqInfo* smap, int s, int Tfix) 
 }
 
 // Element (row, col) of a 64-column operand tile that prep stores in MFMA
-// fragment order (M, A, M^T, A^T, Q^T): the 16 bytes lane (g, i) of wave w
+// fragment order (M, A, Q^T): the 16 bytes lane (g, i) of wave w
 // loads for k-step ks (row 16 w + i, columns 32 ks + 8 g .. +7) sit at
 // ((2 (row / 16) + ks) 64 + 16 g + i) * 8, so one k-step load of a wave reads
 // 1 KiB of whole lines (a row-major fragment would touch 16 half lines).
@@ -1291,22 +1293,22 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
   };
   // The same rows as int16 with one scale per row of the slice (see q_pack4),
   // into the slice's own block: dq = block base, [DK][BV]; ds = its row scales.
-  // A row's 32 columns are spread over the four lanes r16 + 16 g4.
+  // A row's 32 columns are spread over the four lanes r16 + 16 g4; they are
+  // regrouped so that each lane stores 16 bytes (row8_from_pieces), and lane
+  // group g4 stores the scale of row xrow0 + 16 g4 (one store for all rows).
   auto store_state_q = [&](int16_t* dq, float* ds) {
+    float sc = 0.f;
 #pragma unroll
     for (int mt = 0; mt < XMT; ++mt) {
-      float m = 0.f;
-#pragma unroll
-      for (int nt = 0; nt < NTV; ++nt)
-        m = nmax_abs4(m, X[mt][nt]);
+      float m = nmax_abs4(nmax_abs4(0.f, X[mt][0]), X[mt][1]);
       m = rowgroup_max(m);
       const float inv = q_inv_scale(m);
       const long row = xrow0 + 16 * mt;
-#pragma unroll
-      for (int nt = 0; nt < NTV; ++nt)
-        *reinterpret_cast<uint2*>(dq + row * BV + 16 * nt + col0) = q_pack4(X[mt][nt], inv);
-      ds[row] = q_scale(m);  // the four lanes of a row store the same value
+      *reinterpret_cast<uint4*>(dq + row * BV + row8_col()) =
+          row8_from_pieces(q_pack4(X[mt][0], inv), q_pack4(X[mt][1], inv));
+      if (g4 == mt) sc = q_scale(m);
     }
+    if (g4 < XMT) ds[xrow0 + 16 * g4] = sc;
   };
   put_state();
 
@@ -1471,10 +1473,9 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
       m = rowgroup_max(m);
       const float inv = q_inv_scale(m);
       const long row = (chh * NB + zb) * CH + prow;  // the slice's block
-#pragma unroll
-      for (int nt = 0; nt < NTV; ++nt)
-        *reinterpret_cast<uint2*>(Dq + row * BV + 16 * nt + col0) = q_pack4(dl[nt], inv);
-      Ds[row] = q_scale(m);  // the four lanes of a row store the same value
+      *reinterpret_cast<uint4*>(Dq + row * BV + row8_col()) =
+          row8_from_pieces(q_pack4(dl[0], inv), q_pack4(dl[1], inv));
+      if (g4 == 0) Ds[row] = q_scale(m);
     }
     {
       const float edec = __expf(glast - gg);
@@ -1631,21 +1632,20 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
   };
   // the same rows as int16 with one scale per row of the slice (see q_pack4),
   // into the slice's own block: dq = block base, [DK][BV]; ds = its row scales
+  // (16-byte stores and one scale store, as in the forward scan)
   auto store_state_q = [&](int16_t* dq, float* ds) {
+    float sc = 0.f;
 #pragma unroll
     for (int mt = 0; mt < XMT; ++mt) {
-      float m = 0.f;
-#pragma unroll
-      for (int nt = 0; nt < NTV; ++nt)
-        m = nmax_abs4(m, Y[mt][nt]);
+      float m = nmax_abs4(nmax_abs4(0.f, Y[mt][0]), Y[mt][1]);
       m = rowgroup_max(m);
       const float inv = q_inv_scale(m);
       const long row = yrow0 + 16 * mt;
-#pragma unroll
-      for (int nt = 0; nt < NTV; ++nt)
-        *reinterpret_cast<uint2*>(dq + row * BV + 16 * nt + col0) = q_pack4(Y[mt][nt], inv);
-      ds[row] = q_scale(m);  // the four lanes of a row store the same value
+      *reinterpret_cast<uint4*>(dq + row * BV + row8_col()) =
+          row8_from_pieces(q_pack4(Y[mt][0], inv), q_pack4(Y[mt][1], inv));
+      if (g4 == mt) sc = q_scale(m);
     }
+    if (g4 < XMT) ds[yrow0 + 16 * g4] = sc;
   };
   put_state();
 
@@ -1860,10 +1860,9 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
       m = rowgroup_max(m);
       const float inv = q_inv_scale(m);
       const long row = (chh * NB + zb) * CH + prow;  // the slice's block
-#pragma unroll
-      for (int nt = 0; nt < NTV; ++nt)
-        *reinterpret_cast<uint2*>(dRq + row * BV + 16 * nt + col0) = q_pack4(drr[nt], inv);
-      dRs[row] = q_scale(m);  // the four lanes of a row store the same value
+      *reinterpret_cast<uint4*>(dRq + row * BV + row8_col()) =
+          row8_from_pieces(q_pack4(drr[0], inv), q_pack4(drr[1], inv));
+      if (g4 == 0) dRs[row] = q_scale(m);
     }
     {
       const float eg = __expf(gg), begm = bb * __expf(gm);

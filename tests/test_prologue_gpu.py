@@ -84,6 +84,10 @@ CASES = [
     ("bf16_varlen", dict(H=2, dk=128, dv=128, in_dtype="bf16",
                          seqlens=[1, 0, 2, 61, 64, 3, 0, 130, 5])),
     ("f32_varlen", dict(H=1, dk=64, dv=64, in_dtype="f32", seqlens=[63, 1, 66, 0, 2])),
+    # enough tokens that the forward's runs (sized to the device's wave slots)
+    # are tens of tokens long and cross sequence boundaries inside a run
+    ("bf16_varlen_mid", dict(H=16, dk=128, dv=128, in_dtype="bf16",
+                             seqlens=[700, 1, 1333, 0, 95, 2100, 64, 513])),
 ]
 
 
