@@ -1381,10 +1381,6 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     if constexpr (OUT) load_a(0);
     load_rows(0);
     put_rows(0);
-    if constexpr (STORE) {
-      const long xb = (c_chh(0) * NB + zb) * DK;
-      store_state_q(Xq + xb * BV, Xs + xb);
-    }
   }
   __syncthreads();
 
@@ -1420,6 +1416,12 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
           qx[nt] = mfma16(xl, qf[ks], qx[nt]);
         }
       }
+    // the state entering this chunk, stored while the products above run
+    // (stores bunched before a barrier stall all four waves at once)
+    if constexpr (STORE) {
+      const long xb = (chh * NB + zb) * DK;
+      store_state_q(Xq + xb * BV, Xs + xb);
+    }
     // K rows past the chunk end repeat row len - 1; D is zero there
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) *reinterpret_cast<bf16x8*>(Kc + prow * LDKC + 32 * ks + 8 * g4) = kf[ks];
@@ -1464,18 +1466,15 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     load_m(nx);
 #pragma unroll
     for (int nt = 0; nt < NTV; ++nt) dl[nt] *= ms_cur;
+    // D rows as int16 with one scale per row of the slice, stored after the
+    // next phase's products are issued
+    uint4 dpk = make_uint4(0u, 0u, 0u, 0u);
+    float dsc = 0.f;
     if constexpr (STORE) {
-      // D rows as int16 with one scale per row of the slice
-      float m = 0.f;
-#pragma unroll
-      for (int nt = 0; nt < NTV; ++nt)
-        m = nmax_abs4(m, dl[nt]);
-      m = rowgroup_max(m);
+      const float m = rowgroup_max(nmax_abs4(nmax_abs4(0.f, dl[0]), dl[1]));
       const float inv = q_inv_scale(m);
-      const long row = (chh * NB + zb) * CH + prow;  // the slice's block
-      *reinterpret_cast<uint4*>(Dq + row * BV + row8_col()) =
-          row8_from_pieces(q_pack4(dl[0], inv), q_pack4(dl[1], inv));
-      if (g4 == 0) Ds[row] = q_scale(m);
+      dpk = row8_from_pieces(q_pack4(dl[0], inv), q_pack4(dl[1], inv));
+      dsc = q_scale(m);
     }
     {
       const float edec = __expf(glast - gg);
@@ -1517,6 +1516,11 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
         }
       }
     }
+    if constexpr (STORE) {
+      const long row = (chh * NB + zb) * CH + prow;  // the slice's block
+      *reinterpret_cast<uint4*>(Dq + row * BV + row8_col()) = dpk;
+      if (g4 == 0) Ds[row] = dsc;
+    }
 
     // O = Diag(exp G)(Q - d K) X + A D, formed as (A D)^T = D^T A^T
     if constexpr (OUT) {
@@ -1548,13 +1552,15 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
       }
     }
     put_state();
-    // state entering the next chunk (after the last chunk: the final state)
-    if constexpr (STORE) {
-      const long xb = ((more ? c_chh(cc + 1) : (long)s * H + h) * NB + zb) * DK;
-      store_state_q((more ? Xq : Xfq) + xb * BV, (more ? Xs : Xfs) + xb);
-    }
     put_rows(buf ^ 1);
     __syncthreads();
+  }
+  // the state after the last chunk (the backward's sink for it)
+  if constexpr (STORE) {
+    if (n > 0) {
+      const long xb = (((long)s * H + h) * NB + zb) * DK;
+      store_state_q(Xfq + xb * BV, Xfs + xb);
+    }
   }
   if (ht) store_state(ht + soff);
 }
@@ -1771,7 +1777,6 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     const long chh = c_chh(cc);
     const int buf = cc & 1;
     const int clen = c_len(cc);
-    store_state_q(Yq + (chh * NB + zb) * DK * BV, Ys + (chh * NB + zb) * DK);
     load_rows(nx);
     load_do(nx);
     const float glast = Grow[buf][CH - 1];
@@ -1793,6 +1798,9 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
         ky[nt] = mfma16(yh, kf[ks], ky[nt]);
         ky[nt] = mfma16(yl, kf[ks], ky[nt]);
       }
+    // the state gradient of this chunk, stored while the products run (stores
+    // bunched before a barrier stall all four waves at once)
+    store_state_q(Yq + (chh * NB + zb) * DK * BV, Ys + (chh * NB + zb) * DK);
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
       bf16x8 ath, atl;
@@ -1851,18 +1859,15 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
       for (int mt = 0; mt < XMT; ++mt) ktf[ks][mt] = ld_tr8(Kc, LDKC, 32 * ks + 8 * g4, (DK / 4) * w + 16 * mt);
+    // dR rows as int16 with one scale per row of the slice, stored after the
+    // next phase's products are issued
+    uint4 rpk;
+    float rsc;
     {
-      // dR rows as int16 with one scale per row of the slice
-      float m = 0.f;
-#pragma unroll
-      for (int nt = 0; nt < NTV; ++nt)
-        m = nmax_abs4(m, drr[nt]);
-      m = rowgroup_max(m);
+      const float m = rowgroup_max(nmax_abs4(nmax_abs4(0.f, drr[0]), drr[1]));
       const float inv = q_inv_scale(m);
-      const long row = (chh * NB + zb) * CH + prow;  // the slice's block
-      *reinterpret_cast<uint4*>(dRq + row * BV + row8_col()) =
-          row8_from_pieces(q_pack4(drr[0], inv), q_pack4(drr[1], inv));
-      if (g4 == 0) dRs[row] = q_scale(m);
+      rpk = row8_from_pieces(q_pack4(drr[0], inv), q_pack4(drr[1], inv));
+      rsc = q_scale(m);
     }
     {
       const float eg = __expf(gg), begm = bb * __expf(gm);
@@ -1906,6 +1911,11 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
           Y[mt][nt] = mfma16(wl, ktf[ks][mt], Y[mt][nt]);
         }
       }
+    }
+    {
+      const long row = (chh * NB + zb) * CH + prow;  // the slice's block
+      *reinterpret_cast<uint4*>(dRq + row * BV + row8_col()) = rpk;
+      if (g4 == 0) dRs[row] = rsc;
     }
     load_qt(nx);
     // the next chunk's A (this chunk's was read before the first barrier)
