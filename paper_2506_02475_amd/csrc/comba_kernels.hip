@@ -2600,9 +2600,9 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_wide(
   float bv = 0.f;
   float4 fdr;
 
-  for (int kh = 0; kh < KP; ++kh) {
-    const int c0 = kh * DKP;  // this pass's dk columns c0 .. c0 + 127
-    auto issue = [&](int vb) {
+  // block vb of pass kh (its dk columns kh DKP .. + 127) into the registers
+  auto issue = [&](int kh, int vb) {
+    const int c0 = kh * DKP;
       if (vb % 2 == 0) {
         const unsigned rb = 2u * ((unsigned)min(pr, len - 1) * (H * DV) + vb * VB + pc);
         r_do = at(reinterpret_cast<const uint4*>(dO_i), rb);
@@ -2622,7 +2622,10 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_wide(
         s_x[p] = at(Xs_i, 4u * xrow);
         s_y[p] = at(Ys_i, 4u * xrow);
       }
-    };
+  };
+  issue(0, 0);
+  for (int kh = 0; kh < KP; ++kh) {
+    const int c0 = kh * DKP;  // this pass's dk columns c0 .. c0 + 127
     float Fpart = 0.f;
     auto put = [&](int vb) {
       const int j = vb * VB;
@@ -2662,7 +2665,6 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_wide(
 #pragma unroll
     for (int j = 0; j < NTW; ++j) T1[j] = T2[j] = T3[j] = zero4();
     TileRegs<bf16_t, CH, DKP, IB_THR> kr, qr;
-    issue(0);
     // one block per iteration: unrolled, the blocks of dv = 256 keep too many
     // loaded pieces live and spill
 #pragma unroll 1
@@ -2671,7 +2673,7 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_wide(
       put(vb);
       __syncthreads();
       if (vb + 1 < NVB) {
-        issue(vb + 1);
+        issue(kh, vb + 1);
       } else {
         kr.load_clip(k + tok * DK + c0, (long)H * DK, len);
         qr.load_clip(q + tok * DK + c0, (long)H * DK, len);
@@ -2732,6 +2734,9 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_wide(
     kr.store(Ks, LDK);
     qr.store(Qs, LDK);
     __syncthreads();
+    // the next pass's first block loads during this phase 2 (it reads nothing
+    // else from memory)
+    if (kh + 1 < KP) issue(kh + 1, 0);
     const float Glast = Gs[CH - 1];
     {
       floatx4 akk[2], aqk[2];
