@@ -213,6 +213,15 @@ template <typename T>
 __device__ __forceinline__ const T& at(const T* base, unsigned byte_off) {
   return *reinterpret_cast<const T*>(reinterpret_cast<const char*>(base) + byte_off);
 }
+// Stores through a raw buffer whose record count ends at byte nbytes of g: the
+// hardware drops every store at or past it, so the rows past a chunk end need
+// no branch around their stores (nbytes >= 0, g 4-byte aligned).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t clip_rsrc(float* g, int nbytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(g, 0, nbytes, 0x00020000);
+}
+__device__ __forceinline__ void store_clip(float x, __amdgpu_buffer_rsrc_t rs, unsigned byte_off) {
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), rs, byte_off, 0, 0);
+}
 
 // Max over the four lanes r16, r16 + 16, r16 + 32, r16 + 48 (the lanes that
 // hold one row of a transposed MFMA accumulator) of values >= 0 or NaN:
@@ -370,11 +379,16 @@ __device__ __forceinline__ float sum16(float x) {
   x += dpp_upd<0x140>(0.f, x);  // row_mirror
   return x;
 }
-// Sum over the 4 lane groups (lanes l, l^16, l^32, l^48).
+// Sum over the 4 lane groups (lanes l, l^16, l^32, l^48), every lane gets the
+// result: v_permlane16_swap / v_permlane32_swap with both operands x hand lane l
+// the values of lanes l & ~16 and l | 16 (resp. 32), VALU only.
 __device__ __forceinline__ float sum_groups(float x) {
-  x += __shfl_xor(x, 16);
-  x += __shfl_xor(x, 32);
-  return x;
+  const unsigned u = __float_as_uint(x);
+  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  const float y = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const unsigned v = __float_as_uint(y);
+  const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 // Value of `lane` (the readlane builtin moves 32-bit integers).
 __device__ __forceinline__ float read_lane(float x, int lane) {

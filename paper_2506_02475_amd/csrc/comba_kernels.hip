@@ -1954,6 +1954,43 @@ __device__ __forceinline__ void split4v(const float4& x, bf16x4& hi, bf16x4& lo)
   split4(a, hi, lo);
 }
 
+// Per-row values of a lane's four accumulator rows r0 .. r0 + 3 (r0 % 4 == 0,
+// Gs and Bts 16-byte aligned): G_r, G_{r-1} (G_0 stands in at r = 0, where
+// no term uses it) and beta~_r.
+struct RowVals {
+  float g[4], gm[4], bt[4];
+};
+__device__ __forceinline__ RowVals row_vals(const float* Gs, const float* Bts, int r0) {
+  const float4 g = *reinterpret_cast<const float4*>(Gs + r0);
+  const float4 b = *reinterpret_cast<const float4*>(Bts + r0);
+  const float gp = Gs[max(r0 - 1, 0)];
+  return RowVals{{g.x, g.y, g.z, g.w}, {gp, g.x, g.y, g.z}, {b.x, b.y, b.z, b.w}};
+}
+
+// The gate terms of entry (r, c) of the chunk's 64 x 64 gradient products:
+// gam = e^{G_r - G_c} on and below the diagonal, lc = e^{G_{r-1} - G_c} below
+// it.  Branch-free: both exponentials are evaluated for every entry and the
+// masked values are selected away (above the diagonal they may overflow).
+struct GateTerms {
+  float e1, e2, dag, dakk;
+};
+__device__ __forceinline__ GateTerms gate_terms(int r, int c, const RowVals& rv, int e, float Gc,
+                                                float kk, float qk, float da, float dLv, float dh,
+                                                float& rbl) {
+  const bool on = r >= c, below = r > c;
+  const float gam = __expf(rv.g[e] - Gc), lc = __expf(rv.gm[e] - Gc);
+  const float a = (qk - dh * kk) * gam;
+  const float dl = -dLv;
+  const float lck = lc * kk;
+  rbl = below ? rbl + dl * lck : rbl;
+  GateTerms t;
+  t.e1 = on ? da * a : 0.f;
+  t.dag = on ? da * gam : 0.f;
+  t.e2 = below ? dl * rv.bt[e] * lck : 0.f;
+  t.dakk = below ? dl * rv.bt[e] * lc : 0.f;
+  return t;
+}
+
 template <int DK, int DV>
 __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
@@ -1974,7 +2011,7 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
   __shared__ __align__(16) char smem[SM::BYTES];
   // Bs: beta (write strength: dv), Bts: beta~ (feedback strength: L and R's
   // K X term); rowB: <v, dR> per row, the derivative through beta
-  __shared__ float Gs[CH], Bs[CH], Bts[CH], rowB[CH];
+  __shared__ __align__(16) float Gs[CH], Bs[CH], Bts[CH], rowB[CH];
   __shared__ float colpart[4][CH];      // per row tile: column sums of E1 + E2
   __shared__ float rowacc[2][6][CH];    // per column half: E1, E2, BL, p1, p2, p3 row sums
   __shared__ float scal[NW][2];         // per wave: <X, Y>_F, sum k . dQ~
@@ -2296,6 +2333,9 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
   }
   __syncthreads();
   const float Glast = Gs[CH - 1];
+  // this lane's accumulator rows r0 .. r0 + 3: G_r, G_{r-1} (r > 0) and beta~_r,
+  // read once (per-entry reads under the triangle's branches each waited for LDS)
+  const RowVals rv = row_vals(Gs, Bts, 16 * rt + 4 * g4);
   {
     floatx4 akk[2], aqk[2];
     akk[0] = akk[1] = aqk[0] = aqk[1] = zero4();
@@ -2314,33 +2354,18 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
 #pragma unroll
     for (int j2 = 0; j2 < 2; ++j2) {
       const int c = 16 * (2 * ch + j2) + r16;
+      const float Gc = Gs[c];
       float cE = 0.f, dagv[4], pv[4], uv[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int r = 16 * rt + 4 * g4 + e;
-        const float kk = akk[j2][e];
-        float dag = 0.f, e1 = 0.f, e2 = 0.f, dakk = 0.f;
-        if (r >= c) {
-          const float gam = __expf(Gs[r] - Gs[c]);
-          const float a = (aqk[j2][e] - dh * kk) * gam;
-          const float da = dA[j2][e];
-          e1 = da * a;
-          dag = da * gam;
-        }
-        if (r > c) {
-          const float lc = __expf(Gs[r - 1] - Gs[c]);
-          const float dl = -dL[j2][e];
-          const float lck = lc * kk;
-          e2 = dl * Bts[r] * lck;
-          rBL[e] += dl * lck;
-          dakk = dl * Bts[r] * lc;
-        }
-        dagv[e] = dag;
-        pv[e] = dakk;
-        uv[e] = dakk - dh * dag;  // zero above the diagonal like the others
-        rE1[e] += e1;
-        rE2[e] += e2;
-        cE += e1 + e2;
+        const GateTerms t = gate_terms(16 * rt + 4 * g4 + e, c, rv, e, Gc, akk[j2][e], aqk[j2][e],
+                                       dA[j2][e], dL[j2][e], dh, rBL[e]);
+        dagv[e] = t.dag;
+        pv[e] = t.dakk;
+        uv[e] = t.dakk - dh * t.dag;  // zero above the diagonal like the others
+        rE1[e] += t.e1;
+        rE2[e] += t.e2;
+        cE += t.e1 + t.e2;
       }
       const int toff = c * LDC + 16 * rt + 4 * g4;
       put_t4(GTh, GTl, toff, dagv);
@@ -2387,8 +2412,8 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     const int r = 16 * rt + 4 * g4 + e;
-    const float gr = __expf(Gs[r]), dec = __expf(Glast - Gs[r]);
-    const float sr = Bts[r] * __expf(r > 0 ? Gs[r - 1] : 0.f);
+    const float gr = __expf(rv.g[e]), dec = __expf(Glast - rv.g[e]);
+    const float sr = rv.bt[e] * __expf(r > 0 ? rv.gm[e] : 0.f);
 #pragma unroll
     for (int j = 0; j < NTW; ++j) {
       T1[j][e] *= gr;
@@ -2423,8 +2448,9 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     }
   }
   float ddpart = 0.f;
-  float* dq_i = dq + tok * DK;  // this chunk's rows: row r at r H DK
-  float* dk_i = dk + tok * DK;
+  // this chunk's rows (row r at r H DK), bounded at row len
+  const __amdgpu_buffer_rsrc_t rq = clip_rsrc(dq + tok * DK, len * (H * DK * 4));
+  const __amdgpu_buffer_rsrc_t rk = clip_rsrc(dk + tok * DK, len * (H * DK * 4));
 #pragma unroll
   for (int j = 0; j < NTW; ++j) {
     floatx4 dkv;
@@ -2441,10 +2467,8 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     for (int e = 0; e < 4; ++e) {
       const int r = 16 * rt + 4 * g4 + e;
       const unsigned off = 4u * ((unsigned)r * (H * DK) + 16 * (ch * NTW + j) + r16);
-      if (r < len) {
-        at(dq_i, off) = T1[j][e];
-        at(dk_i, off) = dkv[e];
-      }
+      store_clip(T1[j][e], rq, off);  // rows r >= len dropped
+      store_clip(dkv[e], rk, off);
     }
   }
   {
@@ -2543,7 +2567,7 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_wide(
   constexpr int NB = DV / 32;
   static_assert(VB == 32 && NVB % 2 == 0 && CH * 8 == IB_THR, "blocks and pieces");
   __shared__ __align__(16) char smem[SM::BYTES];
-  __shared__ float Gs[CH], Bs[CH], Bts[CH], rowB[CH];
+  __shared__ __align__(16) float Gs[CH], Bs[CH], Bts[CH], rowB[CH];
   __shared__ float colpart[KP][4][CH];
   __shared__ float rowacc[KP][2][6][CH];
   __shared__ float scal[KP][NW][2];
@@ -2593,8 +2617,9 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_wide(
   const float* Xs_i = Xs + chh * NB * DK;
   const float* Ys_i = Ys + chh * NB * DK;
   float* dv_i = dv + tok * DV;
-  float* dq_i = dq + tok * DK;
-  float* dk_i = dk + tok * DK;
+  // this chunk's rows (row r at r H DK), bounded at row len
+  const __amdgpu_buffer_rsrc_t rq = clip_rsrc(dq + tok * DK, len * (H * DK * 4));
+  const __amdgpu_buffer_rsrc_t rk = clip_rsrc(dk + tok * DK, len * (H * DK * 4));
   floatx4 dA[2], dL[2];
   dA[0] = dA[1] = dL[0] = dL[1] = zero4();
   float bv = 0.f;
@@ -2738,6 +2763,7 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_wide(
     // else from memory)
     if (kh + 1 < KP) issue(kh + 1, 0);
     const float Glast = Gs[CH - 1];
+    const RowVals rv = row_vals(Gs, Bts, 16 * rt + 4 * g4);
     {
       floatx4 akk[2], aqk[2];
       akk[0] = akk[1] = aqk[0] = aqk[1] = zero4();
@@ -2756,33 +2782,19 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_wide(
 #pragma unroll
       for (int j2 = 0; j2 < 2; ++j2) {
         const int c = 16 * (2 * ch + j2) + r16;
+        const float Gc = Gs[c];
         float cE = 0.f, dagv[4], pv[4], uv[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const int r = 16 * rt + 4 * g4 + e;
-          const float kk = akk[j2][e];  // this pass's part of k_r . k_c
-          float dag = 0.f, e1 = 0.f, e2 = 0.f, dakk = 0.f;
-          if (r >= c) {
-            const float gam = __expf(Gs[r] - Gs[c]);
-            const float a = (aqk[j2][e] - dh * kk) * gam;
-            const float da = dA[j2][e];
-            e1 = da * a;
-            dag = da * gam;
-          }
-          if (r > c) {
-            const float lc = __expf(Gs[r - 1] - Gs[c]);
-            const float dl = -dL[j2][e];
-            const float lck = lc * kk;
-            e2 = dl * Bts[r] * lck;
-            rBL[e] += dl * lck;
-            dakk = dl * Bts[r] * lc;
-          }
-          dagv[e] = dag;
-          pv[e] = dakk;
-          uv[e] = dakk - dh * dag;
-          rE1[e] += e1;
-          rE2[e] += e2;
-          cE += e1 + e2;
+          // akk: this pass's part of k_r . k_c
+          const GateTerms t = gate_terms(16 * rt + 4 * g4 + e, c, rv, e, Gc, akk[j2][e], aqk[j2][e],
+                                         dA[j2][e], dL[j2][e], dh, rBL[e]);
+          dagv[e] = t.dag;
+          pv[e] = t.dakk;
+          uv[e] = t.dakk - dh * t.dag;
+          rE1[e] += t.e1;
+          rE2[e] += t.e2;
+          cE += t.e1 + t.e2;
         }
         const int toff = c * LDC + 16 * rt + 4 * g4;
         put_t4(GTh, GTl, toff, dagv);
@@ -2824,8 +2836,8 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_wide(
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int r = 16 * rt + 4 * g4 + e;
-      const float gr = __expf(Gs[r]), dec = __expf(Glast - Gs[r]);
-      const float sr = Bts[r] * __expf(r > 0 ? Gs[r - 1] : 0.f);
+      const float gr = __expf(rv.g[e]), dec = __expf(Glast - rv.g[e]);
+      const float sr = rv.bt[e] * __expf(r > 0 ? rv.gm[e] : 0.f);
 #pragma unroll
       for (int j = 0; j < NTW; ++j) {
         T1[j][e] *= gr;
@@ -2870,10 +2882,8 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_wide(
       for (int e = 0; e < 4; ++e) {
         const int r = 16 * rt + 4 * g4 + e;
         const unsigned off = 4u * ((unsigned)r * (H * DK) + c0 + 16 * (ch * NTW + j) + r16);
-        if (r < len) {
-          at(dq_i, off) = T1[j][e];
-          at(dk_i, off) = dkv[e];
-        }
+        store_clip(T1[j][e], rq, off);  // rows r >= len dropped
+        store_clip(dkv[e], rk, off);
       }
     }
     ddpart = wave_sum(ddpart);
