@@ -2408,6 +2408,44 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
   }
   __syncthreads();
 
+  if (w == 0) {
+    // Per-row gradients dg, dbeta (lane = row) from the row and column sums:
+    // LDS reads only, so this wave forms them ahead of its dQ~, dK products
+    // while the other wave on its SIMD keeps the matrix unit busy.
+    const int r = lane;
+    float F = 0.f;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) F += scal[i][0];
+    const float e1 = rowacc[0][0][r] + rowacc[1][0][r];
+    const float e2 = rowacc[0][1][r] + rowacc[1][1][r];
+    const float bl = rowacc[0][2][r] + rowacc[1][2][r];
+    const float p1 = rowacc[0][3][r] + rowacc[1][3][r];
+    const float p2 = rowacc[0][4][r] + rowacc[1][4][r];
+    const float p3 = rowacc[0][5][r] + rowacc[1][5][r];
+    const float col = colpart[0][r] + colpart[1][r] + colpart[2][r] + colpart[3][r];
+    const float egm = __expf(r > 0 ? Gs[r - 1] : 0.f);
+    const float cr = __expf(Glast - Gs[r]) * p2;
+    const float rowg = e1 + __expf(Gs[r]) * p1 - cr;
+    const float rowgm = e2 - Bts[r] * egm * p3;
+    const float rowbt = bl - egm * p3;  // through beta~
+    const float gcs = wave_sum(cr);
+    const float rowgm_next = shift_down1(rowgm);
+    float dG = rowg - col + (r + 1 < CH ? rowgm_next : 0.f);
+    if (r == CH - 1) dG += gcs + __expf(Glast) * F;
+    float x = __shfl(dG, 63 - lane);
+    x = wave_prefix_sum(x);
+    const float dgr = __shfl(x, 63 - lane);
+    if (r < len) {
+      at(dg + tok, 4u * (r * H)) = dgr;
+      if (dbeta_tilde) {
+        at(dbeta + tok, 4u * (r * H)) = rowB[r];
+        at(dbeta_tilde + tok, 4u * (r * H)) = rowbt;
+      } else {
+        at(dbeta + tok, 4u * (r * H)) = rowB[r] + rowbt;
+      }
+    }
+  }
+
   // dQ~ (in T1) and dK (in T2)
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
@@ -2489,44 +2527,11 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
   ddpart = wave_sum(ddpart);
   if (lane == 0) scal[w][1] = ddpart;
   __syncthreads();
-
-  if (w == 0) {
-    const int r = lane;
-    float F = 0.f, dds = 0.f;
+  if (w == 0 && lane == 0) {
+    float dds = 0.f;
 #pragma unroll
-    for (int i = 0; i < NW; ++i) {
-      F += scal[i][0];
-      dds += scal[i][1];
-    }
-    const float e1 = rowacc[0][0][r] + rowacc[1][0][r];
-    const float e2 = rowacc[0][1][r] + rowacc[1][1][r];
-    const float bl = rowacc[0][2][r] + rowacc[1][2][r];
-    const float p1 = rowacc[0][3][r] + rowacc[1][3][r];
-    const float p2 = rowacc[0][4][r] + rowacc[1][4][r];
-    const float p3 = rowacc[0][5][r] + rowacc[1][5][r];
-    const float col = colpart[0][r] + colpart[1][r] + colpart[2][r] + colpart[3][r];
-    const float egm = __expf(r > 0 ? Gs[r - 1] : 0.f);
-    const float cr = __expf(Glast - Gs[r]) * p2;
-    const float rowg = e1 + __expf(Gs[r]) * p1 - cr;
-    const float rowgm = e2 - Bts[r] * egm * p3;
-    const float rowbt = bl - egm * p3;  // through beta~
-    const float gcs = wave_sum(cr);
-    const float rowgm_next = shift_down1(rowgm);
-    float dG = rowg - col + (r + 1 < CH ? rowgm_next : 0.f);
-    if (r == CH - 1) dG += gcs + __expf(Glast) * F;
-    float x = __shfl(dG, 63 - lane);
-    x = wave_prefix_sum(x);
-    const float dgr = __shfl(x, 63 - lane);
-    if (r < len) {
-      at(dg + tok, 4u * (r * H)) = dgr;
-      if (dbeta_tilde) {
-        at(dbeta + tok, 4u * (r * H)) = rowB[r];
-        at(dbeta_tilde + tok, 4u * (r * H)) = rowbt;
-      } else {
-        at(dbeta + tok, 4u * (r * H)) = rowB[r] + rowbt;
-      }
-    }
-    if (lane == 0) ddp[chh] = -dds;
+    for (int i = 0; i < NW; ++i) dds += scal[i][1];
+    ddp[chh] = -dds;
   }
   __syncthreads();  // the next item rewrites Gs, Bs
   }
