@@ -222,6 +222,11 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t clip_rsrc(float* g, int nbytes
 __device__ __forceinline__ void store_clip(float x, __amdgpu_buffer_rsrc_t rs, unsigned byte_off) {
   __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), rs, byte_off, 0, 0);
 }
+__device__ __forceinline__ void store_clip4(const floatx4& x, __amdgpu_buffer_rsrc_t rs, unsigned byte_off) {
+  typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+  const u32x4_t u = {__float_as_uint(x[0]), __float_as_uint(x[1]), __float_as_uint(x[2]), __float_as_uint(x[3])};
+  __builtin_amdgcn_raw_buffer_store_b128(u, rs, byte_off, 0, 0);
+}
 
 // Max over the four lanes r16, r16 + 16, r16 + 32, r16 + 48 (the lanes that
 // hold one row of a transposed MFMA accumulator) of values >= 0 or NaN:

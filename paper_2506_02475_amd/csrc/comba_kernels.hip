@@ -1303,18 +1303,21 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
       float m = nmax_abs4(nmax_abs4(0.f, X[mt][0]), X[mt][1]);
       m = rowgroup_max(m);
       const float inv = q_inv_scale(m);
-      const long row = xrow0 + 16 * mt;
-      *reinterpret_cast<uint4*>(dq + row * BV + row8_col()) =
+      const unsigned row = xrow0 + 16 * mt;
+      at(reinterpret_cast<uint4*>(dq), 2u * (row * BV + row8_col())) =
           row8_from_pieces(q_pack4(X[mt][0], inv), q_pack4(X[mt][1], inv));
       if (g4 == mt) sc = q_scale(m);
     }
-    if (g4 < XMT) ds[xrow0 + 16 * g4] = sc;
+    if (g4 < XMT) at(ds, 4u * (xrow0 + 16 * g4)) = sc;
   };
   put_state();
 
+  // chunk offsets are wave-uniform; readfirstlane keeps them (and every chunk
+  // base address) in scalar registers, so that loads and stores take a scalar
+  // base and a 32-bit lane offset
   auto c_len = [&](int cc) { return min(CH, si.len - cc * CH); };
-  auto c_tok = [&](int cc) { return (long)(si.tok0 + cc * CH) * H + h; };
-  auto c_chh = [&](int cc) { return (long)(si.chunk0 + cc) * H + h; };
+  auto c_tok = [&](int cc) { return (long)__builtin_amdgcn_readfirstlane(si.tok0 + cc * CH) * H + h; };
+  auto c_chh = [&](int cc) { return (long)__builtin_amdgcn_readfirstlane(si.chunk0 + cc) * H + h; };
 
   // per-chunk operands, loaded one chunk ahead: K, Q rows as bf16, the rows of
   // M and A as int16 with M's row scale (applied to the accumulator rows:
@@ -1339,10 +1342,13 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     plen = c_len(cc);
     const long tok = c_tok(cc), chh = c_chh(cc);
     const int t = threadIdx.x & (CH - 1);
-    pgv = Gw[chh * CH + t];
-    pbv = beta[tok + (long)min(t, plen - 1) * H];
-    pbtv = beta_tilde[tok + (long)min(t, plen - 1) * H];
-    pvv = *reinterpret_cast<const uint4*>(v + (tok + (long)min(vr_ld, plen - 1) * H) * DV + j0 + vc);
+    // chunk bases are wave-uniform (scalar registers), lane offsets 32-bit
+    const unsigned tr = 2u * ((unsigned)min(t, plen - 1) * H);
+    pgv = at(Gw + chh * CH, 4u * t);
+    pbv = at(beta + tok, tr);
+    pbtv = at(beta_tilde + tok, tr);
+    pvv = at(reinterpret_cast<const uint4*>(v + tok * DV + j0),
+             2u * ((unsigned)min(vr_ld, plen - 1) * (H * DV) + vc));
   };
   auto put_rows = [&](int buf) {
     const int t = threadIdx.x & (CH - 1);
@@ -1356,24 +1362,26 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
   // rows past the chunk end load a valid row; their K X / Q X results are
   // never used (beta = beta~ = 0 zeroes R there and such outputs are not stored)
   auto load_kq = [&](int cc) {
-    const long rb = (c_tok(cc) + (long)min(prow, c_len(cc) - 1) * H) * DK + 8 * g4;
+    const long tb = c_tok(cc) * DK;
+    const unsigned rb = 2u * ((unsigned)min(prow, c_len(cc) - 1) * (H * DK) + 8 * g4);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      kf[ks] = ld8(k + rb + 32 * ks);
-      if constexpr (OUT) qf[ks] = ld8(q + rb + 32 * ks);
+      kf[ks] = at(reinterpret_cast<const bf16x8*>(k + tb), rb + 64u * ks);
+      if constexpr (OUT) qf[ks] = at(reinterpret_cast<const bf16x8*>(q + tb), rb + 64u * ks);
     }
   };
+  const unsigned foff = 16u * (2 * w * 64 + lane);  // this lane's fragment (fragment order)
   auto load_m = [&](int cc) {
-    const int16_t* p = Mq + c_chh(cc) * CC + (2 * w * 64 + lane) * 8;  // fragment order
+    const uint4* p = reinterpret_cast<const uint4*>(Mq + c_chh(cc) * CC);
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) mq[ks] = *reinterpret_cast<const uint4*>(p + ks * 512);
-    msc = Ms[c_chh(cc) * CH + prow];
+    for (int ks = 0; ks < 2; ++ks) mq[ks] = at(p, foff + 1024u * ks);
+    msc = at(Ms + c_chh(cc) * CH, 4u * prow);
   };
   auto load_a = [&](int cc) {
-    const int16_t* p = Aq + c_chh(cc) * CC + (2 * w * 64 + lane) * 8;  // fragment order
+    const uint4* p = reinterpret_cast<const uint4*>(Aq + c_chh(cc) * CC);
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) aq[ks] = *reinterpret_cast<const uint4*>(p + ks * 512);
-    asc = As[c_chh(cc) * CH + prow];
+    for (int ks = 0; ks < 2; ++ks) aq[ks] = at(p, foff + 1024u * ks);
+    asc = at(As + c_chh(cc) * CH, 4u * prow);
   };
   if (n > 0) {
     load_kq(0);
@@ -1517,9 +1525,9 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
       }
     }
     if constexpr (STORE) {
-      const long row = (chh * NB + zb) * CH + prow;  // the slice's block
-      *reinterpret_cast<uint4*>(Dq + row * BV + row8_col()) = dpk;
-      if (g4 == 0) Ds[row] = dsc;
+      const long blk = (chh * NB + zb) * CH;  // the slice's block
+      at(reinterpret_cast<uint4*>(Dq + blk * BV), 2u * (prow * BV + row8_col())) = dpk;
+      if (g4 == 0) at(Ds + blk, 4u * prow) = dsc;
     }
 
     // O = Diag(exp G)(Q - d K) X + A D, formed as (A D)^T = D^T A^T
@@ -1541,14 +1549,14 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
         }
       }
       load_a(nx);
+      // rows past the chunk end fall past the record count: dropped
+      const __amdgpu_buffer_rsrc_t ro = clip_rsrc(o + tok * DV + j0, len * (H * DV * 4));
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt) {
         floatx4 ov;
 #pragma unroll
         for (int e = 0; e < 4; ++e) ov[e] = oacc[nt][e] + adc[nt][e];
-        float* dst = prow < len ? o + (tok + (long)prow * H) * DV + j0 + 16 * nt + col0
-                                : sink + 4 * lane;
-        store4(dst, ov);
+        store_clip4(ov, ro, 4u * ((unsigned)prow * (H * DV) + 16 * nt + col0));
       }
     }
     put_state();
@@ -1646,18 +1654,19 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
       float m = nmax_abs4(nmax_abs4(0.f, Y[mt][0]), Y[mt][1]);
       m = rowgroup_max(m);
       const float inv = q_inv_scale(m);
-      const long row = yrow0 + 16 * mt;
-      *reinterpret_cast<uint4*>(dq + row * BV + row8_col()) =
+      const unsigned row = yrow0 + 16 * mt;
+      at(reinterpret_cast<uint4*>(dq), 2u * (row * BV + row8_col())) =
           row8_from_pieces(q_pack4(Y[mt][0], inv), q_pack4(Y[mt][1], inv));
       if (g4 == mt) sc = q_scale(m);
     }
-    if (g4 < XMT) ds[yrow0 + 16 * g4] = sc;
+    if (g4 < XMT) at(ds, 4u * (yrow0 + 16 * g4)) = sc;
   };
   put_state();
 
+  // chunk offsets in scalar registers (see the forward scan)
   auto c_len = [&](int cc) { return min(CH, si.len - cc * CH); };
-  auto c_tok = [&](int cc) { return (long)(si.tok0 + cc * CH) * H + h; };
-  auto c_chh = [&](int cc) { return (long)(si.chunk0 + cc) * H + h; };
+  auto c_tok = [&](int cc) { return (long)__builtin_amdgcn_readfirstlane(si.tok0 + cc * CH) * H + h; };
+  auto c_chh = [&](int cc) { return (long)__builtin_amdgcn_readfirstlane(si.chunk0 + cc) * H + h; };
 
   // The chunk's K rows, staged from the K operand registers: the state update
   // takes its K operand (reduction down the chunk rows) from here with
@@ -1687,23 +1696,25 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
   uint4 pdo = make_uint4(0, 0, 0, 0);  // next chunk's dO slice, 16 bytes per thread
   // rows past the chunk end load a valid row; dD is zeroed there at use
   auto load_k = [&](int cc) {
-    const long rb = (c_tok(cc) + (long)min(prow, c_len(cc) - 1) * H) * DK + 8 * g4;
+    const bf16x8* kc = reinterpret_cast<const bf16x8*>(k + c_tok(cc) * DK);
+    const unsigned rb = 2u * ((unsigned)min(prow, c_len(cc) - 1) * (H * DK) + 8 * g4);
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) kf[ks] = ld8(k + rb + 32 * ks);
+    for (int ks = 0; ks < KS; ++ks) kf[ks] = at(kc, rb + 64u * ks);
   };
+  const unsigned foff = 16u * (2 * w * 64 + lane);  // this lane's fragment (fragment order)
   // A's fragments and the column scale of A's column prow
   auto load_a = [&](int cc) {
-    const int16_t* p = Aq + c_chh(cc) * CC + (2 * w * 64 + lane) * 8;  // fragment order
+    const uint4* p = reinterpret_cast<const uint4*>(Aq + c_chh(cc) * CC);
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) aq[ks] = *reinterpret_cast<const uint4*>(p + ks * 512);
-    asc = As[c_chh(cc) * CH + prow];
+    for (int ks = 0; ks < 2; ++ks) aq[ks] = at(p, foff + 1024u * ks);
+    asc = at(As + c_chh(cc) * CH, 4u * prow);
   };
   // M's fragments and the scale of M's row prow
   auto load_m = [&](int cc) {
-    const int16_t* p = Mq + c_chh(cc) * CC + (2 * w * 64 + lane) * 8;  // fragment order
+    const uint4* p = reinterpret_cast<const uint4*>(Mq + c_chh(cc) * CC);
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) mq[ks] = *reinterpret_cast<const uint4*>(p + ks * 512);
-    msc = Ms[c_chh(cc) * CH + prow];
+    for (int ks = 0; ks < 2; ++ks) mq[ks] = at(p, foff + 1024u * ks);
+    msc = at(Ms + c_chh(cc) * CH, 4u * prow);
   };
   // fragment (row 16 w + r16, columns 32 ks + 8 g4 ..) to its row-major place
   // (the fragments by value: a reference to the register arrays would keep
@@ -1716,20 +1727,21 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
   auto get_tr = [&](const int16_t* t, int ks) {
     return __builtin_bit_cast(uint4, ld_tr8(reinterpret_cast<const bf16_t*>(t), LDM, 32 * ks + 8 * g4, 16 * w));
   };
+  const unsigned qoff = 16u * (2 * XMT * w * 64 + lane);
   auto load_qt = [&](int cc) {
     // fragment order: rows (DK/4) w + 16 mt + i are row block w XMT + mt
-    const long base = c_chh(cc) * DK * CH + (2 * XMT * w * 64 + lane) * 8;
+    const bf16x8* p = reinterpret_cast<const bf16x8*>(QTp + c_chh(cc) * DK * CH);
 #pragma unroll
     for (int mt = 0; mt < XMT; ++mt)
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) qtf[mt][ks] = ld8(QTp + base + (2 * mt + ks) * 512);
+      for (int ks = 0; ks < 2; ++ks) qtf[mt][ks] = at(p, qoff + 1024u * (2 * mt + ks));
   };
   auto load_rows = [&](int cc) {
     plen = c_len(cc);
     const long tok = c_tok(cc), chh = c_chh(cc);
     const int t = threadIdx.x & (CH - 1);
-    pgv = Gw[chh * CH + t];
-    pbv = beta_tilde[tok + (long)min(t, plen - 1) * H];
+    pgv = at(Gw + chh * CH, 4u * t);
+    pbv = at(beta_tilde + tok, 2u * ((unsigned)min(t, plen - 1) * H));
   };
   auto put_rows = [&](int buf) {
     const int t = threadIdx.x & (CH - 1);
@@ -1747,7 +1759,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
   auto load_do = [&](int cc) {
     const int len = c_len(cc);
     do_ok = do_thr && dr < len;
-    pdo = *reinterpret_cast<const uint4*>(dO + (c_tok(cc) + (long)min(dr_ld, len - 1) * H) * DV + j0 + dc);
+    pdo = at(reinterpret_cast<const uint4*>(dO + c_tok(cc) * DV + j0),
+             2u * ((unsigned)min(dr_ld, len - 1) * (H * DV) + dc));
   };
   auto put_do = [&](int buf) {
     const uint4 val = do_ok ? pdo : make_uint4(0, 0, 0, 0);
@@ -1913,9 +1926,9 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
       }
     }
     {
-      const long row = (chh * NB + zb) * CH + prow;  // the slice's block
-      *reinterpret_cast<uint4*>(dRq + row * BV + row8_col()) = rpk;
-      if (g4 == 0) dRs[row] = rsc;
+      const long blk = (chh * NB + zb) * CH;  // the slice's block
+      at(reinterpret_cast<uint4*>(dRq + blk * BV), 2u * (prow * BV + row8_col())) = rpk;
+      if (g4 == 0) at(dRs + blk, 4u * prow) = rsc;
     }
     load_qt(nx);
     // the next chunk's A (this chunk's was read before the first barrier)
