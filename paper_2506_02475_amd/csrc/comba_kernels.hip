@@ -882,20 +882,17 @@ __global__ __launch_bounds__(NTHR, 1) void k_intra_bwd(
   }
 }
 
-// dd[h] = sum over chunks of the per-chunk partials (fixed order)
-__global__ __launch_bounds__(NTHR) void k_reduce_dd(const float* __restrict__ ddp, int nc, int H,
-                                                    float* __restrict__ dd) {
-  __shared__ float part[NTHR];
+// dd[h] = sum over chunks of the per-chunk partials, one wave per head in a
+// fixed order (lane l takes chunks l, l + 64, ..., then a butterfly over the
+// wave): no LDS round trips or barriers
+constexpr int RDD_THR = 64;
+__global__ __launch_bounds__(RDD_THR) void k_reduce_dd(const float* __restrict__ ddp, int nc, int H,
+                                                       float* __restrict__ dd) {
   const int h = blockIdx.x;
   float s = 0.f;
-  for (int c = threadIdx.x; c < nc; c += NTHR) s += ddp[(long)c * H + h];
-  part[threadIdx.x] = s;
-  __syncthreads();
-  for (int off = NTHR / 2; off > 0; off >>= 1) {
-    if ((int)threadIdx.x < off) part[threadIdx.x] += part[threadIdx.x + off];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) dd[h] = part[0];
+  for (int c = threadIdx.x; c < nc; c += RDD_THR) s += ddp[(long)c * H + h];
+  s = wave_sum(s);
+  if (threadIdx.x == 0) dd[h] = s;
 }
 
 // ===========================================================================
@@ -3028,7 +3025,7 @@ static hipError_t run_bwd(const LaunchArgs& a) {
   const Tin* dO = static_cast<const Tin*>(a.dO);
   if (a.N == 0) {
     // no sequences: dd (one value per head) is zero
-    k_reduce_dd<<<a.H, NTHR, 0, st>>>(a.ddp, 0, a.H, a.dd);
+    k_reduce_dd<<<a.H, RDD_THR, 0, st>>>(a.ddp, 0, a.H, a.dd);
     return hipGetLastError();
   }
   if (!a.saved) {
@@ -3052,7 +3049,7 @@ static hipError_t run_bwd(const LaunchArgs& a) {
         q, k, v, dO, beta, bt, a.d, a.cmap, a.H, a.Gw, a.Xw, a.Dw, a.Yw, a.dRw, a.dq, a.dk_, a.dv_,
         a.dbeta, a.dbeta_tilde, a.dg, a.ddp);
   a.stage("reduce_dd");
-  k_reduce_dd<<<a.H, NTHR, 0, st>>>(a.ddp, a.ncmax, a.H, a.dd);
+  k_reduce_dd<<<a.H, RDD_THR, 0, st>>>(a.ddp, a.ncmax, a.H, a.dd);
   a.stage(nullptr);
   return hipGetLastError();
 }
@@ -3104,7 +3101,7 @@ static hipError_t run_bwd_bf(const LaunchArgs& a) {
   const bf16_t* bt = static_cast<const bf16_t*>(a.beta_tilde);
   const bf16_t* dO = static_cast<const bf16_t*>(a.dO);
   if (a.N == 0) {
-    k_reduce_dd<<<a.H, NTHR, 0, st>>>(a.ddp, 0, a.H, a.dd);
+    k_reduce_dd<<<a.H, RDD_THR, 0, st>>>(a.ddp, 0, a.H, a.dd);
     return hipGetLastError();
   }
   // fixed-length rows need no tables (closed form in the kernels)
@@ -3143,7 +3140,7 @@ static hipError_t run_bwd_bf(const LaunchArgs& a) {
           a.dRs, a.ncmax, a.dq, a.dk_, a.dv_, a.dbeta, a.dbeta_tilde, a.dg, a.ddp, a.sink);
   }
   a.stage("reduce_dd");
-  k_reduce_dd<<<a.H, NTHR, 0, st>>>(a.ddp, a.ncmax, a.H, a.dd);
+  k_reduce_dd<<<a.H, RDD_THR, 0, st>>>(a.ddp, a.ncmax, a.H, a.dd);
   a.stage(nullptr);
   return hipGetLastError();
 }
