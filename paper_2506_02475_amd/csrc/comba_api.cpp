@@ -95,7 +95,7 @@ comba_status check_shape_recurrent(const comba_shape* s, Dims* out) {
 }
 
 struct Layout {
-  size_t cmap, smap, sord, M, A, G, X, D, Y, dR, ddp, QT, Xfin, sink, total;
+  size_t cmap, smap, sord, M, A, G, X, D, Y, dR, ddp, QT, Xfin, total;
   size_t Xs, Ds, Ys, dRs, Xfs;  // bf16 path: scales of the int16 X, D, Y, dR, final-state sink
   size_t Ms, As;                // bf16 path: row scales of M, column scales of A
 };
@@ -109,7 +109,6 @@ Layout layout(const Dims& d, bool bwd) {
     off += round_up(bytes);
     return at;
   };
-  L.sink = take(1024);
   L.cmap = take((size_t)d.ncmax * sizeof(comba::ChunkInfo));
   L.smap = take((size_t)(d.N > 0 ? d.N : 1) * sizeof(comba::SeqInfo));
   L.sord = take((size_t)(d.N > 0 ? d.N : 1) * sizeof(int));
@@ -199,7 +198,6 @@ void carve(comba::LaunchArgs& a, const Layout& L, void* ws, bool bwd) {
   a.Mw = reinterpret_cast<float*>(base + L.M);
   a.Aw = reinterpret_cast<float*>(base + L.A);
   a.Gw = reinterpret_cast<float*>(base + L.G);
-  a.sink = reinterpret_cast<float*>(base + L.sink);
   if (a.bf16) {
     a.Mq = reinterpret_cast<int16_t*>(base + L.M);
     a.Ms = reinterpret_cast<float*>(base + L.Ms);

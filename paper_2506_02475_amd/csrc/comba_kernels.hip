@@ -1030,7 +1030,7 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const float* __restrict__ g,
     const bf16_t* __restrict__ beta_tilde, const float* __restrict__ d,
     const ChunkInfo* __restrict__ cmap, int Tfix, int H, int16_t* __restrict__ Mq, float* __restrict__ Ms, int16_t* __restrict__ Aq,
-    float* __restrict__ As, bf16_t* __restrict__ QTp, float* __restrict__ Gw, float* __restrict__ sink) {
+    float* __restrict__ As, bf16_t* __restrict__ QTp, float* __restrict__ Gw) {
   // M leaves as int16 with one power-of-two scale per row, A with one per
   // column (see q_pack4).  The forward scan takes M's row scale out of the
   // rows of M R and folds A's column scale into the matching rows of D before
@@ -1221,11 +1221,11 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     const float* __restrict__ Ms, const int16_t* __restrict__ Aq, const float* __restrict__ As,
     const float* __restrict__ Gw, float* __restrict__ o, float* __restrict__ ht, int16_t* __restrict__ Xq,
     float* __restrict__ Xs, int16_t* __restrict__ Dq, float* __restrict__ Ds,
-    int16_t* __restrict__ Xfq, float* __restrict__ Xfs, float* __restrict__ sink) {
+    int16_t* __restrict__ Xfq, float* __restrict__ Xfs) {
   // Every global load and store inside the chunk loop is issued unconditionally
   // (clamped rows and chunk indices, masked values applied at use, padded-row
-  // stores sent to `sink`), so the memory-counter waits stay exact and the
-  // next chunk's loads overlap the current chunk's work.
+  // stores dropped by the record count of a raw buffer), so the memory-counter
+  // waits stay exact and the next chunk's loads overlap the current chunk's work.
   constexpr int NTV = BV / 16, XMT = DK / 64, KS = DK / 32, CC = CH * CH;
   constexpr int NB = DV / 32;
   // row-major BV-wide tiles: 72-byte rows put the four rows of a transposing
@@ -1584,8 +1584,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     const float* __restrict__ Ms, const int16_t* __restrict__ Aq, const float* __restrict__ As,
     const bf16_t* __restrict__ QTp,
     const float* __restrict__ Gw, float* __restrict__ dh0, int16_t* __restrict__ Yq,
-    float* __restrict__ Ys, int16_t* __restrict__ dRq, float* __restrict__ dRs,
-    float* __restrict__ sink) {
+    float* __restrict__ Ys, int16_t* __restrict__ dRq, float* __restrict__ dRs) {
   // as in the forward scan, all loop memory operations are unconditional
   constexpr int NTV = BV / 16, XMT = DK / 64, KS = DK / 32, CC = CH * CH;
   constexpr int NB = DV / 32;
@@ -2011,7 +2010,7 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     const float* __restrict__ Ds, const int16_t* __restrict__ Yq, const float* __restrict__ Ys,
     const int16_t* __restrict__ dRq, const float* __restrict__ dRs, int ncmax, float* __restrict__ dq, float* __restrict__ dk,
     float* __restrict__ dv, float* __restrict__ dbeta, float* __restrict__ dbeta_tilde,
-    float* __restrict__ dg, float* __restrict__ ddp, float* __restrict__ sink) {
+    float* __restrict__ dg, float* __restrict__ ddp) {
   using SM = IntraBwdBfSmem<DK>;
   constexpr int VB = SM::VB, LDB = SM::LDB, LDK = SM::LDK, LDC = SM::LDC;
   constexpr int NTW = DK / 32;          // dk column tiles per wave
@@ -2127,7 +2126,8 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
   };
   float Fpart = 0.f, bv = 0.f;
   float4 fdr;  // this thread's dR piece, kept for <v_r, dR_r> after the barrier
-  float* dv_i = dv + tok * DV;
+  // this chunk's dv rows (row r at r H DV), bounded at row len
+  const __amdgpu_buffer_rsrc_t rdv = clip_rsrc(dv + tok * DV, len * (H * DV * 4));
   auto put = [&](int vb) {
     const int j = vb * VB;
     if (pb == (vb & 1)) {
@@ -2156,9 +2156,8 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
     }
     // dv = Diag(beta) dR
     const float b = Bs[pf_r];
-    const float4 dvv = make_float4(b * fdr.x, b * fdr.y, b * fdr.z, b * fdr.w);
-    float* dst = pf_r < len ? &at(dv_i, 4u * ((unsigned)pf_r * (H * DV) + j + pf_c)) : sink + (tid & 63) * 4;
-    *reinterpret_cast<float4*>(dst) = dvv;
+    store_clip4(floatx4{b * fdr.x, b * fdr.y, b * fdr.z, b * fdr.w}, rdv,
+                4u * ((unsigned)pf_r * (H * DV) + j + pf_c));  // rows >= len dropped
   };
 
   floatx4 T1[NTW], T2[NTW], T3[NTW], dA[2], dL[2];
@@ -2569,8 +2568,7 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_wide(
     const float* __restrict__ Ds, const int16_t* __restrict__ Yq, const float* __restrict__ Ys,
     const int16_t* __restrict__ dRq, const float* __restrict__ dRs, float* __restrict__ dq,
     float* __restrict__ dk, float* __restrict__ dv, float* __restrict__ dbeta,
-    float* __restrict__ dbeta_tilde, float* __restrict__ dg, float* __restrict__ ddp,
-    float* __restrict__ sink) {
+    float* __restrict__ dbeta_tilde, float* __restrict__ dg, float* __restrict__ ddp) {
   constexpr int DKP = 128, KP = DK / DKP;
   static_assert(DK % DKP == 0, "dk slices");
   using SM = IntraBwdBfSmem<DKP>;
@@ -2631,7 +2629,8 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_wide(
   const int16_t* Yq_i = Yq + chh * NB * DK * VB;
   const float* Xs_i = Xs + chh * NB * DK;
   const float* Ys_i = Ys + chh * NB * DK;
-  float* dv_i = dv + tok * DV;
+  // this chunk's dv rows (row r at r H DV), bounded at row len
+  const __amdgpu_buffer_rsrc_t rdv = clip_rsrc(dv + tok * DV, len * (H * DV * 4));
   // this chunk's rows (row r at r H DK), bounded at row len
   const __amdgpu_buffer_rsrc_t rq = clip_rsrc(dq + tok * DK, len * (H * DK * 4));
   const __amdgpu_buffer_rsrc_t rk = clip_rsrc(dk + tok * DK, len * (H * DK * 4));
@@ -2695,9 +2694,8 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_wide(
       }
       if (kh == 0) {  // dv = Diag(beta) dR, once
         const float b = Bs[pf_r];
-        const float4 dvv = make_float4(b * fdr.x, b * fdr.y, b * fdr.z, b * fdr.w);
-        float* dst = pf_r < len ? &at(dv_i, 4u * ((unsigned)pf_r * (H * DV) + j + pf_c)) : sink + (tid & 63) * 4;
-        *reinterpret_cast<float4*>(dst) = dvv;
+        store_clip4(floatx4{b * fdr.x, b * fdr.y, b * fdr.z, b * fdr.w}, rdv,
+                    4u * ((unsigned)pf_r * (H * DV) + j + pf_c));  // rows >= len dropped
       }
     };
 
@@ -3073,20 +3071,20 @@ static hipError_t run_fwd_bf(const LaunchArgs& a) {
   if (a.ncmax > 0) {
     if (a.saved)
       k_prep_bf<DK, true><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
-          q, k, a.g, bt, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.QTp, a.Gw, a.sink);
+          q, k, a.g, bt, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.QTp, a.Gw);
     else
       k_prep_bf<DK, false><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
-          q, k, a.g, bt, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, nullptr, a.Gw, a.sink);
+          q, k, a.g, bt, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, nullptr, a.Gw);
   }
   a.stage(a.saved ? "scan_fwd_save" : "scan_fwd");
   if (a.saved)
     k_scan_fwd_bf<DK, DV, SCAN_BV, true, true><<<scan_blocks(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
         q, k, v, beta, bt, a.d, a.h0, a.smap, sord, a.N, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, a.o, a.ht, a.Xq, a.Xs,
-        a.Dq, a.Ds, a.Xfq, a.Xfs, a.sink);
+        a.Dq, a.Ds, a.Xfq, a.Xfs);
   else
     k_scan_fwd_bf<DK, DV, SCAN_BV, true, false><<<scan_blocks(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
         q, k, v, beta, bt, a.d, a.h0, a.smap, sord, a.N, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, a.o, a.ht, nullptr,
-        nullptr, nullptr, nullptr, nullptr, nullptr, a.sink);
+        nullptr, nullptr, nullptr, nullptr, nullptr);
   a.stage(nullptr);
   return hipGetLastError();
 }
@@ -3115,16 +3113,16 @@ static hipError_t run_bwd_bf(const LaunchArgs& a) {
     a.stage("prep");
     if (a.ncmax > 0)
       k_prep_bf<DK, true><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
-          q, k, a.g, bt, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.QTp, a.Gw, a.sink);
+          q, k, a.g, bt, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.QTp, a.Gw);
     a.stage("scan_fwd_store");
     k_scan_fwd_bf<DK, DV, SCAN_BV, false, true><<<scan_blocks(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
         q, k, v, beta, bt, a.d, a.h0, a.smap, sord, a.N, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, nullptr, nullptr, a.Xq,
-        a.Xs, a.Dq, a.Ds, a.Xfq, a.Xfs, a.sink);
+        a.Xs, a.Dq, a.Ds, a.Xfq, a.Xfs);
   }
   a.stage("scan_bwd");
   k_scan_bwd_bf<DK, DV, SCAN_BV><<<scan_blocks(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
       q, k, dO, bt, a.d, a.dht, a.smap, sord, a.N, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.QTp, a.Gw, a.dh0, a.Yq,
-      a.Ys, a.dRq, a.dRs, a.sink);
+      a.Ys, a.dRq, a.dRs);
   a.stage("intra_bwd");
   if constexpr (DK > 128 || DV > 128) {
     // head dim 256: passes of 128 dk columns, one workgroup per chunk-head (at
@@ -3132,12 +3130,12 @@ static hipError_t run_bwd_bf(const LaunchArgs& a) {
     if (a.ncmax > 0)
       k_intra_bwd_wide<DK, DV><<<dim3(a.ncmax, a.H), IB_THR, 0, st>>>(
           q, k, v, dO, beta, bt, a.d, a.cmap, Tfix, a.H, a.Gw, a.Xq, a.Xs, a.Dq, a.Ds, a.Yq, a.Ys,
-          a.dRq, a.dRs, a.dq, a.dk_, a.dv_, a.dbeta, a.dbeta_tilde, a.dg, a.ddp, a.sink);
+          a.dRq, a.dRs, a.dq, a.dk_, a.dv_, a.dbeta, a.dbeta_tilde, a.dg, a.ddp);
   } else {
     if (a.ncmax > 0)
       k_intra_bwd_bf<DK, DV><<<dim3(intra_bwd_grid((long)a.ncmax * a.H)), IB_THR, 0, st>>>(
           q, k, v, dO, beta, bt, a.d, a.cmap, Tfix, a.H, a.Gw, a.Xq, a.Xs, a.Dq, a.Ds, a.Yq, a.Ys, a.dRq,
-          a.dRs, a.ncmax, a.dq, a.dk_, a.dv_, a.dbeta, a.dbeta_tilde, a.dg, a.ddp, a.sink);
+          a.dRs, a.ncmax, a.dq, a.dk_, a.dv_, a.dbeta, a.dbeta_tilde, a.dg, a.ddp);
   }
   a.stage("reduce_dd");
   k_reduce_dd<<<a.H, RDD_THR, 0, st>>>(a.ddp, a.ncmax, a.H, a.dd);

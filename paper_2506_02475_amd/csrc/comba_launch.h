@@ -58,7 +58,6 @@ struct LaunchArgs {
   float *Xs, *Ds, *Ys, *dRs;
   int16_t* Xfq;  // bf16 path: sink for the state after the last chunk (same layout)
   float* Xfs;    //   and its scales
-  float* sink;  // 1 KiB that absorbs stores of padded rows (never read)
   hipStream_t stream;
   StageHook hook;
   void stage(const char* name) const {
