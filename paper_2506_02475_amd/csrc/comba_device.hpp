@@ -215,9 +215,11 @@ __device__ __forceinline__ const T& at(const T* base, unsigned byte_off) {
 }
 // Stores through a raw buffer whose record count ends at byte nbytes of g: the
 // hardware drops every store at or past it, so the rows past a chunk end need
-// no branch around their stores (nbytes >= 0, g 4-byte aligned).
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t clip_rsrc(float* g, int nbytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(g, 0, nbytes, 0x00020000);
+// no branch around their stores (g 4-byte aligned).  The record count is an
+// unsigned 32-bit field: a chunk's rows at H <= 65535 heads of up to 256
+// values span less than 2^32 bytes.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t clip_rsrc(float* g, unsigned nbytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(g, 0, (int)nbytes, 0x00020000);
 }
 __device__ __forceinline__ void store_clip(float x, __amdgpu_buffer_rsrc_t rs, unsigned byte_off) {
   __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), rs, byte_off, 0, 0);

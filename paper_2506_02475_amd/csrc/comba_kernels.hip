@@ -1547,7 +1547,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
       }
       load_a(nx);
       // rows past the chunk end fall past the record count: dropped
-      const __amdgpu_buffer_rsrc_t ro = clip_rsrc(o + tok * DV + j0, len * (H * DV * 4));
+      const __amdgpu_buffer_rsrc_t ro = clip_rsrc(o + tok * DV + j0, (unsigned)len * (unsigned)(H * DV * 4));
 #pragma unroll
       for (int nt = 0; nt < NTV; ++nt) {
         floatx4 ov;
@@ -2127,7 +2127,7 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
   float Fpart = 0.f, bv = 0.f;
   float4 fdr;  // this thread's dR piece, kept for <v_r, dR_r> after the barrier
   // this chunk's dv rows (row r at r H DV), bounded at row len
-  const __amdgpu_buffer_rsrc_t rdv = clip_rsrc(dv + tok * DV, len * (H * DV * 4));
+  const __amdgpu_buffer_rsrc_t rdv = clip_rsrc(dv + tok * DV, (unsigned)len * (unsigned)(H * DV * 4));
   auto put = [&](int vb) {
     const int j = vb * VB;
     if (pb == (vb & 1)) {
@@ -2496,8 +2496,8 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_bf(
   }
   float ddpart = 0.f;
   // this chunk's rows (row r at r H DK), bounded at row len
-  const __amdgpu_buffer_rsrc_t rq = clip_rsrc(dq + tok * DK, len * (H * DK * 4));
-  const __amdgpu_buffer_rsrc_t rk = clip_rsrc(dk + tok * DK, len * (H * DK * 4));
+  const __amdgpu_buffer_rsrc_t rq = clip_rsrc(dq + tok * DK, (unsigned)len * (unsigned)(H * DK * 4));
+  const __amdgpu_buffer_rsrc_t rk = clip_rsrc(dk + tok * DK, (unsigned)len * (unsigned)(H * DK * 4));
 #pragma unroll
   for (int j = 0; j < NTW; ++j) {
     floatx4 dkv;
@@ -2630,10 +2630,10 @@ __global__ __launch_bounds__(IB_THR, 1) void k_intra_bwd_wide(
   const float* Xs_i = Xs + chh * NB * DK;
   const float* Ys_i = Ys + chh * NB * DK;
   // this chunk's dv rows (row r at r H DV), bounded at row len
-  const __amdgpu_buffer_rsrc_t rdv = clip_rsrc(dv + tok * DV, len * (H * DV * 4));
+  const __amdgpu_buffer_rsrc_t rdv = clip_rsrc(dv + tok * DV, (unsigned)len * (unsigned)(H * DV * 4));
   // this chunk's rows (row r at r H DK), bounded at row len
-  const __amdgpu_buffer_rsrc_t rq = clip_rsrc(dq + tok * DK, len * (H * DK * 4));
-  const __amdgpu_buffer_rsrc_t rk = clip_rsrc(dk + tok * DK, len * (H * DK * 4));
+  const __amdgpu_buffer_rsrc_t rq = clip_rsrc(dq + tok * DK, (unsigned)len * (unsigned)(H * DK * 4));
+  const __amdgpu_buffer_rsrc_t rk = clip_rsrc(dk + tok * DK, (unsigned)len * (unsigned)(H * DK * 4));
   floatx4 dA[2], dL[2];
   dA[0] = dA[1] = dL[0] = dL[1] = zero4();
   float bv = 0.f;
