@@ -16,10 +16,12 @@ bounded sample of the same workload.  The roofline credits the dominant kernel
 with the method's minimal HBM bytes (and flops) of its direction: the
 backward's q, k, v, dO and one fp32 state per chunk in, fp32 dq, dk, dv out
 (method_model), divided by the kernel's average launch time (HIP events
-recorded by the library on its launch stream over the timed region); the
-bytes this design's own intermediates add are reported beside them
-("design_bytes"), and "step_roofline" holds the whole step's method bytes and
-flops over the step time.  Separate forward and backward times, per-kernel MFMA
+recorded by the library on its launch stream over the timed region, right
+before and after that kernel only, on every fourth step: timing every stage
+there would add about 3% to the step); the per-stage breakdown comes from a separate pass before the
+timed region (timed_steps); the bytes this design's own intermediates add are
+reported beside them ("design_bytes"), and "step_roofline" holds the whole
+step's method bytes and flops over the step time.  Separate forward and backward times, per-kernel MFMA
 use (algorithmic, and counted by rocprofv3 where the committed counters match
 the kernel source) are reported too.  Further legs timed after the headline
 region under "variants": the training pair with a separate state-feedback
@@ -352,6 +354,49 @@ def time_decode(comba, torch, steps, warmup, threads=None, with_cpu=False):
 PREFILL256 = dict(B=4, T=4096, H=8, dk=256, dv=256, seed=63)
 
 
+def timed_steps(comba, torch, step, steps, sample_every=4):
+    """The timing protocol of every leg (after its warm-up).  First a stage
+    pass: `steps` steps with a HIP event on the launch stream before every
+    kernel stage, which gives each stage's average launch duration and picks
+    the dominant stage (largest time per step); its step time is not reported.
+    Then the timed region: `steps` steps bracketed by device synchronisations,
+    in which every `sample_every`-th step records events right before and right
+    after the dominant stage only (comba_profile_select; the other steps record
+    none), so the stages run back to back as they do without timing, and the
+    dominant stage's duration is still measured live over the timed region.
+    (An event pair costs the step about 9 us of idle GPU, 1.2% at the 1.3B
+    shape; every stage marked costs 3%.)"""
+    torch.cuda.synchronize()
+    comba.profile_select(None)
+    comba.profile_enable(True)
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    marks = comba.profile_read()
+    comba.profile_enable(False)
+    tot, cnt = {}, {}
+    for name, ms in marks:
+        tot[name] = tot.get(name, 0.0) + ms
+        cnt[name] = cnt.get(name, 0) + 1
+    dom = max(tot, key=tot.get)
+    comba.profile_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        # a name no stage has: that step records nothing
+        comba.profile_select(dom if i % sample_every == 0 else "-")
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    live = [ms for name, ms in comba.profile_read() if name == dom]
+    comba.profile_enable(False)
+    comba.profile_select(None)
+    return {"ms_per_step": (t1 - t0) * 1e3 / steps,
+            "stages_ms": {n: x / steps for n, x in tot.items()},
+            "stage_avg_ms": {n: tot[n] / cnt[n] for n in tot},
+            "dominant": dom, "dom_avg_ms": sum(live) / len(live), "dom_launches_timed": len(live)}
+
+
 def time_train256(comba, torch, steps, warmup):
     """Training pair (comba_chunk_fwd_save + comba_chunk_bwd_saved) at head dim 256:
     B4 T4096 H8 d256 bf16.  Per-stage live timing; roofline of the dominant stage."""
@@ -378,31 +423,18 @@ def time_train256(comba, torch, steps, warmup):
 
     for _ in range(warmup):
         step()
-    torch.cuda.synchronize()
-    comba.profile_enable(True)
-    t0 = time.perf_counter()
-    for _ in range(steps):
-        step()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    marks = comba.profile_read()
-    comba.profile_enable(False)
-    tot, cnt = {}, {}
-    for name, ms in marks:
-        tot[name] = tot.get(name, 0.0) + ms
-        cnt[name] = cnt.get(name, 0) + 1
-    dom = max(tot, key=tot.get)
-    avg = tot[dom] / cnt[dom]
-    ms_step = (t1 - t0) * 1e3 / steps
-    roof = kernel_roofline(dom, avg, method_model(stage_direction(dom), B, T, H, dk, dv),
+    tm = timed_steps(comba, torch, step, steps)
+    dom, ms_step, tot = tm["dominant"], tm["ms_per_step"], tm["stages_ms"]
+    roof = kernel_roofline(dom, tm["dom_avg_ms"],
+                           method_model(stage_direction(dom), B, T, H, dk, dv),
                            design=stage_model(dom, B, T, H, dk, dv),
                            traffic=measured_traffic(dom, TRAIN256_TRAFFIC))
     return {"value": round(B * T / (ms_step * 1e-3), 1), "unit": "tokens/s",
             "ms_per_step": round(ms_step, 4),
-            "ms_fwd": round(sum(x for n, x in tot.items() if n in FWD_STAGES) / steps, 4),
-            "ms_bwd": round(sum(x for n, x in tot.items() if n in BWD_STAGES) / steps, 4),
+            "ms_fwd": round(sum(x for n, x in tot.items() if n in FWD_STAGES), 4),
+            "ms_bwd": round(sum(x for n, x in tot.items() if n in BWD_STAGES), 4),
             "config": {k_: c[k_] for k_ in ("B", "T", "H", "dk", "dv")},
-            "stages_ms": {n: round(x / steps, 4) for n, x in tot.items()},
+            "stages_ms": {n: round(x, 4) for n, x in tot.items()},
             "roofline": roof}
 
 
@@ -431,32 +463,21 @@ def time_prefill256(comba, torch, steps, warmup):
                                t(w.d), t(w.h0))
     B, T, H, dk, dv = c["B"], c["T"], c["H"], c["dk"], c["dv"]
     ws = torch.empty(comba.fwd_workspace_bytes(B, T, H, dk, dv), dtype=torch.uint8, device=dev)
+    def call():
+        return comba.comba_chunk_fwd(q, k, v, g, beta, d, h0, workspace=ws)
+
     for _ in range(warmup):
-        comba.comba_chunk_fwd(q, k, v, g, beta, d, h0, workspace=ws)
-    torch.cuda.synchronize()
-    comba.profile_enable(True)
-    t0 = time.perf_counter()
-    for _ in range(steps):
-        comba.comba_chunk_fwd(q, k, v, g, beta, d, h0, workspace=ws)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    marks = comba.profile_read()
-    comba.profile_enable(False)
-    tot, cnt = {}, {}
-    for name, ms in marks:
-        tot[name] = tot.get(name, 0.0) + ms
-        cnt[name] = cnt.get(name, 0) + 1
-    dom = max(tot, key=tot.get)
-    avg = tot[dom] / cnt[dom]
-    ms_step = (t1 - t0) * 1e3 / steps
-    roof = kernel_roofline(dom, avg,
+        call()
+    tm = timed_steps(comba, torch, call, steps)
+    dom, ms_step, tot = tm["dominant"], tm["ms_per_step"], tm["stages_ms"]
+    roof = kernel_roofline(dom, tm["dom_avg_ms"],
                            method_model(stage_direction(dom, saved=False), B, T, H, dk, dv),
                            design=stage_model(dom, B, T, H, dk, dv),
                            traffic=measured_traffic(dom, PREFILL256_TRAFFIC))
     return {"value": round(B * T / (ms_step * 1e-3), 1), "unit": "tokens/s",
             "ms_per_step": round(ms_step, 4),
             "config": {k_: c[k_] for k_ in ("B", "T", "H", "dk", "dv")},
-            "stages_ms": {n: round(x / steps, 4) for n, x in tot.items()},
+            "stages_ms": {n: round(x, 4) for n, x in tot.items()},
             "roofline": roof}
 
 
@@ -496,31 +517,18 @@ def time_varlen(comba, torch, steps, warmup):
 
     for _ in range(warmup):
         call()
-    torch.cuda.synchronize()
-    comba.profile_enable(True)
-    t0 = time.perf_counter()
-    for _ in range(steps):
-        call()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    marks = comba.profile_read()
-    comba.profile_enable(False)
-    tot, cnt = {}, {}
-    for name, ms in marks:
-        tot[name] = tot.get(name, 0.0) + ms
-        cnt[name] = cnt.get(name, 0) + 1
-    dom = max(tot, key=tot.get)
-    avg = tot[dom] / cnt[dom]
-    ms_step = (t1 - t0) * 1e3 / steps
+    tm = timed_steps(comba, torch, call, steps)
+    dom, ms_step, tot = tm["dominant"], tm["ms_per_step"], tm["stages_ms"]
     fwd = method_model("fwd", 1, T, H, dk, dv, cu_seqlens=cu_host)
-    roof = kernel_roofline(dom, avg, fwd, traffic=measured_traffic(dom, VARLEN_TRAFFIC))
+    roof = kernel_roofline(dom, tm["dom_avg_ms"], fwd,
+                           traffic=measured_traffic(dom, VARLEN_TRAFFIC))
     lens = np.diff(cu_host)
     return {"value": round(T / (ms_step * 1e-3), 1), "unit": "tokens/s",
             "ms_per_step": round(ms_step, 4),
             "config": {"N": int(N), "T_total": int(T), "H": H, "dk": dk, "dv": dv,
                        "longest": int(lens.max()), "shortest": int(lens.min())},
             "workload": spec.name,
-            "stages_ms": {n: round(x / steps, 4) for n, x in tot.items()},
+            "stages_ms": {n: round(x, 4) for n, x in tot.items()},
             "step_roofline": {"method_bytes": fwd[1],
                               "frac_hbm": round(fwd[1] / (ms_step * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
                               "method_flops": fwd[0],
@@ -569,29 +577,18 @@ def time_prologue(comba, torch, steps, warmup):
 
     for _ in range(warmup):
         step()
-    torch.cuda.synchronize()
-    comba.profile_enable(True)
-    t0 = time.perf_counter()
-    for _ in range(steps):
-        step()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    marks = comba.profile_read()
-    comba.profile_enable(False)
-    tot, cnt = {}, {}
-    for name, ms in marks:
-        tot[name] = tot.get(name, 0.0) + ms
-        cnt[name] = cnt.get(name, 0) + 1
+    tm = timed_steps(comba, torch, step, steps)
+    ms_step, tot = tm["ms_per_step"], tm["stages_ms"]
     roof = {}
     for st in ("prologue_fwd", "prologue_bwd"):
-        avg = tot[st] / cnt[st]
+        # the dominant stage live over the timed region, the other from the stage pass
+        avg = tm["dom_avg_ms"] if st == tm["dominant"] else tm["stage_avg_ms"][st]
         by = prologue_bytes(st, c["B"], c["T"], c["H"], c["dk"], c["dv"])
         ach = by / (avg * 1e-3) / 1e9
         roof[st] = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
                     "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4),
                     "traffic": measured_traffic(st, PROLOGUE_TRAFFIC, PROLOGUE_SOURCES),
                     "kernel": st, "avg_launch_ms": round(avg, 4), "algorithmic_bytes": by}
-    ms_step = (t1 - t0) * 1e3 / steps
     # the output gate on the operator's output shape (o fp32, z bf16): stream
     # events around back-to-back calls
     n = c["B"] * c["T"] * c["H"] * c["dv"]
@@ -615,7 +612,7 @@ def time_prologue(comba, torch, steps, warmup):
     return {"value": round(c["B"] * c["T"] / (ms_step * 1e-3), 1), "unit": "tokens/s",
             "ms_per_step": round(ms_step, 4),
             "config": {k_: c[k_] for k_ in ("B", "T", "H", "dk", "dv")},
-            "stages_ms": {n_: round(x / steps, 4) for n_, x in tot.items()},
+            "stages_ms": {n_: round(x, 4) for n_, x in tot.items()},
             "roofline": roof["prologue_bwd"], "roofline_fwd": roof["prologue_fwd"], "gate": gate}
 
 
@@ -845,37 +842,22 @@ def main():
 
     for _ in range(args.warmup):
         step()
-    torch.cuda.synchronize()
-
-    comba.profile_enable(True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    stages = comba.profile_read()
-    comba.profile_enable(False)
-
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    tm = timed_steps(comba, torch, step, args.steps)
+    ms_per_step = tm["ms_per_step"]
     tokens = B * T
-    value = tokens / ((t1 - t0) / args.steps)
-
-    # per-stage average launch duration (ms) over the timed region
-    agg = {}
-    for name, ms in stages:
-        s = agg.setdefault(name, [0.0, 0])
-        s[0] += ms
-        s[1] += 1
-    avg = {n: s[0] / s[1] for n, s in agg.items()}
-    tot = {n: s[0] / args.steps for n, s in agg.items()}
-    dom = max(tot, key=tot.get)
+    value = tokens / (ms_per_step * 1e-3)
+    # per-stage average launch durations (ms) from the stage pass; the dominant
+    # stage's is its live average over the timed region
+    dom, tot = tm["dominant"], tm["stages_ms"]
+    avg = dict(tm["stage_avg_ms"])
+    avg[dom] = tm["dom_avg_ms"]
     models = {dr: method_model(dr, B, T, H, dk, dv) for dr in ("fwd_save", "bwd")}
     # the committed counters cover the headline workload only
     roof = kernel_roofline(dom, avg[dom], models[stage_direction(dom)],
                            design=stage_model(dom, B, T, H, dk, dv, sep_bt=args.beta_tilde),
                            traffic=None if args.beta_tilde else measured_traffic(dom),
                            mfma_counted=None if args.beta_tilde else measured_mfma(dom))
+    roof["launches_timed"] = tm["dom_launches_timed"]
     mfma_by_kernel = {}
     for n in tot:
         dfl, _ = stage_model(n, B, T, H, dk, dv, sep_bt=args.beta_tilde)
@@ -935,22 +917,11 @@ def main():
         # the same training pair with beta~ = b * beta, timed after the headline region
         for _ in range(args.warmup):
             step(bt_var)
-        torch.cuda.synchronize()
-        comba.profile_enable(True)
-        t0 = time.perf_counter()
-        for _ in range(args.steps):
-            step(bt_var)
-        torch.cuda.synchronize()
-        t1 = time.perf_counter()
-        st_bt = comba.profile_read()
-        comba.profile_enable(False)
-        agg_bt = {}
-        for name, ms in st_bt:
-            agg_bt[name] = agg_bt.get(name, 0.0) + ms / args.steps
+        tm_bt = timed_steps(comba, torch, lambda: step(bt_var), args.steps)
         result["variants"] = {"beta_tilde_b_beta": {
-            "value": round(tokens / ((t1 - t0) / args.steps), 1), "unit": "tokens/s",
-            "ms_per_step": round((t1 - t0) * 1e3 / args.steps, 4),
-            "stages_ms": {n: round(x, 4) for n, x in agg_bt.items()}}}
+            "value": round(tokens / (tm_bt["ms_per_step"] * 1e-3), 1), "unit": "tokens/s",
+            "ms_per_step": round(tm_bt["ms_per_step"], 4),
+            "stages_ms": {n: round(x, 4) for n, x in tm_bt["stages_ms"].items()}}}
         result["variants"]["decode_b64_h16_d128"] = time_decode(comba, torch, args.steps,
                                                                 args.warmup)
         result["variants"]["prefill_b4_t4096_h8_d256"] = time_prefill256(comba, torch,

@@ -268,6 +268,17 @@ comba_status comba_gate_bwd(const comba_shape *shape, const float *o, const void
 comba_status comba_profile_enable(int enable);
 int comba_profile_read(float *ms, const char **names, int capacity);
 
+/*
+ * Stage selection for the timing above (benchmarks only).  With a stage name
+ * (for example "intra_bwd"; the name is copied), the calling thread's
+ * recording sessions record only two events per call: one before that stage
+ * and one right after it, so comba_profile_read returns that stage's
+ * durations alone and the other stages run without event records between
+ * them.  NULL (the default) records every stage.  The selection holds until
+ * the next call of this function on the thread.  Always returns COMBA_OK.
+ */
+comba_status comba_profile_select(const char *stage);
+
 /* Human-readable name of a status code (static storage). */
 const char *comba_status_string(comba_status status);
 

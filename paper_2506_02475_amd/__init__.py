@@ -104,6 +104,8 @@ def load_library():
             lib.comba_profile_enable.restype = I
             lib.comba_profile_read.argtypes = [P, P, I]
             lib.comba_profile_read.restype = I
+            lib.comba_profile_select.argtypes = [ctypes.c_char_p]
+            lib.comba_profile_select.restype = I
             lib.comba_status_string.argtypes = [I]
             lib.comba_status_string.restype = ctypes.c_char_p
             _lib = lib
@@ -113,6 +115,12 @@ def load_library():
 def profile_enable(on: bool = True) -> None:
     """Turn per-stage HIP-event timing of the entry points on or off (this thread)."""
     _check(load_library().comba_profile_enable(1 if on else 0))
+
+
+def profile_select(stage=None) -> None:
+    """Record only the named stage's start and end in later timing sessions of
+    this thread (None: every stage)."""
+    _check(load_library().comba_profile_select(None if stage is None else stage.encode()))
 
 
 def profile_read(capacity: int = 4096):

@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <string>
 #include <vector>
 
 #include "comba.h"
@@ -165,11 +166,19 @@ struct Profile {
   size_t n = 0;
   std::vector<hipEvent_t> ev;
   std::vector<const char*> names;
+  std::string only;   // when not empty: record only this stage (its start and its end)
+  bool open = false;  // the selected stage's start is recorded, its end comes next
 };
 thread_local Profile g_prof;
 
 void prof_mark(void* ctx, hipStream_t st, const char* name) {
   Profile* p = static_cast<Profile*>(ctx);
+  if (!p->only.empty()) {
+    const bool sel = name && p->only == name;
+    if (!sel && !p->open) return;  // neither the selected stage's start nor its end
+    if (!sel) name = nullptr;      // the selected stage's end: no stage of its own
+    p->open = sel;
+  }
   if (p->n == p->ev.size()) {
     hipEvent_t e = nullptr;
     if (hipEventCreate(&e) != hipSuccess) return;
@@ -506,6 +515,13 @@ size_t comba_bwd_workspace_bytes(const comba_shape* shape) {
 comba_status comba_profile_enable(int enable) {
   g_prof.on = enable != 0;
   g_prof.n = 0;
+  g_prof.open = false;
+  return COMBA_OK;
+}
+
+comba_status comba_profile_select(const char* stage) {
+  g_prof.only = stage ? stage : "";
+  g_prof.open = false;
   return COMBA_OK;
 }
 

@@ -58,6 +58,7 @@ def test_library_exports_every_declared_symbol():
     assert set(declared) == {"comba_fwd_workspace_bytes", "comba_bwd_workspace_bytes",
                              "comba_chunk_fwd", "comba_chunk_bwd", "comba_status_string",
                              "comba_profile_enable", "comba_profile_read",
+                             "comba_profile_select",
                              "comba_chunk_fwd_save", "comba_chunk_bwd_saved",
                              "comba_recurrent_fwd", "comba_prologue_fwd", "comba_prologue_bwd",
                              "comba_prologue_workspace_bytes", "comba_gate_fwd", "comba_gate_bwd",
@@ -73,6 +74,16 @@ def test_library_exports_every_declared_symbol():
 def test_profile_read_without_calls_is_empty():
     comba.profile_enable(True)
     assert comba.profile_read() == []
+
+
+def test_profile_select_sets_and_clears_without_a_device():
+    # selecting a stage touches no device; a session with a selection and no
+    # calls records nothing
+    comba.profile_select("intra_bwd")
+    comba.profile_enable(True)
+    assert comba.profile_read() == []
+    comba.profile_enable(False)
+    comba.profile_select(None)
     comba.profile_enable(False)
 
 
