@@ -537,6 +537,70 @@ def time_varlen(comba, torch, steps, warmup):
             "roofline": roof}
 
 
+def time_long1(comba, torch, steps, warmup):
+    """One long sequence: the long-context workload's tokens (config 4's 16
+    packed sequences, 525,868 tokens, H16 d128 bf16) cut to 525,824 tokens (a
+    whole number of chunks) and run as ONE sequence through the stateless
+    comba_chunk_fwd with its initial state.  The scan then has only H x dv/32 =
+    64 chains for 256 CUs, so the forward cuts the sequence into segments
+    (segmented scan, COMBA_SCAN_SEGMENTS unset); the same call with
+    COMBA_SCAN_SEGMENTS=1 (one chain per slice over the whole sequence) is
+    timed beside it.  The roofline credits the dominant stage with the
+    forward's method bytes."""
+    import numpy as np
+    from comba_inputs import generate
+
+    w = generate(4)
+    dev = torch.device("cuda:0")
+    bf = torch.bfloat16
+    T = (w.T // 512) * 512       # whole chunks, divisible into up to 8 segments
+    H, dk, dv = w.H, w.dk, w.dv
+
+    def t(x, dt=torch.float32):
+        return torch.from_numpy(np.ascontiguousarray(x)).to(dev, dt)
+
+    q, k, v = t(w.q[:, :T], bf), t(w.k[:, :T], bf), t(w.v[:, :T], bf)
+    g, beta, d = t(w.g[:, :T]), t(w.beta[:, :T], bf), t(w.d)
+    h0 = t(w.h0[:1])
+    del w
+    old = os.environ.get("COMBA_SCAN_SEGMENTS")
+    out = {}
+    try:
+        for mode, env in (("segmented", None), ("plain", "1")):
+            if env is None:
+                os.environ.pop("COMBA_SCAN_SEGMENTS", None)
+            else:
+                os.environ["COMBA_SCAN_SEGMENTS"] = env
+            ws = torch.empty(comba.fwd_workspace_bytes(1, T, H, dk, dv), dtype=torch.uint8,
+                             device=dev)
+
+            def call():
+                return comba.comba_chunk_fwd(q, k, v, g, beta, d, h0, workspace=ws)
+
+            for _ in range(warmup):
+                call()
+            out[mode] = timed_steps(comba, torch, call, steps)
+            del ws
+    finally:
+        if old is None:
+            os.environ.pop("COMBA_SCAN_SEGMENTS", None)
+        else:
+            os.environ["COMBA_SCAN_SEGMENTS"] = old
+    tm = out["segmented"]
+    fwd = method_model("fwd", 1, T, H, dk, dv)
+    roof = kernel_roofline(tm["dominant"], tm["dom_avg_ms"], fwd)
+    ms = tm["ms_per_step"]
+    return {"value": round(T / (ms * 1e-3), 1), "unit": "tokens/s", "ms_per_step": round(ms, 4),
+            "config": {"B": 1, "T": T, "H": H, "dk": dk, "dv": dv},
+            "stages_ms": {n: round(x, 4) for n, x in tm["stages_ms"].items()},
+            "plain_ms_per_step": round(out["plain"]["ms_per_step"], 4),
+            "plain_stages_ms": {n: round(x, 4) for n, x in out["plain"]["stages_ms"].items()},
+            "speedup_vs_plain": round(out["plain"]["ms_per_step"] / ms, 3),
+            "step_roofline": {"method_bytes": fwd[1],
+                              "frac_hbm": round(fwd[1] / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
+            "roofline": roof}
+
+
 PROLOGUE = dict(B=4, T=4096, H=16, dk=128, dv=128, seed=71)
 PROLOGUE_SOURCES = ("comba_prologue.hip", "comba_device.hpp")
 PROLOGUE_TRAFFIC = "traffic_counters_prologue_b4_t4096_h16_d128.md"
@@ -666,6 +730,10 @@ def main():
                          "H8 d256) as the headline")
     ap.add_argument("--train256", action="store_true",
                     help="time the training pair at head dim 256 (B4 T4096 H8 d256) as the headline")
+    ap.add_argument("--long1", action="store_true",
+                    help="time one long sequence (the long-context workload's 525,824 tokens as "
+                         "one row, H16 d128, comba_chunk_fwd, segmented scan vs plain) as the "
+                         "headline")
     ap.add_argument("--prologue", action="store_true",
                     help="time the layer input prologue (short conv, SiLU, L2 norm; fwd + bwd) "
                          "on the 1.3B layer's q, k, v as the headline")
@@ -720,6 +788,24 @@ def main():
             "step": "comba_prologue_fwd + comba_prologue_bwd", "stages_ms": r["stages_ms"],
             "roofline": r["roofline"], "roofline_fwd": r["roofline_fwd"], "gate": r["gate"],
             "cpu_baseline": None}
+        if args.copy_bytes > 0:
+            result["copy_bytes"] = calibration_copy(torch, args.copy_bytes)
+        print(json.dumps(result), flush=True)
+        return
+    if args.long1:
+        torch.cuda.set_device(0)
+        r = time_long1(comba, torch, args.steps, args.warmup)
+        result = {
+            "metric": "Comba forward tokens/s on one long sequence (525,824 tokens, H=16, d=128 "
+                      "bf16; segmented scan)",
+            "value": r["value"], "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": r["ms_per_step"], "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+            "data": "synthetic (seeded PCG64, comba_inputs.generate(4) as one sequence)",
+            "config": {"workload": "long1_525k_fwd", **r["config"]}, "step": "comba_chunk_fwd",
+            "stages_ms": r["stages_ms"], "plain_ms_per_step": r["plain_ms_per_step"],
+            "speedup_vs_plain": r["speedup_vs_plain"], "roofline": r["roofline"],
+            "step_roofline": r["step_roofline"], "cpu_baseline": None}
         if args.copy_bytes > 0:
             result["copy_bytes"] = calibration_copy(torch, args.copy_bytes)
         print(json.dumps(result), flush=True)
@@ -930,6 +1016,7 @@ def main():
                                                                          args.steps, args.warmup)
         result["variants"]["varlen_512k_fwd"] = time_varlen(comba, torch, args.steps,
                                                            args.warmup)
+        result["variants"]["long1_525k_fwd"] = time_long1(comba, torch, args.steps, args.warmup)
         result["variants"]["train_b4_t4096_h8_d256"] = time_train256(comba, torch, args.steps,
                                                                      args.warmup)
     if args.copy_bytes > 0:

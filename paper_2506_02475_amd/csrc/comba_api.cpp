@@ -2,6 +2,7 @@
 // workspace layout and kernel sequencing on the caller's stream.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+#include <stdlib.h>
 
 #include <string>
 #include <vector>
@@ -95,13 +96,40 @@ comba_status check_shape_recurrent(const comba_shape* s, Dims* out) {
   return st;
 }
 
+// Segments of the stateless bf16 forward (comba::LaunchArgs::segP; 1 = off).
+// Rows of fixed length are cut when their scan has at most half as many chains
+// (N H dv / 32) as the device has CUs, into the largest power of two P for
+// which the segments' chains are at most two per CU, P divides the row's
+// chunks and every segment keeps at least 16 chunks.  COMBA_SCAN_SEGMENTS overrides the
+// choice: 1 disables, P >= 2 forces P when it divides the row's chunks (P <= 64).
+int seg_parts(const Dims& d) {
+  if (!d.bf16 || d.N <= 0 || d.Tseq <= 0 || d.Tseq % kChunk) return 1;
+  const int n = d.Tseq / kChunk;
+  if (const char* env = getenv("COMBA_SCAN_SEGMENTS")) {
+    if (*env) {
+      const int P = atoi(env);
+      return P >= 2 && P <= 64 && n % P == 0 ? P : 1;
+    }
+  }
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return 1;
+  const long chains = (long)d.N * d.H * (d.dv / 32);
+  if (cus <= 0 || 2 * chains > cus) return 1;
+  int P = 1;
+  while (P < 64 && chains * 2 * P <= 2L * cus && n % (2 * P) == 0 && n / (2 * P) >= 16) P *= 2;
+  return P;
+}
+
 struct Layout {
   size_t cmap, smap, sord, M, A, G, X, D, Y, dR, ddp, QT, Xfin, total;
+  size_t segF, segPhi, segX0, segHT;  // segmented stateless forward (segP > 1)
   size_t Xs, Ds, Ys, dRs, Xfs;  // bf16 path: scales of the int16 X, D, Y, dR, final-state sink
   size_t Ms, As;                // bf16 path: row scales of M, column scales of A
 };
 
-Layout layout(const Dims& d, bool bwd) {
+Layout layout(const Dims& d, bool bwd, int segP = 1) {
   Layout L{};
   const size_t chh = (size_t)d.ncmax * d.H;
   size_t off = 0;
@@ -148,6 +176,14 @@ Layout layout(const Dims& d, bool bwd) {
     L.Y = take(chh * d.dk * d.dv * sizeof(float));
     L.dR = take(chh * kChunk * d.dv * sizeof(float));
     L.ddp = take(chh * sizeof(float));
+  }
+  if (!bwd && segP > 1) {
+    // per virtual row (segment) and head: F, X0, HT (dk x dv), Phi (dk x dk), fp32
+    const size_t nvr = (size_t)d.N * segP * d.H;
+    L.segF = take(nvr * d.dk * d.dv * sizeof(float));
+    L.segPhi = take(nvr * d.dk * d.dk * sizeof(float));
+    L.segX0 = take(nvr * d.dk * d.dv * sizeof(float));
+    L.segHT = take(nvr * d.dk * d.dv * sizeof(float));
   }
   L.total = off;
   return L;
@@ -262,7 +298,14 @@ comba_status chunk_fwd(bool save, const comba_shape* shape, const void* q, const
       (ht && !aligned(ht, 16)) || !aligned(beta, dm.bf16 ? 2 : 4) ||
       !aligned(beta_tilde, dm.bf16 ? 2 : 4))
     return COMBA_ERR_ALIGN;
-  const Layout L = layout(dm, save);
+  // the segmented scan when the workspace holds its buffers (sized by
+  // comba_fwd_workspace_bytes), else the plain one
+  int segP = save ? 1 : seg_parts(dm);
+  Layout L = layout(dm, save, segP);
+  if (ws_bytes < L.total && segP > 1) {
+    segP = 1;
+    L = layout(dm, save, 1);
+  }
   if (ws_bytes < L.total) return COMBA_ERR_WORKSPACE;
   comba::LaunchArgs a{};
   fill_common(a, dm, shape);
@@ -279,6 +322,14 @@ comba_status chunk_fwd(bool save, const comba_shape* shape, const void* q, const
   a.ht = ht;
   a.stream = static_cast<hipStream_t>(stream);
   carve(a, L, ws, save);
+  a.segP = segP;
+  if (segP > 1) {
+    char* base = static_cast<char*>(ws);
+    a.segF = reinterpret_cast<float*>(base + L.segF);
+    a.segPhi = reinterpret_cast<float*>(base + L.segPhi);
+    a.segX0 = reinterpret_cast<float*>(base + L.segX0);
+    a.segHT = reinterpret_cast<float*>(base + L.segHT);
+  }
   attach_profile(a);
   if (dm.N == 0) return COMBA_OK;
   return comba::launch_fwd(a) == hipSuccess ? COMBA_OK : COMBA_ERR_HIP;
@@ -462,6 +513,16 @@ comba_status gate(const comba_shape* shape, const float* o, const void* z, void*
 
 }  // namespace
 
+namespace comba {
+// The stateless forward's workspace without the segmented scan's buffers: a
+// call given this much runs the plain scan (comba_chunk_fwd_noalloc).
+size_t fwd_workspace_bytes_plain(const comba_shape* shape) {
+  Dims d;
+  if (check_shape(shape, &d, true) != COMBA_OK) return 0;
+  return layout(d, false, 1).total;
+}
+}  // namespace comba
+
 extern "C" {
 
 comba_status comba_gate_fwd(const comba_shape* shape, const float* o, const void* z, void* y,
@@ -503,7 +564,7 @@ comba_status comba_prologue_bwd(const comba_shape* shape, const void* xq, const 
 size_t comba_fwd_workspace_bytes(const comba_shape* shape) {
   Dims d;
   if (check_shape(shape, &d, true) != COMBA_OK) return 0;
-  return layout(d, false).total;
+  return layout(d, false, seg_parts(d)).total;
 }
 
 size_t comba_bwd_workspace_bytes(const comba_shape* shape) {

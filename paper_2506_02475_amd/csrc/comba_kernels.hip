@@ -956,15 +956,19 @@ __device__ __forceinline__ int frag_off(int row, int col) {
 // K, Q, M, A rows they all read are L2 hits for all but the first.  Chains are
 // taken rank-major (r = chain / H), with packed sequences in the order of
 // sorder (longest first); padding workgroups past the last chain return.
+// grp > 1 (the segmented forward's state passes): the rows are groups of grp
+// segments whose last one is skipped, so rank r is row (r / (grp - 1)) grp +
+// r % (grp - 1) and N counts the rows taken.
 template <int NSL>
-__device__ __forceinline__ bool scan_item(int N, int H, const int* sorder, int& s, int& h, int& zb) {
+__device__ __forceinline__ bool scan_item(int N, int H, const int* sorder, int& s, int& h, int& zb,
+                                          int grp = 0) {
   const int L = blockIdx.x;
   zb = (L >> 3) % NSL;
   const int chain = (L / (8 * NSL)) * 8 + (L & 7);
   if (chain >= N * H) return false;
   const int r = chain / H;
   h = chain - r * H;
-  s = sorder ? sorder[r] : r;
+  s = sorder ? sorder[r] : grp > 1 ? (r / (grp - 1)) * grp + r % (grp - 1) : r;
   return true;
 }
 
@@ -1211,7 +1215,11 @@ __global__ __launch_bounds__(NTHR) void k_prep_bf(
 // lane needs the gates and beta of one row only, and the intermediate tiles
 // (state, R, D, Dg) sit row-major in LDS, read as operands with transposing
 // reads.
-template <int DK, int DV, int BV, bool OUT, bool STORE>
+// PHI: the homogeneous recurrence from the identity (no value term, X_0 = I,
+// DV = DK columns): the final state is the product of the chunks' transitions
+// X -> e^{G_63} X - K~^T M Diag(s) K X over the sequence (the segment
+// transition of the segmented scan, run_fwd_bf).
+template <int DK, int DV, int BV, bool OUT, bool STORE, bool PHI = false>
 __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
     const bf16_t* __restrict__ beta, const bf16_t* __restrict__ beta_tilde,
@@ -1221,7 +1229,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     const float* __restrict__ Ms, const int16_t* __restrict__ Aq, const float* __restrict__ As,
     const float* __restrict__ Gw, float* __restrict__ o, float* __restrict__ ht, int16_t* __restrict__ Xq,
     float* __restrict__ Xs, int16_t* __restrict__ Dq, float* __restrict__ Ds,
-    int16_t* __restrict__ Xfq, float* __restrict__ Xfs) {
+    int16_t* __restrict__ Xfq, float* __restrict__ Xfs, int grp = 0) {
   // Every global load and store inside the chunk loop is issued unconditionally
   // (clamped rows and chunk indices, masked values applied at use, padded-row
   // stores dropped by the record count of a raw buffer), so the memory-counter
@@ -1232,6 +1240,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
   // read on disjoint banks
   constexpr int LDT = BV + 4;
   static_assert(BV == 32, "stored states use one scale per 32-column block = one dv slice");
+  static_assert(!PHI || (DV == DK && !OUT && !STORE), "the transition product is a dk x dk state");
   __shared__ __align__(16) bf16_t Xh[DK * LDT];
   __shared__ __align__(16) bf16_t Xl[DK * LDT];
   __shared__ __align__(16) bf16_t Rh[CH * LDT];
@@ -1247,7 +1256,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
   __shared__ __align__(16) bf16_t Kc[CH * LDKC];
 
   int s, h, zb;
-  if (!scan_item<DV / BV>(N, H, sorder, s, h, zb)) return;
+  if (!scan_item<DV / BV>(N, H, sorder, s, h, zb, grp)) return;
   const int j0 = zb * BV;
   const SeqInfo si = seq_at(smap, s, Tfix);
   const int w = wave_id(), lane = lane_id(), r16 = lane & 15, g4 = lane >> 4;
@@ -1265,7 +1274,11 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
   for (int mt = 0; mt < XMT; ++mt)
 #pragma unroll
     for (int nt = 0; nt < NTV; ++nt) {
-      if (h0) {
+      if constexpr (PHI) {
+        const int r = xrow0 + 16 * mt, c = j0 + 16 * nt + col0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) X[mt][nt][e] = r == c + e ? 1.f : 0.f;
+      } else if (h0) {
         const float4 x4 = *reinterpret_cast<const float4*>(h0 + soff + (long)(xrow0 + 16 * mt) * DV + j0 + 16 * nt + col0);
         X[mt][nt] = floatx4{x4.x, x4.y, x4.z, x4.w};
       } else {
@@ -1344,13 +1357,15 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     pgv = at(Gw + chh * CH, 4u * t);
     pbv = at(beta + tok, tr);
     pbtv = at(beta_tilde + tok, tr);
-    pvv = at(reinterpret_cast<const uint4*>(v + tok * DV + j0),
-             2u * ((unsigned)min(vr_ld, plen - 1) * (H * DV) + vc));
+    if constexpr (!PHI)
+      pvv = at(reinterpret_cast<const uint4*>(v + tok * DV + j0),
+               2u * ((unsigned)min(vr_ld, plen - 1) * (H * DV) + vc));
   };
   auto put_rows = [&](int buf) {
     const int t = threadIdx.x & (CH - 1);
     Grow[buf][t] = pgv;
-    Brow[buf][t] = t < plen ? bf2f(pbv) : 0.f;
+    // no value term in the transition product
+    Brow[buf][t] = !PHI && t < plen ? bf2f(pbv) : 0.f;
     BTrow[buf][t] = t < plen ? bf2f(pbtv) : 0.f;
     if (CH * VPR >= NTHR || threadIdx.x < CH * VPR)
       *reinterpret_cast<uint4*>(&Vrow[buf][vr * (BV + 8) + vc]) =
@@ -1568,6 +1583,58 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     }
   }
   if (ht) store_state(ht + soff);
+}
+
+// Boundary states of the segmented forward (run_fwd_bf).  A sequence cut into P
+// segments of equal length is P virtual rows s P + p; the state recurrence is
+// affine in the state entering a segment, so with Phi_p (dk x dk) the product
+// of segment p's chunk transitions and F_p (dk x dv) its final state from a
+// zero start, the true states entering the segments are
+//   X_0 = h0 (or 0),   X_{p+1} = Phi_p X_p + F_p.
+// X_p is written to X0 [row s P + p].  One workgroup per (sequence, head,
+// 32-column slice); the slice of X lives in LDS, thread t forms row t / TPR,
+// columns c0 .. c0 + CPT - 1 of the next one in fp32 (fixed summation order).
+template <int DK, int DV>
+__global__ __launch_bounds__(NTHR) void k_seg_combine(const float* __restrict__ phi,
+                                                      const float* __restrict__ F,
+                                                      const float* __restrict__ h0, int P, int H,
+                                                      float* __restrict__ X0) {
+  constexpr int SL = 32, TPR = NTHR / DK, CPT = SL / TPR;
+  static_assert(NTHR % DK == 0 && SL % TPR == 0, "rows per workgroup");
+  constexpr int NSL = DV / SL;
+  const int zb = blockIdx.x % NSL, sh = blockIdx.x / NSL, h = sh % H, s = sh / H;
+  const int j0 = zb * SL;
+  const int r = threadIdx.x / TPR, c0 = (threadIdx.x % TPR) * CPT;
+  const size_t sdv = (size_t)DK * DV, sdk = (size_t)DK * DK;
+  __shared__ float Xs[DK][SL + 1];
+  for (int i = threadIdx.x; i < DK * SL; i += NTHR) {
+    const int rr = i / SL, cc = i % SL;
+    Xs[rr][cc] = h0 ? h0[((size_t)s * H + h) * sdv + (size_t)rr * DV + j0 + cc] : 0.f;
+  }
+  __syncthreads();
+  for (int p = 0; p < P; ++p) {
+    const size_t row = ((size_t)s * P + p) * H + h;
+    float* x0 = X0 + row * sdv + j0;
+    for (int i = threadIdx.x; i < DK * SL; i += NTHR) {
+      const int rr = i / SL, cc = i % SL;
+      x0[(size_t)rr * DV + cc] = Xs[rr][cc];
+    }
+    if (p + 1 == P) break;
+    const float* ph = phi + row * sdk + (size_t)r * DK;
+    const float* f = F + row * sdv + (size_t)r * DV + j0 + c0;
+    float acc[CPT];
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) acc[j] = f[j];
+    for (int kk = 0; kk < DK; ++kk) {
+      const float a = ph[kk];
+#pragma unroll
+      for (int j = 0; j < CPT; ++j) acc[j] = fmaf(a, Xs[kk][c0 + j], acc[j]);
+    }
+    __syncthreads();  // every row of X_p has been read
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) Xs[r][c0 + j] = acc[j];
+    __syncthreads();
+  }
 }
 
 // Reverse state scan (bf16 inputs): Y = gradient of the state leaving the chunk.
@@ -3079,6 +3146,40 @@ static hipError_t run_fwd_bf(const LaunchArgs& a) {
     else
       k_prep_bf<DK, false><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
           q, k, a.g, bt, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, nullptr, a.Gw);
+  }
+  if (!a.saved && a.segP > 1) {
+    // Segmented forward for few long rows (fewer scan chains than the chip
+    // has CUs): each row is cut into segP segments scanned side by side as
+    // virtual rows of Tseq / segP tokens (chunk and token indices are those of
+    // the real rows).  1. every segment's final state from a zero start and
+    // its transition product (not of a row's last segment, which no later
+    // segment needs); 2. the true state entering each segment
+    // (k_seg_combine); 3. the output scan of every segment from that state.
+    const int P = a.segP, Np = a.N * P, Tp = a.Tseq / P, Nst = a.N * (P - 1);
+    a.stage("scan_seg_state");
+    k_scan_fwd_bf<DK, DV, SCAN_BV, false, false><<<scan_blocks(Nst, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
+        q, k, v, beta, bt, a.d, nullptr, nullptr, nullptr, Nst, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw,
+        nullptr, a.segF, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, P);
+    a.stage("scan_seg_phi");
+    k_scan_fwd_bf<DK, DK, SCAN_BV, false, false, true><<<scan_blocks(Nst, a.H, DK / SCAN_BV), NTHR, 0, st>>>(
+        q, k, v, beta, bt, a.d, nullptr, nullptr, nullptr, Nst, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw,
+        nullptr, a.segPhi, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, P);
+    a.stage("seg_combine");
+    k_seg_combine<DK, DV><<<a.N * a.H * (DV / 32), NTHR, 0, st>>>(a.segPhi, a.segF, a.h0, P, a.H,
+                                                                  a.segX0);
+    a.stage("scan_fwd");
+    k_scan_fwd_bf<DK, DV, SCAN_BV, true, false><<<scan_blocks(Np, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
+        q, k, v, beta, bt, a.d, a.segX0, nullptr, nullptr, Np, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw,
+        a.o, a.ht ? a.segHT : nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
+    // the final state of each row is that of its last segment
+    if (a.ht) {
+      const size_t st_bytes = (size_t)a.H * DK * DV * sizeof(float);
+      if (hipMemcpy2DAsync(a.ht, st_bytes, a.segHT + (size_t)(P - 1) * a.H * DK * DV, P * st_bytes,
+                           st_bytes, a.N, hipMemcpyDeviceToDevice, st) != hipSuccess)
+        return hipErrorLaunchFailure;
+    }
+    a.stage(nullptr);
+    return hipGetLastError();
   }
   a.stage(a.saved ? "scan_fwd_save" : "scan_fwd");
   if (a.saved)

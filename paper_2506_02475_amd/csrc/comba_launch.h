@@ -5,6 +5,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "comba.h"
+
 namespace comba {
 
 // One chunk of at most 64 tokens of one sequence (len == 0: unused slot).
@@ -58,6 +60,13 @@ struct LaunchArgs {
   float *Xs, *Ds, *Ys, *dRs;
   int16_t* Xfq;  // bf16 path: sink for the state after the last chunk (same layout)
   float* Xfs;    //   and its scales
+  // segmented stateless forward (bf16, fixed-length rows; segP > 1 enables it):
+  // each row is scanned as segP virtual rows; per virtual row and head the
+  // final state from a zero start (segF, dk x dv), the transition product
+  // (segPhi, dk x dk), the true state entering it (segX0) and its final
+  // state (segHT)
+  int segP;
+  float *segF, *segPhi, *segX0, *segHT;
   hipStream_t stream;
   StageHook hook;
   void stage(const char* name) const {
@@ -67,6 +76,8 @@ struct LaunchArgs {
 
 hipError_t launch_fwd(const LaunchArgs& a);
 hipError_t launch_bwd(const LaunchArgs& a);
+// The stateless forward's workspace without the segmented scan's buffers.
+size_t fwd_workspace_bytes_plain(const comba_shape* shape);
 
 // Token-by-token recurrence (comba_recurrent_fwd): no workspace.
 struct RecurrentArgs {

@@ -17,6 +17,7 @@
 #include <mutex>
 
 #include "comba.h"
+#include "comba_launch.h"
 
 namespace {
 
@@ -52,7 +53,9 @@ comba_status comba_chunk_fwd_noalloc(const comba_shape* shape, const void* q, co
                                      const void* beta_tilde, const float* d, const float* h0,
                                      float* o, float* ht, void* stream) {
   if (!shape) return COMBA_ERR_NULL;
-  const size_t need = comba_fwd_workspace_bytes(shape);
+  // the plain scan's workspace must fit; the segmented scan runs only when its
+  // buffers fit too (comba_chunk_fwd falls back to the plain scan otherwise)
+  const size_t need = comba::fwd_workspace_bytes_plain(shape);
   if (need == 0) return COMBA_ERR_SHAPE;  // the shape itself is invalid
   if (need > kScratchBytes) return COMBA_ERR_SCRATCH;
   void* ws = device_scratch();
