@@ -601,6 +601,62 @@ def time_long1(comba, torch, steps, warmup):
             "roofline": roof}
 
 
+def time_long1_train(comba, torch, steps, warmup):
+    """Training pair (comba_chunk_fwd_save + comba_chunk_bwd_saved) on one long
+    sequence: B1 T65536 H16 d128 bf16 (the 1.3B layer's heads, its input
+    distributions), with the segmented scans (both scans of the pair cut into
+    segments; 64 chains otherwise) and, timed beside it, with
+    COMBA_SCAN_SEGMENTS=1."""
+    import numpy as np
+    from comba_inputs import random_case
+
+    B, T, H, dk, dv = 1, 65536, 16, 128, 128
+    w = random_case(seed=83, B=B, T=T, H=H, dk=dk, dv=dv, in_dtype="bf16", grad=True)
+    dev = torch.device("cuda:0")
+    bf = torch.bfloat16
+
+    def t(x, dt=torch.float32):
+        return torch.from_numpy(np.ascontiguousarray(x)).to(dev, dt)
+
+    q, k, v, g, beta, d, h0, dO = (t(w.q, bf), t(w.k, bf), t(w.v, bf), t(w.g), t(w.beta, bf),
+                                   t(w.d), t(w.h0), t(w.dO, bf))
+    del w
+    old = os.environ.get("COMBA_SCAN_SEGMENTS")
+    out = {}
+    try:
+        for mode, env in (("segmented", None), ("plain", "1")):
+            if env is None:
+                os.environ.pop("COMBA_SCAN_SEGMENTS", None)
+            else:
+                os.environ["COMBA_SCAN_SEGMENTS"] = env
+            ws = torch.empty(comba.bwd_workspace_bytes(B, T, H, dk, dv), dtype=torch.uint8,
+                             device=dev)
+
+            def step():
+                comba.comba_chunk_fwd_save(q, k, v, g, beta, d, h0, workspace=ws)
+                return comba.comba_chunk_bwd_saved(q, k, v, g, beta, d, h0, dO, None,
+                                                   workspace=ws)
+
+            for _ in range(warmup):
+                step()
+            out[mode] = timed_steps(comba, torch, step, steps)
+            del ws
+    finally:
+        if old is None:
+            os.environ.pop("COMBA_SCAN_SEGMENTS", None)
+        else:
+            os.environ["COMBA_SCAN_SEGMENTS"] = old
+    tm = out["segmented"]
+    ms = tm["ms_per_step"]
+    return {"value": round(B * T / (ms * 1e-3), 1), "unit": "tokens/s", "ms_per_step": round(ms, 4),
+            "config": {"B": B, "T": T, "H": H, "dk": dk, "dv": dv},
+            "step": "comba_chunk_fwd_save + comba_chunk_bwd_saved",
+            "stages_ms": {n: round(x, 4) for n, x in tm["stages_ms"].items()},
+            "plain_ms_per_step": round(out["plain"]["ms_per_step"], 4),
+            "plain_stages_ms": {n: round(x, 4) for n, x in out["plain"]["stages_ms"].items()},
+            "speedup_vs_plain": round(out["plain"]["ms_per_step"] / ms, 3)}
+
+
 PROLOGUE = dict(B=4, T=4096, H=16, dk=128, dv=128, seed=71)
 PROLOGUE_SOURCES = ("comba_prologue.hip", "comba_device.hpp")
 PROLOGUE_TRAFFIC = "traffic_counters_prologue_b4_t4096_h16_d128.md"
@@ -795,6 +851,7 @@ def main():
     if args.long1:
         torch.cuda.set_device(0)
         r = time_long1(comba, torch, args.steps, args.warmup)
+        r["train"] = time_long1_train(comba, torch, args.steps, args.warmup)
         result = {
             "metric": "Comba forward tokens/s on one long sequence (525,824 tokens, H=16, d=128 "
                       "bf16; segmented scan)",
@@ -805,7 +862,7 @@ def main():
             "config": {"workload": "long1_525k_fwd", **r["config"]}, "step": "comba_chunk_fwd",
             "stages_ms": r["stages_ms"], "plain_ms_per_step": r["plain_ms_per_step"],
             "speedup_vs_plain": r["speedup_vs_plain"], "roofline": r["roofline"],
-            "step_roofline": r["step_roofline"], "cpu_baseline": None}
+            "step_roofline": r["step_roofline"], "train_65k": r["train"], "cpu_baseline": None}
         if args.copy_bytes > 0:
             result["copy_bytes"] = calibration_copy(torch, args.copy_bytes)
         print(json.dumps(result), flush=True)
@@ -1017,6 +1074,8 @@ def main():
         result["variants"]["varlen_512k_fwd"] = time_varlen(comba, torch, args.steps,
                                                            args.warmup)
         result["variants"]["long1_525k_fwd"] = time_long1(comba, torch, args.steps, args.warmup)
+        result["variants"]["long1_train_65k"] = time_long1_train(comba, torch, args.steps,
+                                                                 args.warmup)
         result["variants"]["train_b4_t4096_h8_d256"] = time_train256(comba, torch, args.steps,
                                                                      args.warmup)
     if args.copy_bytes > 0:

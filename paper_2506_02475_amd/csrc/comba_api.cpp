@@ -124,7 +124,7 @@ int seg_parts(const Dims& d) {
 
 struct Layout {
   size_t cmap, smap, sord, M, A, G, X, D, Y, dR, ddp, QT, Xfin, total;
-  size_t segF, segPhi, segX0, segHT;  // segmented stateless forward (segP > 1)
+  size_t segF, segPhi, segX0, segHT, segG, segY0, segDH0;  // segmented scans (segP > 1)
   size_t Xs, Ds, Ys, dRs, Xfs;  // bf16 path: scales of the int16 X, D, Y, dR, final-state sink
   size_t Ms, As;                // bf16 path: row scales of M, column scales of A
 };
@@ -177,13 +177,20 @@ Layout layout(const Dims& d, bool bwd, int segP = 1) {
     L.dR = take(chh * kChunk * d.dv * sizeof(float));
     L.ddp = take(chh * sizeof(float));
   }
-  if (!bwd && segP > 1) {
-    // per virtual row (segment) and head: F, X0, HT (dk x dv), Phi (dk x dk), fp32
+  if (segP > 1) {
+    // per virtual row (segment) and head, fp32: F, X0, HT (dk x dv), Phi (dk x
+    // dk); the backward-sized workspace (training pair, stateless backward)
+    // also G, Y0, DH0 (dk x dv)
     const size_t nvr = (size_t)d.N * segP * d.H;
     L.segF = take(nvr * d.dk * d.dv * sizeof(float));
     L.segPhi = take(nvr * d.dk * d.dk * sizeof(float));
     L.segX0 = take(nvr * d.dk * d.dv * sizeof(float));
     L.segHT = take(nvr * d.dk * d.dv * sizeof(float));
+    if (bwd) {
+      L.segG = take(nvr * d.dk * d.dv * sizeof(float));
+      L.segY0 = take(nvr * d.dk * d.dv * sizeof(float));
+      L.segDH0 = take(nvr * d.dk * d.dv * sizeof(float));
+    }
   }
   L.total = off;
   return L;
@@ -235,8 +242,20 @@ void attach_profile(Args& a) {
   a.hook.ctx = &g_prof;
 }
 
-void carve(comba::LaunchArgs& a, const Layout& L, void* ws, bool bwd) {
+void carve(comba::LaunchArgs& a, const Layout& L, void* ws, bool bwd, int segP = 1) {
   char* base = static_cast<char*>(ws);
+  a.segP = segP;
+  if (segP > 1) {
+    a.segF = reinterpret_cast<float*>(base + L.segF);
+    a.segPhi = reinterpret_cast<float*>(base + L.segPhi);
+    a.segX0 = reinterpret_cast<float*>(base + L.segX0);
+    a.segHT = reinterpret_cast<float*>(base + L.segHT);
+    if (bwd) {
+      a.segG = reinterpret_cast<float*>(base + L.segG);
+      a.segY0 = reinterpret_cast<float*>(base + L.segY0);
+      a.segDH0 = reinterpret_cast<float*>(base + L.segDH0);
+    }
+  }
   a.cmap = reinterpret_cast<comba::ChunkInfo*>(base + L.cmap);
   a.smap = reinterpret_cast<comba::SeqInfo*>(base + L.smap);
   a.sorder = reinterpret_cast<int*>(base + L.sord);
@@ -299,8 +318,8 @@ comba_status chunk_fwd(bool save, const comba_shape* shape, const void* q, const
       !aligned(beta_tilde, dm.bf16 ? 2 : 4))
     return COMBA_ERR_ALIGN;
   // the segmented scan when the workspace holds its buffers (sized by
-  // comba_fwd_workspace_bytes), else the plain one
-  int segP = save ? 1 : seg_parts(dm);
+  // comba_fwd_workspace_bytes / comba_bwd_workspace_bytes), else the plain one
+  int segP = seg_parts(dm);
   Layout L = layout(dm, save, segP);
   if (ws_bytes < L.total && segP > 1) {
     segP = 1;
@@ -321,15 +340,7 @@ comba_status chunk_fwd(bool save, const comba_shape* shape, const void* q, const
   a.o = o;
   a.ht = ht;
   a.stream = static_cast<hipStream_t>(stream);
-  carve(a, L, ws, save);
-  a.segP = segP;
-  if (segP > 1) {
-    char* base = static_cast<char*>(ws);
-    a.segF = reinterpret_cast<float*>(base + L.segF);
-    a.segPhi = reinterpret_cast<float*>(base + L.segPhi);
-    a.segX0 = reinterpret_cast<float*>(base + L.segX0);
-    a.segHT = reinterpret_cast<float*>(base + L.segHT);
-  }
+  carve(a, L, ws, save, segP);
   attach_profile(a);
   if (dm.N == 0) return COMBA_OK;
   return comba::launch_fwd(a) == hipSuccess ? COMBA_OK : COMBA_ERR_HIP;
@@ -358,7 +369,14 @@ comba_status chunk_bwd(bool saved, const comba_shape* shape, const void* q, cons
       (dh0 && !aligned(dh0, 16)) || !aligned(beta, dm.bf16 ? 2 : 4) ||
       !aligned(beta_tilde, dm.bf16 ? 2 : 4) || !aligned(dbeta_tilde, 4))
     return COMBA_ERR_ALIGN;
-  const Layout L = layout(dm, true);
+  // segmented as the forward of the pair was (the same shape, device and
+  // COMBA_SCAN_SEGMENTS give the same choice and the same workspace layout)
+  int segP = seg_parts(dm);
+  Layout L = layout(dm, true, segP);
+  if (ws_bytes < L.total && segP > 1) {
+    segP = 1;
+    L = layout(dm, true, 1);
+  }
   if (ws_bytes < L.total) return COMBA_ERR_WORKSPACE;
   comba::LaunchArgs a{};
   fill_common(a, dm, shape);
@@ -382,7 +400,7 @@ comba_status chunk_bwd(bool saved, const comba_shape* shape, const void* q, cons
   a.dd = dd;
   a.dh0 = dh0;
   a.stream = static_cast<hipStream_t>(stream);
-  carve(a, L, ws, true);
+  carve(a, L, ws, true, segP);
   attach_profile(a);
   return comba::launch_bwd(a) == hipSuccess ? COMBA_OK : COMBA_ERR_HIP;
 }
@@ -570,7 +588,7 @@ size_t comba_fwd_workspace_bytes(const comba_shape* shape) {
 size_t comba_bwd_workspace_bytes(const comba_shape* shape) {
   Dims d;
   if (check_shape(shape, &d, true) != COMBA_OK) return 0;
-  return layout(d, true).total;
+  return layout(d, true, seg_parts(d)).total;
 }
 
 comba_status comba_profile_enable(int enable) {

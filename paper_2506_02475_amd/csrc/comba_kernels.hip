@@ -956,19 +956,20 @@ __device__ __forceinline__ int frag_off(int row, int col) {
 // K, Q, M, A rows they all read are L2 hits for all but the first.  Chains are
 // taken rank-major (r = chain / H), with packed sequences in the order of
 // sorder (longest first); padding workgroups past the last chain return.
-// grp > 1 (the segmented forward's state passes): the rows are groups of grp
-// segments whose last one is skipped, so rank r is row (r / (grp - 1)) grp +
-// r % (grp - 1) and N counts the rows taken.
+// grp > 1 (the segmented scans' state passes): the rows are groups of grp
+// segments of which one is skipped (the last, goff = 0, or the first, goff =
+// 1), so rank r is row (r / (grp - 1)) grp + goff + r % (grp - 1) and N counts
+// the rows taken.
 template <int NSL>
 __device__ __forceinline__ bool scan_item(int N, int H, const int* sorder, int& s, int& h, int& zb,
-                                          int grp = 0) {
+                                          int grp = 0, int goff = 0) {
   const int L = blockIdx.x;
   zb = (L >> 3) % NSL;
   const int chain = (L / (8 * NSL)) * 8 + (L & 7);
   if (chain >= N * H) return false;
   const int r = chain / H;
   h = chain - r * H;
-  s = sorder ? sorder[r] : grp > 1 ? (r / (grp - 1)) * grp + r % (grp - 1) : r;
+  s = sorder ? sorder[r] : grp > 1 ? (r / (grp - 1)) * grp + goff + r % (grp - 1) : r;
   return true;
 }
 
@@ -1575,9 +1576,10 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
     put_rows(buf ^ 1);
     __syncthreads();
   }
-  // the state after the last chunk (the backward's sink for it)
+  // the state after the last chunk (the backward's sink for it; none in the
+  // segmented scan)
   if constexpr (STORE) {
-    if (n > 0) {
+    if (n > 0 && Xfq) {
       const long xb = (((long)s * H + h) * NB + zb) * DK;
       store_state_q(Xfq + xb * BV, Xfs + xb);
     }
@@ -1592,14 +1594,16 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_fwd_bf(
 // zero start, the true states entering the segments are
 //   X_0 = h0 (or 0),   X_{p+1} = Phi_p X_p + F_p.
 // X_p is written to X0 [row s P + p].  One workgroup per (sequence, head,
-// 32-column slice); the slice of X lives in LDS, thread t forms row t / TPR,
-// columns c0 .. c0 + CPT - 1 of the next one in fp32 (fixed summation order).
+// SEG_SL-column slice: many small workgroups, since few rows are cut); the
+// slice of X lives in LDS, thread t forms row t / TPR, columns c0 .. c0 + CPT
+// - 1 of the next one in fp32 (fixed summation order).
+constexpr int SEG_SL = 8;
 template <int DK, int DV>
 __global__ __launch_bounds__(NTHR) void k_seg_combine(const float* __restrict__ phi,
                                                       const float* __restrict__ F,
                                                       const float* __restrict__ h0, int P, int H,
                                                       float* __restrict__ X0) {
-  constexpr int SL = 32, TPR = NTHR / DK, CPT = SL / TPR;
+  constexpr int SL = SEG_SL, TPR = NTHR / DK, CPT = SL / TPR;
   static_assert(NTHR % DK == 0 && SL % TPR == 0, "rows per workgroup");
   constexpr int NSL = DV / SL;
   const int zb = blockIdx.x % NSL, sh = blockIdx.x / NSL, h = sh % H, s = sh / H;
@@ -1620,7 +1624,7 @@ __global__ __launch_bounds__(NTHR) void k_seg_combine(const float* __restrict__ 
       x0[(size_t)rr * DV + cc] = Xs[rr][cc];
     }
     if (p + 1 == P) break;
-    const float* ph = phi + row * sdk + (size_t)r * DK;
+    const float* ph = phi + row * sdk + (size_t)r * DK;  // row r of Phi_p
     const float* f = F + row * sdv + (size_t)r * DV + j0 + c0;
     float acc[CPT];
 #pragma unroll
@@ -1637,12 +1641,65 @@ __global__ __launch_bounds__(NTHR) void k_seg_combine(const float* __restrict__ 
   }
 }
 
+// Boundary gradients of the segmented backward.  Y at the end of a row's last
+// segment is dht (or 0); the reverse recurrence is affine in it, with the
+// transposed transition product Phi_p^T of segment p, so with G_p (dk x dv)
+// segment p's state gradient at its start from a zero end (virtual row s P + p
+// of both), the gradient of the state leaving segment p - 1 is
+//   Y_{p-1} = Phi_p^T Y_p + G_p,   p = P-1 .. 1.
+// Y_p goes to Y0 [row s P + p] (the reverse scan's end state of segment p).
+// Workgroups as in k_seg_combine.
+template <int DK, int DV>
+__global__ __launch_bounds__(NTHR) void k_seg_combine_bwd(const float* __restrict__ phi,
+                                                          const float* __restrict__ G,
+                                                          const float* __restrict__ dht, int P,
+                                                          int H, float* __restrict__ Y0) {
+  constexpr int SL = SEG_SL, TPR = NTHR / DK, CPT = SL / TPR;
+  static_assert(NTHR % DK == 0 && SL % TPR == 0, "rows per workgroup");
+  constexpr int NSL = DV / SL;
+  const int zb = blockIdx.x % NSL, sh = blockIdx.x / NSL, h = sh % H, s = sh / H;
+  const int j0 = zb * SL;
+  const int r = threadIdx.x / TPR, c0 = (threadIdx.x % TPR) * CPT;
+  const size_t sdv = (size_t)DK * DV, sdk = (size_t)DK * DK;
+  __shared__ float Ys[DK][SL + 1];
+  for (int i = threadIdx.x; i < DK * SL; i += NTHR) {
+    const int rr = i / SL, cc = i % SL;
+    Ys[rr][cc] = dht ? dht[((size_t)s * H + h) * sdv + (size_t)rr * DV + j0 + cc] : 0.f;
+  }
+  __syncthreads();
+  for (int p = P - 1; p >= 0; --p) {
+    const size_t row = ((size_t)s * P + p) * H + h;
+    float* y0 = Y0 + row * sdv + j0;
+    for (int i = threadIdx.x; i < DK * SL; i += NTHR) {
+      const int rr = i / SL, cc = i % SL;
+      y0[(size_t)rr * DV + cc] = Ys[rr][cc];
+    }
+    if (p == 0) break;
+    const float* ph = phi + row * sdk + r;  // column r of Phi_p
+    const float* gp = G + row * sdv + (size_t)r * DV + j0 + c0;
+    float acc[CPT];
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) acc[j] = gp[j];
+    for (int kk = 0; kk < DK; ++kk) {
+      const float a = ph[(size_t)kk * DK];
+#pragma unroll
+      for (int j = 0; j < CPT; ++j) acc[j] = fmaf(a, Ys[kk][c0 + j], acc[j]);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) Ys[r][c0 + j] = acc[j];
+    __syncthreads();
+  }
+}
+
 // Reverse state scan (bf16 inputs): Y = gradient of the state leaving the chunk.
 // As in the forward scan, every product is formed transposed, so that a lane
 // holds one row and four consecutive columns; the intermediate tiles (Y, dO,
 // dD, Pg, W2) sit row-major in LDS and are read as operands with transposing
 // reads.
-template <int DK, int DV, int BV>
+// STORE = false: the recurrence alone (no Y, dR stores), for the segmented
+// backward's state pass.
+template <int DK, int DV, int BV, bool STORE = true>
 __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ dO,
     const bf16_t* __restrict__ beta_tilde, const float* __restrict__ d, const float* __restrict__ dht,
@@ -1651,7 +1708,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
     const float* __restrict__ Ms, const int16_t* __restrict__ Aq, const float* __restrict__ As,
     const bf16_t* __restrict__ QTp,
     const float* __restrict__ Gw, float* __restrict__ dh0, int16_t* __restrict__ Yq,
-    float* __restrict__ Ys, int16_t* __restrict__ dRq, float* __restrict__ dRs) {
+    float* __restrict__ Ys, int16_t* __restrict__ dRq, float* __restrict__ dRs, int grp = 0,
+    int goff = 0) {
   // as in the forward scan, all loop memory operations are unconditional
   constexpr int NTV = BV / 16, XMT = DK / 64, KS = DK / 32, CC = CH * CH;
   constexpr int NB = DV / 32;
@@ -1668,7 +1726,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
   __shared__ __align__(16) bf16_t W2l[CH * LDT];
 
   int s, h, zb;
-  if (!scan_item<DV / BV>(N, H, sorder, s, h, zb)) return;
+  if (!scan_item<DV / BV>(N, H, sorder, s, h, zb, grp, goff)) return;
   const int j0 = zb * BV;
   const SeqInfo si = seq_at(smap, s, Tfix);
   const int w = wave_id(), lane = lane_id(), r16 = lane & 15, g4 = lane >> 4;
@@ -1880,7 +1938,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
       }
     // the state gradient of this chunk, stored while the products run (stores
     // bunched before a barrier stall all four waves at once)
-    store_state_q(Yq + (chh * NB + zb) * DK * BV, Ys + (chh * NB + zb) * DK);
+    if constexpr (STORE) store_state_q(Yq + (chh * NB + zb) * DK * BV, Ys + (chh * NB + zb) * DK);
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
       bf16x8 ath, atl;
@@ -1992,7 +2050,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_scan_bwd_bf(
         }
       }
     }
-    {
+    if constexpr (STORE) {
       const long blk = (chh * NB + zb) * CH;  // the slice's block
       at(reinterpret_cast<uint4*>(dRq + blk * BV), 2u * (prow * BV + row8_col())) = rpk;
       if (g4 == 0) at(dRs + blk, 4u * prow) = rsc;
@@ -3123,6 +3181,40 @@ static hipError_t run_bwd(const LaunchArgs& a) {
   return hipGetLastError();
 }
 
+// The segmented scans' state passes and boundary states (see run_fwd_bf):
+// each segment's final state from a zero start (not of a row's last segment),
+// its transition product (of every segment when a backward follows, which
+// needs those of all but the first; else not of the last) and the true state
+// entering every segment.
+template <int DK, int DV>
+static void seg_forward_states(const LaunchArgs& a, const bf16_t* q, const bf16_t* k,
+                               const bf16_t* v, const bf16_t* beta, const bf16_t* bt,
+                               bool phi_all) {
+  hipStream_t st = a.stream;
+  const int P = a.segP, Tp = a.Tseq / P, Nst = a.N * (P - 1);
+  const int Nphi = phi_all ? a.N * P : Nst, gphi = phi_all ? 0 : P;
+  a.stage("scan_seg_state");
+  k_scan_fwd_bf<DK, DV, SCAN_BV, false, false><<<scan_blocks(Nst, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
+      q, k, v, beta, bt, a.d, nullptr, nullptr, nullptr, Nst, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw,
+      nullptr, a.segF, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, P);
+  a.stage("scan_seg_phi");
+  k_scan_fwd_bf<DK, DK, SCAN_BV, false, false, true><<<scan_blocks(Nphi, a.H, DK / SCAN_BV), NTHR, 0, st>>>(
+      q, k, v, beta, bt, a.d, nullptr, nullptr, nullptr, Nphi, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw,
+      nullptr, a.segPhi, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, gphi);
+  a.stage("seg_combine");
+  k_seg_combine<DK, DV><<<a.N * a.H * (DV / SEG_SL), NTHR, 0, st>>>(a.segPhi, a.segF, a.h0, P, a.H,
+                                                                a.segX0);
+}
+
+// Row r's state from virtual row r P + p (p = 0: the first segment's, P - 1:
+// the last's) into dst [N, H, dk, dv].
+template <int DK, int DV>
+static hipError_t seg_copy_rows(const LaunchArgs& a, float* dst, const float* src, int p) {
+  const size_t st_bytes = (size_t)a.H * DK * DV * sizeof(float);
+  return hipMemcpy2DAsync(dst, st_bytes, src + (size_t)p * a.H * DK * DV, a.segP * st_bytes,
+                          st_bytes, a.N, hipMemcpyDeviceToDevice, a.stream);
+}
+
 template <int DK, int DV>
 static hipError_t run_fwd_bf(const LaunchArgs& a) {
   hipStream_t st = a.stream;
@@ -3147,37 +3239,30 @@ static hipError_t run_fwd_bf(const LaunchArgs& a) {
       k_prep_bf<DK, false><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
           q, k, a.g, bt, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, nullptr, a.Gw);
   }
-  if (!a.saved && a.segP > 1) {
+  if (a.segP > 1) {
     // Segmented forward for few long rows (fewer scan chains than the chip
     // has CUs): each row is cut into segP segments scanned side by side as
     // virtual rows of Tseq / segP tokens (chunk and token indices are those of
     // the real rows).  1. every segment's final state from a zero start and
     // its transition product (not of a row's last segment, which no later
     // segment needs); 2. the true state entering each segment
-    // (k_seg_combine); 3. the output scan of every segment from that state.
-    const int P = a.segP, Np = a.N * P, Tp = a.Tseq / P, Nst = a.N * (P - 1);
-    a.stage("scan_seg_state");
-    k_scan_fwd_bf<DK, DV, SCAN_BV, false, false><<<scan_blocks(Nst, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-        q, k, v, beta, bt, a.d, nullptr, nullptr, nullptr, Nst, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw,
-        nullptr, a.segF, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, P);
-    a.stage("scan_seg_phi");
-    k_scan_fwd_bf<DK, DK, SCAN_BV, false, false, true><<<scan_blocks(Nst, a.H, DK / SCAN_BV), NTHR, 0, st>>>(
-        q, k, v, beta, bt, a.d, nullptr, nullptr, nullptr, Nst, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw,
-        nullptr, a.segPhi, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, P);
-    a.stage("seg_combine");
-    k_seg_combine<DK, DV><<<a.N * a.H * (DV / 32), NTHR, 0, st>>>(a.segPhi, a.segF, a.h0, P, a.H,
-                                                                  a.segX0);
-    a.stage("scan_fwd");
-    k_scan_fwd_bf<DK, DV, SCAN_BV, true, false><<<scan_blocks(Np, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-        q, k, v, beta, bt, a.d, a.segX0, nullptr, nullptr, Np, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw,
-        a.o, a.ht ? a.segHT : nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
+    // (k_seg_combine); 3. the output scan of every segment from that state
+    // (with the chunk states for the backward in the training pair).
+    const int Np = a.N * a.segP, Tp = a.Tseq / a.segP;
+    seg_forward_states<DK, DV>(a, q, k, v, beta, bt, a.saved);
+    a.stage(a.saved ? "scan_fwd_save" : "scan_fwd");
+    float* htv = a.ht ? a.segHT : nullptr;
+    if (a.saved)
+      k_scan_fwd_bf<DK, DV, SCAN_BV, true, true><<<scan_blocks(Np, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
+          q, k, v, beta, bt, a.d, a.segX0, nullptr, nullptr, Np, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As,
+          a.Gw, a.o, htv, a.Xq, a.Xs, a.Dq, a.Ds, nullptr, nullptr);
+    else
+      k_scan_fwd_bf<DK, DV, SCAN_BV, true, false><<<scan_blocks(Np, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
+          q, k, v, beta, bt, a.d, a.segX0, nullptr, nullptr, Np, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As,
+          a.Gw, a.o, htv, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
     // the final state of each row is that of its last segment
-    if (a.ht) {
-      const size_t st_bytes = (size_t)a.H * DK * DV * sizeof(float);
-      if (hipMemcpy2DAsync(a.ht, st_bytes, a.segHT + (size_t)(P - 1) * a.H * DK * DV, P * st_bytes,
-                           st_bytes, a.N, hipMemcpyDeviceToDevice, st) != hipSuccess)
-        return hipErrorLaunchFailure;
-    }
+    if (a.ht && seg_copy_rows<DK, DV>(a, a.ht, a.segHT, a.segP - 1) != hipSuccess)
+      return hipErrorLaunchFailure;
     a.stage(nullptr);
     return hipGetLastError();
   }
@@ -3210,7 +3295,40 @@ static hipError_t run_bwd_bf(const LaunchArgs& a) {
   // fixed-length rows need no tables (closed form in the kernels)
   const int Tfix = a.cu_seqlens ? -1 : a.Tseq;
   const int* sord = Tfix < 0 ? a.sorder : nullptr;
-  if (!a.saved) {
+  if (a.segP > 1) {
+    // Segmented backward (see run_fwd_bf): the forward's states as there
+    // (the training pair's forward left them in the workspace, with the
+    // transition products); then 1. every segment's state gradient at its
+    // start from a zero end (not of a row's first segment); 2. the gradient of
+    // the state leaving every segment (k_seg_combine_bwd, with Phi_p^T); 3. the
+    // reverse scan of every segment from it, storing Y and dR for the
+    // gradient kernel; dh0 is the first segment's.
+    const int P = a.segP, Np = a.N * P, Tp = a.Tseq / P, Nst = a.N * (P - 1);
+    if (!a.saved) {
+      a.stage("prep");
+      if (a.ncmax > 0)
+        k_prep_bf<DK, true><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
+            q, k, a.g, bt, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.QTp, a.Gw);
+      seg_forward_states<DK, DV>(a, q, k, v, beta, bt, true);
+      a.stage("scan_fwd_store");
+      k_scan_fwd_bf<DK, DV, SCAN_BV, false, true><<<scan_blocks(Np, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
+          q, k, v, beta, bt, a.d, a.segX0, nullptr, nullptr, Np, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As,
+          a.Gw, nullptr, nullptr, a.Xq, a.Xs, a.Dq, a.Ds, nullptr, nullptr);
+    }
+    a.stage("scan_seg_grad");
+    k_scan_bwd_bf<DK, DV, SCAN_BV, false><<<scan_blocks(Nst, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
+        q, k, dO, bt, a.d, nullptr, nullptr, nullptr, Nst, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As, a.QTp,
+        a.Gw, a.segG, nullptr, nullptr, nullptr, nullptr, P, 1);
+    a.stage("seg_combine_bwd");
+    k_seg_combine_bwd<DK, DV><<<a.N * a.H * (DV / SEG_SL), NTHR, 0, st>>>(a.segPhi, a.segG, a.dht, P,
+                                                                      a.H, a.segY0);
+    a.stage("scan_bwd");
+    k_scan_bwd_bf<DK, DV, SCAN_BV><<<scan_blocks(Np, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
+        q, k, dO, bt, a.d, a.segY0, nullptr, nullptr, Np, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As, a.QTp,
+        a.Gw, a.dh0 ? a.segDH0 : nullptr, a.Yq, a.Ys, a.dRq, a.dRs);
+    if (a.dh0 && seg_copy_rows<DK, DV>(a, a.dh0, a.segDH0, 0) != hipSuccess)
+      return hipErrorLaunchFailure;
+  } else if (!a.saved) {
     if (Tfix < 0) {
       a.stage("chunk_map");
       launch_chunk_map(a, st);
@@ -3224,10 +3342,12 @@ static hipError_t run_bwd_bf(const LaunchArgs& a) {
         q, k, v, beta, bt, a.d, a.h0, a.smap, sord, a.N, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, nullptr, nullptr, a.Xq,
         a.Xs, a.Dq, a.Ds, a.Xfq, a.Xfs);
   }
-  a.stage("scan_bwd");
-  k_scan_bwd_bf<DK, DV, SCAN_BV><<<scan_blocks(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-      q, k, dO, bt, a.d, a.dht, a.smap, sord, a.N, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.QTp, a.Gw, a.dh0, a.Yq,
-      a.Ys, a.dRq, a.dRs);
+  if (a.segP <= 1) {
+    a.stage("scan_bwd");
+    k_scan_bwd_bf<DK, DV, SCAN_BV><<<scan_blocks(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
+        q, k, dO, bt, a.d, a.dht, a.smap, sord, a.N, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.QTp, a.Gw, a.dh0, a.Yq,
+        a.Ys, a.dRq, a.dRs);
+  }
   a.stage("intra_bwd");
   if constexpr (DK > 128 || DV > 128) {
     // head dim 256: passes of 128 dk columns, one workgroup per chunk-head (at

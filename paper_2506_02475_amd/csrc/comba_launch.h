@@ -60,13 +60,14 @@ struct LaunchArgs {
   float *Xs, *Ds, *Ys, *dRs;
   int16_t* Xfq;  // bf16 path: sink for the state after the last chunk (same layout)
   float* Xfs;    //   and its scales
-  // segmented stateless forward (bf16, fixed-length rows; segP > 1 enables it):
-  // each row is scanned as segP virtual rows; per virtual row and head the
-  // final state from a zero start (segF, dk x dv), the transition product
-  // (segPhi, dk x dk), the true state entering it (segX0) and its final
-  // state (segHT)
+  // segmented scans (bf16, fixed-length rows; segP > 1 enables them): each
+  // row is scanned as segP virtual rows; per virtual row and head the final
+  // state from a zero start (segF, dk x dv), the transition product (segPhi,
+  // dk x dk), the true state entering it (segX0) and its final state (segHT);
+  // backward: the state gradient at its start from a zero end (segG), the
+  // true one at its end (segY0) and at its start (segDH0)
   int segP;
-  float *segF, *segPhi, *segX0, *segHT;
+  float *segF, *segPhi, *segX0, *segHT, *segG, *segY0, *segDH0;
   hipStream_t stream;
   StageHook hook;
   void stage(const char* name) const {

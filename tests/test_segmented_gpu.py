@@ -1,4 +1,4 @@
-"""GPU parity of the segmented forward scan (few long rows).
+"""GPU parity of the segmented scans (few long rows).
 
 When fixed-length rows give the state scan fewer chains than the chip has CUs
 (for example one long sequence), comba_chunk_fwd cuts each row into P
@@ -7,7 +7,11 @@ product are scanned side by side, the true state entering each segment follows
 from the affine dependence on the initial state (X_{p+1} = Phi_p X_p + F_p),
 and the outputs of all segments are then scanned in parallel.  The result is
 the recurrence of Eq. comba-S, compared here with the fp64 oracle (bar 2e-3 for
-bf16 inputs) and with the unsegmented scan (COMBA_SCAN_SEGMENTS=1).
+bf16 inputs) and with the unsegmented scan (COMBA_SCAN_SEGMENTS=1).  The
+backward (stateless and training pair) is segmented the same way: every
+segment's state gradient at its start from a zero end, the gradient leaving
+each segment from Y_{p-1} = Phi_p^T Y_p + G_p, and the reverse scan of all
+segments in parallel.
 
 The gates are weak (log-gates scaled by 0.002, about 25% of a state surviving
 a 1024-token segment) so that every segment's outputs depend strongly on the
@@ -174,3 +178,59 @@ def test_a_workspace_without_the_segment_buffers_runs_the_plain_scan():
     # with its buffers it ran the segmented one (same result up to rounding)
     assert not np.array_equal(outs[0][0], outs[2][0])
     assert maxrel(outs[2][0], outs[0][0]) <= 2e-4
+
+
+def _grad_case(B, T, H, dk, dv, seed):
+    print("segmented backward case: B%d T%d H%d dk%d dv%d seed %d" % (B, T, H, dk, dv, seed),
+          flush=True)
+    w = random_case(B=B, T=T, H=H, dk=dk, dv=dv, in_dtype="bf16", seed=seed, grad=True, dht=True)
+    w.g = (w.g * np.float32(0.002)).astype(np.float32)
+    return w
+
+
+GRAD_NAMES = ("dq", "dk", "dv", "dg", "dbeta", "dd", "dh0")
+
+
+@pytest.mark.parametrize("B,T,H,dk,dv,P", [
+    (1, 8192, 2, 128, 128, 8),
+    (2, 4096, 1, 128, 64, 4),
+    (1, 8192, 1, 256, 256, 4),
+])
+def test_segmented_backward_matches_the_oracle_and_the_plain_scans(B, T, H, dk, dv, P):
+    from gpu_helpers import check_bwd, gpu_bwd
+
+    w = _grad_case(B, T, H, dk, dv, seed=700 + P + dk)
+    os.environ[ENV] = "1"
+    plain = gpu_bwd(w)
+    os.environ[ENV] = str(P)
+    errs = check_bwd(w)                                # stateless backward, segmented
+    print("backward P=%d: %s" % (P, {k: "%.2e" % v for k, v in errs.items()}), flush=True)
+    seg = gpu_bwd(w)
+    for name in GRAD_NAMES:
+        assert maxrel(seg[name], plain[name]) <= 5e-4, (name, maxrel(seg[name], plain[name]))
+
+
+@pytest.mark.parametrize("P", [4, 8])
+def test_segmented_training_pair_equals_the_stateless_pair(P):
+    import torch
+
+    import paper_2506_02475_amd as comba
+    from gpu_helpers import to_device
+
+    w = _grad_case(1, 8192, 2, 128, 128, seed=61 + P)
+    os.environ[ENV] = str(P)
+    a = to_device(w)
+    args = (a["q"], a["k"], a["v"], a["g"], a["beta"], a["d"], a["h0"])
+    o_s, ht_s = comba.comba_chunk_fwd(*args)
+    g_s = comba.comba_chunk_bwd(*args, a["dO"], a["dht"])
+    comba.profile_enable(True)
+    o_p, ht_p, ws = comba.comba_chunk_fwd_save(*args)
+    g_p = comba.comba_chunk_bwd_saved(*args, a["dO"], a["dht"], workspace=ws)
+    torch.cuda.synchronize()
+    stages = [n for n, _ in comba.profile_read()]
+    comba.profile_enable(False)
+    assert "scan_seg_phi" in stages and "scan_seg_grad" in stages, stages
+    # the same arithmetic in both pairs: bitwise equal
+    assert torch.equal(o_s, o_p) and torch.equal(ht_s, ht_p)
+    for name in GRAD_NAMES:
+        assert torch.equal(g_s[name], g_p[name]), name
