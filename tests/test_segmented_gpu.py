@@ -234,3 +234,27 @@ def test_segmented_training_pair_equals_the_stateless_pair(P):
     assert torch.equal(o_s, o_p) and torch.equal(ht_s, ht_p)
     for name in GRAD_NAMES:
         assert torch.equal(g_s[name], g_p[name]), name
+
+
+def test_segmented_pair_with_separate_feedback_strength_and_no_final_gradient():
+    """beta~ given on its own (dbeta and dbeta~ split) and dht = 0, P = 8."""
+    from comba_inputs import attach_beta_tilde
+    from gpu_helpers import check_bwd, gpu_bwd
+
+    print("segmented case: beta~ independent, no dht, B1 T8192 H2 d128", flush=True)
+    w = random_case(B=1, T=8192, H=2, dk=128, dv=128, in_dtype="bf16", seed=404, grad=True,
+                    dht=False)
+    w.g = (w.g * np.float32(0.002)).astype(np.float32)
+    attach_beta_tilde(w, "independent", seed=405)
+    os.environ[ENV] = "1"
+    plain_o, plain_ht = gpu_fwd(w)
+    plain = gpu_bwd(w)
+    os.environ[ENV] = "8"
+    ferrs = check_fwd(w)
+    berrs = check_bwd(w)
+    print("beta~ P=8: fwd %s bwd %s" % ({k: "%.2e" % v for k, v in ferrs.items()},
+                                        {k: "%.2e" % v for k, v in berrs.items()}), flush=True)
+    seg = gpu_bwd(w)
+    assert "dbeta_tilde" in seg and seg["dbeta_tilde"] is not None
+    for name in GRAD_NAMES + ("dbeta_tilde",):
+        assert maxrel(seg[name], plain[name]) <= 5e-4, (name, maxrel(seg[name], plain[name]))
