@@ -71,9 +71,9 @@
  *    points cut every row into P segments scanned side by side (the state
  *    recurrence is affine in the state entering a segment; Section 3.3's
  *    chunk form, applied between segments).  P is chosen from the shape and
- *    the device; the environment variable COMBA_SCAN_SEGMENTS overrides it (1:
- *    never, P >= 2: P segments when P divides the row's chunks), read at every
- *    call.  The workspace sizes include the segments' buffers; a smaller
+ *    the device; the environment variable COMBA_SCAN_SEGMENTS, read at every
+ *    call, overrides it: 1 never, P in 2..64 P segments when P divides the
+ *    row's chunks (else none), unset or 0 the automatic choice.  The workspace sizes include the segments' buffers; a smaller
  *    workspace that still holds the plain layout runs the plain scans.  The
  *    result equals the plain scans' up to rounding.  A saved pair
  *    (comba_chunk_fwd_save, comba_chunk_bwd_saved) must see the same

@@ -101,15 +101,14 @@ comba_status check_shape_recurrent(const comba_shape* s, Dims* out) {
 // (N H dv / 32) as the device has CUs, into the largest power of two P for
 // which the segments' chains are at most two per CU, P divides the row's
 // chunks and every segment keeps at least 16 chunks.  COMBA_SCAN_SEGMENTS overrides the
-// choice: 1 disables, P >= 2 forces P when it divides the row's chunks (P <= 64).
+// choice: 1 disables, P >= 2 forces P when it divides the row's chunks (P <= 64;
+// any other P disables); unset or 0 keeps the automatic choice.
 int seg_parts(const Dims& d) {
   if (!d.bf16 || d.N <= 0 || d.Tseq <= 0 || d.Tseq % kChunk) return 1;
   const int n = d.Tseq / kChunk;
   if (const char* env = getenv("COMBA_SCAN_SEGMENTS")) {
-    if (*env) {
-      const int P = atoi(env);
-      return P >= 2 && P <= 64 && n % P == 0 ? P : 1;
-    }
+    const int P = atoi(env);  // 0 (or not a number): the automatic choice below
+    if (P != 0) return P >= 2 && P <= 64 && n % P == 0 ? P : 1;
   }
   int dev = 0, cus = 0;
   if (hipGetDevice(&dev) != hipSuccess ||

@@ -364,3 +364,57 @@ def test_binding_checks_host_offsets():
     shp = comba._make_shape(1, 9, 1, 64, 64, 2, ctypes.c_void_p(FAKE), comba.COMBA_BF16,
                             cu_host=a)
     assert shp.cu_seqlens_host == a.ctypes.data
+
+
+@pytest.fixture
+def seg_env():
+    old = os.environ.get("COMBA_SCAN_SEGMENTS")
+    yield
+    if old is None:
+        os.environ.pop("COMBA_SCAN_SEGMENTS", None)
+    else:
+        os.environ["COMBA_SCAN_SEGMENTS"] = old
+
+
+@pytest.mark.parametrize("dk,dv", [(128, 128), (128, 64), (256, 256)])
+def test_segmented_workspace_holds_the_per_segment_states(seg_env, dk, dv):
+    # a forced segment count P: the forward's workspace adds four per-segment
+    # states (F, X0, HT: dk x dv; Phi: dk x dk, fp32), the backward-sized one
+    # three more (G, Y0, DH0), each rounded up to 256 bytes
+    lib = comba.load_library()
+    s = shape(B=2, T=64 * 32, H=3, dk=dk, dv=dv)
+    rnd = lambda x: (x + 255) // 256 * 256
+    os.environ["COMBA_SCAN_SEGMENTS"] = "1"
+    f1, b1 = lib.comba_fwd_workspace_bytes(ctypes.byref(s)), lib.comba_bwd_workspace_bytes(ctypes.byref(s))
+    for P in (2, 4, 8, 16, 32):
+        os.environ["COMBA_SCAN_SEGMENTS"] = str(P)
+        nvr = 2 * P * 3
+        sdv, sdk = rnd(nvr * dk * dv * 4), rnd(nvr * dk * dk * 4)
+        assert lib.comba_fwd_workspace_bytes(ctypes.byref(s)) == f1 + 3 * sdv + sdk
+        assert lib.comba_bwd_workspace_bytes(ctypes.byref(s)) == b1 + 6 * sdv + sdk
+
+
+@pytest.mark.parametrize("T,env", [
+    (64 * 12, "8"),      # 12 chunks: 8 does not divide them
+    (64 * 32 - 1, "2"),  # a partial last chunk
+    (64 * 32, "0"),      # the automatic choice, which needs a device (none here)
+    (64 * 32, "65"),     # beyond the largest count
+])
+def test_segments_not_taken_when_they_do_not_fit_the_rows(seg_env, T, env):
+    lib = comba.load_library()
+    s = shape(B=1, T=T, H=2)
+    os.environ["COMBA_SCAN_SEGMENTS"] = "1"
+    plain = lib.comba_fwd_workspace_bytes(ctypes.byref(s))
+    os.environ["COMBA_SCAN_SEGMENTS"] = env
+    assert lib.comba_fwd_workspace_bytes(ctypes.byref(s)) == plain
+
+
+def test_packed_batches_and_fp32_inputs_are_not_segmented(seg_env):
+    lib = comba.load_library()
+    packed = shape(B=1, T=64 * 32, H=2, N=2, cu=FAKE)
+    f32 = shape(B=1, T=64 * 32, H=2, dk=64, dv=64, dtype=comba.COMBA_F32)
+    for s in (packed, f32):
+        os.environ["COMBA_SCAN_SEGMENTS"] = "1"
+        plain = lib.comba_fwd_workspace_bytes(ctypes.byref(s))
+        os.environ["COMBA_SCAN_SEGMENTS"] = "4"
+        assert lib.comba_fwd_workspace_bytes(ctypes.byref(s)) == plain
