@@ -66,14 +66,16 @@
  *    states) makes the affected outputs and gradients of its sequence and
  *    head non-finite; other sequences and heads are unaffected (dd sums over
  *    all sequences of a head and so takes it up too).
- *  - Few long rows (fixed-length rows whose state scans would have fewer
- *    chains, N H dv / 32, than half the device's CUs): the bf16 chunk entry
- *    points cut every row into P segments scanned side by side (the state
+ *  - Few long rows (rows whose state scans would have fewer chains, N H dv /
+ *    32, than half the device's CUs; packed batches only with
+ *    cu_seqlens_host): the bf16 chunk entry points cut every row into P
+ *    segments scanned side by side (the state
  *    recurrence is affine in the state entering a segment; Section 3.3's
  *    chunk form, applied between segments).  P is chosen from the shape and
  *    the device; the environment variable COMBA_SCAN_SEGMENTS, read at every
- *    call, overrides it: 1 never, P in 2..64 P segments when P divides the
- *    row's chunks (else none), unset or 0 the automatic choice.  The workspace sizes include the segments' buffers; a smaller
+ *    call, overrides it: 1 never, P in 2..64 P segments (fixed-length rows:
+ *    when P divides the row's chunks, else none), unset or 0 the automatic
+ *    choice.  The workspace sizes include the segments' buffers; a smaller
  *    workspace that still holds the plain layout runs the plain scans.  The
  *    result equals the plain scans' up to rounding.  A saved pair
  *    (comba_chunk_fwd_save, comba_chunk_bwd_saved) must see the same

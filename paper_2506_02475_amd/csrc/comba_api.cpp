@@ -18,8 +18,9 @@ constexpr size_t kAlign = 256;
 size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Dims {
-  bool bf16;
+  bool bf16, packed;
   int dk, dv, H, N, Tseq, Ttot, ncmax;
+  int maxch;  // chunks of the longest sequence (packed: 0 without the host offsets)
 };
 
 // Validates the shape; fills dims on success.  `wide` also admits head dim 256
@@ -37,6 +38,7 @@ comba_status check_shape(const comba_shape* s, Dims* out, bool wide = false) {
   if (!big && (!dk_ok || !dv_ok)) return COMBA_ERR_SHAPE;
   Dims d;
   d.bf16 = bf16;
+  d.packed = s->cu_seqlens != nullptr;
   d.dk = s->dk;
   d.dv = s->dv;
   d.H = s->H;
@@ -44,18 +46,23 @@ comba_status check_shape(const comba_shape* s, Dims* out, bool wide = false) {
     if (s->B != 1 || s->num_seqs < 0) return COMBA_ERR_SHAPE;
     d.N = s->num_seqs;
     d.Tseq = 0;
+    d.maxch = 0;
     if (s->cu_seqlens_host) {
       // the host copy of the offsets: 0 = cu[0] <= cu[1] <= ... <= cu[N] = T
       const int32_t* cu = s->cu_seqlens_host;
       if (cu[0] != 0 || cu[d.N] != s->T) return COMBA_ERR_SHAPE;
-      for (int i = 0; i < d.N; ++i)
+      for (int i = 0; i < d.N; ++i) {
         if (cu[i + 1] < cu[i]) return COMBA_ERR_SHAPE;
+        const int nch = (cu[i + 1] - cu[i] + kChunk - 1) / kChunk;
+        if (nch > d.maxch) d.maxch = nch;
+      }
     }
   } else {
     if (s->cu_seqlens_host) return COMBA_ERR_SHAPE;  // offsets without a packed batch
     if (s->num_seqs != s->B) return COMBA_ERR_SHAPE;
     d.N = s->B;
     d.Tseq = s->T;
+    d.maxch = (s->T + kChunk - 1) / kChunk;
   }
   const int64_t ttot = s->cu_seqlens ? (int64_t)s->T : (int64_t)s->B * s->T;
   if (ttot > INT32_MAX / 2) return COMBA_ERR_SHAPE;
@@ -104,12 +111,18 @@ comba_status check_shape_recurrent(const comba_shape* s, Dims* out) {
 // choice: 1 disables, P >= 2 forces P when it divides the row's chunks (P <= 64;
 // any other P disables); unset or 0 keeps the automatic choice.
 int seg_parts(const Dims& d) {
-  if (!d.bf16 || d.N <= 0 || d.Tseq <= 0 || d.Tseq % kChunk) return 1;
-  const int n = d.Tseq / kChunk;
+  if (!d.bf16 || d.N <= 0) return 1;
+  // fixed-length rows: whole chunks, P dividing them; packed sequences: any P
+  // (a sequence's segments are ceil(n / P) chunks, the last ones shorter or
+  // empty), chosen automatically only when the host offsets give the lengths
+  const bool packed = d.packed;
+  if (!packed && (d.Tseq <= 0 || d.Tseq % kChunk)) return 1;
+  const int n = packed ? d.maxch : d.Tseq / kChunk;
   if (const char* env = getenv("COMBA_SCAN_SEGMENTS")) {
     const int P = atoi(env);  // 0 (or not a number): the automatic choice below
-    if (P != 0) return P >= 2 && P <= 64 && n % P == 0 ? P : 1;
+    if (P != 0) return P >= 2 && P <= 64 && (packed || n % P == 0) ? P : 1;
   }
+  if (n <= 0) return 1;
   int dev = 0, cus = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
@@ -117,13 +130,14 @@ int seg_parts(const Dims& d) {
   const long chains = (long)d.N * d.H * (d.dv / 32);
   if (cus <= 0 || 2 * chains > cus) return 1;
   int P = 1;
-  while (P < 64 && chains * 2 * P <= 2L * cus && n % (2 * P) == 0 && n / (2 * P) >= 16) P *= 2;
+  while (P < 64 && chains * 2 * P <= 2L * cus && (packed || n % (2 * P) == 0) && n / (2 * P) >= 16)
+    P *= 2;
   return P;
 }
 
 struct Layout {
   size_t cmap, smap, sord, M, A, G, X, D, Y, dR, ddp, QT, Xfin, total;
-  size_t segF, segPhi, segX0, segHT, segG, segY0, segDH0;  // segmented scans (segP > 1)
+  size_t segF, segPhi, segX0, segHT, segG, segY0, segDH0, segmap;  // segmented scans (segP > 1)
   size_t Xs, Ds, Ys, dRs, Xfs;  // bf16 path: scales of the int16 X, D, Y, dR, final-state sink
   size_t Ms, As;                // bf16 path: row scales of M, column scales of A
 };
@@ -181,6 +195,7 @@ Layout layout(const Dims& d, bool bwd, int segP = 1) {
     // dk); the backward-sized workspace (training pair, stateless backward)
     // also G, Y0, DH0 (dk x dv)
     const size_t nvr = (size_t)d.N * segP * d.H;
+    L.segmap = take((size_t)d.N * segP * sizeof(comba::SeqInfo));  // packed: virtual rows
     L.segF = take(nvr * d.dk * d.dv * sizeof(float));
     L.segPhi = take(nvr * d.dk * d.dk * sizeof(float));
     L.segX0 = take(nvr * d.dk * d.dv * sizeof(float));
@@ -245,6 +260,7 @@ void carve(comba::LaunchArgs& a, const Layout& L, void* ws, bool bwd, int segP =
   char* base = static_cast<char*>(ws);
   a.segP = segP;
   if (segP > 1) {
+    a.segmap = reinterpret_cast<comba::SeqInfo*>(base + L.segmap);
     a.segF = reinterpret_cast<float*>(base + L.segF);
     a.segPhi = reinterpret_cast<float*>(base + L.segPhi);
     a.segX0 = reinterpret_cast<float*>(base + L.segX0);

@@ -116,6 +116,26 @@ __global__ __launch_bounds__(NTHR) void k_seq_map(const int32_t* __restrict__ cu
   }
 }
 
+// k_seg_map: the virtual sequence table of the segmented scans over packed
+// sequences.  Segment p of sequence s is virtual row s P + p: chunks [p L,
+// min((p + 1) L, n)) of the sequence's n chunks with L = ceil(n / P), empty
+// past its end; one thread per virtual row.
+__global__ __launch_bounds__(NTHR) void k_seg_map(const SeqInfo* __restrict__ smap, int N, int P,
+                                                  SeqInfo* __restrict__ vmap) {
+  const int i = blockIdx.x * NTHR + threadIdx.x;
+  if (i >= N * P) return;
+  const int s = i / P, p = i - s * P;
+  const SeqInfo si = smap[s];
+  const int L = (si.nchunks + P - 1) / P;
+  const int c0 = min(p * L, si.nchunks), nc = min(L, si.nchunks - c0);
+  SeqInfo v;
+  v.chunk0 = si.chunk0 + c0;
+  v.nchunks = nc;
+  v.tok0 = si.tok0 + c0 * CH;
+  v.len = nc > 0 ? min(si.len - c0 * CH, nc * CH) : 0;
+  vmap[i] = v;
+}
+
 // k_chunk_fill: one thread per chunk slot c < ncmax.  Its sequence is the last
 // one whose first chunk is <= c (first chunks never decrease, and an empty
 // sequence shares its first chunk with the next one), found by binary search;
@@ -3186,20 +3206,22 @@ static hipError_t run_bwd(const LaunchArgs& a) {
 // its transition product (of every segment when a backward follows, which
 // needs those of all but the first; else not of the last) and the true state
 // entering every segment.
+// vsm, Tv: the virtual rows (packed sequences: the table of k_seg_map, Tv < 0;
+// fixed-length rows: vsm NULL, Tv = Tseq / P tokens each).
 template <int DK, int DV>
 static void seg_forward_states(const LaunchArgs& a, const bf16_t* q, const bf16_t* k,
                                const bf16_t* v, const bf16_t* beta, const bf16_t* bt,
-                               bool phi_all) {
+                               bool phi_all, const SeqInfo* vsm, int Tp) {
   hipStream_t st = a.stream;
-  const int P = a.segP, Tp = a.Tseq / P, Nst = a.N * (P - 1);
+  const int P = a.segP, Nst = a.N * (P - 1);
   const int Nphi = phi_all ? a.N * P : Nst, gphi = phi_all ? 0 : P;
   a.stage("scan_seg_state");
   k_scan_fwd_bf<DK, DV, SCAN_BV, false, false><<<scan_blocks(Nst, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-      q, k, v, beta, bt, a.d, nullptr, nullptr, nullptr, Nst, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw,
+      q, k, v, beta, bt, a.d, nullptr, vsm, nullptr, Nst, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw,
       nullptr, a.segF, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, P);
   a.stage("scan_seg_phi");
   k_scan_fwd_bf<DK, DK, SCAN_BV, false, false, true><<<scan_blocks(Nphi, a.H, DK / SCAN_BV), NTHR, 0, st>>>(
-      q, k, v, beta, bt, a.d, nullptr, nullptr, nullptr, Nphi, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw,
+      q, k, v, beta, bt, a.d, nullptr, vsm, nullptr, Nphi, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw,
       nullptr, a.segPhi, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, gphi);
   a.stage("seg_combine");
   k_seg_combine<DK, DV><<<a.N * a.H * (DV / SEG_SL), NTHR, 0, st>>>(a.segPhi, a.segF, a.h0, P, a.H,
@@ -3248,17 +3270,21 @@ static hipError_t run_fwd_bf(const LaunchArgs& a) {
     // segment needs); 2. the true state entering each segment
     // (k_seg_combine); 3. the output scan of every segment from that state
     // (with the chunk states for the backward in the training pair).
-    const int Np = a.N * a.segP, Tp = a.Tseq / a.segP;
-    seg_forward_states<DK, DV>(a, q, k, v, beta, bt, a.saved);
+    // packed sequences: segments of each sequence from its table entry
+    const SeqInfo* vsm = Tfix < 0 ? a.segmap : nullptr;
+    const int Np = a.N * a.segP, Tp = Tfix < 0 ? -1 : a.Tseq / a.segP;
+    if (Tfix < 0)
+      k_seg_map<<<(Np + NTHR - 1) / NTHR, NTHR, 0, st>>>(a.smap, a.N, a.segP, a.segmap);
+    seg_forward_states<DK, DV>(a, q, k, v, beta, bt, a.saved, vsm, Tp);
     a.stage(a.saved ? "scan_fwd_save" : "scan_fwd");
     float* htv = a.ht ? a.segHT : nullptr;
     if (a.saved)
       k_scan_fwd_bf<DK, DV, SCAN_BV, true, true><<<scan_blocks(Np, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-          q, k, v, beta, bt, a.d, a.segX0, nullptr, nullptr, Np, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As,
+          q, k, v, beta, bt, a.d, a.segX0, vsm, nullptr, Np, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As,
           a.Gw, a.o, htv, a.Xq, a.Xs, a.Dq, a.Ds, nullptr, nullptr);
     else
       k_scan_fwd_bf<DK, DV, SCAN_BV, true, false><<<scan_blocks(Np, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-          q, k, v, beta, bt, a.d, a.segX0, nullptr, nullptr, Np, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As,
+          q, k, v, beta, bt, a.d, a.segX0, vsm, nullptr, Np, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As,
           a.Gw, a.o, htv, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
     // the final state of each row is that of its last segment
     if (a.ht && seg_copy_rows<DK, DV>(a, a.ht, a.segHT, a.segP - 1) != hipSuccess)
@@ -3303,28 +3329,37 @@ static hipError_t run_bwd_bf(const LaunchArgs& a) {
     // the state leaving every segment (k_seg_combine_bwd, with Phi_p^T); 3. the
     // reverse scan of every segment from it, storing Y and dR for the
     // gradient kernel; dh0 is the first segment's.
-    const int P = a.segP, Np = a.N * P, Tp = a.Tseq / P, Nst = a.N * (P - 1);
+    const int P = a.segP, Np = a.N * P, Nst = a.N * (P - 1);
+    // packed sequences: segments of each sequence from its table entry (the
+    // training pair's forward left the table in the workspace)
+    const SeqInfo* vsm = Tfix < 0 ? a.segmap : nullptr;
+    const int Tp = Tfix < 0 ? -1 : a.Tseq / P;
     if (!a.saved) {
+      if (Tfix < 0) {
+        a.stage("chunk_map");
+        launch_chunk_map(a, st);
+        k_seg_map<<<(Np + NTHR - 1) / NTHR, NTHR, 0, st>>>(a.smap, a.N, P, a.segmap);
+      }
       a.stage("prep");
       if (a.ncmax > 0)
         k_prep_bf<DK, true><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
             q, k, a.g, bt, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.QTp, a.Gw);
-      seg_forward_states<DK, DV>(a, q, k, v, beta, bt, true);
+      seg_forward_states<DK, DV>(a, q, k, v, beta, bt, true, vsm, Tp);
       a.stage("scan_fwd_store");
       k_scan_fwd_bf<DK, DV, SCAN_BV, false, true><<<scan_blocks(Np, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-          q, k, v, beta, bt, a.d, a.segX0, nullptr, nullptr, Np, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As,
+          q, k, v, beta, bt, a.d, a.segX0, vsm, nullptr, Np, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As,
           a.Gw, nullptr, nullptr, a.Xq, a.Xs, a.Dq, a.Ds, nullptr, nullptr);
     }
     a.stage("scan_seg_grad");
     k_scan_bwd_bf<DK, DV, SCAN_BV, false><<<scan_blocks(Nst, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-        q, k, dO, bt, a.d, nullptr, nullptr, nullptr, Nst, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As, a.QTp,
+        q, k, dO, bt, a.d, nullptr, vsm, nullptr, Nst, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As, a.QTp,
         a.Gw, a.segG, nullptr, nullptr, nullptr, nullptr, P, 1);
     a.stage("seg_combine_bwd");
     k_seg_combine_bwd<DK, DV><<<a.N * a.H * (DV / SEG_SL), NTHR, 0, st>>>(a.segPhi, a.segG, a.dht, P,
                                                                       a.H, a.segY0);
     a.stage("scan_bwd");
     k_scan_bwd_bf<DK, DV, SCAN_BV><<<scan_blocks(Np, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-        q, k, dO, bt, a.d, a.segY0, nullptr, nullptr, Np, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As, a.QTp,
+        q, k, dO, bt, a.d, a.segY0, vsm, nullptr, Np, Tp, a.H, a.Mq, a.Ms, a.Aq, a.As, a.QTp,
         a.Gw, a.dh0 ? a.segDH0 : nullptr, a.Yq, a.Ys, a.dRq, a.dRs);
     if (a.dh0 && seg_copy_rows<DK, DV>(a, a.dh0, a.segDH0, 0) != hipSuccess)
       return hipErrorLaunchFailure;

@@ -68,6 +68,7 @@ struct LaunchArgs {
   // true one at its end (segY0) and at its start (segDH0)
   int segP;
   float *segF, *segPhi, *segX0, *segHT, *segG, *segY0, *segDH0;
+  SeqInfo* segmap;  // packed sequences: the virtual rows' table (k_seg_map)
   hipStream_t stream;
   StageHook hook;
   void stage(const char* name) const {

@@ -378,9 +378,10 @@ def seg_env():
 
 @pytest.mark.parametrize("dk,dv", [(128, 128), (128, 64), (256, 256)])
 def test_segmented_workspace_holds_the_per_segment_states(seg_env, dk, dv):
-    # a forced segment count P: the forward's workspace adds four per-segment
-    # states (F, X0, HT: dk x dv; Phi: dk x dk, fp32), the backward-sized one
-    # three more (G, Y0, DH0), each rounded up to 256 bytes
+    # a forced segment count P: the forward's workspace adds the virtual rows'
+    # table (16 bytes per segment) and four per-segment states (F, X0, HT:
+    # dk x dv; Phi: dk x dk, fp32), the backward-sized one three more (G, Y0,
+    # DH0), each rounded up to 256 bytes
     lib = comba.load_library()
     s = shape(B=2, T=64 * 32, H=3, dk=dk, dv=dv)
     rnd = lambda x: (x + 255) // 256 * 256
@@ -389,9 +390,9 @@ def test_segmented_workspace_holds_the_per_segment_states(seg_env, dk, dv):
     for P in (2, 4, 8, 16, 32):
         os.environ["COMBA_SCAN_SEGMENTS"] = str(P)
         nvr = 2 * P * 3
-        sdv, sdk = rnd(nvr * dk * dv * 4), rnd(nvr * dk * dk * 4)
-        assert lib.comba_fwd_workspace_bytes(ctypes.byref(s)) == f1 + 3 * sdv + sdk
-        assert lib.comba_bwd_workspace_bytes(ctypes.byref(s)) == b1 + 6 * sdv + sdk
+        sdv, sdk, tab = rnd(nvr * dk * dv * 4), rnd(nvr * dk * dk * 4), rnd(2 * P * 16)
+        assert lib.comba_fwd_workspace_bytes(ctypes.byref(s)) == f1 + tab + 3 * sdv + sdk
+        assert lib.comba_bwd_workspace_bytes(ctypes.byref(s)) == b1 + tab + 6 * sdv + sdk
 
 
 @pytest.mark.parametrize("T,env", [
@@ -409,12 +410,14 @@ def test_segments_not_taken_when_they_do_not_fit_the_rows(seg_env, T, env):
     assert lib.comba_fwd_workspace_bytes(ctypes.byref(s)) == plain
 
 
-def test_packed_batches_and_fp32_inputs_are_not_segmented(seg_env):
+def test_packed_batches_are_segmented_and_fp32_inputs_are_not(seg_env):
+    # packed sequences take any forced count (a sequence's segments are
+    # ceil(n / P) chunks, the last ones shorter or empty); fp32 inputs never
     lib = comba.load_library()
-    packed = shape(B=1, T=64 * 32, H=2, N=2, cu=FAKE)
+    packed = shape(B=1, T=64 * 30 + 5, H=2, N=2, cu=FAKE)
     f32 = shape(B=1, T=64 * 32, H=2, dk=64, dv=64, dtype=comba.COMBA_F32)
-    for s in (packed, f32):
+    for s, grows in ((packed, True), (f32, False)):
         os.environ["COMBA_SCAN_SEGMENTS"] = "1"
         plain = lib.comba_fwd_workspace_bytes(ctypes.byref(s))
         os.environ["COMBA_SCAN_SEGMENTS"] = "4"
-        assert lib.comba_fwd_workspace_bytes(ctypes.byref(s)) == plain
+        assert (lib.comba_fwd_workspace_bytes(ctypes.byref(s)) > plain) == grows

@@ -258,3 +258,64 @@ def test_segmented_pair_with_separate_feedback_strength_and_no_final_gradient():
     assert "dbeta_tilde" in seg and seg["dbeta_tilde"] is not None
     for name in GRAD_NAMES + ("dbeta_tilde",):
         assert maxrel(seg[name], plain[name]) <= 5e-4, (name, maxrel(seg[name], plain[name]))
+
+
+def _packed_case(seqlens, H, seed, grad):
+    print("segmented packed case: lengths %s H%d seed %d" % (seqlens, H, seed), flush=True)
+    w = random_case(B=1, T=0, H=H, dk=128, dv=128, in_dtype="bf16", seed=seed, seqlens=seqlens,
+                    grad=grad, dht=grad)
+    w.g = (w.g * np.float32(0.002)).astype(np.float32)
+    return w
+
+
+@pytest.mark.parametrize("seqlens,P", [
+    ([5000, 64, 0, 12345], 8),    # short and empty sequences: empty segments
+    ([3000, 2999], 4),
+])
+def test_packed_segments_match_the_oracle_and_the_plain_scans(seqlens, P):
+    from gpu_helpers import check_bwd, gpu_bwd
+
+    w = _packed_case(seqlens, 2, seed=31 + P, grad=True)
+    os.environ[ENV] = "1"
+    po, pht = gpu_fwd(w)
+    pg = gpu_bwd(w)
+    os.environ[ENV] = str(P)
+    ferrs = check_fwd(w)
+    berrs = check_bwd(w)
+    print("packed P=%d: fwd %s bwd %s" % (P, {k: "%.2e" % v for k, v in ferrs.items()},
+                                          {k: "%.2e" % v for k, v in berrs.items()}), flush=True)
+    so, sht = gpu_fwd(w)
+    sg = gpu_bwd(w)
+    assert maxrel(so, po) <= 2e-4 and maxrel(sht, pht) <= 2e-4
+    for name in GRAD_NAMES:
+        assert maxrel(sg[name], pg[name]) <= 5e-4, (name, maxrel(sg[name], pg[name]))
+
+
+def test_packed_auto_segments_and_training_pair():
+    import torch
+
+    import paper_2506_02475_amd as comba
+    from gpu_helpers import to_device
+
+    os.environ.pop(ENV, None)
+    w = _packed_case([40000, 30001], 2, seed=12, grad=True)
+    a = to_device(w)
+    cuh = w.cu_seqlens.astype(np.int32)
+    args = (a["q"], a["k"], a["v"], a["g"], a["beta"], a["d"], a["h0"])
+    kw = dict(cu_seqlens=a["cu_seqlens"], cu_seqlens_host=cuh)
+    comba.profile_enable(True)
+    o_s, ht_s = comba.comba_chunk_fwd(*args, **kw)
+    g_s = comba.comba_chunk_bwd(*args, a["dO"], a["dht"], **kw)
+    o_p, ht_p, ws = comba.comba_chunk_fwd_save(*args, **kw)
+    g_p = comba.comba_chunk_bwd_saved(*args, a["dO"], a["dht"], workspace=ws, **kw)
+    torch.cuda.synchronize()
+    stages = [n for n, _ in comba.profile_read()]
+    comba.profile_enable(False)
+    # 2 sequences x 2 heads x 4 slices = 16 chains: the host offsets let the
+    # library cut them
+    assert "scan_seg_state" in stages and "scan_seg_grad" in stages, stages
+    ro, rht = oracle.step_fwd(w.q, w.k, w.v, w.g, w.beta, w.d, w.h0, cu_seqlens=w.cu_seqlens)
+    assert maxrel(o_s.cpu().numpy(), ro) <= 2e-3 and maxrel(ht_s.cpu().numpy(), rht) <= 2e-3
+    assert torch.equal(o_s, o_p) and torch.equal(ht_s, ht_p)
+    for name in GRAD_NAMES:
+        assert torch.equal(g_s[name], g_p[name]), name
