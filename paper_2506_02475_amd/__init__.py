@@ -533,3 +533,65 @@ def comba_chunk_bwd_saved(q, k, v, g, beta, d, h0, dO, dht=None, *, workspace, b
     """Backward reusing the state left by comba_chunk_fwd_save in `workspace`."""
     return _bwd(True, q, k, v, g, beta, d, h0, dO, dht, cu_seqlens, need_dh0, workspace, stream,
                 beta_tilde, cu_seqlens_host)
+
+
+def _autograd_function():
+    import torch
+
+    class _ChunkComba(torch.autograd.Function):
+        """The training pair as one differentiable op: comba_chunk_fwd_save in
+        the forward (its workspace kept for the backward), comba_chunk_bwd_saved
+        in the backward.  Gradients come back in the inputs' dtypes; the
+        upstream gradient of o is rounded to the inputs' dtype (the kernels
+        take dO in in_dtype)."""
+
+        @staticmethod
+        def forward(ctx, q, k, v, g, beta, d, h0, beta_tilde, cu_seqlens, cu_seqlens_host):
+            ctx.set_materialize_grads(False)  # an unused output's gradient arrives as None
+            o, ht, ws = comba_chunk_fwd_save(q, k, v, g, beta, d, h0, beta_tilde=beta_tilde,
+                                             cu_seqlens=cu_seqlens,
+                                             cu_seqlens_host=cu_seqlens_host)
+            ctx.save_for_backward(q, k, v, g, beta, d, h0, beta_tilde, cu_seqlens, ws)
+            ctx.cu_seqlens_host = cu_seqlens_host
+            return o, ht
+
+        @staticmethod
+        def backward(ctx, do, dht):
+            q, k, v, g, beta, d, h0, beta_tilde, cu_seqlens, ws = ctx.saved_tensors
+            if do is None:
+                do = torch.zeros(q.shape[:3] + (v.shape[-1],), dtype=torch.float32,
+                                 device=q.device)
+            need = ctx.needs_input_grad
+            gr = comba_chunk_bwd_saved(q, k, v, g, beta, d, h0,
+                                       do.to(q.dtype).contiguous(),
+                                       None if dht is None else dht.float().contiguous(),
+                                       workspace=ws, beta_tilde=beta_tilde,
+                                       cu_seqlens=cu_seqlens,
+                                       cu_seqlens_host=ctx.cu_seqlens_host,
+                                       need_dh0=h0 is not None and need[6])
+
+            def cast(x, like, i):
+                return None if (x is None or not need[i]) else x.to(like.dtype)
+
+            return (cast(gr["dq"], q, 0), cast(gr["dk"], k, 1), cast(gr["dv"], v, 2),
+                    cast(gr["dg"], g, 3), cast(gr["dbeta"], beta, 4), cast(gr["dd"], d, 5),
+                    None if h0 is None else cast(gr["dh0"], h0, 6),
+                    None if beta_tilde is None else cast(gr["dbeta_tilde"], beta_tilde, 7),
+                    None, None)
+
+    return _ChunkComba
+
+
+_CHUNK_FN = None
+
+
+def comba_chunk(q, k, v, g, beta, d, h0=None, *, beta_tilde=None, cu_seqlens=None,
+                cu_seqlens_host=None):
+    """Differentiable chunk-wise Comba (torch.autograd): returns (o [B,T,H,dv]
+    fp32, ht [N,H,dk,dv] fp32); gradients flow to q, k, v, g, beta, d, h0 and
+    beta~ through the library's training pair.  Each call keeps its
+    backward-sized workspace until the backward has run."""
+    global _CHUNK_FN
+    if _CHUNK_FN is None:
+        _CHUNK_FN = _autograd_function()
+    return _CHUNK_FN.apply(q, k, v, g, beta, d, h0, beta_tilde, cu_seqlens, cu_seqlens_host)
