@@ -185,8 +185,10 @@ comba_status comba_chunk_bwd_saved(const comba_shape *shape, const void *q, cons
 /*
  * Forward without any device allocation, for callers that cannot allocate:
  * code under HIP graph capture, tight serving loops, harnesses that forbid
- * hipMalloc.  Computes exactly what comba_chunk_fwd computes (same kernels,
- * bitwise-equal results), with its workspace in a static device array of
+ * hipMalloc.  Computes what comba_chunk_fwd computes with the same kernels
+ * (bitwise-equal results; the one exception: few long rows whose segmented
+ * scans, see the conventions, need more than the array holds run the plain
+ * scans here, equal up to rounding), with its workspace in a static device array of
  * comba_noalloc_scratch_bytes() bytes (80 MiB) that every device the library
  * runs on holds until the process ends; the caller passes only inputs and
  * outputs.  A shape whose comba_fwd_workspace_bytes exceeds it (more than about
