@@ -103,3 +103,43 @@ def test_autograd_with_separate_feedback_strength():
                                      beta_tilde=bt.detach())
     assert torch.equal(bt.grad, gr["dbeta_tilde"].to(torch.bfloat16))
     assert torch.equal(x["beta"].grad, gr["dbeta"].to(torch.bfloat16))
+
+
+def test_autograd_over_segmented_scans():
+    """One long row cut into 4 segments (forced): the op's gradients equal the
+    directly called pair's under the same setting."""
+    import os
+
+    import torch
+
+    import paper_2506_02475_amd as comba
+
+    w = random_case(B=1, T=4096, H=2, dk=128, dv=128, in_dtype="bf16", seed=16, grad=True)
+    old = os.environ.get("COMBA_SCAN_SEGMENTS")
+    os.environ["COMBA_SCAN_SEGMENTS"] = "4"
+    try:
+        x = _inputs(w, torch.bfloat16)
+        comba.profile_enable(True)
+        o, ht = comba.comba_chunk(x["q"], x["k"], x["v"], x["g"], x["beta"], x["d"], x["h0"])
+        (o.sum() + ht.square().sum()).backward()
+        torch.cuda.synchronize()
+        stages = [n for n, _ in comba.profile_read()]
+        comba.profile_enable(False)
+        # the forward's stages (the session is per host thread; autograd runs
+        # the backward on its own device thread, which records nothing)
+        assert "scan_seg_state" in stages and "seg_combine" in stages, stages
+        det = {n: t.detach() for n, t in x.items()}
+        args = (det["q"], det["k"], det["v"], det["g"], det["beta"], det["d"], det["h0"])
+        o2, ht2, ws = comba.comba_chunk_fwd_save(*args)
+        gr = comba.comba_chunk_bwd_saved(*args, torch.ones_like(o2).to(torch.bfloat16), 2 * ht2,
+                                         workspace=ws)
+        torch.cuda.synchronize()
+    finally:
+        if old is None:
+            os.environ.pop("COMBA_SCAN_SEGMENTS", None)
+        else:
+            os.environ["COMBA_SCAN_SEGMENTS"] = old
+    assert torch.equal(o.detach(), o2) and torch.equal(ht.detach(), ht2)
+    for name, key in (("q", "dq"), ("k", "dk"), ("v", "dv"), ("g", "dg"), ("beta", "dbeta"),
+                      ("d", "dd"), ("h0", "dh0")):
+        assert torch.equal(x[name].grad, gr[key].to(x[name].dtype)), name
