@@ -91,6 +91,10 @@ def stage_model(name, B, T, H, dk, dv, C=64, in_bytes=2, sep_bt=False):
     elif name == "scan_bwd":      # K Y, A^T dO, M^T dD, Q^T Pg, K^T W2; -> Y, dR
         fl = 6 * C * dk * dv + 4 * C * C * dv
         by = 2 * qk + vv + 2 * cc + gb + st + cd      # k, Q^T, dO, M, A, g, beta
+    elif name == "scans":         # the stateless backward's two scans, side by side
+        f1, b1 = stage_model("scan_fwd_store", B, T, H, dk, dv, C, in_bytes, sep_bt)
+        f2, b2 = stage_model("scan_bwd", B, T, H, dk, dv, C, in_bytes, sep_bt)
+        return f1 + f2, b1 + b2
     elif name == "intra_bwd":     # 3 C x dk x dv, 2 C x C x dv, 5 C x C x dk products
         fl = 6 * C * dk * dv + 4 * C * C * dv + 10 * C * C * dk
         by = (2 * qk + 2 * vv + 2 * st + 2 * cd + gb          # q,k,v,dO,X,Y,D,dR
@@ -113,7 +117,7 @@ def op_flops(B, T, H, dk, dv, C=64):
 # Stages of the forward and of the backward direction (the names the library's
 # stage timing records)
 FWD_STAGES = ("chunk_map", "prep", "prep_save", "scan_fwd", "scan_fwd_save")
-BWD_STAGES = ("scan_fwd_store", "scan_bwd", "intra_bwd", "reduce_dd")
+BWD_STAGES = ("scan_fwd_store", "scan_bwd", "scans", "intra_bwd", "reduce_dd")
 
 
 def chunk_lengths(T, B=1, cu_seqlens=None, C=64):

@@ -22,8 +22,13 @@
  * Conventions shared by every entry point
  *  - `shape` (and shape->cu_seqlens_host) points to host memory; every other
  *    pointer (including shape->cu_seqlens) is a DEVICE pointer on the current
- *    HIP device.  The caller owns every buffer; the library allocates nothing
- *    and keeps no state between calls.
+ *    HIP device.  The caller owns every buffer; the library allocates no
+ *    device memory and keeps no data between calls.  It keeps one helper
+ *    stream (default priority) and two events per device, created on the
+ *    first comba_chunk_bwd call that uses them: the stateless backward runs
+ *    its two independent scans side by side, the second on the helper stream,
+ *    forked from and joined back to `stream` (under graph capture of `stream`
+ *    the helper joins the capture).
  *  - Layouts are C-contiguous.  Token-major tensors are [B, T, H, D]; in the
  *    variable-length mode B == 1, T is the packed token count and sequence s
  *    covers tokens [cu_seqlens[s], cu_seqlens[s+1]).  A sequence's last chunk
@@ -146,7 +151,9 @@ comba_status comba_chunk_fwd(const comba_shape *shape, const void *q, const void
 /*
  * Backward: gradients of L = <dO, o> + <dht, ht> with respect to every input.
  * Recomputes the forward internally (no saved state is needed from a forward
- * call).  Inputs as comba_chunk_fwd plus
+ * call); the recomputed chunk states and the reverse state-gradient scan do
+ * not depend on each other and run side by side (see the conventions).
+ * Inputs as comba_chunk_fwd plus
  *   dO    [B,T,H,dv] in_dtype     dht [N,H,dk,dv] fp32 or NULL (zero)
  * Outputs (fp32): dq, dk [B,T,H,dk]; dv [B,T,H,dv]; dg, dbeta [B,T,H];
  *   dbeta_tilde [B,T,H] (see the conventions: NULL only with beta_tilde NULL);

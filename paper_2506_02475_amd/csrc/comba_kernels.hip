@@ -32,6 +32,8 @@
 //   k_reduce_dd  deterministic sum of the partial dd over chunks
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "comba_device.hpp"
 #include "comba_launch.h"
 
@@ -3120,6 +3122,56 @@ static unsigned intra_bwd_grid(long items) {
   return (unsigned)(cus > 0 && cus < items ? cus : items);
 }
 
+// Work that can run beside the caller's stream: a second stream per device
+// (default priority, non-blocking, created on first use and kept until the
+// process ends) with a fork and a join event.  side(st) enqueues, in order, a
+// fork (the side stream waits for everything already on st), the side work,
+// the main work on st and a join (st waits for the side work), under a lock,
+// so that calls from several host threads cannot interleave their event
+// records.  Without a side stream (creation failed) both run on st in turn.
+// Under graph capture of st the side stream joins the capture and rejoins st.
+struct SideStream {
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+  bool failed = false;
+};
+constexpr int kMaxSideDevices = 64;
+static std::mutex g_side_mu;
+static SideStream g_side[kMaxSideDevices];
+
+template <typename Main, typename Side>
+static void side(hipStream_t st, Main&& main_work, Side&& side_work) {
+  int dev = 0;
+  SideStream* ss = nullptr;
+  // an error left by the side stream's own calls is cleared (the work then
+  // runs in turn), unless one was already pending from the caller's launches
+  const bool clean = hipPeekAtLastError() == hipSuccess;
+  std::unique_lock<std::mutex> lock(g_side_mu);
+  if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < kMaxSideDevices) {
+    SideStream& c = g_side[dev];
+    if (!c.s && !c.failed) {
+      if (hipStreamCreateWithFlags(&c.s, hipStreamNonBlocking) != hipSuccess ||
+          hipEventCreateWithFlags(&c.fork, hipEventDisableTiming) != hipSuccess ||
+          hipEventCreateWithFlags(&c.join, hipEventDisableTiming) != hipSuccess) {
+        c.failed = true;  // run in turn from now on
+        c.s = nullptr;
+      }
+    }
+    if (c.s) ss = &c;
+  }
+  if (!ss || hipEventRecord(ss->fork, st) != hipSuccess ||
+      hipStreamWaitEvent(ss->s, ss->fork, 0) != hipSuccess) {
+    if (clean) (void)hipGetLastError();
+    main_work(st);
+    side_work(st);
+    return;
+  }
+  side_work(ss->s);
+  main_work(st);
+  if (hipEventRecord(ss->join, ss->s) != hipSuccess || hipStreamWaitEvent(st, ss->join, 0) != hipSuccess)
+    (void)hipStreamSynchronize(ss->s);  // keep the order on the host if the join cannot be enqueued
+}
+
 // 1-D grid of the bf16 scans: whole groups of 8 chains (see scan_item).
 static unsigned scan_blocks(int N, int H, int nsl) {
   return (unsigned)((((long)N * H + 7) / 8) * 8 * nsl);
@@ -3372,12 +3424,24 @@ static hipError_t run_bwd_bf(const LaunchArgs& a) {
     if (a.ncmax > 0)
       k_prep_bf<DK, true><<<dim3(a.ncmax, a.H), NTHR, 0, st>>>(
           q, k, a.g, bt, a.d, a.cmap, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.QTp, a.Gw);
-    a.stage("scan_fwd_store");
-    k_scan_fwd_bf<DK, DV, SCAN_BV, false, true><<<scan_blocks(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
-        q, k, v, beta, bt, a.d, a.h0, a.smap, sord, a.N, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, nullptr, nullptr, a.Xq,
-        a.Xs, a.Dq, a.Ds, a.Xfq, a.Xfs);
+    // the chunk states (forward recurrence) and the reverse scan depend only on
+    // prep's operands, not on each other (the reverse scan reads no state):
+    // side by side, one workgroup of each per CU (68 + 92 KiB of LDS)
+    a.stage("scans");
+    side(
+        st,
+        [&](hipStream_t s1) {
+          k_scan_fwd_bf<DK, DV, SCAN_BV, false, true><<<scan_blocks(a.N, a.H, DV / SCAN_BV), NTHR, 0, s1>>>(
+              q, k, v, beta, bt, a.d, a.h0, a.smap, sord, a.N, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.Gw, nullptr,
+              nullptr, a.Xq, a.Xs, a.Dq, a.Ds, a.Xfq, a.Xfs);
+        },
+        [&](hipStream_t s2) {
+          k_scan_bwd_bf<DK, DV, SCAN_BV><<<scan_blocks(a.N, a.H, DV / SCAN_BV), NTHR, 0, s2>>>(
+              q, k, dO, bt, a.d, a.dht, a.smap, sord, a.N, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.QTp, a.Gw, a.dh0,
+              a.Yq, a.Ys, a.dRq, a.dRs);
+        });
   }
-  if (a.segP <= 1) {
+  if (a.segP <= 1 && a.saved) {
     a.stage("scan_bwd");
     k_scan_bwd_bf<DK, DV, SCAN_BV><<<scan_blocks(a.N, a.H, DV / SCAN_BV), NTHR, 0, st>>>(
         q, k, dO, bt, a.d, a.dht, a.smap, sord, a.N, Tfix, a.H, a.Mq, a.Ms, a.Aq, a.As, a.QTp, a.Gw, a.dh0, a.Yq,
