@@ -28,7 +28,8 @@
  *    first comba_chunk_bwd call that uses them: the stateless backward runs
  *    its two independent scans side by side, the second on the helper stream,
  *    forked from and joined back to `stream` (under graph capture of `stream`
- *    the helper joins the capture).
+ *    the helper joins the capture; a first call that is itself captured
+ *    creates nothing and runs the two scans in turn).
  *  - Layouts are C-contiguous.  Token-major tensors are [B, T, H, D]; in the
  *    variable-length mode B == 1, T is the packed token count and sequence s
  *    covers tokens [cu_seqlens[s], cu_seqlens[s+1]).  A sequence's last chunk

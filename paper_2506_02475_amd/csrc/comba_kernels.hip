@@ -3128,8 +3128,9 @@ static unsigned intra_bwd_grid(long items) {
 // fork (the side stream waits for everything already on st), the side work,
 // the main work on st and a join (st waits for the side work), under a lock,
 // so that calls from several host threads cannot interleave their event
-// records.  Without a side stream (creation failed) both run on st in turn.
-// Under graph capture of st the side stream joins the capture and rejoins st.
+// records.  Without a side stream (creation failed, or the first use falls
+// in a graph capture of st) both run on st in turn.  Under graph capture of
+// st an existing side stream joins the capture and rejoins st.
 struct SideStream {
   hipStream_t s = nullptr;
   hipEvent_t fork = nullptr, join = nullptr;
@@ -3149,7 +3150,18 @@ static void side(hipStream_t st, Main&& main_work, Side&& side_work) {
   std::unique_lock<std::mutex> lock(g_side_mu);
   if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < kMaxSideDevices) {
     SideStream& c = g_side[dev];
+    // creating a stream or an event is not allowed while st is being captured:
+    // then the work runs in turn (an existing side stream forks and joins as
+    // usual: event records and waits are captured)
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    bool capturing = false;
     if (!c.s && !c.failed) {
+      if (hipStreamIsCapturing(st, &cs) == hipSuccess)
+        capturing = cs != hipStreamCaptureStatusNone;
+      else if (clean)
+        (void)hipGetLastError();  // no capture to be found on this stream
+    }
+    if (!c.s && !c.failed && !capturing) {
       if (hipStreamCreateWithFlags(&c.s, hipStreamNonBlocking) != hipSuccess ||
           hipEventCreateWithFlags(&c.fork, hipEventDisableTiming) != hipSuccess ||
           hipEventCreateWithFlags(&c.join, hipEventDisableTiming) != hipSuccess) {

@@ -89,3 +89,37 @@ def test_stateless_backward_from_two_threads_matches_one_call():
         for gr in res:
             for name in GRADS:
                 assert torch.equal(gr[name], ref[name]), name
+
+
+def test_stateless_backward_replays_from_a_captured_graph():
+    """The fork to the helper stream and the join back are captured with the
+    kernels (the helper exists from an eager call before the capture); every
+    replay, with eager calls and synchronisations between them, equals the
+    eager result."""
+    import torch
+
+    import paper_2506_02475_amd as comba
+
+    args, dO, dht = _args()
+    ref = comba.comba_chunk_bwd(*args, dO, dht)
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        comba.comba_chunk_bwd(*args, dO, dht)  # warm-up on a side stream, as capture expects
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        out = comba.comba_chunk_bwd(*args, dO, dht)
+    torch.cuda.synchronize()
+    for i in range(3):
+        print("graph replay %d" % i, flush=True)
+        graph.replay()
+        torch.cuda.synchronize()
+        for name in GRADS:
+            assert torch.equal(out[name], ref[name]), (i, name)
+        again = comba.comba_chunk_bwd(*args, dO, dht)
+        torch.cuda.synchronize()
+        for name in GRADS:
+            assert torch.equal(again[name], ref[name]), (i, name)
